@@ -1,0 +1,259 @@
+#!/usr/bin/env python3
+"""Throughput of the binarized CNN hot path on one MI355X.
+
+A step is one bnn_forward pass (every layer of the chain: first layer,
+binary 3x3 convs with fused threshold / flip / OR-pool, binary FC layers,
+int32 logits) over one batch of synthetic input already resident in HBM.
+
+Default workload: the CIFAR-shaped net at batch 64 (fp32 32x32x3 input,
+binary convs 128-128(pool)-256-256(pool)-512-512(pool), FC 8192-1024-1024-10).
+value = binary GOPS over the whole step (2 ops per bit multiply-accumulate of
+the binary conv and FC layers; the fp32 first layer is not counted).  The
+same JSON line carries images/s at batch 64 and at batch 1 (1000 fresh images
+fed one at a time, kernels-only GPU time per image, as in the paper's
+protocol), a per-layer breakdown, the roofline of the dominant kernel, and
+the CPU oracle timed on a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+VALU_PEAK_TOPS = 1258.29  # 256 CU x 64 lanes x 2.4 GHz x 32 bit-MACs x 2 ops / 2 instr
+HBM_PEAK_GBS = 8000.0
+
+WORKLOADS = {
+    "cifar_bnn_b64": dict(cfg=3, batch=64, H=32, W=32, C=3),
+    "vehicle_bnn_b256": dict(cfg=4, batch=256, H=96, W=96, C=3),
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="cifar_bnn_b64", choices=sorted(WORKLOADS))
+    ap.add_argument("--b1-images", type=int, default=1000)
+    ap.add_argument("--layer-reps", type=int, default=50)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target length of the CPU-oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def net_layers(cfg):
+    from paper_1808_00209_amd import synth
+    return synth.cfg3_net() if cfg == 3 else synth.cfg4_net()
+
+
+def net_input(cfg, batch):
+    from paper_1808_00209_amd import synth
+    return synth.cfg3_input(batch) if cfg == 3 else synth.cfg4_input(batch)
+
+
+def layer_shapes(layers, H, W, C):
+    """Per layer: (name, kind, geometry dict, bit-MACs per image)."""
+    out = []
+    h, w, c = H, W, C
+    for li, L in enumerate(layers):
+        k = L["kind"]
+        if k == "input_threshold":
+            out.append(("L%d pack %dx%dx%d" % (li, h, w, c), k, dict(H=h, W=w, C=c), 0))
+        elif k in ("fconv", "bconv"):
+            KH, KW, pad, F = L["KH"], L["KW"], L["pad"], L["F"]
+            Ho, Wo = h + 2 * pad - KH + 1, w + 2 * pad - KW + 1
+            macs = Ho * Wo * F * KH * KW * c
+            pool = L.get("pool", 0)
+            name = "L%d %s %dx%dx%d->%d k%d%s" % (li, k, h, w, c, F, KH, " pool" if pool else "")
+            out.append((name, k, dict(H=h, W=w, C=c, F=F, KH=KH, KW=KW, pad=pad, pool=pool),
+                        0 if k == "fconv" else macs))
+            h, w, c = (Ho // 2, Wo // 2, F) if pool else (Ho, Wo, F)
+        else:
+            K, N = L["K"], L["N"]
+            out.append(("L%d %s %d->%d" % (li, k, K, N), k, dict(K=K, N=N), K * N))
+            h, w, c = 1, 1, N
+    return out
+
+
+def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
+    """Average kernel time (ms) of one layer's standalone call on random bits."""
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    s = torch.cuda.current_stream()
+    if kind == "input_threshold":
+        x = torch.randn((batch, g["H"], g["W"], g["C"]), device="cuda", generator=gen)
+        out = torch.empty((batch, g["H"], g["W"], bnn.words(g["C"])), dtype=torch.int32,
+                          device="cuda")
+        fn = lambda: bnn.bnn_pack_bits(x, dev_layer.get("offset"), out=out)
+    elif kind in ("fconv", "bconv"):
+        desc = bnn.conv_desc(batch, g["H"], g["W"], g["C"], g["F"], g["KH"], g["KW"], 1,
+                             g["pad"], g["pool"])
+        Ho, Wo, Hp, Wp = bnn.bnn_conv_output_dims(desc)
+        ob = torch.empty((batch, Hp, Wp, bnn.words(g["F"])), dtype=torch.int32, device="cuda")
+        if kind == "fconv":
+            x = torch.randn((batch, g["H"], g["W"], g["C"]), device="cuda", generator=gen)
+            fn = lambda: bnn.bnn_fconv2d_binw(desc, x, dev_layer["w"], dev_layer["thr"],
+                                              dev_layer.get("flip"), want_sums=False,
+                                              out_bits=ob)
+        else:
+            x = torch.randint(-2 ** 31, 2 ** 31 - 1, (batch, g["H"], g["W"], bnn.words(g["C"])),
+                              dtype=torch.int32, device="cuda", generator=gen)
+            fn = lambda: bnn.bnn_bconv2d(desc, x, dev_layer["w"], dev_layer["thr"],
+                                         dev_layer.get("flip"), want_sums=False, out_bits=ob)
+    else:
+        A = torch.randint(-2 ** 31, 2 ** 31 - 1, (batch, bnn.words(g["K"])), dtype=torch.int32,
+                          device="cuda", generator=gen)
+        if kind == "bfc":
+            ob = torch.empty((batch, bnn.words(g["N"])), dtype=torch.int32, device="cuda")
+            fn = lambda: bnn.bnn_bgemm(A, dev_layer["w"], g["K"], dev_layer["thr"],
+                                       dev_layer.get("flip"), want_sums=False, out_bits=ob)
+        else:
+            os_ = torch.empty((batch, g["N"]), dtype=torch.int32, device="cuda")
+            fn = lambda: bnn.bnn_bgemm(A, dev_layer["w"], g["K"], want_bits=False, out_sums=os_)
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s)
+    for _ in range(reps):
+        fn()
+    e1.record(s)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def cpu_baseline(layers, x, target_s, bin_ops_per_image):
+    import oracle
+    n = 1
+    t0 = time.perf_counter()
+    oracle.forward(layers, x[:1])
+    t1 = time.perf_counter() - t0
+    n = int(max(1, min(len(x), target_s / max(t1, 1e-6))))
+    t0 = time.perf_counter()
+    oracle.forward(layers, x[:n])
+    dt = time.perf_counter() - t0
+    return {"value": round(n * bin_ops_per_image / dt / 1e9, 3), "unit": "GOPS",
+            "images_per_s": round(n / dt, 3), "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": "%d of the %d images of one batch through the whole oracle chain "
+                      "(%.1f s), scaled to binary GOPS" % (n, len(x), dt)}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(requested --gpus %d, WORLD_SIZE=%d)" % (args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_1808_00209_amd import bnn
+    from paper_1808_00209_amd.device import to_device, upload_layer, upload_network
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+    bnn.load()
+    wl = WORKLOADS[args.workload]
+    batch, H, W, C = wl["batch"], wl["H"], wl["W"], wl["C"]
+    layers = net_layers(wl["cfg"])
+    shapes = layer_shapes(layers, H, W, C)
+    bin_macs_img = sum(s[3] for s in shapes)
+    ops_per_step = 2 * bin_macs_img * batch
+
+    x_host = net_input(wl["cfg"], batch)
+    net = upload_network(layers, H, W, C)
+    x = to_device(x_host)
+    ws = net.alloc_workspace(batch)
+    logits = torch.empty((batch, layers[-1]["N"]), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        bnn.bnn_forward(net, x, ws, logits)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        bnn.bnn_forward(net, x, ws, logits)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    gops = ops_per_step / (ms_per_step * 1e-3) / 1e9
+
+    # Batch-1 latency protocol: fresh images one at a time, kernels only.
+    n1 = args.b1_images
+    x1 = to_device(net_input(wl["cfg"], n1))
+    ws1 = net.alloc_workspace(1)
+    lg1 = torch.empty((1, layers[-1]["N"]), dtype=torch.int32, device="cuda")
+    for i in range(3):
+        bnn.bnn_forward(net, x1[i:i + 1], ws1, lg1)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(n1)]
+    for i in range(n1):
+        evs[i][0].record(stream)
+        bnn.bnn_forward(net, x1[i:i + 1], ws1, lg1)
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    per_img_us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+
+    # Per-layer kernel times (Table II analogue) and the dominant kernel.
+    dev_layers = [upload_layer(L) for L in layers]
+    per_layer = []
+    for (name, kind, g, macs), dl in zip(shapes, dev_layers):
+        ms = time_layer(bnn, kind, g, batch, dl, args.layer_reps, torch)
+        row = {"layer": name, "ms": round(ms, 5)}
+        if macs:
+            row["GOPS"] = round(2 * macs * batch / (ms * 1e-3) / 1e9, 1)
+        per_layer.append(row)
+    dom_i = max(range(len(shapes)), key=lambda i: per_layer[i]["ms"] if shapes[i][3] else -1)
+    dom_ms = per_layer[dom_i]["ms"]
+    dom_ops = 2 * shapes[dom_i][3] * batch
+    achieved_tops = dom_ops / (dom_ms * 1e-3) / 1e12
+
+    result = {
+        "metric": "binary conv GOPS (2 ops per bit-MAC) and images/s at batch 1 and 64",
+        "value": round(gops, 1),
+        "unit": "GOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "batch": batch, "input": "%dx%dx%d fp32" % (H, W, C),
+                   "binary_ops_per_step": ops_per_step},
+        "images_per_s": round(batch / (ms_per_step * 1e-3), 1),
+        "batch1": {"images": n1, "mean_us": round(float(per_img_us.mean()), 3),
+                   "median_us": round(float(np.median(per_img_us)), 3),
+                   "images_per_s": round(1e6 / float(per_img_us.mean()), 1)},
+        "wall_s_timed_region": round(t_wall, 4),
+        "per_layer": per_layer,
+        "roofline": {"kernel": shapes[dom_i][0], "bound": "alu",
+                     "achieved": round(achieved_tops, 2), "peak": VALU_PEAK_TOPS,
+                     "unit": "TOP/s", "frac": round(achieved_tops / VALU_PEAK_TOPS, 4),
+                     "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(layers, x_host, args.cpu_seconds,
+                                              2 * bin_macs_img)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

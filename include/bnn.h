@@ -1,0 +1,218 @@
+/*
+ * bnn.h -- C ABI of libbnn.so: binarized convolutional / fully-connected
+ * inference on AMD Instinct MI355X (gfx950).
+ *
+ * Method: Khan, Huttunen, Boutellier, "Binarized Convolutional Neural
+ * Networks for Efficient Inference on GPUs", EUSIPCO 2018.  Weights and
+ * activations are +-1 values packed 32 to a 32-bit word (Sec. II-D, Eq. 2);
+ * a dot product of two packed vectors of W valid bits is
+ * W - 2 * popcount(a XOR b) (Sec. III-A, Eq. 4).
+ *
+ * ---------------------------------------------------------------- layout --
+ * Packed word (Eq. 2 with B = 32): value i (0-based) of a group of 32 goes to
+ * bit (31 - i); bit 1 means +1, bit 0 means -1.  A vector of D values takes
+ * ceil(D / 32) words; the unused low bits of a short last word are "tail"
+ * bits.  Outputs of this library always hold 0 in tail bits; inputs may hold
+ * anything there (every kernel masks them).
+ *
+ * Activations are NHWC with channels packed: u32 [N][H][W][Cw], Cw =
+ * ceil(C / 32).  Conv weights are u32 [F][KH][KW][Cw] (filter f's KHxKWxC
+ * window in the same packing).  FC operands are u32 [rows][ceil(K / 32)].
+ * Output bits use the same packing over filters / output columns, and the
+ * flip vector uses it too: flip bit for channel f is bit (31 - f % 32) of
+ * word f / 32.
+ *
+ * ------------------------------------------------------------- semantics --
+ * Binary conv (Eq. 3, a cross-correlation): for output pixel (n, i, j) and
+ * filter f,
+ *     S = sum_{kh, kw, c} w[f,kh,kw,c] * x[n, i*s + kh - p, j*s + kw - p, c]
+ * over +-1 values, where a tap outside the image reads -1 (bit 0).  Padded
+ * taps count: S has the parity of K = KH * KW * C and |S| <= K.
+ * Threshold (folded BatchNorm + sign; not in the paper): output bit =
+ * (S >= thr[f]) XOR flip[f].  Pooling: 2x2, stride 2, applied to the bits
+ * after the threshold as a bitwise OR (= max over +-1), floor on odd sizes.
+ *
+ * ------------------------------------------------------ memory and errors --
+ * Every pointer argument is a DEVICE pointer owned by the caller, except the
+ * bnn_conv_desc / bnn_layer structs and the size outputs, which are host
+ * memory read or written before the call returns.  The library allocates
+ * nothing and keeps no state except a thread-local error string.  Calls only
+ * enqueue kernels on `stream` and return without synchronising; results are
+ * ready when the stream reaches that point.  Device buffers passed to one
+ * call must not overlap unless stated.
+ *
+ * Every call validates its arguments on the host first and returns a status
+ * other than BNN_OK without launching anything when they are invalid;
+ * bnn_last_error() then describes the problem.  A failed kernel launch
+ * returns BNN_ERR_HIP.  No C++ exception crosses this interface.
+ */
+#ifndef BNN_H
+#define BNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BNN_ABI_VERSION 1
+
+typedef enum bnn_status {
+  BNN_OK = 0,
+  BNN_ERR_NULL = 1,        /* a required pointer is NULL                    */
+  BNN_ERR_SHAPE = 2,       /* a size is out of range or sizes disagree      */
+  BNN_ERR_ALIGN = 3,       /* a pointer is not 16-byte aligned              */
+  BNN_ERR_UNSUPPORTED = 4, /* valid in principle, not implemented (stride)  */
+  BNN_ERR_HIP = 5,         /* the HIP runtime reported an error             */
+  BNN_ERR_WORKSPACE = 6    /* workspace smaller than required               */
+} bnn_status;
+
+/* Text describing the last non-OK status returned on this thread ("" if
+ * none).  The pointer stays valid until the next call on the same thread. */
+const char* bnn_last_error(void);
+
+/* BNN_ABI_VERSION of the loaded library. */
+int32_t bnn_abi_version(void);
+
+/*
+ * Sign to bits (Eq. 1 and Eq. 2; input thresholding of Sec. II-C).
+ *   out[r][j] bit (31 - i) = ((x[r][32 j + i] + offset[32 j + i]) > 0)
+ * for 32 j + i < D, computed in fp32; tail bits are written 0.  x == 0 (after
+ * the offset) gives bit 0 (-1), as does NaN.
+ *   x      [rows][D] fp32, device.
+ *   offset [D] fp32 or NULL (NULL: no offset).  Thresholding an RGB image by
+ *          T in R^{1x1xC} passes rows = N*H*W, D = C, offset = T.
+ *   out    [rows][ceil(D / 32)] u32, device.
+ * rows >= 0 and D >= 1 (rows == 0 launches nothing).  Errors: BNN_ERR_NULL,
+ * BNN_ERR_SHAPE.
+ */
+bnn_status bnn_pack_bits(const float* x, const float* offset, int64_t rows,
+                         int64_t D, uint32_t* out, hipStream_t stream);
+
+/* Shape of one convolution layer (Eq. 3).  stride must be 1 (other strides
+ * return BNN_ERR_UNSUPPORTED); 0 <= pad, KH, KW >= 1 and the output
+ * Ho = H + 2 pad - KH + 1, Wo = W + 2 pad - KW + 1 must be >= 1.  pool is 0
+ * (none) or 2 (2x2 / stride 2; needs Ho, Wo >= 2). */
+typedef struct bnn_conv_desc {
+  int32_t N, H, W, C; /* input batch, height, width, channels (bits)       */
+  int32_t F;          /* filters = output channels                          */
+  int32_t KH, KW;     /* kernel height, width                               */
+  int32_t stride;     /* must be 1                                          */
+  int32_t pad;        /* symmetric padding (pad value -1 / 0.0)            */
+  int32_t pool;       /* 0 or 2                                             */
+} bnn_conv_desc;
+
+/* Output sizes of a conv: Ho x Wo before pooling, Hp x Wp after (Hp = Ho/2,
+ * Wp = Wo/2 when pool == 2, else Ho, Wo).  Validates like bnn_bconv2d. */
+bnn_status bnn_conv_output_dims(const bnn_conv_desc* d, int32_t* Ho,
+                                int32_t* Wo, int32_t* Hp, int32_t* Wp);
+
+/*
+ * Binary convolution with the fused threshold / flip / OR-pool epilogue
+ * (Eq. 3 with Eq. 4 for the window dot products; Sec. III-A).
+ *   in        [N][H][W][Cw] u32 packed activations.
+ *   w         [F][KH][KW][Cw] u32 packed weights.
+ *   thr       [F] int32 thresholds, or NULL when out_bits is NULL.
+ *   flip      [ceil(F / 32)] u32 flip bits, or NULL for all-zero.
+ *   out_sums  [N][Ho][Wo][F] int32 window sums S before the threshold and
+ *             before pooling, or NULL.
+ *   out_bits  [N][Hp][Wp][ceil(F / 32)] u32 thresholded (and pooled) bits,
+ *             or NULL.  Needs thr.
+ * At least one of out_sums / out_bits must be non-NULL.  in, w, out_sums and
+ * out_bits must be 16-byte aligned.  Errors: BNN_ERR_NULL, BNN_ERR_SHAPE,
+ * BNN_ERR_ALIGN, BNN_ERR_UNSUPPORTED (stride != 1), BNN_ERR_HIP.
+ */
+bnn_status bnn_bconv2d(const bnn_conv_desc* d, const uint32_t* in,
+                       const uint32_t* w, const int32_t* thr,
+                       const uint32_t* flip, int32_t* out_sums,
+                       uint32_t* out_bits, hipStream_t stream);
+
+/*
+ * Real-valued first layer with binary weights ("no input binarization",
+ * Table III; the BCNN row of Table I): Eq. 3 with an fp32 image and +-1
+ * weights, pad value 0.0, sums accumulated in fp32, then the same threshold /
+ * flip / OR-pool epilogue as bnn_bconv2d (S >= thr compared in fp32).
+ *   in        [N][H][W][C] fp32.
+ *   w         [F][KH][KW][Cw] u32 packed weights.
+ *   out_sums  [N][Ho][Wo][F] fp32 or NULL; out_bits as for bnn_bconv2d.
+ * The fp32 sums are exact (independent of summation order) when every input
+ * is a multiple of 2^-16 with |x| < 8 and KH*KW*C <= 32 (every partial sum
+ * is then a multiple of 2^-16 below 2^8, within fp32's 24-bit significand).
+ * Errors as for bnn_bconv2d.
+ */
+bnn_status bnn_fconv2d_binw(const bnn_conv_desc* d, const float* in,
+                            const uint32_t* w, const int32_t* thr,
+                            const uint32_t* flip, float* out_sums,
+                            uint32_t* out_bits, hipStream_t stream);
+
+/*
+ * Binary fully-connected layer / GEMM (Sec. III-B, Eq. 4):
+ *   S[m][n] = K - 2 * sum_j popcount(A[m][j] XOR B[n][j])   (valid bits only)
+ *   A         [M][Kw] u32, Kw = ceil(K / 32): M packed input vectors.
+ *   B         [N][Kw] u32: one packed weight row per output.
+ *   thr, flip [N] int32 / [ceil(N / 32)] u32 as for bnn_bconv2d.
+ *   out_sums  [M][N] int32 or NULL.
+ *   out_bits  [M][ceil(N / 32)] u32 or NULL (needs thr).
+ * M, N, K >= 1.  Alignment and errors as for bnn_bconv2d.
+ */
+bnn_status bnn_bgemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
+                     const uint32_t* B, const int32_t* thr,
+                     const uint32_t* flip, int32_t* out_sums,
+                     uint32_t* out_bits, hipStream_t stream);
+
+/* ------------------------------------------------------------ layer chain */
+typedef enum bnn_layer_kind {
+  BNN_LAYER_INPUT_THRESHOLD = 1, /* bnn_pack_bits with per-channel offset  */
+  BNN_LAYER_FCONV_BINW = 2,      /* bnn_fconv2d_binw (fp32 input)           */
+  BNN_LAYER_BCONV = 3,           /* bnn_bconv2d, bits out                   */
+  BNN_LAYER_BFC = 4,             /* bnn_bgemm, bits out                     */
+  BNN_LAYER_BFC_LOGITS = 5       /* bnn_bgemm, int32 sums out (last layer)  */
+} bnn_layer_kind;
+
+/* One layer of a chain.  Fields a kind does not use are ignored.  Device
+ * pointers: w, thr, flip, offset. */
+typedef struct bnn_layer {
+  int32_t kind;              /* bnn_layer_kind                               */
+  int32_t C;                 /* conv / input threshold: input channels       */
+  int32_t F, KH, KW;         /* conv: filters, kernel size                   */
+  int32_t stride, pad, pool; /* conv: as in bnn_conv_desc                    */
+  int32_t K, N;              /* FC: input bits, outputs                      */
+  const uint32_t* w;         /* conv [F][KH][KW][Cw]; FC [N][ceil(K/32)]     */
+  const int32_t* thr;        /* [F] or [N]                                   */
+  const uint32_t* flip;      /* packed flip bits or NULL                     */
+  const float* offset;       /* INPUT_THRESHOLD: [C] offsets T, or NULL      */
+} bnn_layer;
+
+/*
+ * Workspace bytes bnn_forward needs for `batch` images of H x W x C fp32
+ * (two ping-pong buffers of packed activations, 256-byte aligned).  Also
+ * validates the chain: the first layer is INPUT_THRESHOLD or FCONV_BINW, the
+ * last is BFC_LOGITS, shapes agree from layer to layer, and an FC layer that
+ * follows a conv reads its NHWC bits flattened in (h, w, c) order, which needs
+ * the channel count to be a multiple of 32 (or a 1x1 map).
+ */
+bnn_status bnn_forward_workspace_size(const bnn_layer* layers,
+                                      int32_t n_layers, int32_t batch,
+                                      int32_t H, int32_t W, int32_t C,
+                                      size_t* bytes);
+
+/*
+ * Run the chain on input [batch][H][W][C] fp32 and write int32 logits
+ * [batch][N_last] (Table I/II: conv, pool, ..., FC layers).  One kernel per
+ * layer on `stream`; workspace (device, >= the size above, 256-byte aligned)
+ * holds the intermediate bits.  Errors: as the per-layer calls, plus
+ * BNN_ERR_WORKSPACE.
+ */
+bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers,
+                       int32_t batch, int32_t H, int32_t W, int32_t C,
+                       const float* input, void* workspace, size_t ws_bytes,
+                       int32_t* logits, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BNN_H */

@@ -1,0 +1,397 @@
+// C ABI of libbnn.so (include/bnn.h): host-side validation, kernel dispatch
+// and the layer chain.  Every entry point checks its arguments before it
+// launches anything, reports problems through a status code plus a
+// thread-local message, and never lets a C++ exception escape.
+#include "bnn.h"
+
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <new>
+
+#include "kernels.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+bnn_status fail(bnn_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+bnn_status ok() {
+  g_err[0] = '\0';
+  return BNN_OK;
+}
+
+bnn_status hip_status(hipError_t e, const char* where) {
+  if (e == hipSuccess) return ok();
+  return fail(BNN_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int64_t kMaxItems = (int64_t{1} << 31) - 1;
+
+// Validates a conv descriptor and fills the geometry.
+bnn_status conv_geom(const bnn_conv_desc* d, bnn::ConvGeom* g) {
+  if (!d) return fail(BNN_ERR_NULL, "conv descriptor is NULL");
+  if (d->N < 1 || d->H < 1 || d->W < 1 || d->C < 1 || d->F < 1 || d->KH < 1 ||
+      d->KW < 1)
+    return fail(BNN_ERR_SHAPE,
+                "conv sizes must be >= 1 (N=%d H=%d W=%d C=%d F=%d KH=%d KW=%d)",
+                d->N, d->H, d->W, d->C, d->F, d->KH, d->KW);
+  if (d->stride != 1)
+    return fail(BNN_ERR_UNSUPPORTED, "conv stride %d: only stride 1 is implemented",
+                d->stride);
+  if (d->pad < 0) return fail(BNN_ERR_SHAPE, "conv pad %d < 0", d->pad);
+  if (d->pool != 0 && d->pool != 2)
+    return fail(BNN_ERR_SHAPE, "pool must be 0 or 2, got %d", d->pool);
+  const int64_t Ho = int64_t{d->H} + 2 * int64_t{d->pad} - d->KH + 1;
+  const int64_t Wo = int64_t{d->W} + 2 * int64_t{d->pad} - d->KW + 1;
+  if (Ho < 1 || Wo < 1)
+    return fail(BNN_ERR_SHAPE, "conv output %lldx%lld is empty", (long long)Ho,
+                (long long)Wo);
+  if (d->pool == 2 && (Ho < 2 || Wo < 2))
+    return fail(BNN_ERR_SHAPE, "2x2 pooling needs a conv output of at least 2x2");
+  const int64_t Cw = bnn::words_of(d->C);
+  const int64_t in_words = int64_t{d->N} * d->H * d->W * Cw;
+  const int64_t items = int64_t{d->N} * Ho * Wo;
+  const int64_t wwords = int64_t{d->F} * d->KH * d->KW * Cw;
+  // Launch limits: at most 8 work-items per output pixel (32-bit grid size)
+  // and a filter-group count that fits the grid's y dimension.
+  if (in_words > kMaxItems * 4 || items > (int64_t{1} << 28) || d->F > (1 << 20) ||
+      int64_t{d->KH} * d->KW * d->C > kMaxItems / 2 || wwords > kMaxItems)
+    return fail(BNN_ERR_SHAPE, "conv is too large for 32-bit indexing");
+  g->N = d->N;
+  g->H = d->H;
+  g->W = d->W;
+  g->C = d->C;
+  g->F = d->F;
+  g->KH = d->KH;
+  g->KW = d->KW;
+  g->pad = d->pad;
+  g->pool = d->pool;
+  g->Cw = static_cast<int32_t>(Cw);
+  g->Fw = static_cast<int32_t>(bnn::words_of(d->F));
+  g->Ho = static_cast<int32_t>(Ho);
+  g->Wo = static_cast<int32_t>(Wo);
+  g->Hp = d->pool == 2 ? g->Ho / 2 : g->Ho;
+  g->Wp = d->pool == 2 ? g->Wo / 2 : g->Wo;
+  return BNN_OK;
+}
+
+bnn_status check_outputs(const void* in, const uint32_t* w, const int32_t* thr,
+                         const void* sums, const uint32_t* bits) {
+  if (!in) return fail(BNN_ERR_NULL, "input pointer is NULL");
+  if (!w) return fail(BNN_ERR_NULL, "weight pointer is NULL");
+  if (!sums && !bits)
+    return fail(BNN_ERR_NULL, "out_sums and out_bits are both NULL: nothing to compute");
+  if (bits && !thr) return fail(BNN_ERR_NULL, "out_bits requested but thr is NULL");
+  if (!aligned16(in) || !aligned16(w) || (sums && !aligned16(sums)) ||
+      (bits && !aligned16(bits)))
+    return fail(BNN_ERR_ALIGN, "input, weight and output pointers must be 16-byte aligned");
+  return BNN_OK;
+}
+
+bnn_status gemm_check(int64_t M, int64_t N, int64_t K, const uint32_t* A,
+                      const uint32_t* B, const int32_t* thr, const int32_t* sums,
+                      const uint32_t* bits) {
+  if (M < 1 || N < 1 || K < 1)
+    return fail(BNN_ERR_SHAPE, "bgemm sizes must be >= 1 (M=%lld N=%lld K=%lld)",
+                (long long)M, (long long)N, (long long)K);
+  const int64_t Kw = bnn::words_of(K);
+  if (M > (int64_t{1} << 28) || N > (1 << 20) || K > kMaxItems / 2 ||
+      M * Kw > kMaxItems * 4 || N * Kw > kMaxItems)
+    return fail(BNN_ERR_SHAPE, "bgemm is too large for 32-bit indexing");
+  bnn_status st = check_outputs(A, B, thr, sums, bits);
+  if (st != BNN_OK) return st;
+  return BNN_OK;
+}
+
+bnn_status gemm_launch(int64_t M, int64_t N, int64_t K, const uint32_t* A,
+                       const uint32_t* B, const int32_t* thr,
+                       const uint32_t* flip, int32_t* sums, uint32_t* bits,
+                       hipStream_t s) {
+  if (M <= 16)
+    return hip_status(bnn::launch_bgemv_valu(M, N, K, A, B, thr, flip, sums, bits, s),
+                      "bgemm (gemv) launch");
+  // M rows of A are a 1 x M image with K channels; B holds N 1x1 filters.
+  bnn::ConvGeom g;
+  g.N = 1;
+  g.H = 1;
+  g.W = static_cast<int32_t>(M);
+  g.C = static_cast<int32_t>(K);
+  g.F = static_cast<int32_t>(N);
+  g.KH = g.KW = 1;
+  g.pad = 0;
+  g.pool = 0;
+  g.Cw = static_cast<int32_t>(bnn::words_of(K));
+  g.Fw = static_cast<int32_t>(bnn::words_of(N));
+  g.Ho = 1;
+  g.Wo = g.W;
+  g.Hp = 1;
+  g.Wp = g.W;
+  return hip_status(bnn::launch_bconv_valu(g, A, B, thr, flip, sums, bits, s),
+                    "bgemm launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* bnn_last_error(void) { return g_err; }
+
+int32_t bnn_abi_version(void) { return BNN_ABI_VERSION; }
+
+bnn_status bnn_pack_bits(const float* x, const float* offset, int64_t rows,
+                         int64_t D, uint32_t* out, hipStream_t stream) {
+  try {
+    if (rows < 0 || D < 1)
+      return fail(BNN_ERR_SHAPE, "pack: rows must be >= 0 and D >= 1 (rows=%lld D=%lld)",
+                  (long long)rows, (long long)D);
+    if (rows * bnn::words_of(D) > kMaxItems || D > kMaxItems)
+      return fail(BNN_ERR_SHAPE, "pack: too large for 32-bit indexing");
+    if (rows == 0) return ok();
+    if (!x || !out) return fail(BNN_ERR_NULL, "pack: x and out must be non-NULL");
+    return hip_status(bnn::launch_pack_bits(x, offset, rows, D, out, stream), "pack launch");
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "pack: unexpected C++ exception");
+  }
+}
+
+bnn_status bnn_conv_output_dims(const bnn_conv_desc* d, int32_t* Ho, int32_t* Wo,
+                                int32_t* Hp, int32_t* Wp) {
+  bnn::ConvGeom g;
+  bnn_status st = conv_geom(d, &g);
+  if (st != BNN_OK) return st;
+  if (Ho) *Ho = g.Ho;
+  if (Wo) *Wo = g.Wo;
+  if (Hp) *Hp = g.Hp;
+  if (Wp) *Wp = g.Wp;
+  return ok();
+}
+
+bnn_status bnn_bconv2d(const bnn_conv_desc* d, const uint32_t* in, const uint32_t* w,
+                       const int32_t* thr, const uint32_t* flip, int32_t* out_sums,
+                       uint32_t* out_bits, hipStream_t stream) {
+  try {
+    bnn::ConvGeom g;
+    bnn_status st = conv_geom(d, &g);
+    if (st != BNN_OK) return st;
+    st = check_outputs(in, w, thr, out_sums, out_bits);
+    if (st != BNN_OK) return st;
+    return hip_status(
+        bnn::launch_bconv_valu(g, in, w, thr, flip, out_sums, out_bits, stream),
+        "bconv2d launch");
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "bconv2d: unexpected C++ exception");
+  }
+}
+
+bnn_status bnn_fconv2d_binw(const bnn_conv_desc* d, const float* in, const uint32_t* w,
+                            const int32_t* thr, const uint32_t* flip, float* out_sums,
+                            uint32_t* out_bits, hipStream_t stream) {
+  try {
+    bnn::ConvGeom g;
+    bnn_status st = conv_geom(d, &g);
+    if (st != BNN_OK) return st;
+    st = check_outputs(in, w, thr, out_sums, out_bits);
+    if (st != BNN_OK) return st;
+    return hip_status(
+        bnn::launch_fconv_binw(g, in, w, thr, flip, out_sums, out_bits, stream),
+        "fconv2d_binw launch");
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "fconv2d_binw: unexpected C++ exception");
+  }
+}
+
+bnn_status bnn_bgemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
+                     const uint32_t* B, const int32_t* thr, const uint32_t* flip,
+                     int32_t* out_sums, uint32_t* out_bits, hipStream_t stream) {
+  try {
+    bnn_status st = gemm_check(M, N, K, A, B, thr, out_sums, out_bits);
+    if (st != BNN_OK) return st;
+    return gemm_launch(M, N, K, A, B, thr, flip, out_sums, out_bits, stream);
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "bgemm: unexpected C++ exception");
+  }
+}
+
+// ------------------------------------------------------------ layer chain --
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+// Activation state between layers: an NHWC map of packed bits (or, before
+// the first layer, the fp32 input).
+struct Act {
+  int64_t H, W, C;  // C in channels (bits); FC outputs are 1 x 1 x N
+};
+
+// Walks the chain, validating shapes; returns the largest activation size in
+// bytes (packed words) through *max_bytes.
+bnn_status plan_chain(const bnn_layer* L, int32_t n, int32_t batch, int32_t H,
+                      int32_t W, int32_t C, size_t* max_bytes) {
+  if (!L) return fail(BNN_ERR_NULL, "forward: layers is NULL");
+  if (n < 1) return fail(BNN_ERR_SHAPE, "forward: need at least one layer");
+  if (batch < 1 || H < 1 || W < 1 || C < 1)
+    return fail(BNN_ERR_SHAPE, "forward: batch, H, W, C must be >= 1");
+  if (L[0].kind != BNN_LAYER_INPUT_THRESHOLD && L[0].kind != BNN_LAYER_FCONV_BINW)
+    return fail(BNN_ERR_SHAPE, "forward: layer 0 must be INPUT_THRESHOLD or FCONV_BINW");
+  if (L[n - 1].kind != BNN_LAYER_BFC_LOGITS)
+    return fail(BNN_ERR_SHAPE, "forward: the last layer must be BFC_LOGITS");
+  Act a{H, W, C};
+  size_t mx = 0;
+  for (int32_t li = 0; li < n; ++li) {
+    const bnn_layer& l = L[li];
+    switch (l.kind) {
+      case BNN_LAYER_INPUT_THRESHOLD: {
+        if (li != 0) return fail(BNN_ERR_SHAPE, "forward: layer %d: INPUT_THRESHOLD must be first", li);
+        if (l.C != C) return fail(BNN_ERR_SHAPE, "forward: layer 0 C=%d but input has C=%d", l.C, C);
+        break;
+      }
+      case BNN_LAYER_FCONV_BINW:
+      case BNN_LAYER_BCONV: {
+        if (l.kind == BNN_LAYER_FCONV_BINW && li != 0)
+          return fail(BNN_ERR_SHAPE, "forward: layer %d: FCONV_BINW must be first", li);
+        if (l.C != a.C)
+          return fail(BNN_ERR_SHAPE, "forward: layer %d expects C=%d, previous layer gives %lld",
+                      li, l.C, (long long)a.C);
+        if (!l.w || !l.thr) return fail(BNN_ERR_NULL, "forward: layer %d: w and thr are required", li);
+        bnn_conv_desc d{batch, static_cast<int32_t>(a.H), static_cast<int32_t>(a.W), l.C, l.F,
+                        l.KH, l.KW, l.stride, l.pad, l.pool};
+        bnn::ConvGeom g;
+        bnn_status st = conv_geom(&d, &g);
+        if (st != BNN_OK) return fail(st, "forward: layer %d: %s", li, g_err);
+        a = Act{g.Hp, g.Wp, l.F};
+        break;
+      }
+      case BNN_LAYER_BFC:
+      case BNN_LAYER_BFC_LOGITS: {
+        if (li == 0) return fail(BNN_ERR_SHAPE, "forward: an FC layer cannot be first");
+        if ((a.H * a.W) != 1 && (a.C % 32) != 0)
+          return fail(BNN_ERR_SHAPE,
+                      "forward: layer %d: flattening a %lldx%lld map needs C %% 32 == 0 (C=%lld)",
+                      li, (long long)a.H, (long long)a.W, (long long)a.C);
+        const int64_t K = a.H * a.W * a.C;
+        if (l.K != K)
+          return fail(BNN_ERR_SHAPE, "forward: layer %d expects K=%d, previous layer gives %lld",
+                      li, l.K, (long long)K);
+        if (l.N < 1) return fail(BNN_ERR_SHAPE, "forward: layer %d: N must be >= 1", li);
+        if (!l.w) return fail(BNN_ERR_NULL, "forward: layer %d: w is required", li);
+        if (l.kind == BNN_LAYER_BFC && !l.thr)
+          return fail(BNN_ERR_NULL, "forward: layer %d: thr is required", li);
+        if (l.kind == BNN_LAYER_BFC_LOGITS && li != n - 1)
+          return fail(BNN_ERR_SHAPE, "forward: BFC_LOGITS must be the last layer");
+        bnn_status st = gemm_check(batch, l.N, l.K, reinterpret_cast<const uint32_t*>(kAlign),
+                                   l.w, l.thr, reinterpret_cast<const int32_t*>(kAlign), nullptr);
+        if (st != BNN_OK) return fail(st, "forward: layer %d: %s", li, g_err);
+        a = Act{1, 1, l.N};
+        break;
+      }
+      default:
+        return fail(BNN_ERR_SHAPE, "forward: layer %d has unknown kind %d", li, l.kind);
+    }
+    if (l.kind != BNN_LAYER_BFC_LOGITS) {
+      const size_t bytes = static_cast<size_t>(batch) * a.H * a.W * bnn::words_of(a.C) * 4;
+      if (bytes > mx) mx = bytes;
+    }
+  }
+  *max_bytes = mx;
+  return BNN_OK;
+}
+
+}  // namespace
+
+bnn_status bnn_forward_workspace_size(const bnn_layer* layers, int32_t n_layers,
+                                      int32_t batch, int32_t H, int32_t W, int32_t C,
+                                      size_t* bytes) {
+  try {
+    if (!bytes) return fail(BNN_ERR_NULL, "forward_workspace_size: bytes is NULL");
+    size_t mx = 0;
+    bnn_status st = plan_chain(layers, n_layers, batch, H, W, C, &mx);
+    if (st != BNN_OK) return st;
+    *bytes = 2 * align_up(mx);
+    return ok();
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "forward_workspace_size: unexpected C++ exception");
+  }
+}
+
+bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
+                       int32_t H, int32_t W, int32_t C, const float* input,
+                       void* workspace, size_t ws_bytes, int32_t* logits,
+                       hipStream_t stream) {
+  try {
+    size_t mx = 0;
+    bnn_status st = plan_chain(layers, n_layers, batch, H, W, C, &mx);
+    if (st != BNN_OK) return st;
+    if (!input || !logits || !workspace)
+      return fail(BNN_ERR_NULL, "forward: input, logits and workspace must be non-NULL");
+    if (!aligned16(input) || !aligned16(logits) ||
+        (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+      return fail(BNN_ERR_ALIGN,
+                  "forward: input/logits must be 16-byte aligned, workspace 256-byte aligned");
+    const size_t half = align_up(mx);
+    if (ws_bytes < 2 * half)
+      return fail(BNN_ERR_WORKSPACE, "forward: workspace of %zu bytes, need %zu", ws_bytes,
+                  2 * half);
+    uint32_t* buf[2] = {static_cast<uint32_t*>(workspace),
+                        reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + half)};
+    int cur = 0;  // buffer holding the current packed activations
+    int64_t h = H, w = W, c = C;
+    for (int32_t li = 0; li < n_layers; ++li) {
+      const bnn_layer& l = layers[li];
+      uint32_t* dst = buf[li == 0 ? 0 : cur ^ 1];
+      const uint32_t* src = buf[cur];
+      hipError_t e = hipSuccess;
+      switch (l.kind) {
+        case BNN_LAYER_INPUT_THRESHOLD:
+          e = bnn::launch_pack_bits(input, l.offset, int64_t{batch} * h * w, c, dst, stream);
+          break;
+        case BNN_LAYER_FCONV_BINW:
+        case BNN_LAYER_BCONV: {
+          bnn_conv_desc d{batch, static_cast<int32_t>(h), static_cast<int32_t>(w), l.C, l.F,
+                          l.KH, l.KW, l.stride, l.pad, l.pool};
+          bnn::ConvGeom g;
+          conv_geom(&d, &g);
+          if (l.kind == BNN_LAYER_FCONV_BINW)
+            e = bnn::launch_fconv_binw(g, input, l.w, l.thr, l.flip, nullptr, dst, stream);
+          else
+            e = bnn::launch_bconv_valu(g, src, l.w, l.thr, l.flip, nullptr, dst, stream);
+          h = g.Hp;
+          w = g.Wp;
+          c = l.F;
+          break;
+        }
+        case BNN_LAYER_BFC: {
+          st = gemm_launch(batch, l.N, l.K, src, l.w, l.thr, l.flip, nullptr, dst, stream);
+          if (st != BNN_OK) return fail(st, "forward: layer %d: %s", li, g_err);
+          h = w = 1;
+          c = l.N;
+          break;
+        }
+        case BNN_LAYER_BFC_LOGITS: {
+          st = gemm_launch(batch, l.N, l.K, src, l.w, nullptr, nullptr, logits, nullptr, stream);
+          if (st != BNN_OK) return fail(st, "forward: layer %d: %s", li, g_err);
+          break;
+        }
+      }
+      if (e != hipSuccess) return fail(BNN_ERR_HIP, "forward: layer %d launch: %s", li,
+                                       hipGetErrorString(e));
+      cur = (li == 0) ? 0 : cur ^ 1;
+    }
+    return ok();
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "forward: unexpected C++ exception");
+  }
+}
+
+}  // extern "C"

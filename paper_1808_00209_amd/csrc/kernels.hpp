@@ -1,0 +1,49 @@
+// Launchers of the gfx950 kernels behind the C ABI (include/bnn.h).  The
+// C-ABI layer in api.cpp validates every argument before calling these; the
+// launchers assume valid shapes, 16-byte aligned buffers and non-empty work.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bnn {
+
+// Mask of the valid (high) bits of the last word of a packed vector of
+// `bits` values: value i of a word sits in bit 31 - i.
+inline __host__ __device__ uint32_t tail_mask(int64_t bits) {
+  const int r = static_cast<int>(bits & 31);
+  return r ? (~0u << (32 - r)) : ~0u;
+}
+
+inline int64_t words_of(int64_t bits) { return (bits + 31) >> 5; }
+
+// Geometry of one binary conv launch (stride 1).
+struct ConvGeom {
+  int32_t N, H, W, C, F, KH, KW, pad, pool;
+  int32_t Cw, Fw, Ho, Wo, Hp, Wp;
+};
+
+hipError_t launch_pack_bits(const float* x, const float* offset, int64_t rows,
+                            int64_t D, uint32_t* out, hipStream_t s);
+
+// Binary conv via XOR + popcount on the vector ALUs.  sums / bits may be
+// null; thr must be non-null when bits is.  flip may be null.
+hipError_t launch_bconv_valu(const ConvGeom& g, const uint32_t* in,
+                             const uint32_t* w, const int32_t* thr,
+                             const uint32_t* flip, int32_t* sums,
+                             uint32_t* bits, hipStream_t s);
+
+// Binary GEMM for a handful of rows (M <= 16): one output column per lane,
+// the K words split over the waves of a block.
+hipError_t launch_bgemv_valu(int64_t M, int64_t N, int64_t K,
+                             const uint32_t* A, const uint32_t* B,
+                             const int32_t* thr, const uint32_t* flip,
+                             int32_t* sums, uint32_t* bits, hipStream_t s);
+
+// Real-valued input conv with packed +-1 weights (fp32 sums).
+hipError_t launch_fconv_binw(const ConvGeom& g, const float* in,
+                             const uint32_t* w, const int32_t* thr,
+                             const uint32_t* flip, float* sums,
+                             uint32_t* bits, hipStream_t s);
+
+}  // namespace bnn

@@ -1,0 +1,159 @@
+"""The C-ABI library on the CPU: it loads, exports every symbol bnn.h declares,
+and rejects invalid arguments before launching anything (no GPU needed: each
+call here fails validation on the host)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1808_00209_amd import bnn
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bnn.h")
+
+needs_lib = pytest.mark.skipif(not os.path.exists(bnn.LIB_PATH),
+                               reason="libbnn.so not built (run __graft_entry__.build())")
+
+A = 4096  # a 16-byte-aligned stand-in address; never dereferenced here
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"^\S[^\n(]*?\b(bnn_[a-z0-9_]+)\(", src, re.M)))
+
+
+def test_header_lists_the_binding_symbols():
+    assert declared_functions() == sorted(bnn.EXPORTED)
+
+
+@needs_lib
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(bnn.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+@needs_lib
+def test_abi_version_and_empty_error():
+    lib = bnn.load()
+    assert lib.bnn_abi_version() == 1
+    assert isinstance(bnn.last_error(), str)
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    saved = bnn._lib
+    bnn._lib = None
+    try:
+        with pytest.raises(RuntimeError, match="not found"):
+            bnn.load(str(tmp_path / "nope.so"))
+    finally:
+        bnn._lib = saved
+
+
+def _conv(**kw):
+    d = dict(N=1, H=8, W=8, C=64, F=64, KH=3, KW=3, stride=1, pad=1, pool=0)
+    d.update(kw)
+    return bnn.ConvDesc(*[d[k] for k in ("N", "H", "W", "C", "F", "KH", "KW", "stride",
+                                         "pad", "pool")])
+
+
+def _bconv(desc, inp=A, w=A, thr=A, flip=None, sums=A, bits=A):
+    lib = bnn.load()
+    return lib.bnn_bconv2d(ctypes.byref(desc), inp, w, thr, flip, sums, bits, None)
+
+
+@needs_lib
+@pytest.mark.parametrize("kw,status,text", [
+    (dict(stride=2), 4, "stride"),
+    (dict(pool=3), 2, "pool"),
+    (dict(N=0), 2, ">= 1"),
+    (dict(C=-1), 2, ">= 1"),
+    (dict(KH=0), 2, ">= 1"),
+    (dict(pad=-1), 2, "pad"),
+    (dict(H=1, W=1, pad=0), 2, "empty"),
+    (dict(H=2, W=2, pad=0, KH=2, KW=2, pool=2), 2, "pooling"),
+])
+def test_bconv_shape_errors(kw, status, text):
+    assert _bconv(_conv(**kw)) == status
+    assert text in bnn.last_error()
+
+
+@needs_lib
+def test_bconv_null_and_alignment_errors():
+    d = _conv()
+    assert _bconv(d, inp=None) == 1 and "input" in bnn.last_error()
+    assert _bconv(d, w=None) == 1 and "weight" in bnn.last_error()
+    assert _bconv(d, sums=None, bits=None) == 1 and "nothing" in bnn.last_error()
+    assert _bconv(d, thr=None) == 1 and "thr" in bnn.last_error()
+    assert _bconv(d, inp=A + 4) == 3 and "aligned" in bnn.last_error()
+    assert _bconv(d, bits=A + 8) == 3
+    lib = bnn.load()
+    assert lib.bnn_bconv2d(None, A, A, A, None, A, A, None) == 1
+
+
+@needs_lib
+def test_conv_output_dims():
+    assert bnn.bnn_conv_output_dims(_conv(H=32, W=30, pool=2)) == (32, 30, 16, 15)
+    assert bnn.bnn_conv_output_dims(_conv(H=7, W=5, pool=2, KH=1, KW=1, pad=0)) == (7, 5, 3, 2)
+    assert bnn.bnn_conv_output_dims(_conv(H=5, W=5, KH=5, KW=3, pad=0)) == (1, 3, 1, 3)
+    with pytest.raises(bnn.BnnError) as e:
+        bnn.bnn_conv_output_dims(_conv(stride=3))
+    assert e.value.status == 4
+
+
+@needs_lib
+def test_bgemm_errors():
+    lib = bnn.load()
+    assert lib.bnn_bgemm(0, 4, 4, A, A, A, None, A, A, None) == 2
+    assert lib.bnn_bgemm(4, 4, 0, A, A, A, None, A, A, None) == 2
+    assert lib.bnn_bgemm(4, 4, 4, None, A, A, None, A, A, None) == 1
+    assert lib.bnn_bgemm(4, 4, 4, A, A, None, None, A, A, None) == 1
+    assert lib.bnn_bgemm(4, 4, 4, A, A + 4, A, None, A, None, None) == 3
+    assert lib.bnn_bgemm(1 << 40, 4, 4, A, A, A, None, A, A, None) == 2
+
+
+@needs_lib
+def test_pack_errors_and_empty():
+    lib = bnn.load()
+    assert lib.bnn_pack_bits(A, None, -1, 4, A, None) == 2
+    assert lib.bnn_pack_bits(A, None, 4, 0, A, None) == 2
+    assert lib.bnn_pack_bits(None, None, 4, 4, A, None) == 1
+    assert lib.bnn_pack_bits(None, None, 0, 4, None, None) == 0  # nothing to do
+
+
+def _layers(specs):
+    arr = (bnn.Layer * len(specs))()
+    for i, d in enumerate(specs):
+        for k, v in d.items():
+            setattr(arr[i], k, v)
+    return arr
+
+
+@needs_lib
+def test_forward_chain_validation():
+    lib = bnn.load()
+    size = ctypes.c_size_t()
+    good = [dict(kind=1, C=3),
+            dict(kind=3, C=3, F=64, KH=3, KW=3, stride=1, pad=1, pool=2, w=A, thr=A),
+            dict(kind=3, C=64, F=64, KH=3, KW=3, stride=1, pad=1, pool=2, w=A, thr=A),
+            dict(kind=5, K=2 * 2 * 64, N=4, w=A)]
+    L = _layers(good)
+    assert lib.bnn_forward_workspace_size(L, 4, 8, 8, 8, 3, ctypes.byref(size)) == 0
+    # two buffers of the largest packed map, the thresholded input:
+    # 8 images x 8x8 pixels x 1 word x 4 bytes, 256-byte aligned
+    assert size.value == 2 * 256 * ((8 * 8 * 8 * 1 * 4 + 255) // 256)
+    bad_k = [dict(good[0]), dict(good[1]), dict(good[2]), dict(good[3], K=100)]
+    assert lib.bnn_forward_workspace_size(_layers(bad_k), 4, 8, 8, 8, 3, ctypes.byref(size)) == 2
+    assert "expects K" in bnn.last_error()
+    no_logits = good[:3]
+    assert lib.bnn_forward_workspace_size(_layers(no_logits), 3, 8, 8, 8, 3,
+                                          ctypes.byref(size)) == 2
+    # flattening a map whose channel count is not a multiple of 32
+    odd = [dict(kind=1, C=3), dict(kind=3, C=3, F=40, KH=3, KW=3, stride=1, pad=1, w=A, thr=A),
+           dict(kind=5, K=8 * 8 * 40, N=4, w=A)]
+    assert lib.bnn_forward_workspace_size(_layers(odd), 3, 1, 8, 8, 3, ctypes.byref(size)) == 2
+    assert "flattening" in bnn.last_error()
+    # a too-small workspace is refused before any launch
+    assert lib.bnn_forward(L, 4, 8, 8, 8, 3, A, A, 256, A, None) == 6
+    assert lib.bnn_forward(L, 4, 8, 8, 8, 3, A, A + 16, 1 << 20, A, None) == 3

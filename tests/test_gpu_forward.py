@@ -1,0 +1,64 @@
+"""GPU parity of the whole layer chain (bnn_forward) against the oracle.
+
+Small batches are compared in full; the full-size batches (64 images of the
+CIFAR-shaped net, 256 of the vehicle-shaped net) are compared on sampled
+images, which the oracle computes independently (images never interact)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1808_00209_amd import bnn, synth
+from paper_1808_00209_amd.device import to_device, upload_network
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_logits(layers, x):
+    N, H, W, C = x.shape
+    net = upload_network(layers, H, W, C)
+    out = bnn.bnn_forward(net, to_device(x))
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+@pytest.mark.parametrize("batch", [1, 3])
+def test_cifar_net_small_batch(batch):
+    layers, x = synth.cfg3_net(), synth.cfg3_input(batch)
+    got = _gpu_logits(layers, x)
+    ref = oracle.forward(layers, x)
+    assert got.shape == (batch, 10)
+    assert np.array_equal(got, ref)
+
+
+def test_vehicle_net_small_batch():
+    layers, x = synth.cfg4_net(), synth.cfg4_input(2)
+    got = _gpu_logits(layers, x)
+    ref = oracle.forward(layers, x)
+    assert got.shape == (2, 4)
+    assert np.array_equal(got, ref)
+
+
+def test_cifar_net_batch64_sampled_images():
+    layers, x = synth.cfg3_net(), synth.cfg3_input(64)
+    got = _gpu_logits(layers, x)
+    pick = [0, 17, 63]
+    ref = oracle.forward(layers, x[pick])
+    assert np.array_equal(got[pick], ref)
+
+
+def test_vehicle_net_batch256_sampled_images():
+    layers, x = synth.cfg4_net(), synth.cfg4_input(256)
+    got = _gpu_logits(layers, x)
+    pick = [0, 255]
+    ref = oracle.forward(layers, x[pick])
+    assert np.array_equal(got[pick], ref)
+
+
+def test_forward_is_deterministic_and_batch_independent():
+    layers, x = synth.cfg3_net(), synth.cfg3_input(8)
+    a = _gpu_logits(layers, x)
+    b = _gpu_logits(layers, x)
+    c = _gpu_logits(layers, x[5:6])
+    assert np.array_equal(a, b)
+    assert np.array_equal(a[5:6], c)

@@ -1,0 +1,274 @@
+"""GPU parity of the HIP kernels against the CPU oracle (bit-exact).
+
+Inputs are seeded +-1 tensors; the GPU gets them packed by bnn_pack_bits, the
+oracle gets the +-1 int8 arrays.  Expected output bits are the oracle's +-1
+outputs packed with the oracle's Eq. (2) routine.  Sizes span several tiles
+and ragged tails; full-size configurations are checked on sampled outputs.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1808_00209_amd import bnn, synth
+from paper_1808_00209_amd.device import pack_flips, pack_pm1, to_device, words_u32
+
+pytestmark = pytest.mark.gpu
+
+
+def _pm1(rng, shape):
+    return (rng.integers(0, 2, size=shape) * 2 - 1).astype(np.int8)
+
+
+def _garble_tails(words_t, bits_valid):
+    """OR random garbage into the tail bits of every last word (in place)."""
+    r = bits_valid % 32
+    if r == 0:
+        return words_t
+    g = torch.Generator(device="cpu").manual_seed(99)
+    junk = torch.randint(0, 2 ** 31 - 1, words_t[..., -1].shape, generator=g, dtype=torch.int64)
+    tail = (1 << (32 - r)) - 1
+    words_t[..., -1] |= (junk & tail).to(torch.int32).to(words_t.device)
+    return words_t
+
+
+# ------------------------------------------------------------------ pack ---
+@pytest.mark.parametrize("D", [1, 3, 31, 32, 33, 63, 64, 65, 100, 4100])
+@pytest.mark.parametrize("with_offset", [False, True])
+def test_pack_bits_matches_oracle(D, with_offset):
+    rng = np.random.default_rng(1000 + D)
+    rows = 37
+    x = rng.standard_normal((rows, D)).astype(np.float32)
+    x[0, : min(D, 4)] = [0.0, -0.0, 1e-45, -1e-45][: min(D, 4)]  # ties and denormals
+    x[1] = np.round(x[1] * 4) / 4
+    off = None
+    if with_offset:
+        off = np.round(rng.standard_normal(D) * 4).astype(np.float32) / 4
+        x[2] = -off  # x + T == 0 exactly -> bit 0
+    got = words_u32(bnn.bnn_pack_bits(to_device(x), None if off is None else to_device(off)))
+    ref = oracle.pack_eq2(oracle.sign(x, off))
+    assert np.array_equal(got, ref)
+
+
+def test_pack_bits_rgb_thresholding_ties():
+    # Sec. II-C on integer pixels with integer offsets: exact ties occur.
+    g = synth.rng(4, 90, 0)
+    x = synth.pixels(g, (3, 96, 96, 3))
+    T = synth.rgb_offsets(synth.rng(4, 0, 1), 3)
+    got = words_u32(bnn.bnn_pack_bits(to_device(x), to_device(T)))
+    ref = oracle.pack_eq2(oracle.sign(x, T))
+    assert got.shape == (3, 96, 96, 1)
+    assert np.array_equal(got, ref)
+
+
+def test_pack_bits_zero_rows():
+    x = torch.empty((0, 64), dtype=torch.float32, device="cuda")
+    out = bnn.bnn_pack_bits(x)
+    assert out.shape == (0, 2)
+
+
+# ------------------------------------------------------------------ conv ---
+def _run_conv(x, L, pool, want_sums=True, want_bits=True, garble=False):
+    N, H, W, C = x.shape
+    F, KH, KW, _ = L["w"].shape
+    desc = bnn.conv_desc(N, H, W, C, F, KH, KW, 1, L["pad"], pool)
+    xd, wd = pack_pm1(x), pack_pm1(L["w"])
+    if garble:
+        _garble_tails(xd, C)
+        _garble_tails(wd, C)
+    thr = to_device(L["thr"], torch.int32)
+    flip = pack_flips(L["flip"])
+    sums, bits = bnn.bnn_bconv2d(desc, xd, wd, thr, flip, want_sums=want_sums,
+                                 want_bits=want_bits)
+    torch.cuda.synchronize()
+    return sums, bits
+
+
+def _oracle_conv(x, L, pool):
+    S = oracle.conv2d(x, L["w"], 1, L["pad"])
+    b = oracle.threshold(S, L["thr"], L["flip"])
+    if pool:
+        b = oracle.maxpool2(b)
+    return S, oracle.pack_eq2(b)
+
+
+def test_cfg1_single_conv_bit_exact():
+    x, L = synth.cfg1_input(), synth.cfg1_layer()
+    sums, bits = _run_conv(x, L, 0)
+    S, B = _oracle_conv(x, L, 0)
+    assert np.array_equal(sums.cpu().numpy(), S)
+    assert np.array_equal(words_u32(bits), B)
+
+
+CONV_CASES = [
+    # N, H, W, C, F, k, pad, pool
+    (2, 7, 7, 3, 64, 3, 1, 0),
+    (1, 32, 32, 33, 32, 3, 1, 2),
+    (3, 2, 2, 64, 40, 3, 1, 0),
+    (1, 1, 1, 96, 32, 3, 1, 0),
+    (2, 7, 9, 128, 96, 3, 1, 2),
+    (1, 32, 7, 32, 64, 1, 0, 0),
+    (2, 7, 7, 96, 33, 1, 0, 2),
+    (1, 9, 11, 256, 64, 3, 1, 2),
+    (1, 5, 6, 512, 32, 3, 0, 0),
+    (4, 6, 6, 3, 10, 3, 1, 2),
+    (1, 8, 8, 320, 64, 3, 1, 0),
+]
+
+
+@pytest.mark.parametrize("case", CONV_CASES, ids=[str(c) for c in CONV_CASES])
+@pytest.mark.parametrize("garble", [False, True])
+def test_bconv_shapes_bit_exact(case, garble):
+    N, H, W, C, F, k, pad, pool = case
+    rng = np.random.default_rng(hash(case) % 2 ** 32)
+    x = _pm1(rng, (N, H, W, C))
+    K = k * k * C
+    L = dict(w=_pm1(rng, (F, k, k, C)), pad=pad,
+             thr=rng.integers(-2 * int(np.sqrt(K)), 2 * int(np.sqrt(K)) + 1, F).astype(np.int32),
+             flip=rng.integers(0, 2, F).astype(np.uint8))
+    sums, bits = _run_conv(x, L, pool, garble=garble)
+    S, B = _oracle_conv(x, L, pool)
+    assert np.array_equal(sums.cpu().numpy(), S)
+    assert np.array_equal(words_u32(bits), B)
+
+
+def test_bconv_bits_only_and_sums_only_agree():
+    rng = np.random.default_rng(5)
+    x = _pm1(rng, (2, 12, 10, 64))
+    L = dict(w=_pm1(rng, (64, 3, 3, 64)), pad=1, thr=rng.integers(-20, 21, 64).astype(np.int32),
+             flip=rng.integers(0, 2, 64).astype(np.uint8))
+    s1, b1 = _run_conv(x, L, 2)
+    _, b2 = _run_conv(x, L, 2, want_sums=False)
+    s3, _ = _run_conv(x, L, 2, want_bits=False)
+    assert torch.equal(b1, b2) and torch.equal(s1, s3)
+
+
+def test_bconv_threshold_ties_exact():
+    # thr equal to the actual sums: every output is a tie -> bit = 1 ^ flip.
+    rng = np.random.default_rng(6)
+    x = _pm1(rng, (1, 4, 4, 32))
+    w = _pm1(rng, (32, 3, 3, 32))
+    S = oracle.conv2d(x, w, 1, 1)
+    thr = S[0, 1, 1, :].astype(np.int32)
+    flip = rng.integers(0, 2, 32).astype(np.uint8)
+    L = dict(w=w, pad=1, thr=thr, flip=flip)
+    _, bits = _run_conv(x, L, 0)
+    _, B = _oracle_conv(x, L, 0)
+    assert np.array_equal(words_u32(bits), B)
+    expect = oracle.pack_eq2(np.where(flip == 0, 1, -1).astype(np.int8)[None])[0, 0]
+    assert words_u32(bits)[0, 1, 1, 0] == expect
+
+
+def test_bconv_odd_pool_sizes_keep_all_sums():
+    rng = np.random.default_rng(7)
+    x = _pm1(rng, (2, 7, 9, 64))
+    L = dict(w=_pm1(rng, (64, 3, 3, 64)), pad=1, thr=rng.integers(-9, 10, 64).astype(np.int32),
+             flip=rng.integers(0, 2, 64).astype(np.uint8))
+    sums, bits = _run_conv(x, L, 2)
+    S, B = _oracle_conv(x, L, 2)
+    assert sums.shape == (2, 7, 9, 64) and bits.shape == (2, 3, 4, 2)
+    assert np.array_equal(sums.cpu().numpy(), S)
+    assert np.array_equal(words_u32(bits), B)
+
+
+def test_bconv_deterministic_repeat():
+    x, L = synth.cfg5_case("A", N=2)
+    s1, b1 = _run_conv(x, L, 0)
+    s2, b2 = _run_conv(x, L, 0)
+    assert torch.equal(s1, s2) and torch.equal(b1, b2)
+
+
+def _sample_idx(rng, shape, count):
+    N, Ho, Wo, F = shape
+    idx = np.stack([rng.integers(0, s, count) for s in shape], 1)
+    # always include the four corners and edge midpoints of image 0 and N-1
+    extra = []
+    for n in (0, N - 1):
+        for i in (0, Ho // 2, Ho - 1):
+            for j in (0, Wo // 2, Wo - 1):
+                extra.append((n, i, j, rng.integers(0, F)))
+    return np.concatenate([idx, np.array(extra, np.int64)])
+
+
+@pytest.mark.parametrize("name", ["A", "B", "C"])
+def test_cfg5_full_size_sampled(name):
+    """Full-size layers at batch 64: sampled sums vs the oracle, every sum
+    checked for parity and range, and every output bit vs the oracle's
+    threshold of the GPU sums at the sampled points."""
+    x, L = synth.cfg5_case(name)
+    K = L["KH"] * L["KW"] * L["C"]
+    sums, bits = _run_conv(x, L, 0)
+    S = sums.cpu().numpy()
+    assert ((S - K) % 2 == 0).all() and (np.abs(S) <= K).all()
+    rng = np.random.default_rng(55)
+    idx = _sample_idx(rng, S.shape, 3000)
+    ref = oracle.conv2d_at(x, L["w"], idx, 1, L["pad"])
+    assert np.array_equal(S[tuple(idx.T)], ref)
+    # bits: threshold / flip of the (now verified) sums at sampled pixels
+    pix = np.unique(idx[:, :3], axis=0)[:200]
+    Sp = S[pix[:, 0], pix[:, 1], pix[:, 2]]
+    Bp = oracle.pack_eq2(oracle.threshold(Sp, L["thr"], L["flip"]))
+    assert np.array_equal(words_u32(bits)[pix[:, 0], pix[:, 1], pix[:, 2]], Bp)
+
+
+# ------------------------------------------------------------------ GEMM ---
+def _run_gemm(a, L, garble=False):
+    M, K = a.shape
+    A, B = pack_pm1(a), pack_pm1(L["w"])
+    if garble:
+        _garble_tails(A, K)
+        _garble_tails(B, K)
+    thr = to_device(L["thr"], torch.int32)
+    flip = pack_flips(L["flip"])
+    sums, bits = bnn.bnn_bgemm(A, B, K, thr, flip)
+    torch.cuda.synchronize()
+    return sums.cpu().numpy(), words_u32(bits)
+
+
+def _oracle_gemm(a, L):
+    S = oracle.fc(a, L["w"])
+    return S, oracle.pack_eq2(oracle.threshold(S, L["thr"], L["flip"]))
+
+
+@pytest.mark.parametrize("K", [4096, 4100])
+def test_cfg2_fc_gemm_full_size_bit_exact(K):
+    a, L = synth.cfg2(K)
+    S, B = _run_gemm(a, L, garble=(K == 4100))
+    Sr, Br = _oracle_gemm(a, L)
+    assert np.array_equal(S, Sr)
+    assert np.array_equal(B, Br)
+
+
+GEMM_CASES = [(1, 1, 1), (1, 10, 1024), (2, 33, 31), (5, 100, 33), (16, 1024, 8192),
+              (16, 64, 4100), (17, 40, 96), (64, 1024, 8192), (100, 70, 1000), (3, 4, 18432)]
+
+
+@pytest.mark.parametrize("case", GEMM_CASES, ids=[str(c) for c in GEMM_CASES])
+def test_bgemm_shapes_bit_exact(case):
+    M, N, K = case
+    rng = np.random.default_rng(M * 7919 + N * 31 + K)
+    a = _pm1(rng, (M, K))
+    L = dict(w=_pm1(rng, (N, K)), thr=rng.integers(-8, 9, N).astype(np.int32),
+             flip=rng.integers(0, 2, N).astype(np.uint8))
+    S, B = _run_gemm(a, L, garble=True)
+    Sr, Br = _oracle_gemm(a, L)
+    assert np.array_equal(S, Sr)
+    assert np.array_equal(B, Br)
+
+
+# ---------------------------------------------------------- fp32 1st layer -
+@pytest.mark.parametrize("pool", [0, 2])
+@pytest.mark.parametrize("N,H,W", [(2, 32, 32), (1, 7, 5)])
+def test_fconv_first_layer_exact(pool, N, H, W):
+    L = synth.cfg3_net()[0]
+    x = synth.dyadic_normal(np.random.default_rng(N * H + W), (N, H, W, 3))
+    desc = bnn.conv_desc(N, H, W, 3, L["F"], 3, 3, 1, 1, pool)
+    sums, bits = bnn.bnn_fconv2d_binw(desc, to_device(x), pack_pm1(L["w"]),
+                                      to_device(L["thr"], torch.int32), pack_flips(L["flip"]))
+    torch.cuda.synchronize()
+    S = oracle.fconv2d(x, L["w"], 1, 1)
+    b = oracle.threshold(S, L["thr"], L["flip"])
+    if pool:
+        b = oracle.maxpool2(b)
+    assert np.array_equal(sums.cpu().numpy().astype(np.float64), S)
+    assert np.array_equal(words_u32(bits), oracle.pack_eq2(b))
