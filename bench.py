@@ -210,13 +210,23 @@ def main():
     per_img_us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
 
     # Per-layer kernel times (Table II analogue) and the dominant kernel.
+    # Each layer also runs with BNN_ALGO=valu (XOR-popcount vector kernels
+    # only): the matrix-core ablation.
     dev_layers = [upload_layer(L) for L in layers]
     per_layer = []
+    saved_algo = os.environ.get("BNN_ALGO")
     for (name, kind, g, macs), dl in zip(shapes, dev_layers):
         ms = time_layer(bnn, kind, g, batch, dl, args.layer_reps, torch)
-        row = {"layer": name, "ms": round(ms, 5)}
+        os.environ["BNN_ALGO"] = "valu"
+        ms_valu = time_layer(bnn, kind, g, batch, dl, args.layer_reps, torch)
+        if saved_algo is None:
+            del os.environ["BNN_ALGO"]
+        else:
+            os.environ["BNN_ALGO"] = saved_algo
+        row = {"layer": name, "ms": round(ms, 5), "ms_valu": round(ms_valu, 5)}
         if macs:
             row["GOPS"] = round(2 * macs * batch / (ms * 1e-3) / 1e9, 1)
+            row["GOPS_valu"] = round(2 * macs * batch / (ms_valu * 1e-3) / 1e9, 1)
         per_layer.append(row)
     dom_i = max(range(len(shapes)), key=lambda i: per_layer[i]["ms"] if shapes[i][3] else -1)
     dom_ms = per_layer[dom_i]["ms"]

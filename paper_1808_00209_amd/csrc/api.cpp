@@ -6,6 +6,8 @@
 
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
 
 #include <new>
 
@@ -31,6 +33,23 @@ bnn_status ok() {
 bnn_status hip_status(hipError_t e, const char* where) {
   if (e == hipSuccess) return ok();
   return fail(BNN_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+// Kernel family for binary convs / GEMMs: BNN_ALGO=valu forces the
+// XOR-popcount VALU kernels, BNN_ALGO=mfma prefers the fp4 matrix-core kernel
+// wherever it applies; unset or "auto" picks the matrix cores when the shape
+// allows.  (An ablation switch, read on every call.)
+bool use_mfma(const bnn::ConvGeom& g) {
+  const char* e = getenv("BNN_ALGO");
+  if (e && strcmp(e, "valu") == 0) return false;
+  return bnn::bconv_mfma_supported(g);
+}
+
+hipError_t launch_conv(const bnn::ConvGeom& g, const uint32_t* in, const uint32_t* w,
+                       const int32_t* thr, const uint32_t* flip, int32_t* sums,
+                       uint32_t* bits, hipStream_t s) {
+  if (use_mfma(g)) return bnn::launch_bconv_mfma(g, in, w, thr, flip, sums, bits, s);
+  return bnn::launch_bconv_valu(g, in, w, thr, flip, sums, bits, s);
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -136,8 +155,7 @@ bnn_status gemm_launch(int64_t M, int64_t N, int64_t K, const uint32_t* A,
   g.Wo = g.W;
   g.Hp = 1;
   g.Wp = g.W;
-  return hip_status(bnn::launch_bconv_valu(g, A, B, thr, flip, sums, bits, s),
-                    "bgemm launch");
+  return hip_status(launch_conv(g, A, B, thr, flip, sums, bits, s), "bgemm launch");
 }
 
 }  // namespace
@@ -185,9 +203,8 @@ bnn_status bnn_bconv2d(const bnn_conv_desc* d, const uint32_t* in, const uint32_
     if (st != BNN_OK) return st;
     st = check_outputs(in, w, thr, out_sums, out_bits);
     if (st != BNN_OK) return st;
-    return hip_status(
-        bnn::launch_bconv_valu(g, in, w, thr, flip, out_sums, out_bits, stream),
-        "bconv2d launch");
+    return hip_status(launch_conv(g, in, w, thr, flip, out_sums, out_bits, stream),
+                      "bconv2d launch");
   } catch (...) {
     return fail(BNN_ERR_HIP, "bconv2d: unexpected C++ exception");
   }
@@ -365,7 +382,7 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
           if (l.kind == BNN_LAYER_FCONV_BINW)
             e = bnn::launch_fconv_binw(g, input, l.w, l.thr, l.flip, nullptr, dst, stream);
           else
-            e = bnn::launch_bconv_valu(g, src, l.w, l.thr, l.flip, nullptr, dst, stream);
+            e = launch_conv(g, src, l.w, l.thr, l.flip, nullptr, dst, stream);
           h = g.Hp;
           w = g.Wp;
           c = l.F;

@@ -108,6 +108,155 @@ __global__ __launch_bounds__(256) void fconv_binw_kernel(FconvArgs a) {
   }
 }
 
+// Fast path for few input channels (RGB): lane = filter, so each lane keeps
+// its own KH*KW*C weights as +-1.0 floats in registers, and the image values
+// of the wave's pixels are wave-uniform (scalar loads).  Every multiply-
+// accumulate is then one v_fmac_f32 with an SGPR operand.  A wave covers 64
+// filters x a 2x8 tile of output pixels; the 64 threshold bits of a pixel
+// come from one ballot (two output words), and 2x2 pooling ORs the ballots
+// of the window's four pixels.
+typedef __attribute__((address_space(4))) const float cf32;
+
+constexpr int kTileH = 2;
+constexpr int kTileW = 8;
+
+// acc[q] += sum over kw, c of x[q + kw][c] * w[kw][c] for one kernel row.
+template <int C, int KW>
+__device__ __forceinline__ void row_fma(float (&acc)[kTileW], const float (&xs)[kTileW + KW - 1][C],
+                                        const float* w) {
+#pragma unroll
+  for (int kw = 0; kw < KW; ++kw)
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+#pragma unroll
+      for (int q = 0; q < kTileW; ++q) acc[q] = __builtin_fmaf(xs[q + kw][c], w[kw * C + c], acc[q]);
+}
+
+template <int C, int KH, int KW, bool POOL>
+__global__ __launch_bounds__(256) void fconv_lanef_kernel(FconvArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int fg = blockIdx.y * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (fg * 64 >= a.F) return;  // wave-uniform, no barrier in this kernel
+  const int f = fg * 64 + lane;
+  const bool fvalid = f < a.F;
+
+  // This lane's weights as +-1.0 (bit 1 -> +1).
+  float wv[KH * KW * C];
+  {
+    const uint32_t* wr = a.w + static_cast<size_t>(fvalid ? f : 0) * a.fstride;
+#pragma unroll
+    for (int t = 0; t < KH * KW; ++t) {
+#pragma unroll
+      for (int c = 0; c < C; ++c) {
+        const uint32_t word = wr[t * a.Cw + (c >> 5)];
+        wv[t * C + c] = ((word >> (31 - (c & 31))) & 1u) ? 1.0f : -1.0f;
+      }
+    }
+  }
+  const float th = fvalid ? static_cast<float>(a.thr ? a.thr[f] : 0) : 0.0f;
+
+  // Output tile.
+  const int tiles_w = (a.Wo + kTileW - 1) / kTileW;
+  const int tiles_h = (a.Ho + kTileH - 1) / kTileH;
+  int b = blockIdx.x;
+  const int tw = b % tiles_w;
+  b /= tiles_w;
+  const int tt = b % tiles_h;
+  const int n = b / tiles_h;
+  const int i0 = tt * kTileH;
+  const int j0 = tw * kTileW;
+  cf32* img = (cf32*)(a.in) + static_cast<size_t>(n) * a.H * a.W * C;
+
+  uint64_t mask[kTileH][kTileW];
+#pragma unroll
+  for (int r = 0; r < kTileH; ++r) {
+    const int i = i0 + r;
+    float acc[kTileW];
+#pragma unroll
+    for (int q = 0; q < kTileW; ++q) acc[q] = 0.0f;
+#pragma unroll
+    for (int kh = 0; kh < KH; ++kh) {
+      const int hi = i + kh - a.pad;
+      if (hi < 0 || hi >= a.H || i >= a.Ho) continue;  // uniform
+      cf32* row = img + static_cast<size_t>(hi) * a.W * C;
+      const int cfirst = j0 - a.pad;
+      // The multiply-accumulates sit inside each branch so that the image
+      // values stay in SGPRs (no merge of the two paths into VGPRs).
+      if (cfirst >= 0 && cfirst + kTileW + KW - 1 <= a.W) {
+        // Interior: one contiguous run of (kTileW + KW - 1) * C values.
+        cf32* seg = row + cfirst * C;
+        float xs[kTileW + KW - 1][C];
+#pragma unroll
+        for (int q = 0; q < kTileW + KW - 1; ++q)
+#pragma unroll
+          for (int c = 0; c < C; ++c) xs[q][c] = seg[q * C + c];
+        row_fma<C, KW>(acc, xs, wv + kh * KW * C);
+      } else {
+        // Image border: columns outside [0, W) read as 0.0 (the pad value).
+        float xs[kTileW + KW - 1][C];
+#pragma unroll
+        for (int q = 0; q < kTileW + KW - 1; ++q) {
+          const int col = cfirst + q;
+          const bool ok = col >= 0 && col < a.W;
+          const int cl = min(max(col, 0), a.W - 1);
+#pragma unroll
+          for (int c = 0; c < C; ++c) {
+            const float v = row[cl * C + c];
+            xs[q][c] = ok ? v : 0.0f;
+          }
+        }
+        row_fma<C, KW>(acc, xs, wv + kh * KW * C);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kTileW; ++q) {
+      const int j = j0 + q;
+      const bool pix = i < a.Ho && j < a.Wo;
+      if (a.sums && pix && fvalid)
+        a.sums[(static_cast<size_t>(n * a.Ho + i) * a.Wo + j) * a.F + f] = acc[q];
+      mask[r][q] = __ballot(fvalid && acc[q] >= th);
+    }
+  }
+  if (!a.bits) return;
+  // Two output words per pixel: filters 64 fg + 0..31 and + 32..63.
+  const int w0 = 2 * fg;
+  const uint32_t fl0 = a.flip ? a.flip[w0] : 0u;
+  const uint32_t fl1 = (a.flip && w0 + 1 < a.Fw) ? a.flip[w0 + 1] : 0u;
+  const uint32_t tm0 = (w0 == a.Fw - 1) ? tail_mask(a.F) : ~0u;
+  const uint32_t tm1 = (w0 + 1 == a.Fw - 1) ? tail_mask(a.F) : ~0u;
+  if constexpr (POOL) {
+#pragma unroll
+    for (int q = 0; q < kTileW; q += 2) {
+      const int ip = i0 / 2, jp = (j0 + q) / 2;
+      if (ip >= a.Hp || jp >= a.Wp) continue;
+      uint32_t lo = 0, hi = 0;
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int d = 0; d < 2; ++d) {
+          lo |= __brev(static_cast<uint32_t>(mask[r][q + d])) ^ fl0;
+          hi |= __brev(static_cast<uint32_t>(mask[r][q + d] >> 32)) ^ fl1;
+        }
+      uint32_t* op = a.bits + (static_cast<size_t>(n * a.Hp + ip) * a.Wp + jp) * a.Fw + w0;
+      if (lane == 0) op[0] = lo & tm0;
+      if (lane == 1 && w0 + 1 < a.Fw) op[1] = hi & tm1;
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < kTileH; ++r)
+#pragma unroll
+      for (int q = 0; q < kTileW; ++q) {
+        const int i = i0 + r, j = j0 + q;
+        if (i >= a.Ho || j >= a.Wo) continue;
+        const uint32_t lo = (__brev(static_cast<uint32_t>(mask[r][q])) ^ fl0) & tm0;
+        const uint32_t hi = (__brev(static_cast<uint32_t>(mask[r][q] >> 32)) ^ fl1) & tm1;
+        uint32_t* op = a.bits + (static_cast<size_t>(n * a.Ho + i) * a.Wo + j) * a.Fw + w0;
+        if (lane == 0) op[0] = lo;
+        if (lane == 1 && w0 + 1 < a.Fw) op[1] = hi;
+      }
+  }
+}
+
 hipError_t run_fconv(const ConvGeom& g, bool pool, const float* in,
                      const uint32_t* w, const int32_t* thr,
                      const uint32_t* flip, float* sums, uint32_t* bits,
@@ -154,10 +303,60 @@ hipError_t run_fconv(const ConvGeom& g, bool pool, const float* in,
 
 }  // namespace
 
+template <int C>
+hipError_t run_lanef(const ConvGeom& g, bool pool, const float* in, const uint32_t* w,
+                     const int32_t* thr, const uint32_t* flip, float* sums, uint32_t* bits,
+                     hipStream_t s) {
+  FconvArgs a;
+  a.in = in;
+  a.w = w;
+  a.thr = thr;
+  a.flip = flip;
+  a.sums = sums;
+  a.bits = bits;
+  a.N = g.N;
+  a.H = g.H;
+  a.W = g.W;
+  a.C = g.C;
+  a.Cw = g.Cw;
+  a.F = g.F;
+  a.Fw = g.Fw;
+  a.KH = g.KH;
+  a.KW = g.KW;
+  a.pad = g.pad;
+  a.Ho = g.Ho;
+  a.Wo = g.Wo;
+  a.Hp = g.Hp;
+  a.Wp = g.Wp;
+  a.fstride = g.KH * g.KW * g.Cw;
+  a.items = 0;
+  const int fgroups = (g.F + 63) / 64;
+  const int wpb = fgroups < 4 ? fgroups : 4;
+  const unsigned tiles = static_cast<unsigned>(g.N) * ((g.Ho + kTileH - 1) / kTileH) *
+                         ((g.Wo + kTileW - 1) / kTileW);
+  dim3 grid(tiles, static_cast<unsigned>((fgroups + wpb - 1) / wpb));
+  if (pool)
+    fconv_lanef_kernel<C, 3, 3, true><<<grid, dim3(64 * wpb), 0, s>>>(a);
+  else
+    fconv_lanef_kernel<C, 3, 3, false><<<grid, dim3(64 * wpb), 0, s>>>(a);
+  return hipGetLastError();
+}
+
 hipError_t launch_fconv_binw(const ConvGeom& g, const float* in,
                              const uint32_t* w, const int32_t* thr,
                              const uint32_t* flip, float* sums,
                              uint32_t* bits, hipStream_t s) {
+  // Few channels and a 3x3 kernel: the lane-per-filter kernel (its 2x8 pixel
+  // tiles sit on even coordinates, so 2x2 windows never straddle tiles).
+  if (g.KH == 3 && g.KW == 3 && g.C <= 4) {
+    const bool pool = g.pool == 2;
+    switch (g.C) {
+      case 1: return run_lanef<1>(g, pool, in, w, thr, flip, sums, bits, s);
+      case 2: return run_lanef<2>(g, pool, in, w, thr, flip, sums, bits, s);
+      case 3: return run_lanef<3>(g, pool, in, w, thr, flip, sums, bits, s);
+      default: return run_lanef<4>(g, pool, in, w, thr, flip, sums, bits, s);
+    }
+  }
   if (g.pool == 2 && sums && ((g.Ho & 1) || (g.Wo & 1))) {
     hipError_t e = run_fconv(g, false, in, w, thr, flip, sums, nullptr, s);
     if (e != hipSuccess || !bits) return e;

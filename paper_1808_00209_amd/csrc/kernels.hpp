@@ -33,6 +33,14 @@ hipError_t launch_bconv_valu(const ConvGeom& g, const uint32_t* in,
                              const uint32_t* flip, int32_t* sums,
                              uint32_t* bits, hipStream_t s);
 
+// Binary conv on the matrix cores (fp4 MFMA).  Supported when
+// bconv_mfma_supported(g): C a multiple of 128 and F a multiple of 32.
+bool bconv_mfma_supported(const ConvGeom& g);
+hipError_t launch_bconv_mfma(const ConvGeom& g, const uint32_t* in,
+                             const uint32_t* w, const int32_t* thr,
+                             const uint32_t* flip, int32_t* sums,
+                             uint32_t* bits, hipStream_t s);
+
 // Binary GEMM for a handful of rows (M <= 16): one output column per lane,
 // the K words split over the waves of a block.
 hipError_t launch_bgemv_valu(int64_t M, int64_t N, int64_t K,

@@ -14,6 +14,12 @@ from paper_1808_00209_amd.device import to_device, upload_network
 pytestmark = pytest.mark.gpu
 
 
+@pytest.fixture(params=["auto", "valu"])
+def algo(request, monkeypatch):
+    monkeypatch.setenv("BNN_ALGO", request.param)
+    return request.param
+
+
 def _gpu_logits(layers, x):
     N, H, W, C = x.shape
     net = upload_network(layers, H, W, C)
@@ -23,7 +29,7 @@ def _gpu_logits(layers, x):
 
 
 @pytest.mark.parametrize("batch", [1, 3])
-def test_cifar_net_small_batch(batch):
+def test_cifar_net_small_batch(batch, algo):
     layers, x = synth.cfg3_net(), synth.cfg3_input(batch)
     got = _gpu_logits(layers, x)
     ref = oracle.forward(layers, x)
@@ -31,7 +37,7 @@ def test_cifar_net_small_batch(batch):
     assert np.array_equal(got, ref)
 
 
-def test_vehicle_net_small_batch():
+def test_vehicle_net_small_batch(algo):
     layers, x = synth.cfg4_net(), synth.cfg4_input(2)
     got = _gpu_logits(layers, x)
     ref = oracle.forward(layers, x)
@@ -39,7 +45,7 @@ def test_vehicle_net_small_batch():
     assert np.array_equal(got, ref)
 
 
-def test_cifar_net_batch64_sampled_images():
+def test_cifar_net_batch64_sampled_images(algo):
     layers, x = synth.cfg3_net(), synth.cfg3_input(64)
     got = _gpu_logits(layers, x)
     pick = [0, 17, 63]
@@ -47,7 +53,7 @@ def test_cifar_net_batch64_sampled_images():
     assert np.array_equal(got[pick], ref)
 
 
-def test_vehicle_net_batch256_sampled_images():
+def test_vehicle_net_batch256_sampled_images(algo):
     layers, x = synth.cfg4_net(), synth.cfg4_input(256)
     got = _gpu_logits(layers, x)
     pick = [0, 255]

@@ -15,6 +15,17 @@ from paper_1808_00209_amd.device import pack_flips, pack_pm1, to_device, words_u
 
 pytestmark = pytest.mark.gpu
 
+# Kernel families: "auto" takes the fp4 matrix-core kernel wherever the shape
+# allows it (C a multiple of 128, F a multiple of 64), "valu" forces the
+# XOR-popcount vector kernels everywhere.
+ALGOS = ["auto", "valu"]
+
+
+@pytest.fixture(params=ALGOS)
+def algo(request, monkeypatch):
+    monkeypatch.setenv("BNN_ALGO", request.param)
+    return request.param
+
 
 def _pm1(rng, shape):
     return (rng.integers(0, 2, size=shape) * 2 - 1).astype(np.int8)
@@ -92,7 +103,7 @@ def _oracle_conv(x, L, pool):
     return S, oracle.pack_eq2(b)
 
 
-def test_cfg1_single_conv_bit_exact():
+def test_cfg1_single_conv_bit_exact(algo):
     x, L = synth.cfg1_input(), synth.cfg1_layer()
     sums, bits = _run_conv(x, L, 0)
     S, B = _oracle_conv(x, L, 0)
@@ -113,12 +124,25 @@ CONV_CASES = [
     (1, 5, 6, 512, 32, 3, 0, 0),
     (4, 6, 6, 3, 10, 3, 1, 2),
     (1, 8, 8, 320, 64, 3, 1, 0),
+    # shapes the matrix-core kernel takes (C % 128 == 0, F % 64 == 0)
+    (2, 9, 7, 128, 64, 3, 1, 0),
+    (1, 16, 16, 128, 128, 3, 1, 2),
+    (3, 5, 7, 256, 64, 3, 1, 2),
+    (1, 6, 6, 256, 192, 3, 0, 0),
+    (2, 4, 4, 512, 128, 3, 1, 0),
+    (1, 7, 9, 512, 64, 3, 1, 2),
+    (1, 3, 3, 1024, 64, 3, 1, 0),
+    (2, 11, 5, 384, 64, 1, 0, 0),
+    (1, 1, 1, 128, 64, 3, 1, 0),
+    (2, 5, 5, 128, 96, 3, 1, 2),
+    (1, 12, 12, 256, 32, 3, 1, 0),
+    (64, 8, 8, 512, 512, 3, 1, 2),
 ]
 
 
 @pytest.mark.parametrize("case", CONV_CASES, ids=[str(c) for c in CONV_CASES])
 @pytest.mark.parametrize("garble", [False, True])
-def test_bconv_shapes_bit_exact(case, garble):
+def test_bconv_shapes_bit_exact(case, garble, algo):
     N, H, W, C, F, k, pad, pool = case
     rng = np.random.default_rng(hash(case) % 2 ** 32)
     x = _pm1(rng, (N, H, W, C))
@@ -132,10 +156,11 @@ def test_bconv_shapes_bit_exact(case, garble):
     assert np.array_equal(words_u32(bits), B)
 
 
-def test_bconv_bits_only_and_sums_only_agree():
+@pytest.mark.parametrize("C", [64, 128])
+def test_bconv_bits_only_and_sums_only_agree(C, algo):
     rng = np.random.default_rng(5)
-    x = _pm1(rng, (2, 12, 10, 64))
-    L = dict(w=_pm1(rng, (64, 3, 3, 64)), pad=1, thr=rng.integers(-20, 21, 64).astype(np.int32),
+    x = _pm1(rng, (2, 12, 10, C))
+    L = dict(w=_pm1(rng, (64, 3, 3, C)), pad=1, thr=rng.integers(-20, 21, 64).astype(np.int32),
              flip=rng.integers(0, 2, 64).astype(np.uint8))
     s1, b1 = _run_conv(x, L, 2)
     _, b2 = _run_conv(x, L, 2, want_sums=False)
@@ -143,26 +168,39 @@ def test_bconv_bits_only_and_sums_only_agree():
     assert torch.equal(b1, b2) and torch.equal(s1, s3)
 
 
-def test_bconv_threshold_ties_exact():
+@pytest.mark.parametrize("C,F", [(32, 32), (128, 64)])
+def test_bconv_threshold_ties_exact(C, F, algo):
     # thr equal to the actual sums: every output is a tie -> bit = 1 ^ flip.
     rng = np.random.default_rng(6)
-    x = _pm1(rng, (1, 4, 4, 32))
-    w = _pm1(rng, (32, 3, 3, 32))
+    x = _pm1(rng, (1, 4, 4, C))
+    w = _pm1(rng, (F, 3, 3, C))
     S = oracle.conv2d(x, w, 1, 1)
     thr = S[0, 1, 1, :].astype(np.int32)
-    flip = rng.integers(0, 2, 32).astype(np.uint8)
+    flip = rng.integers(0, 2, F).astype(np.uint8)
     L = dict(w=w, pad=1, thr=thr, flip=flip)
     _, bits = _run_conv(x, L, 0)
     _, B = _oracle_conv(x, L, 0)
     assert np.array_equal(words_u32(bits), B)
-    expect = oracle.pack_eq2(np.where(flip == 0, 1, -1).astype(np.int8)[None])[0, 0]
-    assert words_u32(bits)[0, 1, 1, 0] == expect
+    expect = oracle.pack_eq2(np.where(flip == 0, 1, -1).astype(np.int8)[None])[0]
+    assert np.array_equal(words_u32(bits)[0, 1, 1], expect)
 
 
-def test_bconv_odd_pool_sizes_keep_all_sums():
+@pytest.mark.parametrize("C,F", [(64, 32), (128, 64)])
+def test_bconv_extreme_thresholds(C, F, algo):
+    rng = np.random.default_rng(8)
+    x = _pm1(rng, (1, 5, 5, C))
+    thr = np.array(([-2 ** 31, 2 ** 31 - 1, 0, 1, -1, 9 * C, -9 * C, 9 * C + 1] * F)[:F], np.int32)
+    L = dict(w=_pm1(rng, (F, 3, 3, C)), pad=1, thr=thr, flip=rng.integers(0, 2, F).astype(np.uint8))
+    _, bits = _run_conv(x, L, 0)
+    _, B = _oracle_conv(x, L, 0)
+    assert np.array_equal(words_u32(bits), B)
+
+
+@pytest.mark.parametrize("C", [64, 256])
+def test_bconv_odd_pool_sizes_keep_all_sums(C, algo):
     rng = np.random.default_rng(7)
-    x = _pm1(rng, (2, 7, 9, 64))
-    L = dict(w=_pm1(rng, (64, 3, 3, 64)), pad=1, thr=rng.integers(-9, 10, 64).astype(np.int32),
+    x = _pm1(rng, (2, 7, 9, C))
+    L = dict(w=_pm1(rng, (64, 3, 3, C)), pad=1, thr=rng.integers(-9, 10, 64).astype(np.int32),
              flip=rng.integers(0, 2, 64).astype(np.uint8))
     sums, bits = _run_conv(x, L, 2)
     S, B = _oracle_conv(x, L, 2)
@@ -171,7 +209,7 @@ def test_bconv_odd_pool_sizes_keep_all_sums():
     assert np.array_equal(words_u32(bits), B)
 
 
-def test_bconv_deterministic_repeat():
+def test_bconv_deterministic_repeat(algo):
     x, L = synth.cfg5_case("A", N=2)
     s1, b1 = _run_conv(x, L, 0)
     s2, b2 = _run_conv(x, L, 0)
@@ -191,7 +229,7 @@ def _sample_idx(rng, shape, count):
 
 
 @pytest.mark.parametrize("name", ["A", "B", "C"])
-def test_cfg5_full_size_sampled(name):
+def test_cfg5_full_size_sampled(name, algo):
     """Full-size layers at batch 64: sampled sums vs the oracle, every sum
     checked for parity and range, and every output bit vs the oracle's
     threshold of the GPU sums at the sampled points."""
@@ -231,7 +269,7 @@ def _oracle_gemm(a, L):
 
 
 @pytest.mark.parametrize("K", [4096, 4100])
-def test_cfg2_fc_gemm_full_size_bit_exact(K):
+def test_cfg2_fc_gemm_full_size_bit_exact(K, algo):
     a, L = synth.cfg2(K)
     S, B = _run_gemm(a, L, garble=(K == 4100))
     Sr, Br = _oracle_gemm(a, L)
@@ -240,11 +278,12 @@ def test_cfg2_fc_gemm_full_size_bit_exact(K):
 
 
 GEMM_CASES = [(1, 1, 1), (1, 10, 1024), (2, 33, 31), (5, 100, 33), (16, 1024, 8192),
-              (16, 64, 4100), (17, 40, 96), (64, 1024, 8192), (100, 70, 1000), (3, 4, 18432)]
+              (16, 64, 4100), (17, 40, 96), (64, 1024, 8192), (100, 70, 1000), (3, 4, 18432),
+              (65, 128, 1024), (300, 64, 18432), (64, 192, 128)]
 
 
 @pytest.mark.parametrize("case", GEMM_CASES, ids=[str(c) for c in GEMM_CASES])
-def test_bgemm_shapes_bit_exact(case):
+def test_bgemm_shapes_bit_exact(case, algo):
     M, N, K = case
     rng = np.random.default_rng(M * 7919 + N * 31 + K)
     a = _pm1(rng, (M, K))
