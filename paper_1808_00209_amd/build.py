@@ -1,8 +1,9 @@
 """Build libbnn.so (HIP kernels + C ABI) for gfx950 with hipcc.
 
 Usage: ``python -m paper_1808_00209_amd.build`` (always recompiles).
-Every source is compiled with the packed-fp32 instructions switched off and
-with fp32 denormals kept (the sign test ``x > 0`` must see them).
+Every source is compiled with the packed-fp32 instructions switched off, with
+fp32 denormals kept (the sign test ``x > 0`` must see them) and with MFMA
+accumulators in VGPRs.
 """
 from __future__ import annotations
 
@@ -26,6 +27,9 @@ COMMON = [
     "-I", INCLUDE, "-I", CSRC,
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-fno-gpu-flush-denormals-to-zero", "-ffp-contract=off",
+    # MFMA accumulators stay in VGPRs (the AGPR form made the compiler copy
+    # every accumulator out and back around each MFMA of the conv loop).
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-Wall", "-Wno-unused-command-line-argument",
 ]
 

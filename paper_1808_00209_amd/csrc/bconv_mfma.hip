@@ -3,24 +3,24 @@
 // A +-1 value is exactly representable in the 4-bit E2M1 float format, and a
 // dot product of K such values is an integer |S| <= K < 2^24, exact in the
 // fp32 accumulator.  So the XOR-popcount dot product of Eq. 4 can equally be
-// computed by v_mfma_scale_f32_16x16x128_f8f6f4 with both operands in fp4:
-// 16x16x128 multiply-accumulates per instruction, against 32 bit-MACs per
-// v_xor + v_bcnt pair on the vector ALU.  Each packed word is expanded to four
-// fp4 registers (one nibble per bit) right before use; the expansion is the
-// same for weights and activations, so the order of the 32 values inside the
-// MFMA's k dimension does not matter, and a sign-swapped encoding (bit 1 ->
-// -1.0, bit 0 -> +1.0) on both sides leaves every product unchanged.  A pad
-// tap is the word 0, i.e. -1 in the method's encoding, as in the VALU kernel.
+// computed by v_mfma_scale_f32_32x32x64_f8f6f4 with both operands in fp4:
+// 32x32x64 multiply-accumulates per instruction (the fastest fp4 shape on
+// MI355X), against 32 bit-MACs per v_xor + v_bcnt pair on the vector ALU.
+// Each packed word is expanded to four fp4 registers (one nibble per bit)
+// right before use; the expansion is the same for weights and activations,
+// so the order of the 32 values inside the MFMA's k dimension does not
+// matter, and a sign-swapped encoding (bit 1 -> -1.0, bit 0 -> +1.0) on both
+// sides leaves every product unchanged.  A pad tap is the word 0, i.e. -1 in
+// the method's encoding, as in the VALU kernel.
 //
-// Operand roles: A (16 rows) = weights of 16 filters, B (16 columns) =
-// activations of 16 output pixels; lane l supplies row / column l % 16 and
-// the l / 16-th quarter of the 128 k values.  The result tile holds, in lane
-// l, register r, the sum for filter 4*(l/16) + r and pixel l % 16.  A wave
-// computes 64 (or 32) filters x 64 pixels (4 (or 2) x 4 tiles); with pooling,
-// the 16 pixels of a tile are four 2x2 windows so that a window sits in 4
-// adjacent lanes.
+// Operand roles: A (32 rows) = weights of 32 filters, B (32 columns) =
+// activations of 32 output pixels; lane l supplies row / column l % 32 and
+// the (l / 32)-th half of the 64 k values.  Register e of the result holds,
+// in lane l, the sum for filter 8*(e/4) + 4*(l/32) + e%4 and pixel l % 32.  A
+// wave computes 64 (or 32) filters x 64 pixels; with pooling, the 32 pixels
+// of a tile are eight 2x2 windows so that a window sits in 4 adjacent lanes.
 //
-// Requirements (bconv_mfma_supported): stride 1, C a multiple of 128, F a
+// Requirements (bconv_mfma_supported): stride 1, C a multiple of 64, F a
 // multiple of 32, at most 32 taps.
 #include <stdlib.h>
 
@@ -31,21 +31,8 @@ namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
 
-struct MfmaArgs {
-  const uint32_t* in;
-  const uint32_t* w;
-  const int32_t* thr;
-  const uint32_t* flip;
-  int32_t* sums;
-  uint32_t* bits;
-  int32_t N, H, W, Cw, F, Fw, KH, KW, pad, Ho, Wo, Hp, Wp;
-  int32_t fstride;  // words per filter, KH*KW*Cw
-  int32_t items;    // output pixels covered (N*Ho*Wo, or 4*N*Hp*Wp when pooling)
-  int32_t K;        // valid bits per window, KH*KW*C
-  int32_t in_bytes; // size of the input buffer (raw-buffer range)
-  int32_t w_bytes;  // size of the weight buffer
-};
 
 // One packed word -> four fp4 registers: register r, nibble n encodes bit
 // 4n + r of the word (1 -> 0xA = -1.0, 0 -> 0x2 = +1.0).  Each register is
@@ -86,26 +73,66 @@ __device__ __forceinline__ void buf_load(uint32_t (&v)[VW], __amdgpu_buffer_rsrc
   }
 }
 
+// Unsigned division by a run-time invariant divisor d >= 1 with a multiply
+// and shifts (Granlund and Montgomery, "Division by invariant integers using
+// multiplication", 1994): exact for every 32-bit n.
+struct FastDiv {
+  uint32_t d, m;
+  int s1, s2;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+  int l = 0;
+  while ((uint64_t{1} << l) < d) ++l;  // l = ceil(log2 d)
+  FastDiv f;
+  f.d = d;
+  f.m = static_cast<uint32_t>(((uint64_t{1} << 32) * ((uint64_t{1} << l) - d)) / d + 1);
+  f.s1 = l < 1 ? l : 1;
+  f.s2 = l > 1 ? l - 1 : 0;
+  return f;
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
+  const uint32_t t = __umulhi(f.m, n);
+  return (t + ((n - t) >> f.s1)) >> f.s2;
+}
+
+struct Mfma32Args {
+  const uint32_t* in;
+  const uint32_t* w;
+  const int32_t* thr;
+  const uint32_t* flip;
+  int32_t* sums;
+  uint32_t* bits;
+  int32_t H, W, Cw, F, Fw, KH, KW, pad, Ho, Wo, Hp, Wp;
+  int32_t fstride;   // words per filter, KH*KW*Cw
+  int32_t items;     // output pixels covered (N*Ho*Wo, or 4*N*Hp*Wp when pooling)
+  int32_t K;         // valid bits per window, KH*KW*C
+  int32_t in_bytes;  // raw-buffer ranges
+  int32_t w_bytes;
+  FastDiv div_w, div_h;  // Wo, Ho (or Wp, Hp when pooling)
+};
+
 // Template parameters:
-//   VW   words each lane loads per operand row and iteration (1, 2 or 4).  One
-//        MFMA k-step covers 4 words (one per lane quarter), so an iteration
-//        (a chunk of 4*VW words of one tap) feeds VW k-steps.
-//   POOL pixels ordered as 2x2 windows (4 adjacent lanes per window).
-//   TF   16-filter tiles per wave (2: one output word, 4: two).
-//   KS   1: the 4 waves of a block take 4 consecutive 64-pixel tiles;
-//        >1: the KS waves of a block share one tile and split the iterations,
-//        adding their partial sums in LDS (for grids too small to fill the
-//        chip).
-//   PD   iterations whose loads are in flight at once (software pipeline).
-template <int VW, bool POOL, int TF, int KS, int PD>
-__global__ __launch_bounds__(512) void bconv_mfma_kernel(MfmaArgs a) {
+//   VW   words each lane loads per operand row and iteration (1 or 2).  One
+//        MFMA k-step covers 2 words (one per lane half), so an iteration (a
+//        chunk of 2*VW words of one tap) feeds VW k-steps.
+//   POOL pixels of a 32-tile ordered as eight 2x2 windows (4 adjacent lanes).
+//   TF   32-filter tiles per wave (1 or 2); a wave always covers 64 pixels.
+//   KS   1: the 4 waves of a block take 4 consecutive 64-pixel groups;
+//        >1: the KS waves of a block split the iterations of one tile and add
+//        their partial sums in LDS (grids too small to fill the chip).
+// Loads run one iteration ahead of the MFMAs (two register sets).
+template <int VW, bool POOL, int TF, int KS>
+__global__ __launch_bounds__(256) void bconv_mfma32_kernel(Mfma32Args a) {
+  constexpr int TP = 2;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int q = lane >> 4;   // k quarter (operands) / row group (result)
-  const int c = lane & 15;   // operand row / column within a 16-tile
+  const int h = lane >> 5;   // k half (operands) / row quad (result)
+  const int c = lane & 31;   // operand row / column within a 32-tile
   const int p0 = (KS == 1 ? blockIdx.x * 4 + wave : blockIdx.x) * 64;
-  const int f0 = blockIdx.y * (16 * TF);
-  const int nchunk = a.Cw / (4 * VW);
+  const int f0 = blockIdx.y * (32 * TF);
+  const int nchunk = a.Cw / (2 * VW);
   const int iters = a.KH * a.KW * nchunk;
   int it0 = 0, it1 = iters;
   if constexpr (KS > 1) {
@@ -114,49 +141,47 @@ __global__ __launch_bounds__(512) void bconv_mfma_kernel(MfmaArgs a) {
     it1 = min(iters, it0 + per);
   }
 
-  // Pixels this lane loads for (one per pixel tile): word offset of the
-  // pixel in the input, and which of the KH*KW taps fall inside the image.
-  int pbase[4], pn[4], pi[4], pj[4];
-  uint32_t tapmask[4];
-  bool pv[4];
+  // This lane's pixel in each of the TP pixel tiles: byte offset of its
+  // first load, and which taps fall inside the image.
+  int pbase[TP], pn[TP], pi[TP], pj[TP];
+  uint32_t tapmask[TP];
+  bool pv[TP];
 #pragma unroll
-  for (int tp = 0; tp < 4; ++tp) {
-    const int item = p0 + tp * 16 + c;
+  for (int tp = 0; tp < TP; ++tp) {
+    const int item = p0 + tp * 32 + c;
     pv[tp] = item < a.items;
-    const int m = pv[tp] ? item : 0;
+    const uint32_t m = pv[tp] ? static_cast<uint32_t>(item) : 0u;
+    uint32_t pix = POOL ? (m >> 2) : m;
+    const uint32_t t = fdiv(pix, a.div_w);
+    const uint32_t jj = pix - t * a.div_w.d;
+    const uint32_t nn = fdiv(t, a.div_h);
+    const uint32_t ii = t - nn * a.div_h.d;
+    pn[tp] = static_cast<int>(nn);
     if constexpr (POOL) {
-      const int win = m >> 2;
-      const int jp = win % a.Wp;
-      const int t = win / a.Wp;
-      const int ip = t % a.Hp;
-      pn[tp] = t / a.Hp;
-      pi[tp] = 2 * ip + ((m >> 1) & 1);
-      pj[tp] = 2 * jp + (m & 1);
+      pi[tp] = 2 * static_cast<int>(ii) + static_cast<int>((m >> 1) & 1);
+      pj[tp] = 2 * static_cast<int>(jj) + static_cast<int>(m & 1);
     } else {
-      pj[tp] = m % a.Wo;
-      const int t = m / a.Wo;
-      pi[tp] = t % a.Ho;
-      pn[tp] = t / a.Ho;
+      pi[tp] = static_cast<int>(ii);
+      pj[tp] = static_cast<int>(jj);
     }
-    pbase[tp] = (((pn[tp] * a.H + pi[tp]) * a.W + pj[tp]) * a.Cw + q * VW) * 4;
+    pbase[tp] = (((pn[tp] * a.H + pi[tp]) * a.W + pj[tp]) * a.Cw + h * VW) * 4;
+    // rows kh with 0 <= i + kh - pad < H, columns likewise
+    const int rlo = max(0, a.pad - pi[tp]), rhi = min(a.KH, a.H + a.pad - pi[tp]);
+    const int clo = max(0, a.pad - pj[tp]), chi = min(a.KW, a.W + a.pad - pj[tp]);
+    const uint32_t cm = chi > clo ? ((1u << chi) - 1u) & ~((1u << clo) - 1u) : 0u;
     uint32_t mk = 0;
-    for (int kh = 0; kh < a.KH; ++kh)
-      for (int kw = 0; kw < a.KW; ++kw) {
-        const int hi = pi[tp] + kh - a.pad, wi = pj[tp] + kw - a.pad;
-        const bool ok = pv[tp] && static_cast<unsigned>(hi) < static_cast<unsigned>(a.H) &&
-                        static_cast<unsigned>(wi) < static_cast<unsigned>(a.W);
-        mk |= static_cast<uint32_t>(ok) << (kh * a.KW + kw);
-      }
-    tapmask[tp] = mk;
+    for (int kh = rlo; kh < rhi; ++kh) mk |= cm << (kh * a.KW);
+    tapmask[tp] = pv[tp] ? mk : 0u;
   }
 
-  v4f acc[TF][4];
+  v16f acc[TF][TP];
 #pragma unroll
   for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
-    for (int tp = 0; tp < 4; ++tp) acc[tf][tp] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int tp = 0; tp < TP; ++tp)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[tf][tp][e] = 0.0f;
 
-  // Buffer resources; per-lane byte offsets of the weight rows and pixels.
   const __amdgpu_buffer_rsrc_t rin = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint32_t*>(a.in), 0, a.in_bytes, kRsrcWord3);
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
@@ -164,74 +189,87 @@ __global__ __launch_bounds__(512) void bconv_mfma_kernel(MfmaArgs a) {
   uint32_t woff[TF];
 #pragma unroll
   for (int tf = 0; tf < TF; ++tf)
-    woff[tf] = static_cast<uint32_t>(((f0 + tf * 16 + c) * a.fstride + q * VW) * 4);
+    woff[tf] = static_cast<uint32_t>(((f0 + tf * 32 + c) * a.fstride + h * VW) * 4);
   const uint32_t smask = __builtin_amdgcn_readfirstlane(0x88888888u);
   uint32_t vfill;
   asm("v_mov_b32 %0, 0x22222222" : "=v"(vfill));
 
-  // Loads of iteration `it` (clamped into range so that every load is
-  // unconditional; the clamped repeats at the end are never used).
-  auto load_it = [&](int it, uint32_t (&ww)[TF][VW], uint32_t (&aw)[4][VW]) {
-    const int tap = it / nchunk;
-    const int cc = (it - tap * nchunk) * 4 * VW;
-    const int kh = tap / a.KW;
-    const int kw = tap - kh * a.KW;
-    const uint32_t wsoff = static_cast<uint32_t>((tap * a.Cw + cc) * 4);
+  // Loop position of the next load (wave-uniform): tap (kh, kw) and word
+  // chunk cc, advanced incrementally (no divisions inside the loop); it stops
+  // at the last iteration, so the clamped extra loads repeat it.
+  int l_it = it0, l_cc = 0, l_kh = 0, l_kw = 0;
+  {
+    const int tap = it0 / nchunk;
+    l_cc = (it0 - tap * nchunk) * 2 * VW;
+    l_kh = tap / a.KW;
+    l_kw = tap - l_kh * a.KW;
+  }
+  auto load_next = [&](uint32_t (&ww)[TF][VW], uint32_t (&aw)[TP][VW]) {
+    const int tap = l_kh * a.KW + l_kw;
+    const uint32_t wsoff = static_cast<uint32_t>((tap * a.Cw + l_cc) * 4);
 #pragma unroll
     for (int tf = 0; tf < TF; ++tf) buf_load<VW>(ww[tf], rw, woff[tf], wsoff);
-    const int dshift = (((kh - a.pad) * a.W + (kw - a.pad)) * a.Cw + cc) * 4;
+    const int dshift = (((l_kh - a.pad) * a.W + (l_kw - a.pad)) * a.Cw + l_cc) * 4;
     const uint32_t bit = 1u << tap;
 #pragma unroll
-    for (int tp = 0; tp < 4; ++tp) {
+    for (int tp = 0; tp < TP; ++tp) {
       const uint32_t off = (tapmask[tp] & bit) ? static_cast<uint32_t>(pbase[tp] + dshift)
                                                : kOutOfRange;
       buf_load<VW>(aw[tp], rin, off, 0u);
     }
+    if (l_it + 1 < it1) {
+      ++l_it;
+      l_cc += 2 * VW;
+      if (l_cc == a.Cw) {
+        l_cc = 0;
+        if (++l_kw == a.KW) {
+          l_kw = 0;
+          ++l_kh;
+        }
+      }
+    }
   };
-  auto compute = [&](const uint32_t (&ww)[TF][VW], const uint32_t (&aw)[4][VW]) {
+  auto compute = [&](const uint32_t (&ww)[TF][VW], const uint32_t (&aw)[TP][VW]) {
 #pragma unroll
     for (int v = 0; v < VW; ++v) {
-      v8i A[TF], B[4];
+      v8i A[TF], B[TP];
 #pragma unroll
       for (int tf = 0; tf < TF; ++tf) A[tf] = expand_fp4(ww[tf][v], smask, vfill);
 #pragma unroll
-      for (int tp = 0; tp < 4; ++tp) B[tp] = expand_fp4(aw[tp][v], smask, vfill);
+      for (int tp = 0; tp < TP; ++tp) B[tp] = expand_fp4(aw[tp][v], smask, vfill);
 #pragma unroll
       for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
-        for (int tp = 0; tp < 4; ++tp)
-          acc[tf][tp] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
+        for (int tp = 0; tp < TP; ++tp)
+          acc[tf][tp] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
               A[tf], B[tp], acc[tf][tp], 4, 4, 0, 127, 0, 127);
     }
   };
 
-  // A ring of PD register sets: the loads of PD iterations are in flight at
-  // once, so a wave waits for memory about once per PD iterations (each
-  // dependent round trip to L2 / HBM costs far more than one iteration of
-  // MFMAs).  Loads past the end are clamped to the last iteration and unused.
   if (it0 < it1) {
-    uint32_t wr[PD][TF][VW], xr[PD][4][VW];
-#pragma unroll
-    for (int s = 0; s < PD; ++s) load_it(min(it0 + s, it1 - 1), wr[s], xr[s]);
-    __builtin_amdgcn_sched_barrier(0);
-    for (int it = it0; it < it1; it += PD) {
-#pragma unroll
-      for (int s = 0; s < PD; ++s) {
-        if (it + s < it1) compute(wr[s], xr[s]);
-        __builtin_amdgcn_sched_barrier(0);
-        load_it(min(it + s + PD, it1 - 1), wr[s], xr[s]);
-        __builtin_amdgcn_sched_barrier(0);
-      }
+    uint32_t wa[TF][VW], xa[TP][VW], wb[TF][VW], xb[TP][VW];
+    load_next(wa, xa);
+    for (int it = it0; it < it1; it += 2) {
+      // The scheduling barriers keep each prefetch ahead of the MFMAs it
+      // overlaps (the scheduler would otherwise sink the loads below them).
+      load_next(wb, xb);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(wa, xa);
+      __builtin_amdgcn_sched_barrier(0);
+      load_next(wa, xa);
+      __builtin_amdgcn_sched_barrier(0);
+      if (it + 1 < it1) compute(wb, xb);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
   if constexpr (KS > 1) {
-    __shared__ v4f part[KS - 1][TF][4][64];
+    __shared__ v16f part[KS - 1][TF][TP][64];
     if (wave > 0) {
 #pragma unroll
       for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
-        for (int tp = 0; tp < 4; ++tp) part[wave - 1][tf][tp][lane] = acc[tf][tp];
+        for (int tp = 0; tp < TP; ++tp) part[wave - 1][tf][tp][lane] = acc[tf][tp];
     }
     __syncthreads();
     if (wave > 0) return;
@@ -240,26 +278,28 @@ __global__ __launch_bounds__(512) void bconv_mfma_kernel(MfmaArgs a) {
 #pragma unroll
       for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
-        for (int tp = 0; tp < 4; ++tp) acc[tf][tp] += part[w][tf][tp][lane];
+        for (int tp = 0; tp < TP; ++tp) acc[tf][tp] += part[w][tf][tp][lane];
   }
 
-  // Epilogue.  Lane (q, c) holds, for pixel tile tp, the sums of pixel c and
-  // filters f0 + 16 tf + 4 q + r (r = 0..3).
+  // Epilogue.  Lane (h, c) holds, in register e of tile (tf, tp), the sum of
+  // pixel c and filter f0 + 32 tf + 8 (e / 4) + 4 h + (e % 4).
   if (a.sums) {
 #pragma unroll
-    for (int tp = 0; tp < 4; ++tp) {
+    for (int tp = 0; tp < TP; ++tp) {
       if (!pv[tp]) continue;
       int32_t* sp = a.sums + (static_cast<size_t>(pn[tp] * a.Ho + pi[tp]) * a.Wo + pj[tp]) * a.F +
-                    f0 + 4 * q;
+                    f0 + 4 * h;
 #pragma unroll
-      for (int tf = 0; tf < TF; ++tf) {
-        int4 t;
-        t.x = static_cast<int>(acc[tf][tp][0]);
-        t.y = static_cast<int>(acc[tf][tp][1]);
-        t.z = static_cast<int>(acc[tf][tp][2]);
-        t.w = static_cast<int>(acc[tf][tp][3]);
-        *reinterpret_cast<int4*>(sp + tf * 16) = t;
-      }
+      for (int tf = 0; tf < TF; ++tf)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          int4 t;
+          t.x = static_cast<int>(acc[tf][tp][4 * g + 0]);
+          t.y = static_cast<int>(acc[tf][tp][4 * g + 1]);
+          t.z = static_cast<int>(acc[tf][tp][4 * g + 2]);
+          t.w = static_cast<int>(acc[tf][tp][4 * g + 3]);
+          *reinterpret_cast<int4*>(sp + tf * 32 + 8 * g) = t;
+        }
     }
   }
   if (a.bits) {
@@ -267,48 +307,43 @@ __global__ __launch_bounds__(512) void bconv_mfma_kernel(MfmaArgs a) {
     // integer S, so the sign bit of that difference is the output bit.
     // Thresholds are clamped to [-K-1, K+1] first (|S| <= K, so this keeps
     // every comparison) to stay exact in fp32 for any int32 threshold.
-    constexpr int NW = TF / 2;  // output words per pixel in this wave
-    float th[TF][4];
+    float th[TF][16];
 #pragma unroll
     for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int t = a.thr[f0 + tf * 16 + 4 * q + r];
-        th[tf][r] = static_cast<float>(min(max(t, -a.K - 1), a.K + 1)) - 0.5f;
+      for (int e = 0; e < 16; ++e) {
+        const int t = a.thr[f0 + tf * 32 + 8 * (e >> 2) + 4 * h + (e & 3)];
+        th[tf][e] = static_cast<float>(min(max(t, -a.K - 1), a.K + 1)) - 0.5f;
       }
-    uint32_t fl[NW];
+    uint32_t fl[TF];
 #pragma unroll
-    for (int h = 0; h < NW; ++h) fl[h] = a.flip ? a.flip[f0 / 32 + h] : 0u;
+    for (int tf = 0; tf < TF; ++tf) fl[tf] = a.flip ? a.flip[f0 / 32 + tf] : 0u;
 #pragma unroll
-    for (int tp = 0; tp < 4; ++tp) {
-      uint32_t word[NW];
-#pragma unroll
-      for (int h = 0; h < NW; ++h) word[h] = 0u;
+    for (int tp = 0; tp < TP; ++tp) {
+      uint32_t word[TF];
 #pragma unroll
       for (int tf = 0; tf < TF; ++tf) {
+        uint32_t wd = 0u;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float d = th[tf][r] - acc[tf][tp][r];
-          const uint32_t sgn = __float_as_uint(d) >> 31;
-          // filter 16 (tf % 2) + 4 q + r of output word tf / 2 -> bit 31 - that
-          word[tf >> 1] |= sgn << (31 - (16 * (tf & 1) + 4 * q + r));
+        for (int e = 0; e < 16; ++e) {
+          const float d = th[tf][e] - acc[tf][tp][e];
+          // filter 8 (e/4) + 4 h + e%4 of the word -> bit 31 - that
+          const int pos = 31 - (8 * (e >> 2) + 4 * h + (e & 3));
+          wd |= (__float_as_uint(d) >> 31) << pos;
         }
-      }
-#pragma unroll
-      for (int h = 0; h < NW; ++h) {
-        word[h] |= __shfl_xor(word[h], 16);
-        word[h] |= __shfl_xor(word[h], 32);
-        word[h] ^= fl[h];
+        wd |= __shfl_xor(wd, 32);
+        wd ^= fl[tf];
         if constexpr (POOL) {
-          word[h] |= __shfl_xor(word[h], 1);
-          word[h] |= __shfl_xor(word[h], 2);
+          wd |= __shfl_xor(wd, 1);
+          wd |= __shfl_xor(wd, 2);
         }
+        word[tf] = wd;
       }
-      const int item = p0 + tp * 16 + c;
-      const bool writer = POOL ? (q == 0 && (c & 3) == 0 && pv[tp]) : (q == 0 && pv[tp]);
+      const int item = p0 + tp * 32 + c;
+      const bool writer = POOL ? (h == 0 && (c & 3) == 0 && pv[tp]) : (h == 0 && pv[tp]);
       if (writer) {
         uint32_t* op = a.bits + static_cast<size_t>(POOL ? (item >> 2) : item) * a.Fw + f0 / 32;
-        if constexpr (NW == 2)
+        if constexpr (TF == 2)
           *reinterpret_cast<uint2*>(op) = make_uint2(word[0], word[1]);
         else
           *op = word[0];
@@ -317,44 +352,41 @@ __global__ __launch_bounds__(512) void bconv_mfma_kernel(MfmaArgs a) {
   }
 }
 
-template <int VW, bool POOL, int PD>
-hipError_t launch_cfg(const MfmaArgs& a, int tf, int ks, hipStream_t s) {
-  const unsigned fy = static_cast<unsigned>(a.F / (16 * tf));
-  const unsigned tiles = static_cast<unsigned>((a.items + 63) / 64);
-  if (ks == 1) {
-    dim3 grid((tiles + 3) / 4, fy), block(256);
-    if (tf == 4)
-      bconv_mfma_kernel<VW, POOL, 4, 1, PD><<<grid, block, 0, s>>>(a);
-    else
-      bconv_mfma_kernel<VW, POOL, 2, 1, PD><<<grid, block, 0, s>>>(a);
-  } else {
-    dim3 grid(tiles, fy), block(64 * ks);
-    if (ks == 2)
-      bconv_mfma_kernel<VW, POOL, 2, 2, PD><<<grid, block, 0, s>>>(a);
-    else if (ks == 4)
-      bconv_mfma_kernel<VW, POOL, 2, 4, PD><<<grid, block, 0, s>>>(a);
-    else
-      bconv_mfma_kernel<VW, POOL, 2, 8, PD><<<grid, block, 0, s>>>(a);
-  }
-  return hipGetLastError();
-}
-
 int env_int(const char* name, int dflt) {
   const char* e = getenv(name);
   return e ? atoi(e) : dflt;
 }
 
+template <int VW, bool POOL>
+hipError_t launch32(const Mfma32Args& a, int tf, int ks, hipStream_t s) {
+  const unsigned fy = static_cast<unsigned>(a.F / (32 * tf));
+  const unsigned groups = static_cast<unsigned>((a.items + 63) / 64);
+  if (ks == 1) {
+    dim3 grid((groups + 3) / 4, fy), block(256);
+    if (tf == 2)
+      bconv_mfma32_kernel<VW, POOL, 2, 1><<<grid, block, 0, s>>>(a);
+    else
+      bconv_mfma32_kernel<VW, POOL, 1, 1><<<grid, block, 0, s>>>(a);
+  } else {
+    dim3 grid(groups, fy), block(64 * ks);
+    if (ks == 2)
+      bconv_mfma32_kernel<VW, POOL, 1, 2><<<grid, block, 0, s>>>(a);
+    else
+      bconv_mfma32_kernel<VW, POOL, 1, 4><<<grid, block, 0, s>>>(a);
+  }
+  return hipGetLastError();
+}
+
 hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint32_t* w,
                     const int32_t* thr, const uint32_t* flip, int32_t* sums, uint32_t* bits,
                     hipStream_t s) {
-  MfmaArgs a;
+  Mfma32Args a;
   a.in = in;
   a.w = w;
   a.thr = thr;
   a.flip = flip;
   a.sums = sums;
   a.bits = bits;
-  a.N = g.N;
   a.H = g.H;
   a.W = g.W;
   a.Cw = g.Cw;
@@ -372,47 +404,37 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   a.K = g.KH * g.KW * g.C;
   a.in_bytes = static_cast<int32_t>(static_cast<int64_t>(g.N) * g.H * g.W * g.Cw * 4);
   a.w_bytes = static_cast<int32_t>(static_cast<int64_t>(g.F) * a.fstride * 4);
-  // VW = 4 (128-bit loads) doubles the prefetched words and spills with the
-  // 64x64 wave tile, so loads stay at 64 bits.
-  const int vw = (g.Cw % 8 == 0) ? 2 : 1;
-  const int iters = g.KH * g.KW * (g.Cw / (4 * vw));
+  a.div_w = make_fastdiv(static_cast<uint32_t>(pool ? g.Wp : g.Wo));
+  a.div_h = make_fastdiv(static_cast<uint32_t>(pool ? g.Hp : g.Ho));
+  const int vw = (g.Cw % 4 == 0) ? 2 : 1;
+  const int iters = g.KH * g.KW * (g.Cw / (2 * vw));
 
-  // Tile shape and K split (measured on MI355X): 64-filter wave tiles down to
-  // ~1 wave per SIMD (1024 waves), then 32-filter tiles, then a K split.
-  const int64_t tiles = (a.items + 63) / 64;
-  int tf = 4, ks = 1;
-  if (g.F % 64 != 0 || tiles * (g.F / 64) < 1024) {
-    tf = 2;
-    const int64_t base = tiles * (g.F / 32);
-    while (ks < 8 && base * ks < 1024 && iters >= 4 * ks) ks *= 2;
+  // Tile shape and K split: 64-filter wave tiles down to ~1 wave per SIMD
+  // (1024 waves), then 32-filter tiles, then a K split over 2 or 4 waves.
+  const int64_t groups = (a.items + 63) / 64;
+  int tf = 2, ks = 1;
+  if (g.F % 64 != 0 || groups * (g.F / 64) < 1024) {
+    tf = 1;
+    const int64_t base = groups * (g.F / 32);
+    while (ks < 4 && base * ks < 1024 && iters >= 4 * ks) ks *= 2;
   }
-  // Tuning overrides (pipeline depth, filter tiles per wave, K split).
-  int pd = env_int("BNN_MFMA_PD", 2);
+  // Tuning overrides (filter tiles per wave, K split).
   tf = env_int("BNN_MFMA_TF", tf);
   ks = env_int("BNN_MFMA_KS", ks);
-  if (g.F % (16 * tf) != 0 || (ks > 1 && tf != 2)) tf = 2;
-#define BNN_CFG(V, PDV)                                                         \
-  if (vw == V && pd == PDV)                                                     \
-    return pool ? launch_cfg<V, true, PDV>(a, tf, ks, s)                        \
-                : launch_cfg<V, false, PDV>(a, tf, ks, s);
-  BNN_CFG(2, 2)
-  BNN_CFG(2, 4)
-  BNN_CFG(1, 2)
-  BNN_CFG(1, 4)
-  BNN_CFG(1, 8)
-#undef BNN_CFG
-  if (vw == 2) return pool ? launch_cfg<2, true, 2>(a, tf, ks, s) : launch_cfg<2, false, 2>(a, tf, ks, s);
-  return pool ? launch_cfg<1, true, 2>(a, tf, ks, s) : launch_cfg<1, false, 2>(a, tf, ks, s);
-  return hipErrorInvalidValue;
+  if (tf != 1 && tf != 2) tf = 1;
+  if (g.F % (32 * tf) != 0 || (ks > 1 && tf != 1)) tf = 1;
+  if (ks != 1 && ks != 2 && ks != 4) ks = 1;
+  if (vw == 2) return pool ? launch32<2, true>(a, tf, ks, s) : launch32<2, false>(a, tf, ks, s);
+  return pool ? launch32<1, true>(a, tf, ks, s) : launch32<1, false>(a, tf, ks, s);
 }
 
 }  // namespace
 
 bool bconv_mfma_supported(const ConvGeom& g) {
-  // C a multiple of 128 (whole words, 4 words per k-step), F a multiple of
+  // C a multiple of 64 (whole words, 2 words per k-step), F a multiple of
   // 32 (whole output words), at most 32 taps (per-lane tap masks), and inputs
   // and weights under 2 GiB (32-bit byte offsets of the raw buffer loads).
-  return (g.C % 32) == 0 && (g.Cw % 4) == 0 && (g.F % 32) == 0 && g.KH * g.KW <= 32 &&
+  return (g.C % 64) == 0 && (g.F % 32) == 0 && g.KH * g.KW <= 32 &&
          static_cast<int64_t>(g.N) * g.H * g.W * g.Cw < (int64_t{1} << 29) &&
          static_cast<int64_t>(g.F) * g.KH * g.KW * g.Cw < (int64_t{1} << 29);
 }

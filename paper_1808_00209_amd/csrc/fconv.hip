@@ -8,6 +8,9 @@
 // value is loaded once per lane and added to or subtracted from the 32 filter
 // sums according to the (wave-uniform) weight bits: one sign flip and one add
 // per multiply-accumulate.
+#include <stdlib.h>
+#include <string.h>
+
 #include "kernels.hpp"
 
 namespace bnn {
@@ -303,6 +306,211 @@ hipError_t run_fconv(const ConvGeom& g, bool pool, const float* in,
 
 }  // namespace
 
+// Matrix-core path for few input channels: the block stages a zero-padded
+// (8 + KH - 1) x (32 + KW - 1) x C input tile in LDS (the pad value 0.0 comes
+// for free), and v_mfma_f32_16x16x4f32 multiplies the im2col values (B, one
+// per lane per k-step) by the +-1.0 weights (A, kept in registers for the
+// whole block).  Products are exact and the fp32 sums are as exact as the
+// vector kernel's.  Block = 4 waves = an 8 x 32 tile of output pixels (4 x 16
+// 2x2 windows when pooling) x 64 filters; the result layout and epilogue
+// follow the binary matrix-core kernel (lane: one pixel, four filters).
+constexpr int kMfTileH = 8;
+constexpr int kMfTileW = 32;
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+template <int C, int KH, int KW, bool POOL>
+__global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
+  constexpr int K = KH * KW * C;
+  constexpr int KS = (K + 3) / 4;  // k-steps of 4
+  constexpr int LW = kMfTileW + KW - 1;
+  constexpr int LH = kMfTileH + KH - 1;
+  __shared__ float tile[LH * LW * C];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int q = lane >> 4, c = lane & 15;
+  const int tiles_w = (a.Wo + kMfTileW - 1) / kMfTileW;
+  const int tiles_h = (a.Ho + kMfTileH - 1) / kMfTileH;
+  int b = blockIdx.x;
+  const int tw = b % tiles_w;
+  b /= tiles_w;
+  const int th_ = b % tiles_h;
+  const int n = b / tiles_h;
+  const int i0 = th_ * kMfTileH, j0 = tw * kMfTileW;
+  const int f0 = blockIdx.y * 64;
+
+  // Stage the input tile (zero outside the image).
+  for (int e = threadIdx.x; e < LH * LW * C; e += 256) {
+    const int ch = e % C;
+    const int t = e / C;
+    const int col = t % LW, row = t / LW;
+    const int hi = i0 + row - a.pad, wi = j0 + col - a.pad;
+    float v = 0.0f;
+    if (hi >= 0 && hi < a.H && wi >= 0 && wi < a.W)
+      v = a.in[((static_cast<size_t>(n) * a.H + hi) * a.W + wi) * C + ch];
+    tile[e] = v;
+  }
+
+  // This lane's weights (A operand): filter f0 + 16 tf + c, k = 4 s + q.
+  float wa[4][KS];
+  int rel[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    const int k = 4 * s + q;
+    const int tap = k / C, ch = k - (k / C) * C;
+    const int kh = tap / KW, kw = tap - (tap / KW) * KW;
+    rel[s] = k < K ? (kh * LW + kw) * C + ch : 0;
+#pragma unroll
+    for (int tf = 0; tf < 4; ++tf) {
+      const int f = f0 + tf * 16 + c;
+      float v = 0.0f;
+      if (k < K && f < a.F) {
+        const uint32_t word = a.w[static_cast<size_t>(f) * a.fstride + tap * a.Cw + (ch >> 5)];
+        v = ((word >> (31 - (ch & 31))) & 1u) ? 1.0f : -1.0f;
+      }
+      wa[tf][s] = v;
+    }
+  }
+  __syncthreads();
+
+  // This wave's 4 pixel tiles of 16: position of lane c's pixel in the block tile.
+  int pr[4], pc[4];
+#pragma unroll
+  for (int tp = 0; tp < 4; ++tp) {
+    if constexpr (POOL) {
+      const int win = wave * 16 + tp * 4 + (c >> 2);  // 4 x 16 windows
+      pr[tp] = 2 * (win / 16) + ((c >> 1) & 1);
+      pc[tp] = 2 * (win % 16) + (c & 1);
+    } else {
+      pr[tp] = 2 * wave + (tp >> 1);
+      pc[tp] = 16 * (tp & 1) + c;
+    }
+  }
+
+  v4f acc[4][4];
+#pragma unroll
+  for (int tf = 0; tf < 4; ++tf)
+#pragma unroll
+    for (int tp = 0; tp < 4; ++tp) acc[tf][tp] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int tp = 0; tp < 4; ++tp) {
+    const int pbase = (pr[tp] * LW + pc[tp]) * C;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const float x = (4 * s + q < K) ? tile[pbase + rel[s]] : 0.0f;
+#pragma unroll
+      for (int tf = 0; tf < 4; ++tf)
+        acc[tf][tp] = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[tf][s], x, acc[tf][tp], 0, 0, 0);
+    }
+  }
+
+  // Epilogue: lane (q, c) holds pixel c of each tile and filters 16 tf + 4 q + r.
+  const int nf = min(64, a.F - f0);
+#pragma unroll
+  for (int tp = 0; tp < 4; ++tp) {
+    const int i = i0 + pr[tp], j = j0 + pc[tp];
+    const bool pix = i < a.Ho && j < a.Wo;
+    if (a.sums && pix) {
+#pragma unroll
+      for (int tf = 0; tf < 4; ++tf)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int fl = tf * 16 + 4 * q + r;
+          if (fl < nf)
+            a.sums[(static_cast<size_t>(n * a.Ho + i) * a.Wo + j) * a.F + f0 + fl] = acc[tf][tp][r];
+        }
+    }
+  }
+  if (!a.bits) return;
+  float thf[4][4];
+#pragma unroll
+  for (int tf = 0; tf < 4; ++tf)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int fl = tf * 16 + 4 * q + r;
+      thf[tf][r] = fl < nf ? static_cast<float>(a.thr[f0 + fl]) : 0.0f;
+    }
+  const int w0 = f0 / 32;
+#pragma unroll
+  for (int tp = 0; tp < 4; ++tp) {
+    uint32_t word[2] = {0u, 0u};
+#pragma unroll
+    for (int tf = 0; tf < 4; ++tf)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int fl = tf * 16 + 4 * q + r;
+        const uint32_t bit = (fl < nf && acc[tf][tp][r] >= thf[tf][r]) ? 1u : 0u;
+        word[tf >> 1] |= bit << (31 - (16 * (tf & 1) + 4 * q + r));
+      }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      word[h] |= __shfl_xor(word[h], 16);
+      word[h] |= __shfl_xor(word[h], 32);
+      if (w0 + h < a.Fw) {
+        if (a.flip) word[h] ^= a.flip[w0 + h];
+        if (w0 + h == a.Fw - 1) word[h] &= tail_mask(a.F);
+      }
+      if constexpr (POOL) {
+        word[h] |= __shfl_xor(word[h], 1);
+        word[h] |= __shfl_xor(word[h], 2);
+      }
+    }
+    const int i = i0 + pr[tp], j = j0 + pc[tp];
+    if constexpr (POOL) {
+      const int ip = i >> 1, jp = j >> 1;
+      if (q == 0 && (c & 3) == 0 && ip < a.Hp && jp < a.Wp) {
+        uint32_t* op = a.bits + (static_cast<size_t>(n * a.Hp + ip) * a.Wp + jp) * a.Fw + w0;
+        op[0] = word[0];
+        if (w0 + 1 < a.Fw) op[1] = word[1];
+      }
+    } else {
+      if (q == 0 && i < a.Ho && j < a.Wo) {
+        uint32_t* op = a.bits + (static_cast<size_t>(n * a.Ho + i) * a.Wo + j) * a.Fw + w0;
+        op[0] = word[0];
+        if (w0 + 1 < a.Fw) op[1] = word[1];
+      }
+    }
+  }
+}
+
+template <int C>
+hipError_t run_fmfma(const ConvGeom& g, bool pool, const float* in, const uint32_t* w,
+                     const int32_t* thr, const uint32_t* flip, float* sums, uint32_t* bits,
+                     hipStream_t s) {
+  FconvArgs a;
+  a.in = in;
+  a.w = w;
+  a.thr = thr;
+  a.flip = flip;
+  a.sums = sums;
+  a.bits = bits;
+  a.N = g.N;
+  a.H = g.H;
+  a.W = g.W;
+  a.C = g.C;
+  a.Cw = g.Cw;
+  a.F = g.F;
+  a.Fw = g.Fw;
+  a.KH = g.KH;
+  a.KW = g.KW;
+  a.pad = g.pad;
+  a.Ho = g.Ho;
+  a.Wo = g.Wo;
+  a.Hp = g.Hp;
+  a.Wp = g.Wp;
+  a.fstride = g.KH * g.KW * g.Cw;
+  a.items = 0;
+  const unsigned tiles = static_cast<unsigned>(g.N) * ((g.Ho + kMfTileH - 1) / kMfTileH) *
+                         ((g.Wo + kMfTileW - 1) / kMfTileW);
+  dim3 grid(tiles, static_cast<unsigned>((g.F + 63) / 64));
+  if (pool)
+    fconv_mfma_kernel<C, 3, 3, true><<<grid, dim3(256), 0, s>>>(a);
+  else
+    fconv_mfma_kernel<C, 3, 3, false><<<grid, dim3(256), 0, s>>>(a);
+  return hipGetLastError();
+}
+
 template <int C>
 hipError_t run_lanef(const ConvGeom& g, bool pool, const float* in, const uint32_t* w,
                      const int32_t* thr, const uint32_t* flip, float* sums, uint32_t* bits,
@@ -350,6 +558,16 @@ hipError_t launch_fconv_binw(const ConvGeom& g, const float* in,
   // tiles sit on even coordinates, so 2x2 windows never straddle tiles).
   if (g.KH == 3 && g.KW == 3 && g.C <= 4) {
     const bool pool = g.pool == 2;
+    const char* e = getenv("BNN_ALGO");
+    if (!(e && strcmp(e, "valu") == 0)) {
+      // The matrix-core kernel's 8 x 32 pixel tiles sit on even coordinates.
+      switch (g.C) {
+        case 1: return run_fmfma<1>(g, pool, in, w, thr, flip, sums, bits, s);
+        case 2: return run_fmfma<2>(g, pool, in, w, thr, flip, sums, bits, s);
+        case 3: return run_fmfma<3>(g, pool, in, w, thr, flip, sums, bits, s);
+        default: return run_fmfma<4>(g, pool, in, w, thr, flip, sums, bits, s);
+      }
+    }
     switch (g.C) {
       case 1: return run_lanef<1>(g, pool, in, w, thr, flip, sums, bits, s);
       case 2: return run_lanef<2>(g, pool, in, w, thr, flip, sums, bits, s);

@@ -297,17 +297,33 @@ def test_bgemm_shapes_bit_exact(case, algo):
 
 # ---------------------------------------------------------- fp32 1st layer -
 @pytest.mark.parametrize("pool", [0, 2])
-@pytest.mark.parametrize("N,H,W", [(2, 32, 32), (1, 7, 5)])
-def test_fconv_first_layer_exact(pool, N, H, W):
-    L = synth.cfg3_net()[0]
-    x = synth.dyadic_normal(np.random.default_rng(N * H + W), (N, H, W, 3))
-    desc = bnn.conv_desc(N, H, W, 3, L["F"], 3, 3, 1, 1, pool)
-    sums, bits = bnn.bnn_fconv2d_binw(desc, to_device(x), pack_pm1(L["w"]),
-                                      to_device(L["thr"], torch.int32), pack_flips(L["flip"]))
+@pytest.mark.parametrize("N,H,W,C,F", [(2, 32, 32, 3, 128), (1, 7, 5, 3, 128), (1, 9, 33, 3, 40),
+                                       (3, 12, 10, 1, 64), (1, 10, 9, 4, 96), (1, 6, 6, 2, 32)])
+def test_fconv_first_layer_exact(pool, N, H, W, C, F, algo):
+    rng = np.random.default_rng(N * H + W + 7 * C + F)
+    x = synth.dyadic_normal(rng, (N, H, W, C))
+    w = _pm1(rng, (F, 3, 3, C))
+    thr = rng.integers(-9, 10, F).astype(np.int32)
+    flip = rng.integers(0, 2, F).astype(np.uint8)
+    desc = bnn.conv_desc(N, H, W, C, F, 3, 3, 1, 1, pool)
+    sums, bits = bnn.bnn_fconv2d_binw(desc, to_device(x), pack_pm1(w),
+                                      to_device(thr, torch.int32), pack_flips(flip))
     torch.cuda.synchronize()
-    S = oracle.fconv2d(x, L["w"], 1, 1)
-    b = oracle.threshold(S, L["thr"], L["flip"])
+    S = oracle.fconv2d(x, w, 1, 1)
+    b = oracle.threshold(S, thr, flip)
     if pool:
         b = oracle.maxpool2(b)
     assert np.array_equal(sums.cpu().numpy().astype(np.float64), S)
     assert np.array_equal(words_u32(bits), oracle.pack_eq2(b))
+
+
+def test_fconv_cifar_first_layer_batch64(algo):
+    L = synth.cfg3_net()[0]
+    x = synth.cfg3_input(64)
+    desc = bnn.conv_desc(64, 32, 32, 3, L["F"], 3, 3, 1, 1, 0)
+    sums, bits = bnn.bnn_fconv2d_binw(desc, to_device(x), pack_pm1(L["w"]),
+                                      to_device(L["thr"], torch.int32), pack_flips(L["flip"]))
+    torch.cuda.synchronize()
+    S = oracle.fconv2d(x, L["w"], 1, 1)
+    assert np.array_equal(sums.cpu().numpy().astype(np.float64), S)
+    assert np.array_equal(words_u32(bits), oracle.pack_eq2(oracle.threshold(S, L["thr"], L["flip"])))
