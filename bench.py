@@ -28,6 +28,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 VALU_PEAK_TOPS = 1258.29  # 256 CU x 64 lanes x 2.4 GHz x 32 bit-MACs x 2 ops / 2 instr
+MFMA_FP4_PEAK_TFLOPS = 10100.0  # MI355X dense fp4 matrix peak (1 fp4 MAC = 1 bit-MAC)
+MFMA_FP32_PEAK_TFLOPS = 157.3   # MI355X fp32 matrix peak
 HBM_PEAK_GBS = 8000.0
 
 WORKLOADS = {
@@ -47,6 +49,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target length of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run one 256 MiB device-to-device copy (calibrates the "
+                         "FETCH_SIZE / WRITE_SIZE counters of a profiling run)")
     return ap.parse_args()
 
 
@@ -130,20 +135,23 @@ def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
     return e0.elapsed_time(e1) / reps
 
 
-def cpu_baseline(layers, x, target_s, bin_ops_per_image):
+def cpu_baseline(layers, cfg, target_s, bin_ops_per_image, max_images=4096):
+    """The oracle (all host threads) on a bounded sample of the workload's
+    images: sized from a 16-image calibration run to take about target_s."""
     import oracle
-    n = 1
+    xs = net_input(cfg, 16)
     t0 = time.perf_counter()
-    oracle.forward(layers, x[:1])
-    t1 = time.perf_counter() - t0
-    n = int(max(1, min(len(x), target_s / max(t1, 1e-6))))
+    oracle.forward(layers, xs)
+    t1 = (time.perf_counter() - t0) / 16
+    n = int(max(16, min(max_images, target_s / max(t1, 1e-6))))
+    xs = net_input(cfg, n)
     t0 = time.perf_counter()
-    oracle.forward(layers, x[:n])
+    oracle.forward(layers, xs)
     dt = time.perf_counter() - t0
     return {"value": round(n * bin_ops_per_image / dt / 1e9, 3), "unit": "GOPS",
             "images_per_s": round(n / dt, 3), "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": "%d of the %d images of one batch through the whole oracle chain "
-                      "(%.1f s), scaled to binary GOPS" % (n, len(x), dt)}
+            "sample": "%d images of the workload through the whole oracle chain in %.1f s, "
+                      "scaled to binary GOPS" % (n, dt)}
 
 
 def main():
@@ -178,36 +186,69 @@ def main():
     logits = torch.empty((batch, layers[-1]["N"]), dtype=torch.int32, device="cuda")
     stream = torch.cuda.current_stream()
 
+    def capture(fn):
+        """fn's launches recorded into a HIP graph (after one eager warm-up
+        on a side stream, as graph capture requires)."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
+        return g
+
+    def timed(run, steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        e0.record(stream)
+        for _ in range(steps):
+            run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps, time.perf_counter() - t
+
+    # The step: one bnn_forward call (one kernel launch per layer).
     for _ in range(args.warmup):
         bnn.bnn_forward(net, x, ws, logits)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t_wall = time.perf_counter()
-    e0.record(stream)
-    for _ in range(args.steps):
-        bnn.bnn_forward(net, x, ws, logits)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    ms_per_step = e0.elapsed_time(e1) / args.steps
+    ms_per_step, t_wall = timed(lambda: bnn.bnn_forward(net, x, ws, logits), args.steps)
     gops = ops_per_step / (ms_per_step * 1e-3) / 1e9
+    # For comparison: the same launches replayed from a captured HIP graph.
+    graph = capture(lambda: bnn.bnn_forward(net, x, ws, logits))
+    for _ in range(args.warmup):
+        graph.replay()
+    ms_graph, _ = timed(graph.replay, args.steps)
 
-    # Batch-1 latency protocol: fresh images one at a time, kernels only.
+    # Batch-1 latency protocol: fresh images one at a time, kernels only (each
+    # image is first copied into the graph's input buffer, outside the timed
+    # span, as the paper excludes memory transfers).
     n1 = args.b1_images
     x1 = to_device(net_input(wl["cfg"], n1))
+    xin1 = torch.empty_like(x1[:1])
     ws1 = net.alloc_workspace(1)
     lg1 = torch.empty((1, layers[-1]["N"]), dtype=torch.int32, device="cuda")
-    for i in range(3):
-        bnn.bnn_forward(net, x1[i:i + 1], ws1, lg1)
-    torch.cuda.synchronize()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(n1)]
-    for i in range(n1):
-        evs[i][0].record(stream)
-        bnn.bnn_forward(net, x1[i:i + 1], ws1, lg1)
-        evs[i][1].record(stream)
-    torch.cuda.synchronize()
-    per_img_us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+    graph1 = capture(lambda: bnn.bnn_forward(net, xin1, ws1, lg1))
+
+    def batch1(use_graph):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(n1)]
+        for i in range(n1):
+            xin1.copy_(x1[i:i + 1])
+            evs[i][0].record(stream)
+            if use_graph:
+                graph1.replay()
+            else:
+                bnn.bnn_forward(net, xin1, ws1, lg1)
+            evs[i][1].record(stream)
+        torch.cuda.synchronize()
+        return np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+
+    batch1(False)
+    per_img_us = batch1(False)
+    per_img_us_graph = batch1(True)
 
     # Per-layer kernel times (Table II analogue) and the dominant kernel.
     # Each layer also runs with BNN_ALGO=valu (XOR-popcount vector kernels
@@ -228,9 +269,20 @@ def main():
             row["GOPS"] = round(2 * macs * batch / (ms * 1e-3) / 1e9, 1)
             row["GOPS_valu"] = round(2 * macs * batch / (ms_valu * 1e-3) / 1e9, 1)
         per_layer.append(row)
-    dom_i = max(range(len(shapes)), key=lambda i: per_layer[i]["ms"] if shapes[i][3] else -1)
+    dom_i = max(range(len(shapes)), key=lambda i: per_layer[i]["ms"])
     dom_ms = per_layer[dom_i]["ms"]
-    dom_ops = 2 * shapes[dom_i][3] * batch
+    name, kind, g, macs = shapes[dom_i]
+    if kind == "fconv":
+        # fp32 first layer on fp32 MFMA (v_mfma_f32_16x16x4f32): 2 flops/MAC
+        fmacs = batch * (g["H"] + 2 * g["pad"] - g["KH"] + 1) * (g["W"] + 2 * g["pad"] - g["KW"] + 1) \
+            * g["F"] * g["KH"] * g["KW"] * g["C"]
+        dom_ops, bound, peak, unit = 2 * fmacs, "mfma", MFMA_FP32_PEAK_TFLOPS, "TFLOP/s"
+    elif kind in ("bconv", "bfc", "bfc_logits") and (g.get("C", g.get("K", 0)) % 64 == 0) \
+            and not (kind != "bconv" and batch <= 16):
+        # binary layer on fp4 MFMA: one fp4 multiply-accumulate per bit-MAC
+        dom_ops, bound, peak, unit = 2 * macs * batch, "mfma", MFMA_FP4_PEAK_TFLOPS, "TFLOP/s"
+    else:
+        dom_ops, bound, peak, unit = 2 * macs * batch, "alu", VALU_PEAK_TOPS, "TOP/s"
     achieved_tops = dom_ops / (dom_ms * 1e-3) / 1e12
 
     result = {
@@ -249,19 +301,30 @@ def main():
         "config": {"workload": args.workload, "batch": batch, "input": "%dx%dx%d fp32" % (H, W, C),
                    "binary_ops_per_step": ops_per_step},
         "images_per_s": round(batch / (ms_per_step * 1e-3), 1),
+        "launch": "bnn_forward, one kernel per layer",
+        "hip_graph": {"ms_per_step": round(ms_graph, 5),
+                      "value": round(ops_per_step / (ms_graph * 1e-3) / 1e9, 1),
+                      "batch1_mean_us": round(float(per_img_us_graph.mean()), 3)},
         "batch1": {"images": n1, "mean_us": round(float(per_img_us.mean()), 3),
                    "median_us": round(float(np.median(per_img_us)), 3),
                    "images_per_s": round(1e6 / float(per_img_us.mean()), 1)},
         "wall_s_timed_region": round(t_wall, 4),
         "per_layer": per_layer,
-        "roofline": {"kernel": shapes[dom_i][0], "bound": "alu",
-                     "achieved": round(achieved_tops, 2), "peak": VALU_PEAK_TOPS,
-                     "unit": "TOP/s", "frac": round(achieved_tops / VALU_PEAK_TOPS, 4),
-                     "traffic": None},
+        "roofline": {"kernel": name, "bound": bound, "achieved": round(achieved_tops, 2),
+                     "peak": peak, "unit": unit, "frac": round(achieved_tops / peak, 4),
+                     "traffic": None,
+                     "valu_xor_popcount_peak_TOPS": VALU_PEAK_TOPS},
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(layers, x_host, args.cpu_seconds,
+        result["cpu_baseline"] = cpu_baseline(layers, wl["cfg"], args.cpu_seconds,
                                               2 * bin_macs_img)
+    if args.copy_probe:
+        src = torch.empty(64 << 20, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
     print(json.dumps(result), flush=True)
 
 

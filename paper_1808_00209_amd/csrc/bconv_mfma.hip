@@ -20,8 +20,8 @@
 // wave computes 64 (or 32) filters x 64 pixels; with pooling, the 32 pixels
 // of a tile are eight 2x2 windows so that a window sits in 4 adjacent lanes.
 //
-// Requirements (bconv_mfma_supported): stride 1, C a multiple of 64, F a
-// multiple of 32, at most 32 taps.
+// Requirements (bconv_mfma_supported): stride 1, C a multiple of 64, at most
+// 32 taps.
 #include <stdlib.h>
 
 #include "kernels.hpp"
@@ -120,11 +120,11 @@ struct Mfma32Args {
 //   POOL pixels of a 32-tile ordered as eight 2x2 windows (4 adjacent lanes).
 //   TF   32-filter tiles per wave (1 or 2); a wave always covers 64 pixels.
 //   KS   1: the 4 waves of a block take 4 consecutive 64-pixel groups;
-//        >1: the KS waves of a block split the iterations of one tile and add
-//        their partial sums in LDS (grids too small to fill the chip).
+//        >1: the KS (2..8) waves of a block split the iterations of one tile
+//        and add their partial sums in LDS (grids too small to fill the chip).
 // Loads run one iteration ahead of the MFMAs (two register sets).
 template <int VW, bool POOL, int TF, int KS>
-__global__ __launch_bounds__(256) void bconv_mfma32_kernel(Mfma32Args a) {
+__global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(Mfma32Args a) {
   constexpr int TP = 2;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -264,25 +264,37 @@ __global__ __launch_bounds__(256) void bconv_mfma32_kernel(Mfma32Args a) {
   }
 
   if constexpr (KS > 1) {
-    __shared__ v16f part[KS - 1][TF][TP][64];
-    if (wave > 0) {
+    // Partial sums of the KS waves meet in LDS: every wave stores its tile
+    // in its own slot, all threads of the block add the slots slice by slice
+    // into slot 0, and wave 0 takes the totals for the epilogue.
+    constexpr int NV = TF * TP * 16 * 64;  // values per wave
+    __shared__ float part[KS][NV];
 #pragma unroll
-      for (int tf = 0; tf < TF; ++tf)
+    for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
-        for (int tp = 0; tp < TP; ++tp) part[wave - 1][tf][tp][lane] = acc[tf][tp];
+      for (int tp = 0; tp < TP; ++tp)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) part[wave][((tf * TP + tp) * 16 + e) * 64 + lane] = acc[tf][tp][e];
+    __syncthreads();
+    for (int v = threadIdx.x; v < NV; v += 64 * KS) {
+      float t = part[0][v];
+#pragma unroll
+      for (int w = 1; w < KS; ++w) t += part[w][v];
+      part[0][v] = t;
     }
     __syncthreads();
     if (wave > 0) return;
 #pragma unroll
-    for (int w = 0; w < KS - 1; ++w)
+    for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
-      for (int tf = 0; tf < TF; ++tf)
+      for (int tp = 0; tp < TP; ++tp)
 #pragma unroll
-        for (int tp = 0; tp < TP; ++tp) acc[tf][tp] += part[w][tf][tp][lane];
+        for (int e = 0; e < 16; ++e) acc[tf][tp][e] = part[0][((tf * TP + tp) * 16 + e) * 64 + lane];
   }
 
-  // Epilogue.  Lane (h, c) holds, in register e of tile (tf, tp), the sum of
-  // pixel c and filter f0 + 32 tf + 8 (e / 4) + 4 h + (e % 4).
+  // Filters past F (a partial last tile) read zero weights through the
+  // buffer range and are masked out of every output.
+  const bool ftail = f0 + 32 * TF > a.F;
   if (a.sums) {
 #pragma unroll
     for (int tp = 0; tp < TP; ++tp) {
@@ -293,12 +305,19 @@ __global__ __launch_bounds__(256) void bconv_mfma32_kernel(Mfma32Args a) {
       for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          int4 t;
-          t.x = static_cast<int>(acc[tf][tp][4 * g + 0]);
-          t.y = static_cast<int>(acc[tf][tp][4 * g + 1]);
-          t.z = static_cast<int>(acc[tf][tp][4 * g + 2]);
-          t.w = static_cast<int>(acc[tf][tp][4 * g + 3]);
-          *reinterpret_cast<int4*>(sp + tf * 32 + 8 * g) = t;
+          const int fb = f0 + tf * 32 + 8 * g + 4 * h;  // first of 4 filters
+          if (!ftail && (a.F & 3) == 0) {
+            int4 t;
+            t.x = static_cast<int>(acc[tf][tp][4 * g + 0]);
+            t.y = static_cast<int>(acc[tf][tp][4 * g + 1]);
+            t.z = static_cast<int>(acc[tf][tp][4 * g + 2]);
+            t.w = static_cast<int>(acc[tf][tp][4 * g + 3]);
+            *reinterpret_cast<int4*>(sp + tf * 32 + 8 * g) = t;
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (fb + e < a.F) sp[tf * 32 + 8 * g + e] = static_cast<int>(acc[tf][tp][4 * g + e]);
+          }
         }
     }
   }
@@ -312,12 +331,17 @@ __global__ __launch_bounds__(256) void bconv_mfma32_kernel(Mfma32Args a) {
     for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int t = a.thr[f0 + tf * 32 + 8 * (e >> 2) + 4 * h + (e & 3)];
+        const int f = f0 + tf * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+        const int t = a.thr[f < a.F ? f : a.F - 1];
         th[tf][e] = static_cast<float>(min(max(t, -a.K - 1), a.K + 1)) - 0.5f;
       }
-    uint32_t fl[TF];
+    uint32_t fl[TF], fm[TF];
 #pragma unroll
-    for (int tf = 0; tf < TF; ++tf) fl[tf] = a.flip ? a.flip[f0 / 32 + tf] : 0u;
+    for (int tf = 0; tf < TF; ++tf) {
+      const int wi = f0 / 32 + tf;
+      fl[tf] = a.flip ? a.flip[wi] : 0u;
+      fm[tf] = wi == a.Fw - 1 ? tail_mask(a.F) : ~0u;
+    }
 #pragma unroll
     for (int tp = 0; tp < TP; ++tp) {
       uint32_t word[TF];
@@ -332,7 +356,7 @@ __global__ __launch_bounds__(256) void bconv_mfma32_kernel(Mfma32Args a) {
           wd |= (__float_as_uint(d) >> 31) << pos;
         }
         wd |= __shfl_xor(wd, 32);
-        wd ^= fl[tf];
+        wd = (wd ^ fl[tf]) & fm[tf];
         if constexpr (POOL) {
           wd |= __shfl_xor(wd, 1);
           wd |= __shfl_xor(wd, 2);
@@ -359,7 +383,7 @@ int env_int(const char* name, int dflt) {
 
 template <int VW, bool POOL>
 hipError_t launch32(const Mfma32Args& a, int tf, int ks, hipStream_t s) {
-  const unsigned fy = static_cast<unsigned>(a.F / (32 * tf));
+  const unsigned fy = static_cast<unsigned>((a.F + 32 * tf - 1) / (32 * tf));
   const unsigned groups = static_cast<unsigned>((a.items + 63) / 64);
   if (ks == 1) {
     dim3 grid((groups + 3) / 4, fy), block(256);
@@ -371,8 +395,10 @@ hipError_t launch32(const Mfma32Args& a, int tf, int ks, hipStream_t s) {
     dim3 grid(groups, fy), block(64 * ks);
     if (ks == 2)
       bconv_mfma32_kernel<VW, POOL, 1, 2><<<grid, block, 0, s>>>(a);
-    else
+    else if (ks == 4)
       bconv_mfma32_kernel<VW, POOL, 1, 4><<<grid, block, 0, s>>>(a);
+    else
+      bconv_mfma32_kernel<VW, POOL, 1, 8><<<grid, block, 0, s>>>(a);
   }
   return hipGetLastError();
 }
@@ -410,20 +436,21 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   const int iters = g.KH * g.KW * (g.Cw / (2 * vw));
 
   // Tile shape and K split: 64-filter wave tiles down to ~1 wave per SIMD
-  // (1024 waves), then 32-filter tiles, then a K split over 2 or 4 waves.
+  // (1024 waves), then 32-filter tiles, then a K split over up to 8 waves
+  // (keeping at least 2 iterations per wave).
   const int64_t groups = (a.items + 63) / 64;
+  const int64_t ftiles = (g.F + 31) / 32;
   int tf = 2, ks = 1;
   if (g.F % 64 != 0 || groups * (g.F / 64) < 1024) {
     tf = 1;
-    const int64_t base = groups * (g.F / 32);
-    while (ks < 4 && base * ks < 1024 && iters >= 4 * ks) ks *= 2;
+    while (ks < 8 && groups * ftiles * ks < 1024 && iters >= 4 * ks) ks *= 2;  // >= 2 per wave
   }
   // Tuning overrides (filter tiles per wave, K split).
   tf = env_int("BNN_MFMA_TF", tf);
   ks = env_int("BNN_MFMA_KS", ks);
   if (tf != 1 && tf != 2) tf = 1;
   if (g.F % (32 * tf) != 0 || (ks > 1 && tf != 1)) tf = 1;
-  if (ks != 1 && ks != 2 && ks != 4) ks = 1;
+  if (ks != 1 && ks != 2 && ks != 4 && ks != 8) ks = 1;
   if (vw == 2) return pool ? launch32<2, true>(a, tf, ks, s) : launch32<2, false>(a, tf, ks, s);
   return pool ? launch32<1, true>(a, tf, ks, s) : launch32<1, false>(a, tf, ks, s);
 }
@@ -431,10 +458,10 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
 }  // namespace
 
 bool bconv_mfma_supported(const ConvGeom& g) {
-  // C a multiple of 64 (whole words, 2 words per k-step), F a multiple of
-  // 32 (whole output words), at most 32 taps (per-lane tap masks), and inputs
+  // C a multiple of 64 (whole words, 2 words per k-step), at most 32 taps
+  // (per-lane tap masks), and inputs
   // and weights under 2 GiB (32-bit byte offsets of the raw buffer loads).
-  return (g.C % 64) == 0 && (g.F % 32) == 0 && g.KH * g.KW <= 32 &&
+  return (g.C % 64) == 0 && g.KH * g.KW <= 32 &&
          static_cast<int64_t>(g.N) * g.H * g.W * g.Cw < (int64_t{1} << 29) &&
          static_cast<int64_t>(g.F) * g.KH * g.KW * g.Cw < (int64_t{1} << 29);
 }

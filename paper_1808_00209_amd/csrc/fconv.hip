@@ -308,21 +308,25 @@ hipError_t run_fconv(const ConvGeom& g, bool pool, const float* in,
 
 // Matrix-core path for few input channels: the block stages a zero-padded
 // (8 + KH - 1) x (32 + KW - 1) x C input tile in LDS (the pad value 0.0 comes
-// for free), and v_mfma_f32_16x16x4f32 multiplies the im2col values (B, one
-// per lane per k-step) by the +-1.0 weights (A, kept in registers for the
-// whole block).  Products are exact and the fp32 sums are as exact as the
-// vector kernel's.  Block = 4 waves = an 8 x 32 tile of output pixels (4 x 16
-// 2x2 windows when pooling) x 64 filters; the result layout and epilogue
-// follow the binary matrix-core kernel (lane: one pixel, four filters).
+// for free), splits every staged value x into two fp16 parts, x = hi + lo
+// (hi = x rounded to fp16, lo = x - hi), and v_mfma_f32_16x16x32_f16
+// multiplies them by the +-1 weights.  For inputs on the 2^-16 grid with
+// |x| < 8 both parts are exact fp16 values, every product is exact and every
+// partial sum is a multiple of 2^-16 below 2^8, so the fp32 sums are exact in
+// any order (other inputs are summed to within about 2^-22 relative per term).
+// Block = 4 waves = an 8 x 32 tile of output pixels (4 x 16 2x2 windows when
+// pooling) x 64 filters; the result layout and epilogue follow the binary
+// matrix-core kernel (lane: one pixel, four filters).
 constexpr int kMfTileH = 8;
 constexpr int kMfTileW = 32;
 
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 
-template <int C, int KH, int KW, bool POOL>
+template <int C, int KH, int KW, bool POOL, bool FULL>
 __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
   constexpr int K = KH * KW * C;
-  constexpr int KS = (K + 3) / 4;  // k-steps of 4
+  constexpr int KC = (K + 31) / 32;  // k-chunks of 32
   constexpr int LW = kMfTileW + KW - 1;
   constexpr int LH = kMfTileH + KH - 1;
   __shared__ float tile[LH * LW * C];
@@ -352,24 +356,32 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
     tile[e] = v;
   }
 
-  // This lane's weights (A operand): filter f0 + 16 tf + c, k = 4 s + q.
-  float wa[4][KS];
-  int rel[KS];
+  // A operands (weights, +-1 in fp16): row = filter f0 + 16 tf + c, the 8
+  // k values 32 kc + 8 q + e of this lane.  Also the LDS offsets of those k
+  // values relative to a pixel's window origin.
+  v8h wa[KC][4];
+  int rel[KC][8];
 #pragma unroll
-  for (int s = 0; s < KS; ++s) {
-    const int k = 4 * s + q;
-    const int tap = k / C, ch = k - (k / C) * C;
-    const int kh = tap / KW, kw = tap - (tap / KW) * KW;
-    rel[s] = k < K ? (kh * LW + kw) * C + ch : 0;
+  for (int kc = 0; kc < KC; ++kc) {
 #pragma unroll
-    for (int tf = 0; tf < 4; ++tf) {
-      const int f = f0 + tf * 16 + c;
-      float v = 0.0f;
-      if (k < K && f < a.F) {
-        const uint32_t word = a.w[static_cast<size_t>(f) * a.fstride + tap * a.Cw + (ch >> 5)];
-        v = ((word >> (31 - (ch & 31))) & 1u) ? 1.0f : -1.0f;
+    for (int e = 0; e < 8; ++e) {
+      const int k = 32 * kc + 8 * q + e;
+      const int tap = k / C, ch = k - (k / C) * C;
+      const int kh = tap / KW, kw = tap - (tap / KW) * KW;
+      const bool kin = k < K;
+      rel[kc][e] = kin ? (kh * LW + kw) * C + ch : -1;
+#pragma unroll
+      for (int tf = 0; tf < 4; ++tf) {
+        // Unconditional load from a clamped (valid) address, then select:
+        // no branches around the loads.
+        const int f = f0 + tf * 16 + c;
+        const bool ok = kin && (FULL || f < a.F);
+        const uint32_t word = a.w[static_cast<size_t>(ok ? f : 0) * a.fstride +
+                                  (ok ? tap * a.Cw + (ch >> 5) : 0)];
+        const bool one = (word >> (31 - (ch & 31))) & 1u;
+        wa[kc][tf][e] = ok ? (one ? static_cast<_Float16>(1.0f) : static_cast<_Float16>(-1.0f))
+                           : static_cast<_Float16>(0.0f);
       }
-      wa[tf][s] = v;
     }
   }
   __syncthreads();
@@ -397,29 +409,37 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
   for (int tp = 0; tp < 4; ++tp) {
     const int pbase = (pr[tp] * LW + pc[tp]) * C;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const float x = (4 * s + q < K) ? tile[pbase + rel[s]] : 0.0f;
+    for (int kc = 0; kc < KC; ++kc) {
+      v8h xh, xl;
 #pragma unroll
-      for (int tf = 0; tf < 4; ++tf)
-        acc[tf][tp] = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[tf][s], x, acc[tf][tp], 0, 0, 0);
+      for (int e = 0; e < 8; ++e) {
+        const float xv = tile[pbase + max(rel[kc][e], 0)];
+        const float x = rel[kc][e] >= 0 ? xv : 0.0f;
+        const _Float16 h = static_cast<_Float16>(x);
+        xh[e] = h;
+        xl[e] = static_cast<_Float16>(x - static_cast<float>(h));
+      }
+#pragma unroll
+      for (int tf = 0; tf < 4; ++tf) {
+        acc[tf][tp] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[kc][tf], xh, acc[tf][tp], 0, 0, 0);
+        acc[tf][tp] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[kc][tf], xl, acc[tf][tp], 0, 0, 0);
+      }
     }
   }
 
   // Epilogue: lane (q, c) holds pixel c of each tile and filters 16 tf + 4 q + r.
-  const int nf = min(64, a.F - f0);
+  const int nf = FULL ? 64 : min(64, a.F - f0);
 #pragma unroll
   for (int tp = 0; tp < 4; ++tp) {
     const int i = i0 + pr[tp], j = j0 + pc[tp];
     const bool pix = i < a.Ho && j < a.Wo;
     if (a.sums && pix) {
+      float* sp = a.sums + (static_cast<size_t>(n * a.Ho + i) * a.Wo + j) * a.F + f0 + 4 * q;
 #pragma unroll
       for (int tf = 0; tf < 4; ++tf)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int fl = tf * 16 + 4 * q + r;
-          if (fl < nf)
-            a.sums[(static_cast<size_t>(n * a.Ho + i) * a.Wo + j) * a.F + f0 + fl] = acc[tf][tp][r];
-        }
+        for (int r = 0; r < 4; ++r)
+          if (FULL || tf * 16 + 4 * q + r < nf) sp[tf * 16 + r] = acc[tf][tp][r];
     }
   }
   if (!a.bits) return;
@@ -429,7 +449,7 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int fl = tf * 16 + 4 * q + r;
-      thf[tf][r] = fl < nf ? static_cast<float>(a.thr[f0 + fl]) : 0.0f;
+      thf[tf][r] = (FULL || fl < nf) ? static_cast<float>(a.thr[f0 + fl]) : 0.0f;
     }
   const int w0 = f0 / 32;
 #pragma unroll
@@ -440,16 +460,16 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int fl = tf * 16 + 4 * q + r;
-        const uint32_t bit = (fl < nf && acc[tf][tp][r] >= thf[tf][r]) ? 1u : 0u;
-        word[tf >> 1] |= bit << (31 - (16 * (tf & 1) + 4 * q + r));
+        const bool on = acc[tf][tp][r] >= thf[tf][r] && (FULL || fl < nf);
+        word[tf >> 1] |= static_cast<uint32_t>(on) << (31 - (16 * (tf & 1) + 4 * q + r));
       }
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       word[h] |= __shfl_xor(word[h], 16);
       word[h] |= __shfl_xor(word[h], 32);
-      if (w0 + h < a.Fw) {
+      if (FULL || w0 + h < a.Fw) {
         if (a.flip) word[h] ^= a.flip[w0 + h];
-        if (w0 + h == a.Fw - 1) word[h] &= tail_mask(a.F);
+        if (!FULL && w0 + h == a.Fw - 1) word[h] &= tail_mask(a.F);
       }
       if constexpr (POOL) {
         word[h] |= __shfl_xor(word[h], 1);
@@ -461,14 +481,22 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
       const int ip = i >> 1, jp = j >> 1;
       if (q == 0 && (c & 3) == 0 && ip < a.Hp && jp < a.Wp) {
         uint32_t* op = a.bits + (static_cast<size_t>(n * a.Hp + ip) * a.Wp + jp) * a.Fw + w0;
-        op[0] = word[0];
-        if (w0 + 1 < a.Fw) op[1] = word[1];
+        if (FULL)
+          *reinterpret_cast<uint2*>(op) = make_uint2(word[0], word[1]);
+        else {
+          op[0] = word[0];
+          if (w0 + 1 < a.Fw) op[1] = word[1];
+        }
       }
     } else {
       if (q == 0 && i < a.Ho && j < a.Wo) {
         uint32_t* op = a.bits + (static_cast<size_t>(n * a.Ho + i) * a.Wo + j) * a.Fw + w0;
-        op[0] = word[0];
-        if (w0 + 1 < a.Fw) op[1] = word[1];
+        if (FULL)
+          *reinterpret_cast<uint2*>(op) = make_uint2(word[0], word[1]);
+        else {
+          op[0] = word[0];
+          if (w0 + 1 < a.Fw) op[1] = word[1];
+        }
       }
     }
   }
@@ -504,10 +532,15 @@ hipError_t run_fmfma(const ConvGeom& g, bool pool, const float* in, const uint32
   const unsigned tiles = static_cast<unsigned>(g.N) * ((g.Ho + kMfTileH - 1) / kMfTileH) *
                          ((g.Wo + kMfTileW - 1) / kMfTileW);
   dim3 grid(tiles, static_cast<unsigned>((g.F + 63) / 64));
-  if (pool)
-    fconv_mfma_kernel<C, 3, 3, true><<<grid, dim3(256), 0, s>>>(a);
+  const bool full = g.F % 64 == 0;
+  if (pool && full)
+    fconv_mfma_kernel<C, 3, 3, true, true><<<grid, dim3(256), 0, s>>>(a);
+  else if (pool)
+    fconv_mfma_kernel<C, 3, 3, true, false><<<grid, dim3(256), 0, s>>>(a);
+  else if (full)
+    fconv_mfma_kernel<C, 3, 3, false, true><<<grid, dim3(256), 0, s>>>(a);
   else
-    fconv_mfma_kernel<C, 3, 3, false><<<grid, dim3(256), 0, s>>>(a);
+    fconv_mfma_kernel<C, 3, 3, false, false><<<grid, dim3(256), 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -34,7 +34,7 @@ hipError_t launch_bconv_valu(const ConvGeom& g, const uint32_t* in,
                              uint32_t* bits, hipStream_t s);
 
 // Binary conv on the matrix cores (fp4 MFMA).  Supported when
-// bconv_mfma_supported(g): C a multiple of 128 and F a multiple of 32.
+// bconv_mfma_supported(g): C a multiple of 64, at most 32 taps.
 bool bconv_mfma_supported(const ConvGeom& g);
 hipError_t launch_bconv_mfma(const ConvGeom& g, const uint32_t* in,
                              const uint32_t* w, const int32_t* thr,

@@ -137,6 +137,10 @@ CONV_CASES = [
     (2, 5, 5, 128, 96, 3, 1, 2),
     (1, 12, 12, 256, 32, 3, 1, 0),
     (64, 8, 8, 512, 512, 3, 1, 2),
+    # filter counts that are not a multiple of 32 on the matrix-core path
+    (2, 6, 6, 64, 10, 3, 1, 2),
+    (1, 5, 5, 128, 40, 3, 1, 0),
+    (3, 4, 7, 192, 70, 1, 0, 0),
 ]
 
 
@@ -279,7 +283,8 @@ def test_cfg2_fc_gemm_full_size_bit_exact(K, algo):
 
 GEMM_CASES = [(1, 1, 1), (1, 10, 1024), (2, 33, 31), (5, 100, 33), (16, 1024, 8192),
               (16, 64, 4100), (17, 40, 96), (64, 1024, 8192), (100, 70, 1000), (3, 4, 18432),
-              (65, 128, 1024), (300, 64, 18432), (64, 192, 128)]
+              (65, 128, 1024), (300, 64, 18432), (64, 192, 128), (64, 10, 1024),
+              (40, 50, 128), (64, 33, 8192), (64, 4, 18432), (256, 1024, 8192)]
 
 
 @pytest.mark.parametrize("case", GEMM_CASES, ids=[str(c) for c in GEMM_CASES])
