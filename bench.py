@@ -32,6 +32,36 @@ MFMA_FP4_PEAK_TFLOPS = 10100.0  # MI355X dense fp4 matrix peak (1 fp4 MAC = 1 bi
 MFMA_FP32_PEAK_TFLOPS = 157.3   # MI355X fp32 matrix peak
 HBM_PEAK_GBS = 8000.0
 
+# HBM traffic of the dominant kernel from two rocprofv3 --pmc passes
+# (FETCH_SIZE, WRITE_SIZE, KiB per dispatch) over this same script.  The
+# counters are calibrated on a 256 MiB device-to-device copy in the same
+# runs: FETCH_SIZE read 131086.8 KiB for 262144 KiB moved (factor 2.0),
+# WRITE_SIZE read 262144.0 KiB (factor 1.0).  A figure is reported only while
+# the sources it was taken from hash to the values recorded with it.
+MEASURED_TRAFFIC = {
+    ("cifar_bnn_b64", "L5 bconv 8x8x512->512 k3 pool"): dict(
+        fetch_kib=1332.0, write_kib=64.0, fetch_scale=2.0, write_scale=1.0,
+        sources={"paper_1808_00209_amd/csrc/bconv_mfma.hip":
+                 "88c0bee2ed1c86dd0aef09f88e07fb71db61ff1dc15861337e281f43ec58ed4d",
+                 "paper_1808_00209_amd/build.py":
+                 "5a1b9407cd0a1d30edb2c32c08ff6aec4d3deee5a372d7cbcaea3f1d85a4fbe3"}),
+}
+
+
+def measured_traffic(workload, kernel):
+    """Scaled HBM bytes per launch of `kernel`, or None once its sources changed."""
+    import hashlib
+    rec = MEASURED_TRAFFIC.get((workload, kernel))
+    if rec is None:
+        return None
+    for rel, digest in rec["sources"].items():
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != digest:
+                return None
+    return int(round((rec["fetch_kib"] * rec["fetch_scale"]
+                      + rec["write_kib"] * rec["write_scale"]) * 1024))
+
+
 WORKLOADS = {
     "cifar_bnn_b64": dict(cfg=3, batch=64, H=32, W=32, C=3),
     "vehicle_bnn_b256": dict(cfg=4, batch=256, H=96, W=96, C=3),
@@ -87,6 +117,26 @@ def layer_shapes(layers, H, W, C):
             out.append(("L%d %s %d->%d" % (li, k, K, N), k, dict(K=K, N=N), K * N))
             h, w, c = 1, 1, N
     return out
+
+
+def algorithmic_bytes(kind, g, batch):
+    """Bytes one launch of a layer must move: packed input words (fp32 for
+    the first layer), packed weights, thresholds, flips and packed output
+    bits.  No im2col copies, no re-reads."""
+    wd = lambda n: (n + 31) // 32
+    if kind in ("fconv", "bconv"):
+        Ho = g["H"] + 2 * g["pad"] - g["KH"] + 1
+        Wo = g["W"] + 2 * g["pad"] - g["KW"] + 1
+        Hp, Wp = (Ho // 2, Wo // 2) if g["pool"] else (Ho, Wo)
+        x = batch * g["H"] * g["W"] * (4 * g["C"] if kind == "fconv" else 4 * wd(g["C"]))
+        w = g["F"] * g["KH"] * g["KW"] * 4 * wd(g["C"])
+        return x + w + 4 * g["F"] + 4 * wd(g["F"]) + batch * Hp * Wp * 4 * wd(g["F"])
+    if kind in ("bfc", "bfc_logits"):
+        x = batch * 4 * wd(g["K"]) + g["N"] * 4 * wd(g["K"])
+        if kind == "bfc":
+            return x + 4 * g["N"] + 4 * wd(g["N"]) + batch * 4 * wd(g["N"])
+        return x + batch * 4 * g["N"]
+    return batch * g["H"] * g["W"] * (4 * g["C"] + 4 * wd(g["C"])) + 4 * g["C"]
 
 
 def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
@@ -284,6 +334,7 @@ def main():
     else:
         dom_ops, bound, peak, unit = 2 * macs * batch, "alu", VALU_PEAK_TOPS, "TOP/s"
     achieved_tops = dom_ops / (dom_ms * 1e-3) / 1e12
+    dom_bytes = algorithmic_bytes(kind, g, batch)
 
     result = {
         "metric": "binary conv GOPS (2 ops per bit-MAC) and images/s at batch 1 and 64",
@@ -312,7 +363,10 @@ def main():
         "per_layer": per_layer,
         "roofline": {"kernel": name, "bound": bound, "achieved": round(achieved_tops, 2),
                      "peak": peak, "unit": unit, "frac": round(achieved_tops / peak, 4),
-                     "traffic": None,
+                     "traffic": measured_traffic(args.workload, name),
+                     "algorithmic_bytes": dom_bytes,
+                     "frac_of_valu_xor_popcount_peak":
+                         round(achieved_tops / VALU_PEAK_TOPS, 4) if kind != "fconv" else None,
                      "valu_xor_popcount_peak_TOPS": VALU_PEAK_TOPS},
     }
     if not args.no_cpu_baseline:
