@@ -79,6 +79,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target length of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-float-baseline", action="store_true",
+                    help="skip the floating-point network timed on the same GPU")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one 256 MiB device-to-device copy (calibrates the "
                          "FETCH_SIZE / WRITE_SIZE counters of a profiling run)")
@@ -139,6 +141,60 @@ def algorithmic_bytes(kind, g, batch):
     return batch * g["H"] * g["W"] * (4 * g["C"] + 4 * wd(g["C"])) + 4 * g["C"]
 
 
+def float_baseline(layers, H, W, C, batch, dtype, steps, torch):
+    """The same network in floating point on the same GPU (torch conv2d on
+    MIOpen, linear on hipBLASLt): real-valued weights and activations,
+    max-pool and hardtanh in place of the threshold, as the float network a
+    binarized one is compared with (Table I).  Returns ms per forward."""
+    import torch.nn.functional as tf
+    gen = torch.Generator(device="cuda").manual_seed(11)
+    params = []
+    h, w, c = H, W, C
+    for L in layers:
+        k = L["kind"]
+        if k == "input_threshold":
+            continue
+        if k in ("fconv", "bconv"):
+            wt = torch.randn((L["F"], c, L["KH"], L["KW"]), device="cuda", generator=gen,
+                             dtype=torch.float32).to(dtype) * (1.0 / (c * 9) ** 0.5)
+            params.append(("conv", wt, L["pad"], L.get("pool", 0)))
+            h, w = h + 2 * L["pad"] - L["KH"] + 1, w + 2 * L["pad"] - L["KW"] + 1
+            if L.get("pool", 0):
+                h, w = h // 2, w // 2
+            c = L["F"]
+        else:
+            wt = torch.randn((L["N"], L["K"]), device="cuda", generator=gen,
+                             dtype=torch.float32).to(dtype) * (1.0 / L["K"] ** 0.5)
+            params.append(("fc", wt, k == "bfc_logits", 0))
+    x0 = torch.randn((batch, C, H, W), device="cuda", generator=gen, dtype=torch.float32).to(dtype)
+
+    def fwd():
+        x = x0
+        for kind, wt, a, b in params:
+            if kind == "conv":
+                x = tf.conv2d(x, wt, padding=a)
+                if b:
+                    x = tf.max_pool2d(x, 2)
+                x = tf.hardtanh(x)
+            else:
+                x = tf.linear(x.reshape(x.shape[0], -1), wt)
+                if not a:
+                    x = tf.hardtanh(x)
+        return x
+
+    with torch.no_grad():
+        for _ in range(3):
+            fwd()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fwd()
+        e1.record()
+        torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
 def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
     """Average kernel time (ms) of one layer's standalone call on random bits."""
     gen = torch.Generator(device="cuda").manual_seed(7)
@@ -176,10 +232,21 @@ def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
     for _ in range(3):
         fn()
     torch.cuda.synchronize()
+    # The reps launches go into one HIP graph, so the figure is the kernels'
+    # back-to-back time rather than the host's per-call launch cost.
+    side = torch.cuda.Stream()
+    side.wait_stream(s)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph, stream=side):
+            for _ in range(reps):
+                fn()
+    s.wait_stream(side)
+    graph.replay()
+    torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(s)
-    for _ in range(reps):
-        fn()
+    graph.replay()
     e1.record(s)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / reps
@@ -369,6 +436,20 @@ def main():
                          round(achieved_tops / VALU_PEAK_TOPS, 4) if kind != "fconv" else None,
                      "valu_xor_popcount_peak_TOPS": VALU_PEAK_TOPS},
     }
+    if not args.no_float_baseline:
+        fb = {}
+        for name, dt in (("fp32", torch.float32), ("bf16", torch.bfloat16)):
+            t64 = float_baseline(layers, H, W, C, batch, dt, args.steps, torch)
+            t1 = float_baseline(layers, H, W, C, 1, dt, max(20, args.steps), torch)
+            fb[name] = {"ms_per_step": round(t64, 5),
+                        "images_per_s": round(batch / (t64 * 1e-3), 1),
+                        "batch1_us": round(t1 * 1e3, 2),
+                        "speedup_binary_vs_float": round(t64 / ms_per_step, 2),
+                        "speedup_binary_vs_float_batch1": round(
+                            t1 * 1e3 / float(per_img_us.mean()), 2)}
+        result["float_baseline"] = dict(
+            fb, note="same layer shapes in floating point (torch conv2d on MIOpen, linear, "
+                     "max-pool, hardtanh), random weights, eager launches")
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(layers, wl["cfg"], args.cpu_seconds,
                                               2 * bin_macs_img)

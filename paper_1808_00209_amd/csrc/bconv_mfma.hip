@@ -122,8 +122,8 @@ struct Mfma32Args {
 //   KS   1: the 4 waves of a block take 4 consecutive 64-pixel groups;
 //        >1: the KS (2..8) waves of a block split the iterations of one tile
 //        and add their partial sums in LDS (grids too small to fill the chip).
-// Loads run one iteration ahead of the MFMAs (two register sets).
-template <int VW, bool POOL, int TF, int KS>
+//   PD   register sets of loads in flight (prefetch depth).
+template <int VW, bool POOL, int TF, int KS, int PD>
 __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(Mfma32Args a) {
   constexpr int TP = 2;
   const int lane = threadIdx.x & 63;
@@ -247,19 +247,21 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
   };
 
   if (it0 < it1) {
-    uint32_t wa[TF][VW], xa[TP][VW], wb[TF][VW], xb[TP][VW];
-    load_next(wa, xa);
-    for (int it = it0; it < it1; it += 2) {
-      // The scheduling barriers keep each prefetch ahead of the MFMAs it
-      // overlaps (the scheduler would otherwise sink the loads below them).
-      load_next(wb, xb);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(wa, xa);
-      __builtin_amdgcn_sched_barrier(0);
-      load_next(wa, xa);
-      __builtin_amdgcn_sched_barrier(0);
-      if (it + 1 < it1) compute(wb, xb);
-      __builtin_amdgcn_sched_barrier(0);
+    // PD register sets in a ring: the loads of iteration it + PD are issued
+    // right after iteration it's MFMAs, so PD - 1 iterations of loads are
+    // always in flight.  The scheduling barriers keep each load in place
+    // (the scheduler would otherwise sink it below the next MFMAs).
+    uint32_t wr[PD][TF][VW], xr[PD][TP][VW];
+#pragma unroll
+    for (int d = 0; d < PD; ++d) load_next(wr[d], xr[d]);
+    for (int it = it0; it < it1; it += PD) {
+#pragma unroll
+      for (int d = 0; d < PD; ++d) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (it + d < it1) compute(wr[d], xr[d]);
+        __builtin_amdgcn_sched_barrier(0);
+        load_next(wr[d], xr[d]);
+      }
     }
   }
 
@@ -381,26 +383,31 @@ int env_int(const char* name, int dflt) {
   return e ? atoi(e) : dflt;
 }
 
-template <int VW, bool POOL>
+template <int VW, bool POOL, int PD>
 hipError_t launch32(const Mfma32Args& a, int tf, int ks, hipStream_t s) {
   const unsigned fy = static_cast<unsigned>((a.F + 32 * tf - 1) / (32 * tf));
   const unsigned groups = static_cast<unsigned>((a.items + 63) / 64);
   if (ks == 1) {
     dim3 grid((groups + 3) / 4, fy), block(256);
     if (tf == 2)
-      bconv_mfma32_kernel<VW, POOL, 2, 1><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 2, 1, PD><<<grid, block, 0, s>>>(a);
     else
-      bconv_mfma32_kernel<VW, POOL, 1, 1><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 1, PD><<<grid, block, 0, s>>>(a);
   } else {
     dim3 grid(groups, fy), block(64 * ks);
     if (ks == 2)
-      bconv_mfma32_kernel<VW, POOL, 1, 2><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 2, PD><<<grid, block, 0, s>>>(a);
     else if (ks == 4)
-      bconv_mfma32_kernel<VW, POOL, 1, 4><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 4, PD><<<grid, block, 0, s>>>(a);
     else
-      bconv_mfma32_kernel<VW, POOL, 1, 8><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 8, PD><<<grid, block, 0, s>>>(a);
   }
   return hipGetLastError();
+}
+
+template <int VW, bool POOL>
+hipError_t launch32_pd(const Mfma32Args& a, int tf, int ks, int pd, hipStream_t s) {
+  return pd == 4 ? launch32<VW, POOL, 4>(a, tf, ks, s) : launch32<VW, POOL, 2>(a, tf, ks, s);
 }
 
 hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint32_t* w,
@@ -436,23 +443,28 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   const int iters = g.KH * g.KW * (g.Cw / (2 * vw));
 
   // Tile shape and K split: 64-filter wave tiles down to ~1 wave per SIMD
-  // (1024 waves), then 32-filter tiles, then a K split over up to 8 waves
-  // (keeping at least 2 iterations per wave).
+  // (1024 waves), then 32-filter tiles with a K split over up to 4 waves
+  // until there are ~2 waves per SIMD (keeping at least 2 iterations per
+  // wave).  Measured on the layer shapes of both networks: splitting 8 ways
+  // never beat 4 (the LDS reduction then costs more than it hides).
   const int64_t groups = (a.items + 63) / 64;
   const int64_t ftiles = (g.F + 31) / 32;
   int tf = 2, ks = 1;
   if (g.F % 64 != 0 || groups * (g.F / 64) < 1024) {
     tf = 1;
-    while (ks < 8 && groups * ftiles * ks < 1024 && iters >= 4 * ks) ks *= 2;  // >= 2 per wave
+    while (ks < 4 && groups * ftiles * ks < 2048 && iters >= 4 * ks) ks *= 2;
   }
-  // Tuning overrides (filter tiles per wave, K split).
+  // Tuning overrides (filter tiles per wave, K split, prefetch depth).
   tf = env_int("BNN_MFMA_TF", tf);
   ks = env_int("BNN_MFMA_KS", ks);
   if (tf != 1 && tf != 2) tf = 1;
   if (g.F % (32 * tf) != 0 || (ks > 1 && tf != 1)) tf = 1;
   if (ks != 1 && ks != 2 && ks != 4 && ks != 8) ks = 1;
-  if (vw == 2) return pool ? launch32<2, true>(a, tf, ks, s) : launch32<2, false>(a, tf, ks, s);
-  return pool ? launch32<1, true>(a, tf, ks, s) : launch32<1, false>(a, tf, ks, s);
+  int pd = env_int("BNN_MFMA_PD", 2);
+  if (pd != 2 && pd != 4) pd = 2;
+  if (vw == 2)
+    return pool ? launch32_pd<2, true>(a, tf, ks, pd, s) : launch32_pd<2, false>(a, tf, ks, pd, s);
+  return pool ? launch32_pd<1, true>(a, tf, ks, pd, s) : launch32_pd<1, false>(a, tf, ks, pd, s);
 }
 
 }  // namespace

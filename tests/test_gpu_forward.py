@@ -14,9 +14,11 @@ from paper_1808_00209_amd.device import to_device, upload_network
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(params=["auto", "valu"])
+@pytest.fixture(params=["auto", "valu", "pd4"])
 def algo(request, monkeypatch):
-    monkeypatch.setenv("BNN_ALGO", request.param)
+    monkeypatch.setenv("BNN_ALGO", "valu" if request.param == "valu" else "auto")
+    if request.param == "pd4":
+        monkeypatch.setenv("BNN_MFMA_PD", "4")
     return request.param
 
 

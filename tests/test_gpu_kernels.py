@@ -16,14 +16,17 @@ from paper_1808_00209_amd.device import pack_flips, pack_pm1, to_device, words_u
 pytestmark = pytest.mark.gpu
 
 # Kernel families: "auto" takes the fp4 matrix-core kernel wherever the shape
-# allows it (C a multiple of 128, F a multiple of 64), "valu" forces the
-# XOR-popcount vector kernels everywhere.
-ALGOS = ["auto", "valu"]
+# allows it (C a multiple of 64, at most 32 taps), "valu" forces the
+# XOR-popcount vector kernels everywhere, "pd4" is "auto" with four sets of
+# loads in flight in the matrix-core loop instead of the shape's default.
+ALGOS = ["auto", "valu", "pd4"]
 
 
 @pytest.fixture(params=ALGOS)
 def algo(request, monkeypatch):
-    monkeypatch.setenv("BNN_ALGO", request.param)
+    monkeypatch.setenv("BNN_ALGO", "valu" if request.param == "valu" else "auto")
+    if request.param == "pd4":
+        monkeypatch.setenv("BNN_MFMA_PD", "4")
     return request.param
 
 
