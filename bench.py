@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 
 VALU_PEAK_TOPS = 1258.29  # 256 CU x 64 lanes x 2.4 GHz x 32 bit-MACs x 2 ops / 2 instr
 MFMA_FP4_PEAK_TFLOPS = 10100.0  # MI355X dense fp4 matrix peak (1 fp4 MAC = 1 bit-MAC)
-MFMA_FP32_PEAK_TFLOPS = 157.3   # MI355X fp32 matrix peak
+MFMA_FP16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak
 HBM_PEAK_GBS = 8000.0
 
 # HBM traffic of the dominant kernel from two rocprofv3 --pmc passes
@@ -101,22 +101,39 @@ def layer_shapes(layers, H, W, C):
     """Per layer: (name, kind, geometry dict, bit-MACs per image)."""
     out = []
     h, w, c = H, W, C
+    fused = (len(layers) > 1 and layers[0]["kind"] == "input_threshold"
+             and layers[1]["kind"] == "bconv"
+             and layers[1]["KH"] * layers[1]["KW"] * layers[1]["C"] <= 32)
     for li, L in enumerate(layers):
         k = L["kind"]
+        if k == "input_threshold" and fused:
+            continue  # runs inside the next layer's patch-packing kernel
+        if k == "bconv" and li == 1 and fused:
+            KH, KW, pad, F = L["KH"], L["KW"], L["pad"], L["F"]
+            Ho, Wo = h + 2 * pad - KH + 1, w + 2 * pad - KW + 1
+            pool = L.get("pool", 0)
+            name = "L0+L1 threshold+bconv %dx%dx%d->%d k%d%s (patch words)" % (
+                h, w, c, F, KH, " pool" if pool else "")
+            out.append((name, "bconv_input",
+                        dict(H=h, W=w, C=c, F=F, KH=KH, KW=KW, pad=pad, pool=pool,
+                             offset_layer=0),
+                        Ho * Wo * F * KH * KW * c))
+            h, w, c = (Ho // 2, Wo // 2, F) if pool else (Ho, Wo, F)
+            continue
         if k == "input_threshold":
-            out.append(("L%d pack %dx%dx%d" % (li, h, w, c), k, dict(H=h, W=w, C=c), 0))
+            out.append(("L%d pack %dx%dx%d" % (li, h, w, c), k, dict(H=h, W=w, C=c, li=li), 0))
         elif k in ("fconv", "bconv"):
             KH, KW, pad, F = L["KH"], L["KW"], L["pad"], L["F"]
             Ho, Wo = h + 2 * pad - KH + 1, w + 2 * pad - KW + 1
             macs = Ho * Wo * F * KH * KW * c
             pool = L.get("pool", 0)
             name = "L%d %s %dx%dx%d->%d k%d%s" % (li, k, h, w, c, F, KH, " pool" if pool else "")
-            out.append((name, k, dict(H=h, W=w, C=c, F=F, KH=KH, KW=KW, pad=pad, pool=pool),
+            out.append((name, k, dict(H=h, W=w, C=c, F=F, KH=KH, KW=KW, pad=pad, pool=pool, li=li),
                         0 if k == "fconv" else macs))
             h, w, c = (Ho // 2, Wo // 2, F) if pool else (Ho, Wo, F)
         else:
             K, N = L["K"], L["N"]
-            out.append(("L%d %s %d->%d" % (li, k, K, N), k, dict(K=K, N=N), K * N))
+            out.append(("L%d %s %d->%d" % (li, k, K, N), k, dict(K=K, N=N, li=li), K * N))
             h, w, c = 1, 1, N
     return out
 
@@ -126,11 +143,11 @@ def algorithmic_bytes(kind, g, batch):
     the first layer), packed weights, thresholds, flips and packed output
     bits.  No im2col copies, no re-reads."""
     wd = lambda n: (n + 31) // 32
-    if kind in ("fconv", "bconv"):
+    if kind in ("fconv", "bconv", "bconv_input"):
         Ho = g["H"] + 2 * g["pad"] - g["KH"] + 1
         Wo = g["W"] + 2 * g["pad"] - g["KW"] + 1
         Hp, Wp = (Ho // 2, Wo // 2) if g["pool"] else (Ho, Wo)
-        x = batch * g["H"] * g["W"] * (4 * g["C"] if kind == "fconv" else 4 * wd(g["C"]))
+        x = batch * g["H"] * g["W"] * (4 * wd(g["C"]) if kind == "bconv" else 4 * g["C"])
         w = g["F"] * g["KH"] * g["KW"] * 4 * wd(g["C"])
         return x + w + 4 * g["F"] + 4 * wd(g["F"]) + batch * Hp * Wp * 4 * wd(g["F"])
     if kind in ("bfc", "bfc_logits"):
@@ -204,6 +221,17 @@ def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
         out = torch.empty((batch, g["H"], g["W"], bnn.words(g["C"])), dtype=torch.int32,
                           device="cuda")
         fn = lambda: bnn.bnn_pack_bits(x, dev_layer.get("offset"), out=out)
+    elif kind == "bconv_input":
+        desc = bnn.conv_desc(batch, g["H"], g["W"], g["C"], g["F"], g["KH"], g["KW"], 1,
+                             g["pad"], g["pool"])
+        Ho, Wo, Hp, Wp = bnn.bnn_conv_output_dims(desc)
+        ob = torch.empty((batch, Hp, Wp, bnn.words(g["F"])), dtype=torch.int32, device="cuda")
+        x = torch.randint(0, 256, (batch, g["H"], g["W"], g["C"]), device="cuda",
+                          generator=gen).to(torch.float32)
+        off = dev_layer[0].get("offset")
+        wl = dev_layer[1]
+        fn = lambda: bnn.bnn_bconv2d_input(desc, x, off, wl["w"], wl["thr"], wl.get("flip"),
+                                           want_sums=False, out_bits=ob)
     elif kind in ("fconv", "bconv"):
         desc = bnn.conv_desc(batch, g["H"], g["W"], g["C"], g["F"], g["KH"], g["KW"], 1,
                              g["pad"], g["pool"])
@@ -373,7 +401,8 @@ def main():
     dev_layers = [upload_layer(L) for L in layers]
     per_layer = []
     saved_algo = os.environ.get("BNN_ALGO")
-    for (name, kind, g, macs), dl in zip(shapes, dev_layers):
+    for name, kind, g, macs in shapes:
+        dl = (dev_layers[0], dev_layers[1]) if kind == "bconv_input" else dev_layers[g["li"]]
         ms = time_layer(bnn, kind, g, batch, dl, args.layer_reps, torch)
         os.environ["BNN_ALGO"] = "valu"
         ms_valu = time_layer(bnn, kind, g, batch, dl, args.layer_reps, torch)
@@ -390,10 +419,11 @@ def main():
     dom_ms = per_layer[dom_i]["ms"]
     name, kind, g, macs = shapes[dom_i]
     if kind == "fconv":
-        # fp32 first layer on fp32 MFMA (v_mfma_f32_16x16x4f32): 2 flops/MAC
+        # fp32 first layer on the fp16 matrix cores (v_mfma_f32_16x16x32_f16,
+        # x split into two fp16 halves): 2 algorithmic flops per MAC
         fmacs = batch * (g["H"] + 2 * g["pad"] - g["KH"] + 1) * (g["W"] + 2 * g["pad"] - g["KW"] + 1) \
             * g["F"] * g["KH"] * g["KW"] * g["C"]
-        dom_ops, bound, peak, unit = 2 * fmacs, "mfma", MFMA_FP32_PEAK_TFLOPS, "TFLOP/s"
+        dom_ops, bound, peak, unit = 2 * fmacs, "mfma", MFMA_FP16_PEAK_TFLOPS, "TFLOP/s"
     elif kind in ("bconv", "bfc", "bfc_logits") and (g.get("C", g.get("K", 0)) % 64 == 0) \
             and not (kind != "bconv" and batch <= 16):
         # binary layer on fp4 MFMA: one fp4 multiply-accumulate per bit-MAC

@@ -149,6 +149,28 @@ bnn_status bnn_fconv2d_binw(const bnn_conv_desc* d, const float* in,
                             uint32_t* out_bits, hipStream_t stream);
 
 /*
+ * Binary convolution over a real-valued image binarized on the fly: the
+ * input thresholding of Sec. II-C, bit = (x + offset[c]) > 0 in fp32, then
+ * Eq. 3 / Eq. 4 with pad value -1 and the bnn_bconv2d epilogue.  The result
+ * equals bnn_pack_bits(x, offset) followed by bnn_bconv2d, bit for bit.
+ * Each output pixel's whole binarized window is packed into one word (the
+ * patch packing of Algorithm 1 with B = KH*KW*C bits), so every dot product
+ * is a single XOR + popcount; this needs KH*KW*C <= 32 (e.g. a 3x3 conv over
+ * 3 colour channels, 27 bits).
+ *   x         [N][H][W][C] fp32 image.
+ *   offset    [C] fp32 per-channel offsets T_c, or NULL for all-zero.
+ *   w         [F][KH][KW][Cw] u32 packed weights (Cw = 1 here).
+ *   thr, flip, out_sums, out_bits: as for bnn_bconv2d.
+ * Alignment as for bnn_bconv2d.  Errors: as for bnn_bconv2d, and
+ * BNN_ERR_UNSUPPORTED when KH*KW*C > 32.
+ */
+bnn_status bnn_bconv2d_input(const bnn_conv_desc* d, const float* x,
+                             const float* offset, const uint32_t* w,
+                             const int32_t* thr, const uint32_t* flip,
+                             int32_t* out_sums, uint32_t* out_bits,
+                             hipStream_t stream);
+
+/*
  * Binary fully-connected layer / GEMM (Sec. III-B, Eq. 4):
  *   S[m][n] = K - 2 * sum_j popcount(A[m][j] XOR B[n][j])   (valid bits only)
  *   A         [M][Kw] u32, Kw = ceil(K / 32): M packed input vectors.

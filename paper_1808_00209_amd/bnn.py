@@ -28,8 +28,8 @@ LAYER_BFC_LOGITS = 5
 
 # Every symbol include/bnn.h declares.
 EXPORTED = ["bnn_last_error", "bnn_abi_version", "bnn_pack_bits", "bnn_conv_output_dims",
-            "bnn_bconv2d", "bnn_fconv2d_binw", "bnn_bgemm", "bnn_forward_workspace_size",
-            "bnn_forward"]
+            "bnn_bconv2d", "bnn_fconv2d_binw", "bnn_bconv2d_input", "bnn_bgemm",
+            "bnn_forward_workspace_size", "bnn_forward"]
 
 
 class BnnError(RuntimeError):
@@ -188,6 +188,28 @@ def bnn_fconv2d_binw(desc: ConvDesc, x, w, thr=None, flip=None, want_sums=True,
     return out_sums, out_bits
 
 
+def bnn_bconv2d_input(desc: ConvDesc, x, offset, w, thr=None, flip=None, want_sums=True,
+                      want_bits=True, out_sums=None, out_bits=None, stream=None):
+    """Binary conv over an fp32 image thresholded on the fly, bit = x + offset > 0
+    (Sec. II-C), one packed patch word per window (Algorithm 1, KH*KW*C <= 32).
+    Same outputs as bnn_pack_bits followed by bnn_bconv2d."""
+    lib = load()
+    Ho, Wo, Hp, Wp = bnn_conv_output_dims(desc)
+    _dev(x, torch.float32, "x")
+    offset = _dev(offset, torch.float32, "offset")
+    _u32(w)
+    thr = _dev(thr, torch.int32, "thr")
+    flip = _dev(flip, torch.int32, "flip")
+    if want_sums and out_sums is None:
+        out_sums = torch.empty((desc.N, Ho, Wo, desc.F), dtype=torch.int32, device=x.device)
+    if want_bits and out_bits is None:
+        out_bits = torch.empty((desc.N, Hp, Wp, words(desc.F)), dtype=torch.int32,
+                               device=x.device)
+    _check(lib.bnn_bconv2d_input(ctypes.byref(desc), _ptr(x), _ptr(offset), _ptr(w), _ptr(thr),
+                                 _ptr(flip), _ptr(out_sums), _ptr(out_bits), _stream(stream)))
+    return out_sums, out_bits
+
+
 def bnn_bgemm(A, B, K, thr=None, flip=None, want_sums=True, want_bits=True, out_sums=None,
               out_bits=None, stream=None):
     """Binary GEMM / FC (Sec. III-B): A [M,Kw], B [N,Kw] packed -> sums [M,N],
@@ -258,5 +280,6 @@ def bnn_forward(net: Network, x, workspace=None, logits=None, stream=None):
 pack_bits = bnn_pack_bits
 bconv2d = bnn_bconv2d
 fconv2d_binw = bnn_fconv2d_binw
+bconv2d_input = bnn_bconv2d_input
 bgemm = bnn_bgemm
 forward = bnn_forward

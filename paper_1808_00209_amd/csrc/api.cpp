@@ -227,6 +227,29 @@ bnn_status bnn_fconv2d_binw(const bnn_conv_desc* d, const float* in, const uint3
   }
 }
 
+bnn_status bnn_bconv2d_input(const bnn_conv_desc* d, const float* x, const float* offset,
+                             const uint32_t* w, const int32_t* thr, const uint32_t* flip,
+                             int32_t* out_sums, uint32_t* out_bits, hipStream_t stream) {
+  try {
+    bnn::ConvGeom g;
+    bnn_status st = conv_geom(d, &g);
+    if (st != BNN_OK) return st;
+    if (!bnn::bconv_patch_supported(g))
+      return fail(BNN_ERR_UNSUPPORTED,
+                  "bconv2d_input: a window of KH*KW*C = %lld bits does not fit one word (max 32)",
+                  (long long)(int64_t{g.KH} * g.KW * g.C));
+    if (int64_t{g.N} * g.H * g.W * g.C > kMaxItems)
+      return fail(BNN_ERR_SHAPE, "bconv2d_input: image too large for 32-bit indexing");
+    st = check_outputs(x, w, thr, out_sums, out_bits);
+    if (st != BNN_OK) return st;
+    return hip_status(
+        bnn::launch_bconv_patch(g, x, offset, w, thr, flip, out_sums, out_bits, stream),
+        "bconv2d_input launch");
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "bconv2d_input: unexpected C++ exception");
+  }
+}
+
 bnn_status bnn_bgemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
                      const uint32_t* B, const int32_t* thr, const uint32_t* flip,
                      int32_t* out_sums, uint32_t* out_bits, hipStream_t stream) {
@@ -362,6 +385,19 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
                   2 * half);
     uint32_t* buf[2] = {static_cast<uint32_t*>(workspace),
                         reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + half)};
+    // An input threshold followed by a conv whose window fits one word runs
+    // as one patch-packing kernel on the fp32 image (BNN_PATCH=0 keeps the
+    // two separate steps).
+    bool fuse_input = false;
+    if (n_layers > 1 && layers[0].kind == BNN_LAYER_INPUT_THRESHOLD &&
+        layers[1].kind == BNN_LAYER_BCONV) {
+      const char* e = getenv("BNN_PATCH");
+      bnn::ConvGeom g1;
+      g1.KH = layers[1].KH;
+      g1.KW = layers[1].KW;
+      g1.C = layers[1].C;
+      fuse_input = !(e && strcmp(e, "0") == 0) && bnn::bconv_patch_supported(g1);
+    }
     int cur = 0;  // buffer holding the current packed activations
     int64_t h = H, w = W, c = C;
     for (int32_t li = 0; li < n_layers; ++li) {
@@ -371,7 +407,8 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
       hipError_t e = hipSuccess;
       switch (l.kind) {
         case BNN_LAYER_INPUT_THRESHOLD:
-          e = bnn::launch_pack_bits(input, l.offset, int64_t{batch} * h * w, c, dst, stream);
+          if (!fuse_input)
+            e = bnn::launch_pack_bits(input, l.offset, int64_t{batch} * h * w, c, dst, stream);
           break;
         case BNN_LAYER_FCONV_BINW:
         case BNN_LAYER_BCONV: {
@@ -381,6 +418,9 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
           conv_geom(&d, &g);
           if (l.kind == BNN_LAYER_FCONV_BINW)
             e = bnn::launch_fconv_binw(g, input, l.w, l.thr, l.flip, nullptr, dst, stream);
+          else if (li == 1 && fuse_input)
+            e = bnn::launch_bconv_patch(g, input, layers[0].offset, l.w, l.thr, l.flip, nullptr,
+                                        dst, stream);
           else
             e = launch_conv(g, src, l.w, l.thr, l.flip, nullptr, dst, stream);
           h = g.Hp;

@@ -41,6 +41,15 @@ hipError_t launch_bconv_mfma(const ConvGeom& g, const uint32_t* in,
                              const uint32_t* flip, int32_t* sums,
                              uint32_t* bits, hipStream_t s);
 
+// Binary conv over an fp32 image thresholded on the fly, one packed patch
+// word per output pixel.  Supported when bconv_patch_supported(g):
+// KH*KW*C <= 32.
+bool bconv_patch_supported(const ConvGeom& g);
+hipError_t launch_bconv_patch(const ConvGeom& g, const float* x,
+                              const float* offset, const uint32_t* w,
+                              const int32_t* thr, const uint32_t* flip,
+                              int32_t* sums, uint32_t* bits, hipStream_t s);
+
 // Binary GEMM for a handful of rows (M <= 16): one output column per lane,
 // the K words split over the waves of a block.
 hipError_t launch_bgemv_valu(int64_t M, int64_t N, int64_t K,

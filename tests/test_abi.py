@@ -93,6 +93,25 @@ def test_bconv_null_and_alignment_errors():
 
 
 @needs_lib
+def test_bconv_input_errors():
+    lib = bnn.load()
+
+    def call(desc, x=A, off=None, w=A, thr=A, sums=A, bits=A):
+        return lib.bnn_bconv2d_input(ctypes.byref(desc), x, off, w, thr, None, sums, bits, None)
+
+    # a window must fit one word: 3x3x4 = 36 bits does not, 3x3x3 and 5x5x1 do
+    assert call(_conv(C=4)) == 4 and "36 bits" in bnn.last_error()
+    assert call(_conv(C=32, KH=1, KW=2)) == 4
+    assert call(_conv(C=3, stride=2)) == 4 and "stride" in bnn.last_error()
+    assert call(_conv(C=3, pool=3)) == 2
+    assert call(_conv(C=3), x=None) == 1 and "input" in bnn.last_error()
+    assert call(_conv(C=3), thr=None) == 1 and "thr" in bnn.last_error()
+    assert call(_conv(C=3), sums=None, bits=None) == 1
+    assert call(_conv(C=3), x=A + 4) == 3
+    assert lib.bnn_bconv2d_input(None, A, None, A, A, None, A, A, None) == 1
+
+
+@needs_lib
 def test_conv_output_dims():
     assert bnn.bnn_conv_output_dims(_conv(H=32, W=30, pool=2)) == (32, 30, 16, 15)
     assert bnn.bnn_conv_output_dims(_conv(H=7, W=5, pool=2, KH=1, KW=1, pad=0)) == (7, 5, 3, 2)

@@ -14,11 +14,17 @@ from paper_1808_00209_amd.device import to_device, upload_network
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(params=["auto", "valu", "pd4"])
+# "auto": default kernels; "valu": vector-ALU kernels only; "pd4": four sets
+# of loads in flight in the matrix-core loop; "nopatch": the thresholded
+# input packed by bnn_pack_bits and convolved by the generic kernel instead
+# of the fused patch-packing kernel.
+@pytest.fixture(params=["auto", "valu", "pd4", "nopatch"])
 def algo(request, monkeypatch):
     monkeypatch.setenv("BNN_ALGO", "valu" if request.param == "valu" else "auto")
     if request.param == "pd4":
         monkeypatch.setenv("BNN_MFMA_PD", "4")
+    if request.param == "nopatch":
+        monkeypatch.setenv("BNN_PATCH", "0")
     return request.param
 
 

@@ -335,3 +335,66 @@ def test_fconv_cifar_first_layer_batch64(algo):
     S = oracle.fconv2d(x, L["w"], 1, 1)
     assert np.array_equal(sums.cpu().numpy().astype(np.float64), S)
     assert np.array_equal(words_u32(bits), oracle.pack_eq2(oracle.threshold(S, L["thr"], L["flip"])))
+
+
+# --------------------------------------------- thresholded-input patch conv --
+# N, H, W, C, F, KH, KW, pad, pool: several 8x32 tiles with ragged edges, odd
+# sizes under pooling (floor), F tails, 25- and 18-bit windows, pad 0, a
+# one-pixel window of 32 channels, and a 32-tap column window with F > 256
+# (two rounds of staged filters).
+PATCH_CASES = [
+    (2, 12, 40, 3, 64, 3, 3, 1, 0),
+    (1, 17, 35, 3, 64, 3, 3, 1, 2),
+    (1, 9, 9, 3, 40, 3, 3, 1, 2),
+    (2, 10, 11, 1, 32, 5, 5, 2, 0),
+    (1, 8, 70, 2, 96, 3, 3, 0, 0),
+    (1, 6, 6, 32, 33, 1, 1, 0, 2),
+    (1, 40, 3, 1, 300, 32, 1, 3, 0),
+]
+
+
+def _patch_case(seed, N, H, W, C, F, KH, KW, pad):
+    rng = np.random.default_rng(seed)
+    x = synth.pixels(rng, (N, H, W, C))
+    off = synth.rgb_offsets(rng, C)
+    w = _pm1(rng, (F, KH, KW, C))
+    K = KH * KW * C
+    thr = rng.integers(-K // 2, K // 2 + 1, size=F).astype(np.int32)
+    flip = rng.integers(0, 2, size=F).astype(np.uint8)
+    return x, off, w, thr, flip
+
+
+@pytest.mark.parametrize("case", PATCH_CASES)
+def test_bconv_input_patch_bit_exact(case):
+    N, H, W, C, F, KH, KW, pad, pool = case
+    x, off, w, thr, flip = _patch_case(7 + sum(case), N, H, W, C, F, KH, KW, pad)
+    desc = bnn.conv_desc(N, H, W, C, F, KH, KW, 1, pad, pool)
+    sums, bits = bnn.bnn_bconv2d_input(desc, to_device(x), to_device(off), pack_pm1(w),
+                                       to_device(thr, torch.int32), pack_flips(flip))
+    torch.cuda.synchronize()
+    xb = oracle.sign(x.reshape(-1, C), off).reshape(x.shape)
+    S = oracle.conv2d(xb, w, 1, pad)
+    b = oracle.threshold(S, thr, flip)
+    if pool:
+        b = oracle.maxpool2(b)
+    assert np.array_equal(sums.cpu().numpy(), S)
+    assert np.array_equal(words_u32(bits), oracle.pack_eq2(b))
+
+
+def test_bconv_input_matches_pack_then_bconv():
+    """The fused call equals bnn_pack_bits followed by bnn_bconv2d (bits only,
+    no offset), on the vehicle-shaped first layer at batch 8."""
+    N, H, W, C, F = 8, 96, 96, 3, 64
+    x, _, w, thr, flip = _patch_case(11, N, H, W, C, F, 3, 3, 1)
+    x = x - 127.0  # thresholds at 0 without an offset
+    desc = bnn.conv_desc(N, H, W, C, F, 3, 3, 1, 1, 0)
+    xd, wd = to_device(x), pack_pm1(w)
+    td, fd = to_device(thr, torch.int32), pack_flips(flip)
+    _, fused = bnn.bnn_bconv2d_input(desc, xd, None, wd, td, fd, want_sums=False)
+    packed = bnn.bnn_pack_bits(xd)
+    _, twostep = bnn.bnn_bconv2d(desc, packed, wd, td, fd, want_sums=False)
+    torch.cuda.synchronize()
+    assert torch.equal(fused, twostep)
+    xb = oracle.sign(x[[0, 7]].reshape(-1, C)).reshape((2, H, W, C))
+    ref = oracle.pack_eq2(oracle.threshold(oracle.conv2d(xb, w, 1, 1), thr, flip))
+    assert np.array_equal(words_u32(fused)[[0, 7]], ref)
