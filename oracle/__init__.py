@@ -30,7 +30,7 @@ def build(force: bool = False) -> str:
             os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)):
         tmp = _LIB_PATH + ".tmp%d" % os.getpid()
         subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared",
-                               "-std=c11", "-Wall", "-o", tmp, _SRC])
+                               "-std=c11", "-Wall", "-ffp-contract=off", "-o", tmp, _SRC])
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
 
@@ -49,6 +49,8 @@ def _bind(path: str):
     lib.orc_threshold.argtypes = [P, P, P, i64, i64, P]
     lib.orc_threshold_f64.argtypes = [P, P, P, i64, i64, P]
     lib.orc_maxpool2.argtypes = [P, i32, i32, i32, i32, P]
+    lib.orc_gray_threshold.argtypes = [P, ctypes.c_float, i64, P]
+    lib.orc_lbp.argtypes = [P, i32, i32, i32, P]
     lib.orc_num_threads.restype = ctypes.c_int
     return lib
 
@@ -198,11 +200,34 @@ def maxpool2(x):
     return out
 
 
+def gray_threshold(x, T):
+    """Grayscale thresholding (Table III): sign(gray(x) + T), fp32.
+    x [..., 3] RGB -> [..., 1] +-1."""
+    lib = _load()
+    x, xp = _c(x, np.float32)
+    assert x.shape[-1] == 3
+    rows = x.size // 3
+    out = np.empty(x.shape[:-1] + (1,), np.int8)
+    lib.orc_gray_threshold(xp, float(T), rows, out.ctypes.data)
+    return out
+
+
+def lbp(x):
+    """LBP input binarization (Sec. II-C): x [N,H,W,3] RGB -> [N,H,W,3] +-1."""
+    lib = _load()
+    x, xp = _c(x, np.float32)
+    N, H, W, C = x.shape
+    assert C == 3
+    out = np.empty((N, H, W, 3), np.int8)
+    lib.orc_lbp(xp, N, H, W, out.ctypes.data)
+    return out
+
+
 def forward(layers, x, return_all: bool = False):
     """Run a layer chain (Table II order: conv, pool, ..., FC) on ``x``.
 
-    ``layers`` is a list of dicts (kinds: input_threshold, fconv, bconv, bfc,
-    bfc_logits) holding +-1 int8 weights, int32 thresholds and 0/1 flips.
+    ``layers`` is a list of dicts (kinds: input_threshold, input_gray,
+    input_lbp, fconv, bconv, bfc, bfc_logits) holding +-1 int8 weights, int32 thresholds and 0/1 flips.
     Conv activations are NHWC; FC layers flatten them in (h, w, c) order.
     Returns the int32 logits of the last layer (and every intermediate, on
     request, as +-1 arrays or sums).
@@ -213,6 +238,10 @@ def forward(layers, x, return_all: bool = False):
         k = L["kind"]
         if k == "input_threshold":
             a = sign(a, L.get("offset"))
+        elif k == "input_gray":
+            a = gray_threshold(a, float(L["offset"][0]))
+        elif k == "input_lbp":
+            a = lbp(a)
         elif k in ("fconv", "bconv"):
             conv = fconv2d if k == "fconv" else conv2d
             S = conv(a, L["w"], L.get("stride", 1), L["pad"])

@@ -241,6 +241,70 @@ void orc_maxpool2(const int8_t* x, int32_t N, int32_t H, int32_t W, int32_t C,
   }
 }
 
+/*
+ * Grayscale value of an RGB pixel, the input of the grayscale thresholding
+ * and of the LBP binarization (Sec. II-C; Table III).  The paper does not give
+ * the conversion.  The reading taken is the ITU-R BT.601 luma
+ * 0.299 R + 0.587 G + 0.114 B, evaluated in fp32 as (0.299 R + 0.587 G) +
+ * 0.114 B with every product rounded to fp32 on its own.  Both the oracle and
+ * the kernels use exactly these operations, since the binarization decision
+ * depends on their rounding.
+ */
+static float gray_of(const float* px) {
+  const float r = 0.299f * px[0];
+  const float g = 0.587f * px[1];
+  const float b = 0.114f * px[2];
+  const float rg = r + g;
+  return rg + b;
+}
+
+/*
+ * Grayscale thresholding (Table III "Thresholding Grayscale"): one channel,
+ * out = sign(gray(x) + T) with the addition in fp32.  x: [rows, 3] RGB;
+ * out: [rows] +-1.
+ */
+void orc_gray_threshold(const float* x, float T, int64_t rows, int8_t* out) {
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < rows; ++r) {
+    const float v = gray_of(x + 3 * r) + T;
+    out[r] = sign_pm1(v);
+  }
+}
+
+/*
+ * LBP input binarization (Sec. II-C, local binary patterns).  On the
+ * grayscale image, the 8 neighbours at radius 1 of a pixel are numbered
+ * clockwise from the top-left one:
+ *   0: (-1,-1)  1: (-1,0)  2: (-1,+1)  3: (0,+1)
+ *   4: (+1,+1)  5: (+1,0)  6: (+1,-1)  7: (0,-1)      (row, column offsets)
+ * The three artificial channels take neighbours 0, 3 and 6, a clockwise
+ * stride of 3 (the start point is not stated; top-left is the reading taken).
+ * A channel is +1 when its neighbour's gray value exceeds the centre's
+ * (strictly) and -1 otherwise; a neighbour outside the image never exceeds.
+ * x: [N, H, W, 3] RGB; out: [N, H, W, 3] +-1.
+ */
+void orc_lbp(const float* x, int32_t N, int32_t H, int32_t W, int8_t* out) {
+  static const int dr[3] = {-1, 0, 1};
+  static const int dc[3] = {-1, 1, -1};
+#pragma omp parallel for collapse(2) schedule(static)
+  for (int64_t n = 0; n < N; ++n) {
+    for (int64_t i = 0; i < H; ++i) {
+      for (int64_t j = 0; j < W; ++j) {
+        const float centre = gray_of(x + ((n * H + i) * W + j) * 3);
+        for (int ch = 0; ch < 3; ++ch) {
+          const int64_t ni = i + dr[ch], nj = j + dc[ch];
+          int8_t v = -1;
+          if (ni >= 0 && ni < H && nj >= 0 && nj < W) {
+            const float g = gray_of(x + ((n * H + ni) * W + nj) * 3);
+            if (g > centre) v = 1;
+          }
+          out[((n * H + i) * W + j) * 3 + ch] = v;
+        }
+      }
+    }
+  }
+}
+
 /* Number of OpenMP threads a parallel region of this library would use. */
 int orc_num_threads(void) {
   int n = 1;

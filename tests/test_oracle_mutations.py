@@ -43,6 +43,19 @@ MUTATIONS = {
     "fconv_pad_minus_one":
         ("if (hi < 0 || hi >= H || wi < 0 || wi >= W) continue; /* 0.0 */",
          "if (hi < 0 || hi >= H || wi < 0 || wi >= W) { for (int32_t c = 0; c < C; ++c) s -= (double)w[((f * KH + kh) * (int64_t)KW + kw) * C + c]; continue; }"),
+    "gray_red_blue_swapped":
+        ("const float r = 0.299f * px[0];", "const float r = 0.299f * px[2];"),
+    "gray_dropped_blue":
+        ("return rg + b;", "return rg + 0.0f * b;"),
+    "lbp_wrong_neighbour":
+        ("static const int dc[3] = {-1, 1, -1};", "static const int dc[3] = {-1, 1, 1};"),
+    "lbp_counterclockwise":
+        ("static const int dr[3] = {-1, 0, 1};\n  static const int dc[3] = {-1, 1, -1};",
+         "static const int dr[3] = {-1, 1, -1};\n  static const int dc[3] = {-1, 0, 1};"),
+    "lbp_ties_exceed":
+        ("if (g > centre) v = 1;", "if (g >= centre) v = 1;"),
+    "lbp_outside_exceeds":
+        ("          int8_t v = -1;\n          if (ni >= 0", "          int8_t v = 1;\n          if (ni >= 0"),
 }
 
 
@@ -55,7 +68,7 @@ def test_pins_catch_planted_mistake(name, tmp_path):
     mutated.write_text(src.replace(old, new))
     lib = tmp_path / "libmut.so"
     subprocess.check_call(["gcc", "-O1", "-fopenmp", "-fPIC", "-shared", "-std=c11",
-                           "-o", str(lib), str(mutated)])
+                           "-ffp-contract=off", "-o", str(lib), str(mutated)])
     env = dict(os.environ, BNN_ORACLE_LIB=str(lib), OMP_NUM_THREADS="2")
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         os.path.join(ROOT, "tests", "test_oracle_pins.py")],

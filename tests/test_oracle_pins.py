@@ -368,3 +368,92 @@ def test_forward_chain_matches_torch_composition():
     a = torch.where(bit, one, -one)
     ref = a @ torch.from_numpy(layers[4]["w"].astype(np.float64)).T
     assert np.array_equal(got, ref.numpy().astype(np.int32))
+
+
+# ------------------------------------------- grayscale and LBP binarization --
+# Sec. II-C / Table III: the grayscale-thresholded input (one channel) and the
+# LBP input (three channels from the grayscale image).  The grayscale weights
+# are the BT.601 luma (a reading; the paper gives none).
+
+def test_gray_threshold_each_weight_on_its_channel_and_sum_one():
+    """Pure red / green / blue pixels of value v against thresholds just off
+    0.299 v, 0.587 v, 0.114 v, and a gray pixel against v: every weight sits on
+    its own channel and the three add up to one."""
+    v = 200.0
+    for ch, wt in ((0, 0.299), (1, 0.587), (2, 0.114)):
+        px = np.zeros((1, 3), np.float32)
+        px[0, ch] = v
+        assert oracle.gray_threshold(px, -(wt * v) + 0.01)[0, 0] == 1
+        assert oracle.gray_threshold(px, -(wt * v) - 0.01)[0, 0] == -1
+    g = np.full((2, 3), v, np.float32)
+    assert (oracle.gray_threshold(g, -v + 0.01) == 1).all()
+    assert (oracle.gray_threshold(g, -v - 0.01) == -1).all()
+
+
+def test_gray_threshold_tie_is_minus_one_and_shape():
+    x = np.zeros((2, 4, 5, 3), np.float32)
+    out = oracle.gray_threshold(x, 0.0)
+    assert out.shape == (2, 4, 5, 1) and (out == -1).all()
+
+
+def test_lbp_constant_image_is_all_minus_one():
+    x = np.full((2, 5, 7, 3), 77.0, np.float32)
+    assert (oracle.lbp(x) == -1).all()
+
+
+@pytest.mark.parametrize("i,j", [(2, 3), (0, 0), (4, 6), (0, 6), (4, 0), (1, 5)])
+def test_lbp_single_bright_pixel_closed_form(i, j):
+    """One bright pixel at (i, j) of a dark 5x7 image: exactly the pixels that
+    see it as their selected neighbour become +1.  Neighbours are numbered
+    clockwise from the top-left; channels take numbers 0, 3, 6, i.e. offsets
+    (-1,-1), (0,+1), (+1,-1).  So channel 0 fires at (i+1, j+1), channel 1 at
+    (i, j-1) and channel 2 at (i-1, j+1), when inside the image."""
+    x = np.zeros((1, 5, 7, 3), np.float32)
+    x[0, i, j] = (10.0, 20.0, 30.0)
+    out = oracle.lbp(x)
+    expect = -np.ones_like(out)
+    for ch, (pi, pj) in enumerate([(i + 1, j + 1), (i, j - 1), (i - 1, j + 1)]):
+        if 0 <= pi < 5 and 0 <= pj < 7:
+            expect[0, pi, pj, ch] = 1
+    assert np.array_equal(out, expect)
+
+
+def test_lbp_single_dark_pixel_sees_every_neighbour_exceed():
+    """A dark pixel in a bright image: its own three channels are +1 wherever
+    the selected neighbour exists; no other pixel has a brighter neighbour."""
+    for (i, j) in [(2, 3), (0, 0), (4, 6)]:
+        x = np.full((1, 5, 7, 3), 50.0, np.float32)
+        x[0, i, j] = 0.0
+        out = oracle.lbp(x)
+        expect = -np.ones_like(out)
+        for ch, (di, dj) in enumerate([(-1, -1), (0, 1), (1, -1)]):
+            if 0 <= i + di < 5 and 0 <= j + dj < 7:
+                expect[0, i, j, ch] = 1
+        assert np.array_equal(out, expect)
+
+
+def test_lbp_invariant_to_gain_and_brightness():
+    """Comparisons of gray values survive x -> 4x (exact in fp32) and
+    x -> x + 16 (integer pixels: distinct gray values differ by >= 0.001)."""
+    rng = np.random.default_rng(5)
+    x = rng.integers(0, 240, size=(2, 9, 11, 3)).astype(np.float32)
+    ref = oracle.lbp(x)
+    assert np.array_equal(oracle.lbp(4.0 * x), ref)
+    assert np.array_equal(oracle.lbp(x + 16.0), ref)
+    assert (ref == 1).any() and (ref == -1).any()
+
+
+def test_lbp_matches_a_direct_loop_on_a_tiny_image():
+    """Brute force over a 3x4 image with float32 gray values computed by numpy
+    in the same order: every (pixel, channel) by explicit comparison."""
+    rng = np.random.default_rng(6)
+    x = rng.integers(0, 256, size=(1, 3, 4, 3)).astype(np.float32)
+    f = np.float32
+    g = (f(0.299) * x[..., 0] + f(0.587) * x[..., 1]) + f(0.114) * x[..., 2]
+    out = oracle.lbp(x)
+    for i in range(3):
+        for j in range(4):
+            for ch, (di, dj) in enumerate([(-1, -1), (0, 1), (1, -1)]):
+                ni, nj = i + di, j + dj
+                exceed = 0 <= ni < 3 and 0 <= nj < 4 and g[0, ni, nj] > g[0, i, j]
+                assert out[0, i, j, ch] == (1 if exceed else -1)
