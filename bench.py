@@ -62,6 +62,8 @@ def measured_traffic(workload, kernel):
                       + rec["write_kib"] * rec["write_scale"]) * 1024))
 
 
+INPUT_MODES = {"input_threshold": 0, "input_gray": 1, "input_lbp": 2}
+
 WORKLOADS = {
     "cifar_bnn_b64": dict(cfg=3, batch=64, H=32, W=32, C=3),
     "vehicle_bnn_b256": dict(cfg=4, batch=256, H=96, W=96, C=3),
@@ -79,6 +81,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target length of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-paper-net", action="store_true",
+                    help="skip the 5x5 vehicle classifier of Table II under each input binarization")
     ap.add_argument("--no-float-baseline", action="store_true",
                     help="skip the floating-point network timed on the same GPU")
     ap.add_argument("--copy-probe", action="store_true",
@@ -101,27 +105,29 @@ def layer_shapes(layers, H, W, C):
     """Per layer: (name, kind, geometry dict, bit-MACs per image)."""
     out = []
     h, w, c = H, W, C
-    fused = (len(layers) > 1 and layers[0]["kind"] == "input_threshold"
-             and layers[1]["kind"] == "bconv"
-             and layers[1]["KH"] * layers[1]["KW"] * layers[1]["C"] <= 32)
+    first = layers[0]["kind"] if layers else None
+    fused = (len(layers) > 1 and first in INPUT_MODES and layers[1]["kind"] == "bconv"
+             and layers[1]["C"] <= 32 and max(layers[1]["KH"], layers[1]["KW"]) <= 32
+             and layers[1]["KH"] * layers[1]["KW"] * layers[1]["C"] <= 128)
     for li, L in enumerate(layers):
         k = L["kind"]
-        if k == "input_threshold" and fused:
+        if k in INPUT_MODES and fused:
             continue  # runs inside the next layer's patch-packing kernel
         if k == "bconv" and li == 1 and fused:
             KH, KW, pad, F = L["KH"], L["KW"], L["pad"], L["F"]
             Ho, Wo = h + 2 * pad - KH + 1, w + 2 * pad - KW + 1
             pool = L.get("pool", 0)
-            name = "L0+L1 threshold+bconv %dx%dx%d->%d k%d%s (patch words)" % (
-                h, w, c, F, KH, " pool" if pool else "")
+            name = "L0+L1 %s+bconv %dx%dx%d->%d k%d%s (patch words)" % (
+                first.replace("input_", ""), h, w, L["C"], F, KH, " pool" if pool else "")
             out.append((name, "bconv_input",
-                        dict(H=h, W=w, C=c, F=F, KH=KH, KW=KW, pad=pad, pool=pool,
-                             offset_layer=0),
-                        Ho * Wo * F * KH * KW * c))
+                        dict(H=h, W=w, C=L["C"], F=F, KH=KH, KW=KW, pad=pad, pool=pool,
+                             mode=INPUT_MODES[first], cin=c, li=li),
+                        Ho * Wo * F * KH * KW * L["C"]))
             h, w, c = (Ho // 2, Wo // 2, F) if pool else (Ho, Wo, F)
             continue
-        if k == "input_threshold":
-            out.append(("L%d pack %dx%dx%d" % (li, h, w, c), k, dict(H=h, W=w, C=c, li=li), 0))
+        if k in INPUT_MODES:
+            out.append(("L%d %s %dx%dx%d" % (li, k, h, w, c), k, dict(H=h, W=w, C=c, li=li), 0))
+            c = 1 if k == "input_gray" else (3 if k == "input_lbp" else c)
         elif k in ("fconv", "bconv"):
             KH, KW, pad, F = L["KH"], L["KW"], L["pad"], L["F"]
             Ho, Wo = h + 2 * pad - KH + 1, w + 2 * pad - KW + 1
@@ -147,7 +153,8 @@ def algorithmic_bytes(kind, g, batch):
         Ho = g["H"] + 2 * g["pad"] - g["KH"] + 1
         Wo = g["W"] + 2 * g["pad"] - g["KW"] + 1
         Hp, Wp = (Ho // 2, Wo // 2) if g["pool"] else (Ho, Wo)
-        x = batch * g["H"] * g["W"] * (4 * wd(g["C"]) if kind == "bconv" else 4 * g["C"])
+        x = batch * g["H"] * g["W"] * (4 * wd(g["C"]) if kind == "bconv"
+                                       else 4 * g.get("cin", g["C"]))
         w = g["F"] * g["KH"] * g["KW"] * 4 * wd(g["C"])
         return x + w + 4 * g["F"] + 4 * wd(g["F"]) + batch * Hp * Wp * 4 * wd(g["F"])
     if kind in ("bfc", "bfc_logits"):
@@ -212,6 +219,52 @@ def float_baseline(layers, H, W, C, batch, dtype, steps, torch):
     return e0.elapsed_time(e1) / steps
 
 
+def paper_net_latency(bnn, torch, np, images, batch=256, steps=20):
+    """Table II's 5x5 vehicle classifier behind each input binarization of
+    Table III: the paper's batch-1 protocol (fresh images fed one at a time,
+    kernels-only time per image) and throughput at `batch`."""
+    from paper_1808_00209_amd import synth
+    from paper_1808_00209_amd.device import to_device, upload_network
+    out = {}
+    stream = torch.cuda.current_stream()
+    for mode in synth.PAPER_MODES:
+        layers = synth.paper_net(mode)
+        net = upload_network(layers, 96, 96, 3)
+        x1 = to_device(synth.paper_input(images))
+        xin, ws, lg = x1[:1].clone(), net.alloc_workspace(1), None
+        lg = torch.empty((1, 4), dtype=torch.int32, device="cuda")
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(images)]
+        for rep in range(2):
+            for i in range(images):
+                xin.copy_(x1[i:i + 1])
+                evs[i][0].record(stream)
+                bnn.bnn_forward(net, xin, ws, lg)
+                evs[i][1].record(stream)
+            torch.cuda.synchronize()
+        us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+        xb = to_device(synth.paper_input(batch))
+        wsb = net.alloc_workspace(batch)
+        lgb = torch.empty((batch, 4), dtype=torch.int32, device="cuda")
+        for _ in range(3):
+            bnn.bnn_forward(net, xb, wsb, lgb)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            bnn.bnn_forward(net, xb, wsb, lgb)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        out[mode] = {"batch1_mean_us": round(float(us.mean()), 2),
+                     "batch1_median_us": round(float(np.median(us)), 2),
+                     "batch%d_ms" % batch: round(ms, 4),
+                     "batch%d_images_per_s" % batch: round(batch / (ms * 1e-3), 1)}
+    out["net"] = ("input binarization, conv 32@5x5 + pool, conv 32@5x5 + pool, "
+                  "FC 18432-100-100-4 (Table II shapes), synthetic 96x96x3 pixels")
+    out["images"] = images
+    return out
+
+
 def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
     """Average kernel time (ms) of one layer's standalone call on random bits."""
     gen = torch.Generator(device="cuda").manual_seed(7)
@@ -221,17 +274,20 @@ def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
         out = torch.empty((batch, g["H"], g["W"], bnn.words(g["C"])), dtype=torch.int32,
                           device="cuda")
         fn = lambda: bnn.bnn_pack_bits(x, dev_layer.get("offset"), out=out)
+    elif kind in INPUT_MODES:
+        x = torch.randn((batch, g["H"], g["W"], g["C"]), device="cuda", generator=gen)
+        fn = lambda: bnn.bnn_binarize_input(INPUT_MODES[kind], x, dev_layer.get("offset"))
     elif kind == "bconv_input":
         desc = bnn.conv_desc(batch, g["H"], g["W"], g["C"], g["F"], g["KH"], g["KW"], 1,
                              g["pad"], g["pool"])
         Ho, Wo, Hp, Wp = bnn.bnn_conv_output_dims(desc)
         ob = torch.empty((batch, Hp, Wp, bnn.words(g["F"])), dtype=torch.int32, device="cuda")
-        x = torch.randint(0, 256, (batch, g["H"], g["W"], g["C"]), device="cuda",
+        x = torch.randint(0, 256, (batch, g["H"], g["W"], g["cin"]), device="cuda",
                           generator=gen).to(torch.float32)
         off = dev_layer[0].get("offset")
         wl = dev_layer[1]
-        fn = lambda: bnn.bnn_bconv2d_input(desc, x, off, wl["w"], wl["thr"], wl.get("flip"),
-                                           want_sums=False, out_bits=ob)
+        fn = lambda: bnn.bnn_bconv2d_input(desc, g["mode"], x, off, wl["w"], wl["thr"],
+                                           wl.get("flip"), want_sums=False, out_bits=ob)
     elif kind in ("fconv", "bconv"):
         desc = bnn.conv_desc(batch, g["H"], g["W"], g["C"], g["F"], g["KH"], g["KW"], 1,
                              g["pad"], g["pool"])
@@ -466,6 +522,8 @@ def main():
                          round(achieved_tops / VALU_PEAK_TOPS, 4) if kind != "fconv" else None,
                      "valu_xor_popcount_peak_TOPS": VALU_PEAK_TOPS},
     }
+    if not args.no_paper_net:
+        result["paper_net"] = paper_net_latency(bnn, torch, np, max(50, min(args.b1_images, 1000)))
     if not args.no_float_baseline:
         fb = {}
         for name, dt in (("fp32", torch.float32), ("bf16", torch.bfloat16)):

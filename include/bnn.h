@@ -58,7 +58,7 @@
 extern "C" {
 #endif
 
-#define BNN_ABI_VERSION 1
+#define BNN_ABI_VERSION 2
 
 typedef enum bnn_status {
   BNN_OK = 0,
@@ -149,26 +149,64 @@ bnn_status bnn_fconv2d_binw(const bnn_conv_desc* d, const float* in,
                             uint32_t* out_bits, hipStream_t stream);
 
 /*
- * Binary convolution over a real-valued image binarized on the fly: the
- * input thresholding of Sec. II-C, bit = (x + offset[c]) > 0 in fp32, then
- * Eq. 3 / Eq. 4 with pad value -1 and the bnn_bconv2d epilogue.  The result
- * equals bnn_pack_bits(x, offset) followed by bnn_bconv2d, bit for bit.
- * Each output pixel's whole binarized window is packed into one word (the
- * patch packing of Algorithm 1 with B = KH*KW*C bits), so every dot product
- * is a single XOR + popcount; this needs KH*KW*C <= 32 (e.g. a 3x3 conv over
- * 3 colour channels, 27 bits).
- *   x         [N][H][W][C] fp32 image.
- *   offset    [C] fp32 per-channel offsets T_c, or NULL for all-zero.
- *   w         [F][KH][KW][Cw] u32 packed weights (Cw = 1 here).
- *   thr, flip, out_sums, out_bits: as for bnn_bconv2d.
- * Alignment as for bnn_bconv2d.  Errors: as for bnn_bconv2d, and
- * BNN_ERR_UNSUPPORTED when KH*KW*C > 32.
+ * Input binarizations of an fp32 NHWC image (Sec. II-C; Table III), each
+ * giving C <= 32 bits per pixel:
+ *   BNN_INPUT_THRESHOLD  C = Cin channels, bit = (x[c] + offset[c]) > 0
+ *                        (RGB thresholding; offset NULL means 0).
+ *   BNN_INPUT_GRAY       C = 1, bit = (gray + offset[0]) > 0 (grayscale
+ *                        thresholding; offset NULL means 0).  Cin = 3.
+ *   BNN_INPUT_LBP        C = 3 local-binary-pattern channels: on the gray
+ *                        image, the 8 neighbours at radius 1 are numbered
+ *                        clockwise from the top-left and channels 0, 1, 2
+ *                        take neighbours 0, 3, 6, i.e. offsets (-1,-1),
+ *                        (0,+1), (+1,-1); a bit is 1 when that neighbour's
+ *                        gray value exceeds the centre's, and 0 for a
+ *                        neighbour outside the image.  Cin = 3.
+ * gray = (0.299 R + 0.587 G) + 0.114 B in fp32, each product rounded on its
+ * own (the BT.601 luma; the paper names no conversion).  All comparisons
+ * are in fp32.
  */
-bnn_status bnn_bconv2d_input(const bnn_conv_desc* d, const float* x,
-                             const float* offset, const uint32_t* w,
-                             const int32_t* thr, const uint32_t* flip,
-                             int32_t* out_sums, uint32_t* out_bits,
-                             hipStream_t stream);
+typedef enum bnn_input_mode {
+  BNN_INPUT_THRESHOLD = 0,
+  BNN_INPUT_GRAY = 1,
+  BNN_INPUT_LBP = 2
+} bnn_input_mode;
+
+/*
+ * Binarize an image: out[n][i][j] is the pixel's C-bit code, channel 0 at
+ * bit 31 (Eq. 2 packing of the C channels, tail bits 0).
+ *   x    [N][H][W][Cin] fp32.  offset as above.
+ *   out  [N][H][W] u32 (one word per pixel).
+ * mode THRESHOLD needs Cin <= 32 (bnn_pack_bits covers any Cin); GRAY and
+ * LBP need Cin == 3.  x and out 16-byte aligned.  Errors: BNN_ERR_NULL,
+ * BNN_ERR_SHAPE, BNN_ERR_ALIGN, BNN_ERR_HIP.
+ */
+bnn_status bnn_binarize_input(int32_t mode, const float* x, const float* offset,
+                              int32_t N, int32_t H, int32_t W, int32_t Cin,
+                              uint32_t* out, hipStream_t stream);
+
+/*
+ * Binary convolution over an image binarized on the fly by `mode`, with pad
+ * value -1 and the bnn_bconv2d epilogue.  The result equals
+ * bnn_binarize_input (or bnn_pack_bits) followed by bnn_bconv2d, bit for bit.
+ * Each output pixel's whole binarized window is packed into
+ * P = KH*KW*C bits (the patch packing of Algorithm 1 with B = P), in
+ * ceil(P / 32) words, so every dot product takes ceil(P / 32) XOR + popcounts
+ * (one for a 3x3 conv over 3 channels, P = 27).
+ *   d         the conv; d->C is the binarized channel count (Cin for
+ *             THRESHOLD, 1 for GRAY, 3 for LBP).
+ *   x         [N][H][W][Cin] fp32 image (Cin = 3 for GRAY and LBP).
+ *   offset    as for bnn_binarize_input.
+ *   w         [F][KH][KW][1] u32 packed weights.
+ *   thr, flip, out_sums, out_bits: as for bnn_bconv2d.
+ * Needs C <= 32, KH <= 32, KW <= 32 and P <= 128 (else
+ * BNN_ERR_UNSUPPORTED).  Alignment and other errors as for bnn_bconv2d.
+ */
+bnn_status bnn_bconv2d_input(const bnn_conv_desc* d, int32_t mode,
+                             const float* x, const float* offset,
+                             const uint32_t* w, const int32_t* thr,
+                             const uint32_t* flip, int32_t* out_sums,
+                             uint32_t* out_bits, hipStream_t stream);
 
 /*
  * Binary fully-connected layer / GEMM (Sec. III-B, Eq. 4):
@@ -191,28 +229,32 @@ typedef enum bnn_layer_kind {
   BNN_LAYER_FCONV_BINW = 2,      /* bnn_fconv2d_binw (fp32 input)           */
   BNN_LAYER_BCONV = 3,           /* bnn_bconv2d, bits out                   */
   BNN_LAYER_BFC = 4,             /* bnn_bgemm, bits out                     */
-  BNN_LAYER_BFC_LOGITS = 5       /* bnn_bgemm, int32 sums out (last layer)  */
+  BNN_LAYER_BFC_LOGITS = 5,      /* bnn_bgemm, int32 sums out (last layer)  */
+  BNN_LAYER_INPUT_GRAY = 6,      /* bnn_binarize_input, BNN_INPUT_GRAY      */
+  BNN_LAYER_INPUT_LBP = 7        /* bnn_binarize_input, BNN_INPUT_LBP       */
 } bnn_layer_kind;
 
 /* One layer of a chain.  Fields a kind does not use are ignored.  Device
  * pointers: w, thr, flip, offset. */
 typedef struct bnn_layer {
   int32_t kind;              /* bnn_layer_kind                               */
-  int32_t C;                 /* conv / input threshold: input channels       */
+  int32_t C;                 /* conv / input layers: input channels          */
   int32_t F, KH, KW;         /* conv: filters, kernel size                   */
   int32_t stride, pad, pool; /* conv: as in bnn_conv_desc                    */
   int32_t K, N;              /* FC: input bits, outputs                      */
   const uint32_t* w;         /* conv [F][KH][KW][Cw]; FC [N][ceil(K/32)]     */
   const int32_t* thr;        /* [F] or [N]                                   */
   const uint32_t* flip;      /* packed flip bits or NULL                     */
-  const float* offset;       /* INPUT_THRESHOLD: [C] offsets T, or NULL      */
+  const float* offset;       /* INPUT_THRESHOLD: [C] offsets T; INPUT_GRAY:  */
+                             /* [1] offset T; or NULL                        */
 } bnn_layer;
 
 /*
  * Workspace bytes bnn_forward needs for `batch` images of H x W x C fp32
  * (two ping-pong buffers of packed activations, 256-byte aligned).  Also
- * validates the chain: the first layer is INPUT_THRESHOLD or FCONV_BINW, the
- * last is BFC_LOGITS, shapes agree from layer to layer, and an FC layer that
+ * validates the chain: the first layer is an input layer (INPUT_THRESHOLD,
+ * INPUT_GRAY, INPUT_LBP) or FCONV_BINW, the last is BFC_LOGITS, shapes agree
+ * from layer to layer, and an FC layer that
  * follows a conv reads its NHWC bits flattened in (h, w, c) order, which needs
  * the channel count to be a multiple of 32 (or a 1x1 map).
  */
@@ -224,7 +266,8 @@ bnn_status bnn_forward_workspace_size(const bnn_layer* layers,
 /*
  * Run the chain on input [batch][H][W][C] fp32 and write int32 logits
  * [batch][N_last] (Table I/II: conv, pool, ..., FC layers).  One kernel per
- * layer on `stream`; workspace (device, >= the size above, 256-byte aligned)
+ * layer on `stream`, except that an input layer followed by a BCONV whose
+ * window fits bnn_bconv2d_input runs as that one kernel; workspace (device, >= the size above, 256-byte aligned)
  * holds the intermediate bits.  Errors: as the per-layer calls, plus
  * BNN_ERR_WORKSPACE.
  */

@@ -25,10 +25,16 @@ LAYER_FCONV_BINW = 2
 LAYER_BCONV = 3
 LAYER_BFC = 4
 LAYER_BFC_LOGITS = 5
+LAYER_INPUT_GRAY = 6
+LAYER_INPUT_LBP = 7
+INPUT_THRESHOLD = 0
+INPUT_GRAY = 1
+INPUT_LBP = 2
 
 # Every symbol include/bnn.h declares.
 EXPORTED = ["bnn_last_error", "bnn_abi_version", "bnn_pack_bits", "bnn_conv_output_dims",
-            "bnn_bconv2d", "bnn_fconv2d_binw", "bnn_bconv2d_input", "bnn_bgemm",
+            "bnn_bconv2d", "bnn_fconv2d_binw", "bnn_binarize_input", "bnn_bconv2d_input",
+            "bnn_bgemm",
             "bnn_forward_workspace_size", "bnn_forward"]
 
 
@@ -73,6 +79,8 @@ def load(path: str = LIB_PATH):
     lib.bnn_bconv2d.argtypes = [ctypes.POINTER(ConvDesc), P, P, P, P, P, P, P]
     lib.bnn_fconv2d_binw.argtypes = [ctypes.POINTER(ConvDesc), P, P, P, P, P, P, P]
     lib.bnn_bgemm.argtypes = [i64, i64, i64, P, P, P, P, P, P, P]
+    lib.bnn_binarize_input.argtypes = [i32, P, P, i32, i32, i32, i32, P, P]
+    lib.bnn_bconv2d_input.argtypes = [ctypes.POINTER(ConvDesc), i32, P, P, P, P, P, P, P, P]
     lib.bnn_forward_workspace_size.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32,
                                                ctypes.POINTER(ctypes.c_size_t)]
     lib.bnn_forward.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32, P, P,
@@ -188,11 +196,26 @@ def bnn_fconv2d_binw(desc: ConvDesc, x, w, thr=None, flip=None, want_sums=True,
     return out_sums, out_bits
 
 
-def bnn_bconv2d_input(desc: ConvDesc, x, offset, w, thr=None, flip=None, want_sums=True,
+def bnn_binarize_input(mode, x, offset=None, out=None, stream=None):
+    """Input binarization (Sec. II-C): mode INPUT_THRESHOLD / INPUT_GRAY /
+    INPUT_LBP on x [N,H,W,Cin] fp32 -> one code word per pixel [N,H,W,1]."""
+    lib = load()
+    _dev(x, torch.float32, "x")
+    offset = _dev(offset, torch.float32, "offset")
+    N, H, W, Cin = x.shape
+    if out is None:
+        out = torch.empty((N, H, W, 1), dtype=torch.int32, device=x.device)
+    _check(lib.bnn_binarize_input(int(mode), _ptr(x), _ptr(offset), N, H, W, Cin, _ptr(out),
+                                  _stream(stream)))
+    return out
+
+
+def bnn_bconv2d_input(desc: ConvDesc, mode, x, offset, w, thr=None, flip=None, want_sums=True,
                       want_bits=True, out_sums=None, out_bits=None, stream=None):
-    """Binary conv over an fp32 image thresholded on the fly, bit = x + offset > 0
-    (Sec. II-C), one packed patch word per window (Algorithm 1, KH*KW*C <= 32).
-    Same outputs as bnn_pack_bits followed by bnn_bconv2d."""
+    """Binary conv over an fp32 image binarized on the fly by ``mode`` (Sec. II-C),
+    each window packed into ceil(KH*KW*C / 32) words (Algorithm 1's patch
+    packing).  desc.C is the binarized channel count.  Same outputs as
+    bnn_binarize_input / bnn_pack_bits followed by bnn_bconv2d."""
     lib = load()
     Ho, Wo, Hp, Wp = bnn_conv_output_dims(desc)
     _dev(x, torch.float32, "x")
@@ -205,8 +228,9 @@ def bnn_bconv2d_input(desc: ConvDesc, x, offset, w, thr=None, flip=None, want_su
     if want_bits and out_bits is None:
         out_bits = torch.empty((desc.N, Hp, Wp, words(desc.F)), dtype=torch.int32,
                                device=x.device)
-    _check(lib.bnn_bconv2d_input(ctypes.byref(desc), _ptr(x), _ptr(offset), _ptr(w), _ptr(thr),
-                                 _ptr(flip), _ptr(out_sums), _ptr(out_bits), _stream(stream)))
+    _check(lib.bnn_bconv2d_input(ctypes.byref(desc), int(mode), _ptr(x), _ptr(offset), _ptr(w),
+                                 _ptr(thr), _ptr(flip), _ptr(out_sums), _ptr(out_bits),
+                                 _stream(stream)))
     return out_sums, out_bits
 
 
@@ -281,5 +305,6 @@ pack_bits = bnn_pack_bits
 bconv2d = bnn_bconv2d
 fconv2d_binw = bnn_fconv2d_binw
 bconv2d_input = bnn_bconv2d_input
+binarize_input = bnn_binarize_input
 bgemm = bnn_bgemm
 forward = bnn_forward

@@ -227,24 +227,57 @@ bnn_status bnn_fconv2d_binw(const bnn_conv_desc* d, const float* in, const uint3
   }
 }
 
-bnn_status bnn_bconv2d_input(const bnn_conv_desc* d, const float* x, const float* offset,
-                             const uint32_t* w, const int32_t* thr, const uint32_t* flip,
-                             int32_t* out_sums, uint32_t* out_bits, hipStream_t stream) {
+bnn_status bnn_binarize_input(int32_t mode, const float* x, const float* offset, int32_t N,
+                              int32_t H, int32_t W, int32_t Cin, uint32_t* out,
+                              hipStream_t stream) {
+  try {
+    if (mode != BNN_INPUT_THRESHOLD && mode != BNN_INPUT_GRAY && mode != BNN_INPUT_LBP)
+      return fail(BNN_ERR_SHAPE, "binarize_input: unknown mode %d", mode);
+    if (N < 1 || H < 1 || W < 1 || Cin < 1)
+      return fail(BNN_ERR_SHAPE, "binarize_input: N, H, W, Cin must be >= 1");
+    if (mode == BNN_INPUT_THRESHOLD && Cin > 32)
+      return fail(BNN_ERR_SHAPE, "binarize_input: thresholding takes Cin <= 32 (got %d); "
+                  "bnn_pack_bits packs any channel count", Cin);
+    if (mode != BNN_INPUT_THRESHOLD && Cin != 3)
+      return fail(BNN_ERR_SHAPE, "binarize_input: gray and LBP need Cin == 3 (got %d)", Cin);
+    if (int64_t{N} * H * W * Cin > kMaxItems)
+      return fail(BNN_ERR_SHAPE, "binarize_input: image too large for 32-bit indexing");
+    if (!x || !out) return fail(BNN_ERR_NULL, "binarize_input: x and out must be non-NULL");
+    if (!aligned16(x) || !aligned16(out))
+      return fail(BNN_ERR_ALIGN, "binarize_input: x and out must be 16-byte aligned");
+    return hip_status(bnn::launch_binarize(mode, x, offset, N, H, W, Cin, out, stream),
+                      "binarize_input launch");
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "binarize_input: unexpected C++ exception");
+  }
+}
+
+bnn_status bnn_bconv2d_input(const bnn_conv_desc* d, int32_t mode, const float* x,
+                             const float* offset, const uint32_t* w, const int32_t* thr,
+                             const uint32_t* flip, int32_t* out_sums, uint32_t* out_bits,
+                             hipStream_t stream) {
   try {
     bnn::ConvGeom g;
     bnn_status st = conv_geom(d, &g);
     if (st != BNN_OK) return st;
+    if (mode != BNN_INPUT_THRESHOLD && mode != BNN_INPUT_GRAY && mode != BNN_INPUT_LBP)
+      return fail(BNN_ERR_SHAPE, "bconv2d_input: unknown mode %d", mode);
+    if (mode != BNN_INPUT_THRESHOLD && g.C != bnn::input_channels_of(mode, 3))
+      return fail(BNN_ERR_SHAPE, "bconv2d_input: mode %d gives %d channels, desc has C=%d",
+                  mode, bnn::input_channels_of(mode, 3), g.C);
     if (!bnn::bconv_patch_supported(g))
       return fail(BNN_ERR_UNSUPPORTED,
-                  "bconv2d_input: a window of KH*KW*C = %lld bits does not fit one word (max 32)",
-                  (long long)(int64_t{g.KH} * g.KW * g.C));
-    if (int64_t{g.N} * g.H * g.W * g.C > kMaxItems)
+                  "bconv2d_input: a %dx%d window of %d channels (%lld bits) is beyond the "
+                  "supported C, KH, KW <= 32 and 128 bits",
+                  g.KH, g.KW, g.C, (long long)(int64_t{g.KH} * g.KW * g.C));
+    const int64_t cin = mode == BNN_INPUT_THRESHOLD ? g.C : 3;
+    if (int64_t{g.N} * g.H * g.W * cin > kMaxItems)
       return fail(BNN_ERR_SHAPE, "bconv2d_input: image too large for 32-bit indexing");
     st = check_outputs(x, w, thr, out_sums, out_bits);
     if (st != BNN_OK) return st;
-    return hip_status(
-        bnn::launch_bconv_patch(g, x, offset, w, thr, flip, out_sums, out_bits, stream),
-        "bconv2d_input launch");
+    return hip_status(bnn::launch_bconv_patch(g, mode, x, offset, w, thr, flip, out_sums,
+                                              out_bits, stream),
+                      "bconv2d_input launch");
   } catch (...) {
     return fail(BNN_ERR_HIP, "bconv2d_input: unexpected C++ exception");
   }
@@ -275,6 +308,15 @@ struct Act {
   int64_t H, W, C;  // C in channels (bits); FC outputs are 1 x 1 x N
 };
 
+bool is_input_kind(int32_t k) {
+  return k == BNN_LAYER_INPUT_THRESHOLD || k == BNN_LAYER_INPUT_GRAY || k == BNN_LAYER_INPUT_LBP;
+}
+
+int input_mode(int32_t kind) {
+  return kind == BNN_LAYER_INPUT_GRAY ? BNN_INPUT_GRAY
+         : kind == BNN_LAYER_INPUT_LBP ? BNN_INPUT_LBP : BNN_INPUT_THRESHOLD;
+}
+
 // Walks the chain, validating shapes; returns the largest activation size in
 // bytes (packed words) through *max_bytes.
 bnn_status plan_chain(const bnn_layer* L, int32_t n, int32_t batch, int32_t H,
@@ -283,8 +325,10 @@ bnn_status plan_chain(const bnn_layer* L, int32_t n, int32_t batch, int32_t H,
   if (n < 1) return fail(BNN_ERR_SHAPE, "forward: need at least one layer");
   if (batch < 1 || H < 1 || W < 1 || C < 1)
     return fail(BNN_ERR_SHAPE, "forward: batch, H, W, C must be >= 1");
-  if (L[0].kind != BNN_LAYER_INPUT_THRESHOLD && L[0].kind != BNN_LAYER_FCONV_BINW)
-    return fail(BNN_ERR_SHAPE, "forward: layer 0 must be INPUT_THRESHOLD or FCONV_BINW");
+  if (!is_input_kind(L[0].kind) && L[0].kind != BNN_LAYER_FCONV_BINW)
+    return fail(BNN_ERR_SHAPE,
+                "forward: layer 0 must be an input layer (INPUT_THRESHOLD, INPUT_GRAY, "
+                "INPUT_LBP) or FCONV_BINW");
   if (L[n - 1].kind != BNN_LAYER_BFC_LOGITS)
     return fail(BNN_ERR_SHAPE, "forward: the last layer must be BFC_LOGITS");
   Act a{H, W, C};
@@ -292,9 +336,14 @@ bnn_status plan_chain(const bnn_layer* L, int32_t n, int32_t batch, int32_t H,
   for (int32_t li = 0; li < n; ++li) {
     const bnn_layer& l = L[li];
     switch (l.kind) {
-      case BNN_LAYER_INPUT_THRESHOLD: {
-        if (li != 0) return fail(BNN_ERR_SHAPE, "forward: layer %d: INPUT_THRESHOLD must be first", li);
+      case BNN_LAYER_INPUT_THRESHOLD:
+      case BNN_LAYER_INPUT_GRAY:
+      case BNN_LAYER_INPUT_LBP: {
+        if (li != 0) return fail(BNN_ERR_SHAPE, "forward: layer %d: an input layer must be first", li);
         if (l.C != C) return fail(BNN_ERR_SHAPE, "forward: layer 0 C=%d but input has C=%d", l.C, C);
+        if (l.kind != BNN_LAYER_INPUT_THRESHOLD && C != 3)
+          return fail(BNN_ERR_SHAPE, "forward: gray and LBP inputs need C == 3 (got %d)", C);
+        a = Act{H, W, bnn::input_channels_of(input_mode(l.kind), C)};
         break;
       }
       case BNN_LAYER_FCONV_BINW:
@@ -389,8 +438,8 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
     // as one patch-packing kernel on the fp32 image (BNN_PATCH=0 keeps the
     // two separate steps).
     bool fuse_input = false;
-    if (n_layers > 1 && layers[0].kind == BNN_LAYER_INPUT_THRESHOLD &&
-        layers[1].kind == BNN_LAYER_BCONV) {
+    const int mode = input_mode(layers[0].kind);
+    if (n_layers > 1 && is_input_kind(layers[0].kind) && layers[1].kind == BNN_LAYER_BCONV) {
       const char* e = getenv("BNN_PATCH");
       bnn::ConvGeom g1;
       g1.KH = layers[1].KH;
@@ -407,8 +456,17 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
       hipError_t e = hipSuccess;
       switch (l.kind) {
         case BNN_LAYER_INPUT_THRESHOLD:
-          if (!fuse_input)
-            e = bnn::launch_pack_bits(input, l.offset, int64_t{batch} * h * w, c, dst, stream);
+        case BNN_LAYER_INPUT_GRAY:
+        case BNN_LAYER_INPUT_LBP:
+          if (!fuse_input) {
+            if (l.kind == BNN_LAYER_INPUT_THRESHOLD)
+              e = bnn::launch_pack_bits(input, l.offset, int64_t{batch} * h * w, c, dst, stream);
+            else
+              e = bnn::launch_binarize(mode, input, l.offset, batch, static_cast<int32_t>(h),
+                                       static_cast<int32_t>(w), static_cast<int32_t>(c), dst,
+                                       stream);
+          }
+          c = bnn::input_channels_of(mode, static_cast<int>(c));
           break;
         case BNN_LAYER_FCONV_BINW:
         case BNN_LAYER_BCONV: {
@@ -419,8 +477,8 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
           if (l.kind == BNN_LAYER_FCONV_BINW)
             e = bnn::launch_fconv_binw(g, input, l.w, l.thr, l.flip, nullptr, dst, stream);
           else if (li == 1 && fuse_input)
-            e = bnn::launch_bconv_patch(g, input, layers[0].offset, l.w, l.thr, l.flip, nullptr,
-                                        dst, stream);
+            e = bnn::launch_bconv_patch(g, mode, input, layers[0].offset, l.w, l.thr, l.flip,
+                                        nullptr, dst, stream);
           else
             e = launch_conv(g, src, l.w, l.thr, l.flip, nullptr, dst, stream);
           h = g.Hp;

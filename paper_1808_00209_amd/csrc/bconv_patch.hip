@@ -1,54 +1,137 @@
-// First binary conv over a real-valued image that is binarized on the fly.
+// Input binarization (Sec. II-C) and the first binary conv over a
+// real-valued image binarized on the fly.
 //
-// The image is thresholded per channel, bit = (x + T_c) > 0 (the input
-// binarization of §II-C), and convolved with packed +-1 filters, pad -1.
-// When a whole window of KH x KW x C values fits in one 32-bit word
-// (KH*KW*C <= 32; the 3x3x3 RGB layer has 27), the window itself is packed:
-// this is the paper's patch packing (Algorithm 1) with B = KH*KW*C bits per
-// word instead of one word per tap.  Each dot product of Eq. 4 is then a
-// single XOR + popcount, against KH*KW of them (one per tap, 3 valid bits
-// each) in the channel-packed layout.
+// Three binarizations of an fp32 NHWC image, each giving C <= 32 bits per
+// pixel (channel 0 in the highest bit of the pixel's code):
+//   THRESHOLD  C channels, bit = (x + T_c) > 0                (RGB thresholding)
+//   GRAY       1 channel,  bit = (gray + T_0) > 0             (grayscale thresholding)
+//   LBP        3 channels from the grayscale image: neighbours at radius 1
+//              numbered clockwise from the top-left, channels = neighbours
+//              0, 3, 6 (offsets (-1,-1), (0,+1), (+1,-1)), bit = neighbour's
+//              gray > centre's, neighbours outside the image never exceed.
+// gray = (0.299 R + 0.587 G) + 0.114 B in fp32 with each product rounded (the
+// BT.601 luma; the paper names no conversion).
+//
+// The conv packs each output pixel's whole binarized window into P = KH*KW*C
+// bits (the patch packing of Algorithm 1 with B = P bits instead of one word
+// per tap), in PW = ceil(P / 32) <= 4 words, so a dot product of Eq. 4 is PW
+// XOR + popcounts (one for the 3x3 RGB layer, P = 27) instead of one per tap.
 //
 // A block covers an 8 x 32 tile of output pixels, one per thread.  Its
-// threads first threshold the input tile plus halo into C-bit codes in LDS
-// (taps outside the image stay 0, the -1 pad value), then each builds its
-// pixel's patch word from LDS.  The filters are turned into patch words the
-// same way, once per block, together with a per-filter bias b = -q - 1 where
-// q = floor((K - thr) / 2): then S >= thr <=> popcount(a ^ w) <= q <=>
-// popcount(a ^ w) + b < 0, so v_bcnt with accumulate yields the output bit
-// in its sign, and v_alignbit shifts it into the output word: three vector
-// instructions per (pixel, filter).  2x2 OR-pooling uses quad shuffles as in
-// the other binary kernels.
+// threads first binarize the input tile plus halo into codes in LDS (taps
+// outside the image stay 0, the -1 pad value), then each builds its pixel's
+// patch words from LDS.  The filters are turned into patch words the same
+// way, once per block, together with a per-filter bias b = -q - 1 where
+// q = floor((K - thr) / 2): S >= thr <=> popcount(a ^ w) <= q <=>
+// popcount(a ^ w) + b < 0, so v_bcnt with accumulate leaves the output bit in
+// the sign, and v_alignbit shifts it into the output word.  2x2 OR-pooling
+// uses quad shuffles as in the other binary kernels.
+#include "bnn.h"
 #include "kernels.hpp"
 
 namespace bnn {
 namespace {
 
-constexpr int kTH = 8, kTW = 32;  // output tile rows x columns (256 threads)
-constexpr int kFB = 256;          // filters staged in LDS per round
-constexpr int kMaxTile = (kTH + 31) * (kTW + 31);  // KH * KW <= 32
+constexpr int kTH = 8, kTW = 32;                   // output tile (256 threads)
+constexpr int kFB = 256;                           // filters staged per round
+constexpr int kMaxTile = (kTH + 31) * (kTW + 31);  // KH, KW <= 32
 
-struct PatchArgs {
+struct BinArgs {
   const float* x;
   const float* offset;
+  int32_t mode, N, H, W, Cin, C;
+};
+
+__device__ __forceinline__ float gray_of(const float* px) {
+  const float r = 0.299f * px[0];
+  const float g = 0.587f * px[1];
+  const float b = 0.114f * px[2];
+  const float rg = r + g;
+  return rg + b;
+}
+
+// Binarized code of input pixel (n, i, j), which must lie inside the image.
+__device__ uint32_t pixel_code(const BinArgs& a, int n, int i, int j) {
+  const float* px = a.x + ((static_cast<size_t>(n) * a.H + i) * a.W + j) * a.Cin;
+  if (a.mode == BNN_INPUT_THRESHOLD) {
+    uint32_t code = 0;
+    for (int c = 0; c < a.Cin; ++c) {
+      const float v = px[c] + (a.offset ? a.offset[c] : 0.0f);
+      code |= static_cast<uint32_t>(v > 0.0f) << (a.Cin - 1 - c);
+    }
+    return code;
+  }
+  const float g = gray_of(px);
+  if (a.mode == BNN_INPUT_GRAY) return (g + (a.offset ? a.offset[0] : 0.0f)) > 0.0f ? 1u : 0u;
+  // LBP: channel ch compares neighbour (i + dr, j + dc) with the centre.
+  uint32_t code = 0;
+#pragma unroll
+  for (int ch = 0; ch < 3; ++ch) {
+    const int ni = i + (ch == 0 ? -1 : ch == 1 ? 0 : 1);
+    const int nj = j + (ch == 1 ? 1 : -1);
+    uint32_t bit = 0;
+    if (ni >= 0 && ni < a.H && nj >= 0 && nj < a.W) {
+      const float* pn = a.x + ((static_cast<size_t>(n) * a.H + ni) * a.W + nj) * a.Cin;
+      bit = gray_of(pn) > g ? 1u : 0u;
+    }
+    code |= bit << (2 - ch);
+  }
+  return code;
+}
+
+// One thread per pixel: the code, MSB-aligned, as the pixel's packed word.
+__global__ __launch_bounds__(256) void binarize_kernel(BinArgs a, uint32_t* out) {
+  const int64_t p = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t total = static_cast<int64_t>(a.N) * a.H * a.W;
+  if (p >= total) return;
+  const int j = static_cast<int>(p % a.W);
+  const int64_t t = p / a.W;
+  const int i = static_cast<int>(t % a.H);
+  const int n = static_cast<int>(t / a.H);
+  out[p] = pixel_code(a, n, i, j) << (32 - a.C);
+}
+
+struct PatchArgs {
+  BinArgs in;
   const uint32_t* w;
   const int32_t* thr;
   const uint32_t* flip;
   int32_t* sums;
   uint32_t* bits;
-  int32_t N, H, W, C, F, Fw, KH, KW, pad, Ho, Wo;
-  int32_t P;           // KH * KW * C, bits per patch word
-  int32_t tiles_x;     // tiles per output row
-  int32_t tiles_y;     // tiles per output column
+  int32_t F, Fw, KH, KW, pad, Ho, Wo;
+  int32_t P;        // KH * KW * C, bits per window
+  int32_t tiles_x;  // tiles per output row
+  int32_t tiles_y;  // tiles per output column
 };
 
-template <bool POOL, bool SUMS, bool BITS>
+// ORs a code of C bits into a 128-bit big-endian patch (element 0 = bit 127)
+// at elements e0 .. e0 + C - 1.
+__device__ __forceinline__ void put_bits(uint64_t& hi, uint64_t& lo, uint32_t code, int e0, int C) {
+  const int shift = 128 - e0 - C;
+  if (shift >= 64) {
+    hi |= static_cast<uint64_t>(code) << (shift - 64);
+  } else {
+    lo |= static_cast<uint64_t>(code) << shift;
+    if (shift + C > 64) hi |= static_cast<uint64_t>(code) >> (64 - shift);
+  }
+}
+
+template <int PW>
+__device__ __forceinline__ void split_words(uint32_t (&pw)[PW], uint64_t hi, uint64_t lo) {
+  const uint32_t all[4] = {static_cast<uint32_t>(hi >> 32), static_cast<uint32_t>(hi),
+                           static_cast<uint32_t>(lo >> 32), static_cast<uint32_t>(lo)};
+#pragma unroll
+  for (int q = 0; q < PW; ++q) pw[q] = all[q];
+}
+
+template <int PW, bool POOL, bool SUMS, bool BITS>
 __global__ __launch_bounds__(256) void bconv_patch_kernel(PatchArgs a) {
   __shared__ uint32_t tile[kMaxTile];
-  __shared__ uint32_t wpat[kFB];
+  __shared__ uint32_t wpat[kFB * PW];
   __shared__ int32_t wbias[kFB];
 
   const int t = threadIdx.x;
+  const int C = a.in.C;
   int b = blockIdx.x;
   const int bx = b % a.tiles_x;
   b /= a.tiles_x;
@@ -56,21 +139,13 @@ __global__ __launch_bounds__(256) void bconv_patch_kernel(PatchArgs a) {
   const int n = b / a.tiles_y;
   const int i0 = by * kTH, j0 = bx * kTW;
 
-  // Threshold the input tile (plus halo) into C-bit codes, channel 0 in the
-  // code's highest bit.
+  // Binarize the input tile plus halo.
   const int TR = kTH + a.KH - 1, TC = kTW + a.KW - 1;
   for (int e = t; e < TR * TC; e += 256) {
     const int r = e / TC, cc = e - r * TC;
     const int gi = i0 - a.pad + r, gj = j0 - a.pad + cc;
-    uint32_t code = 0;
-    if (gi >= 0 && gi < a.H && gj >= 0 && gj < a.W) {
-      const float* px = a.x + ((static_cast<size_t>(n) * a.H + gi) * a.W + gj) * a.C;
-      for (int c = 0; c < a.C; ++c) {
-        const float v = px[c] + (a.offset ? a.offset[c] : 0.0f);
-        code |= static_cast<uint32_t>(v > 0.0f) << (a.C - 1 - c);
-      }
-    }
-    tile[e] = code;
+    tile[e] = (gi >= 0 && gi < a.in.H && gj >= 0 && gj < a.in.W) ? pixel_code(a.in, n, gi, gj)
+                                                                 : 0u;
   }
 
   // This thread's output pixel; with pooling, lanes 4q..4q+3 are one window.
@@ -87,27 +162,47 @@ __global__ __launch_bounds__(256) void bconv_patch_kernel(PatchArgs a) {
   const bool valid = i < a.Ho && j < a.Wo;
   __syncthreads();
 
-  // Patch word: tap s = kh * KW + kw holds bits 31 - s*C ... 32 - (s+1)*C.
-  uint32_t patch = 0;
-  for (int kh = 0; kh < a.KH; ++kh)
-    for (int kw = 0; kw < a.KW; ++kw) {
-      const int s = kh * a.KW + kw;
-      patch |= tile[(oy + kh) * TC + (ox + kw)] << (32 - (s + 1) * a.C);
-    }
+  // Patch words: tap s = kh * KW + kw holds window elements s*C .. s*C+C-1,
+  // element e at bit 31 - e % 32 of word e / 32.
+  uint32_t patch[PW];
+  if constexpr (PW == 1) {
+    uint32_t p = 0;
+    for (int kh = 0; kh < a.KH; ++kh)
+      for (int kw = 0; kw < a.KW; ++kw) {
+        const int s = kh * a.KW + kw;
+        p |= tile[(oy + kh) * TC + (ox + kw)] << (32 - (s + 1) * C);
+      }
+    patch[0] = p;
+  } else {
+    uint64_t hi = 0, lo = 0;
+    for (int kh = 0; kh < a.KH; ++kh)
+      for (int kw = 0; kw < a.KW; ++kw)
+        put_bits(hi, lo, tile[(oy + kh) * TC + (ox + kw)], (kh * a.KW + kw) * C, C);
+    split_words(patch, hi, lo);
+  }
 
   const int Wp = POOL ? a.Wo / 2 : a.Wo;
   const int Hp = POOL ? a.Ho / 2 : a.Ho;
   for (int f0 = 0; f0 < a.F; f0 += kFB) {
     const int nf = min(kFB, a.F - f0);
-    __syncthreads();  // previous round's filters are no longer read
-    if (t < kFB) {
-      uint32_t wp = 0;
+    __syncthreads();  // the previous round's filters are no longer read
+    {
+      uint32_t wp[PW];
+#pragma unroll
+      for (int q = 0; q < PW; ++q) wp[q] = 0;
       int32_t bias = 0;
       if (t < nf) {
         const int f = f0 + t;
         const uint32_t* wf = a.w + static_cast<size_t>(f) * a.KH * a.KW;  // one word per tap
-        for (int s = 0; s < a.KH * a.KW; ++s)
-          wp |= (wf[s] >> (32 - a.C)) << (32 - (s + 1) * a.C);
+        uint64_t hi = 0, lo = 0;
+        for (int s = 0; s < a.KH * a.KW; ++s) {
+          const uint32_t code = wf[s] >> (32 - C);
+          if constexpr (PW == 1)
+            wp[0] |= code << (32 - (s + 1) * C);
+          else
+            put_bits(hi, lo, code, s * C, C);
+        }
+        if constexpr (PW > 1) split_words(wp, hi, lo);
         if constexpr (BITS) {
           // q = floor((K - thr) / 2), clamped to [-1, K]
           const int64_t d = static_cast<int64_t>(a.P) - a.thr[f];
@@ -116,7 +211,8 @@ __global__ __launch_bounds__(256) void bconv_patch_kernel(PatchArgs a) {
           bias = static_cast<int32_t>(-q - 1);
         }
       }
-      wpat[t] = wp;
+#pragma unroll
+      for (int q = 0; q < PW; ++q) wpat[t * PW + q] = wp[q];
       wbias[t] = bias;
     }
     __syncthreads();
@@ -127,16 +223,22 @@ __global__ __launch_bounds__(256) void bconv_patch_kernel(PatchArgs a) {
         if (valid) {
           int32_t* sp = a.sums + ((static_cast<size_t>(n) * a.Ho + i) * a.Wo + j) * a.F + f0 + g;
           const int m = min(32, nf - g);
-          for (int k = 0; k < m; ++k)
-            sp[k] = a.P - 2 * static_cast<int32_t>(__builtin_popcount(patch ^ wpat[g + k]));
+          for (int k = 0; k < m; ++k) {
+            int32_t cnt = 0;
+#pragma unroll
+            for (int q = 0; q < PW; ++q) cnt += __builtin_popcount(patch[q] ^ wpat[(g + k) * PW + q]);
+            sp[k] = a.P - 2 * cnt;
+          }
         }
       }
       if constexpr (BITS) {
         uint32_t word = 0;
 #pragma unroll
         for (int k = 0; k < 32; ++k) {
-          const uint32_t d = static_cast<uint32_t>(__builtin_popcount(patch ^ wpat[g + k])) +
-                             static_cast<uint32_t>(wbias[g + k]);
+          uint32_t d = static_cast<uint32_t>(wbias[g + k]);
+#pragma unroll
+          for (int q = 0; q < PW; ++q)
+            d += static_cast<uint32_t>(__builtin_popcount(patch[q] ^ wpat[(g + k) * PW + q]));
           word = __builtin_amdgcn_alignbit(word, d, 31);
         }
         if (a.flip) word ^= a.flip[fw];
@@ -154,38 +256,52 @@ __global__ __launch_bounds__(256) void bconv_patch_kernel(PatchArgs a) {
   }
 }
 
-template <bool POOL>
-hipError_t launch_pool(const PatchArgs& a, dim3 grid, hipStream_t s) {
+template <int PW, bool POOL>
+void launch_out(const PatchArgs& a, dim3 grid, hipStream_t s) {
   if (a.sums && a.bits)
-    bconv_patch_kernel<POOL, true, true><<<grid, 256, 0, s>>>(a);
+    bconv_patch_kernel<PW, POOL, true, true><<<grid, 256, 0, s>>>(a);
   else if (a.sums)
-    bconv_patch_kernel<POOL, true, false><<<grid, 256, 0, s>>>(a);
+    bconv_patch_kernel<PW, POOL, true, false><<<grid, 256, 0, s>>>(a);
   else
-    bconv_patch_kernel<POOL, false, true><<<grid, 256, 0, s>>>(a);
-  return hipGetLastError();
+    bconv_patch_kernel<PW, POOL, false, true><<<grid, 256, 0, s>>>(a);
+}
+
+template <int PW>
+void launch_pw(const PatchArgs& a, bool pool, dim3 grid, hipStream_t s) {
+  if (pool)
+    launch_out<PW, true>(a, grid, s);
+  else
+    launch_out<PW, false>(a, grid, s);
 }
 
 }  // namespace
 
-bool bconv_patch_supported(const ConvGeom& g) {
-  return int64_t{g.KH} * g.KW * g.C <= 32;
+int input_channels_of(int mode, int cin) {
+  return mode == BNN_INPUT_GRAY ? 1 : mode == BNN_INPUT_LBP ? 3 : cin;
 }
 
-hipError_t launch_bconv_patch(const ConvGeom& g, const float* x, const float* offset,
+bool bconv_patch_supported(const ConvGeom& g) {
+  return g.C <= 32 && g.KH <= 32 && g.KW <= 32 && int64_t{g.KH} * g.KW * g.C <= 128;
+}
+
+hipError_t launch_binarize(int mode, const float* x, const float* offset, int32_t N, int32_t H,
+                           int32_t W, int32_t Cin, uint32_t* out, hipStream_t s) {
+  BinArgs a{x, offset, mode, N, H, W, Cin, input_channels_of(mode, Cin)};
+  const int64_t total = int64_t{N} * H * W;
+  binarize_kernel<<<dim3(static_cast<unsigned>((total + 255) / 256)), 256, 0, s>>>(a, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_bconv_patch(const ConvGeom& g, int mode, const float* x, const float* offset,
                               const uint32_t* w, const int32_t* thr, const uint32_t* flip,
                               int32_t* sums, uint32_t* bits, hipStream_t s) {
   PatchArgs a;
-  a.x = x;
-  a.offset = offset;
+  a.in = BinArgs{x, offset, mode, g.N, g.H, g.W, mode == BNN_INPUT_THRESHOLD ? g.C : 3, g.C};
   a.w = w;
   a.thr = thr;
   a.flip = flip;
   a.sums = sums;
   a.bits = bits;
-  a.N = g.N;
-  a.H = g.H;
-  a.W = g.W;
-  a.C = g.C;
   a.F = g.F;
   a.Fw = g.Fw;
   a.KH = g.KH;
@@ -197,7 +313,14 @@ hipError_t launch_bconv_patch(const ConvGeom& g, const float* x, const float* of
   a.tiles_x = (g.Wo + kTW - 1) / kTW;
   a.tiles_y = (g.Ho + kTH - 1) / kTH;
   const dim3 grid(static_cast<unsigned>(int64_t{g.N} * a.tiles_x * a.tiles_y));
-  return g.pool == 2 ? launch_pool<true>(a, grid, s) : launch_pool<false>(a, grid, s);
+  const bool pool = g.pool == 2;
+  switch ((a.P + 31) / 32) {
+    case 1: launch_pw<1>(a, pool, grid, s); break;
+    case 2: launch_pw<2>(a, pool, grid, s); break;
+    case 3: launch_pw<3>(a, pool, grid, s); break;
+    default: launch_pw<4>(a, pool, grid, s); break;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace bnn

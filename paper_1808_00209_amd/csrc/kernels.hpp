@@ -41,11 +41,17 @@ hipError_t launch_bconv_mfma(const ConvGeom& g, const uint32_t* in,
                              const uint32_t* flip, int32_t* sums,
                              uint32_t* bits, hipStream_t s);
 
-// Binary conv over an fp32 image thresholded on the fly, one packed patch
-// word per output pixel.  Supported when bconv_patch_supported(g):
-// KH*KW*C <= 32.
+// Input binarization (bnn_input_mode of bnn.h) of an fp32 image into one
+// code word per pixel, and the binary conv over an image binarized on the
+// fly with one window packed into ceil(KH*KW*C / 32) words.  Supported when
+// bconv_patch_supported(g): C, KH, KW <= 32 and KH*KW*C <= 128.  g.C is the
+// binarized channel count, input_channels_of(mode, Cin).
+int input_channels_of(int mode, int cin);
+hipError_t launch_binarize(int mode, const float* x, const float* offset,
+                           int32_t N, int32_t H, int32_t W, int32_t Cin,
+                           uint32_t* out, hipStream_t s);
 bool bconv_patch_supported(const ConvGeom& g);
-hipError_t launch_bconv_patch(const ConvGeom& g, const float* x,
+hipError_t launch_bconv_patch(const ConvGeom& g, int mode, const float* x,
                               const float* offset, const uint32_t* w,
                               const int32_t* thr, const uint32_t* flip,
                               int32_t* sums, uint32_t* bits, hipStream_t s);

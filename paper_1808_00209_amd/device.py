@@ -35,8 +35,10 @@ def upload_layer(L, device="cuda"):
     """A host layer dict (see synth) -> device tensors + C-struct fields."""
     kind = L["kind"]
     d = {}
-    if kind == "input_threshold":
-        d.update(kind=bnn.LAYER_INPUT_THRESHOLD, C=L["C"])
+    if kind in ("input_threshold", "input_gray", "input_lbp"):
+        d.update(kind={"input_threshold": bnn.LAYER_INPUT_THRESHOLD,
+                       "input_gray": bnn.LAYER_INPUT_GRAY,
+                       "input_lbp": bnn.LAYER_INPUT_LBP}[kind], C=L["C"])
         if L.get("offset") is not None:
             d["offset"] = to_device(L["offset"], torch.float32, device)
         return d

@@ -84,6 +84,8 @@ def rgb_offsets(g: np.random.Generator, c: int) -> np.ndarray:
 # --------------------------------------------------------------------------
 # Layer descriptions.  A layer is a dict; binary tensors are +-1 int8.
 #   input_threshold: C, offset[C]
+#   input_gray:      C (= 3), offset[1]
+#   input_lbp:       C (= 3)
 #   fconv / bconv:   C, F, KH, KW, pad, pool, w[F,KH,KW,C], thr[F], flip[F]
 #   bfc:             K, N, w[N,K], thr[N], flip[N]
 #   bfc_logits:      K, N, w[N,K]
@@ -185,6 +187,35 @@ def cfg5_case(name, N=None):
     layer = conv_layer(5, li, "bconv", s["C"], s["F"], k=s["k"], pad=s["pad"])
     x = pm1(rng(5, li, T_X), (s["N"], s["H"], s["W"], s["C"]))
     return x, layer
+
+
+# Paper-shaped vehicle classifier (Table II): an input binarization, binary
+# convs 32@5x5 + 2x2 pool and 32@5x5 + 2x2 pool, FC 18432 -> 100, then the two
+# small FC layers the paper leaves out of Table II (100 -> 100 -> 4; their
+# sizes are not given, 100 is the reading).  Input binarizations of Table III:
+# "rgb" (per-channel thresholds), "gray" (grayscale threshold) and "lbp".
+PAPER_MODES = ("rgb", "gray", "lbp")
+
+
+def paper_net(mode="rgb"):
+    if mode == "rgb":
+        first, c = dict(kind="input_threshold", C=3, offset=rgb_offsets(rng(6, 0, T_W), 3)), 3
+    elif mode == "gray":
+        first, c = dict(kind="input_gray", C=3, offset=rgb_offsets(rng(6, 0, T_W), 1)), 1
+    elif mode == "lbp":
+        first, c = dict(kind="input_lbp", C=3), 3
+    else:
+        raise ValueError(mode)
+    return [first,
+            conv_layer(6, 1, "bconv", c, 32, k=5, pad=2, pool=2),
+            conv_layer(6, 2, "bconv", 32, 32, k=5, pad=2, pool=2),
+            fc_layer(6, 3, 24 * 24 * 32, 100),
+            fc_layer(6, 4, 100, 100),
+            fc_layer(6, 5, 100, 4, logits=True)]
+
+
+def paper_input(batch):
+    return pixels(rng(6, 90, T_X), (batch, 96, 96, 3))
 
 
 def bit_macs_conv(N, Ho, Wo, F, KH, KW, C):

@@ -37,7 +37,8 @@ def test_library_exports_every_declared_symbol():
 @needs_lib
 def test_abi_version_and_empty_error():
     lib = bnn.load()
-    assert lib.bnn_abi_version() == 1
+    header = open(HEADER).read()
+    assert "#define BNN_ABI_VERSION %d" % lib.bnn_abi_version() in header
     assert isinstance(bnn.last_error(), str)
 
 
@@ -96,19 +97,36 @@ def test_bconv_null_and_alignment_errors():
 def test_bconv_input_errors():
     lib = bnn.load()
 
-    def call(desc, x=A, off=None, w=A, thr=A, sums=A, bits=A):
-        return lib.bnn_bconv2d_input(ctypes.byref(desc), x, off, w, thr, None, sums, bits, None)
+    def call(desc, mode=0, x=A, off=None, w=A, thr=A, sums=A, bits=A):
+        return lib.bnn_bconv2d_input(ctypes.byref(desc), mode, x, off, w, thr, None, sums, bits,
+                                     None)
 
-    # a window must fit one word: 3x3x4 = 36 bits does not, 3x3x3 and 5x5x1 do
-    assert call(_conv(C=4)) == 4 and "36 bits" in bnn.last_error()
-    assert call(_conv(C=32, KH=1, KW=2)) == 4
+    # the window must fit 128 bits with C, KH, KW <= 32: 5x5x6 = 150 does not
+    assert call(_conv(C=6, KH=5, KW=5)) == 4 and "150 bits" in bnn.last_error()
+    assert call(_conv(C=33, KH=1, KW=1)) == 4
+    assert call(_conv(C=1, KH=33, KW=1, H=40)) == 4
     assert call(_conv(C=3, stride=2)) == 4 and "stride" in bnn.last_error()
     assert call(_conv(C=3, pool=3)) == 2
+    assert call(_conv(C=3), mode=3) == 2 and "mode" in bnn.last_error()
+    assert call(_conv(C=3), mode=1) == 2 and "channels" in bnn.last_error()  # gray is 1 channel
+    assert call(_conv(C=1), mode=2) == 2                                     # LBP is 3
     assert call(_conv(C=3), x=None) == 1 and "input" in bnn.last_error()
     assert call(_conv(C=3), thr=None) == 1 and "thr" in bnn.last_error()
     assert call(_conv(C=3), sums=None, bits=None) == 1
     assert call(_conv(C=3), x=A + 4) == 3
-    assert lib.bnn_bconv2d_input(None, A, None, A, A, None, A, A, None) == 1
+    assert lib.bnn_bconv2d_input(None, 0, A, None, A, A, None, A, A, None) == 1
+
+
+@needs_lib
+def test_binarize_input_errors():
+    lib = bnn.load()
+    assert lib.bnn_binarize_input(5, A, None, 1, 4, 4, 3, A, None) == 2
+    assert lib.bnn_binarize_input(0, A, None, 0, 4, 4, 3, A, None) == 2
+    assert lib.bnn_binarize_input(0, A, None, 1, 4, 4, 33, A, None) == 2
+    assert lib.bnn_binarize_input(1, A, None, 1, 4, 4, 4, A, None) == 2
+    assert lib.bnn_binarize_input(2, A, None, 1, 4, 4, 1, A, None) == 2
+    assert lib.bnn_binarize_input(2, None, None, 1, 4, 4, 3, A, None) == 1
+    assert lib.bnn_binarize_input(2, A, None, 1, 4, 4, 3, A + 4, None) == 3
 
 
 @needs_lib

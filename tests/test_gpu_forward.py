@@ -76,3 +76,22 @@ def test_forward_is_deterministic_and_batch_independent():
     c = _gpu_logits(layers, x[5:6])
     assert np.array_equal(a, b)
     assert np.array_equal(a[5:6], c)
+
+
+@pytest.mark.parametrize("mode", synth.PAPER_MODES)
+def test_paper_net_small_batch(mode, algo):
+    """Table II's 5x5 vehicle classifier behind each input binarization of
+    Table III (RGB / grayscale thresholding, LBP)."""
+    layers, x = synth.paper_net(mode), synth.paper_input(2)
+    got = _gpu_logits(layers, x)
+    ref = oracle.forward(layers, x)
+    assert got.shape == (2, 4)
+    assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("mode", synth.PAPER_MODES)
+def test_paper_net_batch64_sampled_images(mode):
+    layers, x = synth.paper_net(mode), synth.paper_input(64)
+    got = _gpu_logits(layers, x)
+    pick = [0, 41, 63]
+    assert np.array_equal(got[pick], oracle.forward(layers, x[pick]))

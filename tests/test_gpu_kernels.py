@@ -337,26 +337,49 @@ def test_fconv_cifar_first_layer_batch64(algo):
     assert np.array_equal(words_u32(bits), oracle.pack_eq2(oracle.threshold(S, L["thr"], L["flip"])))
 
 
-# --------------------------------------------- thresholded-input patch conv --
-# N, H, W, C, F, KH, KW, pad, pool: several 8x32 tiles with ragged edges, odd
-# sizes under pooling (floor), F tails, 25- and 18-bit windows, pad 0, a
-# one-pixel window of 32 channels, and a 32-tap column window with F > 256
-# (two rounds of staged filters).
+# ------------------------------- input binarization and patch-packed conv --
+# Sec. II-C / Table III input binarizations and the first conv over them with
+# each window packed into ceil(KH*KW*C / 32) words (Algorithm 1's patch
+# packing).  Cases: N, H, W, C, F, KH, KW, pad, pool, mode.  Several 8x32
+# tiles with ragged edges, odd sizes under pooling (floor), F tails, windows
+# of 18 to 121 bits (1 to 4 words, words straddled by a tap's channels), pad
+# 0, a one-pixel window of 32 channels, a 32-tap column with F > 256 (two
+# rounds of staged filters), and the grayscale and LBP inputs.
+T, G, L = 0, 1, 2  # bnn_input_mode
 PATCH_CASES = [
-    (2, 12, 40, 3, 64, 3, 3, 1, 0),
-    (1, 17, 35, 3, 64, 3, 3, 1, 2),
-    (1, 9, 9, 3, 40, 3, 3, 1, 2),
-    (2, 10, 11, 1, 32, 5, 5, 2, 0),
-    (1, 8, 70, 2, 96, 3, 3, 0, 0),
-    (1, 6, 6, 32, 33, 1, 1, 0, 2),
-    (1, 40, 3, 1, 300, 32, 1, 3, 0),
+    (2, 12, 40, 3, 64, 3, 3, 1, 0, T),
+    (1, 17, 35, 3, 64, 3, 3, 1, 2, T),
+    (1, 9, 9, 3, 40, 3, 3, 1, 2, T),
+    (2, 10, 11, 1, 32, 5, 5, 2, 0, T),
+    (1, 8, 70, 2, 96, 3, 3, 0, 0, T),
+    (1, 6, 6, 32, 33, 1, 1, 0, 2, T),
+    (1, 40, 3, 1, 300, 32, 1, 3, 0, T),
+    (2, 20, 37, 3, 32, 5, 5, 2, 2, T),      # 75 bits, 3 words (the paper's first layer)
+    (1, 13, 19, 8, 48, 3, 3, 1, 0, T),      # 72 bits
+    (1, 15, 15, 2, 40, 7, 7, 3, 0, T),      # 98 bits, 4 words
+    (1, 14, 33, 1, 64, 11, 11, 5, 2, T),    # 121 bits
+    (2, 12, 40, 1, 64, 3, 3, 1, 0, G),
+    (1, 24, 24, 1, 32, 5, 5, 2, 2, G),
+    (2, 12, 40, 3, 64, 3, 3, 1, 2, L),
+    (1, 24, 35, 3, 32, 5, 5, 2, 2, L),
 ]
 
 
-def _patch_case(seed, N, H, W, C, F, KH, KW, pad):
+def _binarized(x, off, mode):
+    """The oracle's +-1 input for a binarization mode."""
+    if mode == T:
+        C = x.shape[-1]
+        return oracle.sign(x.reshape(-1, C), off).reshape(x.shape)
+    if mode == G:
+        return oracle.gray_threshold(x, float(off[0]))
+    return oracle.lbp(x)
+
+
+def _patch_case(seed, N, H, W, C, F, KH, KW, mode):
     rng = np.random.default_rng(seed)
-    x = synth.pixels(rng, (N, H, W, C))
-    off = synth.rgb_offsets(rng, C)
+    cin = C if mode == T else 3
+    x = synth.pixels(rng, (N, H, W, cin))
+    off = synth.rgb_offsets(rng, cin if mode == T else 1)
     w = _pm1(rng, (F, KH, KW, C))
     K = KH * KW * C
     thr = rng.integers(-K // 2, K // 2 + 1, size=F).astype(np.int32)
@@ -366,14 +389,14 @@ def _patch_case(seed, N, H, W, C, F, KH, KW, pad):
 
 @pytest.mark.parametrize("case", PATCH_CASES)
 def test_bconv_input_patch_bit_exact(case):
-    N, H, W, C, F, KH, KW, pad, pool = case
-    x, off, w, thr, flip = _patch_case(7 + sum(case), N, H, W, C, F, KH, KW, pad)
+    N, H, W, C, F, KH, KW, pad, pool, mode = case
+    x, off, w, thr, flip = _patch_case(7 + sum(case), N, H, W, C, F, KH, KW, mode)
     desc = bnn.conv_desc(N, H, W, C, F, KH, KW, 1, pad, pool)
-    sums, bits = bnn.bnn_bconv2d_input(desc, to_device(x), to_device(off), pack_pm1(w),
+    offd = to_device(off) if mode != L else None
+    sums, bits = bnn.bnn_bconv2d_input(desc, mode, to_device(x), offd, pack_pm1(w),
                                        to_device(thr, torch.int32), pack_flips(flip))
     torch.cuda.synchronize()
-    xb = oracle.sign(x.reshape(-1, C), off).reshape(x.shape)
-    S = oracle.conv2d(xb, w, 1, pad)
+    S = oracle.conv2d(_binarized(x, off, mode), w, 1, pad)
     b = oracle.threshold(S, thr, flip)
     if pool:
         b = oracle.maxpool2(b)
@@ -381,16 +404,26 @@ def test_bconv_input_patch_bit_exact(case):
     assert np.array_equal(words_u32(bits), oracle.pack_eq2(b))
 
 
+@pytest.mark.parametrize("mode,cin", [(T, 3), (T, 1), (T, 32), (T, 17), (G, 3), (L, 3)])
+def test_binarize_input_bit_exact(mode, cin):
+    rng = np.random.default_rng(40 + 3 * mode + cin)
+    x = synth.pixels(rng, (2, 13, 37, cin))
+    off = synth.rgb_offsets(rng, cin if mode == T else 1)
+    out = bnn.bnn_binarize_input(mode, to_device(x), to_device(off) if mode != L else None)
+    torch.cuda.synchronize()
+    assert np.array_equal(words_u32(out), oracle.pack_eq2(_binarized(x, off, mode)))
+
+
 def test_bconv_input_matches_pack_then_bconv():
     """The fused call equals bnn_pack_bits followed by bnn_bconv2d (bits only,
     no offset), on the vehicle-shaped first layer at batch 8."""
     N, H, W, C, F = 8, 96, 96, 3, 64
-    x, _, w, thr, flip = _patch_case(11, N, H, W, C, F, 3, 3, 1)
+    x, _, w, thr, flip = _patch_case(11, N, H, W, C, F, 3, 3, T)
     x = x - 127.0  # thresholds at 0 without an offset
     desc = bnn.conv_desc(N, H, W, C, F, 3, 3, 1, 1, 0)
     xd, wd = to_device(x), pack_pm1(w)
     td, fd = to_device(thr, torch.int32), pack_flips(flip)
-    _, fused = bnn.bnn_bconv2d_input(desc, xd, None, wd, td, fd, want_sums=False)
+    _, fused = bnn.bnn_bconv2d_input(desc, T, xd, None, wd, td, fd, want_sums=False)
     packed = bnn.bnn_pack_bits(xd)
     _, twostep = bnn.bnn_bconv2d(desc, packed, wd, td, fd, want_sums=False)
     torch.cuda.synchronize()
