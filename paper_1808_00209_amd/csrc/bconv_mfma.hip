@@ -30,6 +30,7 @@ namespace bnn {
 namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
+typedef int v4i __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
@@ -63,7 +64,14 @@ constexpr int kRsrcWord3 = 0x00020000;
 template <int VW>
 __device__ __forceinline__ void buf_load(uint32_t (&v)[VW], __amdgpu_buffer_rsrc_t r, uint32_t voff,
                                          uint32_t soff) {
-  if constexpr (VW == 2) {
+  if constexpr (VW == 4) {
+    typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+    const u4 t = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    v[0] = t[0];
+    v[1] = t[1];
+    v[2] = t[2];
+    v[3] = t[3];
+  } else if constexpr (VW == 2) {
     typedef unsigned int u2 __attribute__((ext_vector_type(2)));
     const u2 t = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
     v[0] = t[0];
@@ -113,6 +121,184 @@ struct Mfma32Args {
   FastDiv div_w, div_h;  // Wo, Ho (or Wp, Hp when pooling)
 };
 
+// This lane's pixel in each of the TP 32-pixel tiles of a wave: byte offset
+// of its first activation load, which taps fall inside the image, and the
+// output coordinates for the epilogue.
+template <int TP, bool POOL, int VW>
+struct PixTiles {
+  int pbase[TP], pn[TP], pi[TP], pj[TP];
+  uint32_t tapmask[TP];
+  bool pv[TP];
+
+  __device__ __forceinline__ void init(const Mfma32Args& a, int p0, int h, int c) {
+#pragma unroll
+    for (int tp = 0; tp < TP; ++tp) {
+      const int item = p0 + tp * 32 + c;
+      pv[tp] = item < a.items;
+      const uint32_t m = pv[tp] ? static_cast<uint32_t>(item) : 0u;
+      uint32_t pix = POOL ? (m >> 2) : m;
+      const uint32_t t = fdiv(pix, a.div_w);
+      const uint32_t jj = pix - t * a.div_w.d;
+      const uint32_t nn = fdiv(t, a.div_h);
+      const uint32_t ii = t - nn * a.div_h.d;
+      pn[tp] = static_cast<int>(nn);
+      if constexpr (POOL) {
+        pi[tp] = 2 * static_cast<int>(ii) + static_cast<int>((m >> 1) & 1);
+        pj[tp] = 2 * static_cast<int>(jj) + static_cast<int>(m & 1);
+      } else {
+        pi[tp] = static_cast<int>(ii);
+        pj[tp] = static_cast<int>(jj);
+      }
+      pbase[tp] = (((pn[tp] * a.H + pi[tp]) * a.W + pj[tp]) * a.Cw + h * VW) * 4;
+      // rows kh with 0 <= i + kh - pad < H, columns likewise
+      const int rlo = max(0, a.pad - pi[tp]), rhi = min(a.KH, a.H + a.pad - pi[tp]);
+      const int clo = max(0, a.pad - pj[tp]), chi = min(a.KW, a.W + a.pad - pj[tp]);
+      const uint32_t cm = chi > clo ? ((1u << chi) - 1u) & ~((1u << clo) - 1u) : 0u;
+      uint32_t mk = 0;
+      for (int kh = rlo; kh < rhi; ++kh) mk |= cm << (kh * a.KW);
+      tapmask[tp] = pv[tp] ? mk : 0u;
+    }
+  }
+};
+
+// Loop position of the next load (wave-uniform): iteration l_it is tap
+// (l_kh, l_kw), word chunk l_cc.  Advanced incrementally (no divisions in the
+// loop); it stops at the last iteration it1 - 1, so extra loads past the end
+// repeat it.
+struct Cursor {
+  int l_it, l_cc, l_kh, l_kw, it1;
+
+  __device__ __forceinline__ void init(const Mfma32Args& a, int it0, int it1_, int nchunk,
+                                       int vw) {
+    it1 = it1_;
+    l_it = it0;
+    const int tap = it0 / nchunk;
+    l_cc = (it0 - tap * nchunk) * 2 * vw;
+    l_kh = tap / a.KW;
+    l_kw = tap - l_kh * a.KW;
+  }
+  __device__ __forceinline__ int tap(const Mfma32Args& a) const { return l_kh * a.KW + l_kw; }
+  __device__ __forceinline__ void advance(const Mfma32Args& a, int vw) {
+    if (l_it + 1 < it1) {
+      ++l_it;
+      l_cc += 2 * vw;
+      if (l_cc == a.Cw) {
+        l_cc = 0;
+        if (++l_kw == a.KW) {
+          l_kw = 0;
+          ++l_kh;
+        }
+      }
+    }
+  }
+};
+
+// Activation words of the cursor's iteration for the TP pixel tiles; taps
+// outside the image read the out-of-range offset, i.e. the pad word 0.
+template <int TP, bool POOL, int VW>
+__device__ __forceinline__ void load_act(uint32_t (&aw)[TP][VW], const Mfma32Args& a,
+                                         const Cursor& cur, const PixTiles<TP, POOL, VW>& px,
+                                         __amdgpu_buffer_rsrc_t rin) {
+  const int tap = cur.tap(a);
+  const int dshift = (((cur.l_kh - a.pad) * a.W + (cur.l_kw - a.pad)) * a.Cw + cur.l_cc) * 4;
+  const uint32_t bit = 1u << tap;
+#pragma unroll
+  for (int tp = 0; tp < TP; ++tp) {
+    const uint32_t off = (px.tapmask[tp] & bit) ? static_cast<uint32_t>(px.pbase[tp] + dshift)
+                                                : kOutOfRange;
+    buf_load<VW>(aw[tp], rin, off, 0u);
+  }
+}
+
+// Sums, threshold / flip, OR-pool and stores of a wave's TF x TP tiles.
+template <int TF, int TP, bool POOL, int VW>
+__device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP],
+                                         const PixTiles<TP, POOL, VW>& px, int p0, int f0,
+                                         int h, int c) {
+  // Filters past F (a partial last tile) read zero weights through the
+  // buffer range and are masked out of every output.
+  const bool ftail = f0 + 32 * TF > a.F;
+  if (a.sums) {
+#pragma unroll
+    for (int tp = 0; tp < TP; ++tp) {
+      if (!px.pv[tp]) continue;
+      int32_t* sp = a.sums +
+                    (static_cast<size_t>(px.pn[tp] * a.Ho + px.pi[tp]) * a.Wo + px.pj[tp]) * a.F +
+                    f0 + 4 * h;
+#pragma unroll
+      for (int tf = 0; tf < TF; ++tf)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int fb = f0 + tf * 32 + 8 * g + 4 * h;  // first of 4 filters
+          if (!ftail && (a.F & 3) == 0) {
+            int4 t;
+            t.x = static_cast<int>(acc[tf][tp][4 * g + 0]);
+            t.y = static_cast<int>(acc[tf][tp][4 * g + 1]);
+            t.z = static_cast<int>(acc[tf][tp][4 * g + 2]);
+            t.w = static_cast<int>(acc[tf][tp][4 * g + 3]);
+            *reinterpret_cast<int4*>(sp + tf * 32 + 8 * g) = t;
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (fb + e < a.F) sp[tf * 32 + 8 * g + e] = static_cast<int>(acc[tf][tp][4 * g + e]);
+          }
+        }
+    }
+  }
+  if (a.bits) {
+    // Threshold minus one half: S >= thr  <=>  (thr - 0.5) - S < 0 for
+    // integer S, so the sign bit of that difference is the output bit.
+    // Thresholds are clamped to [-K-1, K+1] first (|S| <= K, so this keeps
+    // every comparison) to stay exact in fp32 for any int32 threshold.
+    float th[TF][16];
+#pragma unroll
+    for (int tf = 0; tf < TF; ++tf)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int f = f0 + tf * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+        const int t = a.thr[f < a.F ? f : a.F - 1];
+        th[tf][e] = static_cast<float>(min(max(t, -a.K - 1), a.K + 1)) - 0.5f;
+      }
+    uint32_t fl[TF], fm[TF];
+#pragma unroll
+    for (int tf = 0; tf < TF; ++tf) {
+      const int wi = f0 / 32 + tf;
+      fl[tf] = a.flip ? a.flip[wi < a.Fw ? wi : a.Fw - 1] : 0u;
+      fm[tf] = wi == a.Fw - 1 ? tail_mask(a.F) : ~0u;
+    }
+#pragma unroll
+    for (int tp = 0; tp < TP; ++tp) {
+      uint32_t word[TF];
+#pragma unroll
+      for (int tf = 0; tf < TF; ++tf) {
+        uint32_t wd = 0u;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float d = th[tf][e] - acc[tf][tp][e];
+          // filter 8 (e/4) + 4 h + e%4 of the word -> bit 31 - that
+          const int pos = 31 - (8 * (e >> 2) + 4 * h + (e & 3));
+          wd |= (__float_as_uint(d) >> 31) << pos;
+        }
+        wd |= __shfl_xor(wd, 32);
+        wd = (wd ^ fl[tf]) & fm[tf];
+        if constexpr (POOL) {
+          wd |= __shfl_xor(wd, 1);
+          wd |= __shfl_xor(wd, 2);
+        }
+        word[tf] = wd;
+      }
+      const int item = p0 + tp * 32 + c;
+      const bool writer = POOL ? (h == 0 && (c & 3) == 0 && px.pv[tp]) : (h == 0 && px.pv[tp]);
+      if (writer) {
+        uint32_t* op = a.bits + static_cast<size_t>(POOL ? (item >> 2) : item) * a.Fw + f0 / 32;
+#pragma unroll
+        for (int tf = 0; tf < TF; ++tf)
+          if (f0 / 32 + tf < a.Fw) op[tf] = word[tf];
+      }
+    }
+  }
+}
+
 // Template parameters:
 //   VW   words each lane loads per operand row and iteration (1 or 2).  One
 //        MFMA k-step covers 2 words (one per lane half), so an iteration (a
@@ -120,9 +306,11 @@ struct Mfma32Args {
 //   POOL pixels of a 32-tile ordered as eight 2x2 windows (4 adjacent lanes).
 //   TF   32-filter tiles per wave (1 or 2); a wave always covers 64 pixels.
 //   KS   1: the 4 waves of a block take 4 consecutive 64-pixel groups;
-//        >1: the KS (2..8) waves of a block split the iterations of one tile
-//        and add their partial sums in LDS (grids too small to fill the chip).
+//        >1: the KS (2..8; 2 or 4 with TF = 2) waves of a block split the
+//        iterations of one tile and add their partial sums in LDS (grids too
+//        small to fill the chip).
 //   PD   register sets of loads in flight (prefetch depth).
+// Each wave loads and expands its own weight words in registers.
 template <int VW, bool POOL, int TF, int KS, int PD>
 __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(Mfma32Args a) {
   constexpr int TP = 2;
@@ -141,38 +329,8 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
     it1 = min(iters, it0 + per);
   }
 
-  // This lane's pixel in each of the TP pixel tiles: byte offset of its
-  // first load, and which taps fall inside the image.
-  int pbase[TP], pn[TP], pi[TP], pj[TP];
-  uint32_t tapmask[TP];
-  bool pv[TP];
-#pragma unroll
-  for (int tp = 0; tp < TP; ++tp) {
-    const int item = p0 + tp * 32 + c;
-    pv[tp] = item < a.items;
-    const uint32_t m = pv[tp] ? static_cast<uint32_t>(item) : 0u;
-    uint32_t pix = POOL ? (m >> 2) : m;
-    const uint32_t t = fdiv(pix, a.div_w);
-    const uint32_t jj = pix - t * a.div_w.d;
-    const uint32_t nn = fdiv(t, a.div_h);
-    const uint32_t ii = t - nn * a.div_h.d;
-    pn[tp] = static_cast<int>(nn);
-    if constexpr (POOL) {
-      pi[tp] = 2 * static_cast<int>(ii) + static_cast<int>((m >> 1) & 1);
-      pj[tp] = 2 * static_cast<int>(jj) + static_cast<int>(m & 1);
-    } else {
-      pi[tp] = static_cast<int>(ii);
-      pj[tp] = static_cast<int>(jj);
-    }
-    pbase[tp] = (((pn[tp] * a.H + pi[tp]) * a.W + pj[tp]) * a.Cw + h * VW) * 4;
-    // rows kh with 0 <= i + kh - pad < H, columns likewise
-    const int rlo = max(0, a.pad - pi[tp]), rhi = min(a.KH, a.H + a.pad - pi[tp]);
-    const int clo = max(0, a.pad - pj[tp]), chi = min(a.KW, a.W + a.pad - pj[tp]);
-    const uint32_t cm = chi > clo ? ((1u << chi) - 1u) & ~((1u << clo) - 1u) : 0u;
-    uint32_t mk = 0;
-    for (int kh = rlo; kh < rhi; ++kh) mk |= cm << (kh * a.KW);
-    tapmask[tp] = pv[tp] ? mk : 0u;
-  }
+  PixTiles<TP, POOL, VW> px;
+  px.init(a, p0, h, c);
 
   v16f acc[TF][TP];
 #pragma unroll
@@ -194,40 +352,14 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
   uint32_t vfill;
   asm("v_mov_b32 %0, 0x22222222" : "=v"(vfill));
 
-  // Loop position of the next load (wave-uniform): tap (kh, kw) and word
-  // chunk cc, advanced incrementally (no divisions inside the loop); it stops
-  // at the last iteration, so the clamped extra loads repeat it.
-  int l_it = it0, l_cc = 0, l_kh = 0, l_kw = 0;
-  {
-    const int tap = it0 / nchunk;
-    l_cc = (it0 - tap * nchunk) * 2 * VW;
-    l_kh = tap / a.KW;
-    l_kw = tap - l_kh * a.KW;
-  }
+  Cursor cur;
+  cur.init(a, it0, it1, nchunk, VW);
   auto load_next = [&](uint32_t (&ww)[TF][VW], uint32_t (&aw)[TP][VW]) {
-    const int tap = l_kh * a.KW + l_kw;
-    const uint32_t wsoff = static_cast<uint32_t>((tap * a.Cw + l_cc) * 4);
+    const uint32_t wsoff = static_cast<uint32_t>((cur.tap(a) * a.Cw + cur.l_cc) * 4);
 #pragma unroll
     for (int tf = 0; tf < TF; ++tf) buf_load<VW>(ww[tf], rw, woff[tf], wsoff);
-    const int dshift = (((l_kh - a.pad) * a.W + (l_kw - a.pad)) * a.Cw + l_cc) * 4;
-    const uint32_t bit = 1u << tap;
-#pragma unroll
-    for (int tp = 0; tp < TP; ++tp) {
-      const uint32_t off = (tapmask[tp] & bit) ? static_cast<uint32_t>(pbase[tp] + dshift)
-                                               : kOutOfRange;
-      buf_load<VW>(aw[tp], rin, off, 0u);
-    }
-    if (l_it + 1 < it1) {
-      ++l_it;
-      l_cc += 2 * VW;
-      if (l_cc == a.Cw) {
-        l_cc = 0;
-        if (++l_kw == a.KW) {
-          l_kw = 0;
-          ++l_kh;
-        }
-      }
-    }
+    load_act<TP, POOL, VW>(aw, a, cur, px, rin);
+    cur.advance(a, VW);
   };
   auto compute = [&](const uint32_t (&ww)[TF][VW], const uint32_t (&aw)[TP][VW]) {
 #pragma unroll
@@ -293,89 +425,159 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[tf][tp][e] = part[0][((tf * TP + tp) * 16 + e) * 64 + lane];
   }
+  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c);
+}
 
-  // Filters past F (a partial last tile) read zero weights through the
-  // buffer range and are masked out of every output.
-  const bool ftail = f0 + 32 * TF > a.F;
-  if (a.sums) {
+// The same conv with the weights shared through LDS.  The 4 waves of a block
+// take 4 pixel groups of 64 and the same TF filter tiles (TF = 1 or 2).
+// The weight words of QS iterations at a time (a stage) are loaded once per
+// block, expanded to fp4 once per block (instead of once per wave), and
+// stored in LDS in the exact layout of the MFMA's A operand, so each k-step
+// reads its TF operands with one conflict-free ds_read_b128 each.  Stages are
+// double-buffered: the next stage's words are loaded during the current
+// stage's MFMAs and expanded after them, and one barrier per stage separates
+// the buffers.  Activations are loaded and expanded per wave as above.
+constexpr int kQS = 4;  // iterations per stage
+
+template <int VW, int TF>
+struct LdsStage {
+  // [buffer][iteration q][k-step v][filter tile][lane] x 16 bytes
+  static constexpr int kOps = kQS * VW * TF;            // operand slots per buffer
+  static constexpr int kChunks = kQS * TF * 32;         // (iteration, filter) pairs
+  static constexpr int kPerThread = (kChunks + 255) / 256;
+};
+
+template <int VW, bool POOL, int TF, int PD>
+__global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
+  constexpr int TP = 2;
+  using St = LdsStage<VW, TF>;
+  __shared__ v4i wlds[2][St::kOps * 64];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int h = lane >> 5;
+  const int c = lane & 31;
+  const int p0 = (blockIdx.x * 4 + wave) * 64;
+  const int f0 = blockIdx.y * (32 * TF);
+  const int nchunk = a.Cw / (2 * VW);
+  const int iters = a.KH * a.KW * nchunk;
+  const int stages = (iters + kQS - 1) / kQS;
+
+  PixTiles<TP, POOL, VW> px;
+  px.init(a, p0, h, c);
+
+  v16f acc[TF][TP];
 #pragma unroll
-    for (int tp = 0; tp < TP; ++tp) {
-      if (!pv[tp]) continue;
-      int32_t* sp = a.sums + (static_cast<size_t>(pn[tp] * a.Ho + pi[tp]) * a.Wo + pj[tp]) * a.F +
-                    f0 + 4 * h;
+  for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
-      for (int tf = 0; tf < TF; ++tf)
+    for (int tp = 0; tp < TP; ++tp)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int fb = f0 + tf * 32 + 8 * g + 4 * h;  // first of 4 filters
-          if (!ftail && (a.F & 3) == 0) {
-            int4 t;
-            t.x = static_cast<int>(acc[tf][tp][4 * g + 0]);
-            t.y = static_cast<int>(acc[tf][tp][4 * g + 1]);
-            t.z = static_cast<int>(acc[tf][tp][4 * g + 2]);
-            t.w = static_cast<int>(acc[tf][tp][4 * g + 3]);
-            *reinterpret_cast<int4*>(sp + tf * 32 + 8 * g) = t;
-          } else {
+      for (int e = 0; e < 16; ++e) acc[tf][tp][e] = 0.0f;
+
+  const __amdgpu_buffer_rsrc_t rin = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(a.in), 0, a.in_bytes, kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(a.w), 0, a.w_bytes, kRsrcWord3);
+  const uint32_t smask = __builtin_amdgcn_readfirstlane(0x88888888u);
+  uint32_t vfill;
+  asm("v_mov_b32 %0, 0x22222222" : "=v"(vfill));
+
+  // Staging: thread t handles (iteration q, filter fi) pairs k = t + 256 j,
+  // fi = k % (32 TF), q = k / (32 TF); it loads that filter's 2 VW words of
+  // the stage's q-th iteration and writes their 2 VW expanded operands.
+  uint32_t sw[St::kPerThread][2 * VW];
+  auto stage_load = [&](int s) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (fb + e < a.F) sp[tf * 32 + 8 * g + e] = static_cast<int>(acc[tf][tp][4 * g + e]);
+    for (int j = 0; j < St::kPerThread; ++j) {
+      const int k = threadIdx.x + 256 * j;
+      const int fi = k % (32 * TF), q = k / (32 * TF);
+      const int it = s * kQS + q;
+      uint32_t off = kOutOfRange;
+      if (k < St::kChunks && it < iters) {
+        const int tap = it / nchunk;
+        const int cc = (it - tap * nchunk) * 2 * VW;
+        off = static_cast<uint32_t>(((f0 + fi) * a.fstride + tap * a.Cw + cc) * 4);
+      }
+      if constexpr (VW == 2) {
+        typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+        const u4 t = __builtin_amdgcn_raw_buffer_load_b128(rw, off, 0, 0);
+        sw[j][0] = t[0];
+        sw[j][1] = t[1];
+        sw[j][2] = t[2];
+        sw[j][3] = t[3];
+      } else {
+        typedef unsigned int u2 __attribute__((ext_vector_type(2)));
+        const u2 t = __builtin_amdgcn_raw_buffer_load_b64(rw, off, 0, 0);
+        sw[j][0] = t[0];
+        sw[j][1] = t[1];
+      }
+    }
+  };
+  auto stage_store = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < St::kPerThread; ++j) {
+      const int k = threadIdx.x + 256 * j;
+      if (k >= St::kChunks) continue;
+      const int fi = k % (32 * TF), q = k / (32 * TF);
+      const int tf = fi >> 5, cr = fi & 31;
+#pragma unroll
+      for (int wj = 0; wj < 2 * VW; ++wj) {
+        // word wj of the chunk: lane half hh = wj / VW, k-step v = wj % VW
+        const int hh = wj / VW, v = wj % VW;
+        const v8i e = expand_fp4(sw[j][wj], smask, vfill);
+        wlds[buf][((q * VW + v) * TF + tf) * 64 + hh * 32 + cr] = v4i{e[0], e[1], e[2], e[3]};
+      }
+    }
+  };
+
+  Cursor cur;
+  cur.init(a, 0, iters, nchunk, VW);
+  uint32_t xr[2][TP][VW];
+
+  stage_load(0);
+  stage_store(0);
+#pragma unroll
+  for (int d = 0; d < 2; ++d) {
+    load_act<TP, POOL, VW>(xr[d], a, cur, px, rin);
+    cur.advance(a, VW);
+  }
+  __syncthreads();
+
+  for (int s = 0; s < stages; ++s) {
+    const int buf = s & 1;
+    const bool more = s + 1 < stages;
+    if (more) stage_load(s + 1);
+#pragma unroll
+    for (int q = 0; q < kQS; ++q) {
+      const int it = s * kQS + q;
+      __builtin_amdgcn_sched_barrier(0);
+      if (it < iters) {
+#pragma unroll
+        for (int v = 0; v < VW; ++v) {
+          v8i A[TF], B[TP];
+#pragma unroll
+          for (int tf = 0; tf < TF; ++tf) {
+            const v4i t = wlds[buf][((q * VW + v) * TF + tf) * 64 + lane];
+            A[tf] = v8i{t[0], t[1], t[2], t[3], 0, 0, 0, 0};
           }
+#pragma unroll
+          for (int tp = 0; tp < TP; ++tp) B[tp] = expand_fp4(xr[q & 1][tp][v], smask, vfill);
+#pragma unroll
+          for (int tf = 0; tf < TF; ++tf)
+#pragma unroll
+            for (int tp = 0; tp < TP; ++tp)
+              acc[tf][tp] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                  A[tf], B[tp], acc[tf][tp], 4, 4, 0, 127, 0, 127);
         }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      load_act<TP, POOL, VW>(xr[q & 1], a, cur, px, rin);
+      cur.advance(a, VW);
     }
+    if (more) stage_store(buf ^ 1);
+    __syncthreads();
   }
-  if (a.bits) {
-    // Threshold minus one half: S >= thr  <=>  (thr - 0.5) - S < 0 for
-    // integer S, so the sign bit of that difference is the output bit.
-    // Thresholds are clamped to [-K-1, K+1] first (|S| <= K, so this keeps
-    // every comparison) to stay exact in fp32 for any int32 threshold.
-    float th[TF][16];
-#pragma unroll
-    for (int tf = 0; tf < TF; ++tf)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int f = f0 + tf * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
-        const int t = a.thr[f < a.F ? f : a.F - 1];
-        th[tf][e] = static_cast<float>(min(max(t, -a.K - 1), a.K + 1)) - 0.5f;
-      }
-    uint32_t fl[TF], fm[TF];
-#pragma unroll
-    for (int tf = 0; tf < TF; ++tf) {
-      const int wi = f0 / 32 + tf;
-      fl[tf] = a.flip ? a.flip[wi] : 0u;
-      fm[tf] = wi == a.Fw - 1 ? tail_mask(a.F) : ~0u;
-    }
-#pragma unroll
-    for (int tp = 0; tp < TP; ++tp) {
-      uint32_t word[TF];
-#pragma unroll
-      for (int tf = 0; tf < TF; ++tf) {
-        uint32_t wd = 0u;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float d = th[tf][e] - acc[tf][tp][e];
-          // filter 8 (e/4) + 4 h + e%4 of the word -> bit 31 - that
-          const int pos = 31 - (8 * (e >> 2) + 4 * h + (e & 3));
-          wd |= (__float_as_uint(d) >> 31) << pos;
-        }
-        wd |= __shfl_xor(wd, 32);
-        wd = (wd ^ fl[tf]) & fm[tf];
-        if constexpr (POOL) {
-          wd |= __shfl_xor(wd, 1);
-          wd |= __shfl_xor(wd, 2);
-        }
-        word[tf] = wd;
-      }
-      const int item = p0 + tp * 32 + c;
-      const bool writer = POOL ? (h == 0 && (c & 3) == 0 && pv[tp]) : (h == 0 && pv[tp]);
-      if (writer) {
-        uint32_t* op = a.bits + static_cast<size_t>(POOL ? (item >> 2) : item) * a.Fw + f0 / 32;
-        if constexpr (TF == 2)
-          *reinterpret_cast<uint2*>(op) = make_uint2(word[0], word[1]);
-        else
-          *op = word[0];
-      }
-    }
-  }
+  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c);
 }
 
 int env_int(const char* name, int dflt) {
@@ -383,31 +585,42 @@ int env_int(const char* name, int dflt) {
   return e ? atoi(e) : dflt;
 }
 
-template <int VW, bool POOL, int PD>
-hipError_t launch32(const Mfma32Args& a, int tf, int ks, hipStream_t s) {
+template <int VW, bool POOL>
+hipError_t launch32(const Mfma32Args& a, int tf, int ks, bool lds, hipStream_t s) {
   const unsigned fy = static_cast<unsigned>((a.F + 32 * tf - 1) / (32 * tf));
   const unsigned groups = static_cast<unsigned>((a.items + 63) / 64);
+  if constexpr (VW <= 2) {
+    if (lds) {
+      dim3 grid((groups + 3) / 4, fy), block(256);
+      if (tf == 2)
+        bconv_mfma_lds_kernel<VW, POOL, 2, 2><<<grid, block, 0, s>>>(a);
+      else
+        bconv_mfma_lds_kernel<VW, POOL, 1, 2><<<grid, block, 0, s>>>(a);
+      return hipGetLastError();
+    }
+  }
   if (ks == 1) {
     dim3 grid((groups + 3) / 4, fy), block(256);
     if (tf == 2)
-      bconv_mfma32_kernel<VW, POOL, 2, 1, PD><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 2, 1, 2><<<grid, block, 0, s>>>(a);
     else
-      bconv_mfma32_kernel<VW, POOL, 1, 1, PD><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 1, 2><<<grid, block, 0, s>>>(a);
   } else {
     dim3 grid(groups, fy), block(64 * ks);
-    if (ks == 2)
-      bconv_mfma32_kernel<VW, POOL, 1, 2, PD><<<grid, block, 0, s>>>(a);
-    else if (ks == 4)
-      bconv_mfma32_kernel<VW, POOL, 1, 4, PD><<<grid, block, 0, s>>>(a);
-    else
-      bconv_mfma32_kernel<VW, POOL, 1, 8, PD><<<grid, block, 0, s>>>(a);
+    if (tf == 2) {
+      if (ks == 2)
+        bconv_mfma32_kernel<VW, POOL, 2, 2, 2><<<grid, block, 0, s>>>(a);
+      else
+        bconv_mfma32_kernel<VW, POOL, 2, 4, 2><<<grid, block, 0, s>>>(a);
+    } else if (ks == 2) {
+      bconv_mfma32_kernel<VW, POOL, 1, 2, 2><<<grid, block, 0, s>>>(a);
+    } else if (ks == 4) {
+      bconv_mfma32_kernel<VW, POOL, 1, 4, 2><<<grid, block, 0, s>>>(a);
+    } else {
+      bconv_mfma32_kernel<VW, POOL, 1, 8, 2><<<grid, block, 0, s>>>(a);
+    }
   }
   return hipGetLastError();
-}
-
-template <int VW, bool POOL>
-hipError_t launch32_pd(const Mfma32Args& a, int tf, int ks, int pd, hipStream_t s) {
-  return pd == 4 ? launch32<VW, POOL, 4>(a, tf, ks, s) : launch32<VW, POOL, 2>(a, tf, ks, s);
 }
 
 hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint32_t* w,
@@ -439,32 +652,48 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   a.w_bytes = static_cast<int32_t>(static_cast<int64_t>(g.F) * a.fstride * 4);
   a.div_w = make_fastdiv(static_cast<uint32_t>(pool ? g.Wp : g.Wo));
   a.div_h = make_fastdiv(static_cast<uint32_t>(pool ? g.Hp : g.Ho));
-  const int vw = (g.Cw % 4 == 0) ? 2 : 1;
+  // Words per lane, row and iteration: 8-word chunks (128-bit loads) where
+  // the channels allow, which halves the vector-memory instructions per MFMA
+  // (the texture-address unit is the busiest unit of the small grids), but
+  // not when that leaves fewer than 8 iterations to split.
+  const int64_t groups = (a.items + 63) / 64;
+  const int64_t ftiles = (g.F + 31) / 32;
+  int vw = g.Cw % 8 == 0 ? 4 : g.Cw % 4 == 0 ? 2 : 1;
+  if (vw == 4 && g.KH * g.KW * (g.Cw / 8) < 8) vw = 2;
+  vw = env_int("BNN_MFMA_VW", vw);
+  if (vw != 1 && vw != 2 && vw != 4) vw = 1;
+  if (g.Cw % (2 * vw) != 0) vw = g.Cw % 4 == 0 ? 2 : 1;
   const int iters = g.KH * g.KW * (g.Cw / (2 * vw));
 
   // Tile shape and K split: 64-filter wave tiles down to ~1 wave per SIMD
   // (1024 waves), then 32-filter tiles with a K split over up to 4 waves
-  // until there are ~2 waves per SIMD (keeping at least 2 iterations per
-  // wave).  Measured on the layer shapes of both networks: splitting 8 ways
-  // never beat 4 (the LDS reduction then costs more than it hides).
-  const int64_t groups = (a.items + 63) / 64;
-  const int64_t ftiles = (g.F + 31) / 32;
+  // until there are ~1 (8-word chunks) or ~2 (smaller chunks) waves per
+  // SIMD, keeping at least 2 iterations per wave.  Splitting 8 ways never
+  // beat 4 (the LDS reduction then costs more than it hides).  With 2-word
+  // chunks, grids of >= 4096 64-filter tiles stage the weights through LDS
+  // (5-20 % faster there, slower on smaller grids); 8-word chunks without
+  // staging were as fast or faster wherever the channels allow them.  All
+  // measured on every layer shape of the networks here.
   int tf = 2, ks = 1;
   if (g.F % 64 != 0 || groups * (g.F / 64) < 1024) {
     tf = 1;
-    while (ks < 4 && groups * ftiles * ks < 2048 && iters >= 4 * ks) ks *= 2;
+    const int64_t target = vw == 4 ? 1024 : 2048;
+    while (ks < 4 && groups * ftiles * ks < target && iters >= 4 * ks) ks *= 2;
   }
-  // Tuning overrides (filter tiles per wave, K split, prefetch depth).
+  bool lds = vw <= 2 && tf == 2 && groups * (g.F / 64) >= 4096;
+  // Tuning overrides (filter tiles per wave, K split, weights through LDS).
   tf = env_int("BNN_MFMA_TF", tf);
   ks = env_int("BNN_MFMA_KS", ks);
-  if (tf != 1 && tf != 2) tf = 1;
-  if (g.F % (32 * tf) != 0 || (ks > 1 && tf != 1)) tf = 1;
+  lds = env_int("BNN_MFMA_LDS", lds ? 1 : 0) != 0;
   if (ks != 1 && ks != 2 && ks != 4 && ks != 8) ks = 1;
-  int pd = env_int("BNN_MFMA_PD", 2);
-  if (pd != 2 && pd != 4) pd = 2;
+  if (ks > 1 || vw == 4) lds = false;
+  if (tf != 1 && tf != 2) tf = 1;
+  if (g.F % (32 * tf) != 0 || (ks > 4 && tf != 1)) tf = 1;
+  if (vw == 4)
+    return pool ? launch32<4, true>(a, tf, ks, false, s) : launch32<4, false>(a, tf, ks, false, s);
   if (vw == 2)
-    return pool ? launch32_pd<2, true>(a, tf, ks, pd, s) : launch32_pd<2, false>(a, tf, ks, pd, s);
-  return pool ? launch32_pd<1, true>(a, tf, ks, pd, s) : launch32_pd<1, false>(a, tf, ks, pd, s);
+    return pool ? launch32<2, true>(a, tf, ks, lds, s) : launch32<2, false>(a, tf, ks, lds, s);
+  return pool ? launch32<1, true>(a, tf, ks, lds, s) : launch32<1, false>(a, tf, ks, lds, s);
 }
 
 }  // namespace

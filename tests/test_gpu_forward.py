@@ -14,15 +14,16 @@ from paper_1808_00209_amd.device import to_device, upload_network
 pytestmark = pytest.mark.gpu
 
 
-# "auto": default kernels; "valu": vector-ALU kernels only; "pd4": four sets
-# of loads in flight in the matrix-core loop; "nopatch": the thresholded
+# "auto": default kernels; "valu": vector-ALU kernels only; "lds": the
+# matrix-core kernel with weights staged through LDS; "nopatch": the thresholded
 # input packed by bnn_pack_bits and convolved by the generic kernel instead
 # of the fused patch-packing kernel.
-@pytest.fixture(params=["auto", "valu", "pd4", "nopatch"])
+@pytest.fixture(params=["auto", "valu", "lds", "nopatch"])
 def algo(request, monkeypatch):
     monkeypatch.setenv("BNN_ALGO", "valu" if request.param == "valu" else "auto")
-    if request.param == "pd4":
-        monkeypatch.setenv("BNN_MFMA_PD", "4")
+    if request.param == "lds":
+        monkeypatch.setenv("BNN_MFMA_LDS", "1")
+        monkeypatch.setenv("BNN_MFMA_VW", "2")
     if request.param == "nopatch":
         monkeypatch.setenv("BNN_PATCH", "0")
     return request.param

@@ -17,16 +17,18 @@ pytestmark = pytest.mark.gpu
 
 # Kernel families: "auto" takes the fp4 matrix-core kernel wherever the shape
 # allows it (C a multiple of 64, at most 32 taps), "valu" forces the
-# XOR-popcount vector kernels everywhere, "pd4" is "auto" with four sets of
-# loads in flight in the matrix-core loop instead of the shape's default.
-ALGOS = ["auto", "valu", "pd4"]
+# XOR-popcount vector kernels everywhere, "lds" is "auto" with 2-word chunks
+# and the weights staged through LDS wherever no K split is used (by default
+# only large grids do that; small grids with C % 256 == 0 take 8-word chunks).
+ALGOS = ["auto", "valu", "lds"]
 
 
 @pytest.fixture(params=ALGOS)
 def algo(request, monkeypatch):
     monkeypatch.setenv("BNN_ALGO", "valu" if request.param == "valu" else "auto")
-    if request.param == "pd4":
-        monkeypatch.setenv("BNN_MFMA_PD", "4")
+    if request.param == "lds":
+        monkeypatch.setenv("BNN_MFMA_LDS", "1")
+        monkeypatch.setenv("BNN_MFMA_VW", "2")
     return request.param
 
 
