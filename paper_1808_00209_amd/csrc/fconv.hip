@@ -315,21 +315,26 @@ hipError_t run_fconv(const ConvGeom& g, bool pool, const float* in,
 // partial sum is a multiple of 2^-16 below 2^8, so the fp32 sums are exact in
 // any order (other inputs are summed to within about 2^-22 relative per term).
 // Block = 4 waves = an 8 x 32 tile of output pixels (4 x 16 2x2 windows when
-// pooling) x 64 filters; the result layout and epilogue follow the binary
-// matrix-core kernel (lane: one pixel, four filters).
+// pooling) x FG groups of 64 filters; the result layout and epilogue follow
+// the binary matrix-core kernel (lane: one pixel, four filters).  The +-1
+// weight operands of the FG groups are built once per block into LDS by all
+// its threads (their global loads overlap the input tile's), and every wave
+// reads them with one ds_read_b128 per operand; the fp16 halves of each
+// pixel window are built once and reused by every filter group.
 constexpr int kMfTileH = 8;
 constexpr int kMfTileW = 32;
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 
-template <int C, int KH, int KW, bool POOL, bool FULL>
+template <int C, int KH, int KW, bool POOL, bool FULL, int FG>
 __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
   constexpr int K = KH * KW * C;
   constexpr int KC = (K + 31) / 32;  // k-chunks of 32
   constexpr int LW = kMfTileW + KW - 1;
   constexpr int LH = kMfTileH + KH - 1;
   __shared__ float tile[LH * LW * C];
+  __shared__ v8h wop[FG][KC][4][64];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -342,7 +347,35 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
   const int th_ = b % tiles_h;
   const int n = b / tiles_h;
   const int i0 = th_ * kMfTileH, j0 = tw * kMfTileW;
-  const int f0 = blockIdx.y * 64;
+  const int fb = blockIdx.y * 64 * FG;
+
+  // Weight operands: thread t builds, for each group g and k-chunk kc, the
+  // A operand of filter tile tf = t / 64 for lane (q', c') = t % 64: row
+  // filter fb + 64 g + 16 tf + c', the 8 k values 32 kc + 8 q' + e, as +-1
+  // (0 past K or F).
+  {
+    const int tf = threadIdx.x >> 6, qq = (threadIdx.x >> 4) & 3, cc = threadIdx.x & 15;
+#pragma unroll
+    for (int g = 0; g < FG; ++g)
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) {
+      const int f = fb + 64 * g + 16 * tf + cc;
+      v8h op;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int k = 32 * kc + 8 * qq + e;
+        const int tap = k / C, ch = k - (k / C) * C;
+        const bool ok = k < K && (FULL || f < a.F);
+        // unconditional load from a clamped (valid) address, then select
+        const uint32_t word = a.w[static_cast<size_t>(ok ? f : 0) * a.fstride +
+                                  (ok ? tap * a.Cw + (ch >> 5) : 0)];
+        const bool one = (word >> (31 - (ch & 31))) & 1u;
+        op[e] = ok ? (one ? static_cast<_Float16>(1.0f) : static_cast<_Float16>(-1.0f))
+                   : static_cast<_Float16>(0.0f);
+      }
+      wop[g][kc][tf][threadIdx.x & 63] = op;
+    }
+  }
 
   // Stage the input tile (zero outside the image).
   for (int e = threadIdx.x; e < LH * LW * C; e += 256) {
@@ -356,34 +389,17 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
     tile[e] = v;
   }
 
-  // A operands (weights, +-1 in fp16): row = filter f0 + 16 tf + c, the 8
-  // k values 32 kc + 8 q + e of this lane.  Also the LDS offsets of those k
-  // values relative to a pixel's window origin.
-  v8h wa[KC][4];
+  // LDS offset of this lane's 8 k values relative to a pixel's window origin.
   int rel[KC][8];
 #pragma unroll
-  for (int kc = 0; kc < KC; ++kc) {
+  for (int kc = 0; kc < KC; ++kc)
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int k = 32 * kc + 8 * q + e;
       const int tap = k / C, ch = k - (k / C) * C;
       const int kh = tap / KW, kw = tap - (tap / KW) * KW;
-      const bool kin = k < K;
-      rel[kc][e] = kin ? (kh * LW + kw) * C + ch : -1;
-#pragma unroll
-      for (int tf = 0; tf < 4; ++tf) {
-        // Unconditional load from a clamped (valid) address, then select:
-        // no branches around the loads.
-        const int f = f0 + tf * 16 + c;
-        const bool ok = kin && (FULL || f < a.F);
-        const uint32_t word = a.w[static_cast<size_t>(ok ? f : 0) * a.fstride +
-                                  (ok ? tap * a.Cw + (ch >> 5) : 0)];
-        const bool one = (word >> (31 - (ch & 31))) & 1u;
-        wa[kc][tf][e] = ok ? (one ? static_cast<_Float16>(1.0f) : static_cast<_Float16>(-1.0f))
-                           : static_cast<_Float16>(0.0f);
-      }
+      rel[kc][e] = k < K ? (kh * LW + kw) * C + ch : -1;
     }
-  }
   __syncthreads();
 
   // This wave's 4 pixel tiles of 16: position of lane c's pixel in the block tile.
@@ -399,103 +415,116 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
       pc[tp] = 16 * (tp & 1) + c;
     }
   }
-
-  v4f acc[4][4];
-#pragma unroll
-  for (int tf = 0; tf < 4; ++tf)
-#pragma unroll
-    for (int tp = 0; tp < 4; ++tp) acc[tf][tp] = v4f{0.f, 0.f, 0.f, 0.f};
+  // fp16 halves of the 4 pixel windows (B operands), shared by all groups.
+  v8h xh[KC][4], xl[KC][4];
 #pragma unroll
   for (int tp = 0; tp < 4; ++tp) {
     const int pbase = (pr[tp] * LW + pc[tp]) * C;
 #pragma unroll
-    for (int kc = 0; kc < KC; ++kc) {
-      v8h xh, xl;
+    for (int kc = 0; kc < KC; ++kc)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float xv = tile[pbase + max(rel[kc][e], 0)];
         const float x = rel[kc][e] >= 0 ? xv : 0.0f;
         const _Float16 h = static_cast<_Float16>(x);
-        xh[e] = h;
-        xl[e] = static_cast<_Float16>(x - static_cast<float>(h));
+        xh[kc][tp][e] = h;
+        xl[kc][tp][e] = static_cast<_Float16>(x - static_cast<float>(h));
       }
-#pragma unroll
-      for (int tf = 0; tf < 4; ++tf) {
-        acc[tf][tp] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[kc][tf], xh, acc[tf][tp], 0, 0, 0);
-        acc[tf][tp] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[kc][tf], xl, acc[tf][tp], 0, 0, 0);
-      }
-    }
   }
 
-  // Epilogue: lane (q, c) holds pixel c of each tile and filters 16 tf + 4 q + r.
-  const int nf = FULL ? 64 : min(64, a.F - f0);
 #pragma unroll
-  for (int tp = 0; tp < 4; ++tp) {
-    const int i = i0 + pr[tp], j = j0 + pc[tp];
-    const bool pix = i < a.Ho && j < a.Wo;
-    if (a.sums && pix) {
-      float* sp = a.sums + (static_cast<size_t>(n * a.Ho + i) * a.Wo + j) * a.F + f0 + 4 * q;
+  for (int g = 0; g < FG; ++g) {
+    const int f0 = fb + 64 * g;
+    if (!FULL && f0 >= a.F) break;  // block-uniform
+    v4f acc[4][4];
+#pragma unroll
+    for (int tf = 0; tf < 4; ++tf)
+#pragma unroll
+      for (int tp = 0; tp < 4; ++tp) acc[tf][tp] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) {
+      v8h wa[4];
+#pragma unroll
+      for (int tf = 0; tf < 4; ++tf) wa[tf] = wop[g][kc][tf][lane];
 #pragma unroll
       for (int tf = 0; tf < 4; ++tf)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (FULL || tf * 16 + 4 * q + r < nf) sp[tf * 16 + r] = acc[tf][tp][r];
+        for (int tp = 0; tp < 4; ++tp) {
+          acc[tf][tp] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[tf], xh[kc][tp], acc[tf][tp], 0, 0, 0);
+          acc[tf][tp] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[tf], xl[kc][tp], acc[tf][tp], 0, 0, 0);
+        }
     }
-  }
-  if (!a.bits) return;
-  float thf[4][4];
+
+    // Epilogue: lane (q, c) holds pixel c of each tile and filters 16 tf + 4 q + r.
+    const int nf = FULL ? 64 : min(64, a.F - f0);
 #pragma unroll
-  for (int tf = 0; tf < 4; ++tf)
+    for (int tp = 0; tp < 4; ++tp) {
+      const int i = i0 + pr[tp], j = j0 + pc[tp];
+      const bool pix = i < a.Ho && j < a.Wo;
+      if (a.sums && pix) {
+        float* sp = a.sums + (static_cast<size_t>(n * a.Ho + i) * a.Wo + j) * a.F + f0 + 4 * q;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int fl = tf * 16 + 4 * q + r;
-      thf[tf][r] = (FULL || fl < nf) ? static_cast<float>(a.thr[f0 + fl]) : 0.0f;
+        for (int tf = 0; tf < 4; ++tf)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (FULL || tf * 16 + 4 * q + r < nf) sp[tf * 16 + r] = acc[tf][tp][r];
+      }
     }
-  const int w0 = f0 / 32;
-#pragma unroll
-  for (int tp = 0; tp < 4; ++tp) {
-    uint32_t word[2] = {0u, 0u};
+    if (!a.bits) continue;
+    float thf[4][4];
 #pragma unroll
     for (int tf = 0; tf < 4; ++tf)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int fl = tf * 16 + 4 * q + r;
-        const bool on = acc[tf][tp][r] >= thf[tf][r] && (FULL || fl < nf);
-        word[tf >> 1] |= static_cast<uint32_t>(on) << (31 - (16 * (tf & 1) + 4 * q + r));
+        thf[tf][r] = (FULL || fl < nf) ? static_cast<float>(a.thr[f0 + fl]) : 0.0f;
       }
+    const int w0 = f0 / 32;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      word[h] |= __shfl_xor(word[h], 16);
-      word[h] |= __shfl_xor(word[h], 32);
-      if (FULL || w0 + h < a.Fw) {
-        if (a.flip) word[h] ^= a.flip[w0 + h];
-        if (!FULL && w0 + h == a.Fw - 1) word[h] &= tail_mask(a.F);
-      }
-      if constexpr (POOL) {
-        word[h] |= __shfl_xor(word[h], 1);
-        word[h] |= __shfl_xor(word[h], 2);
-      }
-    }
-    const int i = i0 + pr[tp], j = j0 + pc[tp];
-    if constexpr (POOL) {
-      const int ip = i >> 1, jp = j >> 1;
-      if (q == 0 && (c & 3) == 0 && ip < a.Hp && jp < a.Wp) {
-        uint32_t* op = a.bits + (static_cast<size_t>(n * a.Hp + ip) * a.Wp + jp) * a.Fw + w0;
-        if (FULL)
-          *reinterpret_cast<uint2*>(op) = make_uint2(word[0], word[1]);
-        else {
-          op[0] = word[0];
-          if (w0 + 1 < a.Fw) op[1] = word[1];
+    for (int tp = 0; tp < 4; ++tp) {
+      uint32_t word[2] = {0u, 0u};
+#pragma unroll
+      for (int tf = 0; tf < 4; ++tf)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int fl = tf * 16 + 4 * q + r;
+          const bool on = acc[tf][tp][r] >= thf[tf][r] && (FULL || fl < nf);
+          word[tf >> 1] |= static_cast<uint32_t>(on) << (31 - (16 * (tf & 1) + 4 * q + r));
+        }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        word[h] |= __shfl_xor(word[h], 16);
+        word[h] |= __shfl_xor(word[h], 32);
+        if (FULL || w0 + h < a.Fw) {
+          if (a.flip) word[h] ^= a.flip[w0 + h];
+          if (!FULL && w0 + h == a.Fw - 1) word[h] &= tail_mask(a.F);
+        }
+        if constexpr (POOL) {
+          word[h] |= __shfl_xor(word[h], 1);
+          word[h] |= __shfl_xor(word[h], 2);
         }
       }
-    } else {
-      if (q == 0 && i < a.Ho && j < a.Wo) {
-        uint32_t* op = a.bits + (static_cast<size_t>(n * a.Ho + i) * a.Wo + j) * a.Fw + w0;
-        if (FULL)
-          *reinterpret_cast<uint2*>(op) = make_uint2(word[0], word[1]);
-        else {
-          op[0] = word[0];
-          if (w0 + 1 < a.Fw) op[1] = word[1];
+      const int i = i0 + pr[tp], j = j0 + pc[tp];
+      if constexpr (POOL) {
+        const int ip = i >> 1, jp = j >> 1;
+        if (q == 0 && (c & 3) == 0 && ip < a.Hp && jp < a.Wp) {
+          uint32_t* op = a.bits + (static_cast<size_t>(n * a.Hp + ip) * a.Wp + jp) * a.Fw + w0;
+          if (FULL)
+            *reinterpret_cast<uint2*>(op) = make_uint2(word[0], word[1]);
+          else {
+            op[0] = word[0];
+            if (w0 + 1 < a.Fw) op[1] = word[1];
+          }
+        }
+      } else {
+        if (q == 0 && i < a.Ho && j < a.Wo) {
+          uint32_t* op = a.bits + (static_cast<size_t>(n * a.Ho + i) * a.Wo + j) * a.Fw + w0;
+          if (FULL)
+            *reinterpret_cast<uint2*>(op) = make_uint2(word[0], word[1]);
+          else {
+            op[0] = word[0];
+            if (w0 + 1 < a.Fw) op[1] = word[1];
+          }
         }
       }
     }
@@ -531,16 +560,33 @@ hipError_t run_fmfma(const ConvGeom& g, bool pool, const float* in, const uint32
   a.items = 0;
   const unsigned tiles = static_cast<unsigned>(g.N) * ((g.Ho + kMfTileH - 1) / kMfTileH) *
                          ((g.Wo + kMfTileW - 1) / kMfTileW);
-  dim3 grid(tiles, static_cast<unsigned>((g.F + 63) / 64));
+  // Filter groups of 64 per block: 2 (the input tile and the fp16 halves
+  // then serve 128 filters) only for grids that still have >= 4096 waves;
+  // on smaller grids the extra parallelism of one group per block wins.
+  int fg = (g.F >= 128 && static_cast<int64_t>(tiles) * ((g.F + 127) / 128) * 4 >= 4096) ? 2 : 1;
+  const char* e = getenv("BNN_FCONV_FG");
+  if (e) fg = atoi(e) == 2 ? 2 : 1;
   const bool full = g.F % 64 == 0;
-  if (pool && full)
-    fconv_mfma_kernel<C, 3, 3, true, true><<<grid, dim3(256), 0, s>>>(a);
-  else if (pool)
-    fconv_mfma_kernel<C, 3, 3, true, false><<<grid, dim3(256), 0, s>>>(a);
-  else if (full)
-    fconv_mfma_kernel<C, 3, 3, false, true><<<grid, dim3(256), 0, s>>>(a);
-  else
-    fconv_mfma_kernel<C, 3, 3, false, false><<<grid, dim3(256), 0, s>>>(a);
+  dim3 grid(tiles, static_cast<unsigned>((g.F + 64 * fg - 1) / (64 * fg)));
+  if (fg == 2) {
+    if (pool && full)
+      fconv_mfma_kernel<C, 3, 3, true, true, 2><<<grid, dim3(256), 0, s>>>(a);
+    else if (pool)
+      fconv_mfma_kernel<C, 3, 3, true, false, 2><<<grid, dim3(256), 0, s>>>(a);
+    else if (full)
+      fconv_mfma_kernel<C, 3, 3, false, true, 2><<<grid, dim3(256), 0, s>>>(a);
+    else
+      fconv_mfma_kernel<C, 3, 3, false, false, 2><<<grid, dim3(256), 0, s>>>(a);
+  } else {
+    if (pool && full)
+      fconv_mfma_kernel<C, 3, 3, true, true, 1><<<grid, dim3(256), 0, s>>>(a);
+    else if (pool)
+      fconv_mfma_kernel<C, 3, 3, true, false, 1><<<grid, dim3(256), 0, s>>>(a);
+    else if (full)
+      fconv_mfma_kernel<C, 3, 3, false, true, 1><<<grid, dim3(256), 0, s>>>(a);
+    else
+      fconv_mfma_kernel<C, 3, 3, false, false, 1><<<grid, dim3(256), 0, s>>>(a);
+  }
   return hipGetLastError();
 }
 
