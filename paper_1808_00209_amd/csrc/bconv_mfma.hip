@@ -211,10 +211,23 @@ __device__ __forceinline__ void load_act(uint32_t (&aw)[TP][VW], const Mfma32Arg
 }
 
 // Sums, threshold / flip, OR-pool and stores of a wave's TF x TP tiles.
+// The block's thresholds in LDS, staged before the main loop so that their
+// global loads overlap it: thr - 0.5 as fp32 after clamping to [-K-1, K+1]
+// (|S| <= K, so the clamp keeps every comparison, and the values stay exact
+// in fp32 for any int32 threshold): S >= thr  <=>  (thr - 0.5) - S < 0 for
+// integer S.
+template <int TF>
+__device__ __forceinline__ void stage_thresholds(const Mfma32Args& a, int f0, float* thl) {
+  if (a.bits && threadIdx.x < 32 * TF) {
+    const int f = min(f0 + static_cast<int>(threadIdx.x), a.F - 1);
+    thl[threadIdx.x] = static_cast<float>(min(max(a.thr[f], -a.K - 1), a.K + 1)) - 0.5f;
+  }
+}
+
 template <int TF, int TP, bool POOL, int VW>
 __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP],
                                          const PixTiles<TP, POOL, VW>& px, int p0, int f0,
-                                         int h, int c) {
+                                         int h, int c, const float* thl) {
   // Filters past F (a partial last tile) read zero weights through the
   // buffer range and are masked out of every output.
   const bool ftail = f0 + 32 * TF > a.F;
@@ -246,19 +259,12 @@ __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP
     }
   }
   if (a.bits) {
-    // Threshold minus one half: S >= thr  <=>  (thr - 0.5) - S < 0 for
-    // integer S, so the sign bit of that difference is the output bit.
-    // Thresholds are clamped to [-K-1, K+1] first (|S| <= K, so this keeps
-    // every comparison) to stay exact in fp32 for any int32 threshold.
+    // The sign bit of (thr - 0.5) - S is the output bit.
     float th[TF][16];
 #pragma unroll
     for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int f = f0 + tf * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
-        const int t = a.thr[f < a.F ? f : a.F - 1];
-        th[tf][e] = static_cast<float>(min(max(t, -a.K - 1), a.K + 1)) - 0.5f;
-      }
+      for (int e = 0; e < 16; ++e) th[tf][e] = thl[tf * 32 + 8 * (e >> 2) + 4 * h + (e & 3)];
     uint32_t fl[TF], fm[TF];
 #pragma unroll
     for (int tf = 0; tf < TF; ++tf) {
@@ -271,13 +277,19 @@ __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP
       uint32_t word[TF];
 #pragma unroll
       for (int tf = 0; tf < TF; ++tf) {
+        // Filters 8 g + 4 h + r (r = 0..3) of register group g go to bits
+        // 31 - 8 g - 4 h - r: shift the four signs into a nibble (v_alignbit
+        // takes the sign bit of each difference), then place the nibble.
         uint32_t wd = 0u;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float d = th[tf][e] - acc[tf][tp][e];
-          // filter 8 (e/4) + 4 h + e%4 of the word -> bit 31 - that
-          const int pos = 31 - (8 * (e >> 2) + 4 * h + (e & 3));
-          wd |= (__float_as_uint(d) >> 31) << pos;
+        for (int g = 0; g < 4; ++g) {
+          uint32_t nib = 0u;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float d = th[tf][4 * g + r] - acc[tf][tp][4 * g + r];
+            nib = __builtin_amdgcn_alignbit(nib, __float_as_uint(d), 31);
+          }
+          wd |= (nib & 15u) << (28 - 8 * g - 4 * h);
         }
         wd |= __shfl_xor(wd, 32);
         wd = (wd ^ fl[tf]) & fm[tf];
@@ -328,6 +340,10 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
     it0 = min(iters, wave * per);
     it1 = min(iters, it0 + per);
   }
+
+  __shared__ float thl[32 * TF];
+  stage_thresholds<TF>(a, f0, thl);
+  __syncthreads();
 
   PixTiles<TP, POOL, VW> px;
   px.init(a, p0, h, c);
@@ -425,7 +441,7 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[tf][tp][e] = part[0][((tf * TP + tp) * 16 + e) * 64 + lane];
   }
-  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c);
+  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl);
 }
 
 // The same conv with the weights shared through LDS.  The 4 waves of a block
@@ -534,6 +550,8 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
   cur.init(a, 0, iters, nchunk, VW);
   uint32_t xr[2][TP][VW];
 
+  __shared__ float thl[32 * TF];
+  stage_thresholds<TF>(a, f0, thl);
   stage_load(0);
   stage_store(0);
 #pragma unroll
@@ -577,7 +595,7 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
     if (more) stage_store(buf ^ 1);
     __syncthreads();
   }
-  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c);
+  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl);
 }
 
 int env_int(const char* name, int dflt) {
