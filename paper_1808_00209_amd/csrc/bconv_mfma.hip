@@ -55,6 +55,44 @@ __device__ __forceinline__ v8i expand_fp4(uint32_t w, uint32_t smask, uint32_t v
   return x;
 }
 
+// Two words at once: the pair (w1:w0) is shifted as one 64-bit value
+// (v_lshlrev_b64 runs at full rate), 3 shifts + 8 v_and_or_b32 for two words
+// instead of 3 + 3 + 8.  The bits w0 pushes into w1's low end land at
+// positions 0..2, outside the 0x88888888 mask.
+__device__ __forceinline__ uint64_t shl64(uint64_t x, int s) {
+  uint64_t d;
+  asm("v_lshlrev_b64 %0, %1, %2" : "=v"(d) : "i"(s), "v"(x));
+  return d;
+}
+
+__device__ __forceinline__ void expand_pair(uint32_t w0, uint32_t w1, uint32_t smask,
+                                            uint32_t vfill, v8i& x0, v8i& x1) {
+  const uint64_t p = (static_cast<uint64_t>(w1) << 32) | w0;
+  const uint64_t s1 = shl64(p, 1), s2 = shl64(p, 2), s3 = shl64(p, 3);
+  x0[0] = static_cast<int>(and_or(static_cast<uint32_t>(s3), smask, vfill));
+  x0[1] = static_cast<int>(and_or(static_cast<uint32_t>(s2), smask, vfill));
+  x0[2] = static_cast<int>(and_or(static_cast<uint32_t>(s1), smask, vfill));
+  x0[3] = static_cast<int>(and_or(w0, smask, vfill));
+  x1[0] = static_cast<int>(and_or(static_cast<uint32_t>(s3 >> 32), smask, vfill));
+  x1[1] = static_cast<int>(and_or(static_cast<uint32_t>(s2 >> 32), smask, vfill));
+  x1[2] = static_cast<int>(and_or(static_cast<uint32_t>(s1 >> 32), smask, vfill));
+  x1[3] = static_cast<int>(and_or(w1, smask, vfill));
+  x0[4] = x0[5] = x0[6] = x0[7] = 0;
+  x1[4] = x1[5] = x1[6] = x1[7] = 0;
+}
+
+// Expands VW consecutive words (VW = 1, 2 or 4) into VW operands.
+template <int VW>
+__device__ __forceinline__ void expand_words(const uint32_t (&w)[VW], uint32_t smask,
+                                             uint32_t vfill, v8i (&x)[VW]) {
+  if constexpr (VW == 1) {
+    x[0] = expand_fp4(w[0], smask, vfill);
+  } else {
+#pragma unroll
+    for (int v = 0; v < VW; v += 2) expand_pair(w[v], w[v + 1], smask, vfill, x[v], x[v + 1]);
+  }
+}
+
 // Raw buffer loads: an offset at or beyond the buffer's size returns zeros,
 // which is how taps outside the image read the pad word 0 without a branch
 // (every load is unconditional, so the loop can keep loads in flight).
@@ -378,19 +416,28 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
     cur.advance(a, VW);
   };
   auto compute = [&](const uint32_t (&ww)[TF][VW], const uint32_t (&aw)[TP][VW]) {
+    constexpr int VP = VW == 1 ? 1 : 2;  // k-steps expanded together
 #pragma unroll
-    for (int v = 0; v < VW; ++v) {
-      v8i A[TF], B[TP];
+    for (int v0 = 0; v0 < VW; v0 += VP) {
+      v8i A[TF][VP], B[TP][VP];
 #pragma unroll
-      for (int tf = 0; tf < TF; ++tf) A[tf] = expand_fp4(ww[tf][v], smask, vfill);
+      for (int tf = 0; tf < TF; ++tf) {
+        if constexpr (VP == 1) A[tf][0] = expand_fp4(ww[tf][v0], smask, vfill);
+        else expand_pair(ww[tf][v0], ww[tf][v0 + 1], smask, vfill, A[tf][0], A[tf][1]);
+      }
 #pragma unroll
-      for (int tp = 0; tp < TP; ++tp) B[tp] = expand_fp4(aw[tp][v], smask, vfill);
+      for (int tp = 0; tp < TP; ++tp) {
+        if constexpr (VP == 1) B[tp][0] = expand_fp4(aw[tp][v0], smask, vfill);
+        else expand_pair(aw[tp][v0], aw[tp][v0 + 1], smask, vfill, B[tp][0], B[tp][1]);
+      }
 #pragma unroll
-      for (int tf = 0; tf < TF; ++tf)
+      for (int v = 0; v < VP; ++v)
 #pragma unroll
-        for (int tp = 0; tp < TP; ++tp)
-          acc[tf][tp] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-              A[tf], B[tp], acc[tf][tp], 4, 4, 0, 127, 0, 127);
+        for (int tf = 0; tf < TF; ++tf)
+#pragma unroll
+          for (int tp = 0; tp < TP; ++tp)
+            acc[tf][tp] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                A[tf][v], B[tp][v], acc[tf][tp], 4, 4, 0, 127, 0, 127);
     }
   };
 
@@ -536,12 +583,21 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
       if (k >= St::kChunks) continue;
       const int fi = k % (32 * TF), q = k / (32 * TF);
       const int tf = fi >> 5, cr = fi & 31;
+      // word wj of the chunk: lane half hh = wj / VW, k-step v = wj % VW
+      v8i e[2 * VW];
+      if constexpr (VW == 1) {
+        e[0] = expand_fp4(sw[j][0], smask, vfill);
+        e[1] = expand_fp4(sw[j][1], smask, vfill);
+      } else {
+#pragma unroll
+        for (int wj = 0; wj < 2 * VW; wj += 2)
+          expand_pair(sw[j][wj], sw[j][wj + 1], smask, vfill, e[wj], e[wj + 1]);
+      }
 #pragma unroll
       for (int wj = 0; wj < 2 * VW; ++wj) {
-        // word wj of the chunk: lane half hh = wj / VW, k-step v = wj % VW
         const int hh = wj / VW, v = wj % VW;
-        const v8i e = expand_fp4(sw[j][wj], smask, vfill);
-        wlds[buf][((q * VW + v) * TF + tf) * 64 + hh * 32 + cr] = v4i{e[0], e[1], e[2], e[3]};
+        wlds[buf][((q * VW + v) * TF + tf) * 64 + hh * 32 + cr] =
+            v4i{e[wj][0], e[wj][1], e[wj][2], e[wj][3]};
       }
     }
   };
@@ -570,22 +626,23 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
       const int it = s * kQS + q;
       __builtin_amdgcn_sched_barrier(0);
       if (it < iters) {
+        v8i B[TP][VW];
+#pragma unroll
+        for (int tp = 0; tp < TP; ++tp) expand_words<VW>(xr[q & 1][tp], smask, vfill, B[tp]);
 #pragma unroll
         for (int v = 0; v < VW; ++v) {
-          v8i A[TF], B[TP];
+          v8i A[TF];
 #pragma unroll
           for (int tf = 0; tf < TF; ++tf) {
             const v4i t = wlds[buf][((q * VW + v) * TF + tf) * 64 + lane];
             A[tf] = v8i{t[0], t[1], t[2], t[3], 0, 0, 0, 0};
           }
 #pragma unroll
-          for (int tp = 0; tp < TP; ++tp) B[tp] = expand_fp4(xr[q & 1][tp][v], smask, vfill);
-#pragma unroll
           for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
             for (int tp = 0; tp < TP; ++tp)
               acc[tf][tp] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                  A[tf], B[tp], acc[tf][tp], 4, 4, 0, 127, 0, 127);
+                  A[tf], B[tp][v], acc[tf][tp], 4, 4, 0, 127, 0, 127);
         }
       }
       __builtin_amdgcn_sched_barrier(0);
