@@ -298,58 +298,73 @@ struct GemvArgs {
   const uint32_t* flip;
   int32_t* sums;
   uint32_t* bits;
-  int32_t M, N, Kw, K, Nw, kper;
+  int32_t M, N, Kw, K, Nw;
   uint32_t tmask;
 };
 
+// Binary GEMV / small GEMM for M <= 16 rows: a block of 16 waves computes 32
+// output columns, wave w columns 2w and 2w+1.  Its 64 lanes stride along the
+// K words of those two weight rows (coalesced 256-byte reads) and of the M
+// activation rows, XOR + popcount into per-lane counts, and a wave
+// reduction (cross-lane shuffles) gives each column's counts.  They meet in
+// LDS, where the first 32 M threads turn them into sums and threshold bits,
+// packed 32 columns to a word by ballot.
 constexpr int kGemvWaves = 16;
 
-// One output column per lane; the 16 waves of a block split the K words of
-// the same 64 columns, and the per-row activation words are wave-uniform
-// (scalar loads).  Partial counts meet in LDS, then wave m handles row m so
-// that its 64 lanes' threshold bits form two output words by ballot.
 template <int MT>
 __global__ __launch_bounds__(1024) void bgemv_valu_kernel(GemvArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int col0 = blockIdx.x * 64;
-  const int n = col0 + lane;
-  const bool nvalid = n < a.N;
-  const int k0 = wave * a.kper;
-  const int k1 = min(a.Kw, k0 + a.kper);
-  uint32_t acc[MT];
+  const int n0 = blockIdx.x * 32;
+  const int na = n0 + 2 * wave, nb = na + 1;
+  const bool va = na < a.N, vb = nb < a.N;
+  const uint32_t* ra = a.B + static_cast<size_t>(va ? na : 0) * a.Kw;
+  const uint32_t* rb = a.B + static_cast<size_t>(vb ? nb : 0) * a.Kw;
+  uint32_t ca[MT], cb[MT];
 #pragma unroll
-  for (int m = 0; m < MT; ++m) acc[m] = 0;
-  const uint32_t* brow = a.B + static_cast<size_t>(nvalid ? n : 0) * a.Kw;
-  for (int k = k0; k < k1; ++k) {
-    uint32_t b = nvalid ? brow[k] : 0u;
-    const bool last = (k == a.Kw - 1);
-    if (last) b &= a.tmask;
+  for (int m = 0; m < MT; ++m) ca[m] = cb[m] = 0;
+  for (int j = lane; j < a.Kw; j += 64) {
+    const uint32_t mk = (j == a.Kw - 1) ? a.tmask : ~0u;
+    const uint32_t ba = va ? ra[j] : 0u;
+    const uint32_t bb = vb ? rb[j] : 0u;
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       if (m < a.M) {
-        uint32_t av = a.A[static_cast<size_t>(m) * a.Kw + k];
-        if (last) av &= a.tmask;
-        acc[m] += __builtin_popcount(av ^ b);
+        const uint32_t av = a.A[static_cast<size_t>(m) * a.Kw + j];
+        ca[m] += __builtin_popcount((av ^ ba) & mk);
+        cb[m] += __builtin_popcount((av ^ bb) & mk);
       }
     }
   }
-  __shared__ uint32_t part[kGemvWaves][MT][64];
 #pragma unroll
-  for (int m = 0; m < MT; ++m) part[wave][m][lane] = acc[m];
+  for (int m = 0; m < MT; ++m) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      ca[m] += __shfl_xor(ca[m], off);
+      cb[m] += __shfl_xor(cb[m], off);
+    }
+  }
+  __shared__ uint32_t cnt[MT][32];
+  if (lane == 0) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      cnt[m][2 * wave] = ca[m];
+      cnt[m][2 * wave + 1] = cb[m];
+    }
+  }
   __syncthreads();
-  if (wave >= MT || wave >= a.M) return;  // wave-uniform, after the barrier
-  const int m = wave;
-  uint32_t tot = 0;
-#pragma unroll
-  for (int w = 0; w < kGemvWaves; ++w) tot += part[w][m][lane];
-  const int S = a.K - 2 * static_cast<int>(tot);
+  const int t = threadIdx.x;
+  if (t >= 32 * MT || t >= 32 * a.M) return;
+  const int m = t >> 5, k = t & 31, n = n0 + k;
+  const bool nvalid = n < a.N;
+  const int S = a.K - 2 * static_cast<int>(cnt[m][k]);
   if (a.sums && nvalid) a.sums[static_cast<size_t>(m) * a.N + n] = S;
   if (a.bits) {
+    // lanes 0..31 of a wave hold row m's 32 columns, lanes 32..63 row m + 1
     const bool bit = nvalid && S >= a.thr[n];
     const uint64_t mask = __ballot(bit);
-    const int wi = col0 / 32 + (lane >> 5);
-    if ((lane & 31) == 0 && wi < a.Nw) {
+    if (k == 0) {
+      const int wi = n0 / 32;
       uint32_t word = __brev(static_cast<uint32_t>((lane & 32) ? (mask >> 32) : mask));
       if (a.flip) word ^= a.flip[wi];
       if (wi == a.Nw - 1) word &= tail_mask(a.N);
@@ -390,9 +405,8 @@ hipError_t launch_bgemv_valu(int64_t M, int64_t N, int64_t K,
   a.Kw = static_cast<int32_t>(words_of(K));
   a.K = static_cast<int32_t>(K);
   a.Nw = static_cast<int32_t>(words_of(N));
-  a.kper = (a.Kw + kGemvWaves - 1) / kGemvWaves;
   a.tmask = tail_mask(K);
-  dim3 grid(static_cast<unsigned>((N + 63) / 64));
+  dim3 grid(static_cast<unsigned>((N + 31) / 32));
   dim3 block(64 * kGemvWaves);
   if (M <= 1)
     bgemv_valu_kernel<1><<<grid, block, 0, s>>>(a);

@@ -56,8 +56,8 @@ hipError_t launch_bconv_patch(const ConvGeom& g, int mode, const float* x,
                               const int32_t* thr, const uint32_t* flip,
                               int32_t* sums, uint32_t* bits, hipStream_t s);
 
-// Binary GEMM for a handful of rows (M <= 16): one output column per lane,
-// the K words split over the waves of a block.
+// Binary GEMM for a handful of rows (M <= 16): a wave per two output
+// columns, its lanes along K, a block per 32 columns.
 hipError_t launch_bgemv_valu(int64_t M, int64_t N, int64_t K,
                              const uint32_t* A, const uint32_t* B,
                              const int32_t* thr, const uint32_t* flip,
