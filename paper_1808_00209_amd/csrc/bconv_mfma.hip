@@ -249,23 +249,39 @@ __device__ __forceinline__ void load_act(uint32_t (&aw)[TP][VW], const Mfma32Arg
 }
 
 // Sums, threshold / flip, OR-pool and stores of a wave's TF x TP tiles.
-// The block's thresholds in LDS, staged before the main loop so that their
-// global loads overlap it: thr - 0.5 as fp32 after clamping to [-K-1, K+1]
-// (|S| <= K, so the clamp keeps every comparison, and the values stay exact
-// in fp32 for any int32 threshold): S >= thr  <=>  (thr - 0.5) - S < 0 for
-// integer S.
+// The thresholds and flip words are fetched at kernel start (EpiParams::
+// fetch), so their global loads overlap the main loop instead of delaying its
+// first loads or the epilogue; the block's thresholds then meet in LDS right
+// before the epilogue.  Each is kept as thr - 0.5 in fp32 after clamping to
+// [-K-1, K+1] (|S| <= K, so the clamp keeps every comparison, and the values
+// stay exact in fp32 for any int32 threshold): S >= thr  <=>  (thr - 0.5) - S
+// < 0 for integer S.
 template <int TF>
-__device__ __forceinline__ void stage_thresholds(const Mfma32Args& a, int f0, float* thl) {
-  if (a.bits && threadIdx.x < 32 * TF) {
-    const int f = min(f0 + static_cast<int>(threadIdx.x), a.F - 1);
-    thl[threadIdx.x] = static_cast<float>(min(max(a.thr[f], -a.K - 1), a.K + 1)) - 0.5f;
+struct EpiParams {
+  int32_t thr;       // this thread's filter's threshold (threads < 32 TF)
+  uint32_t fl[TF];   // flip words of the TF filter tiles (wave-uniform)
+
+  __device__ __forceinline__ void fetch(const Mfma32Args& a, int f0) {
+    thr = 0;
+    if (a.bits && threadIdx.x < 32 * TF) thr = a.thr[min(f0 + static_cast<int>(threadIdx.x), a.F - 1)];
+#pragma unroll
+    for (int tf = 0; tf < TF; ++tf) {
+      const int wi = f0 / 32 + tf;
+      fl[tf] = a.flip ? a.flip[wi < a.Fw ? wi : a.Fw - 1] : 0u;
+    }
   }
-}
+  // Writes the block's thresholds to LDS; a barrier must follow.
+  __device__ __forceinline__ void stage(const Mfma32Args& a, float* thl) const {
+    if (a.bits && threadIdx.x < 32 * TF)
+      thl[threadIdx.x] = static_cast<float>(min(max(thr, -a.K - 1), a.K + 1)) - 0.5f;
+  }
+};
 
 template <int TF, int TP, bool POOL, int VW>
 __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP],
                                          const PixTiles<TP, POOL, VW>& px, int p0, int f0,
-                                         int h, int c, const float* thl) {
+                                         int h, int c, const float* thl,
+                                         const EpiParams<TF>& ep) {
   // Filters past F (a partial last tile) read zero weights through the
   // buffer range and are masked out of every output.
   const bool ftail = f0 + 32 * TF > a.F;
@@ -303,13 +319,9 @@ __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP
     for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
       for (int e = 0; e < 16; ++e) th[tf][e] = thl[tf * 32 + 8 * (e >> 2) + 4 * h + (e & 3)];
-    uint32_t fl[TF], fm[TF];
+    uint32_t fm[TF];
 #pragma unroll
-    for (int tf = 0; tf < TF; ++tf) {
-      const int wi = f0 / 32 + tf;
-      fl[tf] = a.flip ? a.flip[wi < a.Fw ? wi : a.Fw - 1] : 0u;
-      fm[tf] = wi == a.Fw - 1 ? tail_mask(a.F) : ~0u;
-    }
+    for (int tf = 0; tf < TF; ++tf) fm[tf] = f0 / 32 + tf == a.Fw - 1 ? tail_mask(a.F) : ~0u;
 #pragma unroll
     for (int tp = 0; tp < TP; ++tp) {
       uint32_t word[TF];
@@ -330,7 +342,7 @@ __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP
           wd |= (nib & 15u) << (28 - 8 * g - 4 * h);
         }
         wd |= __shfl_xor(wd, 32);
-        wd = (wd ^ fl[tf]) & fm[tf];
+        wd = (wd ^ ep.fl[tf]) & fm[tf];
         if constexpr (POOL) {
           wd |= __shfl_xor(wd, 1);
           wd |= __shfl_xor(wd, 2);
@@ -379,9 +391,8 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
     it1 = min(iters, it0 + per);
   }
 
-  __shared__ float thl[32 * TF];
-  stage_thresholds<TF>(a, f0, thl);
-  __syncthreads();
+  EpiParams<TF> ep;
+  ep.fetch(a, f0);
 
   PixTiles<TP, POOL, VW> px;
   px.init(a, p0, h, c);
@@ -460,12 +471,17 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
     }
   }
 
-  if constexpr (KS > 1) {
+  __shared__ float thl[32 * TF];
+  if constexpr (KS == 1) {
+    ep.stage(a, thl);
+    __syncthreads();
+  } else {
     // Partial sums of the KS waves meet in LDS: every wave stores its tile
     // in its own slot, all threads of the block add the slots slice by slice
     // into slot 0, and wave 0 takes the totals for the epilogue.
     constexpr int NV = TF * TP * 16 * 64;  // values per wave
     __shared__ float part[KS][NV];
+    ep.stage(a, thl);
 #pragma unroll
     for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
@@ -488,7 +504,7 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[tf][tp][e] = part[0][((tf * TP + tp) * 16 + e) * 64 + lane];
   }
-  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl);
+  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, ep);
 }
 
 // The same conv with the weights shared through LDS.  The 4 waves of a block
@@ -606,8 +622,9 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
   cur.init(a, 0, iters, nchunk, VW);
   uint32_t xr[2][TP][VW];
 
+  EpiParams<TF> ep;
+  ep.fetch(a, f0);
   __shared__ float thl[32 * TF];
-  stage_thresholds<TF>(a, f0, thl);
   stage_load(0);
   stage_store(0);
 #pragma unroll
@@ -650,9 +667,10 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
       cur.advance(a, VW);
     }
     if (more) stage_store(buf ^ 1);
+    else ep.stage(a, thl);
     __syncthreads();
   }
-  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl);
+  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, ep);
 }
 
 int env_int(const char* name, int dflt) {

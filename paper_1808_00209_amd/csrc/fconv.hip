@@ -377,6 +377,19 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
     }
   }
 
+  // The block's thresholds and flip words go to LDS with the input tile, so
+  // their loads overlap it rather than following the MFMAs.
+  __shared__ float thl[FG * 64];
+  __shared__ uint32_t fll[FG * 2];
+  if (a.bits && threadIdx.x < FG * 64) {
+    const int f = fb + static_cast<int>(threadIdx.x);
+    thl[threadIdx.x] = (FULL || f < a.F) ? static_cast<float>(a.thr[f]) : 0.0f;
+  }
+  if (threadIdx.x < FG * 2) {
+    const int wi = fb / 32 + static_cast<int>(threadIdx.x);
+    fll[threadIdx.x] = (a.flip && wi < a.Fw) ? a.flip[wi] : 0u;
+  }
+
   // Stage the input tile (zero outside the image).
   for (int e = threadIdx.x; e < LH * LW * C; e += 256) {
     const int ch = e % C;
@@ -477,7 +490,7 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int fl = tf * 16 + 4 * q + r;
-        thf[tf][r] = (FULL || fl < nf) ? static_cast<float>(a.thr[f0 + fl]) : 0.0f;
+        thf[tf][r] = thl[64 * g + fl];
       }
     const int w0 = f0 / 32;
 #pragma unroll
@@ -496,7 +509,7 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
         word[h] |= __shfl_xor(word[h], 16);
         word[h] |= __shfl_xor(word[h], 32);
         if (FULL || w0 + h < a.Fw) {
-          if (a.flip) word[h] ^= a.flip[w0 + h];
+          word[h] ^= fll[2 * g + h];
           if (!FULL && w0 + h == a.Fw - 1) word[h] &= tail_mask(a.F);
         }
         if constexpr (POOL) {
