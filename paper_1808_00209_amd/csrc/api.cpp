@@ -397,6 +397,31 @@ bnn_status plan_chain(const bnn_layer* L, int32_t n, int32_t batch, int32_t H,
   return BNN_OK;
 }
 
+// Length of the run of FC layers starting at layer li that bnn_forward sends
+// to the chained FC kernel (1: none).  Every layer in the run has at most
+// kChainWords weight words (each block of the chained kernel reads all of
+// them), the batch is at most 128 rows (beyond that the per-layer kernels
+// have parallelism enough to hide their launches), and BNN_FC_CHAIN=0 keeps
+// one launch per layer.
+int fc_chain_run(const bnn_layer* L, int32_t li, int32_t n, int32_t batch) {
+  constexpr int64_t kChainWords = 8192;
+  const char* e = getenv("BNN_FC_CHAIN");
+  if ((e && strcmp(e, "0") == 0) || batch > 128) return 1;
+  int run = 0;
+  bnn::FcChainLayer fl[bnn::kFcChainMax];
+  while (li + run < n && run < bnn::kFcChainMax) {
+    const bnn_layer& q = L[li + run];
+    if (q.kind != BNN_LAYER_BFC && q.kind != BNN_LAYER_BFC_LOGITS) break;
+    if (int64_t{q.N} * bnn::words_of(q.K) > kChainWords || !aligned16(q.w)) break;
+    const bool lg = q.kind == BNN_LAYER_BFC_LOGITS;
+    fl[run] = bnn::FcChainLayer{q.w, lg ? nullptr : q.thr, lg ? nullptr : q.flip, q.K, q.N};
+    ++run;
+    if (lg) break;
+  }
+  while (run > 1 && !bnn::bfc_chain_supported(fl, run)) --run;
+  return run > 1 ? run : 1;
+}
+
 }  // namespace
 
 bnn_status bnn_forward_workspace_size(const bnn_layer* layers, int32_t n_layers,
@@ -487,6 +512,25 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
           break;
         }
         case BNN_LAYER_BFC: {
+          // A run of small FC layers from here on goes to one chained kernel.
+          const int run = fc_chain_run(layers, li, n_layers, batch);
+          if (run > 1) {
+            bnn::FcChainLayer fl[bnn::kFcChainMax];
+            for (int i = 0; i < run; ++i) {
+              const bnn_layer& q = layers[li + i];
+              const bool lg = q.kind == BNN_LAYER_BFC_LOGITS;
+              fl[i] = bnn::FcChainLayer{q.w, lg ? nullptr : q.thr, lg ? nullptr : q.flip, q.K, q.N};
+            }
+            const bool to_logits = layers[li + run - 1].kind == BNN_LAYER_BFC_LOGITS;
+            e = bnn::launch_bfc_chain(fl, run, batch, src, to_logits ? nullptr : dst,
+                                      to_logits ? logits : nullptr, stream);
+            if (e != hipSuccess) return fail(BNN_ERR_HIP, "forward: layers %d-%d launch: %s", li,
+                                             li + run - 1, hipGetErrorString(e));
+            h = w = 1;
+            c = layers[li + run - 1].N;
+            li += run - 1;  // the run's last layer; its output is in dst
+            break;
+          }
           st = gemm_launch(batch, l.N, l.K, src, l.w, l.thr, l.flip, nullptr, dst, stream);
           if (st != BNN_OK) return fail(st, "forward: layer %d: %s", li, g_err);
           h = w = 1;

@@ -69,4 +69,23 @@ hipError_t launch_fconv_binw(const ConvGeom& g, const float* in,
                              const uint32_t* flip, float* sums,
                              uint32_t* bits, hipStream_t s);
 
+// A run of consecutive binary FC layers in one launch (bfc_chain.hip): every
+// block takes R rows through all of them with the intermediate bits in LDS.
+// Layer i has K_i input bits and N_i outputs; K_{i+1} = N_i; every layer but
+// the last needs thr (its bits feed the next one); the last writes either
+// packed bits [M][ceil(N/32)] (out_bits, with thr) or int32 sums [M][N]
+// (out_sums).  Supported while every layer input is at most 1024 words.
+// Weights must be 16-byte aligned.
+constexpr int kFcChainMax = 4;
+struct FcChainLayer {
+  const uint32_t* w;     // [N][ceil(K/32)]
+  const int32_t* thr;    // [N] or null
+  const uint32_t* flip;  // [ceil(N/32)] or null
+  int32_t K, N;
+};
+bool bfc_chain_supported(const FcChainLayer* layers, int n);
+hipError_t launch_bfc_chain(const FcChainLayer* layers, int n, int64_t M,
+                            const uint32_t* in, uint32_t* out_bits,
+                            int32_t* out_sums, hipStream_t s);
+
 }  // namespace bnn

@@ -1,0 +1,58 @@
+"""GPU parity of the chained FC kernel (a run of small binary FC layers in
+one launch inside bnn_forward) against the per-layer launches and the oracle.
+
+The FC stacks sit behind a real-valued first layer on a 1 x 1 image (3x3
+kernel, pad 1), whose F outputs are the first FC layer's K input bits, so any
+K can be tried: word tails (K, N not multiples of 32), 4-word chunks and
+single words, runs longer than the kernel's limit of 4 layers (split into two
+runs), a layer too large to chain, and batches on both sides of the 64- and
+128-row limits."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1808_00209_amd import bnn, synth
+from paper_1808_00209_amd.device import to_device, upload_network
+
+pytestmark = pytest.mark.gpu
+
+STACKS = {
+    "cifar_tail": (1024, [1024, 10]),
+    "paper_tail": (2048, [100, 100, 4]),
+    "ragged": (96, [257, 33, 7]),
+    "tail_words": (1000, [1000, 10]),
+    "four_then_two": (512, [64, 64, 64, 64, 64, 10]),
+    "one_big_layer": (4096, [5000, 3]),
+}
+
+
+def _net(name):
+    K0, sizes = STACKS[name]
+    layers = [synth.conv_layer(8, 0, "fconv", 3, K0)]
+    k = K0
+    for i, n in enumerate(sizes):
+        layers.append(synth.fc_layer(8, i + 1, k, n, logits=(i == len(sizes) - 1)))
+        k = n
+    return layers
+
+
+def _run(net, xd, monkeypatch, chain):
+    monkeypatch.setenv("BNN_FC_CHAIN", "1" if chain else "0")
+    out = bnn.bnn_forward(net, xd)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+@pytest.mark.parametrize("name", sorted(STACKS))
+@pytest.mark.parametrize("batch", [1, 3, 64, 65, 128, 129])
+def test_fc_chain_matches_per_layer_and_oracle(name, batch, monkeypatch):
+    layers = _net(name)
+    x = synth.dyadic_normal(synth.rng(8, 90, synth.T_X), (batch, 1, 1, 3))
+    net = upload_network(layers, 1, 1, 3)
+    xd = to_device(x)
+    got = _run(net, xd, monkeypatch, True)
+    ref = _run(net, xd, monkeypatch, False)
+    assert np.array_equal(got, ref)
+    pick = sorted({0, batch // 2, batch - 1})
+    assert np.array_equal(got[pick], oracle.forward(layers, x[pick]))

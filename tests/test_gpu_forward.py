@@ -17,10 +17,13 @@ pytestmark = pytest.mark.gpu
 # "auto": default kernels; "valu": vector-ALU kernels only; "lds": the
 # matrix-core kernel with weights staged through LDS; "nopatch": the thresholded
 # input packed by bnn_pack_bits and convolved by the generic kernel instead
-# of the fused patch-packing kernel.
-@pytest.fixture(params=["auto", "valu", "lds", "nopatch"])
+# of the fused patch-packing kernel; "nochain": every FC layer as its own
+# launch instead of runs of small FC layers in the chained kernel.
+@pytest.fixture(params=["auto", "valu", "lds", "nopatch", "nochain"])
 def algo(request, monkeypatch):
     monkeypatch.setenv("BNN_ALGO", "valu" if request.param == "valu" else "auto")
+    if request.param == "nochain":
+        monkeypatch.setenv("BNN_FC_CHAIN", "0")
     if request.param == "lds":
         monkeypatch.setenv("BNN_MFMA_LDS", "1")
         monkeypatch.setenv("BNN_MFMA_VW", "2")
