@@ -372,8 +372,15 @@ __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP
 //        iterations of one tile and add their partial sums in LDS (grids too
 //        small to fill the chip).
 //   PD   register sets of loads in flight (prefetch depth).
+//   LATE (KS = 1) the block's thresholds meet in LDS after the main loop, so
+//        their load latency overlaps it; this costs a block barrier between
+//        the loop and the epilogue, which pays on grids of at most about two
+//        waves per SIMD but not on larger ones, where a wave's epilogue
+//        otherwise overlaps the other waves' loops (then they are staged at
+//        kernel start).  With KS > 1 they always meet after the loop, at the
+//        barrier the partial sums need anyway.
 // Each wave loads and expands its own weight words in registers.
-template <int VW, bool POOL, int TF, int KS, int PD>
+template <int VW, bool POOL, int TF, int KS, int PD, bool LATE>
 __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(Mfma32Args a) {
   constexpr int TP = 2;
   const int lane = threadIdx.x & 63;
@@ -391,8 +398,13 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
     it1 = min(iters, it0 + per);
   }
 
+  __shared__ float thl[32 * TF];
   EpiParams<TF> ep;
   ep.fetch(a, f0);
+  if constexpr (KS == 1 && !LATE) {
+    ep.stage(a, thl);
+    __syncthreads();
+  }
 
   PixTiles<TP, POOL, VW> px;
   px.init(a, p0, h, c);
@@ -471,10 +483,11 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
     }
   }
 
-  __shared__ float thl[32 * TF];
   if constexpr (KS == 1) {
-    ep.stage(a, thl);
-    __syncthreads();
+    if constexpr (LATE) {
+      ep.stage(a, thl);
+      __syncthreads();
+    }
   } else {
     // Partial sums of the KS waves meet in LDS: every wave stores its tile
     // in its own slot, all threads of the block add the slots slice by slice
@@ -622,9 +635,12 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
   cur.init(a, 0, iters, nchunk, VW);
   uint32_t xr[2][TP][VW];
 
+  // Thresholds staged at kernel start (the barrier after the first weight
+  // stage covers them), so no threshold register stays live in the loop.
   EpiParams<TF> ep;
   ep.fetch(a, f0);
   __shared__ float thl[32 * TF];
+  ep.stage(a, thl);
   stage_load(0);
   stage_store(0);
 #pragma unroll
@@ -667,7 +683,6 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
       cur.advance(a, VW);
     }
     if (more) stage_store(buf ^ 1);
-    else ep.stage(a, thl);
     __syncthreads();
   }
   epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, ep);
@@ -679,7 +694,7 @@ int env_int(const char* name, int dflt) {
 }
 
 template <int VW, bool POOL>
-hipError_t launch32(const Mfma32Args& a, int tf, int ks, bool lds, hipStream_t s) {
+hipError_t launch32(const Mfma32Args& a, int tf, int ks, bool lds, bool late, hipStream_t s) {
   const unsigned fy = static_cast<unsigned>((a.F + 32 * tf - 1) / (32 * tf));
   const unsigned groups = static_cast<unsigned>((a.items + 63) / 64);
   if constexpr (VW <= 2) {
@@ -694,23 +709,27 @@ hipError_t launch32(const Mfma32Args& a, int tf, int ks, bool lds, hipStream_t s
   }
   if (ks == 1) {
     dim3 grid((groups + 3) / 4, fy), block(256);
-    if (tf == 2)
-      bconv_mfma32_kernel<VW, POOL, 2, 1, 2><<<grid, block, 0, s>>>(a);
+    if (tf == 2 && late)
+      bconv_mfma32_kernel<VW, POOL, 2, 1, 2, true><<<grid, block, 0, s>>>(a);
+    else if (tf == 2)
+      bconv_mfma32_kernel<VW, POOL, 2, 1, 2, false><<<grid, block, 0, s>>>(a);
+    else if (late)
+      bconv_mfma32_kernel<VW, POOL, 1, 1, 2, true><<<grid, block, 0, s>>>(a);
     else
-      bconv_mfma32_kernel<VW, POOL, 1, 1, 2><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 1, 2, false><<<grid, block, 0, s>>>(a);
   } else {
     dim3 grid(groups, fy), block(64 * ks);
     if (tf == 2) {
       if (ks == 2)
-        bconv_mfma32_kernel<VW, POOL, 2, 2, 2><<<grid, block, 0, s>>>(a);
+        bconv_mfma32_kernel<VW, POOL, 2, 2, 2, true><<<grid, block, 0, s>>>(a);
       else
-        bconv_mfma32_kernel<VW, POOL, 2, 4, 2><<<grid, block, 0, s>>>(a);
+        bconv_mfma32_kernel<VW, POOL, 2, 4, 2, true><<<grid, block, 0, s>>>(a);
     } else if (ks == 2) {
-      bconv_mfma32_kernel<VW, POOL, 1, 2, 2><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 2, 2, true><<<grid, block, 0, s>>>(a);
     } else if (ks == 4) {
-      bconv_mfma32_kernel<VW, POOL, 1, 4, 2><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 4, 2, true><<<grid, block, 0, s>>>(a);
     } else {
-      bconv_mfma32_kernel<VW, POOL, 1, 8, 2><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 8, 2, true><<<grid, block, 0, s>>>(a);
     }
   }
   return hipGetLastError();
@@ -782,11 +801,19 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   if (ks > 1 || vw == 4) lds = false;
   if (tf != 1 && tf != 2) tf = 1;
   if (g.F % (32 * tf) != 0 || (ks > 4 && tf != 1)) tf = 1;
+  // Thresholds staged after the main loop on grids of at most 2 waves per
+  // SIMD (2048 waves), at kernel start on larger ones (BNN_MFMA_LATE
+  // overrides).
+  const int64_t waves = (groups + 3) / 4 * 4 * ((g.F + 32 * tf - 1) / (32 * tf));
+  const bool late = env_int("BNN_MFMA_LATE", waves <= 2048 ? 1 : 0) != 0;
   if (vw == 4)
-    return pool ? launch32<4, true>(a, tf, ks, false, s) : launch32<4, false>(a, tf, ks, false, s);
+    return pool ? launch32<4, true>(a, tf, ks, false, late, s)
+                : launch32<4, false>(a, tf, ks, false, late, s);
   if (vw == 2)
-    return pool ? launch32<2, true>(a, tf, ks, lds, s) : launch32<2, false>(a, tf, ks, lds, s);
-  return pool ? launch32<1, true>(a, tf, ks, lds, s) : launch32<1, false>(a, tf, ks, lds, s);
+    return pool ? launch32<2, true>(a, tf, ks, lds, late, s)
+                : launch32<2, false>(a, tf, ks, lds, late, s);
+  return pool ? launch32<1, true>(a, tf, ks, lds, late, s)
+              : launch32<1, false>(a, tf, ks, lds, late, s);
 }
 
 }  // namespace

@@ -19,8 +19,10 @@ pytestmark = pytest.mark.gpu
 # allows it (C a multiple of 64, at most 32 taps), "valu" forces the
 # XOR-popcount vector kernels everywhere, "lds" is "auto" with 2-word chunks
 # and the weights staged through LDS wherever no K split is used (by default
-# only large grids do that; small grids with C % 256 == 0 take 8-word chunks).
-ALGOS = ["auto", "valu", "lds"]
+# only large grids do that; small grids with C % 256 == 0 take 8-word chunks),
+# "early" is "auto" with the thresholds staged at kernel start (by default
+# only grids of more than 2 waves per SIMD do that).
+ALGOS = ["auto", "valu", "lds", "early"]
 
 
 @pytest.fixture(params=ALGOS)
@@ -29,6 +31,8 @@ def algo(request, monkeypatch):
     if request.param == "lds":
         monkeypatch.setenv("BNN_MFMA_LDS", "1")
         monkeypatch.setenv("BNN_MFMA_VW", "2")
+    if request.param == "early":
+        monkeypatch.setenv("BNN_MFMA_LATE", "0")
     return request.param
 
 
