@@ -139,13 +139,56 @@ __global__ __launch_bounds__(256) void bconv_patch_kernel(PatchArgs a) {
   const int n = b / a.tiles_y;
   const int i0 = by * kTH, j0 = bx * kTW;
 
-  // Binarize the input tile plus halo.
+  // Filter round f0 .. f0 + nf - 1 as patch words and biases in LDS (thread
+  // t takes filter f0 + t).
+  auto stage_filters = [&](int f0, int nf) {
+    uint32_t wp[PW];
+#pragma unroll
+    for (int q = 0; q < PW; ++q) wp[q] = 0;
+    int32_t bias = 0;
+    if (t < nf) {
+      const int f = f0 + t;
+      const uint32_t* wf = a.w + static_cast<size_t>(f) * a.KH * a.KW;  // one word per tap
+      uint64_t hi = 0, lo = 0;
+      for (int s = 0; s < a.KH * a.KW; ++s) {
+        const uint32_t code = wf[s] >> (32 - C);
+        if constexpr (PW == 1)
+          wp[0] |= code << (32 - (s + 1) * C);
+        else
+          put_bits(hi, lo, code, s * C, C);
+      }
+      if constexpr (PW > 1) split_words(wp, hi, lo);
+      if constexpr (BITS) {
+        // q = floor((K - thr) / 2), clamped to [-1, K]
+        const int64_t d = static_cast<int64_t>(a.P) - a.thr[f];
+        int64_t q = d >= 0 ? d / 2 : -((1 - d) / 2);
+        q = q < -1 ? -1 : (q > a.P ? a.P : q);
+        bias = static_cast<int32_t>(-q - 1);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < PW; ++q) wpat[t * PW + q] = wp[q];
+    wbias[t] = bias;
+  };
+
+  // Binarize the input tile plus halo, and stage the first filter round.
+  // With at most 64 filters, wave 0 stages them while waves 1-3 binarize the
+  // tile, so the two chains of global loads overlap.
   const int TR = kTH + a.KH - 1, TC = kTW + a.KW - 1;
-  for (int e = t; e < TR * TC; e += 256) {
-    const int r = e / TC, cc = e - r * TC;
-    const int gi = i0 - a.pad + r, gj = j0 - a.pad + cc;
-    tile[e] = (gi >= 0 && gi < a.in.H && gj >= 0 && gj < a.in.W) ? pixel_code(a.in, n, gi, gj)
-                                                                 : 0u;
+  const int nf0 = min(kFB, a.F);
+  const bool split = nf0 <= 64;
+  if (split && t < 64) {
+    stage_filters(0, nf0);
+  } else {
+    const int e0 = split ? t - 64 : t, step = split ? 192 : 256;
+    for (int e = e0; e < TR * TC; e += step) {
+      const int r = e / TC, cc = e - r * TC;
+      const int gi = i0 - a.pad + r, gj = j0 - a.pad + cc;
+      tile[e] = (gi >= 0 && gi < a.in.H && gj >= 0 && gj < a.in.W)
+                    ? pixel_code(a.in, n, gi, gj)
+                    : 0u;
+    }
+    if (!split) stage_filters(0, nf0);
   }
 
   // This thread's output pixel; with pooling, lanes 4q..4q+3 are one window.
@@ -185,38 +228,11 @@ __global__ __launch_bounds__(256) void bconv_patch_kernel(PatchArgs a) {
   const int Hp = POOL ? a.Ho / 2 : a.Ho;
   for (int f0 = 0; f0 < a.F; f0 += kFB) {
     const int nf = min(kFB, a.F - f0);
-    __syncthreads();  // the previous round's filters are no longer read
-    {
-      uint32_t wp[PW];
-#pragma unroll
-      for (int q = 0; q < PW; ++q) wp[q] = 0;
-      int32_t bias = 0;
-      if (t < nf) {
-        const int f = f0 + t;
-        const uint32_t* wf = a.w + static_cast<size_t>(f) * a.KH * a.KW;  // one word per tap
-        uint64_t hi = 0, lo = 0;
-        for (int s = 0; s < a.KH * a.KW; ++s) {
-          const uint32_t code = wf[s] >> (32 - C);
-          if constexpr (PW == 1)
-            wp[0] |= code << (32 - (s + 1) * C);
-          else
-            put_bits(hi, lo, code, s * C, C);
-        }
-        if constexpr (PW > 1) split_words(wp, hi, lo);
-        if constexpr (BITS) {
-          // q = floor((K - thr) / 2), clamped to [-1, K]
-          const int64_t d = static_cast<int64_t>(a.P) - a.thr[f];
-          int64_t q = d >= 0 ? d / 2 : -((1 - d) / 2);
-          q = q < -1 ? -1 : (q > a.P ? a.P : q);
-          bias = static_cast<int32_t>(-q - 1);
-        }
-      }
-#pragma unroll
-      for (int q = 0; q < PW; ++q) wpat[t * PW + q] = wp[q];
-      wbias[t] = bias;
+    if (f0 > 0) {
+      __syncthreads();  // the previous round's filters are no longer read
+      stage_filters(f0, nf);
+      __syncthreads();
     }
-    __syncthreads();
-
     for (int g = 0; g < nf; g += 32) {
       const int fw = (f0 + g) >> 5;
       if constexpr (SUMS) {
