@@ -266,10 +266,16 @@ bnn_status bnn_forward_workspace_size(const bnn_layer* layers,
 /*
  * Run the chain on input [batch][H][W][C] fp32 and write int32 logits
  * [batch][N_last] (Table I/II: conv, pool, ..., FC layers).  One kernel per
- * layer on `stream`, except that an input layer followed by a BCONV whose
- * window fits bnn_bconv2d_input runs as that one kernel; workspace (device, >= the size above, 256-byte aligned)
- * holds the intermediate bits.  Errors: as the per-layer calls, plus
- * BNN_ERR_WORKSPACE.
+ * layer on `stream`, with two exceptions:
+ *  - an input layer followed by a BCONV whose window fits
+ *    bnn_bconv2d_input runs as that one kernel (environment BNN_PATCH=0
+ *    keeps them apart);
+ *  - a run of 2-4 consecutive FC layers of at most 8192 weight words each,
+ *    at batch <= 128, runs as one kernel that keeps the intermediate bits of
+ *    each row in LDS (environment BNN_FC_CHAIN=0 launches them one by one).
+ * The results are the same either way.  workspace (device, >= the size
+ * above, 256-byte aligned) holds the intermediate bits.  Errors: as the
+ * per-layer calls, plus BNN_ERR_WORKSPACE.
  */
 bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers,
                        int32_t batch, int32_t H, int32_t W, int32_t C,
