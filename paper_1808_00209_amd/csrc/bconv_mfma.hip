@@ -157,7 +157,34 @@ struct Mfma32Args {
   int32_t in_bytes;  // raw-buffer ranges
   int32_t w_bytes;
   FastDiv div_w, div_h;  // Wo, Ho (or Wp, Hp when pooling)
+  int32_t pblocks;   // workgroups along the pixels
+  int32_t xcd_map;   // 1: one-dimensional grid in the XCD order of block_tile
+  FastDiv div_f;     // filter tiles along the filters
 };
+
+// The workgroup's pixel block and filter tile.  The workgroups of a launch
+// are handed to the 8 XCDs in turn (workgroup b to XCD b mod 8), and each
+// XCD has its own L2.  In the XCD order, the k-th workgroup of XCD x takes
+// filter tile k mod fy of pixel block 8 (k div fy) + x: the fy filter tiles
+// of a pixel block run one after another on one XCD, so its activations are
+// fetched into one L2, and each output row (one piece per filter tile) is
+// complete in that L2 before it is written back.  Otherwise (a 2-D grid,
+// pixel blocks varying fastest) a row's pieces come from workgroups far
+// apart in time on all 8 XCDs and are written back piece by piece.  Returns
+// false for the padding workgroups past the last pixel block.
+__device__ __forceinline__ bool block_tile(const Mfma32Args& a, int& pb, int& ft) {
+  if (a.xcd_map) {
+    const uint32_t b = blockIdx.x;
+    const uint32_t k = b >> 3;
+    const uint32_t q = fdiv(k, a.div_f);
+    ft = static_cast<int>(k - q * a.div_f.d);
+    pb = static_cast<int>(q * 8 + (b & 7));
+    return pb < a.pblocks;
+  }
+  pb = blockIdx.x;
+  ft = blockIdx.y;
+  return true;
+}
 
 // This lane's pixel in each of the TP 32-pixel tiles of a wave: byte offset
 // of its first activation load, which taps fall inside the image, and the
@@ -387,8 +414,10 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int h = lane >> 5;   // k half (operands) / row quad (result)
   const int c = lane & 31;   // operand row / column within a 32-tile
-  const int p0 = (KS == 1 ? blockIdx.x * 4 + wave : blockIdx.x) * 64;
-  const int f0 = blockIdx.y * (32 * TF);
+  int pb, ft;
+  if (!block_tile(a, pb, ft)) return;
+  const int p0 = (KS == 1 ? pb * 4 + wave : pb) * 64;
+  const int f0 = ft * (32 * TF);
   const int nchunk = a.Cw / (2 * VW);
   const int iters = a.KH * a.KW * nchunk;
   int it0 = 0, it1 = iters;
@@ -549,8 +578,10 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int h = lane >> 5;
   const int c = lane & 31;
-  const int p0 = (blockIdx.x * 4 + wave) * 64;
-  const int f0 = blockIdx.y * (32 * TF);
+  int pb, ft;
+  if (!block_tile(a, pb, ft)) return;
+  const int p0 = (pb * 4 + wave) * 64;
+  const int f0 = ft * (32 * TF);
   const int nchunk = a.Cw / (2 * VW);
   const int iters = a.KH * a.KW * nchunk;
   const int stages = (iters + kQS - 1) / kQS;
@@ -693,13 +724,22 @@ int env_int(const char* name, int dflt) {
   return e ? atoi(e) : dflt;
 }
 
+// Grid of `pblocks` pixel blocks x `fy` filter tiles: one-dimensional in the
+// XCD order of block_tile (pixel blocks padded to a multiple of 8), or 2-D.
+dim3 tile_grid(Mfma32Args& a, unsigned pblocks, unsigned fy) {
+  a.pblocks = static_cast<int32_t>(pblocks);
+  a.div_f = make_fastdiv(fy);
+  if (a.xcd_map) return dim3((pblocks + 7) / 8 * 8 * fy);
+  return dim3(pblocks, fy);
+}
+
 template <int VW, bool POOL>
-hipError_t launch32(const Mfma32Args& a, int tf, int ks, bool lds, bool late, hipStream_t s) {
+hipError_t launch32(Mfma32Args a, int tf, int ks, bool lds, bool late, hipStream_t s) {
   const unsigned fy = static_cast<unsigned>((a.F + 32 * tf - 1) / (32 * tf));
   const unsigned groups = static_cast<unsigned>((a.items + 63) / 64);
   if constexpr (VW <= 2) {
     if (lds) {
-      dim3 grid((groups + 3) / 4, fy), block(256);
+      const dim3 grid = tile_grid(a, (groups + 3) / 4, fy), block(256);
       if (tf == 2)
         bconv_mfma_lds_kernel<VW, POOL, 2, 2><<<grid, block, 0, s>>>(a);
       else
@@ -708,7 +748,7 @@ hipError_t launch32(const Mfma32Args& a, int tf, int ks, bool lds, bool late, hi
     }
   }
   if (ks == 1) {
-    dim3 grid((groups + 3) / 4, fy), block(256);
+    const dim3 grid = tile_grid(a, (groups + 3) / 4, fy), block(256);
     if (tf == 2 && late)
       bconv_mfma32_kernel<VW, POOL, 2, 1, 2, true><<<grid, block, 0, s>>>(a);
     else if (tf == 2)
@@ -718,7 +758,7 @@ hipError_t launch32(const Mfma32Args& a, int tf, int ks, bool lds, bool late, hi
     else
       bconv_mfma32_kernel<VW, POOL, 1, 1, 2, false><<<grid, block, 0, s>>>(a);
   } else {
-    dim3 grid(groups, fy), block(64 * ks);
+    const dim3 grid = tile_grid(a, groups, fy), block(64 * ks);
     if (tf == 2) {
       if (ks == 2)
         bconv_mfma32_kernel<VW, POOL, 2, 2, 2, true><<<grid, block, 0, s>>>(a);
@@ -764,6 +804,7 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   a.w_bytes = static_cast<int32_t>(static_cast<int64_t>(g.F) * a.fstride * 4);
   a.div_w = make_fastdiv(static_cast<uint32_t>(pool ? g.Wp : g.Wo));
   a.div_h = make_fastdiv(static_cast<uint32_t>(pool ? g.Hp : g.Ho));
+  a.xcd_map = env_int("BNN_XCD_MAP", 1) != 0 ? 1 : 0;
   // Words per lane, row and iteration: 8-word chunks (128-bit loads) where
   // the channels allow, which halves the vector-memory instructions per MFMA
   // (the texture-address unit is the busiest unit of the small grids), but

@@ -21,8 +21,10 @@ pytestmark = pytest.mark.gpu
 # and the weights staged through LDS wherever no K split is used (by default
 # only large grids do that; small grids with C % 256 == 0 take 8-word chunks),
 # "early" is "auto" with the thresholds staged at kernel start (by default
-# only grids of more than 2 waves per SIMD do that).
-ALGOS = ["auto", "valu", "lds", "early"]
+# only grids of more than 2 waves per SIMD do that), "grid2d" is "auto" with
+# the matrix-core workgroups on a 2-D grid (pixel blocks x filter tiles)
+# instead of the one-dimensional XCD order.
+ALGOS = ["auto", "valu", "lds", "early", "grid2d"]
 
 
 @pytest.fixture(params=ALGOS)
@@ -33,6 +35,8 @@ def algo(request, monkeypatch):
         monkeypatch.setenv("BNN_MFMA_VW", "2")
     if request.param == "early":
         monkeypatch.setenv("BNN_MFMA_LATE", "0")
+    if request.param == "grid2d":
+        monkeypatch.setenv("BNN_XCD_MAP", "0")
     return request.param
 
 
