@@ -1,9 +1,10 @@
 // Binary convolution on the gfx950 matrix cores.
 //
 // A +-1 value is exactly representable in the 4-bit E2M1 float format, and a
-// dot product of K such values is an integer |S| <= K < 2^24, exact in the
-// fp32 accumulator.  So the XOR-popcount dot product of Eq. 4 can equally be
-// computed by v_mfma_scale_f32_32x32x64_f8f6f4 with both operands in fp4:
+// dot product of K such values is an integer |S| <= K, exact in the fp32
+// accumulator for the K < 2^22 taken here.  So the XOR-popcount dot product
+// of Eq. 4 can equally be computed by v_mfma_scale_f32_32x32x64_f8f6f4 with
+// both operands in fp4:
 // 32x32x64 multiply-accumulates per instruction (the fastest fp4 shape on
 // MI355X), against 32 bit-MACs per v_xor + v_bcnt pair on the vector ALU.
 // Each packed word is expanded to four fp4 registers (one nibble per bit)
@@ -160,6 +161,7 @@ struct Mfma32Args {
   int32_t pblocks;   // workgroups along the pixels
   int32_t xcd_map;   // 1: one-dimensional grid in the XCD order of block_tile
   FastDiv div_f;     // filter tiles along the filters
+  FastDiv div_c;     // word chunks per tap (Cw / (2 VW))
 };
 
 // The workgroup's pixel block and filter tile.  The workgroups of a launch
@@ -297,18 +299,106 @@ struct EpiParams {
       fl[tf] = a.flip ? a.flip[wi < a.Fw ? wi : a.Fw - 1] : 0u;
     }
   }
-  // Writes the block's thresholds to LDS; a barrier must follow.
-  __device__ __forceinline__ void stage(const Mfma32Args& a, float* thl) const {
-    if (a.bits && threadIdx.x < 32 * TF)
-      thl[threadIdx.x] = static_cast<float>(min(max(thr, -a.K - 1), a.K + 1)) - 0.5f;
+  // Writes the block's thresholds to LDS, as thr - 0.5 (or, with `neg`, as
+  // 0.5 - thr, the accumulators' start value); a barrier must follow.
+  __device__ __forceinline__ void stage(const Mfma32Args& a, float* thl, bool neg) const {
+    if (a.bits && threadIdx.x < 32 * TF) {
+      const float t = static_cast<float>(min(max(thr, -a.K - 1), a.K + 1)) - 0.5f;
+      thl[threadIdx.x] = neg ? -t : t;
+    }
   }
 };
+
+// Accumulator start values.  With `pre` (bits wanted, no sums, thresholds
+// already in LDS as 0.5 - thr) every accumulator of filter f starts at
+// 0.5 - thr_f, so it ends at S - thr_f + 0.5, which is negative exactly when
+// S < thr_f: its sign bit is the complement of the output bit, and the
+// epilogue needs no subtraction.  The sums stay exact: |S - thr + 0.5| <=
+// 2K + 1.5 < 2^23, half-integers exact in fp32 (K < 2^22,
+// bconv_mfma_supported).
+// Otherwise they start at 0.
+template <int TF, int TP>
+__device__ __forceinline__ void init_acc(v16f (&acc)[TF][TP], bool pre, const float* thl, int h) {
+#pragma unroll
+  for (int tf = 0; tf < TF; ++tf) {
+    v16f t;
+    if (pre) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) t[e] = thl[tf * 32 + 8 * (e >> 2) + 4 * h + (e & 3)];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) t[e] = 0.0f;
+    }
+#pragma unroll
+    for (int tp = 0; tp < TP; ++tp) acc[tf][tp] = t;
+  }
+}
+
+// Output bits of a wave's TF x TP tiles: threshold, flip, OR-pool, stores.
+// PRE: the accumulators hold S - thr + 0.5 (init_acc), whose sign bit is the
+// complement of the output bit; otherwise they hold S and the sign bit of
+// (thr - 0.5) - S is the output bit.
+template <bool PRE, int TF, int TP, bool POOL, int VW>
+__device__ __forceinline__ void epi_bits(const Mfma32Args& a, v16f (&acc)[TF][TP],
+                                         const PixTiles<TP, POOL, VW>& px, int p0, int f0,
+                                         int h, int c, const float* thl,
+                                         const EpiParams<TF>& ep) {
+  float th[TF][16];
+  if constexpr (!PRE) {
+#pragma unroll
+    for (int tf = 0; tf < TF; ++tf)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) th[tf][e] = thl[tf * 32 + 8 * (e >> 2) + 4 * h + (e & 3)];
+  }
+  uint32_t fm[TF], fx[TF];
+#pragma unroll
+  for (int tf = 0; tf < TF; ++tf) {
+    fm[tf] = f0 / 32 + tf == a.Fw - 1 ? tail_mask(a.F) : ~0u;
+    fx[tf] = PRE ? ~ep.fl[tf] : ep.fl[tf];
+  }
+#pragma unroll
+  for (int tp = 0; tp < TP; ++tp) {
+    uint32_t word[TF];
+#pragma unroll
+    for (int tf = 0; tf < TF; ++tf) {
+      // Filters 8 g + 4 h + r (r = 0..3) of register group g go to bits
+      // 31 - 8 g - 4 h - r: shift the four signs into a nibble (v_alignbit
+      // takes the sign bit of each value), then place the nibble.
+      uint32_t wd = 0u;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        uint32_t nib = 0u;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float d = PRE ? acc[tf][tp][4 * g + r] : th[tf][4 * g + r] - acc[tf][tp][4 * g + r];
+          nib = __builtin_amdgcn_alignbit(nib, __float_as_uint(d), 31);
+        }
+        wd |= nib << (28 - 8 * g - 4 * h);  // nib < 16: four bits shifted into 0
+      }
+      wd |= __shfl_xor(wd, 32);
+      wd = (wd ^ fx[tf]) & fm[tf];
+      if constexpr (POOL) {
+        wd |= __shfl_xor(wd, 1);
+        wd |= __shfl_xor(wd, 2);
+      }
+      word[tf] = wd;
+    }
+    const int item = p0 + tp * 32 + c;
+    const bool writer = POOL ? (h == 0 && (c & 3) == 0 && px.pv[tp]) : (h == 0 && px.pv[tp]);
+    if (writer) {
+      uint32_t* op = a.bits + static_cast<size_t>(POOL ? (item >> 2) : item) * a.Fw + f0 / 32;
+#pragma unroll
+      for (int tf = 0; tf < TF; ++tf)
+        if (f0 / 32 + tf < a.Fw) op[tf] = word[tf];
+    }
+  }
+}
 
 template <int TF, int TP, bool POOL, int VW>
 __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP],
                                          const PixTiles<TP, POOL, VW>& px, int p0, int f0,
                                          int h, int c, const float* thl,
-                                         const EpiParams<TF>& ep) {
+                                         const EpiParams<TF>& ep, bool pre) {
   // Filters past F (a partial last tile) read zero weights through the
   // buffer range and are masked out of every output.
   const bool ftail = f0 + 32 * TF > a.F;
@@ -340,51 +430,10 @@ __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP
     }
   }
   if (a.bits) {
-    // The sign bit of (thr - 0.5) - S is the output bit.
-    float th[TF][16];
-#pragma unroll
-    for (int tf = 0; tf < TF; ++tf)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) th[tf][e] = thl[tf * 32 + 8 * (e >> 2) + 4 * h + (e & 3)];
-    uint32_t fm[TF];
-#pragma unroll
-    for (int tf = 0; tf < TF; ++tf) fm[tf] = f0 / 32 + tf == a.Fw - 1 ? tail_mask(a.F) : ~0u;
-#pragma unroll
-    for (int tp = 0; tp < TP; ++tp) {
-      uint32_t word[TF];
-#pragma unroll
-      for (int tf = 0; tf < TF; ++tf) {
-        // Filters 8 g + 4 h + r (r = 0..3) of register group g go to bits
-        // 31 - 8 g - 4 h - r: shift the four signs into a nibble (v_alignbit
-        // takes the sign bit of each difference), then place the nibble.
-        uint32_t wd = 0u;
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          uint32_t nib = 0u;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float d = th[tf][4 * g + r] - acc[tf][tp][4 * g + r];
-            nib = __builtin_amdgcn_alignbit(nib, __float_as_uint(d), 31);
-          }
-          wd |= (nib & 15u) << (28 - 8 * g - 4 * h);
-        }
-        wd |= __shfl_xor(wd, 32);
-        wd = (wd ^ ep.fl[tf]) & fm[tf];
-        if constexpr (POOL) {
-          wd |= __shfl_xor(wd, 1);
-          wd |= __shfl_xor(wd, 2);
-        }
-        word[tf] = wd;
-      }
-      const int item = p0 + tp * 32 + c;
-      const bool writer = POOL ? (h == 0 && (c & 3) == 0 && px.pv[tp]) : (h == 0 && px.pv[tp]);
-      if (writer) {
-        uint32_t* op = a.bits + static_cast<size_t>(POOL ? (item >> 2) : item) * a.Fw + f0 / 32;
-#pragma unroll
-        for (int tf = 0; tf < TF; ++tf)
-          if (f0 / 32 + tf < a.Fw) op[tf] = word[tf];
-      }
-    }
+    if (pre)
+      epi_bits<true, TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, ep);
+    else
+      epi_bits<false, TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, ep);
   }
 }
 
@@ -430,8 +479,10 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
   __shared__ float thl[32 * TF];
   EpiParams<TF> ep;
   ep.fetch(a, f0);
+  // Thresholds staged at kernel start: the accumulators start from them.
+  const bool pre = KS == 1 && !LATE && a.bits && !a.sums;
   if constexpr (KS == 1 && !LATE) {
-    ep.stage(a, thl);
+    ep.stage(a, thl, pre);
     __syncthreads();
   }
 
@@ -439,12 +490,7 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
   px.init(a, p0, h, c);
 
   v16f acc[TF][TP];
-#pragma unroll
-  for (int tf = 0; tf < TF; ++tf)
-#pragma unroll
-    for (int tp = 0; tp < TP; ++tp)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[tf][tp][e] = 0.0f;
+  init_acc<TF, TP>(acc, pre, thl, h);
 
   const __amdgpu_buffer_rsrc_t rin = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint32_t*>(a.in), 0, a.in_bytes, kRsrcWord3);
@@ -514,7 +560,7 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
 
   if constexpr (KS == 1) {
     if constexpr (LATE) {
-      ep.stage(a, thl);
+      ep.stage(a, thl, false);
       __syncthreads();
     }
   } else {
@@ -523,7 +569,7 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
     // into slot 0, and wave 0 takes the totals for the epilogue.
     constexpr int NV = TF * TP * 16 * 64;  // values per wave
     __shared__ float part[KS][NV];
-    ep.stage(a, thl);
+    ep.stage(a, thl, false);
 #pragma unroll
     for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
@@ -546,7 +592,7 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[tf][tp][e] = part[0][((tf * TP + tp) * 16 + e) * 64 + lane];
   }
-  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, ep);
+  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, ep, pre);
 }
 
 // The same conv with the weights shared through LDS.  The 4 waves of a block
@@ -568,7 +614,7 @@ struct LdsStage {
   static constexpr int kPerThread = (kChunks + 255) / 256;
 };
 
-template <int VW, bool POOL, int TF, int PD>
+template <int VW, bool POOL, int TF, int PD, bool PRE>
 __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
   constexpr int TP = 2;
   using St = LdsStage<VW, TF>;
@@ -588,14 +634,6 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
 
   PixTiles<TP, POOL, VW> px;
   px.init(a, p0, h, c);
-
-  v16f acc[TF][TP];
-#pragma unroll
-  for (int tf = 0; tf < TF; ++tf)
-#pragma unroll
-    for (int tp = 0; tp < TP; ++tp)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[tf][tp][e] = 0.0f;
 
   const __amdgpu_buffer_rsrc_t rin = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint32_t*>(a.in), 0, a.in_bytes, kRsrcWord3);
@@ -617,7 +655,7 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
       const int it = s * kQS + q;
       uint32_t off = kOutOfRange;
       if (k < St::kChunks && it < iters) {
-        const int tap = it / nchunk;
+        const int tap = static_cast<int>(fdiv(static_cast<uint32_t>(it), a.div_c));
         const int cc = (it - tap * nchunk) * 2 * VW;
         off = static_cast<uint32_t>(((f0 + fi) * a.fstride + tap * a.Cw + cc) * 4);
       }
@@ -667,11 +705,15 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
   uint32_t xr[2][TP][VW];
 
   // Thresholds staged at kernel start (the barrier after the first weight
-  // stage covers them), so no threshold register stays live in the loop.
+  // stage covers them), so no threshold register stays live in the loop;
+  // the accumulators start from them.
   EpiParams<TF> ep;
   ep.fetch(a, f0);
   __shared__ float thl[32 * TF];
-  ep.stage(a, thl);
+  // PRE (a template choice: a run-time one costs registers) = bits wanted
+  // and no sums.
+  constexpr bool pre = PRE;
+  ep.stage(a, thl, pre);
   stage_load(0);
   stage_store(0);
 #pragma unroll
@@ -680,6 +722,8 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
     cur.advance(a, VW);
   }
   __syncthreads();
+  v16f acc[TF][TP];
+  init_acc<TF, TP>(acc, pre, thl, h);
 
   for (int s = 0; s < stages; ++s) {
     const int buf = s & 1;
@@ -716,7 +760,7 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
     if (more) stage_store(buf ^ 1);
     __syncthreads();
   }
-  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, ep);
+  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, ep, pre);
 }
 
 int env_int(const char* name, int dflt) {
@@ -740,10 +784,15 @@ hipError_t launch32(Mfma32Args a, int tf, int ks, bool lds, bool late, hipStream
   if constexpr (VW <= 2) {
     if (lds) {
       const dim3 grid = tile_grid(a, (groups + 3) / 4, fy), block(256);
-      if (tf == 2)
-        bconv_mfma_lds_kernel<VW, POOL, 2, 2><<<grid, block, 0, s>>>(a);
+      const bool pre = a.bits && !a.sums;
+      if (tf == 2 && pre)
+        bconv_mfma_lds_kernel<VW, POOL, 2, 2, true><<<grid, block, 0, s>>>(a);
+      else if (tf == 2)
+        bconv_mfma_lds_kernel<VW, POOL, 2, 2, false><<<grid, block, 0, s>>>(a);
+      else if (pre)
+        bconv_mfma_lds_kernel<VW, POOL, 1, 2, true><<<grid, block, 0, s>>>(a);
       else
-        bconv_mfma_lds_kernel<VW, POOL, 1, 2><<<grid, block, 0, s>>>(a);
+        bconv_mfma_lds_kernel<VW, POOL, 1, 2, false><<<grid, block, 0, s>>>(a);
       return hipGetLastError();
     }
   }
@@ -817,6 +866,7 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   if (vw != 1 && vw != 2 && vw != 4) vw = 1;
   if (g.Cw % (2 * vw) != 0) vw = g.Cw % 4 == 0 ? 2 : 1;
   const int iters = g.KH * g.KW * (g.Cw / (2 * vw));
+  a.div_c = make_fastdiv(static_cast<uint32_t>(g.Cw / (2 * vw)));
 
   // Tile shape and K split: 64-filter wave tiles down to ~1 wave per SIMD
   // (1024 waves), then 32-filter tiles with a K split over up to 4 waves
@@ -861,9 +911,11 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
 
 bool bconv_mfma_supported(const ConvGeom& g) {
   // C a multiple of 64 (whole words, 2 words per k-step), at most 32 taps
-  // (per-lane tap masks), and inputs
-  // and weights under 2 GiB (32-bit byte offsets of the raw buffer loads).
+  // (per-lane tap masks), fewer than 2^22 bits per window (the fp32
+  // accumulators, which may start at 0.5 - thr, stay exact), and inputs and
+  // weights under 2 GiB (32-bit byte offsets of the raw buffer loads).
   return (g.C % 64) == 0 && g.KH * g.KW <= 32 &&
+         static_cast<int64_t>(g.KH) * g.KW * g.C < (int64_t{1} << 22) &&
          static_cast<int64_t>(g.N) * g.H * g.W * g.Cw < (int64_t{1} << 29) &&
          static_cast<int64_t>(g.F) * g.KH * g.KW * g.Cw < (int64_t{1} << 29);
 }
