@@ -472,6 +472,25 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
       g1.C = layers[1].C;
       fuse_input = !(e && strcmp(e, "0") == 0) && bnn::bconv_patch_supported(g1);
     }
+    // A real-valued first layer followed by a 3x3 binary conv that fits runs
+    // as one kernel with the first layer's bits in LDS (a matrix-core kernel,
+    // so not under BNN_ALGO=valu; BNN_FUSE_FIRST=0 keeps the two launches).
+    bool fuse_first = false;
+    bnn::ConvGeom g_first;
+    if (n_layers > 1 && layers[0].kind == BNN_LAYER_FCONV_BINW &&
+        layers[1].kind == BNN_LAYER_BCONV) {
+      const char* e = getenv("BNN_FUSE_FIRST");
+      const bnn_layer& l0 = layers[0];
+      const bnn_layer& l1 = layers[1];
+      bnn_conv_desc d0{batch, H, W, l0.C, l0.F, l0.KH, l0.KW, l0.stride, l0.pad, l0.pool};
+      bnn::ConvGeom g1;
+      if (conv_geom(&d0, &g_first) == BNN_OK) {  // (the chain is validated above)
+        bnn_conv_desc d1{batch, g_first.Hp, g_first.Wp, l1.C, l1.F,
+                         l1.KH, l1.KW, l1.stride, l1.pad, l1.pool};
+        fuse_first = !(e && strcmp(e, "0") == 0) && conv_geom(&d1, &g1) == BNN_OK &&
+                     use_mfma(g1) && bnn::fconv_bconv_supported(g_first, g1);
+      }
+    }
     int cur = 0;  // buffer holding the current packed activations
     int64_t h = H, w = W, c = C;
     for (int32_t li = 0; li < n_layers; ++li) {
@@ -499,8 +518,12 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
                           l.KH, l.KW, l.stride, l.pad, l.pool};
           bnn::ConvGeom g;
           conv_geom(&d, &g);
-          if (l.kind == BNN_LAYER_FCONV_BINW)
-            e = bnn::launch_fconv_binw(g, input, l.w, l.thr, l.flip, nullptr, dst, stream);
+          if (l.kind == BNN_LAYER_FCONV_BINW) {
+            if (!fuse_first)
+              e = bnn::launch_fconv_binw(g, input, l.w, l.thr, l.flip, nullptr, dst, stream);
+          } else if (li == 1 && fuse_first)
+            e = bnn::launch_fconv_bconv(g_first, g, input, layers[0].w, layers[0].thr,
+                                        layers[0].flip, l.w, l.thr, l.flip, dst, stream);
           else if (li == 1 && fuse_input)
             e = bnn::launch_bconv_patch(g, mode, input, layers[0].offset, l.w, l.thr, l.flip,
                                         nullptr, dst, stream);

@@ -1,0 +1,381 @@
+// The real-valued first layer (Eq. 3: fp32 image, +-1 weights, pad 0.0) and
+// the binary conv after it (Eq. 4 on the first layer's output bits) in one
+// launch, for the BCNN without input binarization (Table I): the first
+// layer's output never goes to global memory.
+//
+// A block owns an 8 x 32 tile of the second layer's output pixels of one
+// image (4 x 16 2x2 windows when it pools) and all of its filters (64 or
+// 128; 4 waves per 64 filters).
+//   1. It stages the fp32 input tile the first layer needs for the
+//      (8 + 2) x (32 + 2) pixels of the second layer's windows (halo of one
+//      pixel), zero outside the image, plus both layers' thresholds and the
+//      first layer's +-1 weight operands.
+//   2. All waves compute the first layer's outputs on that 10 x 34 tile with
+//      v_mfma_f32_16x16x32_f16, every input value split into two fp16 parts
+//      x = hi + lo as in the standalone first-layer kernel (for inputs on the
+//      2^-16 grid with |x| < 8 the fp32 sums are exact in any order), then
+//      threshold / flip and pack them into words in LDS.  Pixels outside the
+//      first layer's output are the pad word 0 (-1) of the second conv.
+//   3. Each wave takes 64 pixels (16 windows) x 64 filters of the second
+//      layer on the fp4 matrix cores: activation words from LDS (no bounds
+//      tests: the halo holds the padding), weight words from global memory,
+//      accumulators started at 0.5 - thr (the output bit is the complement
+//      of the sign), OR-pool on lane quads and the packed store.
+#include <stdlib.h>
+
+#include "fp4_expand.hpp"
+#include "kernels.hpp"
+
+namespace bnn {
+namespace {
+
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+
+constexpr int kTH = 8, kTW = 32;             // second-layer output tile
+constexpr int kAH = kTH + 2, kAW = kTW + 2;  // first-layer tile (second layer's windows)
+constexpr int kIH = kAH + 2, kIW = kAW + 2;  // input tile (first layer's windows)
+constexpr int kAPix = kAH * kAW;             // 340
+constexpr int kATiles = (kAPix + 15) / 16;   // 16-pixel tiles of the first layer
+
+struct FbArgs {
+  const float* in;
+  const uint32_t* w0;
+  const int32_t* thr0;
+  const uint32_t* flip0;
+  const uint32_t* w1;
+  const int32_t* thr1;
+  const uint32_t* flip1;
+  uint32_t* bits;
+  int32_t N, H, W;              // input image
+  int32_t pad0, Ho0, Wo0;       // first layer
+  int32_t pad1, Ho1, Wo1;       // second layer (before pooling)
+  int32_t Hp, Wp;               // stored output (pooled dims when pooling)
+  int32_t K1;                   // bits per second-layer window, 9 * F0
+  int32_t w1_bytes;
+  int32_t tiles_w, tiles_h;
+};
+
+constexpr uint32_t kRsrcWord3 = 0x00020000;
+
+template <int C0, int F0, int NFH, bool POOL>
+__global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
+  constexpr int NT = 256 * NFH;        // threads
+  constexpr int NW = 4 * NFH;          // waves
+  constexpr int K0 = 9 * C0;
+  constexpr int KC0 = (K0 + 31) / 32;  // first-layer k-chunks of 32
+  constexpr int FT0 = F0 / 16;         // first-layer filter tiles of 16
+  constexpr int CW1 = F0 / 32;         // words per first-layer output pixel
+  constexpr int VW = CW1 % 4 == 0 ? 2 : 1;  // words per lane and k-step pair
+  constexpr int NCH = CW1 / (2 * VW);       // chunks per tap
+  constexpr int F1 = 64 * NFH;
+  constexpr int FW1 = F1 / 32;
+
+  __shared__ float xin[kIH * kIW * C0];
+  __shared__ v8h wop[FT0][KC0][64];
+  __shared__ __attribute__((aligned(16))) uint32_t act[kAPix * CW1];
+  __shared__ float th0[F0];
+  __shared__ uint32_t fl0[CW1];
+  __shared__ float th1[F1];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int b = blockIdx.x;
+  const int tw = b % a.tiles_w;
+  b /= a.tiles_w;
+  const int tht = b % a.tiles_h;
+  const int n = b / a.tiles_h;
+  const int i0 = tht * kTH, j0 = tw * kTW;  // second-layer output origin
+  const int r0 = i0 - a.pad1, c0 = j0 - a.pad1;  // first-layer tile origin
+  const int y0 = r0 - a.pad0, x0 = c0 - a.pad0;  // input tile origin
+
+  // 1. Staging.
+  for (int e = tid; e < kIH * kIW * C0; e += NT) {
+    const int ch = e % C0, t = e / C0;
+    const int col = t % kIW, row = t / kIW;
+    const int y = y0 + row, x = x0 + col;
+    float v = 0.0f;
+    if (y >= 0 && y < a.H && x >= 0 && x < a.W)
+      v = a.in[((static_cast<size_t>(n) * a.H + y) * a.W + x) * C0 + ch];
+    xin[e] = v;
+  }
+  // First-layer A operands: row = filter 16 ft + (l % 16), 8 k values
+  // 32 kc + 8 (l / 16) + j as +-1 (0 past K0).  One weight word per filter
+  // and tap (C0 <= 4 channels).
+  for (int e = tid; e < FT0 * KC0 * 64; e += NT) {
+    const int l = e & 63, kc = (e >> 6) % KC0, ft = (e >> 6) / KC0;
+    const int f = 16 * ft + (l & 15), q = l >> 4;
+    v8h op;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int k = 32 * kc + 8 * q + j;
+      const int tap = k / C0, ch = k - tap * C0;
+      const bool ok = k < K0;
+      const uint32_t word = a.w0[f * 9 + (ok ? tap : 0)];
+      const bool one = (word >> (31 - ch)) & 1u;
+      op[j] = ok ? (one ? static_cast<_Float16>(1.0f) : static_cast<_Float16>(-1.0f))
+                 : static_cast<_Float16>(0.0f);
+    }
+    wop[ft][kc][l] = op;
+  }
+  for (int e = tid; e < F0; e += NT) th0[e] = static_cast<float>(a.thr0[e]);
+  for (int e = tid; e < CW1; e += NT) fl0[e] = a.flip0 ? a.flip0[e] : 0u;
+  // Second-layer start values 0.5 - thr (thr clamped to [-K1-1, K1+1], which
+  // keeps every comparison since |S| <= K1).
+  for (int e = tid; e < F1; e += NT)
+    th1[e] = 0.5f - static_cast<float>(min(max(a.thr1[e], -a.K1 - 1), a.K1 + 1));
+  __syncthreads();
+
+  // 2. First layer on the 10 x 34 tile: lane (q, c) = (l / 16, l % 16) holds
+  // pixel c of a 16-pixel tile and filters 16 ft + 4 q + r (r = 0..3).
+  {
+    const int q = lane >> 4, c = lane & 15;
+    for (int pt = wave; pt < kATiles; pt += NW) {
+      const int p = 16 * pt + c;
+      const bool pv = p < kAPix;
+      const int pp = pv ? p : 0;
+      const int lr = pp / kAW, lc = pp - (pp / kAW) * kAW;
+      v8h xh[KC0], xl[KC0];
+#pragma unroll
+      for (int kc = 0; kc < KC0; ++kc)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int k = 32 * kc + 8 * q + j;
+          const int tap = k / C0, ch = k - tap * C0;
+          const int kh = tap / 3, kw = tap - kh * 3;
+          const float x = k < K0 ? xin[((lr + kh) * kIW + lc + kw) * C0 + ch] : 0.0f;
+          const _Float16 hi = static_cast<_Float16>(x);
+          xh[kc][j] = hi;
+          xl[kc][j] = static_cast<_Float16>(x - static_cast<float>(hi));
+        }
+      const int rr = r0 + lr, cc = c0 + lc;
+      const bool inside = pv && rr >= 0 && rr < a.Ho0 && cc >= 0 && cc < a.Wo0;
+#pragma unroll
+      for (int wi = 0; wi < CW1; ++wi) {
+        uint32_t word = 0u;
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int ft = 2 * wi + hf;
+          v4f acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int kc = 0; kc < KC0; ++kc) {
+            const v8h wa = wop[ft][kc][lane];
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa, xh[kc], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa, xl[kc], acc, 0, 0, 0);
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int fl = 16 * hf + 4 * q + r;  // filter within the word
+            const bool on = acc[r] >= th0[32 * wi + fl];
+            word |= static_cast<uint32_t>(on) << (31 - fl);
+          }
+        }
+        word |= __shfl_xor(word, 16);
+        word |= __shfl_xor(word, 32);
+        word = inside ? word ^ fl0[wi] : 0u;
+        if (q == 0 && pv) act[p * CW1 + wi] = word;
+      }
+    }
+  }
+  __syncthreads();
+
+  // 3. Second layer: wave = pixel group pg (64 pixels) x filter half fh.
+  const int pg = wave & 3, fh = wave >> 2;
+  const int h = lane >> 5, c = lane & 31;
+  const int f0 = 64 * fh;
+  int pr[2], pc[2], abase[2];
+#pragma unroll
+  for (int tp = 0; tp < 2; ++tp) {
+    const int m = 32 * tp + c;
+    if constexpr (POOL) {
+      pr[tp] = 2 * pg + ((m >> 1) & 1);
+      pc[tp] = 2 * (m >> 2) + (m & 1);
+    } else {
+      pr[tp] = 2 * pg + tp;
+      pc[tp] = c;
+    }
+    abase[tp] = (pr[tp] * kAW + pc[tp]) * CW1 + h * VW;
+  }
+  v16f acc[2][2];
+#pragma unroll
+  for (int tf = 0; tf < 2; ++tf) {
+    v16f t;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) t[e] = th1[f0 + 32 * tf + 8 * (e >> 2) + 4 * h + (e & 3)];
+    acc[tf][0] = t;
+    acc[tf][1] = t;
+  }
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(a.w1), 0, a.w1_bytes, kRsrcWord3);
+  const uint32_t smask = __builtin_amdgcn_readfirstlane(0x88888888u);
+  uint32_t vfill;
+  asm("v_mov_b32 %0, 0x22222222" : "=v"(vfill));
+  uint32_t woff[2];
+#pragma unroll
+  for (int tf = 0; tf < 2; ++tf)
+    woff[tf] = static_cast<uint32_t>(((f0 + 32 * tf + c) * 9 * CW1 + h * VW) * 4);
+
+  auto load_w = [&](int it, uint32_t (&ww)[2][VW]) {
+    const int tap = it / NCH, cc = (it - tap * NCH) * 2 * VW;
+    const uint32_t so = static_cast<uint32_t>((tap * CW1 + cc) * 4);
+#pragma unroll
+    for (int tf = 0; tf < 2; ++tf) {
+      if constexpr (VW == 2) {
+        typedef unsigned int u2 __attribute__((ext_vector_type(2)));
+        const u2 t = __builtin_amdgcn_raw_buffer_load_b64(rw, woff[tf], so, 0);
+        ww[tf][0] = t[0];
+        ww[tf][1] = t[1];
+      } else {
+        ww[tf][0] = __builtin_amdgcn_raw_buffer_load_b32(rw, woff[tf], so, 0);
+      }
+    }
+  };
+  constexpr int ITERS = 9 * NCH;
+  uint32_t wr[2][2][VW];
+  load_w(0, wr[0]);
+#pragma unroll
+  for (int it = 0; it < ITERS; ++it) {
+    const int cur = it & 1;
+    if (it + 1 < ITERS) load_w(it + 1, wr[cur ^ 1]);
+    const int tap = it / NCH, cc = (it - tap * NCH) * 2 * VW;
+    const int kh = tap / 3, kw = tap - kh * 3;
+    const int ao = (kh * kAW + kw) * CW1 + cc;
+    uint32_t xw[2][VW];
+#pragma unroll
+    for (int tp = 0; tp < 2; ++tp)
+#pragma unroll
+      for (int v = 0; v < VW; ++v) xw[tp][v] = act[abase[tp] + ao + v];
+    v8i A[2][VW], B[2][VW];
+#pragma unroll
+    for (int tf = 0; tf < 2; ++tf) expand_words<VW>(wr[cur][tf], smask, vfill, A[tf]);
+#pragma unroll
+    for (int tp = 0; tp < 2; ++tp) expand_words<VW>(xw[tp], smask, vfill, B[tp]);
+#pragma unroll
+    for (int v = 0; v < VW; ++v)
+#pragma unroll
+      for (int tf = 0; tf < 2; ++tf)
+#pragma unroll
+        for (int tp = 0; tp < 2; ++tp)
+          acc[tf][tp] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+              A[tf][v], B[tp][v], acc[tf][tp], 4, 4, 0, 127, 0, 127);
+  }
+
+  // Epilogue: register e of lane (h, c) holds S - thr + 0.5 of filter
+  // f0 + 32 tf + 8 (e / 4) + 4 h + e % 4 at pixel c of tile tp; its sign bit
+  // is the complement of the output bit.
+  uint32_t fx[2];
+#pragma unroll
+  for (int tf = 0; tf < 2; ++tf) {
+    const int wi = f0 / 32 + tf;
+    fx[tf] = ~(a.flip1 ? a.flip1[wi] : 0u);
+  }
+#pragma unroll
+  for (int tp = 0; tp < 2; ++tp) {
+    uint32_t word[2];
+#pragma unroll
+    for (int tf = 0; tf < 2; ++tf) {
+      uint32_t wd = 0u;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        uint32_t nib = 0u;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          nib = __builtin_amdgcn_alignbit(nib, __float_as_uint(acc[tf][tp][4 * g + r]), 31);
+        wd |= nib << (28 - 8 * g - 4 * h);
+      }
+      wd |= __shfl_xor(wd, 32);
+      wd ^= fx[tf];
+      if constexpr (POOL) {
+        wd |= __shfl_xor(wd, 1);
+        wd |= __shfl_xor(wd, 2);
+      }
+      word[tf] = wd;
+    }
+    if constexpr (POOL) {
+      const int ip = (i0 >> 1) + pg, jp = (j0 >> 1) + ((32 * tp + c) >> 2);
+      if (h == 0 && (c & 3) == 0 && ip < a.Hp && jp < a.Wp) {
+        uint32_t* op = a.bits + (static_cast<size_t>(n * a.Hp + ip) * a.Wp + jp) * FW1 + f0 / 32;
+        *reinterpret_cast<uint2*>(op) = make_uint2(word[0], word[1]);
+      }
+    } else {
+      const int i = i0 + pr[tp], j = j0 + pc[tp];
+      if (h == 0 && i < a.Ho1 && j < a.Wo1) {
+        uint32_t* op = a.bits + (static_cast<size_t>(n * a.Ho1 + i) * a.Wo1 + j) * FW1 + f0 / 32;
+        *reinterpret_cast<uint2*>(op) = make_uint2(word[0], word[1]);
+      }
+    }
+  }
+}
+
+template <int C0, int F0>
+hipError_t launch_c0f0(const FbArgs& a, int f1, bool pool, unsigned blocks, hipStream_t s) {
+  if (f1 == 128) {
+    if (pool)
+      fconv_bconv_kernel<C0, F0, 2, true><<<blocks, 512, 0, s>>>(a);
+    else
+      fconv_bconv_kernel<C0, F0, 2, false><<<blocks, 512, 0, s>>>(a);
+  } else {
+    if (pool)
+      fconv_bconv_kernel<C0, F0, 1, true><<<blocks, 256, 0, s>>>(a);
+    else
+      fconv_bconv_kernel<C0, F0, 1, false><<<blocks, 256, 0, s>>>(a);
+  }
+  return hipGetLastError();
+}
+
+template <int C0>
+hipError_t launch_c0(const FbArgs& a, int f0, int f1, bool pool, unsigned blocks, hipStream_t s) {
+  return f0 == 128 ? launch_c0f0<C0, 128>(a, f1, pool, blocks, s)
+                   : launch_c0f0<C0, 64>(a, f1, pool, blocks, s);
+}
+
+}  // namespace
+
+bool fconv_bconv_supported(const ConvGeom& g0, const ConvGeom& g1) {
+  return g0.KH == 3 && g0.KW == 3 && g0.C >= 1 && g0.C <= 4 && g0.pool == 0 &&
+         (g0.pad == 0 || g0.pad == 1) && (g0.F == 64 || g0.F == 128) &&
+         g1.KH == 3 && g1.KW == 3 && g1.C == g0.F && (g1.pad == 0 || g1.pad == 1) &&
+         (g1.F == 64 || g1.F == 128) && (g1.pool == 0 || g1.pool == 2) &&
+         g1.N == g0.N && g1.H == g0.Ho && g1.W == g0.Wo && g1.Ho >= 1 && g1.Wo >= 1 &&
+         static_cast<int64_t>(g0.N) * g0.H * g0.W * g0.C < (int64_t{1} << 31);
+}
+
+hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const float* in,
+                              const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
+                              const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
+                              uint32_t* bits, hipStream_t s) {
+  FbArgs a;
+  a.in = in;
+  a.w0 = w0;
+  a.thr0 = thr0;
+  a.flip0 = flip0;
+  a.w1 = w1;
+  a.thr1 = thr1;
+  a.flip1 = flip1;
+  a.bits = bits;
+  a.N = g0.N;
+  a.H = g0.H;
+  a.W = g0.W;
+  a.pad0 = g0.pad;
+  a.Ho0 = g0.Ho;
+  a.Wo0 = g0.Wo;
+  a.pad1 = g1.pad;
+  a.Ho1 = g1.Ho;
+  a.Wo1 = g1.Wo;
+  a.Hp = g1.Hp;
+  a.Wp = g1.Wp;
+  a.K1 = 9 * g1.C;
+  a.w1_bytes = static_cast<int32_t>(static_cast<int64_t>(g1.F) * 9 * g1.Cw * 4);
+  a.tiles_w = (g1.Wo + kTW - 1) / kTW;
+  a.tiles_h = (g1.Ho + kTH - 1) / kTH;
+  const unsigned blocks = static_cast<unsigned>(g0.N) * a.tiles_w * a.tiles_h;
+  const bool pool = g1.pool == 2;
+  switch (g0.C) {
+    case 1: return launch_c0<1>(a, g0.F, g1.F, pool, blocks, s);
+    case 2: return launch_c0<2>(a, g0.F, g1.F, pool, blocks, s);
+    case 3: return launch_c0<3>(a, g0.F, g1.F, pool, blocks, s);
+    default: return launch_c0<4>(a, g0.F, g1.F, pool, blocks, s);
+  }
+}
+
+}  // namespace bnn

@@ -69,6 +69,18 @@ hipError_t launch_fconv_binw(const ConvGeom& g, const float* in,
                              const uint32_t* flip, float* sums,
                              uint32_t* bits, hipStream_t s);
 
+// The real-valued first layer and the binary 3x3 conv after it in one launch
+// (fconv_bconv.hip), the first layer's output bits kept in LDS.  g0: the
+// first layer (3x3, C <= 4, 64 or 128 filters, no pooling); g1: the second
+// (3x3 over g0's output, 64 or 128 filters, optional 2x2 pooling).  Writes
+// the second layer's packed bits; both thr must be non-null.
+bool fconv_bconv_supported(const ConvGeom& g0, const ConvGeom& g1);
+hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const float* in,
+                              const uint32_t* w0, const int32_t* thr0,
+                              const uint32_t* flip0, const uint32_t* w1,
+                              const int32_t* thr1, const uint32_t* flip1,
+                              uint32_t* bits, hipStream_t s);
+
 // A run of consecutive binary FC layers in one launch (bfc_chain.hip): every
 // block takes R rows through all of them with the intermediate bits in LDS.
 // Layer i has K_i input bits and N_i outputs; K_{i+1} = N_i; every layer but

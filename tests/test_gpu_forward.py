@@ -18,12 +18,16 @@ pytestmark = pytest.mark.gpu
 # matrix-core kernel with weights staged through LDS; "nopatch": the thresholded
 # input packed by bnn_pack_bits and convolved by the generic kernel instead
 # of the fused patch-packing kernel; "nochain": every FC layer as its own
-# launch instead of runs of small FC layers in the chained kernel.
-@pytest.fixture(params=["auto", "valu", "lds", "nopatch", "nochain"])
+# launch instead of runs of small FC layers in the chained kernel; "nofuse":
+# the real-valued first layer and the binary conv after it as two launches
+# instead of the fused first-layer kernel.
+@pytest.fixture(params=["auto", "valu", "lds", "nopatch", "nochain", "nofuse"])
 def algo(request, monkeypatch):
     monkeypatch.setenv("BNN_ALGO", "valu" if request.param == "valu" else "auto")
     if request.param == "nochain":
         monkeypatch.setenv("BNN_FC_CHAIN", "0")
+    if request.param == "nofuse":
+        monkeypatch.setenv("BNN_FUSE_FIRST", "0")
     if request.param == "lds":
         monkeypatch.setenv("BNN_MFMA_LDS", "1")
         monkeypatch.setenv("BNN_MFMA_VW", "2")
