@@ -35,22 +35,24 @@ HBM_PEAK_GBS = 8000.0
 # HBM traffic of the dominant kernel from two rocprofv3 --pmc passes
 # (FETCH_SIZE, WRITE_SIZE, KiB per dispatch) over this same script.  The
 # counters are calibrated on a 256 MiB device-to-device copy in the same
-# runs: FETCH_SIZE read 131087.7 KiB for 262144 KiB moved (factor 2.0),
+# runs: FETCH_SIZE read 131088.1 KiB for 262144 KiB moved (factor 2.0),
 # WRITE_SIZE read 262144.0 KiB (factor 1.0).  A figure is reported only while
 # the sources it was taken from hash to the values recorded with it.
+_BUILD = ("paper_1808_00209_amd/build.py",
+          "72c88ac8739ea58df1e7bf480187bcff54058511792aa1a10abbd4e679e40bd7")
+_FP4 = ("paper_1808_00209_amd/csrc/fp4_expand.hpp",
+        "d025e6c895771b0e8c624d6b14e4559aae203e5a519954919d75dea0192da41b")
 MEASURED_TRAFFIC = {
+    ("cifar_bnn_b64", "L0+L1 fconv+bconv 32x32x3->128->128 k3 pool (fused)"): dict(
+        fetch_kib=715.2, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
+        sources=dict([("paper_1808_00209_amd/csrc/fconv_bconv.hip",
+                       "beb0694adfcd696ad33c10a247cb0acd306f20dd11727cd91382c88a66b835b8"),
+                      _FP4, _BUILD])),
     ("cifar_bnn_b64", "L5 bconv 8x8x512->512 k3 pool"): dict(
-        fetch_kib=1335.0, write_kib=64.0, fetch_scale=2.0, write_scale=1.0,
-        sources={"paper_1808_00209_amd/csrc/bconv_mfma.hip":
-                 "8ab224860433df63e7743d4d3927c97918824c5d803fb6c563aecf33b5bfc1b5",
-                 "paper_1808_00209_amd/build.py":
-                 "a70d702c4ec46372bb37c51cd52826f75815c119113074d34212a1910d85fbb0"}),
-    ("cifar_bnn_b64", "L1 bconv 32x32x128->128 k3 pool"): dict(
-        fetch_kib=724.6, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
-        sources={"paper_1808_00209_amd/csrc/bconv_mfma.hip":
-                 "8ab224860433df63e7743d4d3927c97918824c5d803fb6c563aecf33b5bfc1b5",
-                 "paper_1808_00209_amd/build.py":
-                 "a70d702c4ec46372bb37c51cd52826f75815c119113074d34212a1910d85fbb0"}),
+        fetch_kib=1341.0, write_kib=64.0, fetch_scale=2.0, write_scale=1.0,
+        sources=dict([("paper_1808_00209_amd/csrc/bconv_mfma.hip",
+                       "b870a67eb6f2fbcfaaa76ca153e2a969b27ada8f7dd15183bd41baa99ced312f"),
+                      _FP4, _BUILD])),
 }
 
 
@@ -107,18 +109,47 @@ def net_input(cfg, batch):
     return synth.cfg3_input(batch) if cfg == 3 else synth.cfg4_input(batch)
 
 
-def layer_shapes(layers, H, W, C):
-    """Per layer: (name, kind, geometry dict, bit-MACs per image)."""
+def layer_shapes(layers, H, W, C, batch=None):
+    """Per layer: (name, kind, geometry dict, bit-MACs per image), with the
+    kernels bnn_forward launches at `batch` (fused first layers included)."""
     out = []
     h, w, c = H, W, C
     first = layers[0]["kind"] if layers else None
     fused = (len(layers) > 1 and first in INPUT_MODES and layers[1]["kind"] == "bconv"
              and layers[1]["C"] <= 32 and max(layers[1]["KH"], layers[1]["KW"]) <= 32
              and layers[1]["KH"] * layers[1]["KW"] * layers[1]["C"] <= 128)
+    # bnn_forward's fused first layer: real-valued 3x3 conv + binary 3x3 conv
+    fused_first = False
+    if len(layers) > 1 and first == "fconv" and layers[1]["kind"] == "bconv":
+        L0, L1 = layers[0], layers[1]
+        fused_first = (L0["KH"] == L0["KW"] == 3 and 1 <= C <= 4 and not L0.get("pool", 0)
+                       and L0["F"] in (64, 128) and L0["pad"] in (0, 1)
+                       and L1["KH"] == L1["KW"] == 3 and L1["F"] in (64, 128)
+                       and L1["pad"] in (0, 1) and L1.get("pool", 0) in (0, 2))
+        if fused_first and batch is not None:
+            # bnn_forward fuses from 32 workgroups of 8 x 32 output pixels on
+            Ho1 = H + 2 * L0["pad"] - 2 + 2 * L1["pad"] - 2
+            Wo1 = W + 2 * L0["pad"] - 2 + 2 * L1["pad"] - 2
+            fused_first = batch * ((Ho1 + 7) // 8) * ((Wo1 + 31) // 32) >= 32
     for li, L in enumerate(layers):
         k = L["kind"]
         if k in INPUT_MODES and fused:
             continue  # runs inside the next layer's patch-packing kernel
+        if k == "fconv" and fused_first:
+            continue  # runs inside the fused first-layer kernel
+        if k == "bconv" and li == 1 and fused_first:
+            L0 = layers[0]
+            Ho0, Wo0 = h + 2 * L0["pad"] - 2, w + 2 * L0["pad"] - 2
+            pad, F, pool = L["pad"], L["F"], L.get("pool", 0)
+            Ho, Wo = Ho0 + 2 * pad - 2, Wo0 + 2 * pad - 2
+            name = "L0+L1 fconv+bconv %dx%dx%d->%d->%d k3%s (fused)" % (
+                h, w, c, L0["F"], F, " pool" if pool else "")
+            out.append((name, "fconv_bconv",
+                        dict(H=h, W=w, C=c, F0=L0["F"], pad0=L0["pad"], Ho0=Ho0, Wo0=Wo0,
+                             F=F, KH=3, KW=3, pad=pad, pool=pool, li=li),
+                        Ho * Wo * F * 9 * L0["F"]))
+            h, w, c = (Ho // 2, Wo // 2, F) if pool else (Ho, Wo, F)
+            continue
         if k == "bconv" and li == 1 and fused:
             KH, KW, pad, F = L["KH"], L["KW"], L["pad"], L["F"]
             Ho, Wo = h + 2 * pad - KH + 1, w + 2 * pad - KW + 1
@@ -155,6 +186,13 @@ def algorithmic_bytes(kind, g, batch):
     the first layer), packed weights, thresholds, flips and packed output
     bits.  No im2col copies, no re-reads."""
     wd = lambda n: (n + 31) // 32
+    if kind == "fconv_bconv":
+        Ho, Wo = g["Ho0"] + 2 * g["pad"] - 2, g["Wo0"] + 2 * g["pad"] - 2
+        Hp, Wp = (Ho // 2, Wo // 2) if g["pool"] else (Ho, Wo)
+        x = batch * g["H"] * g["W"] * 4 * g["C"]
+        w = g["F0"] * 9 * 4 * wd(g["C"]) + g["F"] * 9 * 4 * wd(g["F0"])
+        tf = 4 * (g["F0"] + g["F"]) + 4 * (wd(g["F0"]) + wd(g["F"]))
+        return x + w + tf + batch * Hp * Wp * 4 * wd(g["F"])
     if kind in ("fconv", "bconv", "bconv_input"):
         Ho = g["H"] + 2 * g["pad"] - g["KH"] + 1
         Wo = g["W"] + 2 * g["pad"] - g["KW"] + 1
@@ -294,6 +332,16 @@ def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
         wl = dev_layer[1]
         fn = lambda: bnn.bnn_bconv2d_input(desc, g["mode"], x, off, wl["w"], wl["thr"],
                                            wl.get("flip"), want_sums=False, out_bits=ob)
+    elif kind == "fconv_bconv":
+        d0 = bnn.conv_desc(batch, g["H"], g["W"], g["C"], g["F0"], 3, 3, 1, g["pad0"], 0)
+        d1 = bnn.conv_desc(batch, g["Ho0"], g["Wo0"], g["F0"], g["F"], 3, 3, 1, g["pad"],
+                           g["pool"])
+        Ho, Wo, Hp, Wp = bnn.bnn_conv_output_dims(d1)
+        ob = torch.empty((batch, Hp, Wp, bnn.words(g["F"])), dtype=torch.int32, device="cuda")
+        x = torch.randn((batch, g["H"], g["W"], g["C"]), device="cuda", generator=gen)
+        l0, l1 = dev_layer
+        fn = lambda: bnn.bnn_fconv_bconv2d(d0, d1, x, l0["w"], l0["thr"], l0.get("flip"),
+                                           l1["w"], l1["thr"], l1.get("flip"), out_bits=ob)
     elif kind in ("fconv", "bconv"):
         desc = bnn.conv_desc(batch, g["H"], g["W"], g["C"], g["F"], g["KH"], g["KW"], 1,
                              g["pad"], g["pool"])
@@ -382,7 +430,7 @@ def main():
     wl = WORKLOADS[args.workload]
     batch, H, W, C = wl["batch"], wl["H"], wl["W"], wl["C"]
     layers = net_layers(wl["cfg"])
-    shapes = layer_shapes(layers, H, W, C)
+    shapes = layer_shapes(layers, H, W, C, batch)
     bin_macs_img = sum(s[3] for s in shapes)
     ops_per_step = 2 * bin_macs_img * batch
 
@@ -464,18 +512,23 @@ def main():
     per_layer = []
     saved_algo = os.environ.get("BNN_ALGO")
     for name, kind, g, macs in shapes:
-        dl = (dev_layers[0], dev_layers[1]) if kind == "bconv_input" else dev_layers[g["li"]]
+        dl = ((dev_layers[0], dev_layers[1]) if kind in ("bconv_input", "fconv_bconv")
+              else dev_layers[g["li"]])
         ms = time_layer(bnn, kind, g, batch, dl, args.layer_reps, torch)
-        os.environ["BNN_ALGO"] = "valu"
-        ms_valu = time_layer(bnn, kind, g, batch, dl, args.layer_reps, torch)
-        if saved_algo is None:
-            del os.environ["BNN_ALGO"]
-        else:
-            os.environ["BNN_ALGO"] = saved_algo
-        row = {"layer": name, "ms": round(ms, 5), "ms_valu": round(ms_valu, 5)}
+        ms_valu = None
+        if kind != "fconv_bconv":  # a matrix-core kernel only (no vector-ALU form)
+            os.environ["BNN_ALGO"] = "valu"
+            ms_valu = time_layer(bnn, kind, g, batch, dl, args.layer_reps, torch)
+            if saved_algo is None:
+                del os.environ["BNN_ALGO"]
+            else:
+                os.environ["BNN_ALGO"] = saved_algo
+        row = {"layer": name, "ms": round(ms, 5),
+               "ms_valu": round(ms_valu, 5) if ms_valu is not None else None}
         if macs:
             row["GOPS"] = round(2 * macs * batch / (ms * 1e-3) / 1e9, 1)
-            row["GOPS_valu"] = round(2 * macs * batch / (ms_valu * 1e-3) / 1e9, 1)
+            if ms_valu is not None:
+                row["GOPS_valu"] = round(2 * macs * batch / (ms_valu * 1e-3) / 1e9, 1)
         per_layer.append(row)
     dom_i = max(range(len(shapes)), key=lambda i: per_layer[i]["ms"])
     dom_ms = per_layer[dom_i]["ms"]
@@ -486,6 +539,10 @@ def main():
         fmacs = batch * (g["H"] + 2 * g["pad"] - g["KH"] + 1) * (g["W"] + 2 * g["pad"] - g["KW"] + 1) \
             * g["F"] * g["KH"] * g["KW"] * g["C"]
         dom_ops, bound, peak, unit = 2 * fmacs, "mfma", MFMA_FP16_PEAK_TFLOPS, "TFLOP/s"
+    elif kind == "fconv_bconv":
+        # the binary second layer on fp4 MFMA is the counted work; the fused
+        # fp32 first layer (fp16 hi/lo MFMA) is reported beside it
+        dom_ops, bound, peak, unit = 2 * macs * batch, "mfma", MFMA_FP4_PEAK_TFLOPS, "TFLOP/s"
     elif kind in ("bconv", "bfc", "bfc_logits") and (g.get("C", g.get("K", 0)) % 64 == 0) \
             and not (kind != "bconv" and batch <= 16):
         # binary layer on fp4 MFMA: one fp4 multiply-accumulate per bit-MAC
@@ -494,6 +551,12 @@ def main():
         dom_ops, bound, peak, unit = 2 * macs * batch, "alu", VALU_PEAK_TOPS, "TOP/s"
     achieved_tops = dom_ops / (dom_ms * 1e-3) / 1e12
     dom_bytes = algorithmic_bytes(kind, g, batch)
+    extra_roofline = {}
+    if kind == "fconv_bconv":
+        fmacs0 = batch * g["Ho0"] * g["Wo0"] * g["F0"] * 9 * g["C"]
+        extra_roofline["first_layer_fp16_tflops"] = round(2 * fmacs0 / (dom_ms * 1e-3) / 1e12, 3)
+        extra_roofline["first_layer_fp16_frac"] = round(
+            2 * fmacs0 / (dom_ms * 1e-3) / 1e12 / MFMA_FP16_PEAK_TFLOPS, 5)
 
     result = {
         "metric": "binary conv GOPS (2 ops per bit-MAC) and images/s at batch 1 and 64",
@@ -511,7 +574,7 @@ def main():
         "config": {"workload": args.workload, "batch": batch, "input": "%dx%dx%d fp32" % (H, W, C),
                    "binary_ops_per_step": ops_per_step},
         "images_per_s": round(batch / (ms_per_step * 1e-3), 1),
-        "launch": "bnn_forward, one kernel per layer",
+        "launch": "bnn_forward: one kernel per layer, the first two layers fused into one",
         "hip_graph": {"ms_per_step": round(ms_graph, 5),
                       "value": round(ops_per_step / (ms_graph * 1e-3) / 1e9, 1),
                       "batch1_mean_us": round(float(per_img_us_graph.mean()), 3)},
@@ -526,7 +589,7 @@ def main():
                      "algorithmic_bytes": dom_bytes,
                      "frac_of_valu_xor_popcount_peak":
                          round(achieved_tops / VALU_PEAK_TOPS, 4) if kind != "fconv" else None,
-                     "valu_xor_popcount_peak_TOPS": VALU_PEAK_TOPS},
+                     "valu_xor_popcount_peak_TOPS": VALU_PEAK_TOPS, **extra_roofline},
     }
     if not args.no_paper_net:
         result["paper_net"] = paper_net_latency(bnn, torch, np, max(50, min(args.b1_images, 1000)))

@@ -58,7 +58,7 @@
 extern "C" {
 #endif
 
-#define BNN_ABI_VERSION 2
+#define BNN_ABI_VERSION 3
 
 typedef enum bnn_status {
   BNN_OK = 0,
@@ -209,6 +209,33 @@ bnn_status bnn_bconv2d_input(const bnn_conv_desc* d, int32_t mode,
                              uint32_t* out_bits, hipStream_t stream);
 
 /*
+ * The real-valued first layer (bnn_fconv2d_binw) and a binary 3x3 conv over
+ * its output bits (bnn_bconv2d) in one launch, the first layer's bits never
+ * leaving the chip (the BCNN of Table I, first two layers).  The result
+ * equals bnn_fconv2d_binw followed by bnn_bconv2d, bit for bit, whenever the
+ * first layer's sums are exact (see bnn_fconv2d_binw).
+ *   d0        the first layer: 3x3, C <= 4, F = 64 or 128, no pooling,
+ *             pad 0 or 1.
+ *   d1        the second: N, H, W equal to d0's N and output Ho, Wo; 3x3,
+ *             C = d0's F, F = 64 or 128, pad 0 or 1, pool 0 or 2.
+ *   x         [N][H][W][C] fp32 image.
+ *   w0, thr0, flip0   the first layer's packed weights [F0][3][3][1], int32
+ *             thresholds [F0] and flip words [F0 / 32] (flip0 may be NULL).
+ *   w1, thr1, flip1   the second layer's [F1][3][3][F0 / 32], [F1],
+ *             [F1 / 32] (flip1 may be NULL).
+ *   out_bits  [N][Hp][Wp][F1 / 32] u32, the second layer's bits.
+ * Shapes outside the above give BNN_ERR_UNSUPPORTED.  x, w0, w1 and out_bits
+ * 16-byte aligned.  Errors: BNN_ERR_NULL, BNN_ERR_SHAPE, BNN_ERR_ALIGN,
+ * BNN_ERR_UNSUPPORTED, BNN_ERR_HIP.
+ */
+bnn_status bnn_fconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc* d1,
+                             const float* x, const uint32_t* w0,
+                             const int32_t* thr0, const uint32_t* flip0,
+                             const uint32_t* w1, const int32_t* thr1,
+                             const uint32_t* flip1, uint32_t* out_bits,
+                             hipStream_t stream);
+
+/*
  * Binary fully-connected layer / GEMM (Sec. III-B, Eq. 4):
  *   S[m][n] = K - 2 * sum_j popcount(A[m][j] XOR B[n][j])   (valid bits only)
  *   A         [M][Kw] u32, Kw = ceil(K / 32): M packed input vectors.
@@ -266,10 +293,16 @@ bnn_status bnn_forward_workspace_size(const bnn_layer* layers,
 /*
  * Run the chain on input [batch][H][W][C] fp32 and write int32 logits
  * [batch][N_last] (Table I/II: conv, pool, ..., FC layers).  One kernel per
- * layer on `stream`, with two exceptions:
+ * layer on `stream`, with three exceptions:
  *  - an input layer followed by a BCONV whose window fits
  *    bnn_bconv2d_input runs as that one kernel (environment BNN_PATCH=0
  *    keeps them apart);
+ *  - an FCONV_BINW layer (3x3, at most 4 channels, 64 or 128 filters, no
+ *    pooling) followed by a 3x3 BCONV of 64 or 128 filters runs as one
+ *    kernel that keeps the first layer's bits in LDS (bnn_fconv_bconv2d)
+ *    when that kernel has at least 32 workgroups of 8 x 32 output pixels,
+ *    e.g. 8 images of 32 x 32 (environment BNN_FUSE_FIRST=0 keeps them
+ *    apart, =1 fuses at any size);
  *  - a run of 2-4 consecutive FC layers of at most 8192 weight words each,
  *    at batch <= 128, runs as one kernel that keeps the intermediate bits of
  *    each row in LDS (environment BNN_FC_CHAIN=0 launches them one by one).

@@ -34,7 +34,7 @@ INPUT_LBP = 2
 # Every symbol include/bnn.h declares.
 EXPORTED = ["bnn_last_error", "bnn_abi_version", "bnn_pack_bits", "bnn_conv_output_dims",
             "bnn_bconv2d", "bnn_fconv2d_binw", "bnn_binarize_input", "bnn_bconv2d_input",
-            "bnn_bgemm",
+            "bnn_fconv_bconv2d", "bnn_bgemm",
             "bnn_forward_workspace_size", "bnn_forward"]
 
 
@@ -81,6 +81,8 @@ def load(path: str = LIB_PATH):
     lib.bnn_bgemm.argtypes = [i64, i64, i64, P, P, P, P, P, P, P]
     lib.bnn_binarize_input.argtypes = [i32, P, P, i32, i32, i32, i32, P, P]
     lib.bnn_bconv2d_input.argtypes = [ctypes.POINTER(ConvDesc), i32, P, P, P, P, P, P, P, P]
+    lib.bnn_fconv_bconv2d.argtypes = [ctypes.POINTER(ConvDesc), ctypes.POINTER(ConvDesc),
+                                      P, P, P, P, P, P, P, P, P]
     lib.bnn_forward_workspace_size.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32,
                                                ctypes.POINTER(ctypes.c_size_t)]
     lib.bnn_forward.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32, P, P,
@@ -234,6 +236,30 @@ def bnn_bconv2d_input(desc: ConvDesc, mode, x, offset, w, thr=None, flip=None, w
     return out_sums, out_bits
 
 
+def bnn_fconv_bconv2d(desc0: ConvDesc, desc1: ConvDesc, x, w0, thr0, flip0, w1, thr1,
+                      flip1=None, out_bits=None, stream=None):
+    """The real-valued first layer and a binary 3x3 conv over its bits in one
+    launch (the first two layers of Table I's BCNN): returns the second
+    layer's packed bits [N, Hp, Wp, F1/32], the same as bnn_fconv2d_binw
+    followed by bnn_bconv2d."""
+    lib = load()
+    _, _, Hp, Wp = bnn_conv_output_dims(desc1)
+    _dev(x, torch.float32, "x")
+    _u32(w0)
+    _u32(w1)
+    thr0 = _dev(thr0, torch.int32, "thr0")
+    thr1 = _dev(thr1, torch.int32, "thr1")
+    flip0 = _dev(flip0, torch.int32, "flip0")
+    flip1 = _dev(flip1, torch.int32, "flip1")
+    if out_bits is None:
+        out_bits = torch.empty((desc1.N, Hp, Wp, words(desc1.F)), dtype=torch.int32,
+                               device=x.device)
+    _check(lib.bnn_fconv_bconv2d(ctypes.byref(desc0), ctypes.byref(desc1), _ptr(x), _ptr(w0),
+                                 _ptr(thr0), _ptr(flip0), _ptr(w1), _ptr(thr1), _ptr(flip1),
+                                 _ptr(out_bits), _stream(stream)))
+    return out_bits
+
+
 def bnn_bgemm(A, B, K, thr=None, flip=None, want_sums=True, want_bits=True, out_sums=None,
               out_bits=None, stream=None):
     """Binary GEMM / FC (Sec. III-B): A [M,Kw], B [N,Kw] packed -> sums [M,N],
@@ -305,6 +331,7 @@ pack_bits = bnn_pack_bits
 bconv2d = bnn_bconv2d
 fconv2d_binw = bnn_fconv2d_binw
 bconv2d_input = bnn_bconv2d_input
+fconv_bconv2d = bnn_fconv_bconv2d
 binarize_input = bnn_binarize_input
 bgemm = bnn_bgemm
 forward = bnn_forward

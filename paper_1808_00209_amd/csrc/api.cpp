@@ -136,7 +136,13 @@ bnn_status gemm_launch(int64_t M, int64_t N, int64_t K, const uint32_t* A,
                        const uint32_t* B, const int32_t* thr,
                        const uint32_t* flip, int32_t* sums, uint32_t* bits,
                        hipStream_t s) {
-  if (M <= 16)
+  // At most 2 rows go to the vector-ALU GEMV, whose time grows with every
+  // row; from 3 rows on the matrix-core conv kernel (a 1 x M image with 1x1
+  // filters) is as fast or faster, and 3x faster at 16 rows (measured on the
+  // FC shapes of the networks here).  BNN_GEMV_MAX_ROWS (0..16) overrides.
+  const char* e = getenv("BNN_GEMV_MAX_ROWS");
+  const int64_t gemv_rows = e ? atoll(e) : 2;
+  if (M <= gemv_rows && M <= 16)
     return hip_status(bnn::launch_bgemv_valu(M, N, K, A, B, thr, flip, sums, bits, s),
                       "bgemm (gemv) launch");
   // M rows of A are a 1 x M image with K channels; B holds N 1x1 filters.
@@ -280,6 +286,39 @@ bnn_status bnn_bconv2d_input(const bnn_conv_desc* d, int32_t mode, const float* 
                       "bconv2d_input launch");
   } catch (...) {
     return fail(BNN_ERR_HIP, "bconv2d_input: unexpected C++ exception");
+  }
+}
+
+bnn_status bnn_fconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc* d1, const float* x,
+                             const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
+                             const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
+                             uint32_t* out_bits, hipStream_t stream) {
+  try {
+    bnn::ConvGeom g0, g1;
+    bnn_status st = conv_geom(d0, &g0);
+    if (st != BNN_OK) return st;
+    st = conv_geom(d1, &g1);
+    if (st != BNN_OK) return st;
+    if (g1.N != g0.N || g1.H != g0.Hp || g1.W != g0.Wp || g1.C != g0.F)
+      return fail(BNN_ERR_SHAPE,
+                  "fconv_bconv2d: second layer input %dx%dx%dx%d does not match the first "
+                  "layer's output %dx%dx%dx%d",
+                  g1.N, g1.H, g1.W, g1.C, g0.N, g0.Hp, g0.Wp, g0.F);
+    if (!bnn::fconv_bconv_supported(g0, g1))
+      return fail(BNN_ERR_UNSUPPORTED,
+                  "fconv_bconv2d: needs 3x3 convs, first layer C <= 4, 64 or 128 filters and "
+                  "no pooling, second layer 64 or 128 filters, pads 0 or 1");
+    if (!w1) return fail(BNN_ERR_NULL, "fconv_bconv2d: w1 is NULL");
+    if (!thr0) return fail(BNN_ERR_NULL, "fconv_bconv2d: thr0 is NULL");
+    if (!out_bits) return fail(BNN_ERR_NULL, "fconv_bconv2d: out_bits is NULL");
+    if (!aligned16(w1)) return fail(BNN_ERR_ALIGN, "fconv_bconv2d: w1 must be 16-byte aligned");
+    st = check_outputs(x, w0, thr1, nullptr, out_bits);
+    if (st != BNN_OK) return st;
+    return hip_status(bnn::launch_fconv_bconv(g0, g1, x, w0, thr0, flip0, w1, thr1, flip1,
+                                              out_bits, stream),
+                      "fconv_bconv2d launch");
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "fconv_bconv2d: unexpected C++ exception");
   }
 }
 
@@ -487,8 +526,14 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
       if (conv_geom(&d0, &g_first) == BNN_OK) {  // (the chain is validated above)
         bnn_conv_desc d1{batch, g_first.Hp, g_first.Wp, l1.C, l1.F,
                          l1.KH, l1.KW, l1.stride, l1.pad, l1.pool};
+        // Below 32 workgroups of the fused kernel (8 images of 32 x 32) the two
+        // launches are faster: the fused kernel's time is one workgroup's
+        // critical path, which more workgroups do not shorten.
+        // BNN_FUSE_FIRST=1 fuses at any size, 0 never.
+        const bool forced = e && strcmp(e, "1") == 0;
         fuse_first = !(e && strcmp(e, "0") == 0) && conv_geom(&d1, &g1) == BNN_OK &&
-                     use_mfma(g1) && bnn::fconv_bconv_supported(g_first, g1);
+                     use_mfma(g1) && bnn::fconv_bconv_supported(g_first, g1) &&
+                     (forced || bnn::fconv_bconv_workgroups(g1) >= 32);
       }
     }
     int cur = 0;  // buffer holding the current packed activations

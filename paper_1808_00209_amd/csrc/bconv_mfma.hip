@@ -95,7 +95,6 @@ struct Mfma32Args {
   int32_t in_bytes;  // raw-buffer ranges
   int32_t w_bytes;
   FastDiv div_w, div_h;  // Wo, Ho (or Wp, Hp when pooling)
-  int32_t pblocks;   // workgroups along the pixels
   int32_t xcd_map;   // 1: one-dimensional grid in the XCD order of block_tile
   FastDiv div_f;     // filter tiles along the filters
   FastDiv div_c;     // word chunks per tap (Cw / (2 VW))
@@ -109,20 +108,19 @@ struct Mfma32Args {
 // fetched into one L2, and each output row (one piece per filter tile) is
 // complete in that L2 before it is written back.  Otherwise (a 2-D grid,
 // pixel blocks varying fastest) a row's pieces come from workgroups far
-// apart in time on all 8 XCDs and are written back piece by piece.  Returns
-// false for the padding workgroups past the last pixel block.
-__device__ __forceinline__ bool block_tile(const Mfma32Args& a, int& pb, int& ft) {
-  if (a.xcd_map) {
-    const uint32_t b = blockIdx.x;
-    const uint32_t k = b >> 3;
-    const uint32_t q = fdiv(k, a.div_f);
-    ft = static_cast<int>(k - q * a.div_f.d);
-    pb = static_cast<int>(q * 8 + (b & 7));
-    return pb < a.pblocks;
-  }
-  pb = blockIdx.x;
-  ft = blockIdx.y;
-  return true;
+// apart in time on all 8 XCDs and are written back piece by piece.
+// The padding workgroups past the last pixel block run through with every
+// pixel invalid (their loads read the pad word, their stores are skipped):
+// an early return would be a branch on a kernel argument that makes the
+// kernel wait for that argument before it even loads the others.
+__device__ __forceinline__ void block_tile(const Mfma32Args& a, int& pb, int& ft) {
+  const uint32_t b = blockIdx.x;
+  const uint32_t k = b >> 3;
+  const uint32_t q = fdiv(k, a.div_f);
+  const int ftx = static_cast<int>(k - q * a.div_f.d);
+  const int pbx = static_cast<int>(q * 8 + (b & 7));
+  pb = a.xcd_map ? pbx : static_cast<int>(blockIdx.x);
+  ft = a.xcd_map ? ftx : static_cast<int>(blockIdx.y);
 }
 
 // This lane's pixel in each of the TP 32-pixel tiles of a wave: byte offset
@@ -401,7 +399,7 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
   const int h = lane >> 5;   // k half (operands) / row quad (result)
   const int c = lane & 31;   // operand row / column within a 32-tile
   int pb, ft;
-  if (!block_tile(a, pb, ft)) return;
+  block_tile(a, pb, ft);
   const int p0 = (KS == 1 ? pb * 4 + wave : pb) * 64;
   const int f0 = ft * (32 * TF);
   const int nchunk = a.Cw / (2 * VW);
@@ -562,7 +560,7 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
   const int h = lane >> 5;
   const int c = lane & 31;
   int pb, ft;
-  if (!block_tile(a, pb, ft)) return;
+  block_tile(a, pb, ft);
   const int p0 = (pb * 4 + wave) * 64;
   const int f0 = ft * (32 * TF);
   const int nchunk = a.Cw / (2 * VW);
@@ -707,9 +705,12 @@ int env_int(const char* name, int dflt) {
 
 // Grid of `pblocks` pixel blocks x `fy` filter tiles: one-dimensional in the
 // XCD order of block_tile (pixel blocks padded to a multiple of 8), or 2-D.
+// The XCD order needs at least 8 pixel blocks: with fewer it would leave
+// XCDs idle (all filter tiles of pixel block 0 on XCD 0), while the 2-D grid
+// spreads the filter tiles over the XCDs.
 dim3 tile_grid(Mfma32Args& a, unsigned pblocks, unsigned fy) {
-  a.pblocks = static_cast<int32_t>(pblocks);
   a.div_f = make_fastdiv(fy);
+  if (pblocks < 8) a.xcd_map = 0;
   if (a.xcd_map) return dim3((pblocks + 7) / 8 * 8 * fy);
   return dim3(pblocks, fy);
 }

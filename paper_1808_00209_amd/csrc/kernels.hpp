@@ -56,8 +56,8 @@ hipError_t launch_bconv_patch(const ConvGeom& g, int mode, const float* x,
                               const int32_t* thr, const uint32_t* flip,
                               int32_t* sums, uint32_t* bits, hipStream_t s);
 
-// Binary GEMM for a handful of rows (M <= 16): a wave per two output
-// columns, its lanes along K, a block per 32 columns.
+// Binary GEMM for a handful of rows (M <= 16; bnn_bgemm uses it for M <= 2):
+// a wave per two output columns, its lanes along K, a block per 32 columns.
 hipError_t launch_bgemv_valu(int64_t M, int64_t N, int64_t K,
                              const uint32_t* A, const uint32_t* B,
                              const int32_t* thr, const uint32_t* flip,
@@ -75,6 +75,7 @@ hipError_t launch_fconv_binw(const ConvGeom& g, const float* in,
 // (3x3 over g0's output, 64 or 128 filters, optional 2x2 pooling).  Writes
 // the second layer's packed bits; both thr must be non-null.
 bool fconv_bconv_supported(const ConvGeom& g0, const ConvGeom& g1);
+int64_t fconv_bconv_workgroups(const ConvGeom& g1);
 hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const float* in,
                               const uint32_t* w0, const int32_t* thr0,
                               const uint32_t* flip0, const uint32_t* w1,

@@ -1,6 +1,7 @@
 """GPU parity of the fused first-layer kernel (the real-valued first conv and
 the binary 3x3 conv after it in one launch, the first layer's bits kept in
-LDS) inside bnn_forward, against the two separate launches and the oracle.
+LDS), through its own entry point bnn_fconv_bconv2d and inside bnn_forward,
+against the two separate launches and the oracle.
 
 Each net is the pair of convs followed by a logits layer over the flattened
 output; every logit is a sum of +-1 products, so any differing bit of the
@@ -14,7 +15,7 @@ import torch
 
 import oracle
 from paper_1808_00209_amd import bnn, synth
-from paper_1808_00209_amd.device import to_device, upload_network
+from paper_1808_00209_amd.device import to_device, upload_layer, upload_network, words_u32
 
 pytestmark = pytest.mark.gpu
 
@@ -72,3 +73,25 @@ def test_fused_first_cifar_batch64_sampled(monkeypatch):
     assert np.array_equal(got, ref)
     pick = [0, 37, 63]
     assert np.array_equal(got[pick], oracle.forward(layers, x[pick]))
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_fconv_bconv2d_entry_point(name):
+    """bnn_fconv_bconv2d against bnn_fconv2d_binw + bnn_bconv2d and against
+    the oracle's bits of the second layer (Eq. 2 packing)."""
+    H, W, C0, F0, pad0, F1, pad1, pool = CASES[name]
+    N = 3
+    layers = _net(name)[:2]
+    x = synth.dyadic_normal(synth.rng(9, 91, synth.T_X), (N, H, W, C0))
+    xd = to_device(x)
+    l0, l1 = (upload_layer(L) for L in layers)
+    Ho0, Wo0 = H + 2 * pad0 - 2, W + 2 * pad0 - 2
+    d0 = bnn.conv_desc(N, H, W, C0, F0, 3, 3, 1, pad0, 0)
+    d1 = bnn.conv_desc(N, Ho0, Wo0, F0, F1, 3, 3, 1, pad1, pool)
+    got = bnn.bnn_fconv_bconv2d(d0, d1, xd, l0["w"], l0["thr"], l0["flip"], l1["w"], l1["thr"],
+                                l1["flip"])
+    _, b0 = bnn.bnn_fconv2d_binw(d0, xd, l0["w"], l0["thr"], l0["flip"], want_sums=False)
+    _, b1 = bnn.bnn_bconv2d(d1, b0, l1["w"], l1["thr"], l1["flip"], want_sums=False)
+    torch.cuda.synchronize()
+    assert np.array_equal(words_u32(got), words_u32(b1))
+    assert np.array_equal(words_u32(got), oracle.pack_eq2(oracle.forward(layers, x)))

@@ -313,6 +313,26 @@ def test_bgemm_shapes_bit_exact(case, algo):
     assert np.array_equal(B, Br)
 
 
+GEMV_CASES = [(1, 1, 1), (2, 33, 31), (3, 100, 33), (5, 1024, 8192), (8, 64, 4100),
+              (12, 10, 1024), (16, 1024, 8192), (16, 4, 18432)]
+
+
+@pytest.mark.parametrize("case", GEMV_CASES, ids=[str(c) for c in GEMV_CASES])
+def test_bgemv_all_row_counts_bit_exact(case, monkeypatch):
+    """The vector-ALU GEMV kernel at every row count it supports (1..16);
+    bnn_bgemm sends it only M <= 2 by default, BNN_GEMV_MAX_ROWS=16 forces it."""
+    monkeypatch.setenv("BNN_GEMV_MAX_ROWS", "16")
+    M, N, K = case
+    rng = np.random.default_rng(M * 7907 + N * 29 + K)
+    a = _pm1(rng, (M, K))
+    L = dict(w=_pm1(rng, (N, K)), thr=rng.integers(-8, 9, N).astype(np.int32),
+             flip=rng.integers(0, 2, N).astype(np.uint8))
+    S, B = _run_gemm(a, L, garble=True)
+    Sr, Br = _oracle_gemm(a, L)
+    assert np.array_equal(S, Sr)
+    assert np.array_equal(B, Br)
+
+
 # ---------------------------------------------------------- fp32 1st layer -
 @pytest.mark.parametrize("pool", [0, 2])
 @pytest.mark.parametrize("N,H,W,C,F", [(2, 32, 32, 3, 128), (1, 7, 5, 3, 128), (1, 9, 33, 3, 40),
