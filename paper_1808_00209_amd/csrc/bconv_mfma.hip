@@ -27,6 +27,7 @@
 
 #include "fp4_expand.hpp"
 #include "kernels.hpp"
+#include "lane_ops.hpp"
 
 namespace bnn {
 namespace {
@@ -310,11 +311,10 @@ __device__ __forceinline__ void epi_bits(const Mfma32Args& a, v16f (&acc)[TF][TP
         }
         wd |= nib << (28 - 8 * g - 4 * h);  // nib < 16: four bits shifted into 0
       }
-      wd |= __shfl_xor(wd, 32);
+      wd = or_xor32(wd);
       wd = (wd ^ fx[tf]) & fm[tf];
       if constexpr (POOL) {
-        wd |= __shfl_xor(wd, 1);
-        wd |= __shfl_xor(wd, 2);
+        wd = or_quad(wd);
       }
       word[tf] = wd;
     }

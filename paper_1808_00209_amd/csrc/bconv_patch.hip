@@ -28,6 +28,7 @@
 // uses quad shuffles as in the other binary kernels.
 #include "bnn.h"
 #include "kernels.hpp"
+#include "lane_ops.hpp"
 
 namespace bnn {
 namespace {
@@ -260,8 +261,7 @@ __global__ __launch_bounds__(256) void bconv_patch_kernel(PatchArgs a) {
         if (a.flip) word ^= a.flip[fw];
         if (fw == a.Fw - 1) word &= tail_mask(a.F);
         if constexpr (POOL) {
-          word |= __shfl_xor(word, 1);
-          word |= __shfl_xor(word, 2);
+          word = or_quad(word);
           if ((t & 3) == 0 && (i >> 1) < Hp && (j >> 1) < Wp)
             a.bits[((static_cast<size_t>(n) * Hp + (i >> 1)) * Wp + (j >> 1)) * a.Fw + fw] = word;
         } else {

@@ -12,6 +12,7 @@
 #include <string.h>
 
 #include "kernels.hpp"
+#include "lane_ops.hpp"
 
 namespace bnn {
 namespace {
@@ -102,8 +103,7 @@ __global__ __launch_bounds__(256) void fconv_binw_kernel(FconvArgs a) {
     if (a.flip) word ^= a.flip[fg];
     if (!FULL && nf < 32) word &= ~0u << (32 - nf);
     if constexpr (POOL) {
-      word |= __shfl_xor(word, 1);
-      word |= __shfl_xor(word, 2);
+      word = or_quad(word);
       if ((lane & 3) == 0 && valid) a.bits[static_cast<size_t>(item) * a.Fw + fg] = word;
     } else {
       if (valid) a.bits[static_cast<size_t>(item) * a.Fw + fg] = word;
@@ -506,15 +506,13 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
         }
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        word[h] |= __shfl_xor(word[h], 16);
-        word[h] |= __shfl_xor(word[h], 32);
+        word[h] = or_xor32(or_xor16(word[h]));
         if (FULL || w0 + h < a.Fw) {
           word[h] ^= fll[2 * g + h];
           if (!FULL && w0 + h == a.Fw - 1) word[h] &= tail_mask(a.F);
         }
         if constexpr (POOL) {
-          word[h] |= __shfl_xor(word[h], 1);
-          word[h] |= __shfl_xor(word[h], 2);
+          word[h] = or_quad(word[h]);
         }
       }
       const int i = i0 + pr[tp], j = j0 + pc[tp];

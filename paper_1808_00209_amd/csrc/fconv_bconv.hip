@@ -25,6 +25,7 @@
 
 #include "fp4_expand.hpp"
 #include "kernels.hpp"
+#include "lane_ops.hpp"
 
 namespace bnn {
 namespace {
@@ -170,8 +171,7 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
             word |= static_cast<uint32_t>(on) << (31 - fl);
           }
         }
-        word |= __shfl_xor(word, 16);
-        word |= __shfl_xor(word, 32);
+        word = or_xor32(or_xor16(word));
         word = inside ? word ^ fl0[wi] : 0u;
         if (q == 0 && pv) act[p * CW1 + wi] = word;
       }
@@ -283,11 +283,10 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
           nib = __builtin_amdgcn_alignbit(nib, __float_as_uint(acc[tf][tp][4 * g + r]), 31);
         wd |= nib << (28 - 8 * g - 4 * h);
       }
-      wd |= __shfl_xor(wd, 32);
+      wd = or_xor32(wd);
       wd ^= fx[tf];
       if constexpr (POOL) {
-        wd |= __shfl_xor(wd, 1);
-        wd |= __shfl_xor(wd, 2);
+        wd = or_quad(wd);
       }
       word[tf] = wd;
     }
