@@ -799,7 +799,14 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   const int64_t groups = (a.items + 63) / 64;
   const int64_t ftiles = (g.F + 31) / 32;
   int vw = g.Cw % 8 == 0 ? 4 : g.Cw % 4 == 0 ? 2 : 1;
-  if (vw == 4 && g.KH * g.KW * (g.Cw / 8) < 8) vw = 2;
+  // Windows of at most 4 eight-word chunks (K <= 1024 bits, e.g. FC layers
+  // of 1024 inputs) on grids too small to fill the chip keep 8-word chunks
+  // and no K split: there the split's LDS reduction costs more than it
+  // hides (1024 -> 1024 and 1024 -> 10 at 64 rows: 4.15 and 4.30 us against
+  // 4.42 and 4.57 us with 2-word chunks split 4 ways).
+  const int chunks8 = g.KH * g.KW * (g.Cw / 8);
+  const bool short8 = vw == 4 && chunks8 <= 4 && groups * ftiles < 1024;
+  if (vw == 4 && chunks8 < 8 && !short8) vw = 2;
   vw = env_int("BNN_MFMA_VW", vw);
   if (vw != 1 && vw != 2 && vw != 4) vw = 1;
   if (g.Cw % (2 * vw) != 0) vw = g.Cw % 4 == 0 ? 2 : 1;
@@ -819,7 +826,7 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   if (g.F % 64 != 0 || groups * (g.F / 64) < 1024) {
     tf = 1;
     const int64_t target = vw == 4 ? 1024 : 2048;
-    while (ks < 4 && groups * ftiles * ks < target && iters >= 4 * ks) ks *= 2;
+    while (!short8 && ks < 4 && groups * ftiles * ks < target && iters >= 4 * ks) ks *= 2;
   }
   bool lds = vw <= 2 && tf == 2 && groups * (g.F / 64) >= 4096;
   // Tuning overrides (filter tiles per wave, K split, weights through LDS).
@@ -831,10 +838,13 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   if (tf != 1 && tf != 2) tf = 1;
   if (g.F % (32 * tf) != 0 || (ks > 4 && tf != 1)) tf = 1;
   // Thresholds staged after the main loop on grids of at most 2 waves per
-  // SIMD (2048 waves), at kernel start on larger ones (BNN_MFMA_LATE
-  // overrides).
+  // SIMD (2048 waves) with 32-filter tiles, at kernel start otherwise, where
+  // the accumulators can then start from them (16x16x128 -> 256 and
+  // 16x16x256 -> 256 pool at batch 64: 5.98 / 7.50 us early against
+  // 6.25 / 7.94 us late; 8x8x256 -> 512 with 32-filter tiles: 6.11 us late,
+  // 6.22 us early).  BNN_MFMA_LATE overrides.
   const int64_t waves = (groups + 3) / 4 * 4 * ((g.F + 32 * tf - 1) / (32 * tf));
-  const bool late = env_int("BNN_MFMA_LATE", waves <= 2048 ? 1 : 0) != 0;
+  const bool late = env_int("BNN_MFMA_LATE", waves <= 2048 && tf == 1 ? 1 : 0) != 0;
   if (vw == 4)
     return pool ? launch32<4, true>(a, tf, ks, false, late, s)
                 : launch32<4, false>(a, tf, ks, false, late, s);
