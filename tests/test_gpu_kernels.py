@@ -154,6 +154,12 @@ CONV_CASES = [
     (2, 6, 6, 64, 10, 3, 1, 2),
     (1, 5, 5, 128, 40, 3, 1, 0),
     (3, 4, 7, 192, 70, 1, 0, 0),
+    # grids in the XCD order whose pixel blocks are not a multiple of 8, so
+    # padding workgroups run with no valid pixel: a K split over 36 blocks,
+    # 36 blocks of 4 waves, and 23 pooled blocks with a ragged last one
+    (1, 48, 48, 128, 128, 3, 1, 0),
+    (1, 96, 96, 64, 1024, 1, 0, 0),
+    (2, 40, 72, 64, 1024, 1, 0, 2),
 ]
 
 
