@@ -93,6 +93,9 @@ def parse():
                     help="skip the 5x5 vehicle classifier of Table II under each input binarization")
     ap.add_argument("--no-float-baseline", action="store_true",
                     help="skip the floating-point network timed on the same GPU")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the timing of the other configurations (single conv, FC GEMM, "
+                         "vehicle-shaped net, large layers)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one 256 MiB device-to-device copy (calibrates the "
                          "FETCH_SIZE / WRITE_SIZE counters of a profiling run)")
@@ -390,6 +393,106 @@ def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
     return e0.elapsed_time(e1) / reps
 
 
+def graph_time_us(fn, torch, reps=20):
+    """Mean kernel time (us) of `reps` back-to-back calls replayed from a HIP
+    graph, best of 3 replays."""
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    s = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    side.wait_stream(s)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph, stream=side):
+            for _ in range(reps):
+                fn()
+    s.wait_stream(side)
+    torch.cuda.synchronize()
+    best = float("inf")
+    for _ in range(3):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        graph.replay()
+        e1.record(s)
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1) * 1e3 / reps)
+    return best
+
+
+def config_suite(bnn, torch):
+    """Every configuration besides the workload, on seeded synthetic inputs
+    already on the device: the single binary conv (configuration 1, sums and
+    bits), the FC GEMM (configuration 2, K = 4096 and the tail case 4100,
+    sums and bits), the vehicle-shaped net at batch 256 (configuration 4) and
+    the large layers (configuration 5, bits only, plus A with int32 sums)."""
+    from paper_1808_00209_amd import synth
+    from paper_1808_00209_amd.device import pack_pm1, to_device, upload_layer, upload_network
+    out = {}
+
+    def rec(us, macs, nbytes):
+        tops = 2 * macs / (us * 1e-6) / 1e12
+        return {"us": round(us, 3), "binary_TOPs": round(tops, 1),
+                "frac_fp4_peak": round(tops / MFMA_FP4_PEAK_TFLOPS, 4),
+                "frac_valu_peak": round(tops / VALU_PEAK_TOPS, 4),
+                "algorithmic_bytes": int(nbytes),
+                "frac_hbm_peak": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+
+    def conv_case(name, x, L, sums):
+        N, H, W, C = x.shape
+        desc = bnn.conv_desc(N, H, W, C, L["F"], L["KH"], L["KW"], 1, L["pad"], L.get("pool", 0))
+        Ho, Wo, Hp, Wp = bnn.bnn_conv_output_dims(desc)
+        dl = upload_layer(L)
+        xd = pack_pm1(x)
+        ob = torch.empty((N, Hp, Wp, bnn.words(L["F"])), dtype=torch.int32, device="cuda")
+        os_ = (torch.empty((N, Ho, Wo, L["F"]), dtype=torch.int32, device="cuda")
+               if sums else None)
+        us = graph_time_us(lambda: bnn.bnn_bconv2d(desc, xd, dl["w"], dl["thr"], dl.get("flip"),
+                                                   want_sums=sums, out_sums=os_, out_bits=ob),
+                           torch)
+        macs = N * Ho * Wo * L["F"] * L["KH"] * L["KW"] * C
+        nbytes = (N * H * W * 4 * bnn.words(C) + L["F"] * L["KH"] * L["KW"] * 4 * bnn.words(C)
+                  + 4 * L["F"] + 4 * bnn.words(L["F"]) + N * Hp * Wp * 4 * bnn.words(L["F"])
+                  + (N * Ho * Wo * L["F"] * 4 if sums else 0))
+        out[name] = dict(rec(us, macs, nbytes),
+                         shape="%dx%dx%dx%d -> %d, %dx%d, pad %d%s" % (
+                             N, H, W, C, L["F"], L["KH"], L["KW"], L["pad"],
+                             ", int32 sums + bits" if sums else ", bits"))
+
+    conv_case("cfg1_conv_b1", synth.cfg1_input(), synth.cfg1_layer(), True)
+    for K in (4096, 4100):
+        a, L = synth.cfg2(K)
+        M, N = a.shape[0], L["N"]
+        A, B = pack_pm1(a), pack_pm1(L["w"])
+        thr = to_device(L["thr"], torch.int32)
+        os_ = torch.empty((M, N), dtype=torch.int32, device="cuda")
+        ob = torch.empty((M, bnn.words(N)), dtype=torch.int32, device="cuda")
+        us = graph_time_us(lambda: bnn.bnn_bgemm(A, B, K, thr, None, out_sums=os_, out_bits=ob),
+                           torch)
+        kw = bnn.words(K)
+        nbytes = M * kw * 4 + N * kw * 4 + 4 * N + M * N * 4 + M * bnn.words(N) * 4
+        out["cfg2_gemm_K%d" % K] = dict(rec(us, M * N * K, nbytes),
+                                        shape="%d x %d bits x %d, int32 sums + bits" % (M, K, N))
+    layers, batch = synth.cfg4_net(), 256
+    net = upload_network(layers, 96, 96, 3)
+    xv = to_device(synth.cfg4_input(batch))
+    ws = net.alloc_workspace(batch)
+    lg = torch.empty((batch, layers[-1]["N"]), dtype=torch.int32, device="cuda")
+    us = graph_time_us(lambda: bnn.bnn_forward(net, xv, ws, lg), torch, reps=10)
+    macs = sum(sh[3] for sh in layer_shapes(layers, 96, 96, 3, batch)) * batch
+    out["cfg4_vehicle_net_b256"] = dict(
+        us=round(us, 2), binary_TOPs=round(2 * macs / (us * 1e-6) / 1e12, 1),
+        images_per_s=round(batch / (us * 1e-6), 1),
+        note="bnn_forward replayed from a HIP graph; per-layer figures with "
+             "--workload vehicle_bnn_b256")
+    for name in "ABC":
+        x, L = synth.cfg5_case(name)
+        conv_case("cfg5%s" % name, x, L, False)
+    x, L = synth.cfg5_case("A")
+    conv_case("cfg5A_with_sums", x, L, True)
+    return out
+
+
 def cpu_baseline(layers, cfg, target_s, bin_ops_per_image, max_images=4096):
     """The oracle (all host threads) on a bounded sample of the workload's
     images: sized from a 16-image calibration run to take about target_s."""
@@ -607,6 +710,8 @@ def main():
         result["float_baseline"] = dict(
             fb, note="same layer shapes in floating point (torch conv2d on MIOpen, linear, "
                      "max-pool, hardtanh), random weights, eager launches")
+    if not args.no_configs:
+        result["configs"] = config_suite(bnn, torch)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(layers, wl["cfg"], args.cpu_seconds,
                                               2 * bin_macs_img)
