@@ -98,7 +98,10 @@ struct Mfma32Args {
   FastDiv div_w, div_h;  // Wo, Ho (or Wp, Hp when pooling)
   int32_t xcd_map;   // 1: one-dimensional grid in the XCD order of block_tile
   FastDiv div_f;     // filter tiles along the filters
-  FastDiv div_c;     // word chunks per tap (Cw / (2 VW))
+  FastDiv div_c;     // word chunks per tap (Cc / (2 VW))
+  int32_t Cc;        // words per tap the loop walks: Cw rounded up to whole chunks
+  uint32_t tmask_c;  // valid bits of a pixel's last word (tail_mask(C))
+  int32_t pad_bits;  // bit positions per window past C (KH KW (32 Cc - C))
 };
 
 // The workgroup's pixel block and filter tile.  The workgroups of a launch
@@ -185,7 +188,7 @@ struct Cursor {
     if (l_it + 1 < it1) {
       ++l_it;
       l_cc += 2 * vw;
-      if (l_cc == a.Cw) {
+      if (l_cc == a.Cc) {
         l_cc = 0;
         if (++l_kw == a.KW) {
           l_kw = 0;
@@ -239,7 +242,8 @@ struct EpiParams {
   // 0.5 - thr, the accumulators' start value); a barrier must follow.
   __device__ __forceinline__ void stage(const Mfma32Args& a, float* thl, bool neg) const {
     if (a.bits && threadIdx.x < 32 * TF) {
-      const float t = static_cast<float>(min(max(thr, -a.K - 1), a.K + 1)) - 0.5f;
+      // the sums come out pad_bits too high (zeroed padding positions)
+      const float t = static_cast<float>(min(max(thr, -a.K - 1), a.K + 1) + a.pad_bits) - 0.5f;
       thl[threadIdx.x] = neg ? -t : t;
     }
   }
@@ -351,15 +355,16 @@ __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP
           const int fb = f0 + tf * 32 + 8 * g + 4 * h;  // first of 4 filters
           if (!ftail && (a.F & 3) == 0) {
             int4 t;
-            t.x = static_cast<int>(acc[tf][tp][4 * g + 0]);
-            t.y = static_cast<int>(acc[tf][tp][4 * g + 1]);
-            t.z = static_cast<int>(acc[tf][tp][4 * g + 2]);
-            t.w = static_cast<int>(acc[tf][tp][4 * g + 3]);
+            t.x = static_cast<int>(acc[tf][tp][4 * g + 0]) - a.pad_bits;
+            t.y = static_cast<int>(acc[tf][tp][4 * g + 1]) - a.pad_bits;
+            t.z = static_cast<int>(acc[tf][tp][4 * g + 2]) - a.pad_bits;
+            t.w = static_cast<int>(acc[tf][tp][4 * g + 3]) - a.pad_bits;
             *reinterpret_cast<int4*>(sp + tf * 32 + 8 * g) = t;
           } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-              if (fb + e < a.F) sp[tf * 32 + 8 * g + e] = static_cast<int>(acc[tf][tp][4 * g + e]);
+              if (fb + e < a.F)
+                sp[tf * 32 + 8 * g + e] = static_cast<int>(acc[tf][tp][4 * g + e]) - a.pad_bits;
           }
         }
     }
@@ -391,7 +396,7 @@ __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP
 //        kernel start).  With KS > 1 they always meet after the loop, at the
 //        barrier the partial sums need anyway.
 // Each wave loads and expands its own weight words in registers.
-template <int VW, bool POOL, int TF, int KS, int PD, bool LATE>
+template <int VW, bool POOL, int TF, int KS, int PD, bool LATE, bool TAIL = false>
 __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(Mfma32Args a) {
   constexpr int TP = 2;
   const int lane = threadIdx.x & 63;
@@ -402,7 +407,7 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
   block_tile(a, pb, ft);
   const int p0 = (KS == 1 ? pb * 4 + wave : pb) * 64;
   const int f0 = ft * (32 * TF);
-  const int nchunk = a.Cw / (2 * VW);
+  const int nchunk = a.Cc / (2 * VW);
   const int iters = a.KH * a.KW * nchunk;
   int it0 = 0, it1 = iters;
   if constexpr (KS > 1) {
@@ -446,6 +451,21 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
 #pragma unroll
     for (int tf = 0; tf < TF; ++tf) buf_load<VW>(ww[tf], rw, woff[tf], wsoff);
     load_act<TP, POOL, VW>(aw, a, cur, px, rin);
+    if constexpr (TAIL) {
+      // C not a multiple of 64: words past a pixel's Cw (read from the next
+      // tap or pixel) and the tail bits of its last word are zeroed in both
+      // operands.  Each such position then adds (+1)(+1) = 1 to the sum,
+      // pad_bits per window in all, which the epilogue takes off.
+#pragma unroll
+      for (int v = 0; v < VW; ++v) {
+        const int wi = cur.l_cc + h * VW + v;
+        const uint32_t m = wi < a.Cw - 1 ? ~0u : (wi == a.Cw - 1 ? a.tmask_c : 0u);
+#pragma unroll
+        for (int tf = 0; tf < TF; ++tf) ww[tf][v] &= m;
+#pragma unroll
+        for (int tp = 0; tp < TP; ++tp) aw[tp][v] &= m;
+      }
+    }
     cur.advance(a, VW);
   };
   auto compute = [&](const uint32_t (&ww)[TF][VW], const uint32_t (&aw)[TP][VW]) {
@@ -563,7 +583,7 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
   block_tile(a, pb, ft);
   const int p0 = (pb * 4 + wave) * 64;
   const int f0 = ft * (32 * TF);
-  const int nchunk = a.Cw / (2 * VW);
+  const int nchunk = a.Cc / (2 * VW);
   const int iters = a.KH * a.KW * nchunk;
   const int stages = (iters + kQS - 1) / kQS;
 
@@ -720,6 +740,21 @@ hipError_t launch32(Mfma32Args a, int tf, int ks, bool lds, bool late, hipStream
   const unsigned fy = static_cast<unsigned>((a.F + 32 * tf - 1) / (32 * tf));
   const unsigned groups = static_cast<unsigned>((a.items + 63) / 64);
   if constexpr (VW <= 2) {
+    if (a.pad_bits > 0) {
+      // C not a multiple of 64 (run_mfma: 32-filter tiles, thresholds after
+      // the loop, no LDS staging).
+      if (ks == 1) {
+        const dim3 grid = tile_grid(a, (groups + 3) / 4, fy), block(256);
+        bconv_mfma32_kernel<VW, POOL, 1, 1, 2, true, true><<<grid, block, 0, s>>>(a);
+      } else {
+        const dim3 grid = tile_grid(a, groups, fy), block(64 * ks);
+        if (ks == 2)
+          bconv_mfma32_kernel<VW, POOL, 1, 2, 2, true, true><<<grid, block, 0, s>>>(a);
+        else
+          bconv_mfma32_kernel<VW, POOL, 1, 4, 2, true, true><<<grid, block, 0, s>>>(a);
+      }
+      return hipGetLastError();
+    }
     if (lds) {
       const dim3 grid = tile_grid(a, (groups + 3) / 4, fy), block(256);
       const bool pre = a.bits && !a.sums;
@@ -798,6 +833,11 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   // not when that leaves fewer than 8 iterations to split.
   const int64_t groups = (a.items + 63) / 64;
   const int64_t ftiles = (g.F + 31) / 32;
+  // C not a multiple of 64: the loop walks Cc >= Cw words per tap, whole
+  // chunks of 2 VW words, with the words past Cw zeroed (bconv_mfma32_kernel,
+  // TAIL).  VW = 2 where rows are an even number of words (8-byte aligned
+  // loads), else 1.
+  const bool tail = g.C % 64 != 0;
   int vw = g.Cw % 8 == 0 ? 4 : g.Cw % 4 == 0 ? 2 : 1;
   // Windows of at most 4 eight-word chunks (K <= 1024 bits, e.g. FC layers
   // of 1024 inputs) on grids too small to fill the chip keep 8-word chunks
@@ -805,13 +845,17 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   // hides (1024 -> 1024 and 1024 -> 10 at 64 rows: 4.15 and 4.30 us against
   // 4.42 and 4.57 us with 2-word chunks split 4 ways).
   const int chunks8 = g.KH * g.KW * (g.Cw / 8);
-  const bool short8 = vw == 4 && chunks8 <= 4 && groups * ftiles < 1024;
+  const bool short8 = !tail && vw == 4 && chunks8 <= 4 && groups * ftiles < 1024;
   if (vw == 4 && chunks8 < 8 && !short8) vw = 2;
   vw = env_int("BNN_MFMA_VW", vw);
   if (vw != 1 && vw != 2 && vw != 4) vw = 1;
   if (g.Cw % (2 * vw) != 0) vw = g.Cw % 4 == 0 ? 2 : 1;
-  const int iters = g.KH * g.KW * (g.Cw / (2 * vw));
-  a.div_c = make_fastdiv(static_cast<uint32_t>(g.Cw / (2 * vw)));
+  if (tail) vw = g.Cw % 2 == 0 ? 2 : 1;
+  a.Cc = (g.Cw + 2 * vw - 1) / (2 * vw) * (2 * vw);
+  a.tmask_c = tail_mask(g.C);
+  a.pad_bits = g.KH * g.KW * (32 * a.Cc - g.C);
+  const int iters = g.KH * g.KW * (a.Cc / (2 * vw));
+  a.div_c = make_fastdiv(static_cast<uint32_t>(a.Cc / (2 * vw)));
 
   // Tile shape and K split: 64-filter wave tiles down to ~1 wave per SIMD
   // (1024 waves), then 32-filter tiles with a K split over up to 4 waves
@@ -837,6 +881,11 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   if (ks > 1 || vw == 4) lds = false;
   if (tf != 1 && tf != 2) tf = 1;
   if (g.F % (32 * tf) != 0 || (ks > 4 && tf != 1)) tf = 1;
+  if (tail) {
+    tf = 1;
+    lds = false;
+    if (ks > 4) ks = 4;
+  }
   // Thresholds staged after the main loop on grids of at most 2 waves per
   // SIMD (2048 waves) with 32-filter tiles, at kernel start otherwise, where
   // the accumulators can then start from them (16x16x128 -> 256 and
@@ -844,7 +893,7 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   // 6.25 / 7.94 us late; 8x8x256 -> 512 with 32-filter tiles: 6.11 us late,
   // 6.22 us early).  BNN_MFMA_LATE overrides.
   const int64_t waves = (groups + 3) / 4 * 4 * ((g.F + 32 * tf - 1) / (32 * tf));
-  const bool late = env_int("BNN_MFMA_LATE", waves <= 2048 && tf == 1 ? 1 : 0) != 0;
+  const bool late = tail || env_int("BNN_MFMA_LATE", waves <= 2048 && tf == 1 ? 1 : 0) != 0;
   if (vw == 4)
     return pool ? launch32<4, true>(a, tf, ks, false, late, s)
                 : launch32<4, false>(a, tf, ks, false, late, s);
@@ -858,12 +907,14 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
 }  // namespace
 
 bool bconv_mfma_supported(const ConvGeom& g) {
-  // C a multiple of 64 (whole words, 2 words per k-step), at most 32 taps
-  // (per-lane tap masks), fewer than 2^22 bits per window (the fp32
-  // accumulators, which may start at 0.5 - thr, stay exact), and inputs and
-  // weights under 2 GiB (32-bit byte offsets of the raw buffer loads).
-  return (g.C % 64) == 0 && g.KH * g.KW <= 32 &&
-         static_cast<int64_t>(g.KH) * g.KW * g.C < (int64_t{1} << 22) &&
+  // At least 64 channels (a C that is not a multiple of 64 is padded to
+  // whole chunks, at most half of them padding), at most 32 taps (per-lane
+  // tap masks), fewer than 2^22 bit positions per window, padding included
+  // (the fp32 accumulators, which may start at 0.5 - thr, stay exact), and
+  // inputs and weights under 2 GiB (32-bit byte offsets of the raw buffer
+  // loads).
+  return g.C >= 64 && g.KH * g.KW <= 32 &&
+         static_cast<int64_t>(g.KH) * g.KW * 32 * (g.Cw + 3) < (int64_t{1} << 22) &&
          static_cast<int64_t>(g.N) * g.H * g.W * g.Cw < (int64_t{1} << 29) &&
          static_cast<int64_t>(g.F) * g.KH * g.KW * g.Cw < (int64_t{1} << 29);
 }

@@ -154,6 +154,13 @@ CONV_CASES = [
     (2, 6, 6, 64, 10, 3, 1, 2),
     (1, 5, 5, 128, 40, 3, 1, 0),
     (3, 4, 7, 192, 70, 1, 0, 0),
+    # C >= 64 but not a multiple of 64 on the matrix-core path: words past a
+    # pixel's last one and the last word's tail bits are zeroed (even and odd
+    # word counts, 3x3 and 1x1, pooled)
+    (2, 9, 9, 100, 64, 3, 1, 2),
+    (1, 7, 5, 65, 96, 3, 1, 0),
+    (1, 6, 6, 130, 32, 3, 0, 0),
+    (3, 5, 5, 200, 128, 1, 0, 2),
     # grids in the XCD order whose pixel blocks are not a multiple of 8, so
     # padding workgroups run with no valid pixel: a K split over 36 blocks,
     # 36 blocks of 4 waves, and 23 pooled blocks with a ragged last one
@@ -301,6 +308,7 @@ def test_cfg2_fc_gemm_full_size_bit_exact(K, algo):
 
 
 GEMM_CASES = [(1, 1, 1), (1, 10, 1024), (2, 33, 31), (5, 100, 33), (16, 1024, 8192),
+              (3, 40, 100), (64, 96, 4100), (7, 33, 65),
               (16, 64, 4100), (17, 40, 96), (64, 1024, 8192), (100, 70, 1000), (3, 4, 18432),
               (65, 128, 1024), (300, 64, 18432), (64, 192, 128), (64, 10, 1024),
               (40, 50, 128), (64, 33, 8192), (64, 4, 18432), (256, 1024, 8192)]
