@@ -38,10 +38,15 @@ namespace {
 constexpr uint32_t kOutOfRange = 0x80000000u;
 constexpr int kRsrcWord3 = 0x00020000;
 
-template <int VW>
+// SPLIT: VW separate 4-byte loads, for rows whose word count leaves the
+// chunks without 8- or 16-byte alignment.
+template <int VW, bool SPLIT = false>
 __device__ __forceinline__ void buf_load(uint32_t (&v)[VW], __amdgpu_buffer_rsrc_t r, uint32_t voff,
                                          uint32_t soff) {
-  if constexpr (VW == 4) {
+  if constexpr (SPLIT) {
+#pragma unroll
+    for (int i = 0; i < VW; ++i) v[i] = __builtin_amdgcn_raw_buffer_load_b32(r, voff + 4 * i, soff, 0);
+  } else if constexpr (VW == 4) {
     typedef unsigned int u4 __attribute__((ext_vector_type(4)));
     const u4 t = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
     v[0] = t[0];
@@ -201,7 +206,7 @@ struct Cursor {
 
 // Activation words of the cursor's iteration for the TP pixel tiles; taps
 // outside the image read the out-of-range offset, i.e. the pad word 0.
-template <int TP, bool POOL, int VW>
+template <int TP, bool POOL, int VW, bool SPLIT = false>
 __device__ __forceinline__ void load_act(uint32_t (&aw)[TP][VW], const Mfma32Args& a,
                                          const Cursor& cur, const PixTiles<TP, POOL, VW>& px,
                                          __amdgpu_buffer_rsrc_t rin) {
@@ -212,7 +217,7 @@ __device__ __forceinline__ void load_act(uint32_t (&aw)[TP][VW], const Mfma32Arg
   for (int tp = 0; tp < TP; ++tp) {
     const uint32_t off = (px.tapmask[tp] & bit) ? static_cast<uint32_t>(px.pbase[tp] + dshift)
                                                 : kOutOfRange;
-    buf_load<VW>(aw[tp], rin, off, 0u);
+    buf_load<VW, SPLIT>(aw[tp], rin, off, 0u);
   }
 }
 
@@ -449,8 +454,8 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
   auto load_next = [&](uint32_t (&ww)[TF][VW], uint32_t (&aw)[TP][VW]) {
     const uint32_t wsoff = static_cast<uint32_t>((cur.tap(a) * a.Cw + cur.l_cc) * 4);
 #pragma unroll
-    for (int tf = 0; tf < TF; ++tf) buf_load<VW>(ww[tf], rw, woff[tf], wsoff);
-    load_act<TP, POOL, VW>(aw, a, cur, px, rin);
+    for (int tf = 0; tf < TF; ++tf) buf_load<VW, TAIL>(ww[tf], rw, woff[tf], wsoff);
+    load_act<TP, POOL, VW, TAIL>(aw, a, cur, px, rin);
     if constexpr (TAIL) {
       // C not a multiple of 64: words past a pixel's Cw (read from the next
       // tap or pixel) and the tail bits of its last word are zeroed in both
@@ -739,22 +744,22 @@ template <int VW, bool POOL>
 hipError_t launch32(Mfma32Args a, int tf, int ks, bool lds, bool late, hipStream_t s) {
   const unsigned fy = static_cast<unsigned>((a.F + 32 * tf - 1) / (32 * tf));
   const unsigned groups = static_cast<unsigned>((a.items + 63) / 64);
-  if constexpr (VW <= 2) {
-    if (a.pad_bits > 0) {
-      // C not a multiple of 64 (run_mfma: 32-filter tiles, thresholds after
-      // the loop, no LDS staging).
-      if (ks == 1) {
-        const dim3 grid = tile_grid(a, (groups + 3) / 4, fy), block(256);
-        bconv_mfma32_kernel<VW, POOL, 1, 1, 2, true, true><<<grid, block, 0, s>>>(a);
-      } else {
-        const dim3 grid = tile_grid(a, groups, fy), block(64 * ks);
-        if (ks == 2)
-          bconv_mfma32_kernel<VW, POOL, 1, 2, 2, true, true><<<grid, block, 0, s>>>(a);
-        else
-          bconv_mfma32_kernel<VW, POOL, 1, 4, 2, true, true><<<grid, block, 0, s>>>(a);
-      }
-      return hipGetLastError();
+  if (a.pad_bits > 0) {
+    // C not a multiple of 64 (run_mfma: 32-filter tiles, thresholds after
+    // the loop, no LDS staging).
+    if (ks == 1) {
+      const dim3 grid = tile_grid(a, (groups + 3) / 4, fy), block(256);
+      bconv_mfma32_kernel<VW, POOL, 1, 1, 2, true, true><<<grid, block, 0, s>>>(a);
+    } else {
+      const dim3 grid = tile_grid(a, groups, fy), block(64 * ks);
+      if (ks == 2)
+        bconv_mfma32_kernel<VW, POOL, 1, 2, 2, true, true><<<grid, block, 0, s>>>(a);
+      else
+        bconv_mfma32_kernel<VW, POOL, 1, 4, 2, true, true><<<grid, block, 0, s>>>(a);
     }
+    return hipGetLastError();
+  }
+  if constexpr (VW <= 2) {
     if (lds) {
       const dim3 grid = tile_grid(a, (groups + 3) / 4, fy), block(256);
       const bool pre = a.bits && !a.sums;
@@ -834,9 +839,9 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   const int64_t groups = (a.items + 63) / 64;
   const int64_t ftiles = (g.F + 31) / 32;
   // C not a multiple of 64: the loop walks Cc >= Cw words per tap, whole
-  // chunks of 2 VW words, with the words past Cw zeroed (bconv_mfma32_kernel,
-  // TAIL).  VW = 2 where rows are an even number of words (8-byte aligned
-  // loads), else 1.
+  // chunks of 2 VW words, with the words past Cw zeroed and every word
+  // loaded on its own (bconv_mfma32_kernel, TAIL).  VW is the largest of 4,
+  // 2, 1 whose padding stays within 1/8 of the row.
   const bool tail = g.C % 64 != 0;
   int vw = g.Cw % 8 == 0 ? 4 : g.Cw % 4 == 0 ? 2 : 1;
   // Windows of at most 4 eight-word chunks (K <= 1024 bits, e.g. FC layers
@@ -850,7 +855,11 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   vw = env_int("BNN_MFMA_VW", vw);
   if (vw != 1 && vw != 2 && vw != 4) vw = 1;
   if (g.Cw % (2 * vw) != 0) vw = g.Cw % 4 == 0 ? 2 : 1;
-  if (tail) vw = g.Cw % 2 == 0 ? 2 : 1;
+  if (tail) {
+    vw = 1;
+    for (int t = 4; t >= 2 && vw == 1; t /= 2)
+      if (((g.Cw + 2 * t - 1) / (2 * t) * (2 * t) - g.Cw) * 8 <= g.Cw) vw = t;
+  }
   a.Cc = (g.Cw + 2 * vw - 1) / (2 * vw) * (2 * vw);
   a.tmask_c = tail_mask(g.C);
   a.pad_bits = g.KH * g.KW * (32 * a.Cc - g.C);
@@ -914,7 +923,7 @@ bool bconv_mfma_supported(const ConvGeom& g) {
   // inputs and weights under 2 GiB (32-bit byte offsets of the raw buffer
   // loads).
   return g.C >= 64 && g.KH * g.KW <= 32 &&
-         static_cast<int64_t>(g.KH) * g.KW * 32 * (g.Cw + 3) < (int64_t{1} << 22) &&
+         static_cast<int64_t>(g.KH) * g.KW * 32 * (g.Cw + 7) < (int64_t{1} << 22) &&
          static_cast<int64_t>(g.N) * g.H * g.W * g.Cw < (int64_t{1} << 29) &&
          static_cast<int64_t>(g.F) * g.KH * g.KW * g.Cw < (int64_t{1} << 29);
 }
