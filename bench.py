@@ -42,17 +42,19 @@ _BUILD = ("paper_1808_00209_amd/build.py",
           "72c88ac8739ea58df1e7bf480187bcff54058511792aa1a10abbd4e679e40bd7")
 _FP4 = ("paper_1808_00209_amd/csrc/fp4_expand.hpp",
         "d025e6c895771b0e8c624d6b14e4559aae203e5a519954919d75dea0192da41b")
+_LANE = ("paper_1808_00209_amd/csrc/lane_ops.hpp",
+         "0305f935888de7ac63ef2c712b1733ac8f1d1cc002e8baf7658f1891a84b657c")
 MEASURED_TRAFFIC = {
     ("cifar_bnn_b64", "L0+L1 fconv+bconv 32x32x3->128->128 k3 pool (fused)"): dict(
-        fetch_kib=715.3, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
+        fetch_kib=712.2, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/fconv_bconv.hip",
-                       "7c14d87b99d2d5f1a0c9b0cd1c748b4945d90865c5ac41b4eafec387eead5c3e"),
-                      _FP4, _BUILD])),
+                       "66f4424134e3916390524eb68bad2aeed715bf57ffbf9e210772c350ebbc0766"),
+                      _FP4, _LANE, _BUILD])),
     ("cifar_bnn_b64", "L5 bconv 8x8x512->512 k3 pool"): dict(
-        fetch_kib=1342.5, write_kib=64.0, fetch_scale=2.0, write_scale=1.0,
+        fetch_kib=1340.0, write_kib=64.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/bconv_mfma.hip",
-                       "dfda126b259d44a65604a89d6641d256818d76e103cad597214903fe5b05d698"),
-                      _FP4, _BUILD])),
+                       "83c48183919fed267e8795088937bd0bab3da87c2587c8e46ab2084f26010a6a"),
+                      _FP4, _LANE, _BUILD])),
 }
 
 
