@@ -6,22 +6,28 @@
 // A block owns an 8 x 32 tile of the second layer's output pixels of one
 // image (4 x 16 2x2 windows when it pools) and all of its filters (64 or
 // 128; 4 waves per 64 filters).
-//   1. It stages the fp32 input tile the first layer needs for the
-//      (8 + 2) x (32 + 2) pixels of the second layer's windows (halo of one
-//      pixel), zero outside the image, plus both layers' thresholds and the
-//      first layer's +-1 weight operands.
+//   1. It stages the input tile the first layer needs for the (8 + 2) x
+//      (32 + 2) pixels of the second layer's windows (halo of one pixel),
+//      zero outside the image, with every value split once into two fp16
+//      parts x = hi + lo, plus both layers' thresholds and the first layer's
+//      +-1 weight operands.  All global loads are issued before the first
+//      LDS store.
 //   2. All waves compute the first layer's outputs on that 10 x 34 tile with
-//      v_mfma_f32_16x16x32_f16, every input value split into two fp16 parts
-//      x = hi + lo as in the standalone first-layer kernel (for inputs on the
-//      2^-16 grid with |x| < 8 the fp32 sums are exact in any order), then
-//      threshold / flip and pack them into words in LDS.  Pixels outside the
-//      first layer's output are the pad word 0 (-1) of the second conv.
+//      v_mfma_f32_16x16x32_f16 on the hi and lo parts (for inputs on the
+//      2^-16 grid with |x| < 8 the fp32 sums are exact in any order), take
+//      the sign bits of S - thr, OR the four lane rows' parts of the words
+//      together (lane row q then holds word q of its pixel), flip, and store
+//      each word in LDS already expanded to its fp4 operand.  Pixels outside
+//      the first layer's output get the pad word 0 (-1) of the second conv.
 //   3. Each wave takes 64 pixels (16 windows) x 64 filters of the second
-//      layer on the fp4 matrix cores: activation words from LDS (no bounds
-//      tests: the halo holds the padding), weight words from global memory,
-//      accumulators started at 0.5 - thr (the output bit is the complement
-//      of the sign), OR-pool on lane quads and the packed store.
+//      layer on the fp4 matrix cores: activation operands straight from LDS
+//      (no bounds tests: the halo holds the padding), weight words from
+//      global memory, accumulators started at 0.5 - thr (the output bit is
+//      the complement of the sign), OR-pool on lane quads and the packed
+//      store.
 #include <stdlib.h>
+
+#include <type_traits>
 
 #include "fp4_expand.hpp"
 #include "kernels.hpp"
@@ -71,10 +77,19 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
   constexpr int F1 = 64 * NFH;
   constexpr int FW1 = F1 / 32;
 
-  __shared__ float xin[kIH * kIW * C0];
+  constexpr int NX = kIH * kIW * C0;  // input values of the tile
+  constexpr int XIT = (NX + NT - 1) / NT;
+
+  __shared__ _Float16 xs[2][NX];       // input tile, fp16 high and low parts
   __shared__ v8h wop[FT0][KC0][64];
-  __shared__ __attribute__((aligned(16))) uint32_t act[kAPix * CW1];
-  __shared__ float th0[F0];
+  // First-layer output bits, each word already expanded to its fp4 operand:
+  // word wi of tile pixel (r, c) at r RSX + c PSX + wi.  The spare entry per
+  // pixel and the row stride (= 4 mod 8 entries) spread the 16-byte reads of
+  // 8 neighbouring lanes (2 rows x 4 columns) over distinct banks.
+  constexpr int PSX = CW1 + 1;
+  constexpr int RSX = kAW * PSX + ((4 - (kAW * PSX) % 8) + 8) % 8;
+  __shared__ v4i actx[kAH * RSX];
+  __shared__ __attribute__((aligned(16))) float th0[F0];
   __shared__ uint32_t fl0[CW1];
   __shared__ float th1[F1];
 
@@ -90,90 +105,167 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
   const int r0 = i0 - a.pad1, c0 = j0 - a.pad1;  // first-layer tile origin
   const int y0 = r0 - a.pad0, x0 = c0 - a.pad0;  // input tile origin
 
-  // 1. Staging.
-  for (int e = tid; e < kIH * kIW * C0; e += NT) {
+  // 1. Staging.  Every global load of the stage is issued before the first
+  // LDS store, so the block waits for one memory round trip.
+  float xv[XIT];
+#pragma unroll
+  for (int i = 0; i < XIT; ++i) {
+    const int e = tid + i * NT;
     const int ch = e % C0, t = e / C0;
     const int col = t % kIW, row = t / kIW;
     const int y = y0 + row, x = x0 + col;
-    float v = 0.0f;
-    if (y >= 0 && y < a.H && x >= 0 && x < a.W)
-      v = a.in[((static_cast<size_t>(n) * a.H + y) * a.W + x) * C0 + ch];
-    xin[e] = v;
+    xv[i] = 0.0f;
+    if (e < NX && y >= 0 && y < a.H && x >= 0 && x < a.W)
+      xv[i] = a.in[((static_cast<size_t>(n) * a.H + y) * a.W + x) * C0 + ch];
   }
-  // First-layer A operands: row = filter 16 ft + (l % 16), 8 k values
-  // 32 kc + 8 (l / 16) + j as +-1 (0 past K0).  One weight word per filter
-  // and tap (C0 <= 4 channels).
-  for (int e = tid; e < FT0 * KC0 * 64; e += NT) {
-    const int l = e & 63, kc = (e >> 6) % KC0, ft = (e >> 6) / KC0;
-    const int f = 16 * ft + (l & 15), q = l >> 4;
-    v8h op;
+  // First-layer weights: the 9 words of the filter of each A-operand entry
+  // this thread builds (indices clamped, so the loads need no branch).
+  constexpr int NOP = FT0 * KC0 * 64;
+  constexpr int WIT = (NOP + NT - 1) / NT;
+  uint32_t w0v[WIT][9];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int k = 32 * kc + 8 * q + j;
-      const int tap = k / C0, ch = k - tap * C0;
-      const bool ok = k < K0;
-      const uint32_t word = a.w0[f * 9 + (ok ? tap : 0)];
-      const bool one = (word >> (31 - ch)) & 1u;
-      op[j] = ok ? (one ? static_cast<_Float16>(1.0f) : static_cast<_Float16>(-1.0f))
-                 : static_cast<_Float16>(0.0f);
-    }
-    wop[ft][kc][l] = op;
+  for (int i = 0; i < WIT; ++i) {
+    const int e = min(tid + i * NT, NOP - 1);
+    const int f = 16 * ((e >> 6) / KC0) + (e & 15);
+#pragma unroll
+    for (int t = 0; t < 9; ++t) w0v[i][t] = a.w0[f * 9 + t];
   }
-  for (int e = tid; e < F0; e += NT) th0[e] = static_cast<float>(a.thr0[e]);
-  for (int e = tid; e < CW1; e += NT) fl0[e] = a.flip0 ? a.flip0[e] : 0u;
+  const int32_t thr0v = a.thr0[min(tid, F0 - 1)];
+  const int32_t thr1v = a.thr1[min(tid, F1 - 1)];
+  const uint32_t fl0v = a.flip0 ? a.flip0[min(tid, CW1 - 1)] : 0u;
+
+  // First-layer A operands: row = filter 16 ft + (l % 16), 8 k values
+  // 32 kc + 8 (l / 16) + j as +-1 (0 past K0).  The filter's K0 = 9 C0 weight
+  // bits are gathered first, k = C0 tap + ch at bit K0 - 1 - k.
+  using KBits = typename std::conditional<(K0 <= 32), uint32_t, uint64_t>::type;
+#pragma unroll
+  for (int i = 0; i < WIT; ++i) {
+    const int e = tid + i * NT;
+    if (e < NOP) {
+      const int l = e & 63, kc = (e >> 6) % KC0, ft = (e >> 6) / KC0;
+      const int q = l >> 4;
+      KBits bits = 0;
+#pragma unroll
+      for (int t = 0; t < 9; ++t) bits = (bits << C0) | static_cast<KBits>(w0v[i][t] >> (32 - C0));
+      v8h op;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int k = 32 * kc + 8 * q + j;
+        const bool ok = k < K0;
+        const bool one = (bits >> (ok ? K0 - 1 - k : 0)) & 1u;
+        op[j] = ok ? (one ? static_cast<_Float16>(1.0f) : static_cast<_Float16>(-1.0f))
+                   : static_cast<_Float16>(0.0f);
+      }
+      wop[ft][kc][l] = op;
+    }
+  }
+  // First-layer thresholds, clamped to +-2^16 (|S| < 2^8 keeps every
+  // comparison) and stored as -float(-thr), which makes a zero threshold -0.0:
+  // then S - thr is -0.0 only for S < thr, also when S is -0.0.
+  if (tid < F0) th0[tid] = -static_cast<float>(-min(max(thr0v, -65536), 65536));
+  if (tid < CW1) fl0[tid] = fl0v;
   // Second-layer start values 0.5 - thr (thr clamped to [-K1-1, K1+1], which
   // keeps every comparison since |S| <= K1).
-  for (int e = tid; e < F1; e += NT)
-    th1[e] = 0.5f - static_cast<float>(min(max(a.thr1[e], -a.K1 - 1), a.K1 + 1));
+  if (tid < F1) th1[tid] = 0.5f - static_cast<float>(min(max(thr1v, -a.K1 - 1), a.K1 + 1));
+  // Each input value split once into x = hi + lo, both fp16 and exact.
+#pragma unroll
+  for (int i = 0; i < XIT; ++i) {
+    const int e = tid + i * NT;
+    if (e < NX) {
+      const _Float16 hi = static_cast<_Float16>(xv[i]);
+      xs[0][e] = hi;
+      xs[1][e] = static_cast<_Float16>(xv[i] - static_cast<float>(hi));
+    }
+  }
   __syncthreads();
+
+  const uint32_t smask = __builtin_amdgcn_readfirstlane(0x88888888u);
+  uint32_t vfill;
+  asm("v_mov_b32 %0, 0x22222222" : "=v"(vfill));
 
   // 2. First layer on the 10 x 34 tile: lane (q, c) = (l / 16, l % 16) holds
   // pixel c of a 16-pixel tile and filters 16 ft + 4 q + r (r = 0..3).
   {
     const int q = lane >> 4, c = lane & 15;
+    // Offsets of this lane's k values from the window's first input value;
+    // k >= K0 reuses offset 0 (its weight is 0).
+    int koff[KC0][8];
+#pragma unroll
+    for (int kc = 0; kc < KC0; ++kc)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int k = 32 * kc + 8 * q + j;
+        const int tap = k / C0, ch = k - tap * C0;
+        const int kh = tap / 3, kw = tap - kh * 3;
+        koff[kc][j] = k < K0 ? (kh * kIW + kw) * C0 + ch : 0;
+      }
+    v8h wa[FT0][KC0];
+#pragma unroll
+    for (int ft = 0; ft < FT0; ++ft)
+#pragma unroll
+      for (int kc = 0; kc < KC0; ++kc) wa[ft][kc] = wop[ft][kc][lane];
+    v4f thv[2 * CW1];
+#pragma unroll
+    for (int ft = 0; ft < 2 * CW1; ++ft)
+      thv[ft] = *reinterpret_cast<const v4f*>(&th0[16 * ft + 4 * q]);
+    // After the row reduction lane (q, c) holds word q % CW1 of pixel c.
+    const uint32_t nfl = ~fl0[q % CW1];
+
     for (int pt = wave; pt < kATiles; pt += NW) {
       const int p = 16 * pt + c;
       const bool pv = p < kAPix;
       const int pp = pv ? p : 0;
       const int lr = pp / kAW, lc = pp - (pp / kAW) * kAW;
+      const int base = (lr * kIW + lc) * C0;
       v8h xh[KC0], xl[KC0];
 #pragma unroll
       for (int kc = 0; kc < KC0; ++kc)
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          const int k = 32 * kc + 8 * q + j;
-          const int tap = k / C0, ch = k - tap * C0;
-          const int kh = tap / 3, kw = tap - kh * 3;
-          const float x = k < K0 ? xin[((lr + kh) * kIW + lc + kw) * C0 + ch] : 0.0f;
-          const _Float16 hi = static_cast<_Float16>(x);
-          xh[kc][j] = hi;
-          xl[kc][j] = static_cast<_Float16>(x - static_cast<float>(hi));
+          xh[kc][j] = xs[0][base + koff[kc][j]];
+          xl[kc][j] = xs[1][base + koff[kc][j]];
         }
       const int rr = r0 + lr, cc = c0 + lc;
       const bool inside = pv && rr >= 0 && rr < a.Ho0 && cc >= 0 && cc < a.Wo0;
+      // All filter tiles' products first (high parts, then low parts), so
+      // no MFMA waits on the one before it.
+      v4f acc[2 * CW1];
+#pragma unroll
+      for (int ft = 0; ft < 2 * CW1; ++ft) acc[ft] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kc = 0; kc < KC0; ++kc) {
+#pragma unroll
+        for (int ft = 0; ft < 2 * CW1; ++ft)
+          acc[ft] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[ft][kc], xh[kc], acc[ft], 0, 0, 0);
+#pragma unroll
+        for (int ft = 0; ft < 2 * CW1; ++ft)
+          acc[ft] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[ft][kc], xl[kc], acc[ft], 0, 0, 0);
+      }
+      // Sign bits of S - thr, filter fl of word wi at bit 31 - fl.
+      uint32_t sg[CW1];
 #pragma unroll
       for (int wi = 0; wi < CW1; ++wi) {
-        uint32_t word = 0u;
+        sg[wi] = 0u;
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf) {
           const int ft = 2 * wi + hf;
-          v4f acc = {0.f, 0.f, 0.f, 0.f};
+          uint32_t nib = 0u;
 #pragma unroll
-          for (int kc = 0; kc < KC0; ++kc) {
-            const v8h wa = wop[ft][kc][lane];
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa, xh[kc], acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa, xl[kc], acc, 0, 0, 0);
-          }
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int fl = 16 * hf + 4 * q + r;  // filter within the word
-            const bool on = acc[r] >= th0[32 * wi + fl];
-            word |= static_cast<uint32_t>(on) << (31 - fl);
-          }
+          for (int r = 0; r < 4; ++r)
+            nib = __builtin_amdgcn_alignbit(nib, __float_as_uint(acc[ft][r] - thv[ft][r]), 31);
+          sg[wi] |= nib << (28 - 16 * hf - 4 * q);
         }
-        word = or_xor32(or_xor16(word));
-        word = inside ? word ^ fl0[wi] : 0u;
-        if (q == 0 && pv) act[p * CW1 + wi] = word;
+      }
+      uint32_t rows;
+      if constexpr (CW1 == 4)
+        rows = or_rows4(sg[0], sg[1], sg[2], sg[3]);
+      else
+        rows = or_rows4(sg[0], sg[1], sg[0], sg[1]);
+      // Output bit = (S >= thr) xor flip = sign xor ~flip.
+      const uint32_t word = inside ? rows ^ nfl : 0u;
+      if (q < CW1 && pv) {
+        const v8i x = expand_fp4(word, smask, vfill);
+        actx[lr * RSX + lc * PSX + q] = v4i{x[0], x[1], x[2], x[3]};
       }
     }
   }
@@ -194,7 +286,7 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
       pr[tp] = 2 * pg + tp;
       pc[tp] = c;
     }
-    abase[tp] = (pr[tp] * kAW + pc[tp]) * CW1 + h * VW;
+    abase[tp] = pr[tp] * RSX + pc[tp] * PSX + h * VW;
   }
   v16f acc[2][2];
 #pragma unroll
@@ -207,9 +299,6 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
   }
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint32_t*>(a.w1), 0, a.w1_bytes, kRsrcWord3);
-  const uint32_t smask = __builtin_amdgcn_readfirstlane(0x88888888u);
-  uint32_t vfill;
-  asm("v_mov_b32 %0, 0x22222222" : "=v"(vfill));
   uint32_t woff[2];
 #pragma unroll
   for (int tf = 0; tf < 2; ++tf)
@@ -239,17 +328,17 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
     if (it + 1 < ITERS) load_w(it + 1, wr[cur ^ 1]);
     const int tap = it / NCH, cc = (it - tap * NCH) * 2 * VW;
     const int kh = tap / 3, kw = tap - kh * 3;
-    const int ao = (kh * kAW + kw) * CW1 + cc;
-    uint32_t xw[2][VW];
+    const int ao = kh * RSX + kw * PSX + cc;
+    v8i A[2][VW], B[2][VW];
 #pragma unroll
     for (int tp = 0; tp < 2; ++tp)
 #pragma unroll
-      for (int v = 0; v < VW; ++v) xw[tp][v] = act[abase[tp] + ao + v];
-    v8i A[2][VW], B[2][VW];
+      for (int v = 0; v < VW; ++v) {
+        const v4i t = actx[abase[tp] + ao + v];
+        B[tp][v] = v8i{t[0], t[1], t[2], t[3], 0, 0, 0, 0};
+      }
 #pragma unroll
     for (int tf = 0; tf < 2; ++tf) expand_words<VW>(wr[cur][tf], smask, vfill, A[tf]);
-#pragma unroll
-    for (int tp = 0; tp < 2; ++tp) expand_words<VW>(xw[tp], smask, vfill, B[tp]);
 #pragma unroll
     for (int v = 0; v < VW; ++v)
 #pragma unroll
