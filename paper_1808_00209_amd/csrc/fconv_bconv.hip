@@ -351,46 +351,36 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
 
   // Epilogue: register e of lane (h, c) holds S - thr + 0.5 of filter
   // f0 + 32 tf + 8 (e / 4) + 4 h + e % 4 at pixel c of tile tp; its sign bit
-  // is the complement of the output bit.
-  uint32_t fx[2];
-#pragma unroll
-  for (int tf = 0; tf < 2; ++tf) {
-    const int wi = f0 / 32 + tf;
-    fx[tf] = ~(a.flip1 ? a.flip1[wi] : 0u);
-  }
+  // is the complement of the output bit.  Both lane halves hold bits of each
+  // filter tile's word; one v_permlane32_swap of the two tiles' words leaves
+  // lane half h with the whole word of filter tile h.
+  const uint32_t fxh = ~(a.flip1 ? a.flip1[f0 / 32 + h] : 0u);
 #pragma unroll
   for (int tp = 0; tp < 2; ++tp) {
-    uint32_t word[2];
+    uint32_t wd[2];
 #pragma unroll
     for (int tf = 0; tf < 2; ++tf) {
-      uint32_t wd = 0u;
+      wd[tf] = 0u;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         uint32_t nib = 0u;
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           nib = __builtin_amdgcn_alignbit(nib, __float_as_uint(acc[tf][tp][4 * g + r]), 31);
-        wd |= nib << (28 - 8 * g - 4 * h);
+        wd[tf] |= nib << (28 - 8 * g - 4 * h);
       }
-      wd = or_xor32(wd);
-      wd ^= fx[tf];
-      if constexpr (POOL) {
-        wd = or_quad(wd);
-      }
-      word[tf] = wd;
     }
+    const auto sw = __builtin_amdgcn_permlane32_swap(wd[0], wd[1], false, false);
+    uint32_t word = (sw[0] | sw[1]) ^ fxh;
     if constexpr (POOL) {
+      word = or_quad(word);
       const int ip = (i0 >> 1) + pg, jp = (j0 >> 1) + ((32 * tp + c) >> 2);
-      if (h == 0 && (c & 3) == 0 && ip < a.Hp && jp < a.Wp) {
-        uint32_t* op = a.bits + (static_cast<size_t>(n * a.Hp + ip) * a.Wp + jp) * FW1 + f0 / 32;
-        *reinterpret_cast<uint2*>(op) = make_uint2(word[0], word[1]);
-      }
+      if ((c & 3) == 0 && ip < a.Hp && jp < a.Wp)
+        a.bits[(static_cast<size_t>(n * a.Hp + ip) * a.Wp + jp) * FW1 + f0 / 32 + h] = word;
     } else {
       const int i = i0 + pr[tp], j = j0 + pc[tp];
-      if (h == 0 && i < a.Ho1 && j < a.Wo1) {
-        uint32_t* op = a.bits + (static_cast<size_t>(n * a.Ho1 + i) * a.Wo1 + j) * FW1 + f0 / 32;
-        *reinterpret_cast<uint2*>(op) = make_uint2(word[0], word[1]);
-      }
+      if (i < a.Ho1 && j < a.Wo1)
+        a.bits[(static_cast<size_t>(n * a.Ho1 + i) * a.Wo1 + j) * FW1 + f0 / 32 + h] = word;
     }
   }
 }

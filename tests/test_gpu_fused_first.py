@@ -95,3 +95,32 @@ def test_fconv_bconv2d_entry_point(name):
     torch.cuda.synchronize()
     assert np.array_equal(words_u32(got), words_u32(b1))
     assert np.array_equal(words_u32(got), oracle.pack_eq2(oracle.forward(layers, x)))
+
+
+def test_fused_first_ties_zero_windows_and_extreme_thresholds(monkeypatch):
+    """Inputs on a 0.5 grid, so first-layer sums often equal their integer
+    threshold (S >= thr gives bit 1); a block of exact zeros, whose windows
+    sum to 0 against thresholds of 0; and thresholds far outside any sum
+    (INT32_MIN / MAX, +-10^6), which the kernel clamps without changing a
+    comparison.  Fused against the two launches and the oracle."""
+    H, W, C0 = 20, 36, 3
+    l0 = synth.conv_layer(9, 5, "fconv", C0, 128, pad=1)
+    l1 = synth.conv_layer(9, 6, "bconv", 128, 128, pad=1, pool=2)
+    thr0 = l0["thr"].copy()
+    thr0[:24] = 0
+    thr0[24:32] = [np.iinfo(np.int32).min, np.iinfo(np.int32).max, -10**6, 10**6, 1, -1, 2, -2]
+    thr0[32:40] = [0, 1, -1, 0, 3, -3, 0, 0]
+    l0["thr"] = thr0.astype(np.int32)
+    l1["thr"] = l1["thr"].copy()
+    l1["thr"][:4] = [np.iinfo(np.int32).min, np.iinfo(np.int32).max, 0, 9 * 128]
+    layers = [l0, l1, synth.fc_layer(9, 7, (H // 2) * (W // 2) * 128, 10, logits=True)]
+    g = synth.rng(9, 92, synth.T_X)
+    x = (g.integers(-4, 5, size=(4, H, W, C0)) * 0.5).astype(np.float32)
+    x[:, 4:12, 6:20, :] = 0.0
+    x[2] = 0.0
+    net = upload_network(layers, H, W, C0)
+    xd = to_device(x)
+    got = _run(net, xd, monkeypatch, True)
+    ref = _run(net, xd, monkeypatch, False)
+    assert np.array_equal(got, ref)
+    assert np.array_equal(got, oracle.forward(layers, x))
