@@ -283,11 +283,16 @@ __device__ __forceinline__ void init_acc(v16f (&acc)[TF][TP], bool pre, const fl
 // PRE: the accumulators hold S - thr + 0.5 (init_acc), whose sign bit is the
 // complement of the output bit; otherwise they hold S and the sign bit of
 // (thr - 0.5) - S is the output bit.
+// Both lane halves hold bits of every tile's word.  One v_permlane32_swap of
+// two tiles' words leaves lane half h with the whole h-th word of the pair:
+// with TF = 2 the pair is the two filter tiles of a pixel tile, with TF = 1
+// the two pixel tiles, and every lane stores its own word.
 template <bool PRE, int TF, int TP, bool POOL, int VW>
 __device__ __forceinline__ void epi_bits(const Mfma32Args& a, v16f (&acc)[TF][TP],
                                          const PixTiles<TP, POOL, VW>& px, int p0, int f0,
                                          int h, int c, const float* thl,
                                          const EpiParams<TF>& ep) {
+  static_assert(TP == 2 && (TF == 1 || TF == 2), "tile pairs");
   float th[TF][16];
   if constexpr (!PRE) {
 #pragma unroll
@@ -295,46 +300,50 @@ __device__ __forceinline__ void epi_bits(const Mfma32Args& a, v16f (&acc)[TF][TP
 #pragma unroll
       for (int e = 0; e < 16; ++e) th[tf][e] = thl[tf * 32 + 8 * (e >> 2) + 4 * h + (e & 3)];
   }
-  uint32_t fm[TF], fx[TF];
+  // Filters 8 g + 4 h + r (r = 0..3) of register group g go to bits
+  // 31 - 8 g - 4 h - r: shift the four signs into a nibble (v_alignbit takes
+  // the sign bit of each value), then place the nibble.
+  auto signs = [&](int tf, int tp) {
+    uint32_t wd = 0u;
 #pragma unroll
-  for (int tf = 0; tf < TF; ++tf) {
-    fm[tf] = f0 / 32 + tf == a.Fw - 1 ? tail_mask(a.F) : ~0u;
-    fx[tf] = PRE ? ~ep.fl[tf] : ep.fl[tf];
-  }
+    for (int g = 0; g < 4; ++g) {
+      uint32_t nib = 0u;
 #pragma unroll
-  for (int tp = 0; tp < TP; ++tp) {
-    uint32_t word[TF];
-#pragma unroll
-    for (int tf = 0; tf < TF; ++tf) {
-      // Filters 8 g + 4 h + r (r = 0..3) of register group g go to bits
-      // 31 - 8 g - 4 h - r: shift the four signs into a nibble (v_alignbit
-      // takes the sign bit of each value), then place the nibble.
-      uint32_t wd = 0u;
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        uint32_t nib = 0u;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float d = PRE ? acc[tf][tp][4 * g + r] : th[tf][4 * g + r] - acc[tf][tp][4 * g + r];
-          nib = __builtin_amdgcn_alignbit(nib, __float_as_uint(d), 31);
-        }
-        wd |= nib << (28 - 8 * g - 4 * h);  // nib < 16: four bits shifted into 0
+      for (int r = 0; r < 4; ++r) {
+        const float d = PRE ? acc[tf][tp][4 * g + r] : th[tf][4 * g + r] - acc[tf][tp][4 * g + r];
+        nib = __builtin_amdgcn_alignbit(nib, __float_as_uint(d), 31);
       }
-      wd = or_xor32(wd);
-      wd = (wd ^ fx[tf]) & fm[tf];
-      if constexpr (POOL) {
-        wd = or_quad(wd);
-      }
-      word[tf] = wd;
+      wd |= nib << (28 - 8 * g - 4 * h);  // nib < 16: four bits shifted into 0
     }
-    const int item = p0 + tp * 32 + c;
-    const bool writer = POOL ? (h == 0 && (c & 3) == 0 && px.pv[tp]) : (h == 0 && px.pv[tp]);
-    if (writer) {
-      uint32_t* op = a.bits + static_cast<size_t>(POOL ? (item >> 2) : item) * a.Fw + f0 / 32;
+    return wd;
+  };
+  auto pair = [](uint32_t w0, uint32_t w1) {
+    const auto sw = __builtin_amdgcn_permlane32_swap(w0, w1, false, false);
+    return sw[0] | sw[1];
+  };
+  if constexpr (TF == 2) {
+    const int wi = f0 / 32 + h;  // this lane half's filter word
+    const uint32_t fl = h ? ep.fl[1] : ep.fl[0];
+    const uint32_t fx = PRE ? ~fl : fl;
+    const uint32_t fm = wi == a.Fw - 1 ? tail_mask(a.F) : ~0u;
 #pragma unroll
-      for (int tf = 0; tf < TF; ++tf)
-        if (f0 / 32 + tf < a.Fw) op[tf] = word[tf];
+    for (int tp = 0; tp < TP; ++tp) {
+      uint32_t wd = (pair(signs(0, tp), signs(1, tp)) ^ fx) & fm;
+      if constexpr (POOL) wd = or_quad(wd);
+      const int item = p0 + tp * 32 + c;
+      if ((!POOL || (c & 3) == 0) && px.pv[tp] && wi < a.Fw)
+        a.bits[static_cast<size_t>(POOL ? (item >> 2) : item) * a.Fw + wi] = wd;
     }
+  } else {
+    const int wi = f0 / 32;
+    const uint32_t fx = PRE ? ~ep.fl[0] : ep.fl[0];
+    const uint32_t fm = wi == a.Fw - 1 ? tail_mask(a.F) : ~0u;
+    uint32_t wd = (pair(signs(0, 0), signs(0, 1)) ^ fx) & fm;
+    if constexpr (POOL) wd = or_quad(wd);
+    const int item = p0 + h * 32 + c;  // lane half h: pixel tile h
+    const bool pv = h ? px.pv[1] : px.pv[0];
+    if ((!POOL || (c & 3) == 0) && pv)
+      a.bits[static_cast<size_t>(POOL ? (item >> 2) : item) * a.Fw + wi] = wd;
   }
 }
 
