@@ -43,17 +43,17 @@ _BUILD = ("paper_1808_00209_amd/build.py",
 _FP4 = ("paper_1808_00209_amd/csrc/fp4_expand.hpp",
         "d025e6c895771b0e8c624d6b14e4559aae203e5a519954919d75dea0192da41b")
 _LANE = ("paper_1808_00209_amd/csrc/lane_ops.hpp",
-         "0305f935888de7ac63ef2c712b1733ac8f1d1cc002e8baf7658f1891a84b657c")
+         "96ece7042c6ed72e9cd799fdd8e007525e30035bbd8d052a9ece380c5e3fda82")
 MEASURED_TRAFFIC = {
     ("cifar_bnn_b64", "L0+L1 fconv+bconv 32x32x3->128->128 k3 pool (fused)"): dict(
-        fetch_kib=712.2, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
+        fetch_kib=690.3, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/fconv_bconv.hip",
-                       "66f4424134e3916390524eb68bad2aeed715bf57ffbf9e210772c350ebbc0766"),
+                       "04d819767c62096fea3c178dc3f583b251029b7b4ff85157227e4abc3115bf58"),
                       _FP4, _LANE, _BUILD])),
     ("cifar_bnn_b64", "L5 bconv 8x8x512->512 k3 pool"): dict(
-        fetch_kib=1340.0, write_kib=64.0, fetch_scale=2.0, write_scale=1.0,
+        fetch_kib=1342.0, write_kib=64.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/bconv_mfma.hip",
-                       "83c48183919fed267e8795088937bd0bab3da87c2587c8e46ab2084f26010a6a"),
+                       "583714c26a6fb24e147a26e9ea6fd809c376d4810edebf5bdc16e94bd88fae75"),
                       _FP4, _LANE, _BUILD])),
 }
 
