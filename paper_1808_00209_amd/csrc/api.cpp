@@ -45,9 +45,20 @@ bool use_mfma(const bnn::ConvGeom& g) {
   return bnn::bconv_mfma_supported(g);
 }
 
+// 1x1 convs with K <= 256 over >= 65536 pixels, bits only: the kernel that
+// keeps a wave's pixel operands and walks all filters (BNN_1X1=0 sends them
+// to the general matrix-core kernel).
+bool use_1x1(const bnn::ConvGeom& g, bool sums) {
+  const char* e = getenv("BNN_1X1");
+  if (e && strcmp(e, "0") == 0) return false;
+  return bnn::bconv1x1_supported(g, sums);
+}
+
 hipError_t launch_conv(const bnn::ConvGeom& g, const uint32_t* in, const uint32_t* w,
                        const int32_t* thr, const uint32_t* flip, int32_t* sums,
                        uint32_t* bits, hipStream_t s) {
+  if (use_mfma(g) && bits && use_1x1(g, sums != nullptr))
+    return bnn::launch_bconv1x1(g, in, w, thr, flip, bits, s);
   if (use_mfma(g)) return bnn::launch_bconv_mfma(g, in, w, thr, flip, sums, bits, s);
   return bnn::launch_bconv_valu(g, in, w, thr, flip, sums, bits, s);
 }

@@ -33,8 +33,17 @@ hipError_t launch_bconv_valu(const ConvGeom& g, const uint32_t* in,
                              const uint32_t* flip, int32_t* sums,
                              uint32_t* bits, hipStream_t s);
 
+// Binary 1x1 conv with C <= 256 (a multiple of 64), F a multiple of 64 (at
+// most 1024), no padding or pooling, over at least 65536 pixels, bits only:
+// a wave keeps its pixels' fp4 operands and walks all filters.
+bool bconv1x1_supported(const ConvGeom& g, bool sums);
+hipError_t launch_bconv1x1(const ConvGeom& g, const uint32_t* in, const uint32_t* w,
+                           const int32_t* thr, const uint32_t* flip, uint32_t* bits,
+                           hipStream_t s);
+
 // Binary conv on the matrix cores (fp4 MFMA).  Supported when
-// bconv_mfma_supported(g): C a multiple of 64, at most 32 taps.
+// bconv_mfma_supported(g): C >= 64 (padded to whole 64-bit chunks), at most
+// 32 taps.
 bool bconv_mfma_supported(const ConvGeom& g);
 hipError_t launch_bconv_mfma(const ConvGeom& g, const uint32_t* in,
                              const uint32_t* w, const int32_t* thr,
