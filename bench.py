@@ -37,9 +37,9 @@ HBM_PEAK_GBS = 8000.0
 # counters are calibrated on a 256 MiB device-to-device copy in the same
 # runs: FETCH_SIZE read 131087.8 KiB for 262144 KiB moved (factor 2.0),
 # WRITE_SIZE read 262144.0 KiB (factor 1.0).  A figure is reported only while
-# the sources it was taken from hash to the values recorded with it.
-_BUILD = ("paper_1808_00209_amd/build.py",
-          "72c88ac8739ea58df1e7bf480187bcff54058511792aa1a10abbd4e679e40bd7")
+# the kernel's sources hash to the values recorded with it and the compile
+# flags (build.COMMON) to the flags digest.
+_FLAGS = "7f0f1e4600f43c30dc5e3f49f8f5e0aab379e024ad2071ae5cf4f6b47147ced9"
 _FP4 = ("paper_1808_00209_amd/csrc/fp4_expand.hpp",
         "d025e6c895771b0e8c624d6b14e4559aae203e5a519954919d75dea0192da41b")
 _LANE = ("paper_1808_00209_amd/csrc/lane_ops.hpp",
@@ -49,12 +49,12 @@ MEASURED_TRAFFIC = {
         fetch_kib=690.3, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/fconv_bconv.hip",
                        "04d819767c62096fea3c178dc3f583b251029b7b4ff85157227e4abc3115bf58"),
-                      _FP4, _LANE, _BUILD])),
+                      _FP4, _LANE]), flags=_FLAGS),
     ("cifar_bnn_b64", "L5 bconv 8x8x512->512 k3 pool"): dict(
         fetch_kib=1342.0, write_kib=64.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/bconv_mfma.hip",
                        "583714c26a6fb24e147a26e9ea6fd809c376d4810edebf5bdc16e94bd88fae75"),
-                      _FP4, _LANE, _BUILD])),
+                      _FP4, _LANE]), flags=_FLAGS),
 }
 
 
@@ -68,6 +68,9 @@ def measured_traffic(workload, kernel):
         with open(os.path.join(ROOT, rel), "rb") as f:
             if hashlib.sha256(f.read()).hexdigest() != digest:
                 return None
+    from paper_1808_00209_amd import build as _build
+    if hashlib.sha256(" ".join(_build.COMMON).encode()).hexdigest() != rec["flags"]:
+        return None
     return int(round((rec["fetch_kib"] * rec["fetch_scale"]
                       + rec["write_kib"] * rec["write_scale"]) * 1024))
 
