@@ -38,8 +38,8 @@ HBM_PEAK_GBS = 8000.0
 # runs: FETCH_SIZE read 131087.8 KiB for 262144 KiB moved (factor 2.0),
 # WRITE_SIZE read 262144.0 KiB (factor 1.0).  A figure is reported only while
 # the kernel's sources hash to the values recorded with it and the compile
-# flags (build.COMMON) to the flags digest.
-_FLAGS = "7f0f1e4600f43c30dc5e3f49f8f5e0aab379e024ad2071ae5cf4f6b47147ced9"
+# flags (build.COMMON without include paths) to the flags digest.
+_FLAGS = "cfb3b8a417945f0b0125dc066d5529292593229deafe2cb65291c547d733ed6c"
 _FP4 = ("paper_1808_00209_amd/csrc/fp4_expand.hpp",
         "d025e6c895771b0e8c624d6b14e4559aae203e5a519954919d75dea0192da41b")
 _LANE = ("paper_1808_00209_amd/csrc/lane_ops.hpp",
@@ -58,6 +58,14 @@ MEASURED_TRAFFIC = {
 }
 
 
+def compile_flags():
+    """The library's compile flags without the include paths (which depend on
+    where the repository sits)."""
+    from paper_1808_00209_amd import build as _build
+    c = _build.COMMON
+    return [x for i, x in enumerate(c) if x != "-I" and (i == 0 or c[i - 1] != "-I")]
+
+
 def measured_traffic(workload, kernel):
     """Scaled HBM bytes per launch of `kernel`, or None once its sources changed."""
     import hashlib
@@ -68,8 +76,7 @@ def measured_traffic(workload, kernel):
         with open(os.path.join(ROOT, rel), "rb") as f:
             if hashlib.sha256(f.read()).hexdigest() != digest:
                 return None
-    from paper_1808_00209_amd import build as _build
-    if hashlib.sha256(" ".join(_build.COMMON).encode()).hexdigest() != rec["flags"]:
+    if hashlib.sha256(" ".join(compile_flags()).encode()).hexdigest() != rec["flags"]:
         return None
     return int(round((rec["fetch_kib"] * rec["fetch_scale"]
                       + rec["write_kib"] * rec["write_scale"]) * 1024))
