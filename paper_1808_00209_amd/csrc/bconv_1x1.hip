@@ -1,5 +1,5 @@
-// Binary 1x1 conv with short windows (Eq. 4 with a single tap, K = C <= 256
-// bits) on the fp4 matrix cores, for large pixel counts.
+// Binary 1x1 conv with short windows (Eq. 4 with a single tap, K = C = 64,
+// 128 or 256 bits) on the fp4 matrix cores, for large pixel counts.
 //
 // With K <= 256 a 32 x 32 output tile is only 1..4 MFMA k-steps deep, so in
 // the general conv kernel a wave spends more on its pixel operands, its
@@ -177,8 +177,10 @@ __global__ __launch_bounds__(256) void bconv1x1_kernel(B1Args a) {
 
 bool bconv1x1_supported(const ConvGeom& g, bool sums) {
   const int64_t M = static_cast<int64_t>(g.N) * g.H * g.W;
-  return !sums && g.KH == 1 && g.KW == 1 && g.pad == 0 && g.pool == 0 && g.C % 64 == 0 &&
-         g.C <= 256 && g.F % 64 == 0 && g.F <= kMaxF && M >= 256 * kPix &&
+  // C = 64, 128 or 256: 1, 2 or 4 k-steps, the instantiated variants (the
+  // launcher maps Cw = 2 / 4 / 8 onto them and nothing else).
+  return !sums && g.KH == 1 && g.KW == 1 && g.pad == 0 && g.pool == 0 &&
+         (g.C == 64 || g.C == 128 || g.C == 256) && g.F % 64 == 0 && g.F <= kMaxF && M >= 256 * kPix &&
          M * g.Fw < (int64_t{1} << 31);
 }
 
@@ -200,7 +202,8 @@ hipError_t launch_bconv1x1(const ConvGeom& g, const uint32_t* in, const uint32_t
   switch (g.Cw) {
     case 2: bconv1x1_kernel<1><<<blocks, 256, lds, s>>>(a); break;
     case 4: bconv1x1_kernel<2><<<blocks, 256, lds, s>>>(a); break;
-    default: bconv1x1_kernel<4><<<blocks, 256, lds, s>>>(a); break;
+    case 8: bconv1x1_kernel<4><<<blocks, 256, lds, s>>>(a); break;
+    default: return hipErrorInvalidValue;  // not reachable: bconv1x1_supported
   }
   return hipGetLastError();
 }

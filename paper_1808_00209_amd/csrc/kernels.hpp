@@ -33,7 +33,7 @@ hipError_t launch_bconv_valu(const ConvGeom& g, const uint32_t* in,
                              const uint32_t* flip, int32_t* sums,
                              uint32_t* bits, hipStream_t s);
 
-// Binary 1x1 conv with C <= 256 (a multiple of 64), F a multiple of 64 (at
+// Binary 1x1 conv with C = 64, 128 or 256, F a multiple of 64 (at
 // most 1024), no padding or pooling, over at least 65536 pixels, bits only:
 // a wave keeps its pixels' fp4 operands and walks all filters.
 bool bconv1x1_supported(const ConvGeom& g, bool sums);

@@ -99,3 +99,28 @@ def test_conv1x1_cfg5_full_size_bits(monkeypatch):
     assert np.array_equal(got, _bits(x, L, monkeypatch, False))
     pix = _sample_pixels(x.shape[:3], 60, 73)
     assert np.array_equal(got[pix[:, 0], pix[:, 1], pix[:, 2]], _oracle_bits_at(x, L, pix))
+
+
+@pytest.mark.parametrize("K", [256, 192])
+def test_bgemm_bits_only_through_the_1x1_kernel(K, monkeypatch):
+    """An FC layer of 70000 rows and 128 outputs runs as a 1 x M image with
+    1x1 filters, bits only: with K = 256 it takes the 1x1 kernel (K = 192,
+    6 words per row, is not one of its variants and goes to the general
+    kernel either way), and every word must match the general kernel;
+    sampled rows match the oracle's FC sums (Sec. III-B), thresholded and
+    packed."""
+    M, N = 70000, 128
+    a = synth.pm1(synth.rng(8, 80, synth.T_X), (M, K))
+    L = _layer(K, N, 81)
+    w = L["w"].reshape(N, K)
+    outs = []
+    for use in (True, False):
+        monkeypatch.setenv("BNN_1X1", "1" if use else "0")
+        _, bits = bnn.bnn_bgemm(pack_pm1(a), pack_pm1(w), K, to_device(L["thr"], torch.int32),
+                                pack_flips(L["flip"]), want_sums=False)
+        torch.cuda.synchronize()
+        outs.append(words_u32(bits))
+    assert np.array_equal(outs[0], outs[1])
+    rows = np.concatenate([np.random.default_rng(82).integers(0, M, 300), [0, M - 1]])
+    S = oracle.fc(a[rows], w)
+    assert np.array_equal(outs[0][rows], oracle.pack_eq2(oracle.threshold(S, L["thr"], L["flip"])))
