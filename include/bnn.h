@@ -269,7 +269,8 @@ typedef struct bnn_layer {
   int32_t F, KH, KW;         /* conv: filters, kernel size                   */
   int32_t stride, pad, pool; /* conv: as in bnn_conv_desc                    */
   int32_t K, N;              /* FC: input bits, outputs                      */
-  const uint32_t* w;         /* conv [F][KH][KW][Cw]; FC [N][ceil(K/32)]     */
+  const uint32_t* w;         /* conv [F][KH][KW][Cw], 16-byte aligned;       */
+                             /* FC [N][ceil(K/32)]                           */
   const int32_t* thr;        /* [F] or [N]                                   */
   const uint32_t* flip;      /* packed flip bits or NULL                     */
   const float* offset;       /* INPUT_THRESHOLD: [C] offsets T; INPUT_GRAY:  */
@@ -308,7 +309,8 @@ bnn_status bnn_forward_workspace_size(const bnn_layer* layers,
  *    each row in LDS (environment BNN_FC_CHAIN=0 launches them one by one).
  * The results are the same either way.  workspace (device, >= the size
  * above, 256-byte aligned) holds the intermediate bits.  Errors: as the
- * per-layer calls, plus BNN_ERR_WORKSPACE.
+ * per-layer calls (conv weights not 16-byte aligned: BNN_ERR_ALIGN, also
+ * from bnn_forward_workspace_size), plus BNN_ERR_WORKSPACE.
  */
 bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers,
                        int32_t batch, int32_t H, int32_t W, int32_t C,

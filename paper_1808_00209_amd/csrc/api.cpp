@@ -404,6 +404,8 @@ bnn_status plan_chain(const bnn_layer* L, int32_t n, int32_t batch, int32_t H,
           return fail(BNN_ERR_SHAPE, "forward: layer %d expects C=%d, previous layer gives %lld",
                       li, l.C, (long long)a.C);
         if (!l.w || !l.thr) return fail(BNN_ERR_NULL, "forward: layer %d: w and thr are required", li);
+        if (!aligned16(l.w))
+          return fail(BNN_ERR_ALIGN, "forward: layer %d: w must be 16-byte aligned", li);
         bnn_conv_desc d{batch, static_cast<int32_t>(a.H), static_cast<int32_t>(a.W), l.C, l.F,
                         l.KH, l.KW, l.stride, l.pad, l.pool};
         bnn::ConvGeom g;

@@ -224,6 +224,10 @@ def test_forward_chain_validation():
            dict(kind=5, K=8 * 8 * 40, N=4, w=A)]
     assert lib.bnn_forward_workspace_size(_layers(odd), 3, 1, 8, 8, 3, ctypes.byref(size)) == 2
     assert "flattening" in bnn.last_error()
+    # conv weights must be 16-byte aligned, as for bnn_bconv2d
+    skew = [dict(good[0]), dict(good[1], w=A + 4), dict(good[2]), dict(good[3])]
+    assert lib.bnn_forward_workspace_size(_layers(skew), 4, 8, 8, 8, 3, ctypes.byref(size)) == 3
+    assert "16-byte aligned" in bnn.last_error()
     # a too-small workspace is refused before any launch
     assert lib.bnn_forward(L, 4, 8, 8, 8, 3, A, A, 256, A, None) == 6
     assert lib.bnn_forward(L, 4, 8, 8, 8, 3, A, A + 16, 1 << 20, A, None) == 3
