@@ -48,7 +48,7 @@ MEASURED_TRAFFIC = {
     ("cifar_bnn_b64", "L0+L1 fconv+bconv 32x32x3->128->128 k3 pool (fused)"): dict(
         fetch_kib=690.3, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/fconv_bconv.hip",
-                       "04d819767c62096fea3c178dc3f583b251029b7b4ff85157227e4abc3115bf58"),
+                       "1c401b19e914cf02c4dc9c436e952e9e4183e2201895b6a2025c950f5ebfdc85"),
                       _FP4, _LANE]), flags=_FLAGS),
     ("cifar_bnn_b64", "L5 bconv 8x8x512->512 k3 pool"): dict(
         fetch_kib=1342.0, write_kib=64.0, fetch_scale=2.0, write_scale=1.0,

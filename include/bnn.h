@@ -300,10 +300,8 @@ bnn_status bnn_forward_workspace_size(const bnn_layer* layers,
  *    keeps them apart);
  *  - an FCONV_BINW layer (3x3, at most 4 channels, 64 or 128 filters, no
  *    pooling) followed by a 3x3 BCONV of 64 or 128 filters runs as one
- *    kernel that keeps the first layer's bits in LDS (bnn_fconv_bconv2d)
- *    when that kernel has at least 32 workgroups of 8 x 32 output pixels,
- *    e.g. 8 images of 32 x 32 (environment BNN_FUSE_FIRST=0 keeps them
- *    apart, =1 fuses at any size);
+ *    kernel that keeps the first layer's bits in LDS (bnn_fconv_bconv2d;
+ *    environment BNN_FUSE_FIRST=0 keeps them apart);
  *  - a run of 2-4 consecutive FC layers of at most 8192 weight words each,
  *    at batch <= 128, runs as one kernel that keeps the intermediate bits of
  *    each row in LDS (environment BNN_FC_CHAIN=0 launches them one by one).

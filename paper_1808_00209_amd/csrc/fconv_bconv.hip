@@ -418,10 +418,6 @@ bool fconv_bconv_supported(const ConvGeom& g0, const ConvGeom& g1) {
          static_cast<int64_t>(g0.N) * g0.H * g0.W * g0.C < (int64_t{1} << 31);
 }
 
-int64_t fconv_bconv_workgroups(const ConvGeom& g1) {
-  return int64_t{g1.N} * ((g1.Wo + kTW - 1) / kTW) * ((g1.Ho + kTH - 1) / kTH);
-}
-
 hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const float* in,
                               const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
                               const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,

@@ -84,7 +84,6 @@ hipError_t launch_fconv_binw(const ConvGeom& g, const float* in,
 // (3x3 over g0's output, 64 or 128 filters, optional 2x2 pooling).  Writes
 // the second layer's packed bits; both thr must be non-null.
 bool fconv_bconv_supported(const ConvGeom& g0, const ConvGeom& g1);
-int64_t fconv_bconv_workgroups(const ConvGeom& g1);
 hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const float* in,
                               const uint32_t* w0, const int32_t* thr0,
                               const uint32_t* flip0, const uint32_t* w1,
