@@ -457,3 +457,85 @@ def test_lbp_matches_a_direct_loop_on_a_tiny_image():
                 ni, nj = i + di, j + dj
                 exceed = 0 <= ni < 3 and 0 <= nj < 4 and g[0, ni, nj] > g[0, i, j]
                 assert out[0, i, j, ch] == (1 if exceed else -1)
+
+
+def _torch_gray(x):
+    """BT.601 luma in float32, products rounded one by one, then summed as
+    (R + G) + B: written here with torch ops, independently of the oracle."""
+    f = torch.float32
+    r, g, b = x[..., 0], x[..., 1], x[..., 2]
+    return (torch.tensor(0.299, dtype=f) * r + torch.tensor(0.587, dtype=f) * g) + \
+        torch.tensor(0.114, dtype=f) * b
+
+
+def _torch_lbp(gray):
+    """LBP channels of Sec. II-C from a gray image [N, H, W]: neighbours at
+    offsets (-1,-1), (0,+1), (+1,-1) (numbers 0, 3, 6 clockwise from the
+    top-left); +1 where the neighbour is strictly brighter, -1 otherwise and
+    outside the image.  Built from padded shifted copies."""
+    N, H, W = gray.shape
+    pad = torch.full((N, H + 2, W + 2), -float("inf"), dtype=gray.dtype)
+    pad[:, 1:H + 1, 1:W + 1] = gray
+    chans = []
+    for di, dj in ((-1, -1), (0, 1), (1, -1)):
+        nb = pad[:, 1 + di:1 + di + H, 1 + dj:1 + dj + W]
+        chans.append(torch.where(nb > gray, 1.0, -1.0))
+    return torch.stack(chans, dim=-1).to(torch.float64)
+
+
+@pytest.mark.parametrize("mode", ["input_gray", "input_lbp"])
+def test_forward_gray_and_lbp_chains_match_torch_composition(mode):
+    """Table II's layer order behind the grayscale and LBP binarizations of
+    Table III (Sec. II-C): oracle.forward against the same chain composed
+    from torch ops with its own grayscale and LBP, so that the chain's input
+    dispatch (which binarization, which offset, how many channels) is pinned
+    by something other than the HIP path."""
+    rng = np.random.default_rng(15 if mode == "input_gray" else 16)
+    N, H, W = 2, 10, 12
+    x = rng.integers(0, 256, size=(N, H, W, 3)).astype(np.float32)
+    T = np.array([-float(rng.integers(64, 192))], np.float32)
+    C1 = 1 if mode == "input_gray" else 3
+    F1, F2 = 6, 8
+    layers = [dict(kind=mode, C=3, offset=T if mode == "input_gray" else None),
+              dict(kind="bconv", C=C1, F=F1, KH=5, KW=5, pad=2, pool=2,
+                   w=_pm1(rng, (F1, 5, 5, C1)),
+                   thr=rng.integers(-5, 6, size=F1).astype(np.int32),
+                   flip=rng.integers(0, 2, size=F1).astype(np.uint8)),
+              dict(kind="bconv", C=F1, F=F2, KH=3, KW=3, pad=1, pool=0,
+                   w=_pm1(rng, (F2, 3, 3, F1)),
+                   thr=rng.integers(-6, 7, size=F2).astype(np.int32),
+                   flip=rng.integers(0, 2, size=F2).astype(np.uint8)),
+              dict(kind="bfc", K=5 * 6 * F2, N=10, w=_pm1(rng, (10, 5 * 6 * F2)),
+                   thr=rng.integers(-8, 9, size=10).astype(np.int32),
+                   flip=rng.integers(0, 2, size=10).astype(np.uint8)),
+              dict(kind="bfc_logits", K=10, N=4, w=_pm1(rng, (4, 10)))]
+    got, trace = oracle.forward(layers, x, return_all=True)
+
+    xt = torch.from_numpy(x)
+    one = torch.ones((), dtype=torch.float64)
+    gray = _torch_gray(xt)
+    if mode == "input_gray":
+        a = torch.where(gray + torch.tensor(float(T[0]), dtype=torch.float32) > 0, one, -one)
+        a = a.unsqueeze(-1)
+    else:
+        a = _torch_lbp(gray)
+    assert np.array_equal(trace[0], a.numpy().astype(np.int8))  # the binarized input
+    a = a.permute(0, 3, 1, 2)
+    for L in layers[1:3]:
+        p = L["pad"]
+        wt = torch.from_numpy(L["w"].astype(np.float64)).permute(0, 3, 1, 2)
+        s = tF.conv2d(tF.pad(a, (p, p, p, p), value=-1.0), wt)
+        thr = torch.from_numpy(L["thr"].astype(np.float64)).view(1, -1, 1, 1)
+        fl = torch.from_numpy(L["flip"].astype(bool)).view(1, -1, 1, 1)
+        a = torch.where((s >= thr) ^ fl, one, -one)
+        if L["pool"]:
+            a = tF.max_pool2d(a, 2)
+    a = a.permute(0, 2, 3, 1).reshape(N, -1)
+    L = layers[3]
+    s = a @ torch.from_numpy(L["w"].astype(np.float64)).T
+    bit = (s >= torch.from_numpy(L["thr"].astype(np.float64))) ^ \
+        torch.from_numpy(L["flip"].astype(bool))
+    a = torch.where(bit, one, -one)
+    ref = a @ torch.from_numpy(layers[4]["w"].astype(np.float64)).T
+    assert np.array_equal(got, ref.numpy().astype(np.int32))
+    assert len(np.unique(got)) > 2  # the chain is not degenerate
