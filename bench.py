@@ -621,23 +621,18 @@ def main():
     per_img_us_graph = batch1(True)
 
     # Per-layer kernel times (Table II analogue) and the dominant kernel.
-    # Each layer also runs with BNN_ALGO=valu (XOR-popcount vector kernels
-    # only): the matrix-core ablation.
+    # Each layer also runs with the vector-ALU XOR-popcount kernels only
+    # (option algo = ALGO_VALU): the matrix-core ablation.
     dev_layers = [upload_layer(L) for L in layers]
     per_layer = []
-    saved_algo = os.environ.get("BNN_ALGO")
     for name, kind, g, macs in shapes:
         dl = ((dev_layers[0], dev_layers[1]) if kind in ("bconv_input", "fconv_bconv")
               else dev_layers[g["li"]])
         ms = time_layer(bnn, kind, g, batch, dl, args.layer_reps, torch)
         ms_valu = None
         if kind != "fconv_bconv":  # a matrix-core kernel only (no vector-ALU form)
-            os.environ["BNN_ALGO"] = "valu"
-            ms_valu = time_layer(bnn, kind, g, batch, dl, args.layer_reps, torch)
-            if saved_algo is None:
-                del os.environ["BNN_ALGO"]
-            else:
-                os.environ["BNN_ALGO"] = saved_algo
+            with bnn.options(algo=bnn.ALGO_VALU):
+                ms_valu = time_layer(bnn, kind, g, batch, dl, args.layer_reps, torch)
         row = {"layer": name, "ms": round(ms, 5),
                "ms_valu": round(ms_valu, 5) if ms_valu is not None else None}
         if macs:

@@ -36,7 +36,9 @@
  * Every pointer argument is a DEVICE pointer owned by the caller, except the
  * bnn_conv_desc / bnn_layer structs and the size outputs, which are host
  * memory read or written before the call returns.  The library allocates
- * nothing and keeps no state except a thread-local error string.  Calls only
+ * nothing.  Its only state is per thread: the last error string and the
+ * kernel-selection options of bnn_set_options (which never change a result).
+ * It reads no environment variables.  Calls only
  * enqueue kernels on `stream` and return without synchronising; results are
  * ready when the stream reaches that point.  Device buffers passed to one
  * call must not overlap unless stated.
@@ -58,7 +60,7 @@
 extern "C" {
 #endif
 
-#define BNN_ABI_VERSION 3
+#define BNN_ABI_VERSION 4
 
 typedef enum bnn_status {
   BNN_OK = 0,
@@ -76,6 +78,51 @@ const char* bnn_last_error(void);
 
 /* BNN_ABI_VERSION of the loaded library. */
 int32_t bnn_abi_version(void);
+
+/*
+ * Kernel selection.  Not part of the paper's method: every setting computes
+ * the same bits and sums; they choose among kernels that do so, for
+ * ablations (the vector-ALU XOR-popcount kernels of Eq. 4 against the
+ * matrix-core ones) and for tests that must reach each kernel variant.
+ * Options are per thread: bnn_set_options affects later calls made on the
+ * calling thread only, and a thread that never calls it uses the defaults.
+ */
+typedef enum bnn_algo {
+  BNN_ALGO_AUTO = 0, /* matrix cores wherever the shape allows (default)    */
+  BNN_ALGO_VALU = 1  /* XOR + popcount on the vector ALU for every layer    */
+} bnn_algo;
+
+typedef struct bnn_options {
+  int32_t algo;            /* bnn_algo                                       */
+  int32_t fuse_input;      /* bnn_forward: an input layer and a small-window */
+                           /* conv after it as one kernel (1, default) or two */
+  int32_t fuse_first;      /* bnn_forward: FCONV_BINW and the 3x3 conv after */
+                           /* it as one kernel (1, default) or two (0)       */
+  int32_t fc_chain;        /* bnn_forward: runs of small FC layers as one    */
+                           /* kernel (1, default) or one launch each (0)     */
+  int32_t conv1x1;         /* the short-window 1x1 kernel where it applies   */
+                           /* (1, default) or the general one (0)            */
+  int32_t xcd_order;       /* matrix-core conv workgroups in the XCD order   */
+                           /* (1, default) or on a 2-D grid (0)              */
+  int32_t gemv_max_rows;   /* FC layers of at most this many rows use the    */
+                           /* vector-ALU GEMV; 0..16, default 2              */
+  int32_t lds_weights;     /* matrix-core conv weights staged through LDS:   */
+                           /* -1 where the heuristic picks it (default), 0   */
+                           /* never, 1 wherever no K split is used (with     */
+                           /* 2-word chunks)                                 */
+  int32_t late_thresholds; /* thresholds staged after the main loop: -1      */
+                           /* heuristic (default), 0 at kernel start where   */
+                           /* the variant allows, 1 after the loop           */
+} bnn_options;
+
+/* The default options. */
+void bnn_default_options(bnn_options* opt);
+
+/* Set (bnn_set_options) or read (bnn_get_options) the calling thread's
+ * options.  Values outside the ranges above give BNN_ERR_SHAPE and leave the
+ * options unchanged; a NULL pointer gives BNN_ERR_NULL. */
+bnn_status bnn_set_options(const bnn_options* opt);
+bnn_status bnn_get_options(bnn_options* opt);
 
 /*
  * Sign to bits (Eq. 1 and Eq. 2; input thresholding of Sec. II-C).
@@ -296,15 +343,15 @@ bnn_status bnn_forward_workspace_size(const bnn_layer* layers,
  * [batch][N_last] (Table I/II: conv, pool, ..., FC layers).  One kernel per
  * layer on `stream`, with three exceptions:
  *  - an input layer followed by a BCONV whose window fits
- *    bnn_bconv2d_input runs as that one kernel (environment BNN_PATCH=0
+ *    bnn_bconv2d_input runs as that one kernel (option fuse_input = 0
  *    keeps them apart);
  *  - an FCONV_BINW layer (3x3, at most 4 channels, 64 or 128 filters, no
  *    pooling) followed by a 3x3 BCONV of 64 or 128 filters runs as one
  *    kernel that keeps the first layer's bits in LDS (bnn_fconv_bconv2d;
- *    environment BNN_FUSE_FIRST=0 keeps them apart);
+ *    option fuse_first = 0 keeps them apart);
  *  - a run of 2-4 consecutive FC layers of at most 8192 weight words each,
  *    at batch <= 128, runs as one kernel that keeps the intermediate bits of
- *    each row in LDS (environment BNN_FC_CHAIN=0 launches them one by one).
+ *    each row in LDS (option fc_chain = 0 launches them one by one).
  * The results are the same either way.  workspace (device, >= the size
  * above, 256-byte aligned) holds the intermediate bits.  Errors: as the
  * per-layer calls (conv weights not 16-byte aligned: BNN_ERR_ALIGN, also

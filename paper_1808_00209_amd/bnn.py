@@ -8,6 +8,7 @@ libbnn.so has not been built (``python -m paper_1808_00209_amd.build``).
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 
@@ -32,7 +33,8 @@ INPUT_GRAY = 1
 INPUT_LBP = 2
 
 # Every symbol include/bnn.h declares.
-EXPORTED = ["bnn_last_error", "bnn_abi_version", "bnn_pack_bits", "bnn_conv_output_dims",
+EXPORTED = ["bnn_last_error", "bnn_abi_version", "bnn_default_options", "bnn_set_options",
+            "bnn_get_options", "bnn_pack_bits", "bnn_conv_output_dims",
             "bnn_bconv2d", "bnn_fconv2d_binw", "bnn_binarize_input", "bnn_bconv2d_input",
             "bnn_fconv_bconv2d", "bnn_bgemm",
             "bnn_forward_workspace_size", "bnn_forward"]
@@ -42,6 +44,17 @@ class BnnError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__("%s: %s" % (STATUS_NAMES.get(status, status), message))
         self.status = status
+
+
+ALGO_AUTO = 0
+ALGO_VALU = 1
+
+
+class Options(ctypes.Structure):
+    """bnn_options: the calling thread's kernel selection (never changes a result)."""
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("algo", "fuse_input", "fuse_first", "fc_chain", "conv1x1", "xcd_order",
+                 "gemv_max_rows", "lds_weights", "late_thresholds")]
 
 
 class ConvDesc(ctypes.Structure):
@@ -74,6 +87,10 @@ def load(path: str = LIB_PATH):
     lib.bnn_last_error.argtypes = []
     lib.bnn_abi_version.restype = i32
     lib.bnn_abi_version.argtypes = []
+    lib.bnn_default_options.restype = None
+    lib.bnn_default_options.argtypes = [ctypes.POINTER(Options)]
+    lib.bnn_set_options.argtypes = [ctypes.POINTER(Options)]
+    lib.bnn_get_options.argtypes = [ctypes.POINTER(Options)]
     lib.bnn_pack_bits.argtypes = [P, P, i64, i64, P, P]
     lib.bnn_conv_output_dims.argtypes = [ctypes.POINTER(ConvDesc)] + [ctypes.POINTER(i32)] * 4
     lib.bnn_bconv2d.argtypes = [ctypes.POINTER(ConvDesc), P, P, P, P, P, P, P]
@@ -88,7 +105,7 @@ def load(path: str = LIB_PATH):
     lib.bnn_forward.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32, P, P,
                                 ctypes.c_size_t, P, P]
     for name in EXPORTED:
-        if name not in ("bnn_last_error", "bnn_abi_version"):
+        if name not in ("bnn_last_error", "bnn_abi_version", "bnn_default_options"):
             getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -130,6 +147,43 @@ def words(bits: int) -> int:
 def _u32(t):
     """torch has no uint32 arithmetic; packed words travel as int32 storage."""
     return _dev(t, torch.int32, "packed words")
+
+
+# ---------------------------------------------------------------- options ---
+def bnn_default_options() -> Options:
+    o = Options()
+    load().bnn_default_options(ctypes.byref(o))
+    return o
+
+
+def bnn_get_options() -> Options:
+    o = Options()
+    _check(load().bnn_get_options(ctypes.byref(o)))
+    return o
+
+
+def bnn_set_options(opt: Options = None, **fields) -> Options:
+    """Set the calling thread's options: ``opt`` (default: the library
+    defaults) with ``fields`` replaced.  Returns the options in force before."""
+    prev = bnn_get_options()
+    o = Options.from_buffer_copy(opt) if opt is not None else bnn_default_options()
+    for k, v in fields.items():
+        if k not in dict(Options._fields_):
+            raise KeyError("unknown option %r" % k)
+        setattr(o, k, int(v))
+    _check(load().bnn_set_options(ctypes.byref(o)))
+    return prev
+
+
+@contextlib.contextmanager
+def options(**fields):
+    """``with bnn.options(algo=bnn.ALGO_VALU): ...`` -- the defaults with
+    ``fields`` replaced, restored to what was in force on exit."""
+    prev = bnn_set_options(None, **fields)
+    try:
+        yield
+    finally:
+        _check(load().bnn_set_options(ctypes.byref(prev)))
 
 
 # ------------------------------------------------------------------ calls ---

@@ -6,7 +6,6 @@
 
 #include <stdarg.h>
 #include <stdio.h>
-#include <stdlib.h>
 #include <string.h>
 
 #include <new>
@@ -16,6 +15,22 @@
 namespace {
 
 thread_local char g_err[512] = "";
+
+bnn_options default_options() {
+  bnn_options o;
+  o.algo = BNN_ALGO_AUTO;
+  o.fuse_input = 1;
+  o.fuse_first = 1;
+  o.fc_chain = 1;
+  o.conv1x1 = 1;
+  o.xcd_order = 1;
+  o.gemv_max_rows = 2;
+  o.lds_weights = -1;
+  o.late_thresholds = -1;
+  return o;
+}
+
+thread_local bnn_options g_opt = default_options();
 
 bnn_status fail(bnn_status st, const char* fmt, ...) {
   va_list ap;
@@ -35,23 +50,18 @@ bnn_status hip_status(hipError_t e, const char* where) {
   return fail(BNN_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
 }
 
-// Kernel family for binary convs / GEMMs: BNN_ALGO=valu forces the
-// XOR-popcount VALU kernels, BNN_ALGO=mfma prefers the fp4 matrix-core kernel
-// wherever it applies; unset or "auto" picks the matrix cores when the shape
-// allows.  (An ablation switch, read on every call.)
+// Kernel family for binary convs / GEMMs: the fp4 matrix-core kernel where
+// the shape allows it, unless the options ask for the XOR-popcount vector
+// kernels (the ablation).
 bool use_mfma(const bnn::ConvGeom& g) {
-  const char* e = getenv("BNN_ALGO");
-  if (e && strcmp(e, "valu") == 0) return false;
-  return bnn::bconv_mfma_supported(g);
+  return g_opt.algo != BNN_ALGO_VALU && bnn::bconv_mfma_supported(g);
 }
 
 // 1x1 convs with K <= 256 over >= 65536 pixels, bits only: the kernel that
-// keeps a wave's pixel operands and walks all filters (BNN_1X1=0 sends them
-// to the general matrix-core kernel).
+// keeps a wave's pixel operands and walks all filters (option conv1x1 = 0
+// sends them to the general matrix-core kernel).
 bool use_1x1(const bnn::ConvGeom& g, bool sums) {
-  const char* e = getenv("BNN_1X1");
-  if (e && strcmp(e, "0") == 0) return false;
-  return bnn::bconv1x1_supported(g, sums);
+  return g_opt.conv1x1 != 0 && bnn::bconv1x1_supported(g, sums);
 }
 
 hipError_t launch_conv(const bnn::ConvGeom& g, const uint32_t* in, const uint32_t* w,
@@ -150,10 +160,8 @@ bnn_status gemm_launch(int64_t M, int64_t N, int64_t K, const uint32_t* A,
   // At most 2 rows go to the vector-ALU GEMV, whose time grows with every
   // row; from 3 rows on the matrix-core conv kernel (a 1 x M image with 1x1
   // filters) is as fast or faster, and 3x faster at 16 rows (measured on the
-  // FC shapes of the networks here).  BNN_GEMV_MAX_ROWS (0..16) overrides.
-  const char* e = getenv("BNN_GEMV_MAX_ROWS");
-  const int64_t gemv_rows = e ? atoll(e) : 2;
-  if (M <= gemv_rows && M <= 16)
+  // FC shapes of the networks here).  Option gemv_max_rows (0..16) moves it.
+  if (M <= g_opt.gemv_max_rows)
     return hip_status(bnn::launch_bgemv_valu(M, N, K, A, B, thr, flip, sums, bits, s),
                       "bgemm (gemv) launch");
   // M rows of A are a 1 x M image with K channels; B holds N 1x1 filters.
@@ -177,11 +185,43 @@ bnn_status gemm_launch(int64_t M, int64_t N, int64_t K, const uint32_t* A,
 
 }  // namespace
 
+namespace bnn {
+const bnn_options& options() { return g_opt; }
+}  // namespace bnn
+
 extern "C" {
 
 const char* bnn_last_error(void) { return g_err; }
 
 int32_t bnn_abi_version(void) { return BNN_ABI_VERSION; }
+
+void bnn_default_options(bnn_options* opt) {
+  if (opt) *opt = default_options();
+}
+
+bnn_status bnn_set_options(const bnn_options* o) {
+  if (!o) return fail(BNN_ERR_NULL, "set_options: options pointer is NULL");
+  auto flag = [](int32_t v) { return v == 0 || v == 1; };
+  auto tri = [](int32_t v) { return v == -1 || v == 0 || v == 1; };
+  if ((o->algo != BNN_ALGO_AUTO && o->algo != BNN_ALGO_VALU) || !flag(o->fuse_input) ||
+      !flag(o->fuse_first) || !flag(o->fc_chain) || !flag(o->conv1x1) || !flag(o->xcd_order) ||
+      o->gemv_max_rows < 0 || o->gemv_max_rows > 16 || !tri(o->lds_weights) ||
+      !tri(o->late_thresholds))
+    return fail(BNN_ERR_SHAPE,
+                "set_options: out of range (algo %d, fuse_input %d, fuse_first %d, fc_chain %d, "
+                "conv1x1 %d, xcd_order %d, gemv_max_rows %d, lds_weights %d, "
+                "late_thresholds %d)",
+                o->algo, o->fuse_input, o->fuse_first, o->fc_chain, o->conv1x1, o->xcd_order,
+                o->gemv_max_rows, o->lds_weights, o->late_thresholds);
+  g_opt = *o;
+  return ok();
+}
+
+bnn_status bnn_get_options(bnn_options* o) {
+  if (!o) return fail(BNN_ERR_NULL, "get_options: options pointer is NULL");
+  *o = g_opt;
+  return ok();
+}
 
 bnn_status bnn_pack_bits(const float* x, const float* offset, int64_t rows,
                          int64_t D, uint32_t* out, hipStream_t stream) {
@@ -453,12 +493,11 @@ bnn_status plan_chain(const bnn_layer* L, int32_t n, int32_t batch, int32_t H,
 // to the chained FC kernel (1: none).  Every layer in the run has at most
 // kChainWords weight words (each block of the chained kernel reads all of
 // them), the batch is at most 128 rows (beyond that the per-layer kernels
-// have parallelism enough to hide their launches), and BNN_FC_CHAIN=0 keeps
-// one launch per layer.
+// have parallelism enough to hide their launches), and option fc_chain = 0
+// keeps one launch per layer.
 int fc_chain_run(const bnn_layer* L, int32_t li, int32_t n, int32_t batch) {
   constexpr int64_t kChainWords = 8192;
-  const char* e = getenv("BNN_FC_CHAIN");
-  if ((e && strcmp(e, "0") == 0) || batch > 128) return 1;
+  if (g_opt.fc_chain == 0 || batch > 128) return 1;
   int run = 0;
   bnn::FcChainLayer fl[bnn::kFcChainMax];
   while (li + run < n && run < bnn::kFcChainMax) {
@@ -512,26 +551,25 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
     uint32_t* buf[2] = {static_cast<uint32_t*>(workspace),
                         reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + half)};
     // An input threshold followed by a conv whose window fits one word runs
-    // as one patch-packing kernel on the fp32 image (BNN_PATCH=0 keeps the
-    // two separate steps).
+    // as one patch-packing kernel on the fp32 image (option fuse_input = 0
+    // keeps the two separate steps).
     bool fuse_input = false;
     const int mode = input_mode(layers[0].kind);
     if (n_layers > 1 && is_input_kind(layers[0].kind) && layers[1].kind == BNN_LAYER_BCONV) {
-      const char* e = getenv("BNN_PATCH");
       bnn::ConvGeom g1;
       g1.KH = layers[1].KH;
       g1.KW = layers[1].KW;
       g1.C = layers[1].C;
-      fuse_input = !(e && strcmp(e, "0") == 0) && bnn::bconv_patch_supported(g1);
+      fuse_input = g_opt.fuse_input != 0 && bnn::bconv_patch_supported(g1);
     }
     // A real-valued first layer followed by a 3x3 binary conv that fits runs
     // as one kernel with the first layer's bits in LDS (a matrix-core kernel,
-    // so not under BNN_ALGO=valu; BNN_FUSE_FIRST=0 keeps the two launches).
+    // so not under the vector-ALU ablation; option fuse_first = 0 keeps the
+    // two launches).
     bool fuse_first = false;
     bnn::ConvGeom g_first;
     if (n_layers > 1 && layers[0].kind == BNN_LAYER_FCONV_BINW &&
         layers[1].kind == BNN_LAYER_BCONV) {
-      const char* e = getenv("BNN_FUSE_FIRST");
       const bnn_layer& l0 = layers[0];
       const bnn_layer& l1 = layers[1];
       bnn_conv_desc d0{batch, H, W, l0.C, l0.F, l0.KH, l0.KW, l0.stride, l0.pad, l0.pool};
@@ -540,9 +578,8 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
         bnn_conv_desc d1{batch, g_first.Hp, g_first.Wp, l1.C, l1.F,
                          l1.KH, l1.KW, l1.stride, l1.pad, l1.pool};
         // Fused at every batch size (one image of 32 x 32: 38.6 us per
-        // forward fused, 41.0 us as two launches).  BNN_FUSE_FIRST=0 keeps
-        // the two layers apart.
-        fuse_first = !(e && strcmp(e, "0") == 0) && conv_geom(&d1, &g1) == BNN_OK &&
+        // forward fused, 41.0 us as two launches).
+        fuse_first = g_opt.fuse_first != 0 && conv_geom(&d1, &g1) == BNN_OK &&
                      use_mfma(g1) && bnn::fconv_bconv_supported(g_first, g1);
       }
     }

@@ -23,8 +23,6 @@
 //
 // Requirements (bconv_mfma_supported): stride 1, C a multiple of 64, at most
 // 32 taps.
-#include <stdlib.h>
-
 #include "fp4_expand.hpp"
 #include "kernels.hpp"
 #include "lane_ops.hpp"
@@ -732,11 +730,6 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
   epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, ep, pre);
 }
 
-int env_int(const char* name, int dflt) {
-  const char* e = getenv(name);
-  return e ? atoi(e) : dflt;
-}
-
 // Grid of `pblocks` pixel blocks x `fy` filter tiles: one-dimensional in the
 // XCD order of block_tile (pixel blocks padded to a multiple of 8), or 2-D.
 // The XCD order needs at least 8 pixel blocks: with fewer it would leave
@@ -840,7 +833,8 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   a.w_bytes = static_cast<int32_t>(static_cast<int64_t>(g.F) * a.fstride * 4);
   a.div_w = make_fastdiv(static_cast<uint32_t>(pool ? g.Wp : g.Wo));
   a.div_h = make_fastdiv(static_cast<uint32_t>(pool ? g.Hp : g.Ho));
-  a.xcd_map = env_int("BNN_XCD_MAP", 1) != 0 ? 1 : 0;
+  const bnn_options& opt = options();
+  a.xcd_map = opt.xcd_order != 0 ? 1 : 0;
   // Words per lane, row and iteration: 8-word chunks (128-bit loads) where
   // the channels allow, which halves the vector-memory instructions per MFMA
   // (the texture-address unit is the busiest unit of the small grids), but
@@ -861,9 +855,9 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   const int chunks8 = g.KH * g.KW * (g.Cw / 8);
   const bool short8 = !tail && vw == 4 && chunks8 <= 4 && groups * ftiles < 1024;
   if (vw == 4 && chunks8 < 8 && !short8) vw = 2;
-  vw = env_int("BNN_MFMA_VW", vw);
-  if (vw != 1 && vw != 2 && vw != 4) vw = 1;
-  if (g.Cw % (2 * vw) != 0) vw = g.Cw % 4 == 0 ? 2 : 1;
+  // Option lds_weights = 1 asks for the LDS-weights kernel wherever no K
+  // split is used; it takes chunks of at most 2 words.
+  if (opt.lds_weights == 1 && vw == 4) vw = 2;
   if (tail) {
     vw = 1;
     for (int t = 4; t >= 2 && vw == 1; t /= 2)
@@ -890,15 +884,9 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
     const int64_t target = vw == 4 ? 1024 : 2048;
     while (!short8 && ks < 4 && groups * ftiles * ks < target && iters >= 4 * ks) ks *= 2;
   }
-  bool lds = vw <= 2 && tf == 2 && groups * (g.F / 64) >= 4096;
-  // Tuning overrides (filter tiles per wave, K split, weights through LDS).
-  tf = env_int("BNN_MFMA_TF", tf);
-  ks = env_int("BNN_MFMA_KS", ks);
-  lds = env_int("BNN_MFMA_LDS", lds ? 1 : 0) != 0;
-  if (ks != 1 && ks != 2 && ks != 4 && ks != 8) ks = 1;
+  bool lds = opt.lds_weights == -1 ? vw <= 2 && tf == 2 && groups * (g.F / 64) >= 4096
+                                    : opt.lds_weights == 1;
   if (ks > 1 || vw == 4) lds = false;
-  if (tf != 1 && tf != 2) tf = 1;
-  if (g.F % (32 * tf) != 0 || (ks > 4 && tf != 1)) tf = 1;
   if (tail) {
     tf = 1;
     lds = false;
@@ -909,9 +897,10 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   // the accumulators can then start from them (16x16x128 -> 256 and
   // 16x16x256 -> 256 pool at batch 64: 5.98 / 7.50 us early against
   // 6.25 / 7.94 us late; 8x8x256 -> 512 with 32-filter tiles: 6.11 us late,
-  // 6.22 us early).  BNN_MFMA_LATE overrides.
+  // 6.22 us early).  Option late_thresholds overrides.
   const int64_t waves = (groups + 3) / 4 * 4 * ((g.F + 32 * tf - 1) / (32 * tf));
-  const bool late = tail || env_int("BNN_MFMA_LATE", waves <= 2048 && tf == 1 ? 1 : 0) != 0;
+  const bool late = tail || (opt.late_thresholds == -1 ? waves <= 2048 && tf == 1
+                                                       : opt.late_thresholds == 1);
   if (vw == 4)
     return pool ? launch32<4, true>(a, tf, ks, false, late, s)
                 : launch32<4, false>(a, tf, ks, false, late, s);

@@ -8,8 +8,6 @@
 // value is loaded once per lane and added to or subtracted from the 32 filter
 // sums according to the (wave-uniform) weight bits: one sign flip and one add
 // per multiply-accumulate.
-#include <stdlib.h>
-#include <string.h>
 
 #include "kernels.hpp"
 #include "lane_ops.hpp"
@@ -574,9 +572,8 @@ hipError_t run_fmfma(const ConvGeom& g, bool pool, const float* in, const uint32
   // Filter groups of 64 per block: 2 (the input tile and the fp16 halves
   // then serve 128 filters) only for grids that still have >= 4096 waves;
   // on smaller grids the extra parallelism of one group per block wins.
-  int fg = (g.F >= 128 && static_cast<int64_t>(tiles) * ((g.F + 127) / 128) * 4 >= 4096) ? 2 : 1;
-  const char* e = getenv("BNN_FCONV_FG");
-  if (e) fg = atoi(e) == 2 ? 2 : 1;
+  const int fg =
+      (g.F >= 128 && static_cast<int64_t>(tiles) * ((g.F + 127) / 128) * 4 >= 4096) ? 2 : 1;
   const bool full = g.F % 64 == 0;
   dim3 grid(tiles, static_cast<unsigned>((g.F + 64 * fg - 1) / (64 * fg)));
   if (fg == 2) {
@@ -648,8 +645,7 @@ hipError_t launch_fconv_binw(const ConvGeom& g, const float* in,
   // tiles sit on even coordinates, so 2x2 windows never straddle tiles).
   if (g.KH == 3 && g.KW == 3 && g.C <= 4) {
     const bool pool = g.pool == 2;
-    const char* e = getenv("BNN_ALGO");
-    if (!(e && strcmp(e, "valu") == 0)) {
+    if (options().algo != BNN_ALGO_VALU) {
       // The matrix-core kernel's 8 x 32 pixel tiles sit on even coordinates.
       switch (g.C) {
         case 1: return run_fmfma<1>(g, pool, in, w, thr, flip, sums, bits, s);

@@ -25,7 +25,6 @@
 //      global memory, accumulators started at 0.5 - thr (the output bit is
 //      the complement of the sign), OR-pool on lane quads and the packed
 //      store.
-#include <stdlib.h>
 
 #include <type_traits>
 

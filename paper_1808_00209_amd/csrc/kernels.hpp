@@ -6,7 +6,12 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "bnn.h"
+
 namespace bnn {
+
+// The calling thread's kernel-selection options (bnn_set_options).
+const bnn_options& options();
 
 // Mask of the valid (high) bits of the last word of a packed vector of
 // `bits` values: value i of a word sits in bit 31 - i.

@@ -231,3 +231,60 @@ def test_forward_chain_validation():
     # a too-small workspace is refused before any launch
     assert lib.bnn_forward(L, 4, 8, 8, 8, 3, A, A, 256, A, None) == 6
     assert lib.bnn_forward(L, 4, 8, 8, 8, 3, A, A + 16, 1 << 20, A, None) == 3
+
+
+@needs_lib
+def test_options_defaults_set_get_and_range_checks():
+    """Kernel-selection options: defaults, a round trip, per-field range
+    checks (an invalid set leaves the options unchanged), NULL pointers."""
+    lib = bnn.load()
+    d = bnn.bnn_default_options()
+    assert (d.algo, d.fuse_input, d.fuse_first, d.fc_chain, d.conv1x1, d.xcd_order,
+            d.gemv_max_rows, d.lds_weights, d.late_thresholds) == (0, 1, 1, 1, 1, 1, 2, -1, -1)
+    try:
+        bnn.bnn_set_options(algo=bnn.ALGO_VALU, gemv_max_rows=16, lds_weights=1)
+        got = bnn.bnn_get_options()
+        assert (got.algo, got.gemv_max_rows, got.lds_weights) == (1, 16, 1)
+        for field, bad in [("algo", 2), ("fuse_input", 2), ("fuse_first", -1), ("fc_chain", 3),
+                           ("conv1x1", 2), ("xcd_order", -1), ("gemv_max_rows", 17),
+                           ("gemv_max_rows", -1), ("lds_weights", 2), ("late_thresholds", -2)]:
+            with pytest.raises(bnn.BnnError, match="out of range"):
+                bnn.bnn_set_options(**{field: bad})
+            got = bnn.bnn_get_options()
+            assert (got.algo, got.gemv_max_rows, got.lds_weights) == (1, 16, 1)
+        assert lib.bnn_set_options(None) == 1 and "NULL" in bnn.last_error()
+        assert lib.bnn_get_options(None) == 1
+        with bnn.options(fc_chain=0):
+            assert bnn.bnn_get_options().fc_chain == 0
+            assert bnn.bnn_get_options().algo == 0  # the block starts from the defaults
+        assert bnn.bnn_get_options().algo == 1  # restored on exit
+    finally:
+        bnn.bnn_set_options()
+
+
+@needs_lib
+def test_options_are_per_thread():
+    import threading
+    seen = {}
+    try:
+        bnn.bnn_set_options(algo=bnn.ALGO_VALU)
+
+        def other():
+            seen["algo"] = bnn.bnn_get_options().algo
+
+        t = threading.Thread(target=other)
+        t.start()
+        t.join()
+        assert seen["algo"] == bnn.ALGO_AUTO
+        assert bnn.bnn_get_options().algo == bnn.ALGO_VALU
+    finally:
+        bnn.bnn_set_options()
+
+
+def test_library_sources_read_no_environment():
+    """The launch path reads no environment variables: every kernel choice
+    comes from the arguments and the per-thread options."""
+    csrc = os.path.join(ROOT, "paper_1808_00209_amd", "csrc")
+    for f in os.listdir(csrc):
+        src = open(os.path.join(csrc, f)).read()
+        assert "getenv" not in src and "environ" not in src, f

@@ -3,7 +3,7 @@ least 65536 pixels, bits only), which keeps a wave's pixel operands in
 registers and walks all filters in chunks of 64.
 
 Every case runs twice through bnn_bconv2d, once on this kernel and once on
-the general matrix-core kernel (BNN_1X1=0), and the two outputs must agree
+the general matrix-core kernel (option conv1x1 = 0), and the two outputs must agree
 on every word; sampled pixels are also checked against the oracle's sums
 (Eq. 3 with one tap), thresholded, flipped and packed (Eq. 2).  Shapes cover
 C = 64 / 128 / 256 (1, 2 and 4 k-steps), an odd number of filter chunks, a
@@ -34,8 +34,8 @@ def _layer(C, F, seed, lo=None, hi=None):
                 flip=synth.flips(synth.rng(8, seed, synth.T_FLIP), F), pad=0)
 
 
-def _bits(x, L, monkeypatch, use_1x1):
-    monkeypatch.setenv("BNN_1X1", "1" if use_1x1 else "0")
+def _bits(x, L, use_1x1):
+    bnn.bnn_set_options(conv1x1=int(use_1x1))
     N, H, W, C = x.shape
     F = L["w"].shape[0]
     desc = bnn.conv_desc(N, H, W, C, F, 1, 1, 1, 0, 0)
@@ -63,18 +63,18 @@ def _sample_pixels(shape, count, seed):
 
 
 @pytest.mark.parametrize("case", CASES, ids=[str(c) for c in CASES])
-def test_conv1x1_matches_general_kernel_and_oracle(case, monkeypatch):
+def test_conv1x1_matches_general_kernel_and_oracle(case):
     N, H, W, C, F = case
     x = synth.pm1(synth.rng(8, 50 + C, synth.T_X), (N, H, W, C))
     L = _layer(C, F, 60 + F)
-    got = _bits(x, L, monkeypatch, True)
-    ref = _bits(x, L, monkeypatch, False)
+    got = _bits(x, L, True)
+    ref = _bits(x, L, False)
     assert np.array_equal(got, ref)
     pix = _sample_pixels((N, H, W), 150, C + F)
     assert np.array_equal(got[pix[:, 0], pix[:, 1], pix[:, 2]], _oracle_bits_at(x, L, pix))
 
 
-def test_conv1x1_ties_and_extreme_thresholds(monkeypatch):
+def test_conv1x1_ties_and_extreme_thresholds():
     """Thresholds on the sums' parity grid (ties S == thr give bit 1), at
     +-K and beyond it, INT32_MIN / MAX."""
     N, H, W, C, F = 1, 260, 256, 128, 192
@@ -84,25 +84,25 @@ def test_conv1x1_ties_and_extreme_thresholds(monkeypatch):
     thr[thr % 2 == 1] += 1  # even, like every sum with K = 128: ties occur
     thr[:6] = [np.iinfo(np.int32).min, np.iinfo(np.int32).max, -C, C, -C - 1, C + 1]
     L["thr"] = thr.astype(np.int32)
-    got = _bits(x, L, monkeypatch, True)
-    assert np.array_equal(got, _bits(x, L, monkeypatch, False))
+    got = _bits(x, L, True)
+    assert np.array_equal(got, _bits(x, L, False))
     pix = _sample_pixels((N, H, W), 200, 72)
     assert np.array_equal(got[pix[:, 0], pix[:, 1], pix[:, 2]], _oracle_bits_at(x, L, pix))
 
 
-def test_conv1x1_cfg5_full_size_bits(monkeypatch):
+def test_conv1x1_cfg5_full_size_bits():
     """The 1x1 256 -> 1024 layer at 56 x 56, batch 64, bits only (the
     configuration the bench times): every word against the general kernel,
     sampled pixels against the oracle."""
     x, L = synth.cfg5_case("C")
-    got = _bits(x, L, monkeypatch, True)
-    assert np.array_equal(got, _bits(x, L, monkeypatch, False))
+    got = _bits(x, L, True)
+    assert np.array_equal(got, _bits(x, L, False))
     pix = _sample_pixels(x.shape[:3], 60, 73)
     assert np.array_equal(got[pix[:, 0], pix[:, 1], pix[:, 2]], _oracle_bits_at(x, L, pix))
 
 
 @pytest.mark.parametrize("K", [256, 192])
-def test_bgemm_bits_only_through_the_1x1_kernel(K, monkeypatch):
+def test_bgemm_bits_only_through_the_1x1_kernel(K):
     """An FC layer of 70000 rows and 128 outputs runs as a 1 x M image with
     1x1 filters, bits only: with K = 256 it takes the 1x1 kernel (K = 192,
     6 words per row, is not one of its variants and goes to the general
@@ -115,7 +115,7 @@ def test_bgemm_bits_only_through_the_1x1_kernel(K, monkeypatch):
     w = L["w"].reshape(N, K)
     outs = []
     for use in (True, False):
-        monkeypatch.setenv("BNN_1X1", "1" if use else "0")
+        bnn.bnn_set_options(conv1x1=int(use))
         _, bits = bnn.bnn_bgemm(pack_pm1(a), pack_pm1(w), K, to_device(L["thr"], torch.int32),
                                 pack_flips(L["flip"]), want_sums=False)
         torch.cuda.synchronize()

@@ -37,8 +37,8 @@ def _net(name):
     return layers
 
 
-def _run(net, xd, monkeypatch, chain):
-    monkeypatch.setenv("BNN_FC_CHAIN", "1" if chain else "0")
+def _run(net, xd, chain):
+    bnn.bnn_set_options(fc_chain=int(chain))
     out = bnn.bnn_forward(net, xd)
     torch.cuda.synchronize()
     return out.cpu().numpy()
@@ -46,13 +46,13 @@ def _run(net, xd, monkeypatch, chain):
 
 @pytest.mark.parametrize("name", sorted(STACKS))
 @pytest.mark.parametrize("batch", [1, 3, 64, 65, 128, 129])
-def test_fc_chain_matches_per_layer_and_oracle(name, batch, monkeypatch):
+def test_fc_chain_matches_per_layer_and_oracle(name, batch):
     layers = _net(name)
     x = synth.dyadic_normal(synth.rng(8, 90, synth.T_X), (batch, 1, 1, 3))
     net = upload_network(layers, 1, 1, 3)
     xd = to_device(x)
-    got = _run(net, xd, monkeypatch, True)
-    ref = _run(net, xd, monkeypatch, False)
+    got = _run(net, xd, True)
+    ref = _run(net, xd, False)
     assert np.array_equal(got, ref)
     pick = sorted({0, batch // 2, batch - 1})
     assert np.array_equal(got[pick], oracle.forward(layers, x[pick]))

@@ -22,17 +22,11 @@ pytestmark = pytest.mark.gpu
 # the real-valued first layer and the binary conv after it as two launches
 # instead of the fused first-layer kernel.
 @pytest.fixture(params=["auto", "valu", "lds", "nopatch", "nochain", "nofuse"])
-def algo(request, monkeypatch):
-    monkeypatch.setenv("BNN_ALGO", "valu" if request.param == "valu" else "auto")
-    if request.param == "nochain":
-        monkeypatch.setenv("BNN_FC_CHAIN", "0")
-    if request.param == "nofuse":
-        monkeypatch.setenv("BNN_FUSE_FIRST", "0")
-    if request.param == "lds":
-        monkeypatch.setenv("BNN_MFMA_LDS", "1")
-        monkeypatch.setenv("BNN_MFMA_VW", "2")
-    if request.param == "nopatch":
-        monkeypatch.setenv("BNN_PATCH", "0")
+def algo(request):
+    bnn.bnn_set_options(**{"auto": {}, "valu": dict(algo=bnn.ALGO_VALU),
+                           "lds": dict(lds_weights=1), "nopatch": dict(fuse_input=0),
+                           "nochain": dict(fc_chain=0),
+                           "nofuse": dict(fuse_first=0)}[request.param])
     return request.param
 
 

@@ -41,8 +41,8 @@ def _net(name):
             synth.fc_layer(9, 2, Hp * Wp * F1, 10, logits=True)]
 
 
-def _run(net, xd, monkeypatch, fuse):
-    monkeypatch.setenv("BNN_FUSE_FIRST", "1" if fuse else "0")
+def _run(net, xd, fuse):
+    bnn.bnn_set_options(fuse_first=int(fuse))
     out = bnn.bnn_forward(net, xd)
     torch.cuda.synchronize()
     return out.cpu().numpy()
@@ -50,26 +50,26 @@ def _run(net, xd, monkeypatch, fuse):
 
 @pytest.mark.parametrize("name", sorted(CASES))
 @pytest.mark.parametrize("batch", [1, 5])
-def test_fused_first_matches_two_launches_and_oracle(name, batch, monkeypatch):
+def test_fused_first_matches_two_launches_and_oracle(name, batch):
     H, W, C0 = CASES[name][:3]
     layers = _net(name)
     x = synth.dyadic_normal(synth.rng(9, 90, synth.T_X), (batch, H, W, C0))
     net = upload_network(layers, H, W, C0)
     xd = to_device(x)
-    got = _run(net, xd, monkeypatch, True)
-    ref = _run(net, xd, monkeypatch, False)
+    got = _run(net, xd, True)
+    ref = _run(net, xd, False)
     assert np.array_equal(got, ref)
     pick = sorted({0, batch - 1})
     assert np.array_equal(got[pick], oracle.forward(layers, x[pick]))
 
 
-def test_fused_first_cifar_batch64_sampled(monkeypatch):
+def test_fused_first_cifar_batch64_sampled():
     """The CIFAR-shaped net's first two layers at the benchmark's batch."""
     layers, x = synth.cfg3_net(), synth.cfg3_input(64)
     net = upload_network(layers, 32, 32, 3)
     xd = to_device(x)
-    got = _run(net, xd, monkeypatch, True)
-    ref = _run(net, xd, monkeypatch, False)
+    got = _run(net, xd, True)
+    ref = _run(net, xd, False)
     assert np.array_equal(got, ref)
     pick = [0, 37, 63]
     assert np.array_equal(got[pick], oracle.forward(layers, x[pick]))
@@ -97,7 +97,7 @@ def test_fconv_bconv2d_entry_point(name):
     assert np.array_equal(words_u32(got), oracle.pack_eq2(oracle.forward(layers, x)))
 
 
-def test_fused_first_ties_zero_windows_and_extreme_thresholds(monkeypatch):
+def test_fused_first_ties_zero_windows_and_extreme_thresholds():
     """Inputs on a 0.5 grid, so first-layer sums often equal their integer
     threshold (S >= thr gives bit 1); a block of exact zeros, whose windows
     sum to 0 against thresholds of 0; and thresholds far outside any sum
@@ -120,7 +120,7 @@ def test_fused_first_ties_zero_windows_and_extreme_thresholds(monkeypatch):
     x[2] = 0.0
     net = upload_network(layers, H, W, C0)
     xd = to_device(x)
-    got = _run(net, xd, monkeypatch, True)
-    ref = _run(net, xd, monkeypatch, False)
+    got = _run(net, xd, True)
+    ref = _run(net, xd, False)
     assert np.array_equal(got, ref)
     assert np.array_equal(got, oracle.forward(layers, x))

@@ -28,15 +28,10 @@ ALGOS = ["auto", "valu", "lds", "early", "grid2d"]
 
 
 @pytest.fixture(params=ALGOS)
-def algo(request, monkeypatch):
-    monkeypatch.setenv("BNN_ALGO", "valu" if request.param == "valu" else "auto")
-    if request.param == "lds":
-        monkeypatch.setenv("BNN_MFMA_LDS", "1")
-        monkeypatch.setenv("BNN_MFMA_VW", "2")
-    if request.param == "early":
-        monkeypatch.setenv("BNN_MFMA_LATE", "0")
-    if request.param == "grid2d":
-        monkeypatch.setenv("BNN_XCD_MAP", "0")
+def algo(request):
+    bnn.bnn_set_options(**{"auto": {}, "valu": dict(algo=bnn.ALGO_VALU),
+                           "lds": dict(lds_weights=1), "early": dict(late_thresholds=0),
+                           "grid2d": dict(xcd_order=0)}[request.param])
     return request.param
 
 
@@ -332,10 +327,10 @@ GEMV_CASES = [(1, 1, 1), (2, 33, 31), (3, 100, 33), (5, 1024, 8192), (8, 64, 410
 
 
 @pytest.mark.parametrize("case", GEMV_CASES, ids=[str(c) for c in GEMV_CASES])
-def test_bgemv_all_row_counts_bit_exact(case, monkeypatch):
+def test_bgemv_all_row_counts_bit_exact(case):
     """The vector-ALU GEMV kernel at every row count it supports (1..16);
-    bnn_bgemm sends it only M <= 2 by default, BNN_GEMV_MAX_ROWS=16 forces it."""
-    monkeypatch.setenv("BNN_GEMV_MAX_ROWS", "16")
+    bnn_bgemm sends it only M <= 2 by default, option gemv_max_rows = 16 forces it."""
+    bnn.bnn_set_options(gemv_max_rows=16)
     M, N, K = case
     rng = np.random.default_rng(M * 7907 + N * 29 + K)
     a = _pm1(rng, (M, K))
