@@ -362,6 +362,31 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers,
                        const float* input, void* workspace, size_t ws_bytes,
                        int32_t* logits, hipStream_t stream);
 
+/*
+ * bnn_forward without a workspace argument, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  The intermediate bits go to a device array owned by
+ * the library, BNN_FORWARD_SCRATCH_BYTES (64 MiB) on each GPU the library
+ * runs on, held from the first use on that GPU until the process ends.  The
+ * call allocates nothing.  Results are those of bnn_forward, bit for bit.
+ *   layers ... logits, stream: as for bnn_forward.  The stream must belong to
+ *   the current device (else BNN_ERR_UNSUPPORTED).
+ * Every call on one GPU shares that GPU's array: calls that overlap in time
+ * on one GPU (other streams, or other threads without ordering between them)
+ * race and give undefined results; calls on one stream are ordered.  Nothing
+ * in the array needs to start at zero (each layer writes every word of its
+ * output before the next reads it), and a call leaves the last chain's bits
+ * there.  A chain whose bnn_forward_workspace_size exceeds the array gives
+ * BNN_ERR_WORKSPACE before anything is launched.  Other errors as for
+ * bnn_forward.
+ */
+#define BNN_FORWARD_SCRATCH_BYTES ((size_t)64 << 20)
+
+bnn_status bnn_forward_noalloc(const bnn_layer* layers, int32_t n_layers,
+                               int32_t batch, int32_t H, int32_t W, int32_t C,
+                               const float* input, int32_t* logits,
+                               hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -37,7 +37,10 @@ EXPORTED = ["bnn_last_error", "bnn_abi_version", "bnn_default_options", "bnn_set
             "bnn_get_options", "bnn_pack_bits", "bnn_conv_output_dims",
             "bnn_bconv2d", "bnn_fconv2d_binw", "bnn_binarize_input", "bnn_bconv2d_input",
             "bnn_fconv_bconv2d", "bnn_bgemm",
-            "bnn_forward_workspace_size", "bnn_forward"]
+            "bnn_forward_workspace_size", "bnn_forward", "bnn_forward_noalloc"]
+
+# Bytes of bnn_forward_noalloc's per-GPU scratch array (BNN_FORWARD_SCRATCH_BYTES).
+FORWARD_SCRATCH_BYTES = 64 << 20
 
 
 class BnnError(RuntimeError):
@@ -104,6 +107,7 @@ def load(path: str = LIB_PATH):
                                                ctypes.POINTER(ctypes.c_size_t)]
     lib.bnn_forward.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32, P, P,
                                 ctypes.c_size_t, P, P]
+    lib.bnn_forward_noalloc.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32, P, P, P]
     for name in EXPORTED:
         if name not in ("bnn_last_error", "bnn_abi_version", "bnn_default_options"):
             getattr(lib, name).restype = ctypes.c_int
@@ -377,6 +381,22 @@ def bnn_forward(net: Network, x, workspace=None, logits=None, stream=None):
     _check(lib.bnn_forward(net.layers, net.n, batch, net.H, net.W, net.C, _ptr(x),
                            _ptr(workspace), workspace.numel(), _ptr(logits),
                            _stream(stream)))
+    return logits
+
+
+def bnn_forward_noalloc(net: Network, x, logits=None, stream=None):
+    """bnn_forward with the intermediate bits in the library's per-GPU scratch
+    array instead of a workspace (for callers that cannot allocate); returns
+    int32 logits."""
+    lib = load()
+    _dev(x, torch.float32, "x")
+    batch = x.shape[0]
+    n_out = net.layers[net.n - 1].N
+    if logits is None:
+        logits = torch.empty((batch, n_out), dtype=torch.int32, device=x.device)
+    _dev(logits, torch.int32, "logits")
+    _check(lib.bnn_forward_noalloc(net.layers, net.n, batch, net.H, net.W, net.C, _ptr(x),
+                                   _ptr(logits), _stream(stream)))
     return logits
 
 

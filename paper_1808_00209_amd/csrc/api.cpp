@@ -8,6 +8,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
+#include <mutex>
 #include <new>
 
 #include "kernels.hpp"
@@ -390,6 +392,9 @@ namespace {
 
 constexpr size_t kAlign = 256;
 
+// Size of bnn_forward_noalloc's scratch array (BNN_FORWARD_SCRATCH_BYTES).
+constexpr size_t kScratchBytes = BNN_FORWARD_SCRATCH_BYTES;
+
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 // Activation state between layers: an NHWC map of packed bits (or, before
@@ -530,6 +535,181 @@ bnn_status bnn_forward_workspace_size(const bnn_layer* layers, int32_t n_layers,
   }
 }
 
+}  // extern "C"
+
+// Scratch memory of bnn_forward_noalloc: a file-scope device array, one copy
+// per GPU, held from the module's load on that GPU until the process ends.
+// Host code never passes the array's name to a kernel (on the host it is a
+// stand-in, not a device address): each GPU's copy is looked up once with
+// hipGetSymbolAddress, with that GPU current, and that address is used.
+static __device__ __align__(256) unsigned char scratch[BNN_FORWARD_SCRATCH_BYTES];
+
+namespace {
+
+// The layer chain of bnn_forward on a validated plan: `workspace` holds two
+// buffers of `half` bytes (256-byte aligned) for the packed activations.
+bnn_status run_chain(const bnn_layer* layers, int32_t n_layers, int32_t batch, int32_t H,
+                     int32_t W, int32_t C, const float* input, void* workspace, size_t half,
+                     int32_t* logits, hipStream_t stream) {
+  bnn_status st = BNN_OK;
+  uint32_t* buf[2] = {static_cast<uint32_t*>(workspace),
+                      reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + half)};
+  // An input threshold followed by a conv whose window fits one word runs
+  // as one patch-packing kernel on the fp32 image (option fuse_input = 0
+  // keeps the two separate steps).
+  bool fuse_input = false;
+  const int mode = input_mode(layers[0].kind);
+  if (n_layers > 1 && is_input_kind(layers[0].kind) && layers[1].kind == BNN_LAYER_BCONV) {
+    bnn::ConvGeom g1;
+    g1.KH = layers[1].KH;
+    g1.KW = layers[1].KW;
+    g1.C = layers[1].C;
+    fuse_input = g_opt.fuse_input != 0 && bnn::bconv_patch_supported(g1);
+  }
+  // A real-valued first layer followed by a 3x3 binary conv that fits runs
+  // as one kernel with the first layer's bits in LDS (a matrix-core kernel,
+  // so not under the vector-ALU ablation; option fuse_first = 0 keeps the
+  // two launches).
+  bool fuse_first = false;
+  bnn::ConvGeom g_first;
+  if (n_layers > 1 && layers[0].kind == BNN_LAYER_FCONV_BINW &&
+      layers[1].kind == BNN_LAYER_BCONV) {
+    const bnn_layer& l0 = layers[0];
+    const bnn_layer& l1 = layers[1];
+    bnn_conv_desc d0{batch, H, W, l0.C, l0.F, l0.KH, l0.KW, l0.stride, l0.pad, l0.pool};
+    bnn::ConvGeom g1;
+    if (conv_geom(&d0, &g_first) == BNN_OK) {  // (the chain is validated above)
+      bnn_conv_desc d1{batch, g_first.Hp, g_first.Wp, l1.C, l1.F,
+                       l1.KH, l1.KW, l1.stride, l1.pad, l1.pool};
+      // Fused at every batch size (one image of 32 x 32: 38.6 us per
+      // forward fused, 41.0 us as two launches).
+      fuse_first = g_opt.fuse_first != 0 && conv_geom(&d1, &g1) == BNN_OK &&
+                   use_mfma(g1) && bnn::fconv_bconv_supported(g_first, g1);
+    }
+  }
+  int cur = 0;  // buffer holding the current packed activations
+  int64_t h = H, w = W, c = C;
+  for (int32_t li = 0; li < n_layers; ++li) {
+    const bnn_layer& l = layers[li];
+    uint32_t* dst = buf[li == 0 ? 0 : cur ^ 1];
+    const uint32_t* src = buf[cur];
+    hipError_t e = hipSuccess;
+    switch (l.kind) {
+      case BNN_LAYER_INPUT_THRESHOLD:
+      case BNN_LAYER_INPUT_GRAY:
+      case BNN_LAYER_INPUT_LBP:
+        if (!fuse_input) {
+          if (l.kind == BNN_LAYER_INPUT_THRESHOLD)
+            e = bnn::launch_pack_bits(input, l.offset, int64_t{batch} * h * w, c, dst, stream);
+          else
+            e = bnn::launch_binarize(mode, input, l.offset, batch, static_cast<int32_t>(h),
+                                     static_cast<int32_t>(w), static_cast<int32_t>(c), dst,
+                                     stream);
+        }
+        c = bnn::input_channels_of(mode, static_cast<int>(c));
+        break;
+      case BNN_LAYER_FCONV_BINW:
+      case BNN_LAYER_BCONV: {
+        bnn_conv_desc d{batch, static_cast<int32_t>(h), static_cast<int32_t>(w), l.C, l.F,
+                        l.KH, l.KW, l.stride, l.pad, l.pool};
+        bnn::ConvGeom g;
+        conv_geom(&d, &g);
+        if (l.kind == BNN_LAYER_FCONV_BINW) {
+          if (!fuse_first)
+            e = bnn::launch_fconv_binw(g, input, l.w, l.thr, l.flip, nullptr, dst, stream);
+        } else if (li == 1 && fuse_first)
+          e = bnn::launch_fconv_bconv(g_first, g, input, layers[0].w, layers[0].thr,
+                                      layers[0].flip, l.w, l.thr, l.flip, dst, stream);
+        else if (li == 1 && fuse_input)
+          e = bnn::launch_bconv_patch(g, mode, input, layers[0].offset, l.w, l.thr, l.flip,
+                                      nullptr, dst, stream);
+        else
+          e = launch_conv(g, src, l.w, l.thr, l.flip, nullptr, dst, stream);
+        h = g.Hp;
+        w = g.Wp;
+        c = l.F;
+        break;
+      }
+      case BNN_LAYER_BFC: {
+        // A run of small FC layers from here on goes to one chained kernel.
+        const int run = fc_chain_run(layers, li, n_layers, batch);
+        if (run > 1) {
+          bnn::FcChainLayer fl[bnn::kFcChainMax];
+          for (int i = 0; i < run; ++i) {
+            const bnn_layer& q = layers[li + i];
+            const bool lg = q.kind == BNN_LAYER_BFC_LOGITS;
+            fl[i] = bnn::FcChainLayer{q.w, lg ? nullptr : q.thr, lg ? nullptr : q.flip, q.K, q.N};
+          }
+          const bool to_logits = layers[li + run - 1].kind == BNN_LAYER_BFC_LOGITS;
+          e = bnn::launch_bfc_chain(fl, run, batch, src, to_logits ? nullptr : dst,
+                                    to_logits ? logits : nullptr, stream);
+          if (e != hipSuccess) return fail(BNN_ERR_HIP, "forward: layers %d-%d launch: %s", li,
+                                           li + run - 1, hipGetErrorString(e));
+          h = w = 1;
+          c = layers[li + run - 1].N;
+          li += run - 1;  // the run's last layer; its output is in dst
+          break;
+        }
+        st = gemm_launch(batch, l.N, l.K, src, l.w, l.thr, l.flip, nullptr, dst, stream);
+        if (st != BNN_OK) return fail(st, "forward: layer %d: %s", li, g_err);
+        h = w = 1;
+        c = l.N;
+        break;
+      }
+      case BNN_LAYER_BFC_LOGITS: {
+        st = gemm_launch(batch, l.N, l.K, src, l.w, nullptr, nullptr, logits, nullptr, stream);
+        if (st != BNN_OK) return fail(st, "forward: layer %d: %s", li, g_err);
+        break;
+      }
+    }
+    if (e != hipSuccess) return fail(BNN_ERR_HIP, "forward: layer %d launch: %s", li,
+                                     hipGetErrorString(e));
+    cur = (li == 0) ? 0 : cur ^ 1;
+  }
+  return ok();
+}
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// The current device's copy of `scratch`; the stream must belong to it.
+bnn_status scratch_of_device(hipStream_t stream, void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "forward_noalloc: hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(BNN_ERR_UNSUPPORTED, "forward_noalloc: device %d beyond the %d supported", dev,
+                kMaxDevices);
+  if (stream) {
+    hipDevice_t sdev = -1;
+    e = hipStreamGetDevice(stream, &sdev);
+    if (e != hipSuccess) return hip_status(e, "forward_noalloc: hipStreamGetDevice");
+    if (sdev != dev)
+      return fail(BNN_ERR_UNSUPPORTED,
+                  "forward_noalloc: the stream belongs to device %d but device %d is current",
+                  static_cast<int>(sdev), dev);
+  }
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess) return hip_status(e, "forward_noalloc: hipGetSymbolAddress");
+      if (!p || (reinterpret_cast<uintptr_t>(p) % kAlign) != 0)
+        return fail(BNN_ERR_HIP, "forward_noalloc: bad scratch address %p", p);
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return BNN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
                        int32_t H, int32_t W, int32_t C, const float* input,
                        void* workspace, size_t ws_bytes, int32_t* logits,
@@ -548,123 +728,35 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
     if (ws_bytes < 2 * half)
       return fail(BNN_ERR_WORKSPACE, "forward: workspace of %zu bytes, need %zu", ws_bytes,
                   2 * half);
-    uint32_t* buf[2] = {static_cast<uint32_t*>(workspace),
-                        reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + half)};
-    // An input threshold followed by a conv whose window fits one word runs
-    // as one patch-packing kernel on the fp32 image (option fuse_input = 0
-    // keeps the two separate steps).
-    bool fuse_input = false;
-    const int mode = input_mode(layers[0].kind);
-    if (n_layers > 1 && is_input_kind(layers[0].kind) && layers[1].kind == BNN_LAYER_BCONV) {
-      bnn::ConvGeom g1;
-      g1.KH = layers[1].KH;
-      g1.KW = layers[1].KW;
-      g1.C = layers[1].C;
-      fuse_input = g_opt.fuse_input != 0 && bnn::bconv_patch_supported(g1);
-    }
-    // A real-valued first layer followed by a 3x3 binary conv that fits runs
-    // as one kernel with the first layer's bits in LDS (a matrix-core kernel,
-    // so not under the vector-ALU ablation; option fuse_first = 0 keeps the
-    // two launches).
-    bool fuse_first = false;
-    bnn::ConvGeom g_first;
-    if (n_layers > 1 && layers[0].kind == BNN_LAYER_FCONV_BINW &&
-        layers[1].kind == BNN_LAYER_BCONV) {
-      const bnn_layer& l0 = layers[0];
-      const bnn_layer& l1 = layers[1];
-      bnn_conv_desc d0{batch, H, W, l0.C, l0.F, l0.KH, l0.KW, l0.stride, l0.pad, l0.pool};
-      bnn::ConvGeom g1;
-      if (conv_geom(&d0, &g_first) == BNN_OK) {  // (the chain is validated above)
-        bnn_conv_desc d1{batch, g_first.Hp, g_first.Wp, l1.C, l1.F,
-                         l1.KH, l1.KW, l1.stride, l1.pad, l1.pool};
-        // Fused at every batch size (one image of 32 x 32: 38.6 us per
-        // forward fused, 41.0 us as two launches).
-        fuse_first = g_opt.fuse_first != 0 && conv_geom(&d1, &g1) == BNN_OK &&
-                     use_mfma(g1) && bnn::fconv_bconv_supported(g_first, g1);
-      }
-    }
-    int cur = 0;  // buffer holding the current packed activations
-    int64_t h = H, w = W, c = C;
-    for (int32_t li = 0; li < n_layers; ++li) {
-      const bnn_layer& l = layers[li];
-      uint32_t* dst = buf[li == 0 ? 0 : cur ^ 1];
-      const uint32_t* src = buf[cur];
-      hipError_t e = hipSuccess;
-      switch (l.kind) {
-        case BNN_LAYER_INPUT_THRESHOLD:
-        case BNN_LAYER_INPUT_GRAY:
-        case BNN_LAYER_INPUT_LBP:
-          if (!fuse_input) {
-            if (l.kind == BNN_LAYER_INPUT_THRESHOLD)
-              e = bnn::launch_pack_bits(input, l.offset, int64_t{batch} * h * w, c, dst, stream);
-            else
-              e = bnn::launch_binarize(mode, input, l.offset, batch, static_cast<int32_t>(h),
-                                       static_cast<int32_t>(w), static_cast<int32_t>(c), dst,
-                                       stream);
-          }
-          c = bnn::input_channels_of(mode, static_cast<int>(c));
-          break;
-        case BNN_LAYER_FCONV_BINW:
-        case BNN_LAYER_BCONV: {
-          bnn_conv_desc d{batch, static_cast<int32_t>(h), static_cast<int32_t>(w), l.C, l.F,
-                          l.KH, l.KW, l.stride, l.pad, l.pool};
-          bnn::ConvGeom g;
-          conv_geom(&d, &g);
-          if (l.kind == BNN_LAYER_FCONV_BINW) {
-            if (!fuse_first)
-              e = bnn::launch_fconv_binw(g, input, l.w, l.thr, l.flip, nullptr, dst, stream);
-          } else if (li == 1 && fuse_first)
-            e = bnn::launch_fconv_bconv(g_first, g, input, layers[0].w, layers[0].thr,
-                                        layers[0].flip, l.w, l.thr, l.flip, dst, stream);
-          else if (li == 1 && fuse_input)
-            e = bnn::launch_bconv_patch(g, mode, input, layers[0].offset, l.w, l.thr, l.flip,
-                                        nullptr, dst, stream);
-          else
-            e = launch_conv(g, src, l.w, l.thr, l.flip, nullptr, dst, stream);
-          h = g.Hp;
-          w = g.Wp;
-          c = l.F;
-          break;
-        }
-        case BNN_LAYER_BFC: {
-          // A run of small FC layers from here on goes to one chained kernel.
-          const int run = fc_chain_run(layers, li, n_layers, batch);
-          if (run > 1) {
-            bnn::FcChainLayer fl[bnn::kFcChainMax];
-            for (int i = 0; i < run; ++i) {
-              const bnn_layer& q = layers[li + i];
-              const bool lg = q.kind == BNN_LAYER_BFC_LOGITS;
-              fl[i] = bnn::FcChainLayer{q.w, lg ? nullptr : q.thr, lg ? nullptr : q.flip, q.K, q.N};
-            }
-            const bool to_logits = layers[li + run - 1].kind == BNN_LAYER_BFC_LOGITS;
-            e = bnn::launch_bfc_chain(fl, run, batch, src, to_logits ? nullptr : dst,
-                                      to_logits ? logits : nullptr, stream);
-            if (e != hipSuccess) return fail(BNN_ERR_HIP, "forward: layers %d-%d launch: %s", li,
-                                             li + run - 1, hipGetErrorString(e));
-            h = w = 1;
-            c = layers[li + run - 1].N;
-            li += run - 1;  // the run's last layer; its output is in dst
-            break;
-          }
-          st = gemm_launch(batch, l.N, l.K, src, l.w, l.thr, l.flip, nullptr, dst, stream);
-          if (st != BNN_OK) return fail(st, "forward: layer %d: %s", li, g_err);
-          h = w = 1;
-          c = l.N;
-          break;
-        }
-        case BNN_LAYER_BFC_LOGITS: {
-          st = gemm_launch(batch, l.N, l.K, src, l.w, nullptr, nullptr, logits, nullptr, stream);
-          if (st != BNN_OK) return fail(st, "forward: layer %d: %s", li, g_err);
-          break;
-        }
-      }
-      if (e != hipSuccess) return fail(BNN_ERR_HIP, "forward: layer %d launch: %s", li,
-                                       hipGetErrorString(e));
-      cur = (li == 0) ? 0 : cur ^ 1;
-    }
-    return ok();
+    return run_chain(layers, n_layers, batch, H, W, C, input, workspace, half, logits, stream);
   } catch (...) {
     return fail(BNN_ERR_HIP, "forward: unexpected C++ exception");
+  }
+}
+
+bnn_status bnn_forward_noalloc(const bnn_layer* layers, int32_t n_layers, int32_t batch,
+                               int32_t H, int32_t W, int32_t C, const float* input,
+                               int32_t* logits, hipStream_t stream) {
+  try {
+    size_t mx = 0;
+    bnn_status st = plan_chain(layers, n_layers, batch, H, W, C, &mx);
+    if (st != BNN_OK) return st;
+    if (!input || !logits)
+      return fail(BNN_ERR_NULL, "forward_noalloc: input and logits must be non-NULL");
+    if (!aligned16(input) || !aligned16(logits))
+      return fail(BNN_ERR_ALIGN, "forward_noalloc: input/logits must be 16-byte aligned");
+    const size_t half = align_up(mx);
+    if (2 * half > kScratchBytes)
+      return fail(BNN_ERR_WORKSPACE,
+                  "forward_noalloc: the chain needs %zu bytes of intermediate bits, more than "
+                  "the %zu of the library's scratch array (use bnn_forward with a workspace)",
+                  2 * half, kScratchBytes);
+    void* ws = nullptr;
+    st = scratch_of_device(stream, &ws);
+    if (st != BNN_OK) return st;
+    return run_chain(layers, n_layers, batch, H, W, C, input, ws, half, logits, stream);
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "forward_noalloc: unexpected C++ exception");
   }
 }
 

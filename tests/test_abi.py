@@ -234,6 +234,34 @@ def test_forward_chain_validation():
 
 
 @needs_lib
+def test_forward_noalloc_validation_before_any_device_call():
+    """bnn_forward_noalloc checks the chain, its pointers and the size of
+    its intermediate bits against the scratch array before it touches the
+    device: a chain that needs more than BNN_FORWARD_SCRATCH_BYTES gives
+    BNN_ERR_WORKSPACE, NULL / misaligned pointers their errors."""
+    lib = bnn.load()
+    header = open(HEADER).read()
+    assert "#define BNN_FORWARD_SCRATCH_BYTES ((size_t)64 << 20)" in header
+    assert bnn.FORWARD_SCRATCH_BYTES == 64 << 20
+    good = [dict(kind=1, C=3),
+            dict(kind=3, C=3, F=64, KH=3, KW=3, stride=1, pad=1, pool=2, w=A, thr=A),
+            dict(kind=3, C=64, F=64, KH=3, KW=3, stride=1, pad=1, pool=2, w=A, thr=A),
+            dict(kind=5, K=2 * 2 * 64, N=4, w=A)]
+    L = _layers(good)
+    size = ctypes.c_size_t()
+    # 8 x 8 images: two buffers of the thresholded input, batch * 64 pixels *
+    # 1 word * 4 bytes; the largest batch that fits the 64 MiB array is 131072
+    for batch, fits in ((131072, True), (131073, False)):
+        assert lib.bnn_forward_workspace_size(L, 4, batch, 8, 8, 3, ctypes.byref(size)) == 0
+        assert (size.value <= bnn.FORWARD_SCRATCH_BYTES) == fits
+    assert lib.bnn_forward_noalloc(L, 4, 131073, 8, 8, 3, A, A, None) == 6
+    assert "scratch" in bnn.last_error()
+    assert lib.bnn_forward_noalloc(L, 4, 8, 8, 8, 3, None, A, None) == 1
+    assert lib.bnn_forward_noalloc(L, 4, 8, 8, 8, 3, A, A + 4, None) == 3
+    assert lib.bnn_forward_noalloc(L, 3, 8, 8, 8, 3, A, A, None) == 2  # no logits layer
+
+
+@needs_lib
 def test_options_defaults_set_get_and_range_checks():
     """Kernel-selection options: defaults, a round trip, per-field range
     checks (an invalid set leaves the options unchanged), NULL pointers."""
