@@ -180,14 +180,24 @@ bnn_status bnn_bconv2d(const bnn_conv_desc* d, const uint32_t* in,
 /*
  * Real-valued first layer with binary weights ("no input binarization",
  * Table III; the BCNN row of Table I): Eq. 3 with an fp32 image and +-1
- * weights, pad value 0.0, sums accumulated in fp32, then the same threshold /
- * flip / OR-pool epilogue as bnn_bconv2d (S >= thr compared in fp32).
+ * weights, pad value 0.0, then the same threshold / flip / OR-pool epilogue
+ * as bnn_bconv2d.
  *   in        [N][H][W][C] fp32.
  *   w         [F][KH][KW][Cw] u32 packed weights.
  *   out_sums  [N][Ho][Wo][F] fp32 or NULL; out_bits as for bnn_bconv2d.
- * The fp32 sums are exact (independent of summation order) when every input
- * is a multiple of 2^-16 with |x| < 8 and KH*KW*C <= 32 (every partial sum
- * is then a multiple of 2^-16 below 2^8, within fp32's 24-bit significand).
+ * Precision.  Every product x * (+-1) is exact: the matrix-core kernels
+ * split each x exactly into three bf16 parts (exact for finite |x| >= 2^-103
+ * and x = 0; a smaller part may be flushed, losing less than 2^-126), the
+ * vector kernels add +-x directly.  The products are summed in fp32 in an
+ * unspecified order, so for finite sums the result S' satisfies
+ *     |S' - S| <= n * (2^-23 * sum |x| + 2^-126),  n = 3 * KH * KW * C,
+ * the sum of |x| taken over the window.  The output bit is S' >= thr,
+ * compared exactly (no rounding of thr), so it equals the exact bit wherever
+ * |S - thr| exceeds that bound.  When every input is a multiple of 2^-16 and
+ * each window's sum of |x| is below 2^8 (e.g. |x| < 8 with at most 32 values
+ * per window), every partial sum is exact in fp32, S' = S in any order and
+ * the bits are unique.  Non-finite inputs give unspecified sums and bits in
+ * the windows that hold them.
  * Errors as for bnn_bconv2d.
  */
 bnn_status bnn_fconv2d_binw(const bnn_conv_desc* d, const float* in,
@@ -260,7 +270,8 @@ bnn_status bnn_bconv2d_input(const bnn_conv_desc* d, int32_t mode,
  * its output bits (bnn_bconv2d) in one launch, the first layer's bits never
  * leaving the chip (the BCNN of Table I, first two layers).  The result
  * equals bnn_fconv2d_binw followed by bnn_bconv2d, bit for bit, whenever the
- * first layer's sums are exact (see bnn_fconv2d_binw).
+ * first layer's sums are exact, and under the same precision contract
+ * otherwise (see bnn_fconv2d_binw).
  *   d0        the first layer: 3x3, C <= 4, F = 64 or 128, no pooling,
  *             pad 0 or 1.
  *   d1        the second: N, H, W equal to d0's N and output Ho, Wo; 3x3,

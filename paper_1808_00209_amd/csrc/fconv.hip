@@ -1,7 +1,10 @@
 // Real-valued first layer with packed +-1 weights (the paper's BCNN without
 // input binarization, Table I / Table III): Eq. 3 with fp32 image values and
 // +-1 weights, pad value 0.0, fp32 sums, then the threshold / flip / OR-pool
-// epilogue shared with the binary conv.
+// epilogue shared with the binary conv.  Every product with a +-1 weight is
+// exact (the matrix-core path splits x into three bf16 parts), so a sum
+// differs from the exact one only by fp32 rounding in the accumulation; the
+// comparison S >= thr with the integer threshold is exact (thr_ceil_f32).
 //
 // Lane = output pixel, wave = 64 pixels x 32 filters (one output word per
 // lane), pooled windows on lane quads as in the binary conv.  Each image
@@ -9,6 +12,7 @@
 // sums according to the (wave-uniform) weight bits: one sign flip and one add
 // per multiply-accumulate.
 
+#include "fp32_split.hpp"
 #include "kernels.hpp"
 #include "lane_ops.hpp"
 
@@ -97,7 +101,7 @@ __global__ __launch_bounds__(256) void fconv_binw_kernel(FconvArgs a) {
 #pragma unroll
     for (int f = 0; f < 32; ++f)
       if (FULL || f < nf)
-        word |= static_cast<uint32_t>(acc[f] >= static_cast<float>(th[f])) << (31 - f);
+        word |= static_cast<uint32_t>(acc[f] >= thr_ceil_f32(th[f])) << (31 - f);
     if (a.flip) word ^= a.flip[fg];
     if (!FULL && nf < 32) word &= ~0u << (32 - nf);
     if constexpr (POOL) {
@@ -154,7 +158,7 @@ __global__ __launch_bounds__(256) void fconv_lanef_kernel(FconvArgs a) {
       }
     }
   }
-  const float th = fvalid ? static_cast<float>(a.thr ? a.thr[f] : 0) : 0.0f;
+  const float th = thr_ceil_f32(fvalid && a.thr ? a.thr[f] : 0);
 
   // Output tile.
   const int tiles_w = (a.Wo + kTileW - 1) / kTileW;
@@ -306,24 +310,23 @@ hipError_t run_fconv(const ConvGeom& g, bool pool, const float* in,
 
 // Matrix-core path for few input channels: the block stages a zero-padded
 // (8 + KH - 1) x (32 + KW - 1) x C input tile in LDS (the pad value 0.0 comes
-// for free), splits every staged value x into two fp16 parts, x = hi + lo
-// (hi = x rounded to fp16, lo = x - hi), and v_mfma_f32_16x16x32_f16
-// multiplies them by the +-1 weights.  For inputs on the 2^-16 grid with
-// |x| < 8 both parts are exact fp16 values, every product is exact and every
-// partial sum is a multiple of 2^-16 below 2^8, so the fp32 sums are exact in
-// any order (other inputs are summed to within about 2^-22 relative per term).
+// for free), splits every staged value x exactly into three bf16 parts
+// (split3), and v_mfma_f32_16x16x32_bf16 multiplies them by the +-1 weights
+// into fp32 accumulators: every product is exact and only the fp32 additions
+// round.  For inputs on the 2^-16 grid whose window sums of |x| stay below
+// 2^8 every partial sum is a multiple of 2^-16 below 2^8, so the sums are
+// exact in any order.
 // Block = 4 waves = an 8 x 32 tile of output pixels (4 x 16 2x2 windows when
 // pooling) x FG groups of 64 filters; the result layout and epilogue follow
 // the binary matrix-core kernel (lane: one pixel, four filters).  The +-1
 // weight operands of the FG groups are built once per block into LDS by all
 // its threads (their global loads overlap the input tile's), and every wave
-// reads them with one ds_read_b128 per operand; the fp16 halves of each
+// reads them with one ds_read_b128 per operand; the bf16 parts of each
 // pixel window are built once and reused by every filter group.
 constexpr int kMfTileH = 8;
 constexpr int kMfTileW = 32;
 
 typedef float v4f __attribute__((ext_vector_type(4)));
-typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 
 template <int C, int KH, int KW, bool POOL, bool FULL, int FG>
 __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
@@ -332,7 +335,7 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
   constexpr int LW = kMfTileW + KW - 1;
   constexpr int LH = kMfTileH + KH - 1;
   __shared__ float tile[LH * LW * C];
-  __shared__ v8h wop[FG][KC][4][64];
+  __shared__ v8bf wop[FG][KC][4][64];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -358,7 +361,7 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) {
       const int f = fb + 64 * g + 16 * tf + cc;
-      v8h op;
+      uint16_t op[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int k = 32 * kc + 8 * qq + e;
@@ -368,10 +371,9 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
         const uint32_t word = a.w[static_cast<size_t>(ok ? f : 0) * a.fstride +
                                   (ok ? tap * a.Cw + (ch >> 5) : 0)];
         const bool one = (word >> (31 - (ch & 31))) & 1u;
-        op[e] = ok ? (one ? static_cast<_Float16>(1.0f) : static_cast<_Float16>(-1.0f))
-                   : static_cast<_Float16>(0.0f);
+        op[e] = ok ? (one ? kBf16One : kBf16MinusOne) : kBf16Zero;
       }
-      wop[g][kc][tf][threadIdx.x & 63] = op;
+      wop[g][kc][tf][threadIdx.x & 63] = bf16x8(op);
     }
   }
 
@@ -381,7 +383,7 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
   __shared__ uint32_t fll[FG * 2];
   if (a.bits && threadIdx.x < FG * 64) {
     const int f = fb + static_cast<int>(threadIdx.x);
-    thl[threadIdx.x] = (FULL || f < a.F) ? static_cast<float>(a.thr[f]) : 0.0f;
+    thl[threadIdx.x] = thr_ceil_f32((FULL || f < a.F) ? a.thr[f] : 0);
   }
   if (threadIdx.x < FG * 2) {
     const int wi = fb / 32 + static_cast<int>(threadIdx.x);
@@ -426,21 +428,26 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
       pc[tp] = 16 * (tp & 1) + c;
     }
   }
-  // fp16 halves of the 4 pixel windows (B operands), shared by all groups.
-  v8h xh[KC][4], xl[KC][4];
+  // bf16 parts of the 4 pixel windows (B operands), shared by all groups.
+  v8bf xp[3][KC][4];
 #pragma unroll
   for (int tp = 0; tp < 4; ++tp) {
     const int pbase = (pr[tp] * LW + pc[tp]) * C;
 #pragma unroll
-    for (int kc = 0; kc < KC; ++kc)
+    for (int kc = 0; kc < KC; ++kc) {
+      uint16_t p0[8], p1[8], p2[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float xv = tile[pbase + max(rel[kc][e], 0)];
-        const float x = rel[kc][e] >= 0 ? xv : 0.0f;
-        const _Float16 h = static_cast<_Float16>(x);
-        xh[kc][tp][e] = h;
-        xl[kc][tp][e] = static_cast<_Float16>(x - static_cast<float>(h));
+        const Split3 sp = split3(rel[kc][e] >= 0 ? xv : 0.0f);
+        p0[e] = bf16_bits(sp.p0);
+        p1[e] = bf16_bits(sp.p1);
+        p2[e] = bf16_bits(sp.p2);
       }
+      xp[0][kc][tp] = bf16x8(p0);
+      xp[1][kc][tp] = bf16x8(p1);
+      xp[2][kc][tp] = bf16x8(p2);
+    }
   }
 
 #pragma unroll
@@ -454,16 +461,17 @@ __global__ __launch_bounds__(256) void fconv_mfma_kernel(FconvArgs a) {
       for (int tp = 0; tp < 4; ++tp) acc[tf][tp] = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) {
-      v8h wa[4];
+      v8bf wa[4];
 #pragma unroll
       for (int tf = 0; tf < 4; ++tf) wa[tf] = wop[g][kc][tf][lane];
 #pragma unroll
-      for (int tf = 0; tf < 4; ++tf)
+      for (int pt = 0; pt < 3; ++pt)
 #pragma unroll
-        for (int tp = 0; tp < 4; ++tp) {
-          acc[tf][tp] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[tf], xh[kc][tp], acc[tf][tp], 0, 0, 0);
-          acc[tf][tp] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[tf], xl[kc][tp], acc[tf][tp], 0, 0, 0);
-        }
+        for (int tf = 0; tf < 4; ++tf)
+#pragma unroll
+          for (int tp = 0; tp < 4; ++tp)
+            acc[tf][tp] =
+                __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[tf], xp[pt][kc][tp], acc[tf][tp], 0, 0, 0);
     }
 
     // Epilogue: lane (q, c) holds pixel c of each tile and filters 16 tf + 4 q + r.
@@ -569,7 +577,7 @@ hipError_t run_fmfma(const ConvGeom& g, bool pool, const float* in, const uint32
   a.items = 0;
   const unsigned tiles = static_cast<unsigned>(g.N) * ((g.Ho + kMfTileH - 1) / kMfTileH) *
                          ((g.Wo + kMfTileW - 1) / kMfTileW);
-  // Filter groups of 64 per block: 2 (the input tile and the fp16 halves
+  // Filter groups of 64 per block: 2 (the input tile and the bf16 parts
   // then serve 128 filters) only for grids that still have >= 4096 waves;
   // on smaller grids the extra parallelism of one group per block wins.
   const int fg =

@@ -8,13 +8,14 @@
 // 128; 4 waves per 64 filters).
 //   1. It stages the input tile the first layer needs for the (8 + 2) x
 //      (32 + 2) pixels of the second layer's windows (halo of one pixel),
-//      zero outside the image, with every value split once into two fp16
-//      parts x = hi + lo, plus both layers' thresholds and the first layer's
-//      +-1 weight operands.  All global loads are issued before the first
-//      LDS store.
+//      zero outside the image, with every value split once into three bf16
+//      parts, x = p0 + p1 + p2 exactly (split3), plus both layers'
+//      thresholds and the first layer's +-1 weight operands.  All global
+//      loads are issued before the first LDS store.
 //   2. All waves compute the first layer's outputs on that 10 x 34 tile with
-//      v_mfma_f32_16x16x32_f16 on the hi and lo parts (for inputs on the
-//      2^-16 grid with |x| < 8 the fp32 sums are exact in any order), take
+//      v_mfma_f32_16x16x32_bf16 on the three parts (exact products, fp32
+//      accumulation; exact sums in any order for inputs on the 2^-16 grid
+//      whose window sums of |x| stay below 2^8), take
 //      the sign bits of S - thr, OR the four lane rows' parts of the words
 //      together (lane row q then holds word q of its pixel), flip, and store
 //      each word in LDS already expanded to its fp4 operand.  Pixels outside
@@ -28,14 +29,13 @@
 
 #include <type_traits>
 
+#include "fp32_split.hpp"
 #include "fp4_expand.hpp"
 #include "kernels.hpp"
 #include "lane_ops.hpp"
 
 namespace bnn {
 namespace {
-
-typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 
 constexpr int kTH = 8, kTW = 32;             // second-layer output tile
 constexpr int kAH = kTH + 2, kAW = kTW + 2;  // first-layer tile (second layer's windows)
@@ -79,8 +79,8 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
   constexpr int NX = kIH * kIW * C0;  // input values of the tile
   constexpr int XIT = (NX + NT - 1) / NT;
 
-  __shared__ _Float16 xs[2][NX];       // input tile, fp16 high and low parts
-  __shared__ v8h wop[FT0][KC0][64];
+  __shared__ uint16_t xs[3][NX];       // input tile, the three bf16 parts
+  __shared__ v8bf wop[FT0][KC0][64];
   // First-layer output bits, each word already expanded to its fp4 operand:
   // word wi of tile pixel (r, c) at r RSX + c PSX + wi.  The spare entry per
   // pixel and the row stride (= 4 mod 8 entries) spread the 16-byte reads of
@@ -146,34 +146,34 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
       KBits bits = 0;
 #pragma unroll
       for (int t = 0; t < 9; ++t) bits = (bits << C0) | static_cast<KBits>(w0v[i][t] >> (32 - C0));
-      v8h op;
+      uint16_t op[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int k = 32 * kc + 8 * q + j;
         const bool ok = k < K0;
         const bool one = (bits >> (ok ? K0 - 1 - k : 0)) & 1u;
-        op[j] = ok ? (one ? static_cast<_Float16>(1.0f) : static_cast<_Float16>(-1.0f))
-                   : static_cast<_Float16>(0.0f);
+        op[j] = ok ? (one ? kBf16One : kBf16MinusOne) : kBf16Zero;
       }
-      wop[ft][kc][l] = op;
+      wop[ft][kc][l] = bf16x8(op);
     }
   }
-  // First-layer thresholds, clamped to +-2^16 (|S| < 2^8 keeps every
-  // comparison) and stored as -float(-thr), which makes a zero threshold -0.0:
-  // then S - thr is -0.0 only for S < thr, also when S is -0.0.
-  if (tid < F0) th0[tid] = -static_cast<float>(-min(max(thr0v, -65536), 65536));
+  // First-layer thresholds as the smallest fp32 value >= thr (-0.0 for a
+  // zero threshold): the sign bit of S - th0 is then clear exactly when
+  // S >= thr, for every fp32 sum S (thr_ceil_f32).
+  if (tid < F0) th0[tid] = thr_ceil_f32(thr0v);
   if (tid < CW1) fl0[tid] = fl0v;
   // Second-layer start values 0.5 - thr (thr clamped to [-K1-1, K1+1], which
   // keeps every comparison since |S| <= K1).
   if (tid < F1) th1[tid] = 0.5f - static_cast<float>(min(max(thr1v, -a.K1 - 1), a.K1 + 1));
-  // Each input value split once into x = hi + lo, both fp16 and exact.
+  // Each input value split once into its three bf16 parts.
 #pragma unroll
   for (int i = 0; i < XIT; ++i) {
     const int e = tid + i * NT;
     if (e < NX) {
-      const _Float16 hi = static_cast<_Float16>(xv[i]);
-      xs[0][e] = hi;
-      xs[1][e] = static_cast<_Float16>(xv[i] - static_cast<float>(hi));
+      const Split3 sp = split3(xv[i]);
+      xs[0][e] = bf16_bits(sp.p0);
+      xs[1][e] = bf16_bits(sp.p1);
+      xs[2][e] = bf16_bits(sp.p2);
     }
   }
   __syncthreads();
@@ -198,7 +198,7 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
         const int kh = tap / 3, kw = tap - kh * 3;
         koff[kc][j] = k < K0 ? (kh * kIW + kw) * C0 + ch : 0;
       }
-    v8h wa[FT0][KC0];
+    v8bf wa[FT0][KC0];
 #pragma unroll
     for (int ft = 0; ft < FT0; ++ft)
 #pragma unroll
@@ -216,30 +216,31 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
       const int pp = pv ? p : 0;
       const int lr = pp / kAW, lc = pp - (pp / kAW) * kAW;
       const int base = (lr * kIW + lc) * C0;
-      v8h xh[KC0], xl[KC0];
+      v8bf xp[3][KC0];
 #pragma unroll
-      for (int kc = 0; kc < KC0; ++kc)
+      for (int pt = 0; pt < 3; ++pt)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          xh[kc][j] = xs[0][base + koff[kc][j]];
-          xl[kc][j] = xs[1][base + koff[kc][j]];
+        for (int kc = 0; kc < KC0; ++kc) {
+          uint16_t v[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v[j] = xs[pt][base + koff[kc][j]];
+          xp[pt][kc] = bf16x8(v);
         }
       const int rr = r0 + lr, cc = c0 + lc;
       const bool inside = pv && rr >= 0 && rr < a.Ho0 && cc >= 0 && cc < a.Wo0;
-      // All filter tiles' products first (high parts, then low parts), so
+      // All filter tiles' products of one part before the next part's, so
       // no MFMA waits on the one before it.
       v4f acc[2 * CW1];
 #pragma unroll
       for (int ft = 0; ft < 2 * CW1; ++ft) acc[ft] = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int kc = 0; kc < KC0; ++kc) {
+      for (int kc = 0; kc < KC0; ++kc)
 #pragma unroll
-        for (int ft = 0; ft < 2 * CW1; ++ft)
-          acc[ft] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[ft][kc], xh[kc], acc[ft], 0, 0, 0);
+        for (int pt = 0; pt < 3; ++pt)
 #pragma unroll
-        for (int ft = 0; ft < 2 * CW1; ++ft)
-          acc[ft] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[ft][kc], xl[kc], acc[ft], 0, 0, 0);
-      }
+          for (int ft = 0; ft < 2 * CW1; ++ft)
+            acc[ft] =
+                __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[ft][kc], xp[pt][kc], acc[ft], 0, 0, 0);
       // Sign bits of S - thr, filter fl of word wi at bit 31 - fl.
       uint32_t sg[CW1];
 #pragma unroll
