@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 
 VALU_PEAK_TOPS = 1258.29  # 256 CU x 64 lanes x 2.4 GHz x 32 bit-MACs x 2 ops / 2 instr
 MFMA_FP4_PEAK_TFLOPS = 10100.0  # MI355X dense fp4 matrix peak (1 fp4 MAC = 1 bit-MAC)
-MFMA_FP16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 / fp16 matrix peak
 HBM_PEAK_GBS = 8000.0
 
 # HBM traffic of the dominant kernel from two rocprofv3 --pmc passes
@@ -370,8 +370,13 @@ def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
         else:
             x = torch.randint(-2 ** 31, 2 ** 31 - 1, (batch, g["H"], g["W"], bnn.words(g["C"])),
                               dtype=torch.int32, device="cuda", generator=gen)
-            fn = lambda: bnn.bnn_bconv2d(desc, x, dev_layer["w"], dev_layer["thr"],
-                                         dev_layer.get("flip"), want_sums=False, out_bits=ob)
+            if dev_layer.get("wprep") is not None:  # as bnn_forward runs the layer
+                fn = lambda: bnn.bnn_bconv2d_prepared(desc, x, dev_layer["w"], dev_layer["wprep"],
+                                                      dev_layer["thr"], dev_layer.get("flip"),
+                                                      want_sums=False, out_bits=ob)
+            else:
+                fn = lambda: bnn.bnn_bconv2d(desc, x, dev_layer["w"], dev_layer["thr"],
+                                             dev_layer.get("flip"), want_sums=False, out_bits=ob)
     else:
         A = torch.randint(-2 ** 31, 2 ** 31 - 1, (batch, bnn.words(g["K"])), dtype=torch.int32,
                           device="cuda", generator=gen)
@@ -403,6 +408,36 @@ def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
     e1.record(s)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / reps
+
+
+def per_layer_rows(bnn, torch, layers, shapes, batch, reps):
+    """Per-layer kernel times (Table II analogue): each layer's own call as
+    bnn_forward makes it (prepared conv weights included), on the matrix
+    cores, and again with the vector-ALU XOR-popcount kernels only (option
+    algo = ALGO_VALU): the matrix-core ablation."""
+    from paper_1808_00209_amd.device import upload_layer
+    dev_layers = [upload_layer(L) for L in layers]
+    rows = []
+    for name, kind, g, macs in shapes:
+        dl = ((dev_layers[0], dev_layers[1]) if kind in ("bconv_input", "fconv_bconv")
+              else dev_layers[g["li"]])
+        ms = time_layer(bnn, kind, g, batch, dl, reps, torch)
+        ms_valu = None
+        if kind != "fconv_bconv":  # a matrix-core kernel only (no vector-ALU form)
+            with bnn.options(algo=bnn.ALGO_VALU):
+                ms_valu = time_layer(bnn, kind, g, batch, dl, reps, torch)
+        row = {"layer": name, "ms": round(ms, 5),
+               "ms_valu": round(ms_valu, 5) if ms_valu is not None else None}
+        if macs:
+            tops = 2 * macs * batch / (ms * 1e-3) / 1e12
+            row["GOPS"] = round(tops * 1e3, 1)
+            row["frac_fp4_peak"] = round(tops / MFMA_FP4_PEAK_TFLOPS, 4)
+            if ms_valu is not None:
+                tv = 2 * macs * batch / (ms_valu * 1e-3) / 1e12
+                row["GOPS_valu"] = round(tv * 1e3, 1)
+                row["frac_valu_peak_valu"] = round(tv / VALU_PEAK_TOPS, 4)
+        rows.append(row)
+    return rows
 
 
 def graph_time_us(fn, torch, reps=20):
@@ -459,14 +494,22 @@ def config_suite(bnn, torch):
         ob = torch.empty((N, Hp, Wp, bnn.words(L["F"])), dtype=torch.int32, device="cuda")
         os_ = (torch.empty((N, Ho, Wo, L["F"]), dtype=torch.int32, device="cuda")
                if sums else None)
-        us = graph_time_us(lambda: bnn.bnn_bconv2d(desc, xd, dl["w"], dl["thr"], dl.get("flip"),
-                                                   want_sums=sums, out_sums=os_, out_bits=ob),
-                           torch)
+        # the prepared weights go along, as in bnn_forward (the launcher
+        # uses them where they pay)
+        fn = lambda: bnn.bnn_bconv2d_prepared(desc, xd, dl["w"], dl["wprep"], dl["thr"],
+                                              dl.get("flip"), want_sums=sums, out_sums=os_,
+                                              out_bits=ob)
+        us = graph_time_us(fn, torch)
+        with bnn.options(algo=bnn.ALGO_VALU):
+            us_valu = graph_time_us(fn, torch)
         macs = N * Ho * Wo * L["F"] * L["KH"] * L["KW"] * C
         nbytes = (N * H * W * 4 * bnn.words(C) + L["F"] * L["KH"] * L["KW"] * 4 * bnn.words(C)
                   + 4 * L["F"] + 4 * bnn.words(L["F"]) + N * Hp * Wp * 4 * bnn.words(L["F"])
                   + (N * Ho * Wo * L["F"] * 4 if sums else 0))
+        tops_valu = 2 * macs / (us_valu * 1e-6) / 1e12
         out[name] = dict(rec(us, macs, nbytes),
+                         us_valu=round(us_valu, 3), binary_TOPs_valu=round(tops_valu, 1),
+                         frac_valu_peak_valu=round(tops_valu / VALU_PEAK_TOPS, 4),
                          shape="%dx%dx%dx%d -> %d, %dx%d, pad %d%s" % (
                              N, H, W, C, L["F"], L["KH"], L["KW"], L["pad"],
                              ", int32 sums + bits" if sums else ", bits"))
@@ -495,8 +538,11 @@ def config_suite(bnn, torch):
     out["cfg4_vehicle_net_b256"] = dict(
         us=round(us, 2), binary_TOPs=round(2 * macs / (us * 1e-6) / 1e12, 1),
         images_per_s=round(batch / (us * 1e-6), 1),
-        note="bnn_forward replayed from a HIP graph; per-layer figures with "
-             "--workload vehicle_bnn_b256")
+        per_layer=per_layer_rows(bnn, torch, layers, layer_shapes(layers, 96, 96, 3, batch),
+                                 batch, 20),
+        note="bnn_forward replayed from a HIP graph; per layer: the layer's own call "
+             "replayed 20 times from a HIP graph, on the matrix cores (ms) and with the "
+             "vector-ALU kernels only (ms_valu)")
     for name in "ABC":
         x, L = synth.cfg5_case(name)
         conv_case("cfg5%s" % name, x, L, False)
@@ -621,37 +667,19 @@ def main():
     per_img_us_graph = batch1(True)
 
     # Per-layer kernel times (Table II analogue) and the dominant kernel.
-    # Each layer also runs with the vector-ALU XOR-popcount kernels only
-    # (option algo = ALGO_VALU): the matrix-core ablation.
-    dev_layers = [upload_layer(L) for L in layers]
-    per_layer = []
-    for name, kind, g, macs in shapes:
-        dl = ((dev_layers[0], dev_layers[1]) if kind in ("bconv_input", "fconv_bconv")
-              else dev_layers[g["li"]])
-        ms = time_layer(bnn, kind, g, batch, dl, args.layer_reps, torch)
-        ms_valu = None
-        if kind != "fconv_bconv":  # a matrix-core kernel only (no vector-ALU form)
-            with bnn.options(algo=bnn.ALGO_VALU):
-                ms_valu = time_layer(bnn, kind, g, batch, dl, args.layer_reps, torch)
-        row = {"layer": name, "ms": round(ms, 5),
-               "ms_valu": round(ms_valu, 5) if ms_valu is not None else None}
-        if macs:
-            row["GOPS"] = round(2 * macs * batch / (ms * 1e-3) / 1e9, 1)
-            if ms_valu is not None:
-                row["GOPS_valu"] = round(2 * macs * batch / (ms_valu * 1e-3) / 1e9, 1)
-        per_layer.append(row)
+    per_layer = per_layer_rows(bnn, torch, layers, shapes, batch, args.layer_reps)
     dom_i = max(range(len(shapes)), key=lambda i: per_layer[i]["ms"])
     dom_ms = per_layer[dom_i]["ms"]
     name, kind, g, macs = shapes[dom_i]
     if kind == "fconv":
-        # fp32 first layer on the fp16 matrix cores (v_mfma_f32_16x16x32_f16,
-        # x split into two fp16 halves): 2 algorithmic flops per MAC
+        # fp32 first layer on the bf16 matrix cores (v_mfma_f32_16x16x32_bf16,
+        # x split exactly into three bf16 parts): 2 algorithmic flops per MAC
         fmacs = batch * (g["H"] + 2 * g["pad"] - g["KH"] + 1) * (g["W"] + 2 * g["pad"] - g["KW"] + 1) \
             * g["F"] * g["KH"] * g["KW"] * g["C"]
-        dom_ops, bound, peak, unit = 2 * fmacs, "mfma", MFMA_FP16_PEAK_TFLOPS, "TFLOP/s"
+        dom_ops, bound, peak, unit = 2 * fmacs, "mfma", MFMA_BF16_PEAK_TFLOPS, "TFLOP/s"
     elif kind == "fconv_bconv":
         # the binary second layer on fp4 MFMA is the counted work; the fused
-        # fp32 first layer (fp16 hi/lo MFMA) is reported beside it
+        # fp32 first layer (bf16 MFMA on three parts of x) is reported beside it
         dom_ops, bound, peak, unit = 2 * macs * batch, "mfma", MFMA_FP4_PEAK_TFLOPS, "TFLOP/s"
     elif kind in ("bconv", "bfc", "bfc_logits") and (g.get("C", g.get("K", 0)) % 64 == 0) \
             and not (kind != "bconv" and batch <= 16):
@@ -664,9 +692,9 @@ def main():
     extra_roofline = {}
     if kind == "fconv_bconv":
         fmacs0 = batch * g["Ho0"] * g["Wo0"] * g["F0"] * 9 * g["C"]
-        extra_roofline["first_layer_fp16_tflops"] = round(2 * fmacs0 / (dom_ms * 1e-3) / 1e12, 3)
-        extra_roofline["first_layer_fp16_frac"] = round(
-            2 * fmacs0 / (dom_ms * 1e-3) / 1e12 / MFMA_FP16_PEAK_TFLOPS, 5)
+        extra_roofline["first_layer_bf16_tflops"] = round(2 * fmacs0 / (dom_ms * 1e-3) / 1e12, 3)
+        extra_roofline["first_layer_bf16_frac"] = round(
+            2 * fmacs0 / (dom_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 5)
 
     result = {
         "metric": "binary conv GOPS (2 ops per bit-MAC) and images/s at batch 1 and 64",
@@ -679,7 +707,12 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "u32",
+        "dtype": "fp4",
+        "dtype_detail": "binary layers: +-1 operands packed 32 per u32 word (Eq. 2), computed "
+                        "as fp4 E2M1 on the matrix cores (v_mfma_scale_f32_32x32x64_f8f6f4) "
+                        "with fp32 accumulation, exact for these integer sums; real-valued "
+                        "first layer: fp32 input split exactly into three bf16 parts on the "
+                        "bf16 matrix cores, fp32 accumulation",
         "data": "synthetic",
         "config": {"workload": args.workload, "batch": batch, "input": "%dx%dx%d fp32" % (H, W, C),
                    "binary_ops_per_step": ops_per_step},

@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define BNN_ABI_VERSION 4
+#define BNN_ABI_VERSION 5
 
 typedef enum bnn_status {
   BNN_OK = 0,
@@ -176,6 +176,34 @@ bnn_status bnn_bconv2d(const bnn_conv_desc* d, const uint32_t* in,
                        const uint32_t* w, const int32_t* thr,
                        const uint32_t* flip, int32_t* out_sums,
                        uint32_t* out_bits, hipStream_t stream);
+
+/*
+ * Prepared conv weights: the packed weights of a conv layer in the operand
+ * form of the matrix-core kernel, made once per network (like a filter
+ * transform) so that no kernel spends vector-ALU time expanding weight words
+ * while it runs.  The form is private to this library (16-byte entries of
+ * four fp4 registers per weight word, zero past C, then per-filter int32
+ * offsets); only its size is part of the interface.  Results with prepared
+ * weights are those of bnn_bconv2d, bit for bit (Eq. 3 and Eq. 4 with the
+ * same epilogue).
+ *   bnn_prepared_weights_size: bytes of the prepared form of F filters of
+ *     KH x KW x C bits; BNN_ERR_SHAPE when beyond 2 GiB.
+ *   bnn_prepare_weights: w [F][KH][KW][ceil(C/32)] u32 -> out (device,
+ *     16-byte aligned, that many bytes).  Enqueued on `stream`.
+ *   bnn_bconv2d_prepared: bnn_bconv2d with wprep = the prepared form of w.
+ *     The packed w is still required: the vector-ALU ablation and the
+ *     short-window 1x1 kernel read it.  wprep 16-byte aligned.
+ * Errors: BNN_ERR_NULL, BNN_ERR_SHAPE, BNN_ERR_ALIGN, and as for bnn_bconv2d.
+ */
+bnn_status bnn_prepared_weights_size(int32_t F, int32_t KH, int32_t KW, int32_t C,
+                                     size_t* bytes);
+bnn_status bnn_prepare_weights(int32_t F, int32_t KH, int32_t KW, int32_t C,
+                               const uint32_t* w, void* out, hipStream_t stream);
+bnn_status bnn_bconv2d_prepared(const bnn_conv_desc* d, const uint32_t* in,
+                                const uint32_t* w, const void* wprep,
+                                const int32_t* thr, const uint32_t* flip,
+                                int32_t* out_sums, uint32_t* out_bits,
+                                hipStream_t stream);
 
 /*
  * Real-valued first layer with binary weights ("no input binarization",
@@ -333,6 +361,8 @@ typedef struct bnn_layer {
   const uint32_t* flip;      /* packed flip bits or NULL                     */
   const float* offset;       /* INPUT_THRESHOLD: [C] offsets T; INPUT_GRAY:  */
                              /* [1] offset T; or NULL                        */
+  const void* wprep;         /* BCONV: bnn_prepare_weights of w, or NULL     */
+                             /* (16-byte aligned); other kinds ignore it     */
 } bnn_layer;
 
 /*

@@ -35,7 +35,8 @@ INPUT_LBP = 2
 # Every symbol include/bnn.h declares.
 EXPORTED = ["bnn_last_error", "bnn_abi_version", "bnn_default_options", "bnn_set_options",
             "bnn_get_options", "bnn_pack_bits", "bnn_conv_output_dims",
-            "bnn_bconv2d", "bnn_fconv2d_binw", "bnn_binarize_input", "bnn_bconv2d_input",
+            "bnn_bconv2d", "bnn_prepared_weights_size", "bnn_prepare_weights",
+            "bnn_bconv2d_prepared", "bnn_fconv2d_binw", "bnn_binarize_input", "bnn_bconv2d_input",
             "bnn_fconv_bconv2d", "bnn_bgemm",
             "bnn_forward_workspace_size", "bnn_forward", "bnn_forward_noalloc"]
 
@@ -70,7 +71,7 @@ class Layer(ctypes.Structure):
                 ("KH", ctypes.c_int32), ("KW", ctypes.c_int32), ("stride", ctypes.c_int32),
                 ("pad", ctypes.c_int32), ("pool", ctypes.c_int32), ("K", ctypes.c_int32),
                 ("N", ctypes.c_int32), ("w", ctypes.c_void_p), ("thr", ctypes.c_void_p),
-                ("flip", ctypes.c_void_p), ("offset", ctypes.c_void_p)]
+                ("flip", ctypes.c_void_p), ("offset", ctypes.c_void_p), ("wprep", ctypes.c_void_p)]
 
 
 _lib = None
@@ -97,6 +98,9 @@ def load(path: str = LIB_PATH):
     lib.bnn_pack_bits.argtypes = [P, P, i64, i64, P, P]
     lib.bnn_conv_output_dims.argtypes = [ctypes.POINTER(ConvDesc)] + [ctypes.POINTER(i32)] * 4
     lib.bnn_bconv2d.argtypes = [ctypes.POINTER(ConvDesc), P, P, P, P, P, P, P]
+    lib.bnn_prepared_weights_size.argtypes = [i32, i32, i32, i32, ctypes.POINTER(ctypes.c_size_t)]
+    lib.bnn_prepare_weights.argtypes = [i32, i32, i32, i32, P, P, P]
+    lib.bnn_bconv2d_prepared.argtypes = [ctypes.POINTER(ConvDesc), P, P, P, P, P, P, P, P]
     lib.bnn_fconv2d_binw.argtypes = [ctypes.POINTER(ConvDesc), P, P, P, P, P, P, P]
     lib.bnn_bgemm.argtypes = [i64, i64, i64, P, P, P, P, P, P, P]
     lib.bnn_binarize_input.argtypes = [i32, P, P, i32, i32, i32, i32, P, P]
@@ -237,6 +241,45 @@ def bnn_bconv2d(desc: ConvDesc, x, w, thr=None, flip=None, want_sums=True, want_
     return out_sums, out_bits
 
 
+def bnn_prepared_weights_size(F, KH, KW, C) -> int:
+    out = ctypes.c_size_t()
+    _check(load().bnn_prepared_weights_size(F, KH, KW, C, ctypes.byref(out)))
+    return out.value
+
+
+def bnn_prepare_weights(w, F, KH, KW, C, out=None, stream=None):
+    """Packed conv weights [F, KH, KW, ceil(C/32)] -> the matrix-core operand
+    form (a uint8 device buffer of bnn_prepared_weights_size bytes)."""
+    lib = load()
+    _u32(w)
+    if out is None:
+        out = torch.empty(bnn_prepared_weights_size(F, KH, KW, C), dtype=torch.uint8,
+                          device=w.device)
+    _check(lib.bnn_prepare_weights(F, KH, KW, C, _ptr(w), _ptr(out), _stream(stream)))
+    return out
+
+
+def bnn_bconv2d_prepared(desc: ConvDesc, x, w, wprep, thr=None, flip=None, want_sums=True,
+                         want_bits=True, out_sums=None, out_bits=None, stream=None):
+    """bnn_bconv2d with prepared weights (wprep = bnn_prepare_weights of w)."""
+    lib = load()
+    Ho, Wo, Hp, Wp = bnn_conv_output_dims(desc)
+    _u32(x)
+    _u32(w)
+    _dev(wprep, torch.uint8, "wprep")
+    thr = _dev(thr, torch.int32, "thr")
+    flip = _dev(flip, torch.int32, "flip")
+    if want_sums and out_sums is None:
+        out_sums = torch.empty((desc.N, Ho, Wo, desc.F), dtype=torch.int32, device=x.device)
+    if want_bits and out_bits is None:
+        out_bits = torch.empty((desc.N, Hp, Wp, words(desc.F)), dtype=torch.int32,
+                               device=x.device)
+    _check(lib.bnn_bconv2d_prepared(ctypes.byref(desc), _ptr(x), _ptr(w), _ptr(wprep), _ptr(thr),
+                                    _ptr(flip), _ptr(out_sums), _ptr(out_bits),
+                                    _stream(stream)))
+    return out_sums, out_bits
+
+
 def bnn_fconv2d_binw(desc: ConvDesc, x, w, thr=None, flip=None, want_sums=True,
                      want_bits=True, out_sums=None, out_bits=None, stream=None):
     """fp32-input conv with packed +-1 weights; sums fp32 [N,Ho,Wo,F]."""
@@ -351,7 +394,7 @@ class Network:
             L.kind = d["kind"]
             for f in ("C", "F", "KH", "KW", "stride", "pad", "pool", "K", "N"):
                 setattr(L, f, int(d.get(f, 0)))
-            for f in ("w", "thr", "flip", "offset"):
+            for f in ("w", "thr", "flip", "offset", "wprep"):
                 t = d.get(f)
                 setattr(L, f, None if t is None else t.data_ptr())
         self.layers = arr

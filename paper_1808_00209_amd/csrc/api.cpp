@@ -66,12 +66,17 @@ bool use_1x1(const bnn::ConvGeom& g, bool sums) {
   return g_opt.conv1x1 != 0 && bnn::bconv1x1_supported(g, sums);
 }
 
+// wprep: prepared weights (bnn_prepare_weights) for the general matrix-core
+// kernel, or null; the other kernels take the packed w.
 hipError_t launch_conv(const bnn::ConvGeom& g, const uint32_t* in, const uint32_t* w,
-                       const int32_t* thr, const uint32_t* flip, int32_t* sums,
-                       uint32_t* bits, hipStream_t s) {
+                       const void* wprep, const int32_t* thr, const uint32_t* flip,
+                       int32_t* sums, uint32_t* bits, hipStream_t s) {
   if (use_mfma(g) && bits && use_1x1(g, sums != nullptr))
     return bnn::launch_bconv1x1(g, in, w, thr, flip, bits, s);
-  if (use_mfma(g)) return bnn::launch_bconv_mfma(g, in, w, thr, flip, sums, bits, s);
+  if (use_mfma(g))
+    return bnn::launch_bconv_mfma(g, in, w, wprep && bnn::bconv_mfma_prep_supported(g) ? wprep
+                                                                                         : nullptr,
+                                  thr, flip, sums, bits, s);
   return bnn::launch_bconv_valu(g, in, w, thr, flip, sums, bits, s);
 }
 
@@ -182,7 +187,7 @@ bnn_status gemm_launch(int64_t M, int64_t N, int64_t K, const uint32_t* A,
   g.Wo = g.W;
   g.Hp = 1;
   g.Wp = g.W;
-  return hip_status(launch_conv(g, A, B, thr, flip, sums, bits, s), "bgemm launch");
+  return hip_status(launch_conv(g, A, B, nullptr, thr, flip, sums, bits, s), "bgemm launch");
 }
 
 }  // namespace
@@ -262,10 +267,60 @@ bnn_status bnn_bconv2d(const bnn_conv_desc* d, const uint32_t* in, const uint32_
     if (st != BNN_OK) return st;
     st = check_outputs(in, w, thr, out_sums, out_bits);
     if (st != BNN_OK) return st;
-    return hip_status(launch_conv(g, in, w, thr, flip, out_sums, out_bits, stream),
+    return hip_status(launch_conv(g, in, w, nullptr, thr, flip, out_sums, out_bits, stream),
                       "bconv2d launch");
   } catch (...) {
     return fail(BNN_ERR_HIP, "bconv2d: unexpected C++ exception");
+  }
+}
+
+bnn_status bnn_prepared_weights_size(int32_t F, int32_t KH, int32_t KW, int32_t C,
+                                     size_t* bytes) {
+  if (!bytes) return fail(BNN_ERR_NULL, "prepared_weights_size: bytes is NULL");
+  if (F < 1 || KH < 1 || KW < 1 || C < 1)
+    return fail(BNN_ERR_SHAPE, "prepared_weights_size: F, KH, KW, C must be >= 1");
+  if (int64_t{KH} * KW * C > kMaxItems / 2 || F > (1 << 20))
+    return fail(BNN_ERR_SHAPE, "prepared_weights_size: too large for 32-bit indexing");
+  const int64_t b = bnn::prepared_weights_bytes(F, KH, KW, C);
+  if (b >= (int64_t{1} << 31))
+    return fail(BNN_ERR_SHAPE, "prepared_weights_size: %lld bytes, beyond the 2 GiB supported",
+                (long long)b);
+  *bytes = static_cast<size_t>(b);
+  return ok();
+}
+
+bnn_status bnn_prepare_weights(int32_t F, int32_t KH, int32_t KW, int32_t C,
+                               const uint32_t* w, void* out, hipStream_t stream) {
+  try {
+    size_t bytes = 0;
+    bnn_status st = bnn_prepared_weights_size(F, KH, KW, C, &bytes);
+    if (st != BNN_OK) return st;
+    if (!w || !out) return fail(BNN_ERR_NULL, "prepare_weights: w and out must be non-NULL");
+    if (!aligned16(w) || !aligned16(out))
+      return fail(BNN_ERR_ALIGN, "prepare_weights: w and out must be 16-byte aligned");
+    return hip_status(bnn::launch_prepare_weights(F, KH, KW, C, w, out, stream),
+                      "prepare_weights launch");
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "prepare_weights: unexpected C++ exception");
+  }
+}
+
+bnn_status bnn_bconv2d_prepared(const bnn_conv_desc* d, const uint32_t* in, const uint32_t* w,
+                                const void* wprep, const int32_t* thr, const uint32_t* flip,
+                                int32_t* out_sums, uint32_t* out_bits, hipStream_t stream) {
+  try {
+    bnn::ConvGeom g;
+    bnn_status st = conv_geom(d, &g);
+    if (st != BNN_OK) return st;
+    st = check_outputs(in, w, thr, out_sums, out_bits);
+    if (st != BNN_OK) return st;
+    if (!wprep) return fail(BNN_ERR_NULL, "bconv2d_prepared: wprep is NULL");
+    if (!aligned16(wprep))
+      return fail(BNN_ERR_ALIGN, "bconv2d_prepared: wprep must be 16-byte aligned");
+    return hip_status(launch_conv(g, in, w, wprep, thr, flip, out_sums, out_bits, stream),
+                      "bconv2d_prepared launch");
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "bconv2d_prepared: unexpected C++ exception");
   }
 }
 
@@ -449,8 +504,8 @@ bnn_status plan_chain(const bnn_layer* L, int32_t n, int32_t batch, int32_t H,
           return fail(BNN_ERR_SHAPE, "forward: layer %d expects C=%d, previous layer gives %lld",
                       li, l.C, (long long)a.C);
         if (!l.w || !l.thr) return fail(BNN_ERR_NULL, "forward: layer %d: w and thr are required", li);
-        if (!aligned16(l.w))
-          return fail(BNN_ERR_ALIGN, "forward: layer %d: w must be 16-byte aligned", li);
+        if (!aligned16(l.w) || !aligned16(l.wprep))
+          return fail(BNN_ERR_ALIGN, "forward: layer %d: w and wprep must be 16-byte aligned", li);
         bnn_conv_desc d{batch, static_cast<int32_t>(a.H), static_cast<int32_t>(a.W), l.C, l.F,
                         l.KH, l.KW, l.stride, l.pad, l.pool};
         bnn::ConvGeom g;
@@ -624,7 +679,7 @@ bnn_status run_chain(const bnn_layer* layers, int32_t n_layers, int32_t batch, i
           e = bnn::launch_bconv_patch(g, mode, input, layers[0].offset, l.w, l.thr, l.flip,
                                       nullptr, dst, stream);
         else
-          e = launch_conv(g, src, l.w, l.thr, l.flip, nullptr, dst, stream);
+          e = launch_conv(g, src, l.w, l.wprep, l.thr, l.flip, nullptr, dst, stream);
         h = g.Hp;
         w = g.Wp;
         c = l.F;

@@ -23,6 +23,8 @@
 //
 // Requirements (bconv_mfma_supported): stride 1, C a multiple of 64, at most
 // 32 taps.
+#include <type_traits>
+
 #include "fp4_expand.hpp"
 #include "kernels.hpp"
 #include "lane_ops.hpp"
@@ -105,6 +107,11 @@ struct Mfma32Args {
   int32_t Cc;        // words per tap the loop walks: Cw rounded up to whole chunks
   uint32_t tmask_c;  // valid bits of a pixel's last word (tail_mask(C))
   int32_t pad_bits;  // bit positions per window past C (KH KW (32 Cc - C))
+  // Prepared weights (operand form, see prepare_weights_kernel): w holds
+  // 16-byte entries [F / 32][KH][KW][Cp][32] and corr the per-filter offsets
+  // B_f the sums come out too high by; null for packed weights.
+  const int32_t* corr;
+  int32_t Cp;        // entries per tap and filter of the prepared weights
 };
 
 // The workgroup's pixel block and filter tile.  The workgroups of a launch
@@ -230,25 +237,34 @@ __device__ __forceinline__ void load_act(uint32_t (&aw)[TP][VW], const Mfma32Arg
 template <int TF>
 struct EpiParams {
   int32_t thr;       // this thread's filter's threshold (threads < 32 TF)
+  int32_t corr;      // how much too high this thread's filter's sums come out
   uint32_t fl[TF];   // flip words of the TF filter tiles (wave-uniform)
 
   __device__ __forceinline__ void fetch(const Mfma32Args& a, int f0) {
     thr = 0;
-    if (a.bits && threadIdx.x < 32 * TF) thr = a.thr[min(f0 + static_cast<int>(threadIdx.x), a.F - 1)];
+    const int f = min(f0 + static_cast<int>(threadIdx.x), a.F - 1);
+    if (a.bits && threadIdx.x < 32 * TF) thr = a.thr[f];
+    // packed weights: the zeroed padding positions (pad_bits, the same for
+    // every filter); prepared weights: the filter's B_f
+    corr = a.pad_bits;
+    if (a.corr && threadIdx.x < 32 * TF) corr = a.corr[f];
 #pragma unroll
     for (int tf = 0; tf < TF; ++tf) {
       const int wi = f0 / 32 + tf;
       fl[tf] = a.flip ? a.flip[wi < a.Fw ? wi : a.Fw - 1] : 0u;
     }
   }
-  // Writes the block's thresholds to LDS, as thr - 0.5 (or, with `neg`, as
-  // 0.5 - thr, the accumulators' start value); a barrier must follow.
-  __device__ __forceinline__ void stage(const Mfma32Args& a, float* thl, bool neg) const {
+  // Writes the block's thresholds to LDS, as thr + corr - 0.5 (or, with
+  // `neg`, as 0.5 - thr - corr, the accumulators' start value), and with
+  // prepared weights and sums wanted the offsets corr to cl; a barrier must
+  // follow.
+  __device__ __forceinline__ void stage(const Mfma32Args& a, float* thl, int32_t* cl,
+                                        bool neg) const {
     if (a.bits && threadIdx.x < 32 * TF) {
-      // the sums come out pad_bits too high (zeroed padding positions)
-      const float t = static_cast<float>(min(max(thr, -a.K - 1), a.K + 1) + a.pad_bits) - 0.5f;
+      const float t = static_cast<float>(min(max(thr, -a.K - 1), a.K + 1) + corr) - 0.5f;
       thl[threadIdx.x] = neg ? -t : t;
     }
+    if (a.corr && a.sums && threadIdx.x < 32 * TF) cl[threadIdx.x] = corr;
   }
 };
 
@@ -348,7 +364,7 @@ __device__ __forceinline__ void epi_bits(const Mfma32Args& a, v16f (&acc)[TF][TP
 template <int TF, int TP, bool POOL, int VW>
 __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP],
                                          const PixTiles<TP, POOL, VW>& px, int p0, int f0,
-                                         int h, int c, const float* thl,
+                                         int h, int c, const float* thl, const int32_t* cl,
                                          const EpiParams<TF>& ep, bool pre) {
   // Filters past F (a partial last tile) read zero weights through the
   // buffer range and are masked out of every output.
@@ -365,18 +381,21 @@ __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int fb = f0 + tf * 32 + 8 * g + 4 * h;  // first of 4 filters
+          int cb[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) cb[e] = a.corr ? cl[tf * 32 + 8 * g + 4 * h + e] : a.pad_bits;
           if (!ftail && (a.F & 3) == 0) {
             int4 t;
-            t.x = static_cast<int>(acc[tf][tp][4 * g + 0]) - a.pad_bits;
-            t.y = static_cast<int>(acc[tf][tp][4 * g + 1]) - a.pad_bits;
-            t.z = static_cast<int>(acc[tf][tp][4 * g + 2]) - a.pad_bits;
-            t.w = static_cast<int>(acc[tf][tp][4 * g + 3]) - a.pad_bits;
+            t.x = static_cast<int>(acc[tf][tp][4 * g + 0]) - cb[0];
+            t.y = static_cast<int>(acc[tf][tp][4 * g + 1]) - cb[1];
+            t.z = static_cast<int>(acc[tf][tp][4 * g + 2]) - cb[2];
+            t.w = static_cast<int>(acc[tf][tp][4 * g + 3]) - cb[3];
             *reinterpret_cast<int4*>(sp + tf * 32 + 8 * g) = t;
           } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
               if (fb + e < a.F)
-                sp[tf * 32 + 8 * g + e] = static_cast<int>(acc[tf][tp][4 * g + e]) - a.pad_bits;
+                sp[tf * 32 + 8 * g + e] = static_cast<int>(acc[tf][tp][4 * g + e]) - cb[e];
           }
         }
     }
@@ -390,9 +409,9 @@ __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP
 }
 
 // Template parameters:
-//   VW   words each lane loads per operand row and iteration (1 or 2).  One
-//        MFMA k-step covers 2 words (one per lane half), so an iteration (a
-//        chunk of 2*VW words of one tap) feeds VW k-steps.
+//   VW   words each lane loads per operand row and iteration (1, 2 or 4).
+//        One MFMA k-step covers 2 words (one per lane half), so an
+//        iteration (a chunk of 2*VW words of one tap) feeds VW k-steps.
 //   POOL pixels of a 32-tile ordered as eight 2x2 windows (4 adjacent lanes).
 //   TF   32-filter tiles per wave (1 or 2); a wave always covers 64 pixels.
 //   KS   1: the 4 waves of a block take 4 consecutive 64-pixel groups;
@@ -407,10 +426,18 @@ __device__ __forceinline__ void epilogue(const Mfma32Args& a, v16f (&acc)[TF][TP
 //        otherwise overlaps the other waves' loops (then they are staged at
 //        kernel start).  With KS > 1 they always meet after the loop, at the
 //        barrier the partial sums need anyway.
-// Each wave loads and expands its own weight words in registers.
-template <int VW, bool POOL, int TF, int KS, int PD, bool LATE, bool TAIL = false>
+//   TAIL C not a multiple of 64: activation words loaded one by one (rows of
+//        an odd word count leave wider loads unaligned).
+//   PREP weights in the prepared operand form (prepare_weights_kernel): each
+//        weight word is one 16-byte load of its four registers, and the
+//        activations take the cheaper encoding of act_operand; otherwise
+//        each wave loads packed weight words and expands both operands with
+//        expand_fp4 / expand_pair.
+template <int VW, bool POOL, int TF, int KS, int PD, bool LATE, bool TAIL = false,
+          bool PREP = false>
 __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(Mfma32Args a) {
   constexpr int TP = 2;
+  using WReg = typename std::conditional<PREP, v4i, uint32_t>::type;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int h = lane >> 5;   // k half (operands) / row quad (result)
@@ -429,12 +456,13 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
   }
 
   __shared__ float thl[32 * TF];
+  __shared__ int32_t cl[PREP ? 32 * TF : 1];
   EpiParams<TF> ep;
   ep.fetch(a, f0);
   // Thresholds staged at kernel start: the accumulators start from them.
   const bool pre = KS == 1 && !LATE && a.bits && !a.sums;
   if constexpr (KS == 1 && !LATE) {
-    ep.stage(a, thl, pre);
+    ep.stage(a, thl, cl, pre);
     __syncthreads();
   }
 
@@ -448,26 +476,41 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
       const_cast<uint32_t*>(a.in), 0, a.in_bytes, kRsrcWord3);
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint32_t*>(a.w), 0, a.w_bytes, kRsrcWord3);
+  // Byte offset of this lane's first weight word.  Prepared weights: the
+  // 16-byte entries of word j of one tap for 32 consecutive filters are
+  // adjacent, so each load instruction reads two runs of 512 bytes.
   uint32_t woff[TF];
 #pragma unroll
   for (int tf = 0; tf < TF; ++tf)
-    woff[tf] = static_cast<uint32_t>(((f0 + tf * 32 + c) * a.fstride + h * VW) * 4);
+    woff[tf] = PREP ? static_cast<uint32_t>((((f0 / 32 + tf) * a.fstride + h * VW) * 32 + c) * 16)
+                    : static_cast<uint32_t>(((f0 + tf * 32 + c) * a.fstride + h * VW) * 4);
   const uint32_t smask = __builtin_amdgcn_readfirstlane(0x88888888u);
   uint32_t vfill;
   asm("v_mov_b32 %0, 0x22222222" : "=v"(vfill));
 
   Cursor cur;
   cur.init(a, it0, it1, nchunk, VW);
-  auto load_next = [&](uint32_t (&ww)[TF][VW], uint32_t (&aw)[TP][VW]) {
-    const uint32_t wsoff = static_cast<uint32_t>((cur.tap(a) * a.Cw + cur.l_cc) * 4);
+  auto load_next = [&](WReg (&ww)[TF][VW], uint32_t (&aw)[TP][VW]) {
+    if constexpr (PREP) {
+      const uint32_t wsoff = static_cast<uint32_t>((cur.tap(a) * a.Cp + cur.l_cc) * 512);
 #pragma unroll
-    for (int tf = 0; tf < TF; ++tf) buf_load<VW, TAIL>(ww[tf], rw, woff[tf], wsoff);
+      for (int tf = 0; tf < TF; ++tf)
+#pragma unroll
+        for (int v = 0; v < VW; ++v)
+          ww[tf][v] = __builtin_bit_cast(
+              v4i, __builtin_amdgcn_raw_buffer_load_b128(rw, woff[tf] + 512 * v, wsoff, 0));
+    } else {
+      const uint32_t wsoff = static_cast<uint32_t>((cur.tap(a) * a.Cw + cur.l_cc) * 4);
+#pragma unroll
+      for (int tf = 0; tf < TF; ++tf) buf_load<VW, TAIL>(ww[tf], rw, woff[tf], wsoff);
+    }
     load_act<TP, POOL, VW, TAIL>(aw, a, cur, px, rin);
-    if constexpr (TAIL) {
+    if constexpr (TAIL && !PREP) {
       // C not a multiple of 64: words past a pixel's Cw (read from the next
       // tap or pixel) and the tail bits of its last word are zeroed in both
       // operands.  Each such position then adds (+1)(+1) = 1 to the sum,
-      // pad_bits per window in all, which the epilogue takes off.
+      // pad_bits per window in all, which the epilogue takes off.  (Prepared
+      // weights hold 0.0 at those positions, so their products vanish.)
 #pragma unroll
       for (int v = 0; v < VW; ++v) {
         const int wi = cur.l_cc + h * VW + v;
@@ -480,20 +523,28 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
     }
     cur.advance(a, VW);
   };
-  auto compute = [&](const uint32_t (&ww)[TF][VW], const uint32_t (&aw)[TP][VW]) {
-    constexpr int VP = VW == 1 ? 1 : 2;  // k-steps expanded together
+  auto compute = [&](const WReg (&ww)[TF][VW], const uint32_t (&aw)[TP][VW]) {
+    constexpr int VP = (VW == 1 || PREP) ? 1 : 2;  // k-steps expanded together
 #pragma unroll
     for (int v0 = 0; v0 < VW; v0 += VP) {
       v8i A[TF][VP], B[TP][VP];
+      if constexpr (PREP) {
 #pragma unroll
-      for (int tf = 0; tf < TF; ++tf) {
-        if constexpr (VP == 1) A[tf][0] = expand_fp4(ww[tf][v0], smask, vfill);
-        else expand_pair(ww[tf][v0], ww[tf][v0 + 1], smask, vfill, A[tf][0], A[tf][1]);
-      }
+        for (int tf = 0; tf < TF; ++tf)
+          A[tf][0] = v8i{ww[tf][v0][0], ww[tf][v0][1], ww[tf][v0][2], ww[tf][v0][3], 0, 0, 0, 0};
 #pragma unroll
-      for (int tp = 0; tp < TP; ++tp) {
-        if constexpr (VP == 1) B[tp][0] = expand_fp4(aw[tp][v0], smask, vfill);
-        else expand_pair(aw[tp][v0], aw[tp][v0 + 1], smask, vfill, B[tp][0], B[tp][1]);
+        for (int tp = 0; tp < TP; ++tp) B[tp][0] = act_operand(aw[tp][v0], smask, vfill);
+      } else {
+#pragma unroll
+        for (int tf = 0; tf < TF; ++tf) {
+          if constexpr (VP == 1) A[tf][0] = expand_fp4(ww[tf][v0], smask, vfill);
+          else expand_pair(ww[tf][v0], ww[tf][v0 + 1], smask, vfill, A[tf][0], A[tf][1]);
+        }
+#pragma unroll
+        for (int tp = 0; tp < TP; ++tp) {
+          if constexpr (VP == 1) B[tp][0] = expand_fp4(aw[tp][v0], smask, vfill);
+          else expand_pair(aw[tp][v0], aw[tp][v0 + 1], smask, vfill, B[tp][0], B[tp][1]);
+        }
       }
 #pragma unroll
       for (int v = 0; v < VP; ++v)
@@ -511,7 +562,8 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
     // right after iteration it's MFMAs, so PD - 1 iterations of loads are
     // always in flight.  The scheduling barriers keep each load in place
     // (the scheduler would otherwise sink it below the next MFMAs).
-    uint32_t wr[PD][TF][VW], xr[PD][TP][VW];
+    WReg wr[PD][TF][VW];
+    uint32_t xr[PD][TP][VW];
 #pragma unroll
     for (int d = 0; d < PD; ++d) load_next(wr[d], xr[d]);
     for (int it = it0; it < it1; it += PD) {
@@ -527,7 +579,7 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
 
   if constexpr (KS == 1) {
     if constexpr (LATE) {
-      ep.stage(a, thl, false);
+      ep.stage(a, thl, cl, false);
       __syncthreads();
     }
   } else {
@@ -536,7 +588,7 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
     // into slot 0, and wave 0 takes the totals for the epilogue.
     constexpr int NV = TF * TP * 16 * 64;  // values per wave
     __shared__ float part[KS][NV];
-    ep.stage(a, thl, false);
+    ep.stage(a, thl, cl, false);
 #pragma unroll
     for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
@@ -559,7 +611,7 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[tf][tp][e] = part[0][((tf * TP + tp) * 16 + e) * 64 + lane];
   }
-  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, ep, pre);
+  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, cl, ep, pre);
 }
 
 // The same conv with the weights shared through LDS.  The 4 waves of a block
@@ -680,7 +732,8 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
   // PRE (a template choice: a run-time one costs registers) = bits wanted
   // and no sums.
   constexpr bool pre = PRE;
-  ep.stage(a, thl, pre);
+  __shared__ int32_t cl_unused[1];  // (packed weights: no per-filter offsets)
+  ep.stage(a, thl, cl_unused, pre);
   stage_load(0);
   stage_store(0);
 #pragma unroll
@@ -727,7 +780,7 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
     if (more) stage_store(buf ^ 1);
     __syncthreads();
   }
-  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, ep, pre);
+  epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, cl_unused, ep, pre);
 }
 
 // Grid of `pblocks` pixel blocks x `fy` filter tiles: one-dimensional in the
@@ -742,26 +795,27 @@ dim3 tile_grid(Mfma32Args& a, unsigned pblocks, unsigned fy) {
   return dim3(pblocks, fy);
 }
 
-template <int VW, bool POOL>
-hipError_t launch32(Mfma32Args a, int tf, int ks, bool lds, bool late, hipStream_t s) {
+template <int VW, bool POOL, bool PREP>
+hipError_t launch32(Mfma32Args a, int tf, int ks, bool lds, bool late, bool tail,
+                    hipStream_t s) {
   const unsigned fy = static_cast<unsigned>((a.F + 32 * tf - 1) / (32 * tf));
   const unsigned groups = static_cast<unsigned>((a.items + 63) / 64);
-  if (a.pad_bits > 0) {
+  if (tail) {
     // C not a multiple of 64 (run_mfma: 32-filter tiles, thresholds after
     // the loop, no LDS staging).
     if (ks == 1) {
       const dim3 grid = tile_grid(a, (groups + 3) / 4, fy), block(256);
-      bconv_mfma32_kernel<VW, POOL, 1, 1, 2, true, true><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 1, 2, true, true, PREP><<<grid, block, 0, s>>>(a);
     } else {
       const dim3 grid = tile_grid(a, groups, fy), block(64 * ks);
       if (ks == 2)
-        bconv_mfma32_kernel<VW, POOL, 1, 2, 2, true, true><<<grid, block, 0, s>>>(a);
+        bconv_mfma32_kernel<VW, POOL, 1, 2, 2, true, true, PREP><<<grid, block, 0, s>>>(a);
       else
-        bconv_mfma32_kernel<VW, POOL, 1, 4, 2, true, true><<<grid, block, 0, s>>>(a);
+        bconv_mfma32_kernel<VW, POOL, 1, 4, 2, true, true, PREP><<<grid, block, 0, s>>>(a);
     }
     return hipGetLastError();
   }
-  if constexpr (VW <= 2) {
+  if constexpr (VW <= 2 && !PREP) {
     if (lds) {
       const dim3 grid = tile_grid(a, (groups + 3) / 4, fy), block(256);
       const bool pre = a.bits && !a.sums;
@@ -779,37 +833,140 @@ hipError_t launch32(Mfma32Args a, int tf, int ks, bool lds, bool late, hipStream
   if (ks == 1) {
     const dim3 grid = tile_grid(a, (groups + 3) / 4, fy), block(256);
     if (tf == 2 && late)
-      bconv_mfma32_kernel<VW, POOL, 2, 1, 2, true><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 2, 1, 2, true, false, PREP><<<grid, block, 0, s>>>(a);
     else if (tf == 2)
-      bconv_mfma32_kernel<VW, POOL, 2, 1, 2, false><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 2, 1, 2, false, false, PREP><<<grid, block, 0, s>>>(a);
     else if (late)
-      bconv_mfma32_kernel<VW, POOL, 1, 1, 2, true><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 1, 2, true, false, PREP><<<grid, block, 0, s>>>(a);
     else
-      bconv_mfma32_kernel<VW, POOL, 1, 1, 2, false><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 1, 2, false, false, PREP><<<grid, block, 0, s>>>(a);
   } else {
     const dim3 grid = tile_grid(a, groups, fy), block(64 * ks);
     if (tf == 2) {
       if (ks == 2)
-        bconv_mfma32_kernel<VW, POOL, 2, 2, 2, true><<<grid, block, 0, s>>>(a);
+        bconv_mfma32_kernel<VW, POOL, 2, 2, 2, true, false, PREP><<<grid, block, 0, s>>>(a);
       else
-        bconv_mfma32_kernel<VW, POOL, 2, 4, 2, true><<<grid, block, 0, s>>>(a);
+        bconv_mfma32_kernel<VW, POOL, 2, 4, 2, true, false, PREP><<<grid, block, 0, s>>>(a);
     } else if (ks == 2) {
-      bconv_mfma32_kernel<VW, POOL, 1, 2, 2, true><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 2, 2, true, false, PREP><<<grid, block, 0, s>>>(a);
     } else if (ks == 4) {
-      bconv_mfma32_kernel<VW, POOL, 1, 4, 2, true><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 4, 2, true, false, PREP><<<grid, block, 0, s>>>(a);
     } else {
-      bconv_mfma32_kernel<VW, POOL, 1, 8, 2, true><<<grid, block, 0, s>>>(a);
+      bconv_mfma32_kernel<VW, POOL, 1, 8, 2, true, false, PREP><<<grid, block, 0, s>>>(a);
     }
   }
   return hipGetLastError();
 }
 
+template <int VW, bool POOL>
+hipError_t launch_vw(Mfma32Args a, int tf, int ks, bool lds, bool late, bool tail,
+                     hipStream_t s) {
+  if (a.corr) return launch32<VW, POOL, true>(a, tf, ks, false, late, tail, s);
+  return launch32<VW, POOL, false>(a, tf, ks, lds, late, tail, s);
+}
+
+// Launch plan of the matrix-core conv for a geometry: words per lane and
+// iteration (vw), filter tiles per wave (tf), K split (ks), weights through
+// LDS (lds), late threshold staging (late), C not a multiple of 64 (tail),
+// and whether prepared weights pay (prep).
+struct Plan {
+  int vw, tf, ks;
+  bool lds, late, tail, short8, prep;
+};
+
+Plan plan_mfma(const ConvGeom& g, bool pool) {
+  const bnn_options& opt = options();
+  Plan p;
+  const int64_t items = pool ? 4 * int64_t{g.N} * g.Hp * g.Wp : int64_t{g.N} * g.Ho * g.Wo;
+  const int64_t groups = (items + 63) / 64;
+  const int64_t ftiles = (g.F + 31) / 32;
+  // Words per lane, row and iteration: 8-word chunks (128-bit loads) where
+  // the channels allow, which halves the vector-memory instructions per MFMA
+  // (the texture-address unit is the busiest unit of the small grids), but
+  // not when that leaves fewer than 8 iterations to split.
+  // C not a multiple of 64: the loop walks Cc >= Cw words per tap, whole
+  // chunks of 2 VW words, with the words past Cw zeroed and every word
+  // loaded on its own (bconv_mfma32_kernel, TAIL).  VW is the largest of 4,
+  // 2, 1 whose padding stays within 1/8 of the row.
+  p.tail = g.C % 64 != 0;
+  int vw = g.Cw % 8 == 0 ? 4 : g.Cw % 4 == 0 ? 2 : 1;
+  // Windows of at most 4 eight-word chunks (K <= 1024 bits, e.g. FC layers
+  // of 1024 inputs) on grids too small to fill the chip keep 8-word chunks
+  // and no K split: there the split's LDS reduction costs more than it
+  // hides (1024 -> 1024 and 1024 -> 10 at 64 rows: 4.15 and 4.30 us against
+  // 4.42 and 4.57 us with 2-word chunks split 4 ways).
+  const int chunks8 = g.KH * g.KW * (g.Cw / 8);
+  p.short8 = !p.tail && vw == 4 && chunks8 <= 4 && groups * ftiles < 1024;
+  if (vw == 4 && chunks8 < 8 && !p.short8) vw = 2;
+  // Option lds_weights = 1 asks for the LDS-weights kernel wherever no K
+  // split is used; it takes chunks of at most 2 words.
+  if (opt.lds_weights == 1 && vw == 4) vw = 2;
+  if (p.tail) {
+    vw = 1;
+    for (int t = 4; t >= 2 && vw == 1; t /= 2)
+      if (((g.Cw + 2 * t - 1) / (2 * t) * (2 * t) - g.Cw) * 8 <= g.Cw) vw = t;
+  }
+  p.vw = vw;
+  const int Cc = (g.Cw + 2 * vw - 1) / (2 * vw) * (2 * vw);
+  const int iters = g.KH * g.KW * (Cc / (2 * vw));
+
+  // Tile shape and K split: 64-filter wave tiles down to ~1 wave per SIMD
+  // (1024 waves), then 32-filter tiles with a K split over up to 4 waves
+  // until there are ~1 (8-word chunks) or ~2 (smaller chunks) waves per
+  // SIMD, keeping at least 2 iterations per wave.  Splitting 8 ways never
+  // beat 4 (the LDS reduction then costs more than it hides).  With 2-word
+  // chunks, grids of >= 4096 64-filter tiles stage the weights through LDS
+  // (5-20 % faster there, slower on smaller grids); 8-word chunks without
+  // staging were as fast or faster wherever the channels allow them.  All
+  // measured on every layer shape of the networks here.
+  int tf = 2, ks = 1;
+  if (g.F % 64 != 0 || groups * (g.F / 64) < 1024) {
+    tf = 1;
+    const int64_t target = vw == 4 ? 1024 : 2048;
+    while (!p.short8 && ks < 4 && groups * ftiles * ks < target && iters >= 4 * ks) ks *= 2;
+  }
+  bool lds = opt.lds_weights == -1 ? vw <= 2 && tf == 2 && groups * (g.F / 64) >= 4096
+                                    : opt.lds_weights == 1;
+  if (ks > 1 || vw == 4) lds = false;
+  if (p.tail) {
+    tf = 1;
+    lds = false;
+    if (ks > 4) ks = 4;
+  }
+  p.tf = tf;
+  p.ks = ks;
+  p.lds = lds;
+  // Thresholds staged after the main loop on grids of at most 2 waves per
+  // SIMD (2048 waves) with 32-filter tiles, at kernel start otherwise, where
+  // the accumulators can then start from them (16x16x128 -> 256 and
+  // 16x16x256 -> 256 pool at batch 64: 5.98 / 7.50 us early against
+  // 6.25 / 7.94 us late; 8x8x256 -> 512 with 32-filter tiles: 6.11 us late,
+  // 6.22 us early).  Option late_thresholds overrides.
+  const int64_t waves = (groups + 3) / 4 * 4 * ((g.F + 32 * tf - 1) / (32 * tf));
+  p.late = p.tail || (opt.late_thresholds == -1 ? waves <= 2048 && tf == 1
+                                                 : opt.late_thresholds == 1);
+  // Prepared weights where they pay (graph-timed on every conv shape of the
+  // networks here): 32-filter tiles, where a wave's vector-ALU work per MFMA
+  // then drops from 12 to 8 instructions (8x8x512 -> 512 pool at batch 64:
+  // 9.7 -> 8.2 us; 8x8x256 -> 512: 6.6 -> 6.0 us), and rows of at most 2
+  // words.  With 64-filter tiles over 256 or more channels the prepared
+  // operands' registers cost a wave per SIMD (180 against 154 VGPRs) and
+  // 4x the weight bytes through L1: 56x56x256 -> 256 took 54 us packed and
+  // 60-65 us prepared.
+  p.prep = tf == 1 || g.Cw <= 2;
+  return p;
+}
+
+// wprep: prepared weights (prepare_weights_kernel), used instead of the
+// packed w where plan_mfma says they pay, or null.
 hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint32_t* w,
-                    const int32_t* thr, const uint32_t* flip, int32_t* sums, uint32_t* bits,
-                    hipStream_t s) {
+                    const void* wprep, const int32_t* thr, const uint32_t* flip, int32_t* sums,
+                    uint32_t* bits, hipStream_t s) {
+  const Plan p = plan_mfma(g, pool);
+  if (!p.prep) wprep = nullptr;
   Mfma32Args a;
   a.in = in;
-  a.w = w;
+  a.w = wprep ? static_cast<const uint32_t*>(wprep) : w;
   a.thr = thr;
   a.flip = flip;
   a.sums = sums;
@@ -831,84 +988,79 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   a.K = g.KH * g.KW * g.C;
   a.in_bytes = static_cast<int32_t>(static_cast<int64_t>(g.N) * g.H * g.W * g.Cw * 4);
   a.w_bytes = static_cast<int32_t>(static_cast<int64_t>(g.F) * a.fstride * 4);
+  a.corr = nullptr;
+  a.Cp = 0;
+  if (wprep) {
+    a.Cp = prepared_words_per_tap(g.C);
+    a.fstride = g.KH * g.KW * a.Cp;  // entries per filter
+    a.w_bytes = static_cast<int32_t>(static_cast<int64_t>(g.F + 31) / 32 * 32 * a.fstride * 16);
+    a.corr = reinterpret_cast<const int32_t*>(static_cast<const char*>(wprep) + a.w_bytes);
+  }
   a.div_w = make_fastdiv(static_cast<uint32_t>(pool ? g.Wp : g.Wo));
   a.div_h = make_fastdiv(static_cast<uint32_t>(pool ? g.Hp : g.Ho));
-  const bnn_options& opt = options();
-  a.xcd_map = opt.xcd_order != 0 ? 1 : 0;
-  // Words per lane, row and iteration: 8-word chunks (128-bit loads) where
-  // the channels allow, which halves the vector-memory instructions per MFMA
-  // (the texture-address unit is the busiest unit of the small grids), but
-  // not when that leaves fewer than 8 iterations to split.
-  const int64_t groups = (a.items + 63) / 64;
-  const int64_t ftiles = (g.F + 31) / 32;
-  // C not a multiple of 64: the loop walks Cc >= Cw words per tap, whole
-  // chunks of 2 VW words, with the words past Cw zeroed and every word
-  // loaded on its own (bconv_mfma32_kernel, TAIL).  VW is the largest of 4,
-  // 2, 1 whose padding stays within 1/8 of the row.
-  const bool tail = g.C % 64 != 0;
-  int vw = g.Cw % 8 == 0 ? 4 : g.Cw % 4 == 0 ? 2 : 1;
-  // Windows of at most 4 eight-word chunks (K <= 1024 bits, e.g. FC layers
-  // of 1024 inputs) on grids too small to fill the chip keep 8-word chunks
-  // and no K split: there the split's LDS reduction costs more than it
-  // hides (1024 -> 1024 and 1024 -> 10 at 64 rows: 4.15 and 4.30 us against
-  // 4.42 and 4.57 us with 2-word chunks split 4 ways).
-  const int chunks8 = g.KH * g.KW * (g.Cw / 8);
-  const bool short8 = !tail && vw == 4 && chunks8 <= 4 && groups * ftiles < 1024;
-  if (vw == 4 && chunks8 < 8 && !short8) vw = 2;
-  // Option lds_weights = 1 asks for the LDS-weights kernel wherever no K
-  // split is used; it takes chunks of at most 2 words.
-  if (opt.lds_weights == 1 && vw == 4) vw = 2;
-  if (tail) {
-    vw = 1;
-    for (int t = 4; t >= 2 && vw == 1; t /= 2)
-      if (((g.Cw + 2 * t - 1) / (2 * t) * (2 * t) - g.Cw) * 8 <= g.Cw) vw = t;
-  }
+  a.xcd_map = options().xcd_order != 0 ? 1 : 0;
+  const int vw = p.vw;
   a.Cc = (g.Cw + 2 * vw - 1) / (2 * vw) * (2 * vw);
   a.tmask_c = tail_mask(g.C);
-  a.pad_bits = g.KH * g.KW * (32 * a.Cc - g.C);
-  const int iters = g.KH * g.KW * (a.Cc / (2 * vw));
+  // (prepared weights hold 0.0 at the padding positions: no correction)
+  a.pad_bits = wprep ? 0 : g.KH * g.KW * (32 * a.Cc - g.C);
   a.div_c = make_fastdiv(static_cast<uint32_t>(a.Cc / (2 * vw)));
-
-  // Tile shape and K split: 64-filter wave tiles down to ~1 wave per SIMD
-  // (1024 waves), then 32-filter tiles with a K split over up to 4 waves
-  // until there are ~1 (8-word chunks) or ~2 (smaller chunks) waves per
-  // SIMD, keeping at least 2 iterations per wave.  Splitting 8 ways never
-  // beat 4 (the LDS reduction then costs more than it hides).  With 2-word
-  // chunks, grids of >= 4096 64-filter tiles stage the weights through LDS
-  // (5-20 % faster there, slower on smaller grids); 8-word chunks without
-  // staging were as fast or faster wherever the channels allow them.  All
-  // measured on every layer shape of the networks here.
-  int tf = 2, ks = 1;
-  if (g.F % 64 != 0 || groups * (g.F / 64) < 1024) {
-    tf = 1;
-    const int64_t target = vw == 4 ? 1024 : 2048;
-    while (!short8 && ks < 4 && groups * ftiles * ks < target && iters >= 4 * ks) ks *= 2;
-  }
-  bool lds = opt.lds_weights == -1 ? vw <= 2 && tf == 2 && groups * (g.F / 64) >= 4096
-                                    : opt.lds_weights == 1;
-  if (ks > 1 || vw == 4) lds = false;
-  if (tail) {
-    tf = 1;
-    lds = false;
-    if (ks > 4) ks = 4;
-  }
-  // Thresholds staged after the main loop on grids of at most 2 waves per
-  // SIMD (2048 waves) with 32-filter tiles, at kernel start otherwise, where
-  // the accumulators can then start from them (16x16x128 -> 256 and
-  // 16x16x256 -> 256 pool at batch 64: 5.98 / 7.50 us early against
-  // 6.25 / 7.94 us late; 8x8x256 -> 512 with 32-filter tiles: 6.11 us late,
-  // 6.22 us early).  Option late_thresholds overrides.
-  const int64_t waves = (groups + 3) / 4 * 4 * ((g.F + 32 * tf - 1) / (32 * tf));
-  const bool late = tail || (opt.late_thresholds == -1 ? waves <= 2048 && tf == 1
-                                                       : opt.late_thresholds == 1);
   if (vw == 4)
-    return pool ? launch32<4, true>(a, tf, ks, false, late, s)
-                : launch32<4, false>(a, tf, ks, false, late, s);
+    return pool ? launch_vw<4, true>(a, p.tf, p.ks, false, p.late, p.tail, s)
+                : launch_vw<4, false>(a, p.tf, p.ks, false, p.late, p.tail, s);
   if (vw == 2)
-    return pool ? launch32<2, true>(a, tf, ks, lds, late, s)
-                : launch32<2, false>(a, tf, ks, lds, late, s);
-  return pool ? launch32<1, true>(a, tf, ks, lds, late, s)
-              : launch32<1, false>(a, tf, ks, lds, late, s);
+    return pool ? launch_vw<2, true>(a, p.tf, p.ks, p.lds, p.late, p.tail, s)
+                : launch_vw<2, false>(a, p.tf, p.ks, p.lds, p.late, p.tail, s);
+  return pool ? launch_vw<1, true>(a, p.tf, p.ks, p.lds, p.late, p.tail, s)
+              : launch_vw<1, false>(a, p.tf, p.ks, p.lds, p.late, p.tail, s);
+}
+
+// Prepared weights: entry (f, tap, j), j < Cp, holds the four fp4 registers
+// of weight word j of filter f at that tap in the encoding act_operand pairs
+// with.  Register r, nibble n carries bit 4n + r of the word: for r = 3 it is
+// -1.0 (bit 1) or +1.0 (bit 0), for r = 0, 1, 2 it is +m or -m (bit 1 / bit
+// 0) with m = 4, 2, 1; positions past C (tail bits, words past Cw) and
+// filters past F hold 0.0.  The entries are stored [F / 32][tap][j][f % 32],
+// the order in which a wave's 32-filter tile reads them.  corr[f] = B_f, the
+// sum of s(w) over the valid positions of registers 0-2, is how much too high
+// the matrix cores' window sums come out.  One block per filter (F rounded up
+// to 32); done once per network, so written for clarity.
+__global__ __launch_bounds__(256) void prepare_weights_kernel(const uint32_t* w, int32_t F,
+                                                              int32_t taps, int32_t Cw,
+                                                              int32_t Cp, int32_t C, v4i* out,
+                                                              int32_t* corr) {
+  const int f = blockIdx.x;
+  __shared__ int32_t total;
+  if (threadIdx.x == 0) total = 0;
+  __syncthreads();
+  int32_t cnt = 0;
+  for (int e = threadIdx.x; e < taps * Cp; e += blockDim.x) {
+    const int t = e / Cp, j = e - t * Cp;
+    const bool fv = f < F;
+    const uint32_t word = fv && j < Cw ? w[(static_cast<size_t>(f) * taps + t) * Cw + j] : 0u;
+    const uint32_t valid =
+        !fv ? 0u : j < Cw - 1 ? ~0u : (j == Cw - 1 ? tail_mask(C) : 0u);
+    uint32_t reg[4] = {0u, 0u, 0u, 0u};
+    for (int b = 0; b < 32; ++b) {
+      if (!((valid >> b) & 1u)) continue;
+      const int r = b & 3, n = b >> 2;
+      const bool one = (word >> b) & 1u;
+      uint32_t nib;
+      if (r == 3) {
+        nib = one ? 0xAu : 0x2u;
+      } else {
+        nib = (r == 0 ? 0x6u : r == 1 ? 0x4u : 0x2u) | (one ? 0u : 0x8u);
+        cnt += one ? 1 : -1;
+      }
+      reg[r] |= nib << (4 * n);
+    }
+    out[((static_cast<size_t>(f / 32) * taps + t) * Cp + j) * 32 + f % 32] =
+        v4i{static_cast<int>(reg[0]), static_cast<int>(reg[1]), static_cast<int>(reg[2]),
+            static_cast<int>(reg[3])};
+  }
+  atomicAdd(&total, cnt);
+  __syncthreads();
+  if (threadIdx.x == 0 && f < F) corr[f] = total;
 }
 
 }  // namespace
@@ -927,14 +1079,39 @@ bool bconv_mfma_supported(const ConvGeom& g) {
 }
 
 hipError_t launch_bconv_mfma(const ConvGeom& g, const uint32_t* in, const uint32_t* w,
-                             const int32_t* thr, const uint32_t* flip, int32_t* sums,
-                             uint32_t* bits, hipStream_t s) {
+                             const void* wprep, const int32_t* thr, const uint32_t* flip,
+                             int32_t* sums, uint32_t* bits, hipStream_t s) {
   if (g.pool == 2 && sums && ((g.Ho & 1) || (g.Wo & 1))) {
-    hipError_t e = run_mfma(g, false, in, w, thr, flip, sums, nullptr, s);
+    hipError_t e = run_mfma(g, false, in, w, wprep, thr, flip, sums, nullptr, s);
     if (e != hipSuccess || !bits) return e;
-    return run_mfma(g, true, in, w, thr, flip, nullptr, bits, s);
+    return run_mfma(g, true, in, w, wprep, thr, flip, nullptr, bits, s);
   }
-  return run_mfma(g, g.pool == 2, in, w, thr, flip, sums, bits, s);
+  return run_mfma(g, g.pool == 2, in, w, wprep, thr, flip, sums, bits, s);
+}
+
+int32_t prepared_words_per_tap(int32_t C) {
+  return static_cast<int32_t>((words_of(C) + 7) / 8 * 8);
+}
+
+int64_t prepared_weights_bytes(int32_t F, int32_t KH, int32_t KW, int32_t C) {
+  return (int64_t{F} + 31) / 32 * 32 * KH * KW * prepared_words_per_tap(C) * 16 +
+         (int64_t{F} * 4 + 15) / 16 * 16;
+}
+
+bool bconv_mfma_prep_supported(const ConvGeom& g) {
+  return bconv_mfma_supported(g) &&
+         prepared_weights_bytes(g.F, g.KH, g.KW, g.C) < (int64_t{1} << 31);
+}
+
+hipError_t launch_prepare_weights(int32_t F, int32_t KH, int32_t KW, int32_t C,
+                                  const uint32_t* w, void* out, hipStream_t s) {
+  const int32_t Cp = prepared_words_per_tap(C);
+  const int32_t Fp = (F + 31) / 32 * 32;
+  const int64_t entries = int64_t{Fp} * KH * KW * Cp;
+  prepare_weights_kernel<<<dim3(static_cast<unsigned>(Fp)), dim3(256), 0, s>>>(
+      w, F, KH * KW, static_cast<int32_t>(words_of(C)), Cp, C, static_cast<v4i*>(out),
+      reinterpret_cast<int32_t*>(static_cast<char*>(out) + entries * 16));
+  return hipGetLastError();
 }
 
 }  // namespace bnn

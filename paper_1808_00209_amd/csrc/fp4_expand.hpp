@@ -61,6 +61,27 @@ __device__ __forceinline__ void expand_pair(uint32_t w0, uint32_t w1, uint32_t s
   x1[4] = x1[5] = x1[6] = x1[7] = 0;
 }
 
+// An activation word as the B operand against prepared weights (the
+// operand form of prepare_weights_kernel).  Register r < 3 keeps bits 4n + r
+// of the word where they are, so nibble n is the E2M1 value 0 (bit 0) or
+// 2^(r-1) (bit 1: 0.5, 1.0, 2.0), one v_and_b32 each; register 3 is the +-1
+// form of expand_fp4 (bit 1 -> -1.0).  The prepared weights hold +-4, +-2,
+// +-1 in registers 0, 1, 2 (bit 1 -> +) and -1/+1 in register 3 (bit 1 ->
+// -1), so with a the activation bit and s(b) = 2b - 1 every product is
+// 2 a s(w) = s(a) s(w) + s(w) in registers 0-2 and s(a) s(w) in register 3:
+// a window's sum comes out S + B_f, B_f = sum of s(w) over the positions of
+// registers 0-2, a constant of the filter that the epilogue takes off.
+// Four VALU instructions per word, against 5.5 for expand_pair.
+__device__ __forceinline__ v8i act_operand(uint32_t x, uint32_t smask, uint32_t vfill) {
+  v8i r;
+  r[0] = static_cast<int>(x & 0x11111111u);
+  r[1] = static_cast<int>(x & 0x22222222u);
+  r[2] = static_cast<int>(x & 0x44444444u);
+  r[3] = static_cast<int>(and_or(x, smask, vfill));
+  r[4] = r[5] = r[6] = r[7] = 0;
+  return r;
+}
+
 // Expands VW consecutive words (VW = 1, 2 or 4) into VW operands.
 template <int VW>
 __device__ __forceinline__ void expand_words(const uint32_t (&w)[VW], uint32_t smask,

@@ -49,11 +49,23 @@ hipError_t launch_bconv1x1(const ConvGeom& g, const uint32_t* in, const uint32_t
 // Binary conv on the matrix cores (fp4 MFMA).  Supported when
 // bconv_mfma_supported(g): C >= 64 (padded to whole 64-bit chunks), at most
 // 32 taps.
+// wprep: the weights prepared by launch_prepare_weights (used instead of w),
+// or null.
 bool bconv_mfma_supported(const ConvGeom& g);
 hipError_t launch_bconv_mfma(const ConvGeom& g, const uint32_t* in,
-                             const uint32_t* w, const int32_t* thr,
-                             const uint32_t* flip, int32_t* sums,
-                             uint32_t* bits, hipStream_t s);
+                             const uint32_t* w, const void* wprep,
+                             const int32_t* thr, const uint32_t* flip,
+                             int32_t* sums, uint32_t* bits, hipStream_t s);
+
+// Prepared ("operand form") conv weights for the matrix-core kernel: 16-byte
+// entries [ceil(F / 32)][KH][KW][Cp][32] (Cp = ceil(Cw / 8) * 8) holding each
+// weight word's four fp4 registers, then F int32 per-filter offsets.  Supported where
+// bconv_mfma_supported holds and the buffer stays under 2 GiB.
+int32_t prepared_words_per_tap(int32_t C);
+int64_t prepared_weights_bytes(int32_t F, int32_t KH, int32_t KW, int32_t C);
+bool bconv_mfma_prep_supported(const ConvGeom& g);
+hipError_t launch_prepare_weights(int32_t F, int32_t KH, int32_t KW, int32_t C,
+                                  const uint32_t* w, void* out, hipStream_t s);
 
 // Input binarization (bnn_input_mode of bnn.h) of an fp32 image into one
 // code word per pixel, and the binary conv over an image binarized on the

@@ -31,8 +31,10 @@ def pack_flips(flip, device="cuda"):
     return pack_pm1(pm, device)
 
 
-def upload_layer(L, device="cuda"):
-    """A host layer dict (see synth) -> device tensors + C-struct fields."""
+def upload_layer(L, device="cuda", prepare=True):
+    """A host layer dict (see synth) -> device tensors + C-struct fields.
+    Binary conv layers also get their weights in the prepared operand form
+    (bnn_prepare_weights) unless ``prepare`` is False."""
     kind = L["kind"]
     d = {}
     if kind in ("input_threshold", "input_gray", "input_lbp"):
@@ -50,6 +52,8 @@ def upload_layer(L, device="cuda"):
         d.update(kind=bnn.LAYER_BFC if kind == "bfc" else bnn.LAYER_BFC_LOGITS,
                  K=L["K"], N=L["N"])
     d["w"] = pack_pm1(L["w"], device)
+    if prepare and kind == "bconv":
+        d["wprep"] = bnn.bnn_prepare_weights(d["w"], L["F"], L["KH"], L["KW"], L["C"])
     if L.get("thr") is not None:
         d["thr"] = to_device(L["thr"], torch.int32, device)
     if L.get("flip") is not None:
@@ -57,8 +61,8 @@ def upload_layer(L, device="cuda"):
     return d
 
 
-def upload_network(layers, H, W, C, device="cuda"):
-    return bnn.Network([upload_layer(L, device) for L in layers], H, W, C)
+def upload_network(layers, H, W, C, device="cuda", prepare=True):
+    return bnn.Network([upload_layer(L, device, prepare) for L in layers], H, W, C)
 
 
 def words_u32(t) -> np.ndarray:

@@ -22,18 +22,26 @@ pytestmark = pytest.mark.gpu
 # launch instead of runs of small FC layers in the chained kernel; "nofuse":
 # the real-valued first layer and the binary conv after it as two launches
 # instead of the fused first-layer kernel.
-@pytest.fixture(params=["auto", "valu", "lds", "nopatch", "nochain", "nofuse"])
+# "packed": "auto" with packed conv weights only (no prepared operand form,
+# which every other family passes in each binary conv layer).
+_PREPARE = True
+
+
+@pytest.fixture(params=["auto", "valu", "lds", "nopatch", "nochain", "nofuse", "packed"])
 def algo(request):
+    global _PREPARE
     bnn.bnn_set_options(**{"auto": {}, "valu": dict(algo=bnn.ALGO_VALU),
                            "lds": dict(lds_weights=1), "nopatch": dict(fuse_input=0),
-                           "nochain": dict(fc_chain=0),
-                           "nofuse": dict(fuse_first=0)}[request.param])
-    return request.param
+                           "nochain": dict(fc_chain=0), "nofuse": dict(fuse_first=0),
+                           "packed": {}}[request.param])
+    _PREPARE = request.param != "packed"
+    yield request.param
+    _PREPARE = True
 
 
 def _gpu_logits(layers, x):
     N, H, W, C = x.shape
-    net = upload_network(layers, H, W, C)
+    net = upload_network(layers, H, W, C, prepare=_PREPARE)
     out = bnn.bnn_forward(net, to_device(x))
     torch.cuda.synchronize()
     return out.cpu().numpy()

@@ -24,10 +24,13 @@ from paper_1808_00209_amd.device import pack_pm1, to_device, upload_layer, words
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(params=["auto", "valu"])
+@pytest.fixture(params=["auto", "prep", "valu"])
 def algo(request):
-    """"auto": the default kernels (the matrix cores); "valu": the vector-ALU
-    XOR-popcount kernels (the ablation the benchmark also times)."""
+    """"auto": the default kernels (the matrix cores) with packed weights;
+    "prep": the same with the conv weights in the prepared operand form
+    (bnn_bconv2d_prepared, as bnn_forward runs the networks and bench.py
+    times the layers); "valu": the vector-ALU XOR-popcount kernels (the
+    ablation the benchmark also times)."""
     bnn.bnn_set_options(**({"algo": bnn.ALGO_VALU} if request.param == "valu" else {}))
     return request.param
 
@@ -40,15 +43,23 @@ def _cfg5_oracle(name):
     return S, oracle.pack_eq2(oracle.threshold(S, L["thr"], L["flip"]))
 
 
-def _cfg5_gpu(name, want_sums):
+def _conv(desc, src, d, algo, want_sums):
+    """One conv layer through bnn_bconv2d_prepared (family "prep") or
+    bnn_bconv2d."""
+    if algo == "prep":
+        return bnn.bnn_bconv2d_prepared(desc, src, d["w"], d["wprep"], d["thr"], d.get("flip"),
+                                        want_sums=want_sums)
+    return bnn.bnn_bconv2d(desc, src, d["w"], d["thr"], d.get("flip"), want_sums=want_sums)
+
+
+def _cfg5_gpu(name, want_sums, algo):
     """The call bench.py times: packed input and layer on the device, one
-    bnn_bconv2d, bits only unless sums are asked for."""
+    conv call, bits only unless sums are asked for."""
     x, L = synth.cfg5_case(name)
     N, H, W, C = x.shape
     desc = bnn.conv_desc(N, H, W, C, L["F"], L["KH"], L["KW"], 1, L["pad"], L.get("pool", 0))
     dl = upload_layer(L)
-    sums, bits = bnn.bnn_bconv2d(desc, pack_pm1(x), dl["w"], dl["thr"], dl.get("flip"),
-                                 want_sums=want_sums)
+    sums, bits = _conv(desc, pack_pm1(x), dl, algo, want_sums)
     torch.cuda.synchronize()
     return (sums.cpu().numpy() if want_sums else None), words_u32(bits)
 
@@ -56,7 +67,7 @@ def _cfg5_gpu(name, want_sums):
 @pytest.mark.parametrize("name", ["A", "B", "C"])
 def test_cfg5_bits_only_every_word(name, algo):
     print("cfg5 %s bits only, %s" % (name, algo), flush=True)
-    _, bits = _cfg5_gpu(name, False)
+    _, bits = _cfg5_gpu(name, False, algo)
     _, B = _cfg5_oracle(name)
     assert bits.shape == B.shape
     assert np.array_equal(bits, B)
@@ -65,7 +76,7 @@ def test_cfg5_bits_only_every_word(name, algo):
 @pytest.mark.parametrize("name", ["A", "B", "C"])
 def test_cfg5_sums_and_bits_every_value(name, algo):
     print("cfg5 %s sums + bits, %s" % (name, algo), flush=True)
-    sums, bits = _cfg5_gpu(name, True)
+    sums, bits = _cfg5_gpu(name, True, algo)
     S, B = _cfg5_oracle(name)
     assert np.array_equal(sums, S)
     assert np.array_equal(bits, B)
@@ -117,13 +128,11 @@ def test_every_layer_bits_at_full_batch(cfg, batch, algo):
                 _, bits = bnn.bnn_fconv2d_binw(desc, xd, d["w"], d["thr"], d.get("flip"),
                                                want_sums=False)
             else:
-                src = pack_pm1(outs[li - 1])
-                _, bits = bnn.bnn_bconv2d(desc, src, d["w"], d["thr"], d.get("flip"),
-                                          want_sums=False)
+                _, bits = _conv(desc, pack_pm1(outs[li - 1]), d, algo, False)
             torch.cuda.synchronize()
             assert np.array_equal(words_u32(bits), _packed(outs[li])), "layer %d" % li
             # the fused kernels bnn_forward runs for the first two layers
-            if li == 1 and layers[0]["kind"] == "fconv" and algo == "auto":
+            if li == 1 and layers[0]["kind"] == "fconv" and algo != "valu":
                 d0 = bnn.conv_desc(N, H, W, C, layers[0]["F"], 3, 3, 1, layers[0]["pad"], 0)
                 fb = bnn.bnn_fconv_bconv2d(d0, desc, xd, dev[0]["w"], dev[0]["thr"],
                                            dev[0].get("flip"), d["w"], d["thr"], d.get("flip"))

