@@ -316,3 +316,37 @@ def test_library_sources_read_no_environment():
     for f in os.listdir(csrc):
         src = open(os.path.join(csrc, f)).read()
         assert "getenv" not in src and "environ" not in src, f
+
+
+@needs_lib
+def test_prepared_weights_size_and_argument_errors():
+    """bnn_prepared_weights_size: 16-byte entries [ceil(F/32)*32][KH][KW][Cp]
+    with Cp = ceil(ceil(C/32) / 8) * 8, then F int32 offsets rounded up to 16
+    bytes; shape, NULL and alignment errors of the three calls come before
+    any launch."""
+    lib = bnn.load()
+    size = ctypes.c_size_t()
+    for F, KH, KW, C in [(64, 3, 3, 64), (40, 3, 3, 96), (1024, 1, 1, 4100), (1, 1, 1, 1)]:
+        assert lib.bnn_prepared_weights_size(F, KH, KW, C, ctypes.byref(size)) == 0
+        Cp = ((C + 31) // 32 + 7) // 8 * 8
+        assert size.value == (F + 31) // 32 * 32 * KH * KW * Cp * 16 + (4 * F + 15) // 16 * 16
+    assert lib.bnn_prepared_weights_size(0, 3, 3, 64, ctypes.byref(size)) == 2
+    assert lib.bnn_prepared_weights_size(64, 3, 3, 64, None) == 1
+    # beyond 2 GiB
+    assert lib.bnn_prepared_weights_size(1 << 20, 3, 3, 4096, ctypes.byref(size)) == 2
+    assert "2 GiB" in bnn.last_error()
+    assert lib.bnn_prepare_weights(64, 3, 3, 64, None, A, None) == 1
+    assert lib.bnn_prepare_weights(64, 3, 3, 64, A, A + 4, None) == 3
+    assert lib.bnn_prepare_weights(64, 3, 0, 64, A, A, None) == 2
+    d = _conv()
+    assert lib.bnn_bconv2d_prepared(ctypes.byref(d), A, A, None, A, None, A, A, None) == 1
+    assert "wprep" in bnn.last_error()
+    assert lib.bnn_bconv2d_prepared(ctypes.byref(d), A, A, A + 8, A, None, A, A, None) == 3
+    assert lib.bnn_bconv2d_prepared(ctypes.byref(_conv(stride=2)), A, A, A, A, None, A, A,
+                                    None) == 4
+    # bnn_forward checks a conv layer's wprep alignment like its w
+    good = [dict(kind=1, C=3),
+            dict(kind=3, C=3, F=64, KH=3, KW=3, stride=1, pad=1, pool=2, w=A, thr=A, wprep=A + 4),
+            dict(kind=5, K=4 * 4 * 64, N=4, w=A)]
+    assert lib.bnn_forward_workspace_size(_layers(good), 3, 8, 8, 8, 3, ctypes.byref(size)) == 3
+    assert "wprep" in bnn.last_error()
