@@ -356,7 +356,8 @@ def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
         x = torch.randn((batch, g["H"], g["W"], g["C"]), device="cuda", generator=gen)
         l0, l1 = dev_layer
         fn = lambda: bnn.bnn_fconv_bconv2d(d0, d1, x, l0["w"], l0["thr"], l0.get("flip"),
-                                           l1["w"], l1["thr"], l1.get("flip"), out_bits=ob)
+                                           l1["w"], l1["thr"], l1.get("flip"), out_bits=ob,
+                                           w1prep=l1.get("wprep"))
     elif kind in ("fconv", "bconv"):
         desc = bnn.conv_desc(batch, g["H"], g["W"], g["C"], g["F"], g["KH"], g["KW"], 1,
                              g["pad"], g["pool"])

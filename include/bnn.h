@@ -103,7 +103,10 @@ typedef struct bnn_options {
   int32_t conv1x1;         /* the short-window 1x1 kernel where it applies   */
                            /* (1, default) or the general one (0)            */
   int32_t xcd_order;       /* matrix-core conv workgroups in the XCD order   */
-                           /* (1, default) or on a 2-D grid (0)              */
+                           /* (1, default), on a 2-D grid (0), or in the XCD */
+                           /* order with the filter tiles split over XCD     */
+                           /* groups when that cuts the bytes the L2s move   */
+                           /* (2)                                            */
   int32_t gemv_max_rows;   /* FC layers of at most this many rows use the    */
                            /* vector-ALU GEMV; 0..16, default 2              */
   int32_t lds_weights;     /* matrix-core conv weights staged through LDS:   */
@@ -309,17 +312,19 @@ bnn_status bnn_bconv2d_input(const bnn_conv_desc* d, int32_t mode,
  *             thresholds [F0] and flip words [F0 / 32] (flip0 may be NULL).
  *   w1, thr1, flip1   the second layer's [F1][3][3][F0 / 32], [F1],
  *             [F1 / 32] (flip1 may be NULL).
+ *   w1prep    bnn_prepare_weights of w1 (then the second layer reads its
+ *             weights in operand form), or NULL.
  *   out_bits  [N][Hp][Wp][F1 / 32] u32, the second layer's bits.
- * Shapes outside the above give BNN_ERR_UNSUPPORTED.  x, w0, w1 and out_bits
- * 16-byte aligned.  Errors: BNN_ERR_NULL, BNN_ERR_SHAPE, BNN_ERR_ALIGN,
+ * Shapes outside the above give BNN_ERR_UNSUPPORTED.  x, w0, w1, w1prep and
+ * out_bits 16-byte aligned.  Errors: BNN_ERR_NULL, BNN_ERR_SHAPE, BNN_ERR_ALIGN,
  * BNN_ERR_UNSUPPORTED, BNN_ERR_HIP.
  */
 bnn_status bnn_fconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc* d1,
                              const float* x, const uint32_t* w0,
                              const int32_t* thr0, const uint32_t* flip0,
-                             const uint32_t* w1, const int32_t* thr1,
-                             const uint32_t* flip1, uint32_t* out_bits,
-                             hipStream_t stream);
+                             const uint32_t* w1, const void* w1prep,
+                             const int32_t* thr1, const uint32_t* flip1,
+                             uint32_t* out_bits, hipStream_t stream);
 
 /*
  * Binary fully-connected layer / GEMM (Sec. III-B, Eq. 4):

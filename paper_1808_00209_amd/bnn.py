@@ -106,7 +106,7 @@ def load(path: str = LIB_PATH):
     lib.bnn_binarize_input.argtypes = [i32, P, P, i32, i32, i32, i32, P, P]
     lib.bnn_bconv2d_input.argtypes = [ctypes.POINTER(ConvDesc), i32, P, P, P, P, P, P, P, P]
     lib.bnn_fconv_bconv2d.argtypes = [ctypes.POINTER(ConvDesc), ctypes.POINTER(ConvDesc),
-                                      P, P, P, P, P, P, P, P, P]
+                                      P, P, P, P, P, P, P, P, P, P]
     lib.bnn_forward_workspace_size.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32,
                                                ctypes.POINTER(ctypes.c_size_t)]
     lib.bnn_forward.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32, P, P,
@@ -338,11 +338,11 @@ def bnn_bconv2d_input(desc: ConvDesc, mode, x, offset, w, thr=None, flip=None, w
 
 
 def bnn_fconv_bconv2d(desc0: ConvDesc, desc1: ConvDesc, x, w0, thr0, flip0, w1, thr1,
-                      flip1=None, out_bits=None, stream=None):
+                      flip1=None, out_bits=None, stream=None, w1prep=None):
     """The real-valued first layer and a binary 3x3 conv over its bits in one
     launch (the first two layers of Table I's BCNN): returns the second
     layer's packed bits [N, Hp, Wp, F1/32], the same as bnn_fconv2d_binw
-    followed by bnn_bconv2d."""
+    followed by bnn_bconv2d.  w1prep: bnn_prepare_weights of w1, or None."""
     lib = load()
     _, _, Hp, Wp = bnn_conv_output_dims(desc1)
     _dev(x, torch.float32, "x")
@@ -355,9 +355,10 @@ def bnn_fconv_bconv2d(desc0: ConvDesc, desc1: ConvDesc, x, w0, thr0, flip0, w1, 
     if out_bits is None:
         out_bits = torch.empty((desc1.N, Hp, Wp, words(desc1.F)), dtype=torch.int32,
                                device=x.device)
+    _dev(w1prep, torch.uint8, "w1prep")
     _check(lib.bnn_fconv_bconv2d(ctypes.byref(desc0), ctypes.byref(desc1), _ptr(x), _ptr(w0),
-                                 _ptr(thr0), _ptr(flip0), _ptr(w1), _ptr(thr1), _ptr(flip1),
-                                 _ptr(out_bits), _stream(stream)))
+                                 _ptr(thr0), _ptr(flip0), _ptr(w1), _ptr(w1prep), _ptr(thr1),
+                                 _ptr(flip1), _ptr(out_bits), _stream(stream)))
     return out_bits
 
 

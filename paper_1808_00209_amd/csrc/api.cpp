@@ -211,7 +211,8 @@ bnn_status bnn_set_options(const bnn_options* o) {
   auto flag = [](int32_t v) { return v == 0 || v == 1; };
   auto tri = [](int32_t v) { return v == -1 || v == 0 || v == 1; };
   if ((o->algo != BNN_ALGO_AUTO && o->algo != BNN_ALGO_VALU) || !flag(o->fuse_input) ||
-      !flag(o->fuse_first) || !flag(o->fc_chain) || !flag(o->conv1x1) || !flag(o->xcd_order) ||
+      !flag(o->fuse_first) || !flag(o->fc_chain) || !flag(o->conv1x1) ||
+      o->xcd_order < 0 || o->xcd_order > 2 ||
       o->gemv_max_rows < 0 || o->gemv_max_rows > 16 || !tri(o->lds_weights) ||
       !tri(o->late_thresholds))
     return fail(BNN_ERR_SHAPE,
@@ -399,8 +400,8 @@ bnn_status bnn_bconv2d_input(const bnn_conv_desc* d, int32_t mode, const float* 
 
 bnn_status bnn_fconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc* d1, const float* x,
                              const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
-                             const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
-                             uint32_t* out_bits, hipStream_t stream) {
+                             const uint32_t* w1, const void* w1prep, const int32_t* thr1,
+                             const uint32_t* flip1, uint32_t* out_bits, hipStream_t stream) {
   try {
     bnn::ConvGeom g0, g1;
     bnn_status st = conv_geom(d0, &g0);
@@ -419,10 +420,11 @@ bnn_status bnn_fconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc* d1, c
     if (!w1) return fail(BNN_ERR_NULL, "fconv_bconv2d: w1 is NULL");
     if (!thr0) return fail(BNN_ERR_NULL, "fconv_bconv2d: thr0 is NULL");
     if (!out_bits) return fail(BNN_ERR_NULL, "fconv_bconv2d: out_bits is NULL");
-    if (!aligned16(w1)) return fail(BNN_ERR_ALIGN, "fconv_bconv2d: w1 must be 16-byte aligned");
+    if (!aligned16(w1) || !aligned16(w1prep))
+      return fail(BNN_ERR_ALIGN, "fconv_bconv2d: w1 and w1prep must be 16-byte aligned");
     st = check_outputs(x, w0, thr1, nullptr, out_bits);
     if (st != BNN_OK) return st;
-    return hip_status(bnn::launch_fconv_bconv(g0, g1, x, w0, thr0, flip0, w1, thr1, flip1,
+    return hip_status(bnn::launch_fconv_bconv(g0, g1, x, w0, thr0, flip0, w1, w1prep, thr1, flip1,
                                               out_bits, stream),
                       "fconv_bconv2d launch");
   } catch (...) {
@@ -674,7 +676,7 @@ bnn_status run_chain(const bnn_layer* layers, int32_t n_layers, int32_t batch, i
             e = bnn::launch_fconv_binw(g, input, l.w, l.thr, l.flip, nullptr, dst, stream);
         } else if (li == 1 && fuse_first)
           e = bnn::launch_fconv_bconv(g_first, g, input, layers[0].w, layers[0].thr,
-                                      layers[0].flip, l.w, l.thr, l.flip, dst, stream);
+                                      layers[0].flip, l.w, l.wprep, l.thr, l.flip, dst, stream);
         else if (li == 1 && fuse_input)
           e = bnn::launch_bconv_patch(g, mode, input, layers[0].offset, l.w, l.thr, l.flip,
                                       nullptr, dst, stream);

@@ -101,8 +101,10 @@ struct Mfma32Args {
   int32_t in_bytes;  // raw-buffer ranges
   int32_t w_bytes;
   FastDiv div_w, div_h;  // Wo, Ho (or Wp, Hp when pooling)
-  int32_t xcd_map;   // 1: one-dimensional grid in the XCD order of block_tile
-  FastDiv div_f;     // filter tiles along the filters
+  int32_t xcd_map;   // 1: one-dimensional grid in the XCD order of block_tile;
+                     // 2: the same with the filter tiles split over XCD groups
+  FastDiv div_f;     // filter tiles per XCD group (all of them with xcd_fs = 0)
+  int32_t xcd_fs;    // log2 of the XCD groups the filter tiles are split over
   FastDiv div_c;     // word chunks per tap (Cc / (2 VW))
   int32_t Cc;        // words per tap the loop walks: Cw rounded up to whole chunks
   uint32_t tmask_c;  // valid bits of a pixel's last word (tail_mask(C))
@@ -116,23 +118,28 @@ struct Mfma32Args {
 
 // The workgroup's pixel block and filter tile.  The workgroups of a launch
 // are handed to the 8 XCDs in turn (workgroup b to XCD b mod 8), and each
-// XCD has its own L2.  In the XCD order, the k-th workgroup of XCD x takes
-// filter tile k mod fy of pixel block 8 (k div fy) + x: the fy filter tiles
-// of a pixel block run one after another on one XCD, so its activations are
-// fetched into one L2, and each output row (one piece per filter tile) is
-// complete in that L2 before it is written back.  Otherwise (a 2-D grid,
-// pixel blocks varying fastest) a row's pieces come from workgroups far
-// apart in time on all 8 XCDs and are written back piece by piece.
-// The padding workgroups past the last pixel block run through with every
-// pixel invalid (their loads read the pad word, their stores are skipped):
-// an early return would be a branch on a kernel argument that makes the
-// kernel wait for that argument before it even loads the others.
+// XCD has its own L2.  In the XCD order the XCDs form p = 8 / g pixel groups
+// times g filter groups (g = 2^xcd_fs): XCD x takes the filter tiles
+// t = x mod g (mod g) and the pixel blocks x div g (mod p), and its k-th
+// workgroup takes its filter tile k mod (fy / g) of its pixel block
+// k div (fy / g).  The filter tiles of a pixel block run one after another
+// on one XCD, so its activations are fetched into one L2, and with g = 1
+// each output row (one piece per filter tile) is complete in that L2 before
+// it is written back.  With g > 1 each L2 fetches only 1/g of the weights
+// (tile_grid picks g from the layer's activation and weight bytes).
+// Otherwise (a 2-D grid, pixel blocks varying fastest) a row's pieces come
+// from workgroups far apart in time on all 8 XCDs and are written back piece
+// by piece.  The padding workgroups past the last pixel block run through
+// with every pixel invalid (their loads read the pad word, their stores are
+// skipped): an early return would be a branch on a kernel argument that
+// makes the kernel wait for that argument before it even loads the others.
 __device__ __forceinline__ void block_tile(const Mfma32Args& a, int& pb, int& ft) {
   const uint32_t b = blockIdx.x;
-  const uint32_t k = b >> 3;
+  const uint32_t k = b >> 3, x = b & 7;
   const uint32_t q = fdiv(k, a.div_f);
-  const int ftx = static_cast<int>(k - q * a.div_f.d);
-  const int pbx = static_cast<int>(q * 8 + (b & 7));
+  const uint32_t g1 = (1u << a.xcd_fs) - 1u;
+  const int ftx = static_cast<int>(((k - q * a.div_f.d) << a.xcd_fs) + (x & g1));
+  const int pbx = static_cast<int>((q << (3 - a.xcd_fs)) + (x >> a.xcd_fs));
   pb = a.xcd_map ? pbx : static_cast<int>(blockIdx.x);
   ft = a.xcd_map ? ftx : static_cast<int>(blockIdx.y);
 }
@@ -784,15 +791,39 @@ __global__ __launch_bounds__(256) void bconv_mfma_lds_kernel(Mfma32Args a) {
 }
 
 // Grid of `pblocks` pixel blocks x `fy` filter tiles: one-dimensional in the
-// XCD order of block_tile (pixel blocks padded to a multiple of 8), or 2-D.
-// The XCD order needs at least 8 pixel blocks: with fewer it would leave
-// XCDs idle (all filter tiles of pixel block 0 on XCD 0), while the 2-D grid
-// spreads the filter tiles over the XCDs.
+// XCD order of block_tile, or 2-D.  The XCD order needs at least 8 pixel
+// blocks: with fewer it would leave XCDs idle (all filter tiles of pixel
+// block 0 on XCD 0), while the 2-D grid spreads the filter tiles over the
+// XCDs.  With xcd_map = 2 the filter tiles are split over g = 1, 2, 4 or 8
+// XCD groups (g dividing fy), g chosen to minimise the bytes the 8 L2s move
+// in all, g * (activation bytes) + (8 / g) * (weight bytes) + g * (output
+// bytes): each L2 then fetches 1/g of the weights, but every output row is
+// written back in g pieces from g L2s.  (8x8x512 -> 512 pool at batch 64
+// with prepared weights: 3.3 instead of 9.6 MB fetched, 0.5 instead of
+// 0.06 MB written, 2 % slower; 8x8x256 -> 512: 6 % slower.  So xcd_map = 1,
+// g = 1, is the default.)
 dim3 tile_grid(Mfma32Args& a, unsigned pblocks, unsigned fy) {
-  a.div_f = make_fastdiv(fy);
+  a.xcd_fs = 0;
   if (pblocks < 8) a.xcd_map = 0;
-  if (a.xcd_map) return dim3((pblocks + 7) / 8 * 8 * fy);
-  return dim3(pblocks, fy);
+  if (!a.xcd_map) {
+    a.div_f = make_fastdiv(fy);
+    return dim3(pblocks, fy);
+  }
+  if (a.xcd_map == 2) {
+    const int64_t out = a.sums ? int64_t{a.items} * a.F * 4 : int64_t{a.items} * a.Fw * 4;
+    int64_t best = int64_t{a.in_bytes} + 8 * int64_t{a.w_bytes} + out;
+    for (int fs = 1; fs <= 3; ++fs) {
+      const int64_t g = int64_t{1} << fs;
+      const int64_t t = g * a.in_bytes + (8 / g) * int64_t{a.w_bytes} + g * out;
+      if (fy % g == 0 && t < best) {
+        best = t;
+        a.xcd_fs = fs;
+      }
+    }
+  }
+  const unsigned fyx = fy >> a.xcd_fs, p = 8u >> a.xcd_fs;
+  a.div_f = make_fastdiv(fyx);
+  return dim3((pblocks + p - 1) / p * 8 * fyx);
 }
 
 template <int VW, bool POOL, bool PREP>
@@ -998,7 +1029,7 @@ hipError_t run_mfma(const ConvGeom& g, bool pool, const uint32_t* in, const uint
   }
   a.div_w = make_fastdiv(static_cast<uint32_t>(pool ? g.Wp : g.Wo));
   a.div_h = make_fastdiv(static_cast<uint32_t>(pool ? g.Hp : g.Ho));
-  a.xcd_map = options().xcd_order != 0 ? 1 : 0;
+  a.xcd_map = options().xcd_order;
   const int vw = p.vw;
   a.Cc = (g.Cw + 2 * vw - 1) / (2 * vw) * (2 * vw);
   a.tmask_c = tail_mask(g.C);
@@ -1089,8 +1120,12 @@ hipError_t launch_bconv_mfma(const ConvGeom& g, const uint32_t* in, const uint32
   return run_mfma(g, g.pool == 2, in, w, wprep, thr, flip, sums, bits, s);
 }
 
+// Entries per tap and filter: Cw where C % 64 == 0 (every chunk width the
+// launcher picks then divides Cw), else Cw rounded up to 8 (the loop walks
+// whole chunks of up to 8 words past Cw, whose entries must read 0.0).
 int32_t prepared_words_per_tap(int32_t C) {
-  return static_cast<int32_t>((words_of(C) + 7) / 8 * 8);
+  const int32_t Cw = static_cast<int32_t>(words_of(C));
+  return C % 64 == 0 ? Cw : (Cw + 7) / 8 * 8;
 }
 
 int64_t prepared_weights_bytes(int32_t F, int32_t KH, int32_t KW, int32_t C) {

@@ -58,12 +58,17 @@ struct FbArgs {
   int32_t Hp, Wp;               // stored output (pooled dims when pooling)
   int32_t K1;                   // bits per second-layer window, 9 * F0
   int32_t w1_bytes;
+  const int32_t* corr1;         // prepared w1 (PREP1): per-filter offsets B_f
   int32_t tiles_w, tiles_h;
 };
 
 constexpr uint32_t kRsrcWord3 = 0x00020000;
 
-template <int C0, int F0, int NFH, bool POOL>
+// PREP1: w1 holds the second layer's weights in the prepared operand form
+// (bnn_prepare_weights: 16-byte entries [F1 / 32][9][F0 / 32][32], then the
+// offsets corr1), so the second layer loads its A operands whole, and the
+// first layer stores its bits as act_operand instead of expand_fp4 operands.
+template <int C0, int F0, int NFH, bool POOL, bool PREP1>
 __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
   constexpr int NT = 256 * NFH;        // threads
   constexpr int NW = 4 * NFH;          // waves
@@ -131,6 +136,7 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
   }
   const int32_t thr0v = a.thr0[min(tid, F0 - 1)];
   const int32_t thr1v = a.thr1[min(tid, F1 - 1)];
+  const int32_t corr1v = PREP1 ? a.corr1[min(tid, F1 - 1)] : 0;
   const uint32_t fl0v = a.flip0 ? a.flip0[min(tid, CW1 - 1)] : 0u;
 
   // First-layer A operands: row = filter 16 ft + (l % 16), 8 k values
@@ -163,8 +169,10 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
   if (tid < F0) th0[tid] = thr_ceil_f32(thr0v);
   if (tid < CW1) fl0[tid] = fl0v;
   // Second-layer start values 0.5 - thr (thr clamped to [-K1-1, K1+1], which
-  // keeps every comparison since |S| <= K1).
-  if (tid < F1) th1[tid] = 0.5f - static_cast<float>(min(max(thr1v, -a.K1 - 1), a.K1 + 1));
+  // keeps every comparison since |S| <= K1); with prepared weights the sums
+  // come out B_f too high, so the start value is 0.5 - thr - B_f.
+  if (tid < F1)
+    th1[tid] = 0.5f - static_cast<float>(min(max(thr1v, -a.K1 - 1), a.K1 + 1) + corr1v);
   // Each input value split once into its three bf16 parts.
 #pragma unroll
   for (int i = 0; i < XIT; ++i) {
@@ -264,7 +272,7 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
       // Output bit = (S >= thr) xor flip = sign xor ~flip.
       const uint32_t word = inside ? rows ^ nfl : 0u;
       if (q < CW1 && pv) {
-        const v8i x = expand_fp4(word, smask, vfill);
+        const v8i x = PREP1 ? act_operand(word, smask, vfill) : expand_fp4(word, smask, vfill);
         actx[lr * RSX + lc * PSX + q] = v4i{x[0], x[1], x[2], x[3]};
       }
     }
@@ -299,13 +307,25 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
   }
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint32_t*>(a.w1), 0, a.w1_bytes, kRsrcWord3);
+  using WReg = typename std::conditional<PREP1, v4i, uint32_t>::type;
   uint32_t woff[2];
 #pragma unroll
   for (int tf = 0; tf < 2; ++tf)
-    woff[tf] = static_cast<uint32_t>(((f0 + 32 * tf + c) * 9 * CW1 + h * VW) * 4);
+    woff[tf] = PREP1 ? static_cast<uint32_t>((((f0 / 32 + tf) * 9 * CW1 + h * VW) * 32 + c) * 16)
+                     : static_cast<uint32_t>(((f0 + 32 * tf + c) * 9 * CW1 + h * VW) * 4);
 
-  auto load_w = [&](int it, uint32_t (&ww)[2][VW]) {
+  auto load_w = [&](int it, WReg (&ww)[2][VW]) {
     const int tap = it / NCH, cc = (it - tap * NCH) * 2 * VW;
+    if constexpr (PREP1) {
+      const uint32_t so = static_cast<uint32_t>((tap * CW1 + cc) * 512);
+#pragma unroll
+      for (int tf = 0; tf < 2; ++tf)
+#pragma unroll
+        for (int v = 0; v < VW; ++v)
+          ww[tf][v] = __builtin_bit_cast(
+              v4i, __builtin_amdgcn_raw_buffer_load_b128(rw, woff[tf] + 512 * v, so, 0));
+      return;
+    }
     const uint32_t so = static_cast<uint32_t>((tap * CW1 + cc) * 4);
 #pragma unroll
     for (int tf = 0; tf < 2; ++tf) {
@@ -320,7 +340,7 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
     }
   };
   constexpr int ITERS = 9 * NCH;
-  uint32_t wr[2][2][VW];
+  WReg wr[2][2][VW];
   load_w(0, wr[0]);
 #pragma unroll
   for (int it = 0; it < ITERS; ++it) {
@@ -338,7 +358,16 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
         B[tp][v] = v8i{t[0], t[1], t[2], t[3], 0, 0, 0, 0};
       }
 #pragma unroll
-    for (int tf = 0; tf < 2; ++tf) expand_words<VW>(wr[cur][tf], smask, vfill, A[tf]);
+    for (int tf = 0; tf < 2; ++tf) {
+      if constexpr (PREP1) {
+#pragma unroll
+        for (int v = 0; v < VW; ++v)
+          A[tf][v] = v8i{wr[cur][tf][v][0], wr[cur][tf][v][1], wr[cur][tf][v][2],
+                         wr[cur][tf][v][3], 0, 0, 0, 0};
+      } else {
+        expand_words<VW>(wr[cur][tf], smask, vfill, A[tf]);
+      }
+    }
 #pragma unroll
     for (int v = 0; v < VW; ++v)
 #pragma unroll
@@ -385,26 +414,29 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
   }
 }
 
-template <int C0, int F0>
+template <int C0, int F0, bool PREP1>
 hipError_t launch_c0f0(const FbArgs& a, int f1, bool pool, unsigned blocks, hipStream_t s) {
   if (f1 == 128) {
     if (pool)
-      fconv_bconv_kernel<C0, F0, 2, true><<<blocks, 512, 0, s>>>(a);
+      fconv_bconv_kernel<C0, F0, 2, true, PREP1><<<blocks, 512, 0, s>>>(a);
     else
-      fconv_bconv_kernel<C0, F0, 2, false><<<blocks, 512, 0, s>>>(a);
+      fconv_bconv_kernel<C0, F0, 2, false, PREP1><<<blocks, 512, 0, s>>>(a);
   } else {
     if (pool)
-      fconv_bconv_kernel<C0, F0, 1, true><<<blocks, 256, 0, s>>>(a);
+      fconv_bconv_kernel<C0, F0, 1, true, PREP1><<<blocks, 256, 0, s>>>(a);
     else
-      fconv_bconv_kernel<C0, F0, 1, false><<<blocks, 256, 0, s>>>(a);
+      fconv_bconv_kernel<C0, F0, 1, false, PREP1><<<blocks, 256, 0, s>>>(a);
   }
   return hipGetLastError();
 }
 
 template <int C0>
 hipError_t launch_c0(const FbArgs& a, int f0, int f1, bool pool, unsigned blocks, hipStream_t s) {
-  return f0 == 128 ? launch_c0f0<C0, 128>(a, f1, pool, blocks, s)
-                   : launch_c0f0<C0, 64>(a, f1, pool, blocks, s);
+  if (a.corr1)
+    return f0 == 128 ? launch_c0f0<C0, 128, true>(a, f1, pool, blocks, s)
+                     : launch_c0f0<C0, 64, true>(a, f1, pool, blocks, s);
+  return f0 == 128 ? launch_c0f0<C0, 128, false>(a, f1, pool, blocks, s)
+                   : launch_c0f0<C0, 64, false>(a, f1, pool, blocks, s);
 }
 
 }  // namespace
@@ -420,14 +452,14 @@ bool fconv_bconv_supported(const ConvGeom& g0, const ConvGeom& g1) {
 
 hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const float* in,
                               const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
-                              const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
-                              uint32_t* bits, hipStream_t s) {
+                              const uint32_t* w1, const void* w1prep, const int32_t* thr1,
+                              const uint32_t* flip1, uint32_t* bits, hipStream_t s) {
   FbArgs a;
   a.in = in;
   a.w0 = w0;
   a.thr0 = thr0;
   a.flip0 = flip0;
-  a.w1 = w1;
+  a.w1 = w1prep ? static_cast<const uint32_t*>(w1prep) : w1;
   a.thr1 = thr1;
   a.flip1 = flip1;
   a.bits = bits;
@@ -444,6 +476,11 @@ hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const floa
   a.Wp = g1.Wp;
   a.K1 = 9 * g1.C;
   a.w1_bytes = static_cast<int32_t>(static_cast<int64_t>(g1.F) * 9 * g1.Cw * 4);
+  a.corr1 = nullptr;
+  if (w1prep) {  // F1 and F0 are multiples of 64: entries [F1 / 32][9][F0 / 32][32]
+    a.w1_bytes = g1.F * 9 * g1.Cw * 16;
+    a.corr1 = reinterpret_cast<const int32_t*>(static_cast<const char*>(w1prep) + a.w1_bytes);
+  }
   a.tiles_w = (g1.Wo + kTW - 1) / kTW;
   a.tiles_h = (g1.Ho + kTH - 1) / kTH;
   const unsigned blocks = static_cast<unsigned>(g0.N) * a.tiles_w * a.tiles_h;

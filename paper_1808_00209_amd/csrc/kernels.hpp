@@ -58,7 +58,8 @@ hipError_t launch_bconv_mfma(const ConvGeom& g, const uint32_t* in,
                              int32_t* sums, uint32_t* bits, hipStream_t s);
 
 // Prepared ("operand form") conv weights for the matrix-core kernel: 16-byte
-// entries [ceil(F / 32)][KH][KW][Cp][32] (Cp = ceil(Cw / 8) * 8) holding each
+// entries [ceil(F / 32)][KH][KW][Cp][32] (Cp = Cw when C % 64 == 0, else
+// Cw rounded up to 8) holding each
 // weight word's four fp4 registers, then F int32 per-filter offsets.  Supported where
 // bconv_mfma_supported holds and the buffer stays under 2 GiB.
 int32_t prepared_words_per_tap(int32_t C);
@@ -101,11 +102,13 @@ hipError_t launch_fconv_binw(const ConvGeom& g, const float* in,
 // (3x3 over g0's output, 64 or 128 filters, optional 2x2 pooling).  Writes
 // the second layer's packed bits; both thr must be non-null.
 bool fconv_bconv_supported(const ConvGeom& g0, const ConvGeom& g1);
+// w1prep: the second layer's weights prepared by launch_prepare_weights, or
+// null (packed w1).
 hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const float* in,
                               const uint32_t* w0, const int32_t* thr0,
                               const uint32_t* flip0, const uint32_t* w1,
-                              const int32_t* thr1, const uint32_t* flip1,
-                              uint32_t* bits, hipStream_t s);
+                              const void* w1prep, const int32_t* thr1,
+                              const uint32_t* flip1, uint32_t* bits, hipStream_t s);
 
 // A run of consecutive binary FC layers in one launch (bfc_chain.hip): every
 // block takes R rows through all of them with the intermediate bits in LDS.

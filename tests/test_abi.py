@@ -125,7 +125,7 @@ def test_fconv_bconv_errors():
 
     def call(a=d0, b=d1, x=A, w0=A, thr0=A, w1=A, thr1=A, bits=A):
         return lib.bnn_fconv_bconv2d(ctypes.byref(a), ctypes.byref(b), x, w0, thr0, None, w1,
-                                     thr1, None, bits, None)
+                                     None, thr1, None, bits, None)
 
     # the second layer must read the first one's output
     assert call(b=_conv(N=2, H=30, W=32, C=128, F=128)) == 2 and "match" in bnn.last_error()
@@ -274,7 +274,8 @@ def test_options_defaults_set_get_and_range_checks():
         got = bnn.bnn_get_options()
         assert (got.algo, got.gemv_max_rows, got.lds_weights) == (1, 16, 1)
         for field, bad in [("algo", 2), ("fuse_input", 2), ("fuse_first", -1), ("fc_chain", 3),
-                           ("conv1x1", 2), ("xcd_order", -1), ("gemv_max_rows", 17),
+                           ("conv1x1", 2), ("xcd_order", -1), ("xcd_order", 3),
+                           ("gemv_max_rows", 17),
                            ("gemv_max_rows", -1), ("lds_weights", 2), ("late_thresholds", -2)]:
             with pytest.raises(bnn.BnnError, match="out of range"):
                 bnn.bnn_set_options(**{field: bad})
@@ -321,14 +322,16 @@ def test_library_sources_read_no_environment():
 @needs_lib
 def test_prepared_weights_size_and_argument_errors():
     """bnn_prepared_weights_size: 16-byte entries [ceil(F/32)*32][KH][KW][Cp]
-    with Cp = ceil(ceil(C/32) / 8) * 8, then F int32 offsets rounded up to 16
+    with Cp = Cw = ceil(C/32) when C % 64 == 0, else Cw rounded up to 8, then
+    F int32 offsets rounded up to 16
     bytes; shape, NULL and alignment errors of the three calls come before
     any launch."""
     lib = bnn.load()
     size = ctypes.c_size_t()
     for F, KH, KW, C in [(64, 3, 3, 64), (40, 3, 3, 96), (1024, 1, 1, 4100), (1, 1, 1, 1)]:
         assert lib.bnn_prepared_weights_size(F, KH, KW, C, ctypes.byref(size)) == 0
-        Cp = ((C + 31) // 32 + 7) // 8 * 8
+        Cw = (C + 31) // 32
+        Cp = Cw if C % 64 == 0 else (Cw + 7) // 8 * 8
         assert size.value == (F + 31) // 32 * 32 * KH * KW * Cp * 16 + (4 * F + 15) // 16 * 16
     assert lib.bnn_prepared_weights_size(0, 3, 3, 64, ctypes.byref(size)) == 2
     assert lib.bnn_prepared_weights_size(64, 3, 3, 64, None) == 1

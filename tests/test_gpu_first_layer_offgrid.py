@@ -126,8 +126,10 @@ def test_fused_first_offgrid_second_layer_exact_where_decided():
     d0, d1 = upload_layer(L0), upload_layer(L1)
     desc0 = bnn.conv_desc(N, H, W, C0, F0, 3, 3, 1, 1, 0)
     desc1 = bnn.conv_desc(N, H, W, F0, F1, 3, 3, 1, 1, 2)
-    got = words_u32(bnn.bnn_fconv_bconv2d(desc0, desc1, to_device(x), d0["w"], d0["thr"],
-                                          d0.get("flip"), d1["w"], d1["thr"], d1.get("flip")))
-    torch.cuda.synchronize()
     assert (~skip).mean() > 0.8
-    assert np.array_equal(got[~skip], want[~skip])
+    for w1prep in (None, d1["wprep"]):  # packed / prepared second-layer weights
+        got = words_u32(bnn.bnn_fconv_bconv2d(desc0, desc1, to_device(x), d0["w"], d0["thr"],
+                                              d0.get("flip"), d1["w"], d1["thr"], d1.get("flip"),
+                                              w1prep=w1prep))
+        torch.cuda.synchronize()
+        assert np.array_equal(got[~skip], want[~skip])

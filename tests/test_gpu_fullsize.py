@@ -135,7 +135,8 @@ def test_every_layer_bits_at_full_batch(cfg, batch, algo):
             if li == 1 and layers[0]["kind"] == "fconv" and algo != "valu":
                 d0 = bnn.conv_desc(N, H, W, C, layers[0]["F"], 3, 3, 1, layers[0]["pad"], 0)
                 fb = bnn.bnn_fconv_bconv2d(d0, desc, xd, dev[0]["w"], dev[0]["thr"],
-                                           dev[0].get("flip"), d["w"], d["thr"], d.get("flip"))
+                                           dev[0].get("flip"), d["w"], d["thr"], d.get("flip"),
+                                           w1prep=d["wprep"] if algo == "prep" else None)
                 torch.cuda.synchronize()
                 assert np.array_equal(words_u32(fb), _packed(outs[li])), "fused L0+L1"
             if li == 1 and layers[0]["kind"] == "input_threshold":

@@ -90,11 +90,15 @@ def test_fconv_bconv2d_entry_point(name):
     d1 = bnn.conv_desc(N, Ho0, Wo0, F0, F1, 3, 3, 1, pad1, pool)
     got = bnn.bnn_fconv_bconv2d(d0, d1, xd, l0["w"], l0["thr"], l0["flip"], l1["w"], l1["thr"],
                                 l1["flip"])
+    got_p = bnn.bnn_fconv_bconv2d(d0, d1, xd, l0["w"], l0["thr"], l0["flip"], l1["w"],
+                                  l1["thr"], l1["flip"], w1prep=l1["wprep"])
     _, b0 = bnn.bnn_fconv2d_binw(d0, xd, l0["w"], l0["thr"], l0["flip"], want_sums=False)
     _, b1 = bnn.bnn_bconv2d(d1, b0, l1["w"], l1["thr"], l1["flip"], want_sums=False)
     torch.cuda.synchronize()
+    ref = oracle.pack_eq2(oracle.forward(layers, x))
     assert np.array_equal(words_u32(got), words_u32(b1))
-    assert np.array_equal(words_u32(got), oracle.pack_eq2(oracle.forward(layers, x)))
+    assert np.array_equal(words_u32(got), ref)
+    assert np.array_equal(words_u32(got_p), ref)  # prepared second-layer weights
 
 
 def test_fused_first_ties_zero_windows_and_extreme_thresholds():

@@ -25,8 +25,10 @@ pytestmark = pytest.mark.gpu
 # the matrix-core workgroups on a 2-D grid (pixel blocks x filter tiles)
 # instead of the one-dimensional XCD order; "prep" is "auto" with the conv
 # weights in the prepared operand form (bnn_bconv2d_prepared), and
-# "prep_early2d" that with early thresholds on the 2-D grid.
-ALGOS = ["auto", "valu", "lds", "early", "grid2d", "prep", "prep_early2d"]
+# "prep_early2d" that with early thresholds on the 2-D grid; "prep_xcdsplit"
+# is "prep" with the filter tiles split over XCD groups where that cuts the
+# bytes the L2s move (option xcd_order = 2).
+ALGOS = ["auto", "valu", "lds", "early", "grid2d", "prep", "prep_early2d", "prep_xcdsplit"]
 _PREP = False  # whether _run_conv passes prepared weights
 
 
@@ -36,7 +38,8 @@ def algo(request):
     bnn.bnn_set_options(**{"auto": {}, "valu": dict(algo=bnn.ALGO_VALU),
                            "lds": dict(lds_weights=1), "early": dict(late_thresholds=0),
                            "grid2d": dict(xcd_order=0), "prep": {},
-                           "prep_early2d": dict(late_thresholds=0, xcd_order=0)}[request.param])
+                           "prep_early2d": dict(late_thresholds=0, xcd_order=0),
+                           "prep_xcdsplit": dict(xcd_order=2)}[request.param])
     _PREP = request.param.startswith("prep")
     yield request.param
     _PREP = False
@@ -451,6 +454,37 @@ def test_bconv_input_matches_pack_then_bconv():
     assert np.array_equal(words_u32(fused)[[0, 7]], ref)
 
 
+# ------------------------------------------------ XCD groups of filters ---
+# Grids of >= 8 pixel blocks run in the XCD order; with option xcd_order = 2
+# the filter tiles are split over g = 1, 2, 4 or 8 XCD groups chosen from
+# the layer's activation, weight and output bytes (tile_grid): these shapes
+# span the choices (family "prep_xcdsplit"; the others run them unsplit).
+XCD_CASES = [  # N, H, W, C, F, pool
+    (8, 16, 16, 512, 512, 2),
+    (4, 16, 32, 256, 256, 0),
+    (8, 16, 16, 128, 128, 2),
+    (16, 16, 16, 64, 64, 0),
+    (32, 32, 32, 64, 64, 2),
+]
+
+
+@pytest.mark.parametrize("case", XCD_CASES, ids=[str(c) for c in XCD_CASES])
+def test_bconv_xcd_filter_groups_bit_exact(case, algo):
+    N, H, W, C, F, pool = case
+    rng = np.random.default_rng(N * 100 + C)
+    x = _pm1(rng, (N, H, W, C))
+    L = dict(w=_pm1(rng, (F, 3, 3, C)), pad=1,
+             thr=rng.integers(-3 * int(np.sqrt(9 * C)), 3 * int(np.sqrt(9 * C)) + 1,
+                              size=F).astype(np.int32),
+             flip=rng.integers(0, 2, size=F).astype(np.uint8))
+    sums, bits = _run_conv(x, L, pool)
+    S, B = _oracle_conv(x, L, pool)
+    assert np.array_equal(sums.cpu().numpy(), S)
+    assert np.array_equal(words_u32(bits), B)
+    _, bits_only = _run_conv(x, L, pool, want_sums=False)
+    assert np.array_equal(words_u32(bits_only), B)
+
+
 # ---------------------------------------------------- prepared weights ---
 @pytest.mark.parametrize("F,KH,KW,C", [(40, 3, 3, 96), (33, 1, 1, 4100), (64, 3, 3, 64),
                                        (32, 5, 5, 32)])
@@ -468,7 +502,7 @@ def test_prepared_weights_decode_to_the_packed_weights(F, KH, KW, C):
     torch.cuda.synchronize()
     raw = prep.cpu().numpy()
     Cw = (C + 31) // 32
-    Cp = (Cw + 7) // 8 * 8
+    Cp = Cw if C % 64 == 0 else (Cw + 7) // 8 * 8
     Fp = (F + 31) // 32 * 32
     n_ent = Fp * KH * KW * Cp
     assert raw.size == bnn.bnn_prepared_weights_size(F, KH, KW, C) >= n_ent * 16 + 4 * F
