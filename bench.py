@@ -35,26 +35,32 @@ HBM_PEAK_GBS = 8000.0
 # HBM traffic of the dominant kernel from two rocprofv3 --pmc passes
 # (FETCH_SIZE, WRITE_SIZE, KiB per dispatch) over this same script.  The
 # counters are calibrated on a 256 MiB device-to-device copy in the same
-# runs: FETCH_SIZE read 131087.8 KiB for 262144 KiB moved (factor 2.0),
+# runs: FETCH_SIZE read 131088.0 KiB for 262144 KiB moved (factor 2.0),
 # WRITE_SIZE read 262144.0 KiB (factor 1.0).  A figure is reported only while
 # the kernel's sources hash to the values recorded with it and the compile
 # flags (build.COMMON without include paths) to the flags digest.
 _FLAGS = "cfb3b8a417945f0b0125dc066d5529292593229deafe2cb65291c547d733ed6c"
 _FP4 = ("paper_1808_00209_amd/csrc/fp4_expand.hpp",
-        "d025e6c895771b0e8c624d6b14e4559aae203e5a519954919d75dea0192da41b")
+        "0e9682bb144ead3c1db16be7650c740fd04372b1500d13fc31e17b78cafc61b4")
 _LANE = ("paper_1808_00209_amd/csrc/lane_ops.hpp",
          "96ece7042c6ed72e9cd799fdd8e007525e30035bbd8d052a9ece380c5e3fda82")
+_KERN = ("paper_1808_00209_amd/csrc/kernels.hpp",
+         "6ff0b384ee272b0a0f05b0dc5f0d03bc7994e1fe108f4d06bc066fb8652ebbf2")
 MEASURED_TRAFFIC = {
+    # profiles/fconv_bconv_cifar_b64.md
     ("cifar_bnn_b64", "L0+L1 fconv+bconv 32x32x3->128->128 k3 pool (fused)"): dict(
-        fetch_kib=690.3, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
+        fetch_kib=904.7, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/fconv_bconv.hip",
-                       "1c401b19e914cf02c4dc9c436e952e9e4183e2201895b6a2025c950f5ebfdc85"),
-                      _FP4, _LANE]), flags=_FLAGS),
+                       "7ced5f651797ed566b799fea7a057d712aa9f3ab31e7e71c0ea6694199df2f6c"),
+                      ("paper_1808_00209_amd/csrc/fp32_split.hpp",
+                       "7f3a9f6b25af5be34fb5b304976e0225cd491d935c5a4e567bc43c134b6ceb13"),
+                      _FP4, _LANE, _KERN]), flags=_FLAGS),
+    # profiles/bconv_mfma_cifar_b64.md
     ("cifar_bnn_b64", "L5 bconv 8x8x512->512 k3 pool"): dict(
-        fetch_kib=1342.0, write_kib=64.0, fetch_scale=2.0, write_scale=1.0,
+        fetch_kib=4806.0, write_kib=64.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/bconv_mfma.hip",
-                       "583714c26a6fb24e147a26e9ea6fd809c376d4810edebf5bdc16e94bd88fae75"),
-                      _FP4, _LANE]), flags=_FLAGS),
+                       "430e988963e1a69883cfa46ec7a72a2f16f4332250770061e08135ab39f09c52"),
+                      _FP4, _LANE, _KERN]), flags=_FLAGS),
 }
 
 
@@ -108,6 +114,9 @@ def parse():
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the timing of the other configurations (single conv, FC GEMM, "
                          "vehicle-shaped net, large layers)")
+    ap.add_argument("--only-configs", action="store_true",
+                    help="time only the other configurations (for profiling them alone); "
+                         "prints their figures as one JSON object, not the bench line")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one 256 MiB device-to-device copy (calibrates the "
                          "FETCH_SIZE / WRITE_SIZE counters of a profiling run)")
@@ -571,6 +580,17 @@ def cpu_baseline(layers, cfg, target_s, bin_ops_per_image, max_images=4096):
                       "scaled to binary GOPS" % (n, dt)}
 
 
+def copy_probe(torch):
+    """One 256 MiB device-to-device copy: the known byte count against which
+    a profiling run calibrates the FETCH_SIZE / WRITE_SIZE counters."""
+    src = torch.empty(64 << 20, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -589,6 +609,12 @@ def main():
         sys.exit(2)
     torch.cuda.set_device(0)
     bnn.load()
+    if args.only_configs:
+        res = {"configs": config_suite(bnn, torch)}
+        if args.copy_probe:
+            copy_probe(torch)
+        print(json.dumps(res), flush=True)
+        return
     wl = WORKLOADS[args.workload]
     batch, H, W, C = wl["batch"], wl["H"], wl["W"], wl["C"]
     layers = net_layers(wl["cfg"])
@@ -757,12 +783,7 @@ def main():
         result["cpu_baseline"] = cpu_baseline(layers, wl["cfg"], args.cpu_seconds,
                                               2 * bin_macs_img)
     if args.copy_probe:
-        src = torch.empty(64 << 20, dtype=torch.int32, device="cuda")
-        dst = torch.empty_like(src)
-        src.fill_(1)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
+        copy_probe(torch)
     print(json.dumps(result), flush=True)
 
 
