@@ -983,8 +983,11 @@ Plan plan_mfma(const ConvGeom& g, bool pool) {
   // words.  With 64-filter tiles over 256 or more channels the prepared
   // operands' registers cost a wave per SIMD (180 against 154 VGPRs) and
   // 4x the weight bytes through L1: 56x56x256 -> 256 took 54 us packed and
-  // 60-65 us prepared.
-  p.prep = tf == 1 || g.Cw <= 2;
+  // 60-65 us prepared.  Rows of 4 words without LDS staging also pay
+  // (16x16x128 -> 256 at batch 64: 6.3 -> 5.9 us); with LDS staging the
+  // packed words are expanded once per block, which prepared operands
+  // cannot match (48x48x128 -> 128 pool at batch 256: 48 against 54 us).
+  p.prep = tf == 1 || g.Cw <= 2 || (g.Cw <= 4 && !lds);
   return p;
 }
 
