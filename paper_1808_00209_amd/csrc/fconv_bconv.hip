@@ -3,16 +3,16 @@
 // launch, for the BCNN without input binarization (Table I): the first
 // layer's output never goes to global memory.
 //
-// A block owns an 8 x 32 tile of the second layer's output pixels of one
-// image (4 x 16 2x2 windows when it pools) and all of its filters (64 or
-// 128; 4 waves per 64 filters).
-//   1. It stages the input tile the first layer needs for the (8 + 2) x
+// A block owns a TH x 32 tile of the second layer's output pixels of one
+// image (TH = 8, or 4 on small grids; TH / 2 x 16 2x2 windows when it pools)
+// and all of its filters (64 or 128; TH / 2 waves per 64 filters).
+//   1. It stages the input tile the first layer needs for the (TH + 2) x
 //      (32 + 2) pixels of the second layer's windows (halo of one pixel),
 //      zero outside the image, with every value split once into three bf16
 //      parts, x = p0 + p1 + p2 exactly (split3), plus both layers'
 //      thresholds and the first layer's +-1 weight operands.  All global
 //      loads are issued before the first LDS store.
-//   2. All waves compute the first layer's outputs on that 10 x 34 tile with
+//   2. All waves compute the first layer's outputs on that (TH + 2) x 34 tile with
 //      v_mfma_f32_16x16x32_bf16 on the three parts (exact products, fp32
 //      accumulation; exact sums in any order for inputs on the 2^-16 grid
 //      whose window sums of |x| stay below 2^8), take
@@ -37,11 +37,9 @@
 namespace bnn {
 namespace {
 
-constexpr int kTH = 8, kTW = 32;             // second-layer output tile
-constexpr int kAH = kTH + 2, kAW = kTW + 2;  // first-layer tile (second layer's windows)
-constexpr int kIH = kAH + 2, kIW = kAW + 2;  // input tile (first layer's windows)
-constexpr int kAPix = kAH * kAW;             // 340
-constexpr int kATiles = (kAPix + 15) / 16;   // 16-pixel tiles of the first layer
+constexpr int kTW = 32;         // second-layer output tile width (height TH = 8 or 4)
+constexpr int kAW = kTW + 2;    // first-layer tile width (second layer's windows)
+constexpr int kIW = kAW + 2;    // input tile width (first layer's windows)
 
 struct FbArgs {
   const float* in;
@@ -63,15 +61,25 @@ struct FbArgs {
 };
 
 constexpr uint32_t kRsrcWord3 = 0x00020000;
+constexpr int64_t kSmallGrid = 128;  // workgroups
 
 // PREP1: w1 holds the second layer's weights in the prepared operand form
 // (bnn_prepare_weights: 16-byte entries [F1 / 32][9][F0 / 32][32], then the
 // offsets corr1), so the second layer loads its A operands whole, and the
 // first layer stores its bits as act_operand instead of expand_fp4 operands.
-template <int C0, int F0, int NFH, bool POOL, bool PREP1>
-__global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
-  constexpr int NT = 256 * NFH;        // threads
-  constexpr int NW = 4 * NFH;          // waves
+// TH: rows of the second layer's output tile, 8, or 4 on grids too small to
+// fill the chip (half the workgroups' work each, for 1.25 times the
+// first-layer work per output row).
+template <int TH, int C0, int F0, int NFH, bool POOL, bool PREP1>
+__global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
+  constexpr int kTH = TH;
+  constexpr int kAH = kTH + 2;                // first-layer tile rows
+  constexpr int kIH = kAH + 2;                // input tile rows
+  constexpr int kAPix = kAH * kAW;            // 340 (TH = 8), 204 (TH = 4)
+  constexpr int kATiles = (kAPix + 15) / 16;  // 16-pixel tiles of the first layer
+  constexpr int PG = TH / 2;                  // 64-pixel groups of the second layer
+  constexpr int NW = PG * NFH;                // waves
+  constexpr int NT = 64 * NW;                 // threads
   constexpr int K0 = 9 * C0;
   constexpr int KC0 = (K0 + 31) / 32;  // first-layer k-chunks of 32
   constexpr int FT0 = F0 / 16;         // first-layer filter tiles of 16
@@ -190,7 +198,7 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
   uint32_t vfill;
   asm("v_mov_b32 %0, 0x22222222" : "=v"(vfill));
 
-  // 2. First layer on the 10 x 34 tile: lane (q, c) = (l / 16, l % 16) holds
+  // 2. First layer on the (TH + 2) x 34 tile: lane (q, c) = (l / 16, l % 16) holds
   // pixel c of a 16-pixel tile and filters 16 ft + 4 q + r (r = 0..3).
   {
     const int q = lane >> 4, c = lane & 15;
@@ -280,7 +288,7 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
   __syncthreads();
 
   // 3. Second layer: wave = pixel group pg (64 pixels) x filter half fh.
-  const int pg = wave & 3, fh = wave >> 2;
+  const int pg = wave % PG, fh = wave / PG;
   const int h = lane >> 5, c = lane & 31;
   const int f0 = 64 * fh;
   int pr[2], pc[2], abase[2];
@@ -414,29 +422,37 @@ __global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
   }
 }
 
-template <int C0, int F0, bool PREP1>
-hipError_t launch_c0f0(const FbArgs& a, int f1, bool pool, unsigned blocks, hipStream_t s) {
+template <int TH, int C0, int F0, bool PREP1>
+hipError_t launch_th(const FbArgs& a, int f1, bool pool, unsigned blocks, hipStream_t s) {
   if (f1 == 128) {
     if (pool)
-      fconv_bconv_kernel<C0, F0, 2, true, PREP1><<<blocks, 512, 0, s>>>(a);
+      fconv_bconv_kernel<TH, C0, F0, 2, true, PREP1><<<blocks, 64 * TH, 0, s>>>(a);
     else
-      fconv_bconv_kernel<C0, F0, 2, false, PREP1><<<blocks, 512, 0, s>>>(a);
+      fconv_bconv_kernel<TH, C0, F0, 2, false, PREP1><<<blocks, 64 * TH, 0, s>>>(a);
   } else {
     if (pool)
-      fconv_bconv_kernel<C0, F0, 1, true, PREP1><<<blocks, 256, 0, s>>>(a);
+      fconv_bconv_kernel<TH, C0, F0, 1, true, PREP1><<<blocks, 32 * TH, 0, s>>>(a);
     else
-      fconv_bconv_kernel<C0, F0, 1, false, PREP1><<<blocks, 256, 0, s>>>(a);
+      fconv_bconv_kernel<TH, C0, F0, 1, false, PREP1><<<blocks, 32 * TH, 0, s>>>(a);
   }
   return hipGetLastError();
 }
 
+template <int C0, int F0, bool PREP1>
+hipError_t launch_c0f0(const FbArgs& a, int th, int f1, bool pool, unsigned blocks,
+                       hipStream_t s) {
+  return th == 8 ? launch_th<8, C0, F0, PREP1>(a, f1, pool, blocks, s)
+                 : launch_th<4, C0, F0, PREP1>(a, f1, pool, blocks, s);
+}
+
 template <int C0>
-hipError_t launch_c0(const FbArgs& a, int f0, int f1, bool pool, unsigned blocks, hipStream_t s) {
+hipError_t launch_c0(const FbArgs& a, int th, int f0, int f1, bool pool, unsigned blocks,
+                     hipStream_t s) {
   if (a.corr1)
-    return f0 == 128 ? launch_c0f0<C0, 128, true>(a, f1, pool, blocks, s)
-                     : launch_c0f0<C0, 64, true>(a, f1, pool, blocks, s);
-  return f0 == 128 ? launch_c0f0<C0, 128, false>(a, f1, pool, blocks, s)
-                   : launch_c0f0<C0, 64, false>(a, f1, pool, blocks, s);
+    return f0 == 128 ? launch_c0f0<C0, 128, true>(a, th, f1, pool, blocks, s)
+                     : launch_c0f0<C0, 64, true>(a, th, f1, pool, blocks, s);
+  return f0 == 128 ? launch_c0f0<C0, 128, false>(a, th, f1, pool, blocks, s)
+                   : launch_c0f0<C0, 64, false>(a, th, f1, pool, blocks, s);
 }
 
 }  // namespace
@@ -459,6 +475,17 @@ hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const floa
   a.w0 = w0;
   a.thr0 = thr0;
   a.flip0 = flip0;
+  // 8-row tiles, or 4-row tiles where 8-row tiles would leave more than
+  // half of the 256 compute units idle (CIFAR L0 + L1 at batch 1: 7.70
+  // against 7.97 us).  Prepared second-layer weights only with 8-row tiles:
+  // on the small grids the 4x larger operands come from beyond L2 and the
+  // packed words are faster (batch 1 / 16: 7.25 / 7.70 us packed against
+  // 7.77 / 8.11 prepared; batch 32 / 64: 8.98 / 9.74 packed, 8.70 / 9.36
+  // prepared).
+  const int64_t tiles8 =
+      int64_t{g0.N} * ((g1.Wo + kTW - 1) / kTW) * ((g1.Ho + 7) / 8);
+  const int th = tiles8 < kSmallGrid ? 4 : 8;
+  if (th == 4) w1prep = nullptr;
   a.w1 = w1prep ? static_cast<const uint32_t*>(w1prep) : w1;
   a.thr1 = thr1;
   a.flip1 = flip1;
@@ -482,14 +509,14 @@ hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const floa
     a.corr1 = reinterpret_cast<const int32_t*>(static_cast<const char*>(w1prep) + a.w1_bytes);
   }
   a.tiles_w = (g1.Wo + kTW - 1) / kTW;
-  a.tiles_h = (g1.Ho + kTH - 1) / kTH;
+  a.tiles_h = (g1.Ho + th - 1) / th;
   const unsigned blocks = static_cast<unsigned>(g0.N) * a.tiles_w * a.tiles_h;
   const bool pool = g1.pool == 2;
   switch (g0.C) {
-    case 1: return launch_c0<1>(a, g0.F, g1.F, pool, blocks, s);
-    case 2: return launch_c0<2>(a, g0.F, g1.F, pool, blocks, s);
-    case 3: return launch_c0<3>(a, g0.F, g1.F, pool, blocks, s);
-    default: return launch_c0<4>(a, g0.F, g1.F, pool, blocks, s);
+    case 1: return launch_c0<1>(a, th, g0.F, g1.F, pool, blocks, s);
+    case 2: return launch_c0<2>(a, th, g0.F, g1.F, pool, blocks, s);
+    case 3: return launch_c0<3>(a, th, g0.F, g1.F, pool, blocks, s);
+    default: return launch_c0<4>(a, th, g0.F, g1.F, pool, blocks, s);
   }
 }
 

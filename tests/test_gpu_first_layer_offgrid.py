@@ -101,11 +101,12 @@ def test_fconv_offgrid_sums_within_bound_bits_exact_where_decided(case, pool, al
     assert np.array_equal(gb[d], wb[d])
 
 
-def test_fused_first_offgrid_second_layer_exact_where_decided():
+@pytest.mark.parametrize("N", [3, 34])  # 4-row tiles with packed, 8-row with prepared w1
+def test_fused_first_offgrid_second_layer_exact_where_decided(N):
     """bnn_fconv_bconv2d on N(0,1) input: the second layer's pooled bits
     against the oracle chain on every output whose 4 x 4 x F0 receptive
     field in the first layer's output holds only decided values."""
-    N, H, W, C0, F0, F1 = 3, 32, 32, 3, 128, 128
+    H, W, C0, F0, F1 = 32, 32, 3, 128, 128
     rng, x = _inputs(2024, (N, H, W, C0), 1.0)
     L0 = synth.conv_layer(9, 0, "fconv", C0, F0, pad=1)
     L0["thr"] = _thresholds(rng, F0, 1.0, 9 * C0)

@@ -49,7 +49,7 @@ def _run(net, xd, fuse):
 
 
 @pytest.mark.parametrize("name", sorted(CASES))
-@pytest.mark.parametrize("batch", [1, 5])
+@pytest.mark.parametrize("batch", [1, 5, 40])  # 4-row tiles at 1 and 5, mostly 8-row at 40
 def test_fused_first_matches_two_launches_and_oracle(name, batch):
     H, W, C0 = CASES[name][:3]
     layers = _net(name)
