@@ -590,33 +590,48 @@ __global__ __launch_bounds__(KS == 1 ? 256 : 64 * KS) void bconv_mfma32_kernel(M
       __syncthreads();
     }
   } else {
-    // Partial sums of the KS waves meet in LDS: every wave stores its tile
-    // in its own slot, all threads of the block add the slots slice by slice
-    // into slot 0, and wave 0 takes the totals for the epilogue.
+    // Partial sums of the KS waves meet in LDS.  KS = 2: wave 1 stores its
+    // tile and, after one barrier, wave 0 adds it to its own.  KS >= 4: every
+    // wave stores its tile, all threads add the slots slice by slice into
+    // slot 0 and wave 0 takes the totals (one barrier more, but wave 0 then
+    // reads one tile instead of KS - 1).  Exact either way: integer sums
+    // below 2^24.  (256 x 4096 -> 4096 GEMM, KS = 2: 8.36 -> 7.51 us with
+    // the one-barrier form; the conv layers at batch 1, KS = 4: 0.04-0.12 us
+    // slower with it.)
     constexpr int NV = TF * TP * 16 * 64;  // values per wave
-    __shared__ float part[KS][NV];
+    constexpr int SLOTS = KS == 2 ? 1 : KS;
+    __shared__ float part[SLOTS][NV];
     ep.stage(a, thl, cl, false);
+    if (KS > 2 || wave > 0) {
+      const int slot = KS == 2 ? 0 : wave;
 #pragma unroll
-    for (int tf = 0; tf < TF; ++tf)
+      for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
-      for (int tp = 0; tp < TP; ++tp)
+        for (int tp = 0; tp < TP; ++tp)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) part[wave][((tf * TP + tp) * 16 + e) * 64 + lane] = acc[tf][tp][e];
-    __syncthreads();
-    for (int v = threadIdx.x; v < NV; v += 64 * KS) {
-      float t = part[0][v];
-#pragma unroll
-      for (int w = 1; w < KS; ++w) t += part[w][v];
-      part[0][v] = t;
+          for (int e = 0; e < 16; ++e)
+            part[slot][((tf * TP + tp) * 16 + e) * 64 + lane] = acc[tf][tp][e];
     }
     __syncthreads();
+    if constexpr (KS > 2) {
+      for (int v = threadIdx.x; v < NV; v += 64 * KS) {
+        float t = part[0][v];
+#pragma unroll
+        for (int w = 1; w < KS; ++w) t += part[w][v];
+        part[0][v] = t;
+      }
+      __syncthreads();
+    }
     if (wave > 0) return;
 #pragma unroll
     for (int tf = 0; tf < TF; ++tf)
 #pragma unroll
       for (int tp = 0; tp < TP; ++tp)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) acc[tf][tp][e] = part[0][((tf * TP + tp) * 16 + e) * 64 + lane];
+        for (int e = 0; e < 16; ++e) {
+          const float t = part[0][((tf * TP + tp) * 16 + e) * 64 + lane];
+          acc[tf][tp][e] = KS == 2 ? acc[tf][tp][e] + t : t;
+        }
   }
   epilogue<TF, TP, POOL, VW>(a, acc, px, p0, f0, h, c, thl, cl, ep, pre);
 }
