@@ -130,6 +130,7 @@ __global__ __launch_bounds__(256) void bconv_patch_kernel(PatchArgs a) {
   __shared__ uint32_t tile[kMaxTile];
   __shared__ uint32_t wpat[kFB * PW];
   __shared__ int32_t wbias[kFB];
+  __shared__ uint32_t wflip[kFB / 32];
 
   const int t = threadIdx.x;
   const int C = a.in.C;
@@ -170,6 +171,9 @@ __global__ __launch_bounds__(256) void bconv_patch_kernel(PatchArgs a) {
 #pragma unroll
     for (int q = 0; q < PW; ++q) wpat[t * PW + q] = wp[q];
     wbias[t] = bias;
+    // the round's flip words (read once here rather than after each word's
+    // popcounts, where the load's round trip would stall the wave)
+    if (t < kFB / 32) wflip[t] = a.flip && 32 * t < nf ? a.flip[(f0 >> 5) + t] : 0u;
   };
 
   // Binarize the input tile plus halo, and stage the first filter round.
@@ -258,7 +262,7 @@ __global__ __launch_bounds__(256) void bconv_patch_kernel(PatchArgs a) {
             d += static_cast<uint32_t>(__builtin_popcount(patch[q] ^ wpat[(g + k) * PW + q]));
           word = __builtin_amdgcn_alignbit(word, d, 31);
         }
-        if (a.flip) word ^= a.flip[fw];
+        word ^= wflip[g >> 5];
         if (fw == a.Fw - 1) word &= tail_mask(a.F);
         if constexpr (POOL) {
           word = or_quad(word);
