@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define BNN_ABI_VERSION 5
+#define BNN_ABI_VERSION 6
 
 typedef enum bnn_status {
   BNN_OK = 0,
@@ -94,8 +94,8 @@ typedef enum bnn_algo {
 
 typedef struct bnn_options {
   int32_t algo;            /* bnn_algo                                       */
-  int32_t fuse_input;      /* bnn_forward: an input layer and a small-window */
-                           /* conv after it as one kernel (1, default) or two */
+  int32_t fuse_input;      /* bnn_forward: an input layer and the conv(s)    */
+                           /* after it as one kernel (1, default) or apart  */
   int32_t fuse_first;      /* bnn_forward: FCONV_BINW and the 3x3 conv after */
                            /* it as one kernel (1, default) or two (0)       */
   int32_t fc_chain;        /* bnn_forward: runs of small FC layers as one    */
@@ -327,6 +327,31 @@ bnn_status bnn_fconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc* d1,
                              uint32_t* out_bits, hipStream_t stream);
 
 /*
+ * Input thresholding (Sec. II-C), a binary 3x3 conv over the thresholded
+ * image and a binary 3x3 conv over its output bits in one launch, the first
+ * conv's bits never leaving the chip (the vehicle classifier's first layers,
+ * Table III thresholded RGB input).  The result equals bnn_bconv2d_input
+ * followed by bnn_bconv2d, bit for bit.
+ *   d0        the first conv: C = 3 (the image's channels), 3x3, F = 64 or
+ *             128, no pooling, pad 0 or 1 (pad value -1).
+ *   d1        the second: N, H, W equal to d0's N and output Ho, Wo; 3x3,
+ *             C = d0's F, F = 64 or 128, pad 0 or 1, pool 0 or 2.
+ *   mode      BNN_INPUT_THRESHOLD (other modes: BNN_ERR_UNSUPPORTED).
+ *   x, offset as for bnn_bconv2d_input ([N][H][W][3] fp32, offsets [3] or
+ *             NULL).
+ *   w0, thr0, flip0, w1, w1prep, thr1, flip1, out_bits: as for
+ *             bnn_fconv_bconv2d.
+ * Alignment and errors as for bnn_fconv_bconv2d.
+ */
+bnn_status bnn_input_bconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc* d1,
+                                  int32_t mode, const float* x, const float* offset,
+                                  const uint32_t* w0, const int32_t* thr0,
+                                  const uint32_t* flip0, const uint32_t* w1,
+                                  const void* w1prep, const int32_t* thr1,
+                                  const uint32_t* flip1, uint32_t* out_bits,
+                                  hipStream_t stream);
+
+/*
  * Binary fully-connected layer / GEMM (Sec. III-B, Eq. 4):
  *   S[m][n] = K - 2 * sum_j popcount(A[m][j] XOR B[n][j])   (valid bits only)
  *   A         [M][Kw] u32, Kw = ceil(K / 32): M packed input vectors.
@@ -388,9 +413,11 @@ bnn_status bnn_forward_workspace_size(const bnn_layer* layers,
  * Run the chain on input [batch][H][W][C] fp32 and write int32 logits
  * [batch][N_last] (Table I/II: conv, pool, ..., FC layers).  One kernel per
  * layer on `stream`, with three exceptions:
- *  - an input layer followed by a BCONV whose window fits
- *    bnn_bconv2d_input runs as that one kernel (option fuse_input = 0
- *    keeps them apart);
+ *  - an INPUT_THRESHOLD layer of 3 channels followed by two 3x3 BCONVs of
+ *    64 or 128 filters (the first without pooling) runs as one kernel
+ *    (bnn_input_bconv_bconv2d); otherwise an input layer followed by a BCONV
+ *    whose window fits bnn_bconv2d_input runs as that one kernel (option
+ *    fuse_input = 0 keeps them all apart);
  *  - an FCONV_BINW layer (3x3, at most 4 channels, 64 or 128 filters, no
  *    pooling) followed by a 3x3 BCONV of 64 or 128 filters runs as one
  *    kernel that keeps the first layer's bits in LDS (bnn_fconv_bconv2d;

@@ -37,7 +37,7 @@ EXPORTED = ["bnn_last_error", "bnn_abi_version", "bnn_default_options", "bnn_set
             "bnn_get_options", "bnn_pack_bits", "bnn_conv_output_dims",
             "bnn_bconv2d", "bnn_prepared_weights_size", "bnn_prepare_weights",
             "bnn_bconv2d_prepared", "bnn_fconv2d_binw", "bnn_binarize_input", "bnn_bconv2d_input",
-            "bnn_fconv_bconv2d", "bnn_bgemm",
+            "bnn_fconv_bconv2d", "bnn_input_bconv_bconv2d", "bnn_bgemm",
             "bnn_forward_workspace_size", "bnn_forward", "bnn_forward_noalloc"]
 
 # Bytes of bnn_forward_noalloc's per-GPU scratch array (BNN_FORWARD_SCRATCH_BYTES).
@@ -107,6 +107,8 @@ def load(path: str = LIB_PATH):
     lib.bnn_bconv2d_input.argtypes = [ctypes.POINTER(ConvDesc), i32, P, P, P, P, P, P, P, P]
     lib.bnn_fconv_bconv2d.argtypes = [ctypes.POINTER(ConvDesc), ctypes.POINTER(ConvDesc),
                                       P, P, P, P, P, P, P, P, P, P]
+    lib.bnn_input_bconv_bconv2d.argtypes = [ctypes.POINTER(ConvDesc), ctypes.POINTER(ConvDesc),
+                                            i32, P, P, P, P, P, P, P, P, P, P, P]
     lib.bnn_forward_workspace_size.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32,
                                                ctypes.POINTER(ctypes.c_size_t)]
     lib.bnn_forward.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32, P, P,
@@ -359,6 +361,33 @@ def bnn_fconv_bconv2d(desc0: ConvDesc, desc1: ConvDesc, x, w0, thr0, flip0, w1, 
     _check(lib.bnn_fconv_bconv2d(ctypes.byref(desc0), ctypes.byref(desc1), _ptr(x), _ptr(w0),
                                  _ptr(thr0), _ptr(flip0), _ptr(w1), _ptr(w1prep), _ptr(thr1),
                                  _ptr(flip1), _ptr(out_bits), _stream(stream)))
+    return out_bits
+
+
+def bnn_input_bconv_bconv2d(desc0: ConvDesc, desc1: ConvDesc, mode, x, offset, w0, thr0, flip0,
+                            w1, thr1, flip1=None, out_bits=None, stream=None, w1prep=None):
+    """Input thresholding, a binary 3x3 conv and a binary 3x3 conv over its
+    bits in one launch: returns the second conv's packed bits
+    [N, Hp, Wp, F1/32], the same as bnn_bconv2d_input followed by
+    bnn_bconv2d.  w1prep: bnn_prepare_weights of w1, or None."""
+    lib = load()
+    _, _, Hp, Wp = bnn_conv_output_dims(desc1)
+    _dev(x, torch.float32, "x")
+    offset = _dev(offset, torch.float32, "offset")
+    _u32(w0)
+    _u32(w1)
+    thr0 = _dev(thr0, torch.int32, "thr0")
+    thr1 = _dev(thr1, torch.int32, "thr1")
+    flip0 = _dev(flip0, torch.int32, "flip0")
+    flip1 = _dev(flip1, torch.int32, "flip1")
+    if out_bits is None:
+        out_bits = torch.empty((desc1.N, Hp, Wp, words(desc1.F)), dtype=torch.int32,
+                               device=x.device)
+    _dev(w1prep, torch.uint8, "w1prep")
+    _check(lib.bnn_input_bconv_bconv2d(ctypes.byref(desc0), ctypes.byref(desc1), int(mode),
+                                       _ptr(x), _ptr(offset), _ptr(w0), _ptr(thr0), _ptr(flip0),
+                                       _ptr(w1), _ptr(w1prep), _ptr(thr1), _ptr(flip1),
+                                       _ptr(out_bits), _stream(stream)))
     return out_bits
 
 

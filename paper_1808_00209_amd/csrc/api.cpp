@@ -432,6 +432,45 @@ bnn_status bnn_fconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc* d1, c
   }
 }
 
+bnn_status bnn_input_bconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc* d1,
+                                  int32_t mode, const float* x, const float* offset,
+                                  const uint32_t* w0, const int32_t* thr0,
+                                  const uint32_t* flip0, const uint32_t* w1,
+                                  const void* w1prep, const int32_t* thr1,
+                                  const uint32_t* flip1, uint32_t* out_bits,
+                                  hipStream_t stream) {
+  try {
+    bnn::ConvGeom g0, g1;
+    bnn_status st = conv_geom(d0, &g0);
+    if (st != BNN_OK) return st;
+    st = conv_geom(d1, &g1);
+    if (st != BNN_OK) return st;
+    if (mode != BNN_INPUT_THRESHOLD && mode != BNN_INPUT_GRAY && mode != BNN_INPUT_LBP)
+      return fail(BNN_ERR_SHAPE, "input_bconv_bconv2d: unknown mode %d", mode);
+    if (g1.N != g0.N || g1.H != g0.Hp || g1.W != g0.Wp || g1.C != g0.F)
+      return fail(BNN_ERR_SHAPE,
+                  "input_bconv_bconv2d: second layer input %dx%dx%dx%d does not match the "
+                  "first layer's output %dx%dx%dx%d",
+                  g1.N, g1.H, g1.W, g1.C, g0.N, g0.Hp, g0.Wp, g0.F);
+    if (!bnn::input_bconv_bconv_supported(mode, g0, g1))
+      return fail(BNN_ERR_UNSUPPORTED,
+                  "input_bconv_bconv2d: needs mode THRESHOLD, 3 input channels, 3x3 convs, "
+                  "64 or 128 filters, no pooling in the first, pads 0 or 1");
+    if (!w1) return fail(BNN_ERR_NULL, "input_bconv_bconv2d: w1 is NULL");
+    if (!thr0) return fail(BNN_ERR_NULL, "input_bconv_bconv2d: thr0 is NULL");
+    if (!out_bits) return fail(BNN_ERR_NULL, "input_bconv_bconv2d: out_bits is NULL");
+    if (!aligned16(w1) || !aligned16(w1prep))
+      return fail(BNN_ERR_ALIGN, "input_bconv_bconv2d: w1 and w1prep must be 16-byte aligned");
+    st = check_outputs(x, w0, thr1, nullptr, out_bits);
+    if (st != BNN_OK) return st;
+    return hip_status(bnn::launch_input_bconv_bconv(g0, g1, x, offset, w0, thr0, flip0, w1,
+                                                    w1prep, thr1, flip1, out_bits, stream),
+                      "input_bconv_bconv2d launch");
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "input_bconv_bconv2d: unexpected C++ exception");
+  }
+}
+
 bnn_status bnn_bgemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
                      const uint32_t* B, const int32_t* thr, const uint32_t* flip,
                      int32_t* out_sums, uint32_t* out_bits, hipStream_t stream) {
@@ -623,6 +662,25 @@ bnn_status run_chain(const bnn_layer* layers, int32_t n_layers, int32_t batch, i
     g1.C = layers[1].C;
     fuse_input = g_opt.fuse_input != 0 && bnn::bconv_patch_supported(g1);
   }
+  // Input thresholding, a 3x3 binary conv of 64 or 128 filters over 3
+  // channels and a second 3x3 binary conv run as one kernel that keeps the
+  // first conv's bits in LDS (fconv_bconv.hip; a matrix-core kernel, so not
+  // under the vector-ALU ablation; option fuse_input = 0 keeps all three
+  // apart).
+  bool fuse_input3 = false;
+  bnn::ConvGeom g_in1;
+  if (fuse_input && n_layers > 2 && layers[2].kind == BNN_LAYER_BCONV) {
+    const bnn_layer& l1 = layers[1];
+    const bnn_layer& l2 = layers[2];
+    bnn_conv_desc d1{batch, H, W, l1.C, l1.F, l1.KH, l1.KW, l1.stride, l1.pad, l1.pool};
+    bnn::ConvGeom g2;
+    if (conv_geom(&d1, &g_in1) == BNN_OK) {  // (the chain is validated above)
+      bnn_conv_desc d2{batch, g_in1.Hp, g_in1.Wp, l2.C, l2.F,
+                       l2.KH, l2.KW, l2.stride, l2.pad, l2.pool};
+      fuse_input3 = conv_geom(&d2, &g2) == BNN_OK && use_mfma(g2) &&
+                    bnn::input_bconv_bconv_supported(mode, g_in1, g2);
+    }
+  }
   // A real-valued first layer followed by a 3x3 binary conv that fits runs
   // as one kernel with the first layer's bits in LDS (a matrix-core kernel,
   // so not under the vector-ALU ablation; option fuse_first = 0 keeps the
@@ -674,10 +732,16 @@ bnn_status run_chain(const bnn_layer* layers, int32_t n_layers, int32_t batch, i
         if (l.kind == BNN_LAYER_FCONV_BINW) {
           if (!fuse_first)
             e = bnn::launch_fconv_binw(g, input, l.w, l.thr, l.flip, nullptr, dst, stream);
-        } else if (li == 1 && fuse_first)
+        } else if (li == 1 && fuse_first) {
           e = bnn::launch_fconv_bconv(g_first, g, input, layers[0].w, layers[0].thr,
                                       layers[0].flip, l.w, l.wprep, l.thr, l.flip, dst, stream);
-        else if (li == 1 && fuse_input)
+        } else if (li == 1 && fuse_input3) {
+          // (computed with layer 2)
+        } else if (li == 2 && fuse_input3) {
+          e = bnn::launch_input_bconv_bconv(g_in1, g, input, layers[0].offset, layers[1].w,
+                                            layers[1].thr, layers[1].flip, l.w, l.wprep, l.thr,
+                                            l.flip, dst, stream);
+        } else if (li == 1 && fuse_input)
           e = bnn::launch_bconv_patch(g, mode, input, layers[0].offset, l.w, l.thr, l.flip,
                                       nullptr, dst, stream);
         else

@@ -58,6 +58,7 @@ struct FbArgs {
   int32_t w1_bytes;
   const int32_t* corr1;         // prepared w1 (PREP1): per-filter offsets B_f
   int32_t tiles_w, tiles_h;
+  const float* offset;          // NPART = 1: per-channel thresholds T (or NULL)
 };
 
 constexpr uint32_t kRsrcWord3 = 0x00020000;
@@ -70,7 +71,12 @@ constexpr int64_t kSmallGrid = 128;  // workgroups
 // TH: rows of the second layer's output tile, 8, or 4 on grids too small to
 // fill the chip (half the workgroups' work each, for 1.25 times the
 // first-layer work per output row).
-template <int TH, int C0, int F0, int NFH, bool POOL, bool PREP1>
+// NPART = 3: the first layer is the real-valued one (fp32 input split into
+// three bf16 parts, pad 0.0).  NPART = 1: the first layer is a binary conv
+// over the input thresholded per channel (bit = x + T_c > 0, Sec. II-C), each
+// value +-1.0 in bf16 and the pad -1, exactly the binary conv
+// bnn_bconv2d_input computes with the same thresholds and flips.
+template <int TH, int C0, int F0, int NFH, bool POOL, bool PREP1, int NPART>
 __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
   constexpr int kTH = TH;
   constexpr int kAH = kTH + 2;                // first-layer tile rows
@@ -92,7 +98,7 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
   constexpr int NX = kIH * kIW * C0;  // input values of the tile
   constexpr int XIT = (NX + NT - 1) / NT;
 
-  __shared__ uint16_t xs[3][NX];       // input tile, the three bf16 parts
+  __shared__ uint16_t xs[NPART][NX];   // input tile: the three bf16 parts, or +-1
   __shared__ v8bf wop[FT0][KC0][64];
   // First-layer output bits, each word already expanded to its fp4 operand:
   // word wi of tile pixel (r, c) at r RSX + c PSX + wi.  The spare entry per
@@ -119,7 +125,8 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
 
   // 1. Staging.  Every global load of the stage is issued before the first
   // LDS store, so the block waits for one memory round trip.
-  float xv[XIT];
+  float xv[XIT], xoff[XIT];
+  bool xin[XIT];
 #pragma unroll
   for (int i = 0; i < XIT; ++i) {
     const int e = tid + i * NT;
@@ -127,8 +134,9 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
     const int col = t % kIW, row = t / kIW;
     const int y = y0 + row, x = x0 + col;
     xv[i] = 0.0f;
-    if (e < NX && y >= 0 && y < a.H && x >= 0 && x < a.W)
-      xv[i] = a.in[((static_cast<size_t>(n) * a.H + y) * a.W + x) * C0 + ch];
+    xin[i] = e < NX && y >= 0 && y < a.H && x >= 0 && x < a.W;
+    if (xin[i]) xv[i] = a.in[((static_cast<size_t>(n) * a.H + y) * a.W + x) * C0 + ch];
+    xoff[i] = NPART == 1 && a.offset ? a.offset[ch] : 0.0f;
   }
   // First-layer weights: the 9 words of the filter of each A-operand entry
   // this thread builds (indices clamped, so the loads need no branch).
@@ -174,22 +182,33 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
   // First-layer thresholds as the smallest fp32 value >= thr (-0.0 for a
   // zero threshold): the sign bit of S - th0 is then clear exactly when
   // S >= thr, for every fp32 sum S (thr_ceil_f32).
-  if (tid < F0) th0[tid] = thr_ceil_f32(thr0v);
+  // Binary first layer (NPART = 1): integer sums |S| <= K0, so the
+  // accumulators can start at 0.5 - thr (thr clamped to [-K0-1, K0+1]) and
+  // their sign bit is that of S - thr + 0.5, exact in fp32, with no
+  // subtraction after the MFMAs.
+  if (tid < F0)
+    th0[tid] = NPART == 3 ? thr_ceil_f32(thr0v)
+                          : 0.5f - static_cast<float>(min(max(thr0v, -K0 - 1), K0 + 1));
   if (tid < CW1) fl0[tid] = fl0v;
   // Second-layer start values 0.5 - thr (thr clamped to [-K1-1, K1+1], which
   // keeps every comparison since |S| <= K1); with prepared weights the sums
   // come out B_f too high, so the start value is 0.5 - thr - B_f.
   if (tid < F1)
     th1[tid] = 0.5f - static_cast<float>(min(max(thr1v, -a.K1 - 1), a.K1 + 1) + corr1v);
-  // Each input value split once into its three bf16 parts.
+  // Each input value split once into its three bf16 parts, or thresholded
+  // to +-1 (outside the image: the pad -1).
 #pragma unroll
   for (int i = 0; i < XIT; ++i) {
     const int e = tid + i * NT;
     if (e < NX) {
-      const Split3 sp = split3(xv[i]);
-      xs[0][e] = bf16_bits(sp.p0);
-      xs[1][e] = bf16_bits(sp.p1);
-      xs[2][e] = bf16_bits(sp.p2);
+      if constexpr (NPART == 3) {
+        const Split3 sp = split3(xv[i]);
+        xs[0][e] = bf16_bits(sp.p0);
+        xs[1][e] = bf16_bits(sp.p1);
+        xs[2][e] = bf16_bits(sp.p2);
+      } else {
+        xs[0][e] = xin[i] && xv[i] + xoff[i] > 0.0f ? kBf16One : kBf16MinusOne;
+      }
     }
   }
   __syncthreads();
@@ -232,9 +251,9 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
       const int pp = pv ? p : 0;
       const int lr = pp / kAW, lc = pp - (pp / kAW) * kAW;
       const int base = (lr * kIW + lc) * C0;
-      v8bf xp[3][KC0];
+      v8bf xp[NPART][KC0];
 #pragma unroll
-      for (int pt = 0; pt < 3; ++pt)
+      for (int pt = 0; pt < NPART; ++pt)
 #pragma unroll
         for (int kc = 0; kc < KC0; ++kc) {
           uint16_t v[8];
@@ -248,11 +267,12 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
       // no MFMA waits on the one before it.
       v4f acc[2 * CW1];
 #pragma unroll
-      for (int ft = 0; ft < 2 * CW1; ++ft) acc[ft] = v4f{0.f, 0.f, 0.f, 0.f};
+      for (int ft = 0; ft < 2 * CW1; ++ft)
+        acc[ft] = NPART == 3 ? v4f{0.f, 0.f, 0.f, 0.f} : thv[ft];
 #pragma unroll
       for (int kc = 0; kc < KC0; ++kc)
 #pragma unroll
-        for (int pt = 0; pt < 3; ++pt)
+        for (int pt = 0; pt < NPART; ++pt)
 #pragma unroll
           for (int ft = 0; ft < 2 * CW1; ++ft)
             acc[ft] =
@@ -268,7 +288,8 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
           uint32_t nib = 0u;
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            nib = __builtin_amdgcn_alignbit(nib, __float_as_uint(acc[ft][r] - thv[ft][r]), 31);
+            nib = __builtin_amdgcn_alignbit(
+                nib, __float_as_uint(NPART == 3 ? acc[ft][r] - thv[ft][r] : acc[ft][r]), 31);
           sg[wi] |= nib << (28 - 16 * hf - 4 * q);
         }
       }
@@ -422,56 +443,48 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
   }
 }
 
-template <int TH, int C0, int F0, bool PREP1>
+template <int TH, int C0, int F0, bool PREP1, int NPART>
 hipError_t launch_th(const FbArgs& a, int f1, bool pool, unsigned blocks, hipStream_t s) {
   if (f1 == 128) {
     if (pool)
-      fconv_bconv_kernel<TH, C0, F0, 2, true, PREP1><<<blocks, 64 * TH, 0, s>>>(a);
+      fconv_bconv_kernel<TH, C0, F0, 2, true, PREP1, NPART><<<blocks, 64 * TH, 0, s>>>(a);
     else
-      fconv_bconv_kernel<TH, C0, F0, 2, false, PREP1><<<blocks, 64 * TH, 0, s>>>(a);
+      fconv_bconv_kernel<TH, C0, F0, 2, false, PREP1, NPART><<<blocks, 64 * TH, 0, s>>>(a);
   } else {
     if (pool)
-      fconv_bconv_kernel<TH, C0, F0, 1, true, PREP1><<<blocks, 32 * TH, 0, s>>>(a);
+      fconv_bconv_kernel<TH, C0, F0, 1, true, PREP1, NPART><<<blocks, 32 * TH, 0, s>>>(a);
     else
-      fconv_bconv_kernel<TH, C0, F0, 1, false, PREP1><<<blocks, 32 * TH, 0, s>>>(a);
+      fconv_bconv_kernel<TH, C0, F0, 1, false, PREP1, NPART><<<blocks, 32 * TH, 0, s>>>(a);
   }
   return hipGetLastError();
 }
 
-template <int C0, int F0, bool PREP1>
+template <int C0, int F0, bool PREP1, int NPART>
 hipError_t launch_c0f0(const FbArgs& a, int th, int f1, bool pool, unsigned blocks,
                        hipStream_t s) {
-  return th == 8 ? launch_th<8, C0, F0, PREP1>(a, f1, pool, blocks, s)
-                 : launch_th<4, C0, F0, PREP1>(a, f1, pool, blocks, s);
+  return th == 8 ? launch_th<8, C0, F0, PREP1, NPART>(a, f1, pool, blocks, s)
+                 : launch_th<4, C0, F0, PREP1, NPART>(a, f1, pool, blocks, s);
 }
 
-template <int C0>
+template <int C0, int NPART>
 hipError_t launch_c0(const FbArgs& a, int th, int f0, int f1, bool pool, unsigned blocks,
                      hipStream_t s) {
   if (a.corr1)
-    return f0 == 128 ? launch_c0f0<C0, 128, true>(a, th, f1, pool, blocks, s)
-                     : launch_c0f0<C0, 64, true>(a, th, f1, pool, blocks, s);
-  return f0 == 128 ? launch_c0f0<C0, 128, false>(a, th, f1, pool, blocks, s)
-                   : launch_c0f0<C0, 64, false>(a, th, f1, pool, blocks, s);
+    return f0 == 128 ? launch_c0f0<C0, 128, true, NPART>(a, th, f1, pool, blocks, s)
+                     : launch_c0f0<C0, 64, true, NPART>(a, th, f1, pool, blocks, s);
+  return f0 == 128 ? launch_c0f0<C0, 128, false, NPART>(a, th, f1, pool, blocks, s)
+                   : launch_c0f0<C0, 64, false, NPART>(a, th, f1, pool, blocks, s);
 }
 
-}  // namespace
-
-bool fconv_bconv_supported(const ConvGeom& g0, const ConvGeom& g1) {
-  return g0.KH == 3 && g0.KW == 3 && g0.C >= 1 && g0.C <= 4 && g0.pool == 0 &&
-         (g0.pad == 0 || g0.pad == 1) && (g0.F == 64 || g0.F == 128) &&
-         g1.KH == 3 && g1.KW == 3 && g1.C == g0.F && (g1.pad == 0 || g1.pad == 1) &&
-         (g1.F == 64 || g1.F == 128) && (g1.pool == 0 || g1.pool == 2) &&
-         g1.N == g0.N && g1.H == g0.Ho && g1.W == g0.Wo && g1.Ho >= 1 && g1.Wo >= 1 &&
-         static_cast<int64_t>(g0.N) * g0.H * g0.W * g0.C < (int64_t{1} << 31);
-}
-
-hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const float* in,
-                              const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
-                              const uint32_t* w1, const void* w1prep, const int32_t* thr1,
-                              const uint32_t* flip1, uint32_t* bits, hipStream_t s) {
-  FbArgs a;
+// Kernel arguments and grid shared by both first-layer forms; returns the
+// tile height and the block count.
+void fill_args(FbArgs& a, const ConvGeom& g0, const ConvGeom& g1, const float* in,
+               const float* offset, const uint32_t* w0, const int32_t* thr0,
+               const uint32_t* flip0, const uint32_t* w1, const void* w1prep,
+               const int32_t* thr1, const uint32_t* flip1, uint32_t* bits, int& th,
+               unsigned& blocks) {
   a.in = in;
+  a.offset = offset;
   a.w0 = w0;
   a.thr0 = thr0;
   a.flip0 = flip0;
@@ -484,7 +497,7 @@ hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const floa
   // prepared).
   const int64_t tiles8 =
       int64_t{g0.N} * ((g1.Wo + kTW - 1) / kTW) * ((g1.Ho + 7) / 8);
-  const int th = tiles8 < kSmallGrid ? 4 : 8;
+  th = tiles8 < kSmallGrid ? 4 : 8;
   if (th == 4) w1prep = nullptr;
   a.w1 = w1prep ? static_cast<const uint32_t*>(w1prep) : w1;
   a.thr1 = thr1;
@@ -510,14 +523,52 @@ hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const floa
   }
   a.tiles_w = (g1.Wo + kTW - 1) / kTW;
   a.tiles_h = (g1.Ho + th - 1) / th;
-  const unsigned blocks = static_cast<unsigned>(g0.N) * a.tiles_w * a.tiles_h;
+  blocks = static_cast<unsigned>(g0.N) * a.tiles_w * a.tiles_h;
+}
+
+}  // namespace
+
+bool fconv_bconv_supported(const ConvGeom& g0, const ConvGeom& g1) {
+  return g0.KH == 3 && g0.KW == 3 && g0.C >= 1 && g0.C <= 4 && g0.pool == 0 &&
+         (g0.pad == 0 || g0.pad == 1) && (g0.F == 64 || g0.F == 128) &&
+         g1.KH == 3 && g1.KW == 3 && g1.C == g0.F && (g1.pad == 0 || g1.pad == 1) &&
+         (g1.F == 64 || g1.F == 128) && (g1.pool == 0 || g1.pool == 2) &&
+         g1.N == g0.N && g1.H == g0.Ho && g1.W == g0.Wo && g1.Ho >= 1 && g1.Wo >= 1 &&
+         static_cast<int64_t>(g0.N) * g0.H * g0.W * g0.C < (int64_t{1} << 31);
+}
+
+bool input_bconv_bconv_supported(int mode, const ConvGeom& g0, const ConvGeom& g1) {
+  return mode == BNN_INPUT_THRESHOLD && g0.C == 3 && fconv_bconv_supported(g0, g1);
+}
+
+hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const float* in,
+                              const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
+                              const uint32_t* w1, const void* w1prep, const int32_t* thr1,
+                              const uint32_t* flip1, uint32_t* bits, hipStream_t s) {
+  FbArgs a;
+  int th;
+  unsigned blocks;
+  fill_args(a, g0, g1, in, nullptr, w0, thr0, flip0, w1, w1prep, thr1, flip1, bits, th, blocks);
   const bool pool = g1.pool == 2;
   switch (g0.C) {
-    case 1: return launch_c0<1>(a, th, g0.F, g1.F, pool, blocks, s);
-    case 2: return launch_c0<2>(a, th, g0.F, g1.F, pool, blocks, s);
-    case 3: return launch_c0<3>(a, th, g0.F, g1.F, pool, blocks, s);
-    default: return launch_c0<4>(a, th, g0.F, g1.F, pool, blocks, s);
+    case 1: return launch_c0<1, 3>(a, th, g0.F, g1.F, pool, blocks, s);
+    case 2: return launch_c0<2, 3>(a, th, g0.F, g1.F, pool, blocks, s);
+    case 3: return launch_c0<3, 3>(a, th, g0.F, g1.F, pool, blocks, s);
+    default: return launch_c0<4, 3>(a, th, g0.F, g1.F, pool, blocks, s);
   }
+}
+
+hipError_t launch_input_bconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const float* in,
+                                    const float* offset, const uint32_t* w0,
+                                    const int32_t* thr0, const uint32_t* flip0,
+                                    const uint32_t* w1, const void* w1prep,
+                                    const int32_t* thr1, const uint32_t* flip1,
+                                    uint32_t* bits, hipStream_t s) {
+  FbArgs a;
+  int th;
+  unsigned blocks;
+  fill_args(a, g0, g1, in, offset, w0, thr0, flip0, w1, w1prep, thr1, flip1, bits, th, blocks);
+  return launch_c0<3, 1>(a, th, g0.F, g1.F, g1.pool == 2, blocks, s);
 }
 
 }  // namespace bnn

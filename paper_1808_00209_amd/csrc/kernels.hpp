@@ -109,6 +109,17 @@ hipError_t launch_fconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const floa
                               const uint32_t* flip0, const uint32_t* w1,
                               const void* w1prep, const int32_t* thr1,
                               const uint32_t* flip1, uint32_t* bits, hipStream_t s);
+// The same kernel with the first layer a binary conv over the input
+// thresholded per channel (bnn_bconv2d_input, mode THRESHOLD, 3 channels):
+// input thresholding, the first binary conv and the second in one launch.
+// g0 is the first binary conv (C = 3).
+bool input_bconv_bconv_supported(int mode, const ConvGeom& g0, const ConvGeom& g1);
+hipError_t launch_input_bconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const float* in,
+                                    const float* offset, const uint32_t* w0,
+                                    const int32_t* thr0, const uint32_t* flip0,
+                                    const uint32_t* w1, const void* w1prep,
+                                    const int32_t* thr1, const uint32_t* flip1,
+                                    uint32_t* bits, hipStream_t s);
 
 // A run of consecutive binary FC layers in one launch (bfc_chain.hip): every
 // block takes R rows through all of them with the intermediate bits in LDS.

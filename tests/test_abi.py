@@ -151,6 +151,41 @@ def test_fconv_bconv_errors():
 
 
 @needs_lib
+def test_input_bconv_bconv_errors():
+    lib = bnn.load()
+    d0 = _conv(N=2, H=32, W=32, C=3, F=64)
+    d1 = _conv(N=2, H=32, W=32, C=64, F=64, pool=2)
+
+    def call(a=d0, b=d1, mode=0, x=A, w0=A, thr0=A, w1=A, thr1=A, bits=A):
+        return lib.bnn_input_bconv_bconv2d(ctypes.byref(a), ctypes.byref(b), mode, x, None, w0,
+                                           thr0, None, w1, None, thr1, None, bits, None)
+
+    # modes: unknown, or not thresholding
+    assert call(mode=3) == 2 and "mode" in bnn.last_error()
+    assert call(mode=1) == 4 and "THRESHOLD" in bnn.last_error()
+    assert call(mode=2) == 4
+    # the second layer must read the first one's output
+    assert call(b=_conv(N=2, H=30, W=32, C=64, F=64)) == 2 and "match" in bnn.last_error()
+    assert call(b=_conv(N=2, H=32, W=32, C=128, F=64)) == 2
+    # shapes the fused kernel does not cover: 3 input channels only
+    assert call(a=_conv(N=2, H=32, W=32, C=4, F=64), b=d1) == 4
+    assert call(a=_conv(N=2, H=32, W=32, C=1, F=64), b=d1) == 4
+    assert call(a=_conv(N=2, H=32, W=32, C=3, F=96),
+                b=_conv(N=2, H=32, W=32, C=96, F=64)) == 4
+    assert call(b=_conv(N=2, H=32, W=32, C=64, F=256)) == 4
+    assert call(a=_conv(N=2, H=32, W=32, C=3, F=64, pool=2),
+                b=_conv(N=2, H=16, W=16, C=64, F=64)) == 4
+    # pointers and alignment
+    assert call(x=None) == 1
+    assert call(w1=None) == 1 and "w1" in bnn.last_error()
+    assert call(thr0=None) == 1 and "thr0" in bnn.last_error()
+    assert call(thr1=None) == 1
+    assert call(bits=None) == 1
+    assert call(w1=A + 4) == 3
+    assert call(x=A + 4) == 3
+
+
+@needs_lib
 def test_binarize_input_errors():
     lib = bnn.load()
     assert lib.bnn_binarize_input(5, A, None, 1, 4, 4, 3, A, None) == 2
