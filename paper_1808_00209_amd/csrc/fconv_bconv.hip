@@ -125,18 +125,29 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
 
   // 1. Staging.  Every global load of the stage is issued before the first
   // LDS store, so the block waits for one memory round trip.
-  float xv[XIT], xoff[XIT];
+  // (Addresses clamped into the image, so the loads need no branch and all
+  // issue back to back; values outside the image are replaced afterwards.)
+  float xv[XIT];
   bool xin[XIT];
+  int xch[XIT];
 #pragma unroll
   for (int i = 0; i < XIT; ++i) {
     const int e = tid + i * NT;
     const int ch = e % C0, t = e / C0;
     const int col = t % kIW, row = t / kIW;
     const int y = y0 + row, x = x0 + col;
-    xv[i] = 0.0f;
     xin[i] = e < NX && y >= 0 && y < a.H && x >= 0 && x < a.W;
-    if (xin[i]) xv[i] = a.in[((static_cast<size_t>(n) * a.H + y) * a.W + x) * C0 + ch];
-    xoff[i] = NPART == 1 && a.offset ? a.offset[ch] : 0.0f;
+    xch[i] = ch;
+    const int yc = min(max(y, 0), a.H - 1), xc = min(max(x, 0), a.W - 1);
+    xv[i] = a.in[((static_cast<size_t>(n) * a.H + yc) * a.W + xc) * C0 + ch];
+  }
+  // NPART = 1: the per-channel thresholds (one uniform load each).
+  float off[C0];
+#pragma unroll
+  for (int ch = 0; ch < C0; ++ch) off[ch] = 0.0f;
+  if (NPART == 1 && a.offset) {
+#pragma unroll
+    for (int ch = 0; ch < C0; ++ch) off[ch] = a.offset[ch];
   }
   // First-layer weights: the 9 words of the filter of each A-operand entry
   // this thread builds (indices clamped, so the loads need no branch).
@@ -202,12 +213,15 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
     const int e = tid + i * NT;
     if (e < NX) {
       if constexpr (NPART == 3) {
-        const Split3 sp = split3(xv[i]);
+        const Split3 sp = split3(xin[i] ? xv[i] : 0.0f);
         xs[0][e] = bf16_bits(sp.p0);
         xs[1][e] = bf16_bits(sp.p1);
         xs[2][e] = bf16_bits(sp.p2);
       } else {
-        xs[0][e] = xin[i] && xv[i] + xoff[i] > 0.0f ? kBf16One : kBf16MinusOne;
+        float o = off[0];
+#pragma unroll
+        for (int ch = 1; ch < C0; ++ch) o = xch[i] == ch ? off[ch] : o;
+        xs[0][e] = xin[i] && xv[i] + o > 0.0f ? kBf16One : kBf16MinusOne;
       }
     }
   }
