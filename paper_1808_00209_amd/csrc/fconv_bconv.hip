@@ -96,10 +96,19 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
   constexpr int FW1 = F1 / 32;
 
   constexpr int NX = kIH * kIW * C0;  // input values of the tile
-  constexpr int XIT = (NX + NT - 1) / NT;
+  constexpr int XIT = NPART == 3 ? (NX + NT - 1) / NT : 1;
+  constexpr int NPIX = kIH * kIW;     // input pixels of the tile
+  constexpr int XIP = NPART == 1 ? (NPIX + NT - 1) / NT : 1;
+  static_assert(NPART == 3 || K0 <= 32, "a thresholded window fits one word");
 
-  __shared__ uint16_t xs[NPART][NX];   // input tile: the three bf16 parts, or +-1
-  __shared__ v8bf wop[FT0][KC0][64];
+  // NPART = 3: the input tile as three bf16 parts and the first layer's
+  // operands for v_mfma_f32_16x16x32_bf16.  NPART = 1: each input pixel's
+  // C0 threshold bits (xcode) and each filter's K0 weight bits (wp0), for
+  // v_mfma_scale_f32_32x32x64_f8f6f4 on +-1 fp4 operands.
+  __shared__ uint16_t xs[NPART == 3 ? 3 : 1][NPART == 3 ? NX : 1];
+  __shared__ v8bf wop[NPART == 3 ? FT0 : 1][KC0][64];
+  __shared__ uint32_t xcode[NPART == 1 ? NPIX : 1];
+  __shared__ uint32_t wp0[NPART == 1 ? F0 : 1];
   // First-layer output bits, each word already expanded to its fp4 operand:
   // word wi of tile pixel (r, c) at r RSX + c PSX + wi.  The spare entry per
   // pixel and the row stride (= 4 mod 8 entries) spread the 16-byte reads of
@@ -129,17 +138,32 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
   // issue back to back; values outside the image are replaced afterwards.)
   float xv[XIT];
   bool xin[XIT];
-  int xch[XIT];
+  float pxv[XIP][C0];
+  bool pin[XIP];
+  if constexpr (NPART == 3) {
 #pragma unroll
-  for (int i = 0; i < XIT; ++i) {
-    const int e = tid + i * NT;
-    const int ch = e % C0, t = e / C0;
-    const int col = t % kIW, row = t / kIW;
-    const int y = y0 + row, x = x0 + col;
-    xin[i] = e < NX && y >= 0 && y < a.H && x >= 0 && x < a.W;
-    xch[i] = ch;
-    const int yc = min(max(y, 0), a.H - 1), xc = min(max(x, 0), a.W - 1);
-    xv[i] = a.in[((static_cast<size_t>(n) * a.H + yc) * a.W + xc) * C0 + ch];
+    for (int i = 0; i < XIT; ++i) {
+      const int e = tid + i * NT;
+      const int ch = e % C0, t = e / C0;
+      const int col = t % kIW, row = t / kIW;
+      const int y = y0 + row, x = x0 + col;
+      xin[i] = e < NX && y >= 0 && y < a.H && x >= 0 && x < a.W;
+      const int yc = min(max(y, 0), a.H - 1), xc = min(max(x, 0), a.W - 1);
+      xv[i] = a.in[((static_cast<size_t>(n) * a.H + yc) * a.W + xc) * C0 + ch];
+    }
+  } else {
+    // whole pixels per thread (their C0 values make one code)
+#pragma unroll
+    for (int i = 0; i < XIP; ++i) {
+      const int q = tid + i * NT;
+      const int col = q % kIW, row = q / kIW;
+      const int y = y0 + row, x = x0 + col;
+      pin[i] = q < NPIX && y >= 0 && y < a.H && x >= 0 && x < a.W;
+      const int yc = min(max(y, 0), a.H - 1), xc = min(max(x, 0), a.W - 1);
+      const size_t base = ((static_cast<size_t>(n) * a.H + yc) * a.W + xc) * C0;
+#pragma unroll
+      for (int ch = 0; ch < C0; ++ch) pxv[i][ch] = a.in[base + ch];
+    }
   }
   // NPART = 1: the per-channel thresholds (one uniform load each).
   float off[C0];
@@ -152,12 +176,12 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
   // First-layer weights: the 9 words of the filter of each A-operand entry
   // this thread builds (indices clamped, so the loads need no branch).
   constexpr int NOP = FT0 * KC0 * 64;
-  constexpr int WIT = (NOP + NT - 1) / NT;
+  constexpr int WIT = NPART == 3 ? (NOP + NT - 1) / NT : 1;
   uint32_t w0v[WIT][9];
 #pragma unroll
   for (int i = 0; i < WIT; ++i) {
     const int e = min(tid + i * NT, NOP - 1);
-    const int f = 16 * ((e >> 6) / KC0) + (e & 15);
+    const int f = NPART == 3 ? 16 * ((e >> 6) / KC0) + (e & 15) : min(tid, F0 - 1);
 #pragma unroll
     for (int t = 0; t < 9; ++t) w0v[i][t] = a.w0[f * 9 + t];
   }
@@ -173,7 +197,7 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
 #pragma unroll
   for (int i = 0; i < WIT; ++i) {
     const int e = tid + i * NT;
-    if (e < NOP) {
+    if (NPART == 3 && e < NOP) {
       const int l = e & 63, kc = (e >> 6) % KC0, ft = (e >> 6) / KC0;
       const int q = l >> 4;
       KBits bits = 0;
@@ -189,6 +213,14 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
       }
       wop[ft][kc][l] = bf16x8(op);
     }
+  }
+  // NPART = 1: filter tid's K0 weight bits, element k = C0 tap + ch at bit
+  // 31 - k (the unused low bits 0).
+  if (NPART == 1 && tid < F0) {
+    uint32_t pw = 0u;
+#pragma unroll
+    for (int t = 0; t < 9; ++t) pw |= (w0v[0][t] >> (32 - C0)) << (32 - (t + 1) * C0);
+    wp0[tid] = pw;
   }
   // First-layer thresholds as the smallest fp32 value >= thr (-0.0 for a
   // zero threshold): the sign bit of S - th0 is then clear exactly when
@@ -206,23 +238,29 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
   // come out B_f too high, so the start value is 0.5 - thr - B_f.
   if (tid < F1)
     th1[tid] = 0.5f - static_cast<float>(min(max(thr1v, -a.K1 - 1), a.K1 + 1) + corr1v);
-  // Each input value split once into its three bf16 parts, or thresholded
-  // to +-1 (outside the image: the pad -1).
+  // Each input value split once into its three bf16 parts, or each input
+  // pixel thresholded into its code: bit C0 - 1 - ch = (x_ch + T_ch > 0);
+  // outside the image the code is 0, the pad -1.
+  if constexpr (NPART == 3) {
 #pragma unroll
-  for (int i = 0; i < XIT; ++i) {
-    const int e = tid + i * NT;
-    if (e < NX) {
-      if constexpr (NPART == 3) {
+    for (int i = 0; i < XIT; ++i) {
+      const int e = tid + i * NT;
+      if (e < NX) {
         const Split3 sp = split3(xin[i] ? xv[i] : 0.0f);
         xs[0][e] = bf16_bits(sp.p0);
         xs[1][e] = bf16_bits(sp.p1);
         xs[2][e] = bf16_bits(sp.p2);
-      } else {
-        float o = off[0];
-#pragma unroll
-        for (int ch = 1; ch < C0; ++ch) o = xch[i] == ch ? off[ch] : o;
-        xs[0][e] = xin[i] && xv[i] + o > 0.0f ? kBf16One : kBf16MinusOne;
       }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < XIP; ++i) {
+      const int q = tid + i * NT;
+      uint32_t code = 0u;
+#pragma unroll
+      for (int ch = 0; ch < C0; ++ch)
+        code |= static_cast<uint32_t>(pin[i] && pxv[i][ch] + off[ch] > 0.0f) << (C0 - 1 - ch);
+      if (q < NPIX) xcode[q] = code;
     }
   }
   __syncthreads();
@@ -233,7 +271,7 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
 
   // 2. First layer on the (TH + 2) x 34 tile: lane (q, c) = (l / 16, l % 16) holds
   // pixel c of a 16-pixel tile and filters 16 ft + 4 q + r (r = 0..3).
-  {
+  if constexpr (NPART == 3) {
     const int q = lane >> 4, c = lane & 15;
     // Offsets of this lane's k values from the window's first input value;
     // k >= K0 reuses offset 0 (its weight is 0).
@@ -317,6 +355,92 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
       if (q < CW1 && pv) {
         const v8i x = PREP1 ? act_operand(word, smask, vfill) : expand_fp4(word, smask, vfill);
         actx[lr * RSX + lc * PSX + q] = v4i{x[0], x[1], x[2], x[3]};
+      }
+    }
+  } else {
+    // NPART = 1, 32 pixels per round on the fp4 matrix cores: lane (h, c)
+    // holds pixel c and, as operands, K half h of the window (h = 0: the
+    // K0 <= 32 bits, k = C0 tap + ch at bit 31 - k, as +-1 fp4; h = 1:
+    // zeros) and of filter 32 tf + c.  Result register e of lane (h, c):
+    // filter 32 tf + 8 (e / 4) + 4 h + e % 4 at pixel c.  Positions past K0
+    // are 0.0 in the weights, so their products vanish.
+    const int h = lane >> 5, c = lane & 31;
+    constexpr int kATiles32 = (kAPix + 31) / 32;
+    v8i wa1[CW1];
+#pragma unroll
+    for (int tf = 0; tf < CW1; ++tf) {
+      const v8i x = expand_fp4(wp0[32 * tf + c], smask, vfill);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        // nibble n of register r is bit 4 n + r: clear the bits below 32 - K0
+        uint32_t m = 0xFFFFFFFFu;
+#pragma unroll
+        for (int bb = r; bb < 32 - K0; bb += 4) m &= ~(0xFu << (4 * (bb / 4)));
+        wa1[tf][r] = h ? 0 : static_cast<int>(static_cast<uint32_t>(x[r]) & m);
+      }
+#pragma unroll
+      for (int r = 4; r < 8; ++r) wa1[tf][r] = 0;
+    }
+    // After the lane-half exchange, lane half h holds the word of tile h
+    // (and of tile 2 + h when CW1 = 4).
+    const uint32_t nfl0 = ~fl0[h];
+    const uint32_t nfl1 = ~fl0[CW1 == 4 ? 2 + h : h];
+    for (int pt = wave; pt < kATiles32; pt += NW) {
+      const int p = 32 * pt + c;
+      const bool pv = p < kAPix;
+      const int pp = pv ? p : 0;
+      const int lr = pp / kAW, lc = pp - (pp / kAW) * kAW;
+      uint32_t patch = 0u;
+#pragma unroll
+      for (int kh = 0; kh < 3; ++kh)
+#pragma unroll
+        for (int kw = 0; kw < 3; ++kw)
+          patch |= xcode[(lr + kh) * kIW + lc + kw] << (32 - (3 * kh + kw + 1) * C0);
+      v8i B = expand_fp4(patch, smask, vfill);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) B[r] = h ? 0 : B[r];
+      uint32_t wd[CW1];
+#pragma unroll
+      for (int tf = 0; tf < CW1; ++tf) {
+        v16f t;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const v4f q4 = *reinterpret_cast<const v4f*>(&th0[32 * tf + 8 * g + 4 * h]);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) t[4 * g + r] = q4[r];
+        }
+        const v16f acc =
+            __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wa1[tf], B, t, 4, 4, 0, 127, 0, 127);
+        // sign bits of S - thr + 0.5: filter 8 g + 4 h + r at bit 31 - 8 g - 4 h - r
+        wd[tf] = 0u;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          uint32_t nib = 0u;
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            nib = __builtin_amdgcn_alignbit(nib, __float_as_uint(acc[4 * g + r]), 31);
+          wd[tf] |= nib << (28 - 8 * g - 4 * h);
+        }
+      }
+      const auto s01 = __builtin_amdgcn_permlane32_swap(wd[0], wd[1], false, false);
+      uint32_t wlo = s01[0] | s01[1], whi = 0u;
+      if constexpr (CW1 == 4) {
+        const auto s23 = __builtin_amdgcn_permlane32_swap(wd[2], wd[3], false, false);
+        whi = s23[0] | s23[1];
+      }
+      const int rr = r0 + lr, cc = c0 + lc;
+      const bool inside = pv && rr >= 0 && rr < a.Ho0 && cc >= 0 && cc < a.Wo0;
+      // Output bit = (S >= thr) xor flip = sign xor ~flip.
+      if (pv) {
+        const uint32_t w0w = inside ? wlo ^ nfl0 : 0u;
+        const v8i x0 = PREP1 ? act_operand(w0w, smask, vfill) : expand_fp4(w0w, smask, vfill);
+        actx[lr * RSX + lc * PSX + h] = v4i{x0[0], x0[1], x0[2], x0[3]};
+        if constexpr (CW1 == 4) {
+          const uint32_t w1w = inside ? whi ^ nfl1 : 0u;
+          const v8i x1 =
+              PREP1 ? act_operand(w1w, smask, vfill) : expand_fp4(w1w, smask, vfill);
+          actx[lr * RSX + lc * PSX + 2 + h] = v4i{x1[0], x1[1], x1[2], x1[3]};
+        }
       }
     }
   }
