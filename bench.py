@@ -150,15 +150,34 @@ def layer_shapes(layers, H, W, C, batch=None):
                        and L0["F"] in (64, 128) and L0["pad"] in (0, 1)
                        and L1["KH"] == L1["KW"] == 3 and L1["F"] in (64, 128)
                        and L1["pad"] in (0, 1) and L1.get("pool", 0) in (0, 2))
-        if fused_first and batch is not None:
-            # bnn_forward fuses from 32 workgroups of 8 x 32 output pixels on
-            Ho1 = H + 2 * L0["pad"] - 2 + 2 * L1["pad"] - 2
-            Wo1 = W + 2 * L0["pad"] - 2 + 2 * L1["pad"] - 2
-            fused_first = batch * ((Ho1 + 7) // 8) * ((Wo1 + 31) // 32) >= 32
+    # bnn_forward's thresholded input + binary 3x3 conv + binary 3x3 conv in
+    # one kernel (bnn_input_bconv_bconv2d)
+    fused_input3 = False
+    if fused and first == "input_threshold" and len(layers) > 2 and layers[2]["kind"] == "bconv":
+        L1, L2 = layers[1], layers[2]
+        fused_input3 = (C == 3 and L1["KH"] == L1["KW"] == 3 and L1["F"] in (64, 128)
+                        and L1["pad"] in (0, 1) and not L1.get("pool", 0)
+                        and L2["KH"] == L2["KW"] == 3 and L2["F"] in (64, 128)
+                        and L2["pad"] in (0, 1) and L2.get("pool", 0) in (0, 2))
     for li, L in enumerate(layers):
         k = L["kind"]
         if k in INPUT_MODES and fused:
             continue  # runs inside the next layer's patch-packing kernel
+        if k == "bconv" and li == 1 and fused_input3:
+            continue  # runs inside the next layer's fused kernel
+        if k == "bconv" and li == 2 and fused_input3:
+            L1 = layers[1]
+            Ho1, Wo1 = h + 2 * L1["pad"] - 2, w + 2 * L1["pad"] - 2
+            pad, F, pool = L["pad"], L["F"], L.get("pool", 0)
+            Ho, Wo = Ho1 + 2 * pad - 2, Wo1 + 2 * pad - 2
+            name = "L0-L2 threshold+bconv+bconv %dx%dx%d->%d->%d k3%s (fused)" % (
+                h, w, c, L1["F"], F, " pool" if pool else "")
+            out.append((name, "input_bconv_bconv",
+                        dict(H=h, W=w, C=c, F0=L1["F"], pad0=L1["pad"], Ho0=Ho1, Wo0=Wo1,
+                             F=F, KH=3, KW=3, pad=pad, pool=pool, li=li),
+                        Ho1 * Wo1 * L1["F"] * 9 * c + Ho * Wo * F * 9 * L1["F"]))
+            h, w, c = (Ho // 2, Wo // 2, F) if pool else (Ho, Wo, F)
+            continue
         if k == "fconv" and fused_first:
             continue  # runs inside the fused first-layer kernel
         if k == "bconv" and li == 1 and fused_first:
@@ -210,7 +229,7 @@ def algorithmic_bytes(kind, g, batch):
     the first layer), packed weights, thresholds, flips and packed output
     bits.  No im2col copies, no re-reads."""
     wd = lambda n: (n + 31) // 32
-    if kind == "fconv_bconv":
+    if kind in ("fconv_bconv", "input_bconv_bconv"):
         Ho, Wo = g["Ho0"] + 2 * g["pad"] - 2, g["Wo0"] + 2 * g["pad"] - 2
         Hp, Wp = (Ho // 2, Wo // 2) if g["pool"] else (Ho, Wo)
         x = batch * g["H"] * g["W"] * 4 * g["C"]
@@ -367,6 +386,19 @@ def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
         fn = lambda: bnn.bnn_fconv_bconv2d(d0, d1, x, l0["w"], l0["thr"], l0.get("flip"),
                                            l1["w"], l1["thr"], l1.get("flip"), out_bits=ob,
                                            w1prep=l1.get("wprep"))
+    elif kind == "input_bconv_bconv":
+        d0 = bnn.conv_desc(batch, g["H"], g["W"], g["C"], g["F0"], 3, 3, 1, g["pad0"], 0)
+        d1 = bnn.conv_desc(batch, g["Ho0"], g["Wo0"], g["F0"], g["F"], 3, 3, 1, g["pad"],
+                           g["pool"])
+        Ho, Wo, Hp, Wp = bnn.bnn_conv_output_dims(d1)
+        ob = torch.empty((batch, Hp, Wp, bnn.words(g["F"])), dtype=torch.int32, device="cuda")
+        x = torch.randint(0, 256, (batch, g["H"], g["W"], g["C"]), device="cuda",
+                          generator=gen).to(torch.float32)
+        l0, l1, l2 = dev_layer
+        fn = lambda: bnn.bnn_input_bconv_bconv2d(d0, d1, bnn.INPUT_THRESHOLD, x, l0.get("offset"),
+                                                 l1["w"], l1["thr"], l1.get("flip"), l2["w"],
+                                                 l2["thr"], l2.get("flip"), out_bits=ob,
+                                                 w1prep=l2.get("wprep"))
     elif kind in ("fconv", "bconv"):
         desc = bnn.conv_desc(batch, g["H"], g["W"], g["C"], g["F"], g["KH"], g["KW"], 1,
                              g["pad"], g["pool"])
@@ -430,10 +462,12 @@ def per_layer_rows(bnn, torch, layers, shapes, batch, reps):
     rows = []
     for name, kind, g, macs in shapes:
         dl = ((dev_layers[0], dev_layers[1]) if kind in ("bconv_input", "fconv_bconv")
+              else tuple(dev_layers[:3]) if kind == "input_bconv_bconv"
               else dev_layers[g["li"]])
         ms = time_layer(bnn, kind, g, batch, dl, reps, torch)
         ms_valu = None
-        if kind != "fconv_bconv":  # a matrix-core kernel only (no vector-ALU form)
+        # (the fused kernels are matrix-core kernels only: no vector-ALU form)
+        if kind not in ("fconv_bconv", "input_bconv_bconv"):
             with bnn.options(algo=bnn.ALGO_VALU):
                 ms_valu = time_layer(bnn, kind, g, batch, dl, reps, torch)
         row = {"layer": name, "ms": round(ms, 5),
@@ -708,6 +742,9 @@ def main():
         # the binary second layer on fp4 MFMA is the counted work; the fused
         # fp32 first layer (bf16 MFMA on three parts of x) is reported beside it
         dom_ops, bound, peak, unit = 2 * macs * batch, "mfma", MFMA_FP4_PEAK_TFLOPS, "TFLOP/s"
+    elif kind == "input_bconv_bconv":
+        # both binary convs on fp4 MFMA (the thresholding is part of staging)
+        dom_ops, bound, peak, unit = 2 * macs * batch, "mfma", MFMA_FP4_PEAK_TFLOPS, "TFLOP/s"
     elif kind in ("bconv", "bfc", "bfc_logits") and (g.get("C", g.get("K", 0)) % 64 == 0) \
             and not (kind != "bconv" and batch <= 16):
         # binary layer on fp4 MFMA: one fp4 multiply-accumulate per bit-MAC
@@ -744,7 +781,8 @@ def main():
         "config": {"workload": args.workload, "batch": batch, "input": "%dx%dx%d fp32" % (H, W, C),
                    "binary_ops_per_step": ops_per_step},
         "images_per_s": round(batch / (ms_per_step * 1e-3), 1),
-        "launch": "bnn_forward: one kernel per layer, the first two layers fused into one",
+        "launch": "bnn_forward: one kernel per layer, the first two layers (the vehicle-shaped "
+                  "net: the input thresholding and the first two convs) fused into one",
         "hip_graph": {"ms_per_step": round(ms_graph, 5),
                       "value": round(ops_per_step / (ms_graph * 1e-3) / 1e9, 1),
                       "batch1_mean_us": round(float(per_img_us_graph.mean()), 3)},
