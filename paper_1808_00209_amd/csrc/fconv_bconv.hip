@@ -62,7 +62,7 @@ struct FbArgs {
 };
 
 constexpr uint32_t kRsrcWord3 = 0x00020000;
-constexpr int64_t kSmallGrid = 128;  // workgroups
+constexpr int64_t kCUs = 256;  // compute units of the chip
 
 // PREP1: w1 holds the second layer's weights in the prepared operand form
 // (bnn_prepare_weights: 16-byte entries [F1 / 32][9][F0 / 32][32], then the
@@ -77,14 +77,18 @@ constexpr int64_t kSmallGrid = 128;  // workgroups
 // value +-1.0 in bf16 and the pad -1, exactly the binary conv
 // bnn_bconv2d_input computes with the same thresholds and flips.
 template <int TH, int C0, int F0, int NFH, bool POOL, bool PREP1, int NPART>
-__global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
+__global__ __launch_bounds__(256 * NFH) void fconv_bconv_kernel(FbArgs a) {
   constexpr int kTH = TH;
   constexpr int kAH = kTH + 2;                // first-layer tile rows
   constexpr int kIH = kAH + 2;                // input tile rows
   constexpr int kAPix = kAH * kAW;            // 340 (TH = 8), 204 (TH = 4)
   constexpr int kATiles = (kAPix + 15) / 16;  // 16-pixel tiles of the first layer
   constexpr int PG = TH / 2;                  // 64-pixel groups of the second layer
-  constexpr int NW = PG * NFH;                // waves
+  constexpr int NW2 = PG * NFH;               // second-layer waves
+  // With 4-row tiles (small grids) the block has twice as many waves as the
+  // second layer uses: the staging and the first layer spread over all of
+  // them, the extra ones then stop.
+  constexpr int NW = TH == 4 ? 2 * NW2 : NW2;  // waves
   constexpr int NT = 64 * NW;                 // threads
   constexpr int K0 = 9 * C0;
   constexpr int KC0 = (K0 + 31) / 32;  // first-layer k-chunks of 32
@@ -447,6 +451,7 @@ __global__ __launch_bounds__(32 * TH * NFH) void fconv_bconv_kernel(FbArgs a) {
   __syncthreads();
 
   // 3. Second layer: wave = pixel group pg (64 pixels) x filter half fh.
+  if (wave >= NW2) return;  // (no barrier follows)
   const int pg = wave % PG, fh = wave / PG;
   const int h = lane >> 5, c = lane & 31;
   const int f0 = 64 * fh;
@@ -585,14 +590,14 @@ template <int TH, int C0, int F0, bool PREP1, int NPART>
 hipError_t launch_th(const FbArgs& a, int f1, bool pool, unsigned blocks, hipStream_t s) {
   if (f1 == 128) {
     if (pool)
-      fconv_bconv_kernel<TH, C0, F0, 2, true, PREP1, NPART><<<blocks, 64 * TH, 0, s>>>(a);
+      fconv_bconv_kernel<TH, C0, F0, 2, true, PREP1, NPART><<<blocks, 512, 0, s>>>(a);
     else
-      fconv_bconv_kernel<TH, C0, F0, 2, false, PREP1, NPART><<<blocks, 64 * TH, 0, s>>>(a);
+      fconv_bconv_kernel<TH, C0, F0, 2, false, PREP1, NPART><<<blocks, 512, 0, s>>>(a);
   } else {
     if (pool)
-      fconv_bconv_kernel<TH, C0, F0, 1, true, PREP1, NPART><<<blocks, 32 * TH, 0, s>>>(a);
+      fconv_bconv_kernel<TH, C0, F0, 1, true, PREP1, NPART><<<blocks, 256, 0, s>>>(a);
     else
-      fconv_bconv_kernel<TH, C0, F0, 1, false, PREP1, NPART><<<blocks, 32 * TH, 0, s>>>(a);
+      fconv_bconv_kernel<TH, C0, F0, 1, false, PREP1, NPART><<<blocks, 256, 0, s>>>(a);
   }
   return hipGetLastError();
 }
@@ -626,16 +631,19 @@ void fill_args(FbArgs& a, const ConvGeom& g0, const ConvGeom& g1, const float* i
   a.w0 = w0;
   a.thr0 = thr0;
   a.flip0 = flip0;
-  // 8-row tiles, or 4-row tiles where 8-row tiles would leave more than
-  // half of the 256 compute units idle (CIFAR L0 + L1 at batch 1: 7.70
-  // against 7.97 us).  Prepared second-layer weights only with 8-row tiles:
-  // on the small grids the 4x larger operands come from beyond L2 and the
-  // packed words are faster (batch 1 / 16: 7.25 / 7.70 us packed against
-  // 7.77 / 8.11 prepared; batch 32 / 64: 8.98 / 9.74 packed, 8.70 / 9.36
-  // prepared).
+  // 8-row tiles, or 4-row tiles (blocks of twice the waves for the staging
+  // and the first layer) where those still fit one workgroup per compute
+  // unit: CIFAR L0 + L1 at batch 1 / 32 take 6.2 / 7.0 us with 4-row tiles
+  // against 8.0 / 8.8 us with 8-row ones, at batch 48 / 64 11.0 / 11.3
+  // against 9.2 / 9.5 us.  Prepared second-layer weights only with 8-row
+  // tiles: on the small grids the 4x larger operands come from beyond L2
+  // and the packed words are faster (batch 1 / 16: 7.25 / 7.70 us packed
+  // against 7.77 / 8.11 prepared, measured with 4-row tiles of the block's
+  // own waves only; batch 32 / 64 with 8-row tiles: 8.98 / 9.74 packed,
+  // 8.70 / 9.36 prepared).
   const int64_t tiles8 =
       int64_t{g0.N} * ((g1.Wo + kTW - 1) / kTW) * ((g1.Ho + 7) / 8);
-  th = tiles8 < kSmallGrid ? 4 : 8;
+  th = 2 * tiles8 <= kCUs ? 4 : 8;
   if (th == 4) w1prep = nullptr;
   a.w1 = w1prep ? static_cast<const uint32_t*>(w1prep) : w1;
   a.thr1 = thr1;
