@@ -45,13 +45,13 @@ _FP4 = ("paper_1808_00209_amd/csrc/fp4_expand.hpp",
 _LANE = ("paper_1808_00209_amd/csrc/lane_ops.hpp",
          "96ece7042c6ed72e9cd799fdd8e007525e30035bbd8d052a9ece380c5e3fda82")
 _KERN = ("paper_1808_00209_amd/csrc/kernels.hpp",
-         "6ff0b384ee272b0a0f05b0dc5f0d03bc7994e1fe108f4d06bc066fb8652ebbf2")
+         "75b55b2430a784f32576e9d322c1d0fb9f9e8f807d4416d32188e764e6d2d083")
 MEASURED_TRAFFIC = {
     # profiles/fconv_bconv_cifar_b64.md
     ("cifar_bnn_b64", "L0+L1 fconv+bconv 32x32x3->128->128 k3 pool (fused)"): dict(
-        fetch_kib=904.7, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
+        fetch_kib=980.7, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/fconv_bconv.hip",
-                       "7ced5f651797ed566b799fea7a057d712aa9f3ab31e7e71c0ea6694199df2f6c"),
+                       "b9775a39d56ce451c281b54dceafe567d2fc9cc81ff7a7752a4c1a83d8de96f3"),
                       ("paper_1808_00209_amd/csrc/fp32_split.hpp",
                        "7f3a9f6b25af5be34fb5b304976e0225cd491d935c5a4e567bc43c134b6ceb13"),
                       _FP4, _LANE, _KERN]), flags=_FLAGS),
@@ -59,7 +59,7 @@ MEASURED_TRAFFIC = {
     ("cifar_bnn_b64", "L5 bconv 8x8x512->512 k3 pool"): dict(
         fetch_kib=4806.0, write_kib=64.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/bconv_mfma.hip",
-                       "430e988963e1a69883cfa46ec7a72a2f16f4332250770061e08135ab39f09c52"),
+                       "577fcd293919a87dfc1693ed6e1822c4c76eb2fa47e901fc1dd7c0566802b975"),
                       _FP4, _LANE, _KERN]), flags=_FLAGS),
 }
 
