@@ -133,6 +133,16 @@ def net_input(cfg, batch):
     return synth.cfg3_input(batch) if cfg == 3 else synth.cfg4_input(batch)
 
 
+def pair_fusable(L0, L1, w, c):
+    """Whether bnn_forward runs these two binary convs as one kernel
+    (bnn_bconv_bconv2d): 3x3, pad 1, 256 filters each on a 16-wide map,
+    64 / 128 / 256 input channels, no pooling in the first."""
+    return (L0["KH"] == L0["KW"] == 3 and L0["pad"] == 1 and not L0.get("pool", 0)
+            and w == 16 and c in (64, 128, 256) and L0["F"] == 256
+            and L1["KH"] == L1["KW"] == 3 and L1["pad"] == 1 and L1["F"] == 256
+            and L1.get("pool", 0) in (0, 2))
+
+
 def layer_shapes(layers, H, W, C, batch=None):
     """Per layer: (name, kind, geometry dict, bit-MACs per image), with the
     kernels bnn_forward launches at `batch` (fused first layers included)."""
@@ -159,8 +169,11 @@ def layer_shapes(layers, H, W, C, batch=None):
                         and L1["pad"] in (0, 1) and not L1.get("pool", 0)
                         and L2["KH"] == L2["KW"] == 3 and L2["F"] in (64, 128)
                         and L2["pad"] in (0, 1) and L2.get("pool", 0) in (0, 2))
+    paired = set()  # second convs of the pairs bnn_forward runs as one kernel
     for li, L in enumerate(layers):
         k = L["kind"]
+        if li in paired:
+            continue
         if k in INPUT_MODES and fused:
             continue  # runs inside the next layer's patch-packing kernel
         if k == "bconv" and li == 1 and fused_input3:
@@ -208,6 +221,19 @@ def layer_shapes(layers, H, W, C, batch=None):
         if k in INPUT_MODES:
             out.append(("L%d %s %dx%dx%d" % (li, k, h, w, c), k, dict(H=h, W=w, C=c, li=li), 0))
             c = 1 if k == "input_gray" else (3 if k == "input_lbp" else c)
+        elif (k == "bconv" and li + 1 < len(layers) and layers[li + 1]["kind"] == "bconv"
+              and pair_fusable(L, layers[li + 1], w, c)):
+            # bnn_forward's two 3x3 binary convs in one kernel (bnn_bconv_bconv2d)
+            L1 = layers[li + 1]
+            F0, F, pool = L["F"], L1["F"], L1.get("pool", 0)
+            name = "L%d+L%d bconv+bconv %dx%dx%d->%d->%d k3%s (fused)" % (
+                li, li + 1, h, w, c, F0, F, " pool" if pool else "")
+            out.append((name, "bconv_bconv",
+                        dict(H=h, W=w, C=c, F0=F0, pad0=1, Ho0=h, Wo0=w, F=F, KH=3, KW=3, pad=1,
+                             pool=pool, li=li),
+                        h * w * F0 * 9 * c + h * w * F * 9 * F0))
+            paired.add(li + 1)
+            h, w, c = (h // 2, w // 2, F) if pool else (h, w, F)
         elif k in ("fconv", "bconv"):
             KH, KW, pad, F = L["KH"], L["KW"], L["pad"], L["F"]
             Ho, Wo = h + 2 * pad - KH + 1, w + 2 * pad - KW + 1
@@ -229,10 +255,10 @@ def algorithmic_bytes(kind, g, batch):
     the first layer), packed weights, thresholds, flips and packed output
     bits.  No im2col copies, no re-reads."""
     wd = lambda n: (n + 31) // 32
-    if kind in ("fconv_bconv", "input_bconv_bconv"):
+    if kind in ("fconv_bconv", "input_bconv_bconv", "bconv_bconv"):
         Ho, Wo = g["Ho0"] + 2 * g["pad"] - 2, g["Wo0"] + 2 * g["pad"] - 2
         Hp, Wp = (Ho // 2, Wo // 2) if g["pool"] else (Ho, Wo)
-        x = batch * g["H"] * g["W"] * 4 * g["C"]
+        x = batch * g["H"] * g["W"] * 4 * (wd(g["C"]) if kind == "bconv_bconv" else g["C"])
         w = g["F0"] * 9 * 4 * wd(g["C"]) + g["F"] * 9 * 4 * wd(g["F0"])
         tf = 4 * (g["F0"] + g["F"]) + 4 * (wd(g["F0"]) + wd(g["F"]))
         return x + w + tf + batch * Hp * Wp * 4 * wd(g["F"])
@@ -399,6 +425,16 @@ def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
                                                  l1["w"], l1["thr"], l1.get("flip"), l2["w"],
                                                  l2["thr"], l2.get("flip"), out_bits=ob,
                                                  w1prep=l2.get("wprep"))
+    elif kind == "bconv_bconv":
+        d0 = bnn.conv_desc(batch, g["H"], g["W"], g["C"], g["F0"], 3, 3, 1, 1, 0)
+        d1 = bnn.conv_desc(batch, g["H"], g["W"], g["F0"], g["F"], 3, 3, 1, 1, g["pool"])
+        Ho, Wo, Hp, Wp = bnn.bnn_conv_output_dims(d1)
+        ob = torch.empty((batch, Hp, Wp, bnn.words(g["F"])), dtype=torch.int32, device="cuda")
+        x = torch.randint(-2 ** 31, 2 ** 31 - 1, (batch, g["H"], g["W"], bnn.words(g["C"])),
+                          dtype=torch.int32, device="cuda", generator=gen)
+        l0, l1 = dev_layer
+        fn = lambda: bnn.bnn_bconv_bconv2d(d0, d1, x, l0["w"], l0["thr"], l0.get("flip"),
+                                           l1["w"], l1["thr"], l1.get("flip"), out_bits=ob)
     elif kind in ("fconv", "bconv"):
         desc = bnn.conv_desc(batch, g["H"], g["W"], g["C"], g["F"], g["KH"], g["KW"], 1,
                              g["pad"], g["pool"])
@@ -463,11 +499,20 @@ def per_layer_rows(bnn, torch, layers, shapes, batch, reps):
     for name, kind, g, macs in shapes:
         dl = ((dev_layers[0], dev_layers[1]) if kind in ("bconv_input", "fconv_bconv")
               else tuple(dev_layers[:3]) if kind == "input_bconv_bconv"
+              else (dev_layers[g["li"]], dev_layers[g["li"] + 1]) if kind == "bconv_bconv"
               else dev_layers[g["li"]])
         ms = time_layer(bnn, kind, g, batch, dl, reps, torch)
         ms_valu = None
-        # (the fused kernels are matrix-core kernels only: no vector-ALU form)
-        if kind not in ("fconv_bconv", "input_bconv_bconv"):
+        # (the fused first-layer kernels are matrix-core kernels only: no
+        # vector-ALU form; a fused conv pair's ablation is its two convs on
+        # the vector ALU)
+        if kind == "bconv_bconv":
+            g0 = dict(H=g["H"], W=g["W"], C=g["C"], F=g["F0"], KH=3, KW=3, pad=1, pool=0)
+            g1 = dict(H=g["H"], W=g["W"], C=g["F0"], F=g["F"], KH=3, KW=3, pad=1, pool=g["pool"])
+            with bnn.options(algo=bnn.ALGO_VALU):
+                ms_valu = (time_layer(bnn, "bconv", g0, batch, dl[0], reps, torch)
+                           + time_layer(bnn, "bconv", g1, batch, dl[1], reps, torch))
+        elif kind not in ("fconv_bconv", "input_bconv_bconv"):
             with bnn.options(algo=bnn.ALGO_VALU):
                 ms_valu = time_layer(bnn, kind, g, batch, dl, reps, torch)
         row = {"layer": name, "ms": round(ms, 5),
@@ -742,7 +787,7 @@ def main():
         # the binary second layer on fp4 MFMA is the counted work; the fused
         # fp32 first layer (bf16 MFMA on three parts of x) is reported beside it
         dom_ops, bound, peak, unit = 2 * macs * batch, "mfma", MFMA_FP4_PEAK_TFLOPS, "TFLOP/s"
-    elif kind == "input_bconv_bconv":
+    elif kind in ("input_bconv_bconv", "bconv_bconv"):
         # both binary convs on fp4 MFMA (the thresholding is part of staging)
         dom_ops, bound, peak, unit = 2 * macs * batch, "mfma", MFMA_FP4_PEAK_TFLOPS, "TFLOP/s"
     elif kind in ("bconv", "bfc", "bfc_logits") and (g.get("C", g.get("K", 0)) % 64 == 0) \
@@ -781,8 +826,9 @@ def main():
         "config": {"workload": args.workload, "batch": batch, "input": "%dx%dx%d fp32" % (H, W, C),
                    "binary_ops_per_step": ops_per_step},
         "images_per_s": round(batch / (ms_per_step * 1e-3), 1),
-        "launch": "bnn_forward: one kernel per layer, the first two layers (the vehicle-shaped "
-                  "net: the input thresholding and the first two convs) fused into one",
+        "launch": "bnn_forward: one kernel per layer, with the first two layers (the "
+                  "vehicle-shaped net: the input thresholding and the first two convs) and "
+                  "the 16x16 pair of 256-filter convs each fused into one",
         "hip_graph": {"ms_per_step": round(ms_graph, 5),
                       "value": round(ops_per_step / (ms_graph * 1e-3) / 1e9, 1),
                       "batch1_mean_us": round(float(per_img_us_graph.mean()), 3)},

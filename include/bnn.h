@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define BNN_ABI_VERSION 6
+#define BNN_ABI_VERSION 7
 
 typedef enum bnn_status {
   BNN_OK = 0,
@@ -116,6 +116,9 @@ typedef struct bnn_options {
   int32_t late_thresholds; /* thresholds staged after the main loop: -1      */
                            /* heuristic (default), 0 at kernel start where   */
                            /* the variant allows, 1 after the loop           */
+  int32_t fuse_pair;       /* bnn_forward: two 3x3 BCONVs that fit           */
+                           /* bnn_bconv_bconv2d as one kernel (1, default)   */
+                           /* or two (0)                                     */
 } bnn_options;
 
 /* The default options. */
@@ -352,6 +355,33 @@ bnn_status bnn_input_bconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc*
                                   hipStream_t stream);
 
 /*
+ * Two binary 3x3 convs in one launch (Eq. 3 and Eq. 4 with the threshold,
+ * flip and pool epilogue of bnn_bconv2d, twice; a conv -> conv step of
+ * Table II's layer order), the first conv's output bits never leaving the
+ * chip.  The result equals bnn_bconv2d(d0) followed by bnn_bconv2d(d1), bit
+ * for bit.
+ *   d0        the first conv: W = 16, pad 1, 3x3, C = 64, 128 or 256,
+ *             F = 256, no pooling.
+ *   d1        the second: N, H, W equal to d0's N and output Ho, Wo; 3x3,
+ *             pad 1, C = F = 256, pool 0 or 2.
+ *   x         [N][H][16][C / 32] u32, the first conv's packed input bits.
+ *   w0, thr0, flip0   the first conv's packed weights [256][3][3][C / 32],
+ *             int32 thresholds [256] and flip words [8] (flip0 may be NULL).
+ *   w1, thr1, flip1   the second conv's [256][3][3][8], [256], [8] (flip1
+ *             may be NULL).
+ *   out_bits  [N][Hp][Wp][8] u32, the second conv's bits.
+ * Shapes outside the above give BNN_ERR_UNSUPPORTED.  x, w0, w1 and
+ * out_bits 16-byte aligned.  Errors: BNN_ERR_NULL, BNN_ERR_SHAPE,
+ * BNN_ERR_ALIGN, BNN_ERR_UNSUPPORTED, BNN_ERR_HIP.
+ */
+bnn_status bnn_bconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc* d1,
+                             const uint32_t* x, const uint32_t* w0,
+                             const int32_t* thr0, const uint32_t* flip0,
+                             const uint32_t* w1, const int32_t* thr1,
+                             const uint32_t* flip1, uint32_t* out_bits,
+                             hipStream_t stream);
+
+/*
  * Binary fully-connected layer / GEMM (Sec. III-B, Eq. 4):
  *   S[m][n] = K - 2 * sum_j popcount(A[m][j] XOR B[n][j])   (valid bits only)
  *   A         [M][Kw] u32, Kw = ceil(K / 32): M packed input vectors.
@@ -412,7 +442,7 @@ bnn_status bnn_forward_workspace_size(const bnn_layer* layers,
 /*
  * Run the chain on input [batch][H][W][C] fp32 and write int32 logits
  * [batch][N_last] (Table I/II: conv, pool, ..., FC layers).  One kernel per
- * layer on `stream`, with three exceptions:
+ * layer on `stream`, with four exceptions:
  *  - an INPUT_THRESHOLD layer of 3 channels followed by two 3x3 BCONVs of
  *    64 or 128 filters (the first without pooling) runs as one kernel
  *    (bnn_input_bconv_bconv2d); otherwise an input layer followed by a BCONV
@@ -422,6 +452,9 @@ bnn_status bnn_forward_workspace_size(const bnn_layer* layers,
  *    pooling) followed by a 3x3 BCONV of 64 or 128 filters runs as one
  *    kernel that keeps the first layer's bits in LDS (bnn_fconv_bconv2d;
  *    option fuse_first = 0 keeps them apart);
+ *  - two consecutive BCONVs that fit bnn_bconv_bconv2d (3x3, pad 1, 256
+ *    filters each, on a 16-pixel-wide map) run as that one kernel (option
+ *    fuse_pair = 0 keeps them apart);
  *  - a run of 2-4 consecutive FC layers of at most 8192 weight words each,
  *    at batch <= 128, runs as one kernel that keeps the intermediate bits of
  *    each row in LDS (option fc_chain = 0 launches them one by one).

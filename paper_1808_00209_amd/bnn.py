@@ -37,7 +37,7 @@ EXPORTED = ["bnn_last_error", "bnn_abi_version", "bnn_default_options", "bnn_set
             "bnn_get_options", "bnn_pack_bits", "bnn_conv_output_dims",
             "bnn_bconv2d", "bnn_prepared_weights_size", "bnn_prepare_weights",
             "bnn_bconv2d_prepared", "bnn_fconv2d_binw", "bnn_binarize_input", "bnn_bconv2d_input",
-            "bnn_fconv_bconv2d", "bnn_input_bconv_bconv2d", "bnn_bgemm",
+            "bnn_fconv_bconv2d", "bnn_input_bconv_bconv2d", "bnn_bconv_bconv2d", "bnn_bgemm",
             "bnn_forward_workspace_size", "bnn_forward", "bnn_forward_noalloc"]
 
 # Bytes of bnn_forward_noalloc's per-GPU scratch array (BNN_FORWARD_SCRATCH_BYTES).
@@ -58,7 +58,7 @@ class Options(ctypes.Structure):
     """bnn_options: the calling thread's kernel selection (never changes a result)."""
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("algo", "fuse_input", "fuse_first", "fc_chain", "conv1x1", "xcd_order",
-                 "gemv_max_rows", "lds_weights", "late_thresholds")]
+                 "gemv_max_rows", "lds_weights", "late_thresholds", "fuse_pair")]
 
 
 class ConvDesc(ctypes.Structure):
@@ -109,6 +109,8 @@ def load(path: str = LIB_PATH):
                                       P, P, P, P, P, P, P, P, P, P]
     lib.bnn_input_bconv_bconv2d.argtypes = [ctypes.POINTER(ConvDesc), ctypes.POINTER(ConvDesc),
                                             i32, P, P, P, P, P, P, P, P, P, P, P]
+    lib.bnn_bconv_bconv2d.argtypes = [ctypes.POINTER(ConvDesc), ctypes.POINTER(ConvDesc),
+                                      P, P, P, P, P, P, P, P, P]
     lib.bnn_forward_workspace_size.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32,
                                                ctypes.POINTER(ctypes.c_size_t)]
     lib.bnn_forward.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32, P, P,
@@ -388,6 +390,29 @@ def bnn_input_bconv_bconv2d(desc0: ConvDesc, desc1: ConvDesc, mode, x, offset, w
                                        _ptr(x), _ptr(offset), _ptr(w0), _ptr(thr0), _ptr(flip0),
                                        _ptr(w1), _ptr(w1prep), _ptr(thr1), _ptr(flip1),
                                        _ptr(out_bits), _stream(stream)))
+    return out_bits
+
+
+def bnn_bconv_bconv2d(desc0: ConvDesc, desc1: ConvDesc, x, w0, thr0, flip0, w1, thr1,
+                      flip1=None, out_bits=None, stream=None):
+    """Two binary 3x3 convs in one launch, the first conv's bits kept on
+    chip: returns the second conv's packed bits [N, Hp, Wp, F1/32], the same
+    as bnn_bconv2d(desc0) followed by bnn_bconv2d(desc1)."""
+    lib = load()
+    _, _, Hp, Wp = bnn_conv_output_dims(desc1)
+    _u32(x)
+    _u32(w0)
+    _u32(w1)
+    thr0 = _dev(thr0, torch.int32, "thr0")
+    thr1 = _dev(thr1, torch.int32, "thr1")
+    flip0 = _dev(flip0, torch.int32, "flip0")
+    flip1 = _dev(flip1, torch.int32, "flip1")
+    if out_bits is None:
+        out_bits = torch.empty((desc1.N, Hp, Wp, words(desc1.F)), dtype=torch.int32,
+                               device=x.device)
+    _check(lib.bnn_bconv_bconv2d(ctypes.byref(desc0), ctypes.byref(desc1), _ptr(x), _ptr(w0),
+                                 _ptr(thr0), _ptr(flip0), _ptr(w1), _ptr(thr1), _ptr(flip1),
+                                 _ptr(out_bits), _stream(stream)))
     return out_bits
 
 

@@ -29,6 +29,7 @@ bnn_options default_options() {
   o.gemv_max_rows = 2;
   o.lds_weights = -1;
   o.late_thresholds = -1;
+  o.fuse_pair = 1;
   return o;
 }
 
@@ -214,13 +215,13 @@ bnn_status bnn_set_options(const bnn_options* o) {
       !flag(o->fuse_first) || !flag(o->fc_chain) || !flag(o->conv1x1) ||
       o->xcd_order < 0 || o->xcd_order > 2 ||
       o->gemv_max_rows < 0 || o->gemv_max_rows > 16 || !tri(o->lds_weights) ||
-      !tri(o->late_thresholds))
+      !tri(o->late_thresholds) || !flag(o->fuse_pair))
     return fail(BNN_ERR_SHAPE,
                 "set_options: out of range (algo %d, fuse_input %d, fuse_first %d, fc_chain %d, "
                 "conv1x1 %d, xcd_order %d, gemv_max_rows %d, lds_weights %d, "
-                "late_thresholds %d)",
+                "late_thresholds %d, fuse_pair %d)",
                 o->algo, o->fuse_input, o->fuse_first, o->fc_chain, o->conv1x1, o->xcd_order,
-                o->gemv_max_rows, o->lds_weights, o->late_thresholds);
+                o->gemv_max_rows, o->lds_weights, o->late_thresholds, o->fuse_pair);
   g_opt = *o;
   return ok();
 }
@@ -468,6 +469,40 @@ bnn_status bnn_input_bconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc*
                       "input_bconv_bconv2d launch");
   } catch (...) {
     return fail(BNN_ERR_HIP, "input_bconv_bconv2d: unexpected C++ exception");
+  }
+}
+
+bnn_status bnn_bconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc* d1, const uint32_t* x,
+                             const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
+                             const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
+                             uint32_t* out_bits, hipStream_t stream) {
+  try {
+    bnn::ConvGeom g0, g1;
+    bnn_status st = conv_geom(d0, &g0);
+    if (st != BNN_OK) return st;
+    st = conv_geom(d1, &g1);
+    if (st != BNN_OK) return st;
+    if (g1.N != g0.N || g1.H != g0.Hp || g1.W != g0.Wp || g1.C != g0.F)
+      return fail(BNN_ERR_SHAPE,
+                  "bconv_bconv2d: second conv input %dx%dx%dx%d does not match the first "
+                  "conv's output %dx%dx%dx%d",
+                  g1.N, g1.H, g1.W, g1.C, g0.N, g0.Hp, g0.Wp, g0.F);
+    if (!bnn::bconv_bconv_supported(g0, g1))
+      return fail(BNN_ERR_UNSUPPORTED,
+                  "bconv_bconv2d: needs 3x3 convs with pad 1 on 16-pixel-wide images, the "
+                  "first with 64, 128 or 256 channels, 256 filters and no pooling, the second "
+                  "with 256 filters");
+    if (!w1) return fail(BNN_ERR_NULL, "bconv_bconv2d: w1 is NULL");
+    if (!thr0) return fail(BNN_ERR_NULL, "bconv_bconv2d: thr0 is NULL");
+    if (!out_bits) return fail(BNN_ERR_NULL, "bconv_bconv2d: out_bits is NULL");
+    if (!aligned16(w1)) return fail(BNN_ERR_ALIGN, "bconv_bconv2d: w1 must be 16-byte aligned");
+    st = check_outputs(x, w0, thr1, nullptr, out_bits);
+    if (st != BNN_OK) return st;
+    return hip_status(bnn::launch_bconv_bconv(g0, g1, x, w0, thr0, flip0, w1, thr1, flip1,
+                                              out_bits, stream),
+                      "bconv_bconv2d launch");
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "bconv_bconv2d: unexpected C++ exception");
   }
 }
 
@@ -729,6 +764,33 @@ bnn_status run_chain(const bnn_layer* layers, int32_t n_layers, int32_t batch, i
                         l.KH, l.KW, l.stride, l.pad, l.pool};
         bnn::ConvGeom g;
         conv_geom(&d, &g);
+        // Two 3x3 binary convs on a 16-pixel-wide map that fit one kernel
+        // run as one, the first conv's bits kept in LDS (a matrix-core
+        // kernel, so not under the vector-ALU ablation; option fuse_pair = 0
+        // launches them apart).
+        const bool handled = (li == 1 && (fuse_first || fuse_input || fuse_input3)) ||
+                             (li == 2 && fuse_input3);
+        bnn::ConvGeom g2;
+        bool pair = false;
+        if (!handled && l.kind == BNN_LAYER_BCONV && g_opt.fuse_pair != 0 &&
+            li + 1 < n_layers && layers[li + 1].kind == BNN_LAYER_BCONV && use_mfma(g)) {
+          const bnn_layer& l2 = layers[li + 1];
+          bnn_conv_desc d2{batch, g.Hp, g.Wp, l2.C, l2.F, l2.KH, l2.KW, l2.stride, l2.pad, l2.pool};
+          pair = conv_geom(&d2, &g2) == BNN_OK && use_mfma(g2) &&
+                 bnn::bconv_bconv_supported(g, g2);
+        }
+        if (pair) {
+          const bnn_layer& l2 = layers[li + 1];
+          e = bnn::launch_bconv_bconv(g, g2, src, l.w, l.thr, l.flip, l2.w, l2.thr, l2.flip, dst,
+                                      stream);
+          if (e != hipSuccess) return fail(BNN_ERR_HIP, "forward: layers %d-%d launch: %s", li,
+                                           li + 1, hipGetErrorString(e));
+          h = g2.Hp;
+          w = g2.Wp;
+          c = l2.F;
+          ++li;  // the pair's second conv; its output is in dst
+          break;
+        }
         if (l.kind == BNN_LAYER_FCONV_BINW) {
           if (!fuse_first)
             e = bnn::launch_fconv_binw(g, input, l.w, l.thr, l.flip, nullptr, dst, stream);

@@ -121,6 +121,17 @@ hipError_t launch_input_bconv_bconv(const ConvGeom& g0, const ConvGeom& g1, cons
                                     const int32_t* thr1, const uint32_t* flip1,
                                     uint32_t* bits, hipStream_t s);
 
+// Two consecutive binary 3x3 convs in one launch (bconv_bconv.hip), the first
+// conv's output bits kept in LDS: 16-pixel-wide images, pad 1 in both, the
+// first with 64, 128 or 256 input channels, 256 filters and no pooling, the
+// second with 256 filters and optional 2x2 pooling.  Packed weights; writes
+// the second conv's packed bits; both thr must be non-null.
+bool bconv_bconv_supported(const ConvGeom& g0, const ConvGeom& g1);
+hipError_t launch_bconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const uint32_t* in,
+                              const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
+                              const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
+                              uint32_t* bits, hipStream_t s);
+
 // A run of consecutive binary FC layers in one launch (bfc_chain.hip): every
 // block takes R rows through all of them with the intermediate bits in LDS.
 // Layer i has K_i input bits and N_i outputs; K_{i+1} = N_i; every layer but

@@ -186,6 +186,49 @@ def test_input_bconv_bconv_errors():
 
 
 @needs_lib
+def test_bconv_bconv_errors():
+    """bnn_bconv_bconv2d: shape chaining, the shapes its kernel covers, NULL
+    pointers and alignment, all refused on the host before any launch."""
+    lib = bnn.load()
+    d0 = _conv(N=2, H=16, W=16, C=128, F=256, pad=1)
+    d1 = _conv(N=2, H=16, W=16, C=256, F=256, pad=1, pool=2)
+
+    def call(a=d0, b=d1, x=A, w0=A, thr0=A, w1=A, thr1=A, bits=A):
+        return lib.bnn_bconv_bconv2d(ctypes.byref(a), ctypes.byref(b), x, w0, thr0, None, w1,
+                                     thr1, None, bits, None)
+
+    assert lib.bnn_bconv_bconv2d(None, ctypes.byref(d1), A, A, A, None, A, A, None, A,
+                                 None) == 1
+    # the second conv must read the first one's output
+    assert call(b=_conv(N=2, H=14, W=16, C=256, F=256, pad=1)) == 2 and "match" in bnn.last_error()
+    assert call(b=_conv(N=1, H=16, W=16, C=256, F=256, pad=1)) == 2
+    assert call(b=_conv(N=2, H=16, W=16, C=128, F=256, pad=1)) == 2
+    # shapes the kernel does not cover
+    assert call(a=_conv(N=2, H=8, W=8, C=256, F=256, pad=1),
+                b=_conv(N=2, H=8, W=8, C=256, F=256, pad=1)) == 4
+    assert call(a=_conv(N=2, H=16, W=16, C=96, F=256, pad=1)) == 4
+    assert call(a=_conv(N=2, H=16, W=16, C=128, F=128, pad=1),
+                b=_conv(N=2, H=16, W=16, C=128, F=256, pad=1)) == 4
+    assert call(b=_conv(N=2, H=16, W=16, C=256, F=512, pad=1)) == 4
+    assert call(a=_conv(N=2, H=16, W=16, C=128, F=256, pad=0),
+                b=_conv(N=2, H=14, W=14, C=256, F=256, pad=1)) == 4
+    assert call(b=_conv(N=2, H=16, W=16, C=256, F=256, pad=0)) == 4
+    assert call(a=_conv(N=2, H=16, W=16, C=128, F=256, pad=1, pool=2),
+                b=_conv(N=2, H=8, W=8, C=256, F=256, pad=1)) == 4
+    # pointers and alignment
+    assert call(x=None) == 1
+    assert call(w0=None) == 1
+    assert call(w1=None) == 1 and "w1" in bnn.last_error()
+    assert call(thr0=None) == 1 and "thr0" in bnn.last_error()
+    assert call(thr1=None) == 1
+    assert call(bits=None) == 1
+    assert call(w1=A + 4) == 3
+    assert call(w0=A + 4) == 3
+    assert call(x=A + 4) == 3
+    assert call(bits=A + 4) == 3
+
+
+@needs_lib
 def test_binarize_input_errors():
     lib = bnn.load()
     assert lib.bnn_binarize_input(5, A, None, 1, 4, 4, 3, A, None) == 2
@@ -303,7 +346,8 @@ def test_options_defaults_set_get_and_range_checks():
     lib = bnn.load()
     d = bnn.bnn_default_options()
     assert (d.algo, d.fuse_input, d.fuse_first, d.fc_chain, d.conv1x1, d.xcd_order,
-            d.gemv_max_rows, d.lds_weights, d.late_thresholds) == (0, 1, 1, 1, 1, 1, 2, -1, -1)
+            d.gemv_max_rows, d.lds_weights, d.late_thresholds,
+            d.fuse_pair) == (0, 1, 1, 1, 1, 1, 2, -1, -1, 1)
     try:
         bnn.bnn_set_options(algo=bnn.ALGO_VALU, gemv_max_rows=16, lds_weights=1)
         got = bnn.bnn_get_options()
@@ -311,7 +355,8 @@ def test_options_defaults_set_get_and_range_checks():
         for field, bad in [("algo", 2), ("fuse_input", 2), ("fuse_first", -1), ("fc_chain", 3),
                            ("conv1x1", 2), ("xcd_order", -1), ("xcd_order", 3),
                            ("gemv_max_rows", 17),
-                           ("gemv_max_rows", -1), ("lds_weights", 2), ("late_thresholds", -2)]:
+                           ("gemv_max_rows", -1), ("lds_weights", 2), ("late_thresholds", -2),
+                           ("fuse_pair", 2), ("fuse_pair", -1)]:
             with pytest.raises(bnn.BnnError, match="out of range"):
                 bnn.bnn_set_options(**{field: bad})
             got = bnn.bnn_get_options()

@@ -106,6 +106,15 @@ def _packed(a):
     return oracle.pack_eq2(a)
 
 
+def _pair_fusable(L0, L1, w, c):
+    """The conv pairs bnn_bconv_bconv2d takes (and bnn_forward fuses): 3x3,
+    pad 1, 256 filters each, a 16-wide map, 64 / 128 / 256 input channels,
+    no pooling in the first."""
+    return (L0["KH"] == L0["KW"] == 3 and L0["pad"] == 1 and not L0.get("pool", 0)
+            and w == 16 and c in (64, 128, 256) and L0["F"] == 256
+            and L1["KH"] == L1["KW"] == 3 and L1["pad"] == 1 and L1["F"] == 256)
+
+
 @pytest.mark.parametrize("cfg,batch", [(3, 64), (4, 256)], ids=["cifar_b64", "vehicle_b256"])
 def test_every_layer_bits_at_full_batch(cfg, batch, algo):
     layers, x, outs = _chain_oracle(cfg, batch)
@@ -113,6 +122,7 @@ def test_every_layer_bits_at_full_batch(cfg, batch, algo):
     dev = [upload_layer(L) for L in layers]
     xd = to_device(x)
     h, w = H, W
+    descs = {}
     for li, L in enumerate(layers):
         k = L["kind"]
         print("cfg%d batch %d layer %d (%s), %s" % (cfg, batch, li, k, algo), flush=True)
@@ -144,6 +154,16 @@ def test_every_layer_bits_at_full_batch(cfg, batch, algo):
                                               d["w"], d["thr"], d.get("flip"), want_sums=False)
                 torch.cuda.synchronize()
                 assert np.array_equal(words_u32(pb), _packed(outs[li])), "patch L0+L1"
+            # the conv pair bnn_forward runs as one kernel (bnn_bconv_bconv2d)
+            p = descs.get(li - 1)
+            if (k == "bconv" and p is not None and layers[li - 1]["kind"] == "bconv"
+                    and algo != "valu" and _pair_fusable(layers[li - 1], L, p.W, p.C)):
+                dp = dev[li - 1]
+                pb = bnn.bnn_bconv_bconv2d(p, desc, pack_pm1(outs[li - 2]), dp["w"], dp["thr"],
+                                           dp.get("flip"), d["w"], d["thr"], d.get("flip"))
+                torch.cuda.synchronize()
+                assert np.array_equal(words_u32(pb), _packed(outs[li])), "fused pair %d" % li
+            descs[li] = desc
             Ho, Wo, Hp, Wp = bnn.bnn_conv_output_dims(desc)
             h, w = Hp, Wp
             continue
