@@ -243,11 +243,30 @@ def layer_shapes(layers, H, W, C, batch=None):
             out.append((name, k, dict(H=h, W=w, C=c, F=F, KH=KH, KW=KW, pad=pad, pool=pool, li=li),
                         0 if k == "fconv" else macs))
             h, w, c = (Ho // 2, Wo // 2, F) if pool else (Ho, Wo, F)
+        elif (k == "bfc" and batch is not None and batch > 2 and li + 1 < len(layers)
+              and layers[li + 1]["kind"] in ("bfc", "bfc_logits")
+              and L["K"] in (512, 1024) and L["N"] in (256, 512, 1024)
+              and layers[li + 1]["N"] <= 32 and not fc_chained(layers, li, batch)):
+            # bnn_forward's two FC layers in one kernel (bnn_bfc_pair)
+            L1 = layers[li + 1]
+            K, N0, N1 = L["K"], L["N"], L1["N"]
+            out.append(("L%d+L%d %s+%s %d->%d->%d (fused)" % (li, li + 1, k, L1["kind"], K, N0, N1),
+                        "bfc_pair", dict(K=K, N0=N0, N=N1, logits=L1["kind"] == "bfc_logits", li=li),
+                        K * N0 + N0 * N1))
+            paired.add(li + 1)
+            h, w, c = 1, 1, N1
         else:
             K, N = L["K"], L["N"]
             out.append(("L%d %s %d->%d" % (li, k, K, N), k, dict(K=K, N=N, li=li), K * N))
             h, w, c = 1, 1, N
     return out
+
+
+def fc_chained(layers, li, batch):
+    """Whether bnn_forward's chained small-FC kernel takes layer li with the
+    next (each layer at most 8192 weight words, at most 128 rows)."""
+    small = lambda q: q["kind"] in ("bfc", "bfc_logits") and q["N"] * ((q["K"] + 31) // 32) <= 8192
+    return (batch <= 128 and li + 1 < len(layers) and small(layers[li]) and small(layers[li + 1]))
 
 
 def algorithmic_bytes(kind, g, batch):
@@ -270,6 +289,12 @@ def algorithmic_bytes(kind, g, batch):
                                        else 4 * g.get("cin", g["C"]))
         w = g["F"] * g["KH"] * g["KW"] * 4 * wd(g["C"])
         return x + w + 4 * g["F"] + 4 * wd(g["F"]) + batch * Hp * Wp * 4 * wd(g["F"])
+    if kind == "bfc_pair":
+        x = batch * 4 * wd(g["K"]) + g["N0"] * 4 * wd(g["K"]) + 4 * g["N0"] + 4 * wd(g["N0"])
+        x += g["N"] * 4 * wd(g["N0"])
+        if g["logits"]:
+            return x + batch * 4 * g["N"]
+        return x + 4 * g["N"] + 4 * wd(g["N"]) + batch * 4 * wd(g["N"])
     if kind in ("bfc", "bfc_logits"):
         x = batch * 4 * wd(g["K"]) + g["N"] * 4 * wd(g["K"])
         if kind == "bfc":
@@ -455,6 +480,15 @@ def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
             else:
                 fn = lambda: bnn.bnn_bconv2d(desc, x, dev_layer["w"], dev_layer["thr"],
                                              dev_layer.get("flip"), want_sums=False, out_bits=ob)
+    elif kind == "bfc_pair":
+        A = torch.randint(-2 ** 31, 2 ** 31 - 1, (batch, bnn.words(g["K"])), dtype=torch.int32,
+                          device="cuda", generator=gen)
+        l0, l1 = dev_layer
+        ob = torch.empty((batch, g["N"]) if g["logits"] else (batch, 1), dtype=torch.int32,
+                         device="cuda")
+        fn = lambda: bnn.bnn_bfc_pair(A, g["K"], l0["w"], l0["thr"], l0.get("flip"), l1["w"], g["N"],
+                                      None if g["logits"] else l1["thr"],
+                                      None if g["logits"] else l1.get("flip"), out=ob)
     else:
         A = torch.randint(-2 ** 31, 2 ** 31 - 1, (batch, bnn.words(g["K"])), dtype=torch.int32,
                           device="cuda", generator=gen)
@@ -499,7 +533,8 @@ def per_layer_rows(bnn, torch, layers, shapes, batch, reps):
     for name, kind, g, macs in shapes:
         dl = ((dev_layers[0], dev_layers[1]) if kind in ("bconv_input", "fconv_bconv")
               else tuple(dev_layers[:3]) if kind == "input_bconv_bconv"
-              else (dev_layers[g["li"]], dev_layers[g["li"] + 1]) if kind == "bconv_bconv"
+              else (dev_layers[g["li"]], dev_layers[g["li"] + 1]) if kind in ("bconv_bconv",
+                                                                             "bfc_pair")
               else dev_layers[g["li"]])
         ms = time_layer(bnn, kind, g, batch, dl, reps, torch)
         ms_valu = None
@@ -512,6 +547,13 @@ def per_layer_rows(bnn, torch, layers, shapes, batch, reps):
             with bnn.options(algo=bnn.ALGO_VALU):
                 ms_valu = (time_layer(bnn, "bconv", g0, batch, dl[0], reps, torch)
                            + time_layer(bnn, "bconv", g1, batch, dl[1], reps, torch))
+        elif kind == "bfc_pair":
+            g0 = dict(K=g["K"], N=g["N0"])
+            g1 = dict(K=g["N0"], N=g["N"])
+            with bnn.options(algo=bnn.ALGO_VALU):
+                ms_valu = (time_layer(bnn, "bfc", g0, batch, dl[0], reps, torch)
+                           + time_layer(bnn, "bfc_logits" if g["logits"] else "bfc", g1, batch,
+                                        dl[1], reps, torch))
         elif kind not in ("fconv_bconv", "input_bconv_bconv"):
             with bnn.options(algo=bnn.ALGO_VALU):
                 ms_valu = time_layer(bnn, kind, g, batch, dl, reps, torch)
@@ -787,7 +829,7 @@ def main():
         # the binary second layer on fp4 MFMA is the counted work; the fused
         # fp32 first layer (bf16 MFMA on three parts of x) is reported beside it
         dom_ops, bound, peak, unit = 2 * macs * batch, "mfma", MFMA_FP4_PEAK_TFLOPS, "TFLOP/s"
-    elif kind in ("input_bconv_bconv", "bconv_bconv"):
+    elif kind in ("input_bconv_bconv", "bconv_bconv") or (kind == "bfc_pair" and batch > 16):
         # both binary convs on fp4 MFMA (the thresholding is part of staging)
         dom_ops, bound, peak, unit = 2 * macs * batch, "mfma", MFMA_FP4_PEAK_TFLOPS, "TFLOP/s"
     elif kind in ("bconv", "bfc", "bfc_logits") and (g.get("C", g.get("K", 0)) % 64 == 0) \

@@ -117,8 +117,9 @@ typedef struct bnn_options {
                            /* heuristic (default), 0 at kernel start where   */
                            /* the variant allows, 1 after the loop           */
   int32_t fuse_pair;       /* bnn_forward: two 3x3 BCONVs that fit           */
-                           /* bnn_bconv_bconv2d as one kernel (1, default)   */
-                           /* or two (0)                                     */
+                           /* bnn_bconv_bconv2d, or two FC layers that fit   */
+                           /* bnn_bfc_pair, as one kernel (1, default) or    */
+                           /* two (0)                                        */
 } bnn_options;
 
 /* The default options. */
@@ -382,6 +383,34 @@ bnn_status bnn_bconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc* d1,
                              hipStream_t stream);
 
 /*
+ * Two binary FC layers in one launch (Sec. III-B, Eq. 4 twice), the first
+ * layer's output bits never leaving the chip: out = layer 1 (layer 0 (A)),
+ * layer 0 with its threshold and flip as in bnn_bgemm, layer 1 to int32 sums
+ * (out_sums, e.g. the logits) or to bits (out_bits, with thr1).  The result
+ * equals two bnn_bgemm calls, bit for bit.
+ *   M         rows (>= 1, at most 2^26).
+ *   K0        layer 0's input bits: 512 or 1024.
+ *   N0        layer 0's outputs = layer 1's input bits: 256, 512 or 1024.
+ *   N1        layer 1's outputs: 1..32.
+ *   A         [M][K0 / 32] u32 packed rows.
+ *   w0, thr0, flip0   layer 0's packed weights [N0][K0 / 32], int32
+ *             thresholds [N0], flip words [N0 / 32] (flip0 may be NULL).
+ *   w1, thr1, flip1   layer 1's [N1][N0 / 32], [N1], [1]; thr1 and flip1
+ *             are read only for out_bits (flip1 may be NULL).
+ *   out_sums  [M][N1] int32, or NULL;  out_bits  [M][1] u32 (tail bits 0),
+ *             or NULL: exactly one of the two.
+ * Shapes outside the above give BNN_ERR_UNSUPPORTED.  A, w0, w1 and the
+ * output 16-byte aligned.  Errors: BNN_ERR_NULL, BNN_ERR_SHAPE (also both
+ * outputs given), BNN_ERR_ALIGN, BNN_ERR_UNSUPPORTED, BNN_ERR_HIP.
+ */
+bnn_status bnn_bfc_pair(int64_t M, int64_t K0, int64_t N0, int64_t N1,
+                        const uint32_t* A, const uint32_t* w0,
+                        const int32_t* thr0, const uint32_t* flip0,
+                        const uint32_t* w1, const int32_t* thr1,
+                        const uint32_t* flip1, int32_t* out_sums,
+                        uint32_t* out_bits, hipStream_t stream);
+
+/*
  * Binary fully-connected layer / GEMM (Sec. III-B, Eq. 4):
  *   S[m][n] = K - 2 * sum_j popcount(A[m][j] XOR B[n][j])   (valid bits only)
  *   A         [M][Kw] u32, Kw = ceil(K / 32): M packed input vectors.
@@ -453,7 +482,9 @@ bnn_status bnn_forward_workspace_size(const bnn_layer* layers,
  *    kernel that keeps the first layer's bits in LDS (bnn_fconv_bconv2d;
  *    option fuse_first = 0 keeps them apart);
  *  - two consecutive BCONVs that fit bnn_bconv_bconv2d (3x3, pad 1, 256
- *    filters each, on a 16-pixel-wide map) run as that one kernel (option
+ *    filters each, on a 16-pixel-wide map) run as that one kernel, and so do
+ *    two consecutive FC layers that fit bnn_bfc_pair, are not part of a
+ *    chained run and have more rows than option gemv_max_rows (option
  *    fuse_pair = 0 keeps them apart);
  *  - a run of 2-4 consecutive FC layers of at most 8192 weight words each,
  *    at batch <= 128, runs as one kernel that keeps the intermediate bits of

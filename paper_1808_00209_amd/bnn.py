@@ -37,7 +37,7 @@ EXPORTED = ["bnn_last_error", "bnn_abi_version", "bnn_default_options", "bnn_set
             "bnn_get_options", "bnn_pack_bits", "bnn_conv_output_dims",
             "bnn_bconv2d", "bnn_prepared_weights_size", "bnn_prepare_weights",
             "bnn_bconv2d_prepared", "bnn_fconv2d_binw", "bnn_binarize_input", "bnn_bconv2d_input",
-            "bnn_fconv_bconv2d", "bnn_input_bconv_bconv2d", "bnn_bconv_bconv2d", "bnn_bgemm",
+            "bnn_fconv_bconv2d", "bnn_input_bconv_bconv2d", "bnn_bconv_bconv2d", "bnn_bfc_pair", "bnn_bgemm",
             "bnn_forward_workspace_size", "bnn_forward", "bnn_forward_noalloc"]
 
 # Bytes of bnn_forward_noalloc's per-GPU scratch array (BNN_FORWARD_SCRATCH_BYTES).
@@ -111,6 +111,7 @@ def load(path: str = LIB_PATH):
                                             i32, P, P, P, P, P, P, P, P, P, P, P]
     lib.bnn_bconv_bconv2d.argtypes = [ctypes.POINTER(ConvDesc), ctypes.POINTER(ConvDesc),
                                       P, P, P, P, P, P, P, P, P]
+    lib.bnn_bfc_pair.argtypes = [i64, i64, i64, i64, P, P, P, P, P, P, P, P, P, P]
     lib.bnn_forward_workspace_size.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32,
                                                ctypes.POINTER(ctypes.c_size_t)]
     lib.bnn_forward.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32, P, P,
@@ -414,6 +415,29 @@ def bnn_bconv_bconv2d(desc0: ConvDesc, desc1: ConvDesc, x, w0, thr0, flip0, w1, 
                                  _ptr(thr0), _ptr(flip0), _ptr(w1), _ptr(thr1), _ptr(flip1),
                                  _ptr(out_bits), _stream(stream)))
     return out_bits
+
+
+def bnn_bfc_pair(A, K0, w0, thr0, flip0, w1, N1, thr1=None, flip1=None, out=None,
+                 stream=None):
+    """Two binary FC layers in one launch: layer 0 (K0 -> N0 outputs, its
+    threshold and flip) then layer 1 (N0 -> N1 <= 32).  With thr1 None the
+    result is layer 1's int32 sums [M, N1]; otherwise its bits [M, 1].  The
+    same as two bnn_bgemm calls."""
+    lib = load()
+    _u32(A)
+    _u32(w0)
+    _u32(w1)
+    M, N0 = A.shape[0], w0.shape[0]
+    thr0 = _dev(thr0, torch.int32, "thr0")
+    flip0 = _dev(flip0, torch.int32, "flip0")
+    thr1 = _dev(thr1, torch.int32, "thr1")
+    flip1 = _dev(flip1, torch.int32, "flip1")
+    if out is None:
+        out = torch.empty((M, N1) if thr1 is None else (M, 1), dtype=torch.int32, device=A.device)
+    _check(lib.bnn_bfc_pair(M, K0, N0, N1, _ptr(A), _ptr(w0), _ptr(thr0), _ptr(flip0), _ptr(w1),
+                            _ptr(thr1), _ptr(flip1), _ptr(out) if thr1 is None else None,
+                            None if thr1 is None else _ptr(out), _stream(stream)))
+    return out
 
 
 def bnn_bgemm(A, B, K, thr=None, flip=None, want_sums=True, want_bits=True, out_sums=None,

@@ -506,6 +506,36 @@ bnn_status bnn_bconv_bconv2d(const bnn_conv_desc* d0, const bnn_conv_desc* d1, c
   }
 }
 
+bnn_status bnn_bfc_pair(int64_t M, int64_t K0, int64_t N0, int64_t N1, const uint32_t* A,
+                        const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
+                        const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
+                        int32_t* out_sums, uint32_t* out_bits, hipStream_t stream) {
+  try {
+    if (M < 1 || K0 < 1 || N0 < 1 || N1 < 1)
+      return fail(BNN_ERR_SHAPE, "bfc_pair: sizes must be >= 1 (M=%lld K0=%lld N0=%lld N1=%lld)",
+                  (long long)M, (long long)K0, (long long)N0, (long long)N1);
+    if (!bnn::bfc_pair_supported(M, K0, N0, N1))
+      return fail(BNN_ERR_UNSUPPORTED,
+                  "bfc_pair: needs K0 = 512 or 1024, N0 = 256, 512 or 1024, N1 <= 32 "
+                  "and at most 2^26 rows");
+    if (!A || !w0 || !w1) return fail(BNN_ERR_NULL, "bfc_pair: A, w0 or w1 is NULL");
+    if (!thr0) return fail(BNN_ERR_NULL, "bfc_pair: thr0 is NULL");
+    if (!out_sums && !out_bits)
+      return fail(BNN_ERR_NULL, "bfc_pair: out_sums and out_bits are both NULL");
+    if (out_sums && out_bits)
+      return fail(BNN_ERR_SHAPE, "bfc_pair: give out_sums or out_bits, not both");
+    if (out_bits && !thr1) return fail(BNN_ERR_NULL, "bfc_pair: out_bits requested but thr1 is NULL");
+    if (!aligned16(A) || !aligned16(w0) || !aligned16(w1) || !aligned16(out_sums) ||
+        !aligned16(out_bits))
+      return fail(BNN_ERR_ALIGN, "bfc_pair: A, weights and outputs must be 16-byte aligned");
+    return hip_status(bnn::launch_bfc_pair(M, K0, N0, N1, A, w0, thr0, flip0, w1, thr1, flip1,
+                                           out_sums, out_bits, stream),
+                      "bfc_pair launch");
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "bfc_pair: unexpected C++ exception");
+  }
+}
+
 bnn_status bnn_bgemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
                      const uint32_t* B, const int32_t* thr, const uint32_t* flip,
                      int32_t* out_sums, uint32_t* out_bits, hipStream_t stream) {
@@ -831,6 +861,29 @@ bnn_status run_chain(const bnn_layer* layers, int32_t n_layers, int32_t batch, i
           h = w = 1;
           c = layers[li + run - 1].N;
           li += run - 1;  // the run's last layer; its output is in dst
+          break;
+        }
+        // Two FC layers that fit one kernel (the second with at most 32
+        // outputs, often the logits) run as one, the first layer's bits kept
+        // in LDS, where the GEMM path would take them (rows above
+        // gemv_max_rows; the GEMVs are faster below: 1024 -> 1024 -> 10 at one
+        // row 5.2 us as two GEMVs, 7.4 us fused; at 64 rows 8.6 us as two
+        // GEMMs, 7.45 us fused).  A matrix-core kernel, so not under the
+        // vector-ALU ablation; option fuse_pair = 0 launches them apart.
+        if (g_opt.fuse_pair != 0 && g_opt.algo != BNN_ALGO_VALU && batch > g_opt.gemv_max_rows &&
+            li + 1 < n_layers &&
+            (layers[li + 1].kind == BNN_LAYER_BFC || layers[li + 1].kind == BNN_LAYER_BFC_LOGITS) &&
+            layers[li + 1].K == l.N && bnn::bfc_pair_supported(batch, l.K, l.N, layers[li + 1].N)) {
+          const bnn_layer& l2 = layers[li + 1];
+          const bool lg = l2.kind == BNN_LAYER_BFC_LOGITS;
+          e = bnn::launch_bfc_pair(batch, l.K, l.N, l2.N, src, l.w, l.thr, l.flip, l2.w,
+                                   lg ? nullptr : l2.thr, lg ? nullptr : l2.flip,
+                                   lg ? logits : nullptr, lg ? nullptr : dst, stream);
+          if (e != hipSuccess) return fail(BNN_ERR_HIP, "forward: layers %d-%d launch: %s", li,
+                                           li + 1, hipGetErrorString(e));
+          h = w = 1;
+          c = l2.N;
+          ++li;  // the pair's second layer; its output is in dst (or the logits)
           break;
         }
         st = gemm_launch(batch, l.N, l.K, src, l.w, l.thr, l.flip, nullptr, dst, stream);

@@ -132,6 +132,17 @@ hipError_t launch_bconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const uint
                               const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
                               uint32_t* bits, hipStream_t s);
 
+// Two consecutive binary FC layers in one launch (bfc_pair.hip), the first
+// layer's output bits kept in LDS: K0 = 512 or 1024 input bits,
+// N0 = 256, 512 or 1024 first-layer outputs (thresholded, with flips), N1 <= 32
+// second-layer outputs as int32 sums [M][N1] (sums non-null) or bits [M][1]
+// (thr1 non-null).  Packed weights.
+bool bfc_pair_supported(int64_t M, int64_t K0, int64_t N0, int64_t N1);
+hipError_t launch_bfc_pair(int64_t M, int64_t K0, int64_t N0, int64_t N1, const uint32_t* A,
+                           const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
+                           const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
+                           int32_t* sums, uint32_t* bits, hipStream_t s);
+
 // A run of consecutive binary FC layers in one launch (bfc_chain.hip): every
 // block takes R rows through all of them with the intermediate bits in LDS.
 // Layer i has K_i input bits and N_i outputs; K_{i+1} = N_i; every layer but

@@ -229,6 +229,35 @@ def test_bconv_bconv_errors():
 
 
 @needs_lib
+def test_bfc_pair_errors():
+    """bnn_bfc_pair: sizes, the shapes its kernel covers, one output of the
+    two, NULL pointers and alignment, all refused on the host."""
+    lib = bnn.load()
+
+    def call(M=64, K0=1024, N0=1024, N1=10, a=A, w0=A, thr0=A, w1=A, thr1=None, sums=A,
+             bits=None):
+        return lib.bnn_bfc_pair(M, K0, N0, N1, a, w0, thr0, None, w1, thr1, None, sums, bits,
+                                None)
+
+    for bad in (dict(M=0), dict(K0=0), dict(N0=0), dict(N1=0), dict(N1=-3)):
+        assert call(**bad) == 2, bad
+    for uns in (dict(K0=1000), dict(K0=2048), dict(K0=4096), dict(N0=128), dict(N0=2048), dict(N1=33),
+                dict(M=(1 << 26) + 1)):
+        assert call(**uns) == 4, uns
+    assert call(a=None) == 1
+    assert call(w0=None) == 1
+    assert call(w1=None) == 1
+    assert call(thr0=None) == 1 and "thr0" in bnn.last_error()
+    assert call(sums=None, bits=None) == 1
+    assert call(sums=A, bits=A, thr1=A) == 2 and "not both" in bnn.last_error()
+    assert call(sums=None, bits=A, thr1=None) == 1 and "thr1" in bnn.last_error()
+    assert call(a=A + 4) == 3
+    assert call(w1=A + 4) == 3
+    assert call(sums=A + 4) == 3
+    assert call(sums=None, bits=A + 4, thr1=A) == 3
+
+
+@needs_lib
 def test_binarize_input_errors():
     lib = bnn.load()
     assert lib.bnn_binarize_input(5, A, None, 1, 4, 4, 3, A, None) == 2
