@@ -32,14 +32,10 @@ namespace bnn {
 namespace {
 
 constexpr int kW = 16;              // image width (both convs, pad 1)
-constexpr int kTH = 4;              // second-conv output rows per block
 constexpr int kF = 256;             // filters of each conv
 constexpr int kNW = kF / 32;        // waves: one per 32-filter tile
 constexpr int kNT = 64 * kNW;       // threads
-constexpr int kRA = kTH + 2;        // first-conv rows a block computes
-constexpr int kRI = kTH + 4;        // input rows it stages
 constexpr int kCols = kW + 2;       // staged columns (one pad column each side)
-constexpr int kPTA = kRA * kW / 32; // first-conv pixel tiles (3)
 constexpr int kCW1 = kF / 32;       // words per first-conv output pixel (8)
 constexpr uint32_t kRsrcWord3 = 0x00020000;
 
@@ -57,6 +53,8 @@ struct BbArgs {
   int32_t w0_bytes, w1_bytes;
   int32_t Hp, Wp;         // stored output (pooled dims when pooling)
 };
+
+constexpr int64_t kCUs = 256;       // compute units of the chip
 
 // LDS row stride (in 16-byte entries) of a staged row of kCols pixels with
 // ps entries each: a multiple of 8 plus 4, so that the 16-byte reads of
@@ -134,8 +132,16 @@ __device__ __forceinline__ uint32_t sign_word(const v16f& acc, int h) {
   return wd;
 }
 
-template <int CW0, bool POOL>
+// TH: second-conv output rows per block, 4, or 2 on grids smaller than the
+// chip (twice the blocks, each with 4 first-conv rows for 2 output rows
+// instead of 6 for 4).
+template <int TH, int CW0, bool POOL>
 __global__ __launch_bounds__(kNT) void bconv_bconv_kernel(BbArgs a) {
+  constexpr int kTH = TH;
+  constexpr int kRA = kTH + 2;         // first-conv rows a block computes
+  constexpr int kRI = kTH + 4;         // input rows it stages
+  constexpr int kPTA = kRA * kW / 32;  // first-conv pixel tiles (3 or 2)
+  constexpr int kPTB = kTH * kW / 32;  // second-conv pixel tiles (2 or 1)
   constexpr int PSA = CW0 + 1;  // entries per staged input pixel (one spare)
   constexpr int RSA = row_stride(PSA);
   constexpr int PSB = kCW1 + 1;
@@ -151,7 +157,7 @@ __global__ __launch_bounds__(kNT) void bconv_bconv_kernel(BbArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int tiles_h = (a.H + kTH - 1) / kTH;
+  const int tiles_h = (a.H + kTH - 1) / kTH;  // (kTH rows per block)
   const int n = blockIdx.x / tiles_h;
   const int i0 = (blockIdx.x - n * tiles_h) * kTH;
 
@@ -207,7 +213,7 @@ __global__ __launch_bounds__(kNT) void bconv_bconv_kernel(BbArgs a) {
   __syncthreads();
 
   const int h = lane >> 5, c = lane & 31;
-  // 2. First conv, filter tile `wave`, pixel tiles 0..2 of the 6 x 16 region
+  // 2. First conv, filter tile `wave`, pixel tiles 0..kPTA-1 of the region
   // (pixel q = 32 tp + c at region row q / 16 = image row i0 - 1 + q / 16,
   // column q % 16).  Its window starts at staged row q / 16, column q % 16.
   {
@@ -225,11 +231,10 @@ __global__ __launch_bounds__(kNT) void bconv_bconv_kernel(BbArgs a) {
     }
     conv_tile<CW0, kPTA, RSA, PSA>(xa, abase, a.w0, a.w0_bytes, wave, lane, smask, vfill, acc);
     // Lane half h assembles the word of pixel tile h (tiles 0, 1) with one
-    // v_permlane32_swap, and every lane the word of tile 2.
+    // v_permlane32_swap, and every lane the word of tile 2 (when there is one).
     const auto s01 = __builtin_amdgcn_permlane32_swap(sign_word(acc[0], h), sign_word(acc[1], h),
                                                       false, false);
     const uint32_t w01 = s01[0] | s01[1];
-    const uint32_t w2 = or_xor32(sign_word(acc[2], h));
     auto put = [&](int tp, uint32_t word) {
       const int rq = 2 * tp + (c >> 4), cq = c & 15;
       const int y = i0 - 1 + rq;
@@ -239,51 +244,71 @@ __global__ __launch_bounds__(kNT) void bconv_bconv_kernel(BbArgs a) {
       xb[rq * RSB + (cq + 1) * PSB + wave] = v4i{x[0], x[1], x[2], x[3]};
     };
     put(h, w01);
-    if (h == 0) put(2, w2);
+    if constexpr (kPTA == 3) {
+      const uint32_t w2 = or_xor32(sign_word(acc[2], h));
+      if (h == 0) put(2, w2);
+    }
   }
   __syncthreads();
 
-  // 3. Second conv, filter tile `wave`, pixel tiles 0..1 of the 4 x 16
-  // output rows: tile tp, lane c is output pixel (2 tp + (c / 2) % 2,
+  // 3. Second conv, filter tile `wave`, pixel tiles 0..kPTB-1 of the output
+  // rows: tile tp, lane c is output pixel (2 tp + (c / 2) % 2,
   // 2 (c / 4) + c % 2), so each 2x2 pooling window sits in 4 adjacent lanes.
   // Its window starts at first-conv region row 2 tp + (c / 2) % 2, column
   // 2 (c / 4) + c % 2 (the region and its pad columns are offset by one).
-  int bbase[2];
+  int bbase[kPTB];
 #pragma unroll
-  for (int tp = 0; tp < 2; ++tp)
+  for (int tp = 0; tp < kPTB; ++tp)
     bbase[tp] = (2 * tp + ((c >> 1) & 1)) * RSB + (2 * (c >> 2) + (c & 1)) * PSB + h * 2;
-  v16f acc[2];
+  v16f acc[kPTB];
   {
     v16f t;
 #pragma unroll
     for (int e = 0; e < 16; ++e) t[e] = th1[32 * wave + 8 * (e >> 2) + 4 * h + (e & 3)];
-    acc[0] = t;
-    acc[1] = t;
+#pragma unroll
+    for (int tp = 0; tp < kPTB; ++tp) acc[tp] = t;
   }
-  conv_tile<kCW1, 2, RSB, PSB>(xb, bbase, a.w1, a.w1_bytes, wave, lane, smask, vfill, acc);
-  // Lane half h gets the word of pixel tile h.
-  const auto sw = __builtin_amdgcn_permlane32_swap(sign_word(acc[0], h), sign_word(acc[1], h),
-                                                   false, false);
-  uint32_t word = (sw[0] | sw[1]) ^ nf1;
+  conv_tile<kCW1, kPTB, RSB, PSB>(xb, bbase, a.w1, a.w1_bytes, wave, lane, smask, vfill, acc);
+  // Lane half h gets the word of pixel tile h (with one tile, both halves
+  // hold tile 0's word and half 0 stores it).
+  uint32_t word;
+  if constexpr (kPTB == 2) {
+    const auto sw = __builtin_amdgcn_permlane32_swap(sign_word(acc[0], h), sign_word(acc[1], h),
+                                                     false, false);
+    word = (sw[0] | sw[1]) ^ nf1;
+  } else {
+    word = or_xor32(sign_word(acc[0], h)) ^ nf1;
+  }
+  const bool owner = kPTB == 2 || h == 0;
   const int pr = 2 * h + ((c >> 1) & 1), pc = 2 * (c >> 2) + (c & 1);
   if constexpr (POOL) {
     word = or_quad(word);
     const int ip = (i0 >> 1) + h, jp = c >> 2;
-    if ((c & 3) == 0 && ip < a.Hp)
+    if (owner && (c & 3) == 0 && ip < a.Hp)
       a.bits[(static_cast<size_t>(n * a.Hp + ip) * a.Wp + jp) * kCW1 + wave] = word;
   } else {
     const int i = i0 + pr;
-    if (i < a.H) a.bits[(static_cast<size_t>(n * a.H + i) * kW + pc) * kCW1 + wave] = word;
+    if (owner && i < a.H) a.bits[(static_cast<size_t>(n * a.H + i) * kW + pc) * kCW1 + wave] = word;
   }
 }
 
-template <int CW0>
+template <int TH, int CW0>
 hipError_t launch_cw(const BbArgs& a, bool pool, unsigned blocks, hipStream_t s) {
   if (pool)
-    bconv_bconv_kernel<CW0, true><<<blocks, kNT, 0, s>>>(a);
+    bconv_bconv_kernel<TH, CW0, true><<<blocks, kNT, 0, s>>>(a);
   else
-    bconv_bconv_kernel<CW0, false><<<blocks, kNT, 0, s>>>(a);
+    bconv_bconv_kernel<TH, CW0, false><<<blocks, kNT, 0, s>>>(a);
   return hipGetLastError();
+}
+
+template <int TH>
+hipError_t launch_th(const BbArgs& a, int cw0, bool pool, hipStream_t s) {
+  const unsigned blocks = static_cast<unsigned>(a.N) * ((a.H + TH - 1) / TH);
+  switch (cw0) {
+    case 2: return launch_cw<TH, 2>(a, pool, blocks, s);
+    case 4: return launch_cw<TH, 4>(a, pool, blocks, s);
+    default: return launch_cw<TH, 8>(a, pool, blocks, s);
+  }
 }
 
 }  // namespace
@@ -293,7 +318,7 @@ bool bconv_bconv_supported(const ConvGeom& g0, const ConvGeom& g1) {
          (g0.C == 64 || g0.C == 128 || g0.C == 256) && g0.F == kF &&
          g1.KH == 3 && g1.KW == 3 && g1.pad == 1 && (g1.pool == 0 || g1.pool == 2) &&
          g1.C == kF && g1.F == kF && g1.N == g0.N && g1.H == g0.Ho && g1.W == g0.Wo &&
-         static_cast<int64_t>(g0.N) * ((g0.H + kTH - 1) / kTH) < (int64_t{1} << 31);
+         static_cast<int64_t>(g0.N) * ((g0.H + 1) / 2) < (int64_t{1} << 31);
 }
 
 hipError_t launch_bconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const uint32_t* in,
@@ -317,13 +342,11 @@ hipError_t launch_bconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const uint
   a.w1_bytes = g1.F * 9 * g1.Cw * 4;
   a.Hp = g1.Hp;
   a.Wp = g1.Wp;
-  const unsigned blocks = static_cast<unsigned>(g0.N) * ((g0.H + kTH - 1) / kTH);
+  // 4-row tiles while they give at least one block per compute unit, 2-row
+  // tiles on smaller grids.
   const bool pool = g1.pool == 2;
-  switch (g0.Cw) {
-    case 2: return launch_cw<2>(a, pool, blocks, s);
-    case 4: return launch_cw<4>(a, pool, blocks, s);
-    default: return launch_cw<8>(a, pool, blocks, s);
-  }
+  return int64_t{g0.N} * ((g0.H + 3) / 4) >= kCUs ? launch_th<4>(a, g0.Cw, pool, s)
+                                                  : launch_th<2>(a, g0.Cw, pool, s);
 }
 
 }  // namespace bnn

@@ -2,7 +2,7 @@
 net's 16 x 16 stage, a conv -> conv step of Table II's layer order): bit-exact
 against the oracle chain (Eq. 3 / Eq. 4 sums with the -1 pad, threshold and
 flip, 2x2 OR-pool, Eq. 2 packing) and against two bnn_bconv2d launches, on
-whole and ragged 4-row tiles, every input width the kernel takes, with and
+whole and ragged 4-row and 2-row tiles, every input width the kernel takes, with and
 without pooling, NULL flips, extreme and tied thresholds, and inside
 bnn_forward with option fuse_pair on and off."""
 import numpy as np
@@ -15,16 +15,22 @@ from paper_1808_00209_amd.device import pack_pm1, to_device, upload_layer, uploa
 
 pytestmark = pytest.mark.gpu
 
+# Grids of at least 256 blocks of 4 rows take 4-row tiles, smaller ones 2-row
+# tiles.
 #        N,  H,  C0, pool
 CASES = [
-    (2, 16, 128, 2),    # the CIFAR-shaped stage
+    (2, 16, 128, 2),    # the CIFAR-shaped stage, 2-row tiles
     (3, 16, 64, 0),
     (1, 16, 256, 2),
-    (2, 6, 128, 2),     # a ragged last tile (rows 4 and 5 only)
-    (1, 5, 256, 0),     # odd height, no pooling
-    (1, 3, 64, 2),      # one tile, odd height with pooling (one pooled row)
+    (2, 6, 128, 2),
+    (1, 5, 256, 0),     # odd height, no pooling: a last tile with one row
+    (1, 3, 64, 2),      # odd height with pooling (one pooled row)
     (1, 1, 128, 0),     # a single row
     (5, 12, 128, 2),
+    (86, 12, 128, 2),   # 4-row tiles
+    (43, 22, 256, 0),   # 4-row tiles, a last tile with two rows
+    (128, 8, 64, 2),
+    (52, 19, 128, 2),   # 4-row tiles, a last tile with three rows
 ]
 
 
