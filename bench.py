@@ -45,17 +45,22 @@ _FP4 = ("paper_1808_00209_amd/csrc/fp4_expand.hpp",
 _LANE = ("paper_1808_00209_amd/csrc/lane_ops.hpp",
          "96ece7042c6ed72e9cd799fdd8e007525e30035bbd8d052a9ece380c5e3fda82")
 _KERN = ("paper_1808_00209_amd/csrc/kernels.hpp",
-         "75b55b2430a784f32576e9d322c1d0fb9f9e8f807d4416d32188e764e6d2d083")
+         "9a21bf69b19c895655c75a3f608f82f06a7b7509b8907579cfa0253773adf174")
 MEASURED_TRAFFIC = {
     # profiles/fconv_bconv_cifar_b64.md
     ("cifar_bnn_b64", "L0+L1 fconv+bconv 32x32x3->128->128 k3 pool (fused)"): dict(
-        fetch_kib=980.7, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
+        fetch_kib=980.8, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/fconv_bconv.hip",
                        "b9775a39d56ce451c281b54dceafe567d2fc9cc81ff7a7752a4c1a83d8de96f3"),
                       ("paper_1808_00209_amd/csrc/fp32_split.hpp",
                        "7f3a9f6b25af5be34fb5b304976e0225cd491d935c5a4e567bc43c134b6ceb13"),
                       _FP4, _LANE, _KERN]), flags=_FLAGS),
     # profiles/bconv_mfma_cifar_b64.md
+    ("cifar_bnn_b64", "L2+L3 bconv+bconv 16x16x128->256->256 k3 pool (fused)"): dict(
+        fetch_kib=858.1, write_kib=128.0, fetch_scale=2.0, write_scale=1.0,
+        sources=dict([("paper_1808_00209_amd/csrc/bconv_bconv.hip",
+                       "e8087610efe7b3a873602132098efa7e62b9183ba10c134d9662028921117045"),
+                      _FP4, _LANE, _KERN]), flags=_FLAGS),
     ("cifar_bnn_b64", "L5 bconv 8x8x512->512 k3 pool"): dict(
         fetch_kib=4806.0, write_kib=64.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/bconv_mfma.hip",
