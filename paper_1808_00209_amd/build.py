@@ -20,7 +20,7 @@ LIB = os.path.join(PKG, "libbnn.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
 SOURCES = ["pack.hip", "bconv_valu.hip", "bconv_mfma.hip", "bconv_1x1.hip", "bconv_patch.hip", "fconv.hip",
-           "fconv_bconv.hip", "bconv_bconv.hip", "bfc_chain.hip", "bfc_pair.hip",
+           "fconv_bconv.hip", "bconv_bconv.hip", "bfc_chain.hip", "bfc_pair.hip", "bfc_gemm.hip",
            "api.cpp"]
 ARCH = os.environ.get("BNN_OFFLOAD_ARCH", "gfx950")
 

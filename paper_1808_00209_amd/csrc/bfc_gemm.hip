@@ -1,0 +1,196 @@
+// Binary FC layer / GEMM (Sec. III-B, Eq. 4) for long rows at modest row
+// counts: S[m][n] = sum_k a[m][k] b[n][k] over +-1 values, with the
+// threshold / flip epilogue of bnn_bgemm.  K is a multiple of 1024 bits and N
+// a multiple of 32.
+//
+// A workgroup computes one 32 x 32 output tile (32 rows x 32 outputs) with 8
+// waves, each taking one eighth of the K bits.  A wave loads its slice of
+// both operands -- 32 weight rows and 32 data rows -- in chunks of up to 32
+// words per row with 16-byte loads that cover whole cache lines, stages them
+// in its own LDS region (only that wave touches it, and LDS operations of a
+// wave complete in order, so no barrier), and runs the chunk's k-steps from
+// there on the fp4 matrix cores.  The 8 partial tiles are summed in LDS
+// (exact: integer sums below 2^24) and wave 0 writes the sums and/or bits.
+// The general matrix-core kernel loads each operand row straight from memory,
+// 32 rows per load instruction, and runs the K split inside a workgroup of
+// one output tile column: the 8192 -> 1024 layer at 64 rows ran on 32
+// workgroups there, bound by those CUs' fetch path.
+
+#include "fp4_expand.hpp"
+#include "kernels.hpp"
+#include "lane_ops.hpp"
+
+namespace bnn {
+namespace {
+
+constexpr int kNW = 8;
+constexpr int kNT = 64 * kNW;
+constexpr int kCH = 32;        // words per row and chunk
+constexpr int kRS = kCH + 2;   // LDS words per staged row (8-byte aligned rows)
+
+struct GmArgs {
+  const uint32_t* A;      // [M][Kw]
+  const uint32_t* B;      // [N][Kw]
+  const int32_t* thr;     // [N] (bits) or null
+  const uint32_t* flip;   // [N / 32] or null
+  int32_t* sums;          // [M][N] or null
+  uint32_t* bits;         // [M][N / 32] or null
+  int32_t M, N, Kw;       // Kw = K / 32, a multiple of 32
+  int32_t a_bytes, b_bytes;
+};
+
+constexpr uint32_t kRsrcWord3 = 0x00020000;
+
+// Sign bits of a 32 x 32 tile's accumulators: register e of lane (h, c)
+// holds output 8 (e / 4) + 4 h + e % 4 of row c, which goes to bit 31 - that
+// output; each lane half holds half of every row's word.
+__device__ __forceinline__ uint32_t sign_word(const v16f& acc, int h) {
+  uint32_t wd = 0u;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    uint32_t nib = 0u;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      nib = __builtin_amdgcn_alignbit(nib, __float_as_uint(acc[4 * g + r]), 31);
+    wd |= nib << (28 - 8 * g - 4 * h);
+  }
+  return wd;
+}
+
+__global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a) {
+  __shared__ __attribute__((aligned(16))) uint32_t stg[kNW][2][32 * kRS];
+  __shared__ float part[kNW][16 * 64];
+  __shared__ float th[32];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = lane >> 5, c = lane & 31;
+  const int ft = blockIdx.x % (a.N / 32);
+  const int m0 = (blockIdx.x / (a.N / 32)) * 32;
+  const int n0 = 32 * ft;
+  const bool want_bits = a.bits != nullptr;
+  if (want_bits && tid < 32) {
+    const int32_t K = 32 * a.Kw;
+    th[tid] = 0.5f - static_cast<float>(min(max(a.thr[n0 + tid], -K - 1), K + 1));
+  }
+
+  const __amdgpu_buffer_rsrc_t ra =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(a.A), 0, a.a_bytes, kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rb =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(a.B), 0, a.b_bytes, kRsrcWord3);
+  const uint32_t smask = __builtin_amdgcn_readfirstlane(0x88888888u);
+  uint32_t vfill;
+  asm("v_mov_b32 %0, 0x22222222" : "=v"(vfill));
+
+  // This wave's K slice: words k0 .. k0 + sw - 1 of every row.
+  const int sw = a.Kw / kNW;
+  const int k0 = wave * sw;
+  v16f acc = {};
+  // A chunk of ch words (a multiple of 4, at most 32) of 32 rows is 8 ch
+  // 16-byte pieces; piece p = row (p / (ch / 4)), words 4 (p % (ch / 4)) ..
+  // +3.  Load i of lane l takes piece 64 i + l.  Rows past M read row M - 1.
+  for (int kc = 0; kc < sw; kc += kCH) {
+    const int ch = min(kCH, sw - kc);
+    const int ppr = ch / 4;  // pieces per row
+    v4i pa[4], pb[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int p = min(64 * i + lane, 8 * ch - 1);
+      const int row = p / ppr, col = 4 * (p - row * ppr);
+      const int m = min(m0 + row, a.M - 1);
+      const uint32_t wo = static_cast<uint32_t>(k0 + kc + col) * 4;
+      pa[i] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
+                                          ra, static_cast<uint32_t>(m) * a.Kw * 4 + wo, 0, 0));
+      pb[i] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
+                                          rb, static_cast<uint32_t>(n0 + row) * a.Kw * 4 + wo, 0, 0));
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int p = 64 * i + lane;
+      if (p < 8 * ch) {
+        const int row = p / ppr, col = 4 * (p - row * ppr);
+        uint32_t* da = &stg[wave][0][row * kRS + col];  // 8-byte aligned
+        uint32_t* db = &stg[wave][1][row * kRS + col];
+        *reinterpret_cast<uint2*>(da) = uint2{static_cast<uint32_t>(pa[i][0]),
+                                              static_cast<uint32_t>(pa[i][1])};
+        *reinterpret_cast<uint2*>(da + 2) = uint2{static_cast<uint32_t>(pa[i][2]),
+                                                  static_cast<uint32_t>(pa[i][3])};
+        *reinterpret_cast<uint2*>(db) = uint2{static_cast<uint32_t>(pb[i][0]),
+                                              static_cast<uint32_t>(pb[i][1])};
+        *reinterpret_cast<uint2*>(db + 2) = uint2{static_cast<uint32_t>(pb[i][2]),
+                                                  static_cast<uint32_t>(pb[i][3])};
+      }
+    }
+    // k-steps: lane (h, c) takes words 4 it + 2 h and 4 it + 2 h + 1 of
+    // weight row c (operand A) and of data row c (operand B).
+    for (int it = 0; it < ch / 4; ++it) {
+      const uint2 wv = *reinterpret_cast<const uint2*>(&stg[wave][1][c * kRS + 4 * it + 2 * h]);
+      const uint2 xv = *reinterpret_cast<const uint2*>(&stg[wave][0][c * kRS + 4 * it + 2 * h]);
+      v8i A0, A1, B0, B1;
+      expand_pair(wv.x, wv.y, smask, vfill, A0, A1);
+      expand_pair(xv.x, xv.y, smask, vfill, B0, B1);
+      acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(A0, B0, acc, 4, 4, 0, 127, 0, 127);
+      acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(A1, B1, acc, 4, 4, 0, 127, 0, 127);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 16; ++e) part[wave][e * 64 + lane] = acc[e];
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 16 * 64 / kNT; ++i) {
+    const int v = tid + i * kNT;
+    float t = part[0][v];
+#pragma unroll
+    for (int w = 1; w < kNW; ++w) t += part[w][v];
+    part[0][v] = t;
+  }
+  __syncthreads();
+  if (wave > 0) return;
+  const int m = m0 + c;
+  if (a.sums && m < a.M) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      a.sums[static_cast<size_t>(m) * a.N + n0 + 8 * (e >> 2) + 4 * h + (e & 3)] =
+          static_cast<int32_t>(part[0][e * 64 + lane]);
+  }
+  if (want_bits) {
+    v16f d;
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      d[e] = part[0][e * 64 + lane] + th[8 * (e >> 2) + 4 * h + (e & 3)];
+    // output bit = (S >= thr) xor flip = sign xor ~flip
+    const uint32_t word = or_xor32(sign_word(d, h)) ^ ~(a.flip ? a.flip[ft] : 0u);
+    if (h == 0 && m < a.M) a.bits[static_cast<size_t>(m) * (a.N / 32) + ft] = word;
+  }
+}
+
+}  // namespace
+
+bool bfc_gemm_supported(int64_t M, int64_t N, int64_t K) {
+  return M >= 1 && N >= 32 && N % 32 == 0 && K >= 1024 && K % 1024 == 0 &&
+         M * (K / 8) < (int64_t{1} << 31) && N * (K / 8) < (int64_t{1} << 31) &&
+         ((M + 31) / 32) * (N / 32) < (int64_t{1} << 31);
+}
+
+hipError_t launch_bfc_gemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
+                           const uint32_t* B, const int32_t* thr, const uint32_t* flip,
+                           int32_t* sums, uint32_t* bits, hipStream_t s) {
+  GmArgs a;
+  a.A = A;
+  a.B = B;
+  a.thr = thr;
+  a.flip = flip;
+  a.sums = sums;
+  a.bits = bits;
+  a.M = static_cast<int32_t>(M);
+  a.N = static_cast<int32_t>(N);
+  a.Kw = static_cast<int32_t>(K / 32);
+  a.a_bytes = static_cast<int32_t>(M * (K / 8));
+  a.b_bytes = static_cast<int32_t>(N * (K / 8));
+  const unsigned blocks = static_cast<unsigned>(((M + 31) / 32) * (N / 32));
+  bfc_gemm_kernel<<<blocks, kNT, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace bnn

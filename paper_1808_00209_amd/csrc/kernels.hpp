@@ -132,6 +132,15 @@ hipError_t launch_bconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const uint
                               const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
                               uint32_t* bits, hipStream_t s);
 
+// Binary FC layer / GEMM with K a multiple of 1024 bits and N a multiple of
+// 32 (bfc_gemm.hip): a workgroup per 32 x 32 output tile, K split over its 8
+// waves, both operands staged per wave through LDS with whole-line loads.
+// sums [M][N] and/or bits [M][N / 32]; thr non-null when bits is.
+bool bfc_gemm_supported(int64_t M, int64_t N, int64_t K);
+hipError_t launch_bfc_gemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
+                           const uint32_t* B, const int32_t* thr, const uint32_t* flip,
+                           int32_t* sums, uint32_t* bits, hipStream_t s);
+
 // Two consecutive binary FC layers in one launch (bfc_pair.hip), the first
 // layer's output bits kept in LDS: K0 = 512 or 1024 input bits,
 // N0 = 256, 512 or 1024 first-layer outputs (thresholded, with flips), N1 <= 32

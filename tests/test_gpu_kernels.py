@@ -288,7 +288,11 @@ GEMM_CASES = [(1, 1, 1), (1, 10, 1024), (2, 33, 31), (5, 100, 33), (16, 1024, 81
               (3, 40, 100), (64, 96, 4100), (7, 33, 65),
               (16, 64, 4100), (17, 40, 96), (64, 1024, 8192), (100, 70, 1000), (3, 4, 18432),
               (65, 128, 1024), (300, 64, 18432), (64, 192, 128), (64, 10, 1024),
-              (40, 50, 128), (64, 33, 8192), (64, 4, 18432), (256, 1024, 8192)]
+              (40, 50, 128), (64, 33, 8192), (64, 4, 18432), (256, 1024, 8192),
+              # K a multiple of 1024, N of 32, at most 512 output tiles: the
+              # FC kernel with a workgroup per tile (ragged row tiles, K slices
+              # of one chunk, of several chunks and of a short last chunk)
+              (3, 32, 1024), (33, 64, 2048), (97, 96, 8192), (40, 32, 18432), (512, 1024, 1024)]
 
 
 @pytest.mark.parametrize("case", GEMM_CASES, ids=[str(c) for c in GEMM_CASES])
