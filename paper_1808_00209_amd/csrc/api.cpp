@@ -74,6 +74,8 @@ hipError_t launch_conv(const bnn::ConvGeom& g, const uint32_t* in, const uint32_
                        int32_t* sums, uint32_t* bits, hipStream_t s) {
   if (use_mfma(g) && bits && use_1x1(g, sums != nullptr))
     return bnn::launch_bconv1x1(g, in, w, thr, flip, bits, s);
+  if (use_mfma(g) && bits && !sums && bnn::bconv_img8_supported(g))
+    return bnn::launch_bconv_img8(g, in, w, thr, flip, bits, s);
   if (use_mfma(g))
     return bnn::launch_bconv_mfma(g, in, w, wprep && bnn::bconv_mfma_prep_supported(g) ? wprep
                                                                                          : nullptr,

@@ -61,18 +61,23 @@ constexpr int64_t kCUs = 256;       // compute units of the chip
 // lanes two rows apart fall on different banks.
 constexpr int row_stride(int ps) { return kCols * ps + ((4 - (kCols * ps) % 8) + 8) % 8; }
 
+// Iterations of a 3x3 window over CW words per pixel: one tap and a chunk
+// of 2 VW words each.
+template <int CW>
+constexpr int window_iters() { return 9 * (CW / (2 * (CW % 4 == 0 ? 2 : 1))); }
+
 // One 32-filter tile (filter tile `ft`) over TP pixel tiles of a conv whose
 // activation operands sit in LDS: act[abase[tp] + tap offset + word] holds
-// pixel tp's word as its fp4 operand.  Weights: packed words [256][9][CW],
-// read through a buffer resource, expanded per k-step.  Accumulators start
-// from acc (0.5 - thr per filter).
-template <int CW, int TP, int RS, int PS>
+// pixel tp's word as its fp4 operand.  Weights: packed words [F][9][CW],
+// read through a buffer resource, expanded per k-step.  Iterations IT0 ..
+// IT1 - 1 of the window (all of it by default).  Accumulators start from
+// acc.
+template <int CW, int TP, int RS, int PS, int IT0 = 0, int IT1 = window_iters<CW>()>
 __device__ __forceinline__ void conv_tile(const v4i* act, const int (&abase)[TP],
                                           const uint32_t* w, int w_bytes, int ft, int lane,
                                           uint32_t smask, uint32_t vfill, v16f (&acc)[TP]) {
   constexpr int VW = CW % 4 == 0 ? 2 : 1;  // words per lane per iteration
   constexpr int NCH = CW / (2 * VW);       // iterations per tap
-  constexpr int ITERS = 9 * NCH;
   const int h = lane >> 5, c = lane & 31;
   const __amdgpu_buffer_rsrc_t rw =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(w), 0, w_bytes, kRsrcWord3);
@@ -90,11 +95,11 @@ __device__ __forceinline__ void conv_tile(const v4i* act, const int (&abase)[TP]
     }
   };
   uint32_t wr[2][VW];
-  load_w(0, wr[0]);
+  load_w(IT0, wr[0]);
 #pragma unroll
-  for (int it = 0; it < ITERS; ++it) {
-    const int cur = it & 1;
-    if (it + 1 < ITERS) load_w(it + 1, wr[cur ^ 1]);
+  for (int it = IT0; it < IT1; ++it) {
+    const int cur = (it - IT0) & 1;
+    if (it + 1 < IT1) load_w(it + 1, wr[cur ^ 1]);
     const int tap = it / NCH, cc = (it - tap * NCH) * 2 * VW;
     const int kh = tap / 3, kw = tap - kh * 3;
     const int ao = kh * RS + kw * PS + cc;
@@ -311,7 +316,172 @@ hipError_t launch_th(const BbArgs& a, int cw0, bool pool, hipStream_t s) {
   }
 }
 
+// One binary 3x3 conv with pad 1 on 8 x 8 maps (Eq. 3 and Eq. 4 with the
+// threshold / flip / OR-pool epilogue), bits only.  An 8 x 8 image is
+// exactly two 32-pixel tiles, so a block takes one image and 128 filters,
+// with 8 waves: filter tile w / 2, half w % 2 of the window's iterations
+// (the halves' partial tiles meet in LDS).  The image and its pad ring
+// (10 x 10 pixels) are staged once per block, each word already expanded to
+// its fp4 operand, so the k-steps read activations straight from LDS: no
+// activation loads or expansion in the loop, where the general kernel loads
+// every pixel's words once per tap and expands them per use.
+struct ImArgs {
+  const uint32_t* in;     // [N][8][8][CW]
+  const uint32_t* w;      // [F][9][CW]
+  const int32_t* thr;     // [F]
+  const uint32_t* flip;   // [F / 32] or null
+  uint32_t* bits;         // [N][Hp][Wp][F / 32]
+  int32_t N, F, K;        // K = 9 C
+  int32_t w_bytes;
+};
+
+constexpr int row_stride10(int ps) { return 10 * ps + ((4 - (10 * ps) % 8) + 8) % 8; }
+
+template <int CW, bool POOL>
+__global__ __launch_bounds__(kNT) void bconv_img8_kernel(ImArgs a) {
+  constexpr int PS = CW + 1;  // entries per staged pixel (one spare)
+  constexpr int RS = row_stride10(PS);
+  constexpr int NX = 100 * CW;  // staged words
+  constexpr int XIT = (NX + kNT - 1) / kNT;
+  constexpr int ITERS = window_iters<CW>();
+  constexpr int HALF = ITERS / 2;
+  __shared__ v4i xa[10 * RS];
+  __shared__ float th[128];
+  __shared__ float part[4][2 * 16 * 64];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int fgroups = a.F / 128;
+  const int n = blockIdx.x / fgroups;
+  const int fg = blockIdx.x - n * fgroups;
+  const int ft = 4 * fg + (wave >> 1);  // filter tile
+  const int kh = wave & 1;              // half of the window
+
+  // Staging (clamped addresses; the pad ring gets the word 0, i.e. -1).
+  uint32_t xw[XIT];
+  bool xin[XIT];
+#pragma unroll
+  for (int i = 0; i < XIT; ++i) {
+    const int e = tid + i * kNT;
+    const int wd = e % CW, t = e / CW;
+    const int col = t % 10, row = t / 10;
+    const int y = row - 1, x = col - 1;
+    xin[i] = e < NX && y >= 0 && y < 8 && x >= 0 && x < 8;
+    const int yc = min(max(y, 0), 7), xc = min(max(x, 0), 7);
+    xw[i] = a.in[((static_cast<size_t>(n) * 8 + yc) * 8 + xc) * CW + wd];
+  }
+  const int32_t thv = a.thr[min(128 * fg + tid, a.F - 1)];
+  const uint32_t nfl = ~(a.flip ? a.flip[ft] : 0u);
+  const uint32_t smask = __builtin_amdgcn_readfirstlane(0x88888888u);
+  uint32_t vfill;
+  asm("v_mov_b32 %0, 0x22222222" : "=v"(vfill));
+#pragma unroll
+  for (int i = 0; i < XIT; ++i) {
+    const int e = tid + i * kNT;
+    if (e < NX) {
+      const int wd = e % CW, t = e / CW;
+      const v8i x = expand_fp4(xin[i] ? xw[i] : 0u, smask, vfill);
+      xa[(t / 10) * RS + (t % 10) * PS + wd] = v4i{x[0], x[1], x[2], x[3]};
+    }
+  }
+  // Start values 0.5 - thr (clamped to [-K-1, K+1]) for the first half;
+  // the sign bit of the total is then the complement of the output bit.
+  if (tid < 128) th[tid] = 0.5f - static_cast<float>(min(max(thv, -a.K - 1), a.K + 1));
+  __syncthreads();
+
+  // Pixel tile tp = image rows 4 tp .. 4 tp + 3; lane c holds pixel
+  // (4 tp + 2 (c / 16) + (c / 2) % 2, 2 ((c / 4) % 4) + c % 2), so each 2x2
+  // pooling window sits in 4 adjacent lanes.  Its window starts at staged
+  // row = that row, column = that column (the pad ring offsets by one).
+  const int h = lane >> 5, c = lane & 31;
+  const int qr = 2 * (c >> 4) + ((c >> 1) & 1), qc = 2 * ((c >> 2) & 3) + (c & 1);
+  int bbase[2];
+#pragma unroll
+  for (int tp = 0; tp < 2; ++tp)
+    bbase[tp] = (4 * tp + qr) * RS + qc * PS + h * (CW % 4 == 0 ? 2 : 1);
+  v16f acc[2];
+  {
+    v16f t;
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      t[e] = kh ? 0.0f : th[32 * (wave >> 1) + 8 * (e >> 2) + 4 * h + (e & 3)];
+    acc[0] = t;
+    acc[1] = t;
+  }
+  if (kh)
+    conv_tile<CW, 2, RS, PS, HALF, ITERS>(xa, bbase, a.w, a.w_bytes, ft, lane, smask, vfill, acc);
+  else
+    conv_tile<CW, 2, RS, PS, 0, HALF>(xa, bbase, a.w, a.w_bytes, ft, lane, smask, vfill, acc);
+  // The second half's partial tiles to LDS, one barrier, the first half adds
+  // them (exact: integer sums below 2^24).
+  float* pp = part[wave >> 1];
+  if (kh) {
+#pragma unroll
+    for (int tp = 0; tp < 2; ++tp)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) pp[(tp * 16 + e) * 64 + lane] = acc[tp][e];
+  }
+  __syncthreads();
+  if (kh) return;
+#pragma unroll
+  for (int tp = 0; tp < 2; ++tp)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[tp][e] += pp[(tp * 16 + e) * 64 + lane];
+  // Lane half h gets the word of pixel tile h; output bit = sign xor ~flip.
+  const auto sw = __builtin_amdgcn_permlane32_swap(sign_word(acc[0], h), sign_word(acc[1], h),
+                                                   false, false);
+  uint32_t word = (sw[0] | sw[1]) ^ nfl;
+  const int fw = a.F / 32;
+  if constexpr (POOL) {
+    word = or_quad(word);
+    const int ip = 2 * h + (c >> 4), jp = (c >> 2) & 3;
+    if ((c & 3) == 0) a.bits[((static_cast<size_t>(n) * 4 + ip) * 4 + jp) * fw + ft] = word;
+  } else {
+    const int i = 4 * h + qr;
+    a.bits[((static_cast<size_t>(n) * 8 + i) * 8 + qc) * fw + ft] = word;
+  }
+}
+
+template <int CW>
+hipError_t launch_img8_cw(const ImArgs& a, bool pool, unsigned blocks, hipStream_t s) {
+  if (pool)
+    bconv_img8_kernel<CW, true><<<blocks, kNT, 0, s>>>(a);
+  else
+    bconv_img8_kernel<CW, false><<<blocks, kNT, 0, s>>>(a);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+bool bconv_img8_supported(const ConvGeom& g) {
+  return g.KH == 3 && g.KW == 3 && g.pad == 1 && g.H == 8 && g.W == 8 &&
+         (g.C == 64 || g.C == 128 || g.C == 256 || g.C == 512) && g.F % 128 == 0 &&
+         (g.pool == 0 || g.pool == 2) && int64_t{g.N} * (g.F / 128) < (int64_t{1} << 31);
+}
+
+hipError_t launch_bconv_img8(const ConvGeom& g, const uint32_t* in, const uint32_t* w,
+                             const int32_t* thr, const uint32_t* flip, uint32_t* bits,
+                             hipStream_t s) {
+  ImArgs a;
+  a.in = in;
+  a.w = w;
+  a.thr = thr;
+  a.flip = flip;
+  a.bits = bits;
+  a.N = g.N;
+  a.F = g.F;
+  a.K = 9 * g.C;
+  a.w_bytes = g.F * 9 * g.Cw * 4;
+  const unsigned blocks = static_cast<unsigned>(g.N) * (g.F / 128);
+  const bool pool = g.pool == 2;
+  switch (g.Cw) {
+    case 2: return launch_img8_cw<2>(a, pool, blocks, s);
+    case 4: return launch_img8_cw<4>(a, pool, blocks, s);
+    case 8: return launch_img8_cw<8>(a, pool, blocks, s);
+    default: return launch_img8_cw<16>(a, pool, blocks, s);
+  }
+}
 
 bool bconv_bconv_supported(const ConvGeom& g0, const ConvGeom& g1) {
   return g0.KH == 3 && g0.KW == 3 && g0.pad == 1 && g0.pool == 0 && g0.W == kW &&

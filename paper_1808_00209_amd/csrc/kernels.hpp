@@ -132,6 +132,14 @@ hipError_t launch_bconv_bconv(const ConvGeom& g0, const ConvGeom& g1, const uint
                               const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
                               uint32_t* bits, hipStream_t s);
 
+// One binary 3x3 conv with pad 1 on 8 x 8 maps, C = 64..512 (a power of
+// two), F a multiple of 128, bits only (bconv_bconv.hip): a block per image
+// and 128 filters, the image staged once in LDS as fp4 operands.
+bool bconv_img8_supported(const ConvGeom& g);
+hipError_t launch_bconv_img8(const ConvGeom& g, const uint32_t* in, const uint32_t* w,
+                             const int32_t* thr, const uint32_t* flip, uint32_t* bits,
+                             hipStream_t s);
+
 // Binary FC layer / GEMM with K a multiple of 1024 bits and N a multiple of
 // 32 (bfc_gemm.hip): a workgroup per 32 x 32 output tile, K split over its 8
 // waves, both operands staged per wave through LDS with whole-line loads.
