@@ -318,9 +318,9 @@ hipError_t launch_th(const BbArgs& a, int cw0, bool pool, hipStream_t s) {
 
 // One binary 3x3 conv with pad 1 on 8 x 8 maps (Eq. 3 and Eq. 4 with the
 // threshold / flip / OR-pool epilogue), bits only.  An 8 x 8 image is
-// exactly two 32-pixel tiles, so a block takes one image and 128 filters,
-// with 8 waves: filter tile w / 2, half w % 2 of the window's iterations
-// (the halves' partial tiles meet in LDS).  The image and its pad ring
+// exactly two 32-pixel tiles, so a block takes one image and 128 filters (64
+// on small grids), with 2 waves per 32-filter tile: filter tile w / 2, half
+// w % 2 of the window's iterations (the halves' partial tiles meet in LDS).  The image and its pad ring
 // (10 x 10 pixels) are staged once per block, each word already expanded to
 // its fp4 operand, so the k-steps read activations straight from LDS: no
 // activation loads or expansion in the loop, where the general kernel loads
@@ -337,25 +337,27 @@ struct ImArgs {
 
 constexpr int row_stride10(int ps) { return 10 * ps + ((4 - (10 * ps) % 8) + 8) % 8; }
 
-template <int CW, bool POOL>
-__global__ __launch_bounds__(kNT) void bconv_img8_kernel(ImArgs a) {
+// FPB: filters per block (128 or 64); 2 FPB / 32 waves.
+template <int CW, bool POOL, int FPB>
+__global__ __launch_bounds__(2 * FPB * 2) void bconv_img8_kernel(ImArgs a) {
+  constexpr int NT = 2 * FPB * 2;  // threads: 2 waves per 32-filter tile
   constexpr int PS = CW + 1;  // entries per staged pixel (one spare)
   constexpr int RS = row_stride10(PS);
   constexpr int NX = 100 * CW;  // staged words
-  constexpr int XIT = (NX + kNT - 1) / kNT;
+  constexpr int XIT = (NX + NT - 1) / NT;
   constexpr int ITERS = window_iters<CW>();
   constexpr int HALF = ITERS / 2;
   __shared__ v4i xa[10 * RS];
-  __shared__ float th[128];
-  __shared__ float part[4][2 * 16 * 64];
+  __shared__ float th[FPB];
+  __shared__ float part[FPB / 32][2 * 16 * 64];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int fgroups = a.F / 128;
+  const int fgroups = a.F / FPB;
   const int n = blockIdx.x / fgroups;
   const int fg = blockIdx.x - n * fgroups;
-  const int ft = 4 * fg + (wave >> 1);  // filter tile
+  const int ft = (FPB / 32) * fg + (wave >> 1);  // filter tile
   const int kh = wave & 1;              // half of the window
 
   // Staging (clamped addresses; the pad ring gets the word 0, i.e. -1).
@@ -363,7 +365,7 @@ __global__ __launch_bounds__(kNT) void bconv_img8_kernel(ImArgs a) {
   bool xin[XIT];
 #pragma unroll
   for (int i = 0; i < XIT; ++i) {
-    const int e = tid + i * kNT;
+    const int e = tid + i * NT;
     const int wd = e % CW, t = e / CW;
     const int col = t % 10, row = t / 10;
     const int y = row - 1, x = col - 1;
@@ -371,14 +373,14 @@ __global__ __launch_bounds__(kNT) void bconv_img8_kernel(ImArgs a) {
     const int yc = min(max(y, 0), 7), xc = min(max(x, 0), 7);
     xw[i] = a.in[((static_cast<size_t>(n) * 8 + yc) * 8 + xc) * CW + wd];
   }
-  const int32_t thv = a.thr[min(128 * fg + tid, a.F - 1)];
+  const int32_t thv = a.thr[min(FPB * fg + tid, a.F - 1)];
   const uint32_t nfl = ~(a.flip ? a.flip[ft] : 0u);
   const uint32_t smask = __builtin_amdgcn_readfirstlane(0x88888888u);
   uint32_t vfill;
   asm("v_mov_b32 %0, 0x22222222" : "=v"(vfill));
 #pragma unroll
   for (int i = 0; i < XIT; ++i) {
-    const int e = tid + i * kNT;
+    const int e = tid + i * NT;
     if (e < NX) {
       const int wd = e % CW, t = e / CW;
       const v8i x = expand_fp4(xin[i] ? xw[i] : 0u, smask, vfill);
@@ -387,7 +389,7 @@ __global__ __launch_bounds__(kNT) void bconv_img8_kernel(ImArgs a) {
   }
   // Start values 0.5 - thr (clamped to [-K-1, K+1]) for the first half;
   // the sign bit of the total is then the complement of the output bit.
-  if (tid < 128) th[tid] = 0.5f - static_cast<float>(min(max(thv, -a.K - 1), a.K + 1));
+  if (tid < FPB) th[tid] = 0.5f - static_cast<float>(min(max(thv, -a.K - 1), a.K + 1));
   __syncthreads();
 
   // Pixel tile tp = image rows 4 tp .. 4 tp + 3; lane c holds pixel
@@ -443,12 +445,12 @@ __global__ __launch_bounds__(kNT) void bconv_img8_kernel(ImArgs a) {
   }
 }
 
-template <int CW>
+template <int CW, int FPB>
 hipError_t launch_img8_cw(const ImArgs& a, bool pool, unsigned blocks, hipStream_t s) {
   if (pool)
-    bconv_img8_kernel<CW, true><<<blocks, kNT, 0, s>>>(a);
+    bconv_img8_kernel<CW, true, FPB><<<blocks, 4 * FPB, 0, s>>>(a);
   else
-    bconv_img8_kernel<CW, false><<<blocks, kNT, 0, s>>>(a);
+    bconv_img8_kernel<CW, false, FPB><<<blocks, 4 * FPB, 0, s>>>(a);
   return hipGetLastError();
 }
 
@@ -473,13 +475,25 @@ hipError_t launch_bconv_img8(const ConvGeom& g, const uint32_t* in, const uint32
   a.F = g.F;
   a.K = 9 * g.C;
   a.w_bytes = g.F * 9 * g.Cw * 4;
-  const unsigned blocks = static_cast<unsigned>(g.N) * (g.F / 128);
+  // 128 filters per block where that gives a block per compute unit, 64 on
+  // smaller grids (CIFAR L4 / L5 at batch 64: 5.1 / 6.7 us with 128, 5.3 /
+  // 6.9 us with 64; the batch-1 forward 30.4 us with 64, 31.1 us with 128).
   const bool pool = g.pool == 2;
+  if (int64_t{g.N} * (g.F / 128) >= kCUs) {
+    const unsigned blocks = static_cast<unsigned>(g.N) * (g.F / 128);
+    switch (g.Cw) {
+      case 2: return launch_img8_cw<2, 128>(a, pool, blocks, s);
+      case 4: return launch_img8_cw<4, 128>(a, pool, blocks, s);
+      case 8: return launch_img8_cw<8, 128>(a, pool, blocks, s);
+      default: return launch_img8_cw<16, 128>(a, pool, blocks, s);
+    }
+  }
+  const unsigned blocks = static_cast<unsigned>(g.N) * (g.F / 64);
   switch (g.Cw) {
-    case 2: return launch_img8_cw<2>(a, pool, blocks, s);
-    case 4: return launch_img8_cw<4>(a, pool, blocks, s);
-    case 8: return launch_img8_cw<8>(a, pool, blocks, s);
-    default: return launch_img8_cw<16>(a, pool, blocks, s);
+    case 2: return launch_img8_cw<2, 64>(a, pool, blocks, s);
+    case 4: return launch_img8_cw<4, 64>(a, pool, blocks, s);
+    case 8: return launch_img8_cw<8, 64>(a, pool, blocks, s);
+    default: return launch_img8_cw<16, 64>(a, pool, blocks, s);
   }
 }
 

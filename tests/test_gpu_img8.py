@@ -15,6 +15,8 @@ from paper_1808_00209_amd.device import pack_flips, pack_pm1, to_device, words_u
 
 pytestmark = pytest.mark.gpu
 
+# Grids of at least 256 blocks of 128 filters take those, smaller ones blocks
+# of 64 filters.
 #        N,   C,   F, pool
 CASES = [
     (64, 256, 512, 0),   # the CIFAR-shaped net's L4 at batch 64
@@ -23,6 +25,7 @@ CASES = [
     (3, 128, 256, 2),
     (5, 512, 128, 0),
     (2, 256, 384, 2),
+    (200, 128, 256, 2),  # blocks of 128 filters with a filter group count of 2
 ]
 
 
