@@ -45,7 +45,7 @@ _FP4 = ("paper_1808_00209_amd/csrc/fp4_expand.hpp",
 _LANE = ("paper_1808_00209_amd/csrc/lane_ops.hpp",
          "96ece7042c6ed72e9cd799fdd8e007525e30035bbd8d052a9ece380c5e3fda82")
 _KERN = ("paper_1808_00209_amd/csrc/kernels.hpp",
-         "9a21bf69b19c895655c75a3f608f82f06a7b7509b8907579cfa0253773adf174")
+         "43844ac76042685c6998681919abec925b4eee23c45b886f3800e646ab1541fa")
 MEASURED_TRAFFIC = {
     # profiles/fconv_bconv_cifar_b64.md
     ("cifar_bnn_b64", "L0+L1 fconv+bconv 32x32x3->128->128 k3 pool (fused)"): dict(
@@ -57,14 +57,14 @@ MEASURED_TRAFFIC = {
                       _FP4, _LANE, _KERN]), flags=_FLAGS),
     # profiles/bconv_mfma_cifar_b64.md
     ("cifar_bnn_b64", "L2+L3 bconv+bconv 16x16x128->256->256 k3 pool (fused)"): dict(
-        fetch_kib=858.1, write_kib=128.0, fetch_scale=2.0, write_scale=1.0,
+        fetch_kib=858.2, write_kib=128.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/bconv_bconv.hip",
-                       "e8087610efe7b3a873602132098efa7e62b9183ba10c134d9662028921117045"),
+                       "a420dbc535694f6a02d8b0f9334f472acb9aeacd217f74d9783b7da0beed81b4"),
                       _FP4, _LANE, _KERN]), flags=_FLAGS),
     ("cifar_bnn_b64", "L5 bconv 8x8x512->512 k3 pool"): dict(
-        fetch_kib=4806.0, write_kib=64.0, fetch_scale=2.0, write_scale=1.0,
-        sources=dict([("paper_1808_00209_amd/csrc/bconv_mfma.hip",
-                       "577fcd293919a87dfc1693ed6e1822c4c76eb2fa47e901fc1dd7c0566802b975"),
+        fetch_kib=898.0, write_kib=128.0, fetch_scale=2.0, write_scale=1.0,
+        sources=dict([("paper_1808_00209_amd/csrc/bconv_bconv.hip",
+                       "a420dbc535694f6a02d8b0f9334f472acb9aeacd217f74d9783b7da0beed81b4"),
                       _FP4, _LANE, _KERN]), flags=_FLAGS),
 }
 
