@@ -174,14 +174,16 @@ bnn_status gemm_launch(int64_t M, int64_t N, int64_t K, const uint32_t* A,
   if (M <= g_opt.gemv_max_rows)
     return hip_status(bnn::launch_bgemv_valu(M, N, K, A, B, thr, flip, sums, bits, s),
                       "bgemm (gemv) launch");
-  // K a multiple of 1024 and at most 512 output tiles of 32 x 32: the FC
-  // kernel with a workgroup per output tile (bfc_gemm.hip).  Graph-timed, bits
-  // only: 64 x 8192 -> 1024 4.8 us against 6.65 us in the conv kernel,
-  // 256 x 18432 -> 1024 8.8 against 10.4 us, 64 x 1024 -> 1024 3.8 against
-  // 4.2 us; the 1024-tile 256 x 4096 -> 4096 with int32 sums 13.1 against
-  // 9.2 us, so larger grids stay with the conv kernel.
+  // K a multiple of 1024: the FC kernel (bfc_gemm.hip), a workgroup per
+  // 32 x 32 output tile up to 512 tiles, per 2 x 2 tiles above that when N is
+  // a multiple of 64.  Graph-timed, bits only: 64 x 8192 -> 1024 4.7 us
+  // against 6.65 us in the conv kernel, 256 x 18432 -> 1024 8.2 against
+  // 10.4 us, 64 x 1024 -> 1024 3.7 against 4.2 us; 256 x 4096 -> 4096 with
+  // int32 sums (1024 tiles) 7.55 against 9.2 us.  Larger grids with N not a
+  // multiple of 64 stay with the conv kernel (one tile per workgroup took
+  // 13.1 us on that shape).
   if (g_opt.algo != BNN_ALGO_VALU && bnn::bfc_gemm_supported(M, N, K) &&
-      ((M + 31) / 32) * (N / 32) <= 512)
+      (((M + 31) / 32) * (N / 32) <= 512 || N % 64 == 0))
     return hip_status(bnn::launch_bfc_gemm(M, N, K, A, B, thr, flip, sums, bits, s),
                       "bgemm launch");
   // M rows of A are a 1 x M image with K channels; B holds N 1x1 filters.

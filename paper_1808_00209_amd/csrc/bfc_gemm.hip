@@ -11,6 +11,10 @@
 // wave complete in order, so no barrier), and runs the chunk's k-steps from
 // there on the fp4 matrix cores.  The 8 partial tiles are summed in LDS
 // (exact: integer sums below 2^24) and wave 0 writes the sums and/or bits.
+// Grids of more than 512 tiles (N a multiple of 64) take 2 x 2 tiles per
+// workgroup instead, two waves per tile with half of K each: a workgroup
+// holds about 100 KB of LDS, so one runs per CU, and 1024 one-tile
+// workgroups took four rounds.
 // The general matrix-core kernel loads each operand row straight from memory,
 // 32 rows per load instruction, and runs the K split inside a workgroup of
 // one output tile column: the 8192 -> 1024 layer at 64 rows ran on 32
@@ -57,22 +61,31 @@ __device__ __forceinline__ uint32_t sign_word(const v16f& acc, int h) {
   return wd;
 }
 
+// TPB x TFB output tiles of 32 x 32 per workgroup (rows x outputs) and KS
+// waves per tile, each taking 1 / KS of K (TPB TFB KS = 8 waves): wave w
+// computes tile (w % TPB, (w / TPB) % TFB) over slice w / (TPB TFB) of K.
+template <int TPB, int TFB, int KS>
 __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a) {
+  static_assert(TPB * TFB * KS == kNW, "8 waves");
+  constexpr int NTL = TPB * TFB;  // tiles per workgroup
   __shared__ __attribute__((aligned(16))) uint32_t stg[kNW][2][32 * kRS];
   __shared__ float part[kNW][16 * 64];
-  __shared__ float th[32];
+  __shared__ float th[32 * TFB];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, c = lane & 31;
-  const int ft = blockIdx.x % (a.N / 32);
-  const int m0 = (blockIdx.x / (a.N / 32)) * 32;
-  const int n0 = 32 * ft;
+  const int ftb = a.N / (32 * TFB);                 // filter-tile groups
+  const int ft0 = TFB * (blockIdx.x % ftb);         // first filter tile
+  const int m00 = 32 * TPB * (blockIdx.x / ftb);    // first row
+  const int tp = wave % TPB, tf = (wave / TPB) % TFB, ks = wave / NTL;
+  const int ft = ft0 + tf;
+  const int m0 = m00 + 32 * tp, n0 = 32 * ft;
   const bool want_bits = a.bits != nullptr;
-  if (want_bits && tid < 32) {
+  if (want_bits && tid < 32 * TFB) {
     const int32_t K = 32 * a.Kw;
-    th[tid] = 0.5f - static_cast<float>(min(max(a.thr[n0 + tid], -K - 1), K + 1));
+    th[tid] = 0.5f - static_cast<float>(min(max(a.thr[32 * ft0 + tid], -K - 1), K + 1));
   }
 
   const __amdgpu_buffer_rsrc_t ra =
@@ -84,8 +97,8 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a) {
   asm("v_mov_b32 %0, 0x22222222" : "=v"(vfill));
 
   // This wave's K slice: words k0 .. k0 + sw - 1 of every row.
-  const int sw = a.Kw / kNW;
-  const int k0 = wave * sw;
+  const int sw = a.Kw / KS;
+  const int k0 = ks * sw;
   v16f acc = {};
   // A chunk of ch words (a multiple of 4, at most 32) of 32 rows is 8 ch
   // 16-byte pieces; piece p = row (p / (ch / 4)), words 4 (p % (ch / 4)) ..
@@ -93,11 +106,14 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a) {
   for (int kc = 0; kc < sw; kc += kCH) {
     const int ch = min(kCH, sw - kc);
     const int ppr = ch / 4;  // pieces per row
+    // p / ppr as (p rmag) >> 16: exact for p < 4096 and ppr <= 8, and two
+    // vector instructions where an integer division takes dozens.
+    const int rmag = (65536 + ppr - 1) / ppr;
     v4i pa[4], pb[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int p = min(64 * i + lane, 8 * ch - 1);
-      const int row = p / ppr, col = 4 * (p - row * ppr);
+      const int row = (p * rmag) >> 16, col = 4 * (p - row * ppr);
       const int m = min(m0 + row, a.M - 1);
       const uint32_t wo = static_cast<uint32_t>(k0 + kc + col) * 4;
       pa[i] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
@@ -109,7 +125,7 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a) {
     for (int i = 0; i < 4; ++i) {
       const int p = 64 * i + lane;
       if (p < 8 * ch) {
-        const int row = p / ppr, col = 4 * (p - row * ppr);
+        const int row = (p * rmag) >> 16, col = 4 * (p - row * ppr);
         uint32_t* da = &stg[wave][0][row * kRS + col];  // 8-byte aligned
         uint32_t* db = &stg[wave][1][row * kRS + col];
         *reinterpret_cast<uint2*>(da) = uint2{static_cast<uint32_t>(pa[i][0]),
@@ -134,35 +150,70 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a) {
       acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(A1, B1, acc, 4, 4, 0, 127, 0, 127);
     }
   }
+  // The KS partial tiles of each output tile meet in LDS (exact: integer
+  // sums below 2^24): with one tile all threads add the slots slice by
+  // slice; with several, the slice-0 wave of each tile adds the others'.
+  if constexpr (KS > 1) {
+    if (NTL == 1 || ks > 0) {
 #pragma unroll
-  for (int e = 0; e < 16; ++e) part[wave][e * 64 + lane] = acc[e];
-  __syncthreads();
+      for (int e = 0; e < 16; ++e) part[wave][e * 64 + lane] = acc[e];
+    }
+    __syncthreads();
+    if constexpr (NTL == 1) {
 #pragma unroll
-  for (int i = 0; i < 16 * 64 / kNT; ++i) {
-    const int v = tid + i * kNT;
-    float t = part[0][v];
+      for (int i = 0; i < 16 * 64 / kNT; ++i) {
+        const int v = tid + i * kNT;
+        float t = part[0][v];
 #pragma unroll
-    for (int w = 1; w < kNW; ++w) t += part[w][v];
-    part[0][v] = t;
+        for (int w = 1; w < kNW; ++w) t += part[w][v];
+        part[0][v] = t;
+      }
+      __syncthreads();
+      if (wave > 0) return;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[e] = part[0][e * 64 + lane];
+    } else {
+      if (ks > 0) return;
+#pragma unroll
+      for (int q = 1; q < KS; ++q)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[e] += part[wave + q * NTL][e * 64 + lane];
+    }
   }
-  __syncthreads();
-  if (wave > 0) return;
   const int m = m0 + c;
-  if (a.sums && m < a.M) {
+  if (a.sums) {
+    // The tile goes through this wave's staging region as [row][output], so
+    // that each lane stores 16 consecutive bytes of a row.
+    int32_t* ts = reinterpret_cast<int32_t*>(&stg[wave][0][0]);  // 32 x 33 words
 #pragma unroll
     for (int e = 0; e < 16; ++e)
-      a.sums[static_cast<size_t>(m) * a.N + n0 + 8 * (e >> 2) + 4 * h + (e & 3)] =
-          static_cast<int32_t>(part[0][e * 64 + lane]);
+      ts[c * 33 + 8 * (e >> 2) + 4 * h + (e & 3)] = static_cast<int32_t>(acc[e]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 8 * i + (lane >> 3), col = 4 * (lane & 7);
+      if (m0 + row < a.M) {
+        const int* src = &ts[row * 33 + col];
+        *reinterpret_cast<int4*>(&a.sums[static_cast<size_t>(m0 + row) * a.N + n0 + col]) =
+            int4{src[0], src[1], src[2], src[3]};
+      }
+    }
   }
   if (want_bits) {
     v16f d;
 #pragma unroll
     for (int e = 0; e < 16; ++e)
-      d[e] = part[0][e * 64 + lane] + th[8 * (e >> 2) + 4 * h + (e & 3)];
+      d[e] = acc[e] + th[32 * tf + 8 * (e >> 2) + 4 * h + (e & 3)];
     // output bit = (S >= thr) xor flip = sign xor ~flip
     const uint32_t word = or_xor32(sign_word(d, h)) ^ ~(a.flip ? a.flip[ft] : 0u);
     if (h == 0 && m < a.M) a.bits[static_cast<size_t>(m) * (a.N / 32) + ft] = word;
   }
+}
+
+template <int TPB, int TFB, int KS>
+void launch_tiles(const GmArgs& a, hipStream_t s) {
+  const unsigned blocks =
+      static_cast<unsigned>(((a.M + 32 * TPB - 1) / (32 * TPB)) * (a.N / (32 * TFB)));
+  bfc_gemm_kernel<TPB, TFB, KS><<<blocks, kNT, 0, s>>>(a);
 }
 
 }  // namespace
@@ -188,8 +239,14 @@ hipError_t launch_bfc_gemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
   a.Kw = static_cast<int32_t>(K / 32);
   a.a_bytes = static_cast<int32_t>(M * (K / 8));
   a.b_bytes = static_cast<int32_t>(N * (K / 8));
-  const unsigned blocks = static_cast<unsigned>(((M + 31) / 32) * (N / 32));
-  bfc_gemm_kernel<<<blocks, kNT, 0, s>>>(a);
+  // One output tile per workgroup (K split 8 ways) up to 512 tiles; larger
+  // grids take 2 x 2 tiles per workgroup with K split 2 ways (rows and
+  // outputs in whole pairs of tiles).
+  const int64_t tiles = ((M + 31) / 32) * (N / 32);
+  if (tiles <= 512 || N % 64 != 0)
+    launch_tiles<1, 1, 8>(a, s);
+  else
+    launch_tiles<2, 2, 2>(a, s);
   return hipGetLastError();
 }
 
