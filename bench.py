@@ -248,15 +248,19 @@ def layer_shapes(layers, H, W, C, batch=None):
             out.append((name, k, dict(H=h, W=w, C=c, F=F, KH=KH, KW=KW, pad=pad, pool=pool, li=li),
                         0 if k == "fconv" else macs))
             h, w, c = (Ho // 2, Wo // 2, F) if pool else (Ho, Wo, F)
-        elif (k == "bfc" and batch is not None and batch > 2 and li + 1 < len(layers)
+        elif (k == "bfc" and batch is not None and li + 1 < len(layers)
               and layers[li + 1]["kind"] in ("bfc", "bfc_logits")
-              and L["K"] in (512, 1024) and L["N"] in (256, 512, 1024)
-              and layers[li + 1]["N"] <= 32 and not fc_chained(layers, li, batch)):
-            # bnn_forward's two FC layers in one kernel (bnn_bfc_pair)
+              and not fc_chained(layers, li, batch)
+              and (tail_fusable(L, layers[li + 1], batch)
+                   or (batch > 2 and L["K"] in (512, 1024) and L["N"] in (256, 512, 1024)
+                       and layers[li + 1]["N"] <= 32))):
+            # bnn_forward's two FC layers in one kernel: the FC tail kernel
+            # (bnn_bfc_tail) where it fits, else bnn_bfc_pair
             L1 = layers[li + 1]
             K, N0, N1 = L["K"], L["N"], L1["N"]
+            kind = "bfc_tail" if tail_fusable(L, L1, batch) else "bfc_pair"
             out.append(("L%d+L%d %s+%s %d->%d->%d (fused)" % (li, li + 1, k, L1["kind"], K, N0, N1),
-                        "bfc_pair", dict(K=K, N0=N0, N=N1, logits=L1["kind"] == "bfc_logits", li=li),
+                        kind, dict(K=K, N0=N0, N=N1, logits=L1["kind"] == "bfc_logits", li=li),
                         K * N0 + N0 * N1))
             paired.add(li + 1)
             h, w, c = 1, 1, N1
@@ -265,6 +269,15 @@ def layer_shapes(layers, H, W, C, batch=None):
             out.append(("L%d %s %d->%d" % (li, k, K, N), k, dict(K=K, N=N, li=li), K * N))
             h, w, c = 1, 1, N
     return out
+
+
+def tail_fusable(L0, L1, batch):
+    """Whether bnn_forward runs two FC layers as the FC tail kernel: at most
+    512 rows, the first layer's K a multiple of 1024 and N of 32 with at most
+    512 tiles of 32 x 32, the second with at most 32 outputs."""
+    K, N0, N1 = L0["K"], L0["N"], L1["N"]
+    return (batch <= 512 and K % 1024 == 0 and N0 % 32 == 0 and N1 <= 32
+            and ((batch + 31) // 32) * (N0 // 32) <= 512)
 
 
 def fc_chained(layers, li, batch):
@@ -294,7 +307,7 @@ def algorithmic_bytes(kind, g, batch):
                                        else 4 * g.get("cin", g["C"]))
         w = g["F"] * g["KH"] * g["KW"] * 4 * wd(g["C"])
         return x + w + 4 * g["F"] + 4 * wd(g["F"]) + batch * Hp * Wp * 4 * wd(g["F"])
-    if kind == "bfc_pair":
+    if kind in ("bfc_pair", "bfc_tail"):
         x = batch * 4 * wd(g["K"]) + g["N0"] * 4 * wd(g["K"]) + 4 * g["N0"] + 4 * wd(g["N0"])
         x += g["N"] * 4 * wd(g["N0"])
         if g["logits"]:
@@ -485,15 +498,21 @@ def time_layer(bnn, kind, g, batch, dev_layer, reps, torch):
             else:
                 fn = lambda: bnn.bnn_bconv2d(desc, x, dev_layer["w"], dev_layer["thr"],
                                              dev_layer.get("flip"), want_sums=False, out_bits=ob)
-    elif kind == "bfc_pair":
+    elif kind in ("bfc_pair", "bfc_tail"):
         A = torch.randint(-2 ** 31, 2 ** 31 - 1, (batch, bnn.words(g["K"])), dtype=torch.int32,
                           device="cuda", generator=gen)
         l0, l1 = dev_layer
         ob = torch.empty((batch, g["N"]) if g["logits"] else (batch, 1), dtype=torch.int32,
                          device="cuda")
-        fn = lambda: bnn.bnn_bfc_pair(A, g["K"], l0["w"], l0["thr"], l0.get("flip"), l1["w"], g["N"],
-                                      None if g["logits"] else l1["thr"],
-                                      None if g["logits"] else l1.get("flip"), out=ob)
+        if kind == "bfc_tail":
+            accum = bnn.accum_buffer()
+            fn = lambda: bnn.bnn_bfc_tail(A, g["K"], l0["w"], l0["thr"], l0.get("flip"), l1["w"],
+                                          g["N"], accum, None if g["logits"] else l1["thr"],
+                                          None if g["logits"] else l1.get("flip"), out=ob)
+        else:
+            fn = lambda: bnn.bnn_bfc_pair(A, g["K"], l0["w"], l0["thr"], l0.get("flip"), l1["w"],
+                                          g["N"], None if g["logits"] else l1["thr"],
+                                          None if g["logits"] else l1.get("flip"), out=ob)
     else:
         A = torch.randint(-2 ** 31, 2 ** 31 - 1, (batch, bnn.words(g["K"])), dtype=torch.int32,
                           device="cuda", generator=gen)
@@ -539,7 +558,8 @@ def per_layer_rows(bnn, torch, layers, shapes, batch, reps):
         dl = ((dev_layers[0], dev_layers[1]) if kind in ("bconv_input", "fconv_bconv")
               else tuple(dev_layers[:3]) if kind == "input_bconv_bconv"
               else (dev_layers[g["li"]], dev_layers[g["li"] + 1]) if kind in ("bconv_bconv",
-                                                                             "bfc_pair")
+                                                                             "bfc_pair",
+                                                                             "bfc_tail")
               else dev_layers[g["li"]])
         ms = time_layer(bnn, kind, g, batch, dl, reps, torch)
         ms_valu = None
@@ -552,7 +572,7 @@ def per_layer_rows(bnn, torch, layers, shapes, batch, reps):
             with bnn.options(algo=bnn.ALGO_VALU):
                 ms_valu = (time_layer(bnn, "bconv", g0, batch, dl[0], reps, torch)
                            + time_layer(bnn, "bconv", g1, batch, dl[1], reps, torch))
-        elif kind == "bfc_pair":
+        elif kind in ("bfc_pair", "bfc_tail"):
             g0 = dict(K=g["K"], N=g["N0"])
             g1 = dict(K=g["N0"], N=g["N"])
             with bnn.options(algo=bnn.ALGO_VALU):
@@ -834,7 +854,8 @@ def main():
         # the binary second layer on fp4 MFMA is the counted work; the fused
         # fp32 first layer (bf16 MFMA on three parts of x) is reported beside it
         dom_ops, bound, peak, unit = 2 * macs * batch, "mfma", MFMA_FP4_PEAK_TFLOPS, "TFLOP/s"
-    elif kind in ("input_bconv_bconv", "bconv_bconv") or (kind == "bfc_pair" and batch > 16):
+    elif kind in ("input_bconv_bconv", "bconv_bconv") or (kind in ("bfc_pair", "bfc_tail")
+                                                           and batch > 16):
         # both binary convs on fp4 MFMA (the thresholding is part of staging)
         dom_ops, bound, peak, unit = 2 * macs * batch, "mfma", MFMA_FP4_PEAK_TFLOPS, "TFLOP/s"
     elif kind in ("bconv", "bfc", "bfc_logits") and (g.get("C", g.get("K", 0)) % 64 == 0) \

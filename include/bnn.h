@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define BNN_ABI_VERSION 7
+#define BNN_ABI_VERSION 8
 
 typedef enum bnn_status {
   BNN_OK = 0,
@@ -411,6 +411,44 @@ bnn_status bnn_bfc_pair(int64_t M, int64_t K0, int64_t N0, int64_t N1,
                         uint32_t* out_bits, hipStream_t stream);
 
 /*
+ * Accumulators of the FC tail kernel (bnn_bfc_tail, and bnn_forward's FC
+ * tails at the head of its workspace): 512 rows x 32 outputs x 4 bytes plus
+ * 512 x 8 bytes, 68 KiB.  They must be zero before the first call that uses
+ * them; every call that completes leaves them zero.
+ */
+#define BNN_FORWARD_SYNC_BYTES ((size_t)69632)
+
+/*
+ * Two binary FC layers in one launch (Sec. III-B, Eq. 4 twice), the second
+ * with at most 32 outputs (the classifier tail), spread over the first
+ * layer's output tiles: a workgroup per 32 rows x 32 outputs of layer 0
+ * thresholds them (threshold and flip as in bnn_bgemm) and adds layer 1's
+ * partial sums over those 32 inputs into atomic accumulators in `accum`;
+ * the add that completes an output writes it as an int32 sum (out_sums,
+ * e.g. the logits) or, with thr1, as a bit (out_bits), and zeroes its
+ * accumulator.  The result equals two bnn_bgemm calls, bit for bit.
+ *   M         rows, 1..512.
+ *   K0        layer 0's input bits: a multiple of 1024.
+ *   N0        layer 0's outputs = layer 1's input bits: a multiple of 32,
+ *             with ceil(M / 32) * N0 / 32 <= 512.
+ *   N1        layer 1's outputs: 1..32.
+ *   A, w0, thr0, flip0, w1, thr1, flip1, out_sums, out_bits   as for
+ *             bnn_bfc_pair.
+ *   accum     device, BNN_FORWARD_SYNC_BYTES, 16-byte aligned, zero on
+ *             entry and left zero.  Calls that share it must not overlap in
+ *             time (calls on one stream are ordered).
+ * Shapes outside the above give BNN_ERR_UNSUPPORTED.  A, w0, w1, the output
+ * and accum 16-byte aligned.  Errors: BNN_ERR_NULL, BNN_ERR_SHAPE (also both
+ * outputs given), BNN_ERR_ALIGN, BNN_ERR_UNSUPPORTED, BNN_ERR_HIP.
+ */
+bnn_status bnn_bfc_tail(int64_t M, int64_t K0, int64_t N0, int64_t N1,
+                        const uint32_t* A, const uint32_t* w0,
+                        const int32_t* thr0, const uint32_t* flip0,
+                        const uint32_t* w1, const int32_t* thr1,
+                        const uint32_t* flip1, int32_t* out_sums,
+                        uint32_t* out_bits, void* accum, hipStream_t stream);
+
+/*
  * Binary fully-connected layer / GEMM (Sec. III-B, Eq. 4):
  *   S[m][n] = K - 2 * sum_j popcount(A[m][j] XOR B[n][j])   (valid bits only)
  *   A         [M][Kw] u32, Kw = ceil(K / 32): M packed input vectors.
@@ -455,8 +493,9 @@ typedef struct bnn_layer {
 } bnn_layer;
 
 /*
- * Workspace bytes bnn_forward needs for `batch` images of H x W x C fp32
- * (two ping-pong buffers of packed activations, 256-byte aligned).  Also
+ * Workspace bytes bnn_forward needs for `batch` images of H x W x C fp32:
+ * BNN_FORWARD_SYNC_BYTES of accumulators and two ping-pong buffers of
+ * packed activations (256-byte aligned).  Also
  * validates the chain: the first layer is an input layer (INPUT_THRESHOLD,
  * INPUT_GRAY, INPUT_LBP) or FCONV_BINW, the last is BFC_LOGITS, shapes agree
  * from layer to layer, and an FC layer that
@@ -482,17 +521,30 @@ bnn_status bnn_forward_workspace_size(const bnn_layer* layers,
  *    kernel that keeps the first layer's bits in LDS (bnn_fconv_bconv2d;
  *    option fuse_first = 0 keeps them apart);
  *  - two consecutive BCONVs that fit bnn_bconv_bconv2d (3x3, pad 1, 256
- *    filters each, on a 16-pixel-wide map) run as that one kernel, and so do
- *    two consecutive FC layers that fit bnn_bfc_pair, are not part of a
- *    chained run and have more rows than option gemv_max_rows (option
+ *    filters each, on a 16-pixel-wide map) run as that one kernel (option
  *    fuse_pair = 0 keeps them apart);
+ *  - two consecutive FC layers not part of a chained run, the second with
+ *    at most 32 outputs (Sec. III-B, Eq. 4: the classifier tail), run as
+ *    one kernel: when the batch is at most 512 and the first has K a
+ *    multiple of 1024, N a multiple of 32 and at most 512 output tiles of
+ *    32 rows x 32 outputs, a workgroup per tile adds the second layer's
+ *    partial sums over its 32 outputs into atomic accumulators (the
+ *    workspace's first BNN_FORWARD_SYNC_BYTES: bnn_bfc_tail), and the add
+ *    that completes an output writes it; otherwise, when they fit bnn_bfc_pair and have
+ *    more rows than option gemv_max_rows, that kernel (option fuse_pair = 0
+ *    keeps them apart);
  *  - a run of 2-4 consecutive FC layers of at most 8192 weight words each,
  *    at batch <= 128, runs as one kernel that keeps the intermediate bits of
  *    each row in LDS (option fc_chain = 0 launches them one by one).
  * The results are the same either way.  workspace (device, >= the size
- * above, 256-byte aligned) holds the intermediate bits.  Errors: as the
- * per-layer calls (conv weights not 16-byte aligned: BNN_ERR_ALIGN, also
- * from bnn_forward_workspace_size), plus BNN_ERR_WORKSPACE.
+ * above, 256-byte aligned) holds the intermediate bits, and in its first
+ * BNN_FORWARD_SYNC_BYTES the FC tail's accumulators: those bytes must be zero
+ * before the first call that uses the workspace (one hipMemset after
+ * allocating it), and every call that completes leaves them zero; the rest
+ * needs no initialization.  Calls that use one workspace must not overlap
+ * in time.  Errors: as the per-layer calls (conv weights not 16-byte
+ * aligned: BNN_ERR_ALIGN, also from bnn_forward_workspace_size), plus
+ * BNN_ERR_WORKSPACE.
  */
 bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers,
                        int32_t batch, int32_t H, int32_t W, int32_t C,
@@ -510,10 +562,13 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers,
  *   the current device (else BNN_ERR_UNSUPPORTED).
  * Every call on one GPU shares that GPU's array: calls that overlap in time
  * on one GPU (other streams, or other threads without ordering between them)
- * race and give undefined results; calls on one stream are ordered.  Nothing
- * in the array needs to start at zero (each layer writes every word of its
- * output before the next reads it), and a call leaves the last chain's bits
- * there.  A chain whose bnn_forward_workspace_size exceeds the array gives
+ * race and give undefined results; calls on one stream are ordered.  The
+ * array is laid out as bnn_forward's workspace: its first
+ * BNN_FORWARD_SYNC_BYTES (the FC tail's accumulators) are zero when the library
+ * is loaded and every completed call leaves them zero; nothing else in it
+ * needs to start at zero (each layer writes every word of its output before
+ * the next reads it), and a call leaves the last chain's bits there.  A
+ * chain whose bnn_forward_workspace_size exceeds the array gives
  * BNN_ERR_WORKSPACE before anything is launched.  Other errors as for
  * bnn_forward.
  */

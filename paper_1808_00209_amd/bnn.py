@@ -37,11 +37,15 @@ EXPORTED = ["bnn_last_error", "bnn_abi_version", "bnn_default_options", "bnn_set
             "bnn_get_options", "bnn_pack_bits", "bnn_conv_output_dims",
             "bnn_bconv2d", "bnn_prepared_weights_size", "bnn_prepare_weights",
             "bnn_bconv2d_prepared", "bnn_fconv2d_binw", "bnn_binarize_input", "bnn_bconv2d_input",
-            "bnn_fconv_bconv2d", "bnn_input_bconv_bconv2d", "bnn_bconv_bconv2d", "bnn_bfc_pair", "bnn_bgemm",
+            "bnn_fconv_bconv2d", "bnn_input_bconv_bconv2d", "bnn_bconv_bconv2d", "bnn_bfc_pair", "bnn_bfc_tail",
+            "bnn_bgemm",
             "bnn_forward_workspace_size", "bnn_forward", "bnn_forward_noalloc"]
 
 # Bytes of bnn_forward_noalloc's per-GPU scratch array (BNN_FORWARD_SCRATCH_BYTES).
 FORWARD_SCRATCH_BYTES = 64 << 20
+# Leading workspace bytes that must be zero before a workspace's first use
+# (BNN_FORWARD_SYNC_BYTES: the FC tail kernel's accumulators, left zero by every call).
+FORWARD_SYNC_BYTES = 69632
 
 
 class BnnError(RuntimeError):
@@ -112,6 +116,7 @@ def load(path: str = LIB_PATH):
     lib.bnn_bconv_bconv2d.argtypes = [ctypes.POINTER(ConvDesc), ctypes.POINTER(ConvDesc),
                                       P, P, P, P, P, P, P, P, P]
     lib.bnn_bfc_pair.argtypes = [i64, i64, i64, i64, P, P, P, P, P, P, P, P, P, P]
+    lib.bnn_bfc_tail.argtypes = [i64, i64, i64, i64, P, P, P, P, P, P, P, P, P, P, P]
     lib.bnn_forward_workspace_size.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32,
                                                ctypes.POINTER(ctypes.c_size_t)]
     lib.bnn_forward.argtypes = [ctypes.POINTER(Layer), i32, i32, i32, i32, i32, P, P,
@@ -440,6 +445,33 @@ def bnn_bfc_pair(A, K0, w0, thr0, flip0, w1, N1, thr1=None, flip1=None, out=None
     return out
 
 
+def bnn_bfc_tail(A, K0, w0, thr0, flip0, w1, N1, accum, thr1=None, flip1=None, out=None,
+                 stream=None):
+    """The FC tail kernel: the same two layers as bnn_bfc_pair, spread over
+    layer 0's 32 x 32 output tiles, layer 1's partial sums added in `accum`
+    (FORWARD_SYNC_BYTES, zero on entry and left zero: see accum_buffer)."""
+    lib = load()
+    _u32(A)
+    _u32(w0)
+    _u32(w1)
+    M, N0 = A.shape[0], w0.shape[0]
+    thr0 = _dev(thr0, torch.int32, "thr0")
+    flip0 = _dev(flip0, torch.int32, "flip0")
+    thr1 = _dev(thr1, torch.int32, "thr1")
+    flip1 = _dev(flip1, torch.int32, "flip1")
+    if out is None:
+        out = torch.empty((M, N1) if thr1 is None else (M, 1), dtype=torch.int32, device=A.device)
+    _check(lib.bnn_bfc_tail(M, K0, N0, N1, _ptr(A), _ptr(w0), _ptr(thr0), _ptr(flip0), _ptr(w1),
+                            _ptr(thr1), _ptr(flip1), _ptr(out) if thr1 is None else None,
+                            None if thr1 is None else _ptr(out), _ptr(accum), _stream(stream)))
+    return out
+
+
+def accum_buffer(device="cuda"):
+    """A zeroed accumulator buffer for bnn_bfc_tail (FORWARD_SYNC_BYTES)."""
+    return torch.zeros(FORWARD_SYNC_BYTES, dtype=torch.uint8, device=device)
+
+
 def bnn_bgemm(A, B, K, thr=None, flip=None, want_sums=True, want_bits=True, out_sums=None,
               out_bits=None, stream=None):
     """Binary GEMM / FC (Sec. III-B): A [M,Kw], B [N,Kw] packed -> sums [M,N],
@@ -487,7 +519,10 @@ class Network:
         return out.value
 
     def alloc_workspace(self, batch: int, device="cuda"):
-        return torch.empty(self.workspace_size(batch), dtype=torch.uint8, device=device)
+        """A bnn_forward workspace for `batch` images, its accumulator bytes zeroed."""
+        ws = torch.empty(self.workspace_size(batch), dtype=torch.uint8, device=device)
+        ws[:FORWARD_SYNC_BYTES].zero_()
+        return ws
 
 
 def bnn_forward(net: Network, x, workspace=None, logits=None, stream=None):

@@ -550,6 +550,39 @@ bnn_status bnn_bfc_pair(int64_t M, int64_t K0, int64_t N0, int64_t N1, const uin
   }
 }
 
+bnn_status bnn_bfc_tail(int64_t M, int64_t K0, int64_t N0, int64_t N1, const uint32_t* A,
+                        const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
+                        const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
+                        int32_t* out_sums, uint32_t* out_bits, void* accum,
+                        hipStream_t stream) {
+  try {
+    if (M < 1 || K0 < 1 || N0 < 1 || N1 < 1)
+      return fail(BNN_ERR_SHAPE, "bfc_tail: sizes must be >= 1 (M=%lld K0=%lld N0=%lld N1=%lld)",
+                  (long long)M, (long long)K0, (long long)N0, (long long)N1);
+    if (!bnn::bfc_tail_supported(M, K0, N0, N1))
+      return fail(BNN_ERR_UNSUPPORTED,
+                  "bfc_tail: needs M <= 512, K0 a multiple of 1024, N0 a multiple of 32 with "
+                  "ceil(M / 32) * N0 / 32 <= 512, and N1 <= 32");
+    if (!A || !w0 || !w1) return fail(BNN_ERR_NULL, "bfc_tail: A, w0 or w1 is NULL");
+    if (!thr0) return fail(BNN_ERR_NULL, "bfc_tail: thr0 is NULL");
+    if (!accum) return fail(BNN_ERR_NULL, "bfc_tail: accum is NULL");
+    if (!out_sums && !out_bits)
+      return fail(BNN_ERR_NULL, "bfc_tail: out_sums and out_bits are both NULL");
+    if (out_sums && out_bits)
+      return fail(BNN_ERR_SHAPE, "bfc_tail: give out_sums or out_bits, not both");
+    if (out_bits && !thr1) return fail(BNN_ERR_NULL, "bfc_tail: out_bits requested but thr1 is NULL");
+    if (!aligned16(A) || !aligned16(w0) || !aligned16(w1) || !aligned16(out_sums) ||
+        !aligned16(out_bits) || !aligned16(accum))
+      return fail(BNN_ERR_ALIGN,
+                  "bfc_tail: A, weights, outputs and accum must be 16-byte aligned");
+    return hip_status(bnn::launch_bfc_tail(M, K0, N0, N1, A, w0, thr0, flip0, w1, thr1, flip1,
+                                           out_sums, out_bits, accum, stream),
+                      "bfc_tail launch");
+  } catch (...) {
+    return fail(BNN_ERR_HIP, "bfc_tail: unexpected C++ exception");
+  }
+}
+
 bnn_status bnn_bgemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
                      const uint32_t* B, const int32_t* thr, const uint32_t* flip,
                      int32_t* out_sums, uint32_t* out_bits, hipStream_t stream) {
@@ -572,6 +605,15 @@ constexpr size_t kScratchBytes = BNN_FORWARD_SCRATCH_BYTES;
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
+// bnn_forward's workspace: BNN_FORWARD_SYNC_BYTES of the FC tail kernel's
+// accumulators (zero between calls), then two buffers of `half` bytes for
+// the packed activations.
+static_assert(bnn::kTailAccumBytes <= BNN_FORWARD_SYNC_BYTES, "tail accumulators fit");
+struct WsPlan {
+  size_t half = 0;
+  size_t total() const { return BNN_FORWARD_SYNC_BYTES + 2 * half; }
+};
+
 // Activation state between layers: an NHWC map of packed bits (or, before
 // the first layer, the fp32 input).
 struct Act {
@@ -587,10 +629,10 @@ int input_mode(int32_t kind) {
          : kind == BNN_LAYER_INPUT_LBP ? BNN_INPUT_LBP : BNN_INPUT_THRESHOLD;
 }
 
-// Walks the chain, validating shapes; returns the largest activation size in
-// bytes (packed words) through *max_bytes.
+// Walks the chain, validating shapes; returns the workspace layout (from the
+// largest activation size in bytes, packed words).
 bnn_status plan_chain(const bnn_layer* L, int32_t n, int32_t batch, int32_t H,
-                      int32_t W, int32_t C, size_t* max_bytes) {
+                      int32_t W, int32_t C, WsPlan* plan) {
   if (!L) return fail(BNN_ERR_NULL, "forward: layers is NULL");
   if (n < 1) return fail(BNN_ERR_SHAPE, "forward: need at least one layer");
   if (batch < 1 || H < 1 || W < 1 || C < 1)
@@ -665,7 +707,7 @@ bnn_status plan_chain(const bnn_layer* L, int32_t n, int32_t batch, int32_t H,
       if (bytes > mx) mx = bytes;
     }
   }
-  *max_bytes = mx;
+  plan->half = align_up(mx);
   return BNN_OK;
 }
 
@@ -700,10 +742,10 @@ bnn_status bnn_forward_workspace_size(const bnn_layer* layers, int32_t n_layers,
                                       size_t* bytes) {
   try {
     if (!bytes) return fail(BNN_ERR_NULL, "forward_workspace_size: bytes is NULL");
-    size_t mx = 0;
-    bnn_status st = plan_chain(layers, n_layers, batch, H, W, C, &mx);
+    WsPlan plan;
+    bnn_status st = plan_chain(layers, n_layers, batch, H, W, C, &plan);
     if (st != BNN_OK) return st;
-    *bytes = 2 * align_up(mx);
+    *bytes = plan.total();
     return ok();
   } catch (...) {
     return fail(BNN_ERR_HIP, "forward_workspace_size: unexpected C++ exception");
@@ -721,14 +763,16 @@ static __device__ __align__(256) unsigned char scratch[BNN_FORWARD_SCRATCH_BYTES
 
 namespace {
 
-// The layer chain of bnn_forward on a validated plan: `workspace` holds two
-// buffers of `half` bytes (256-byte aligned) for the packed activations.
+// The layer chain of bnn_forward on a validated plan, with the workspace
+// laid out as WsPlan says (256-byte aligned).
 bnn_status run_chain(const bnn_layer* layers, int32_t n_layers, int32_t batch, int32_t H,
-                     int32_t W, int32_t C, const float* input, void* workspace, size_t half,
-                     int32_t* logits, hipStream_t stream) {
+                     int32_t W, int32_t C, const float* input, void* workspace,
+                     const WsPlan& plan, int32_t* logits, hipStream_t stream) {
   bnn_status st = BNN_OK;
-  uint32_t* buf[2] = {static_cast<uint32_t*>(workspace),
-                      reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + half)};
+  char* const ws = static_cast<char*>(workspace);
+  void* const tail_accum = ws;
+  uint32_t* buf[2] = {reinterpret_cast<uint32_t*>(ws + BNN_FORWARD_SYNC_BYTES),
+                      reinterpret_cast<uint32_t*>(ws + BNN_FORWARD_SYNC_BYTES + plan.half)};
   // An input threshold followed by a conv whose window fits one word runs
   // as one patch-packing kernel on the fp32 image (option fuse_input = 0
   // keeps the two separate steps).
@@ -877,6 +921,27 @@ bnn_status run_chain(const bnn_layer* layers, int32_t n_layers, int32_t batch, i
           li += run - 1;  // the run's last layer; its output is in dst
           break;
         }
+        // Two FC layers, the second with at most 32 outputs (often the
+        // logits), as one launch of the FC kernel over the first layer's
+        // output tiles, which add the second layer's partial sums into
+        // atomic accumulators in the workspace (bfc_gemm.hip).  A
+        // matrix-core kernel, so not under the vector-ALU ablation; option
+        // fuse_pair = 0 launches them apart.
+        if (g_opt.fuse_pair != 0 && g_opt.algo != BNN_ALGO_VALU && li + 1 < n_layers &&
+            (layers[li + 1].kind == BNN_LAYER_BFC || layers[li + 1].kind == BNN_LAYER_BFC_LOGITS) &&
+            layers[li + 1].K == l.N && bnn::bfc_tail_supported(batch, l.K, l.N, layers[li + 1].N)) {
+          const bnn_layer& l2 = layers[li + 1];
+          const bool lg = l2.kind == BNN_LAYER_BFC_LOGITS;
+          e = bnn::launch_bfc_tail(batch, l.K, l.N, l2.N, src, l.w, l.thr, l.flip, l2.w,
+                                   lg ? nullptr : l2.thr, lg ? nullptr : l2.flip,
+                                   lg ? logits : nullptr, lg ? nullptr : dst, tail_accum, stream);
+          if (e != hipSuccess) return fail(BNN_ERR_HIP, "forward: layers %d-%d launch: %s", li,
+                                           li + 1, hipGetErrorString(e));
+          h = w = 1;
+          c = l2.N;
+          ++li;  // the pair's second layer; its output is in dst (or the logits)
+          break;
+        }
         // Two FC layers that fit one kernel (the second with at most 32
         // outputs, often the logits) run as one, the first layer's bits kept
         // in LDS, where the GEMM path would take them (rows above
@@ -965,8 +1030,8 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
                        void* workspace, size_t ws_bytes, int32_t* logits,
                        hipStream_t stream) {
   try {
-    size_t mx = 0;
-    bnn_status st = plan_chain(layers, n_layers, batch, H, W, C, &mx);
+    WsPlan plan;
+    bnn_status st = plan_chain(layers, n_layers, batch, H, W, C, &plan);
     if (st != BNN_OK) return st;
     if (!input || !logits || !workspace)
       return fail(BNN_ERR_NULL, "forward: input, logits and workspace must be non-NULL");
@@ -974,11 +1039,10 @@ bnn_status bnn_forward(const bnn_layer* layers, int32_t n_layers, int32_t batch,
         (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
       return fail(BNN_ERR_ALIGN,
                   "forward: input/logits must be 16-byte aligned, workspace 256-byte aligned");
-    const size_t half = align_up(mx);
-    if (ws_bytes < 2 * half)
+    if (ws_bytes < plan.total())
       return fail(BNN_ERR_WORKSPACE, "forward: workspace of %zu bytes, need %zu", ws_bytes,
-                  2 * half);
-    return run_chain(layers, n_layers, batch, H, W, C, input, workspace, half, logits, stream);
+                  plan.total());
+    return run_chain(layers, n_layers, batch, H, W, C, input, workspace, plan, logits, stream);
   } catch (...) {
     return fail(BNN_ERR_HIP, "forward: unexpected C++ exception");
   }
@@ -988,23 +1052,22 @@ bnn_status bnn_forward_noalloc(const bnn_layer* layers, int32_t n_layers, int32_
                                int32_t H, int32_t W, int32_t C, const float* input,
                                int32_t* logits, hipStream_t stream) {
   try {
-    size_t mx = 0;
-    bnn_status st = plan_chain(layers, n_layers, batch, H, W, C, &mx);
+    WsPlan plan;
+    bnn_status st = plan_chain(layers, n_layers, batch, H, W, C, &plan);
     if (st != BNN_OK) return st;
     if (!input || !logits)
       return fail(BNN_ERR_NULL, "forward_noalloc: input and logits must be non-NULL");
     if (!aligned16(input) || !aligned16(logits))
       return fail(BNN_ERR_ALIGN, "forward_noalloc: input/logits must be 16-byte aligned");
-    const size_t half = align_up(mx);
-    if (2 * half > kScratchBytes)
+    if (plan.total() > kScratchBytes)
       return fail(BNN_ERR_WORKSPACE,
-                  "forward_noalloc: the chain needs %zu bytes of intermediate bits, more than "
-                  "the %zu of the library's scratch array (use bnn_forward with a workspace)",
-                  2 * half, kScratchBytes);
+                  "forward_noalloc: the chain needs %zu bytes of workspace, more than the %zu "
+                  "of the library's scratch array (use bnn_forward with a workspace)",
+                  plan.total(), kScratchBytes);
     void* ws = nullptr;
     st = scratch_of_device(stream, &ws);
     if (st != BNN_OK) return st;
-    return run_chain(layers, n_layers, batch, H, W, C, input, ws, half, logits, stream);
+    return run_chain(layers, n_layers, batch, H, W, C, input, ws, plan, logits, stream);
   } catch (...) {
     return fail(BNN_ERR_HIP, "forward_noalloc: unexpected C++ exception");
   }

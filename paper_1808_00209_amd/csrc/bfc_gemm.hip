@@ -43,6 +43,21 @@ struct GmArgs {
   int32_t a_bytes, b_bytes;
 };
 
+// The second layer of an FC tail (bnn_forward's FC pairs whose second layer
+// has at most 32 outputs): w1 [N1][N / 32], thr1 / flip1 for bits out (else
+// int32 sums out), and the accumulators: acc [kTailMaxRows][32] and wacc
+// [kTailMaxRows], zero on entry and left zero.
+struct TailArgs {
+  const uint32_t* w1;
+  const int32_t* thr1;
+  const uint32_t* flip1;
+  int32_t* sums;   // [M][N1] or null
+  uint32_t* bits;  // [M][1] or null
+  uint32_t* acc;
+  unsigned long long* wacc;
+  int32_t N1;
+};
+
 constexpr uint32_t kRsrcWord3 = 0x00020000;
 
 // Sign bits of a 32 x 32 tile's accumulators: register e of lane (h, c)
@@ -64,13 +79,76 @@ __device__ __forceinline__ uint32_t sign_word(const v16f& acc, int h) {
 // TPB x TFB output tiles of 32 x 32 per workgroup (rows x outputs) and KS
 // waves per tile, each taking 1 / KS of K (TPB TFB KS = 8 waves): wave w
 // computes tile (w % TPB, (w / TPB) % TFB) over slice w / (TPB TFB) of K.
-template <int TPB, int TFB, int KS>
-__global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a) {
+// The tail of an FC pair, run by every thread of the workgroup that holds
+// the first layer's 32 x 32 sums of rows m0 .. m0 + 31 and outputs
+// 32 ft .. 32 ft + 31 in `tile` (MFMA layout).  Wave 0 thresholds them into
+// one word per row; then each (row, tail output j) adds its partial sum over
+// these 32 inputs, p = 32 - 2 popcount(word xor w1[j][ft]) (Eq. 4 on one
+// word), to its accumulator with one atomic add of 2^17 + (p + 32): the high
+// bits count the slices added, the low 17 bits their biased sum (at most
+// 64 G < 2^17 for G = N / 32 <= 1024 slices).  The add that brings the count
+// to G returns every other slice's contribution, so that thread alone writes
+// the sum S = low bits + p + 32 - 32 G (or its bit) and zeroes the
+// accumulator.  Bits out: the thread that finishes output j of a row adds
+// 2^32 + its bit to the row's 64-bit word accumulator, and the add that
+// brings that count to N1 writes the flipped word.  Read-modify-writes on
+// one location are totally ordered, so no fence and no waiting between
+// workgroups is needed, whichever XCD each runs on.
+__device__ __forceinline__ void fc_tail(const GmArgs& a, const TailArgs& t, const float* tile,
+                                        const float* th, const uint32_t* w1c,
+                                        const int32_t* thr1s, int tid, int lane, int h, int c,
+                                        int ft, int m0) {
+  __shared__ uint32_t wrow[32];
+  const int G = a.N / 32;
+  if (tid < 64) {
+    v16f d;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) d[e] = tile[e * 64 + lane] + th[8 * (e >> 2) + 4 * h + (e & 3)];
+    // output bit = (S >= thr) xor flip = sign xor ~flip
+    const uint32_t word = or_xor32(sign_word(d, h)) ^ ~(a.flip ? a.flip[ft] : 0u);
+    if (h == 0) wrow[c] = word;
+  }
+  __syncthreads();
+  const int rows = min(32, a.M - m0);
+  for (int e = tid; e < rows * t.N1; e += kNT) {
+    const int cc = e / t.N1, j = e - cc * t.N1;
+    const int m = m0 + cc;
+    const int p = 32 - 2 * __builtin_popcount(wrow[cc] ^ w1c[j]);
+    uint32_t* acc = &t.acc[m * 32 + j];
+    const uint32_t add = (1u << 17) + static_cast<uint32_t>(p + 32);
+    const uint32_t old =
+        __hip_atomic_fetch_add(acc, add, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (static_cast<int>(old >> 17) != G - 1) continue;
+    __hip_atomic_store(acc, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int32_t S = static_cast<int32_t>(old & 0x1FFFFu) + p + 32 - 32 * G;
+    if (t.sums) {
+      t.sums[static_cast<size_t>(m) * t.N1 + j] = S;
+      continue;
+    }
+    const unsigned long long wadd =
+        (1ull << 32) | (S >= thr1s[j] ? (0x80000000ull >> j) : 0ull);
+    unsigned long long* wa = &t.wacc[m];
+    const unsigned long long wold =
+        __hip_atomic_fetch_add(wa, wadd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (static_cast<int>(wold >> 32) != t.N1 - 1) continue;
+    __hip_atomic_store(wa, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t word = static_cast<uint32_t>(wold + wadd);
+    t.bits[m] = (word ^ (t.flip1 ? t.flip1[0] : 0u)) & tail_mask(t.N1);
+  }
+}
+
+// With TAIL (one tile per workgroup only) the tile's thresholded bits feed the
+// tail layer instead of memory (fc_tail below).
+template <int TPB, int TFB, int KS, bool TAIL = false>
+__global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a, TailArgs t) {
   static_assert(TPB * TFB * KS == kNW, "8 waves");
+  static_assert(!TAIL || (TPB * TFB == 1 && KS > 1), "the tail takes one tile per workgroup");
   constexpr int NTL = TPB * TFB;  // tiles per workgroup
   __shared__ __attribute__((aligned(16))) uint32_t stg[kNW][2][32 * kRS];
   __shared__ float part[kNW][16 * 64];
   __shared__ float th[32 * TFB];
+  __shared__ uint32_t w1c[TAIL ? 32 : 1];
+  __shared__ int32_t thr1s[TAIL ? 32 : 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -82,10 +160,18 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a) {
   const int tp = wave % TPB, tf = (wave / TPB) % TFB, ks = wave / NTL;
   const int ft = ft0 + tf;
   const int m0 = m00 + 32 * tp, n0 = 32 * ft;
-  const bool want_bits = a.bits != nullptr;
-  if (want_bits && tid < 32 * TFB) {
-    const int32_t K = 32 * a.Kw;
-    th[tid] = 0.5f - static_cast<float>(min(max(a.thr[32 * ft0 + tid], -K - 1), K + 1));
+  const bool want_bits = TAIL || a.bits != nullptr;
+  // Thresholds (and the tail's weight words and thresholds) are loaded here
+  // but stored to LDS only after the main loop, so that the wait for them
+  // does not hold back the first operand loads.
+  int32_t thv = 0, t1v = 0;
+  uint32_t w1v = 0;
+  const bool th_lane = want_bits && tid < 32 * TFB;
+  if (th_lane) thv = a.thr[32 * ft0 + tid];
+  const bool tail_lane = TAIL && tid >= 64 && tid < 64 + t.N1;
+  if (tail_lane) {
+    w1v = t.w1[static_cast<size_t>(tid - 64) * (a.N / 32) + ft0];
+    if (t.thr1) t1v = t.thr1[tid - 64];
   }
 
   const __amdgpu_buffer_rsrc_t ra =
@@ -150,6 +236,14 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a) {
       acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(A1, B1, acc, 4, 4, 0, 127, 0, 127);
     }
   }
+  if (th_lane) {
+    const int32_t K = 32 * a.Kw;
+    th[tid] = 0.5f - static_cast<float>(min(max(thv, -K - 1), K + 1));
+  }
+  if (tail_lane) {
+    w1c[tid - 64] = w1v;
+    thr1s[tid - 64] = t1v;
+  }
   // The KS partial tiles of each output tile meet in LDS (exact: integer
   // sums below 2^24): with one tile all threads add the slots slice by
   // slice; with several, the slice-0 wave of each tile adds the others'.
@@ -169,6 +263,10 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a) {
         part[0][v] = t;
       }
       __syncthreads();
+      if constexpr (TAIL) {
+        fc_tail(a, t, part[0], th, w1c, thr1s, tid, lane, h, c, ft, m0);
+        return;
+      }
       if (wave > 0) return;
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[e] = part[0][e * 64 + lane];
@@ -213,7 +311,7 @@ template <int TPB, int TFB, int KS>
 void launch_tiles(const GmArgs& a, hipStream_t s) {
   const unsigned blocks =
       static_cast<unsigned>(((a.M + 32 * TPB - 1) / (32 * TPB)) * (a.N / (32 * TFB)));
-  bfc_gemm_kernel<TPB, TFB, KS><<<blocks, kNT, 0, s>>>(a);
+  bfc_gemm_kernel<TPB, TFB, KS><<<blocks, kNT, 0, s>>>(a, TailArgs{});
 }
 
 }  // namespace
@@ -247,6 +345,42 @@ hipError_t launch_bfc_gemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
     launch_tiles<1, 1, 8>(a, s);
   else
     launch_tiles<2, 2, 2>(a, s);
+  return hipGetLastError();
+}
+
+bool bfc_tail_supported(int64_t M, int64_t K0, int64_t N0, int64_t N1) {
+  return bfc_gemm_supported(M, N0, K0) && M <= kTailMaxRows && N0 <= 32 * 1024 && N1 >= 1 &&
+         N1 <= 32 && ((M + 31) / 32) * (N0 / 32) <= 512;
+}
+
+hipError_t launch_bfc_tail(int64_t M, int64_t K0, int64_t N0, int64_t N1, const uint32_t* A,
+                           const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
+                           const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
+                           int32_t* sums, uint32_t* bits, void* accum, hipStream_t s) {
+  GmArgs a;
+  a.A = A;
+  a.B = w0;
+  a.thr = thr0;
+  a.flip = flip0;
+  a.sums = nullptr;
+  a.bits = nullptr;
+  a.M = static_cast<int32_t>(M);
+  a.N = static_cast<int32_t>(N0);
+  a.Kw = static_cast<int32_t>(K0 / 32);
+  a.a_bytes = static_cast<int32_t>(M * (K0 / 8));
+  a.b_bytes = static_cast<int32_t>(N0 * (K0 / 8));
+  TailArgs t;
+  t.w1 = w1;
+  t.thr1 = thr1;
+  t.flip1 = flip1;
+  t.sums = sums;
+  t.bits = bits;
+  t.acc = static_cast<uint32_t*>(accum);
+  t.wacc = reinterpret_cast<unsigned long long*>(static_cast<uint32_t*>(accum) +
+                                                  kTailMaxRows * 32);
+  t.N1 = static_cast<int32_t>(N1);
+  const unsigned blocks = static_cast<unsigned>(((M + 31) / 32) * (N0 / 32));
+  bfc_gemm_kernel<1, 1, 8, true><<<blocks, kNT, 0, s>>>(a, t);
   return hipGetLastError();
 }
 

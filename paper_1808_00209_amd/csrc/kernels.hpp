@@ -149,6 +149,22 @@ hipError_t launch_bfc_gemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
                            const uint32_t* B, const int32_t* thr, const uint32_t* flip,
                            int32_t* sums, uint32_t* bits, hipStream_t s);
 
+// Two consecutive binary FC layers, the second with N1 <= 32 outputs, in one
+// launch of the FC kernel (bfc_gemm.hip): a workgroup per 32 x 32 tile of the
+// first layer (K0 a multiple of 1024, N0 of 32, at most 512 tiles, at most
+// kTailMaxRows rows), each adding the second layer's partial sums over its
+// 32 inputs to accumulators in `accum` (kTailAccumBytes, zero on entry and
+// left zero) with atomic adds; the add that completes an output writes it:
+// int32 sums [M][N1] (sums non-null) or bits [M][1] (thr1 non-null).
+// Packed weights; w1 [N1][N0 / 32].
+constexpr int kTailMaxRows = 512;
+constexpr size_t kTailAccumBytes = size_t{kTailMaxRows} * 32 * 4 + size_t{kTailMaxRows} * 8;
+bool bfc_tail_supported(int64_t M, int64_t K0, int64_t N0, int64_t N1);
+hipError_t launch_bfc_tail(int64_t M, int64_t K0, int64_t N0, int64_t N1, const uint32_t* A,
+                           const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
+                           const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
+                           int32_t* sums, uint32_t* bits, void* accum, hipStream_t s);
+
 // Two consecutive binary FC layers in one launch (bfc_pair.hip), the first
 // layer's output bits kept in LDS: K0 = 512 or 1024 input bits,
 // N0 = 256, 512 or 1024 first-layer outputs (thresholded, with flips), N1 <= 32

@@ -258,6 +258,40 @@ def test_bfc_pair_errors():
 
 
 @needs_lib
+def test_bfc_tail_errors():
+    """bnn_bfc_tail: sizes, the shapes its kernel covers (rows, K0, N0, tile
+    count, N1), one output of the two, NULL pointers (accum included) and
+    alignment, all refused on the host."""
+    lib = bnn.load()
+
+    def call(M=64, K0=1024, N0=1024, N1=10, a=A, w0=A, thr0=A, w1=A, thr1=None, sums=A,
+             bits=None, accum=A):
+        return lib.bnn_bfc_tail(M, K0, N0, N1, a, w0, thr0, None, w1, thr1, None, sums, bits,
+                                accum, None)
+
+    for bad in (dict(M=0), dict(K0=0), dict(N0=0), dict(N1=0), dict(N1=-3)):
+        assert call(**bad) == 2, bad
+    # K0 not a multiple of 1024, N0 not of 32, more than 512 rows or 512
+    # tiles (64 rows x 9216 outputs: 2 x 288), N1 > 32
+    for uns in (dict(K0=1000), dict(K0=1536), dict(N0=1000), dict(M=513), dict(N0=9216),
+                dict(M=40, N0=9216), dict(N1=33)):
+        assert call(**uns) == 4, uns
+    assert call(a=None) == 1
+    assert call(w0=None) == 1
+    assert call(w1=None) == 1
+    assert call(thr0=None) == 1 and "thr0" in bnn.last_error()
+    assert call(accum=None) == 1 and "accum" in bnn.last_error()
+    assert call(sums=None, bits=None) == 1
+    assert call(sums=A, bits=A, thr1=A) == 2 and "not both" in bnn.last_error()
+    assert call(sums=None, bits=A, thr1=None) == 1 and "thr1" in bnn.last_error()
+    assert call(a=A + 4) == 3
+    assert call(w1=A + 4) == 3
+    assert call(sums=A + 4) == 3
+    assert call(accum=A + 4) == 3
+    assert call(sums=None, bits=A + 4, thr1=A) == 3
+
+
+@needs_lib
 def test_binarize_input_errors():
     lib = bnn.load()
     assert lib.bnn_binarize_input(5, A, None, 1, 4, 4, 3, A, None) == 2
@@ -317,9 +351,10 @@ def test_forward_chain_validation():
             dict(kind=5, K=2 * 2 * 64, N=4, w=A)]
     L = _layers(good)
     assert lib.bnn_forward_workspace_size(L, 4, 8, 8, 8, 3, ctypes.byref(size)) == 0
-    # two buffers of the largest packed map, the thresholded input:
-    # 8 images x 8x8 pixels x 1 word x 4 bytes, 256-byte aligned
-    assert size.value == 2 * 256 * ((8 * 8 * 8 * 1 * 4 + 255) // 256)
+    # the FC tail's 69632 accumulator bytes and two buffers of the largest
+    # packed map, the thresholded input: 8 images x 8x8 pixels x 1 word x 4
+    # bytes, 256-byte aligned
+    assert size.value == 69632 + 2 * 256 * ((8 * 8 * 8 * 1 * 4 + 255) // 256)
     bad_k = [dict(good[0]), dict(good[1]), dict(good[2]), dict(good[3], K=100)]
     assert lib.bnn_forward_workspace_size(_layers(bad_k), 4, 8, 8, 8, 3, ctypes.byref(size)) == 2
     assert "expects K" in bnn.last_error()
@@ -356,12 +391,16 @@ def test_forward_noalloc_validation_before_any_device_call():
             dict(kind=5, K=2 * 2 * 64, N=4, w=A)]
     L = _layers(good)
     size = ctypes.c_size_t()
-    # 8 x 8 images: two buffers of the thresholded input, batch * 64 pixels *
-    # 1 word * 4 bytes; the largest batch that fits the 64 MiB array is 131072
-    for batch, fits in ((131072, True), (131073, False)):
+    # 8 x 8 images: BNN_FORWARD_SYNC_BYTES of accumulators and two buffers of
+    # the thresholded input, batch * 64 pixels * 1 word * 4 bytes; the
+    # largest batch that fits the 64 MiB array is (64 MiB - 69632) / 512 = 130936
+    assert "#define BNN_FORWARD_SYNC_BYTES ((size_t)69632)" in header
+    assert bnn.FORWARD_SYNC_BYTES == 69632
+    for batch, fits in ((130936, True), (130937, False)):
         assert lib.bnn_forward_workspace_size(L, 4, batch, 8, 8, 3, ctypes.byref(size)) == 0
+        assert size.value == 69632 + 2 * batch * 256
         assert (size.value <= bnn.FORWARD_SCRATCH_BYTES) == fits
-    assert lib.bnn_forward_noalloc(L, 4, 131073, 8, 8, 3, A, A, None) == 6
+    assert lib.bnn_forward_noalloc(L, 4, 130937, 8, 8, 3, A, A, None) == 6
     assert "scratch" in bnn.last_error()
     assert lib.bnn_forward_noalloc(L, 4, 8, 8, 8, 3, None, A, None) == 1
     assert lib.bnn_forward_noalloc(L, 4, 8, 8, 8, 3, A, A + 4, None) == 3

@@ -7,8 +7,10 @@ full-size workloads is compared with the CPU oracle:
   int32 sums (Eq. 3 and Eq. 4 with the threshold / flip epilogue);
 * each layer of the CIFAR-shaped net at batch 64 and of the vehicle-shaped
   net at batch 256 through its own entry point, bits only as bnn_forward
-  calls it, fed with the oracle's activations of the layer before (the
-  logits of every image through bnn_forward are in test_gpu_forward.py).
+  calls it, fed with the oracle's activations of the layer before, and the
+  fused kernels bnn_forward runs (first layers, conv pairs, the FC tail)
+  the same way (the logits of every image through bnn_forward are in
+  test_gpu_forward.py).
 The oracle's results are computed once per module run.
 """
 import functools
@@ -177,3 +179,18 @@ def test_every_layer_bits_at_full_batch(cfg, batch, algo):
             sums, _ = bnn.bnn_bgemm(src, d["w"], L["K"], want_bits=False)
             torch.cuda.synchronize()
             assert np.array_equal(sums.cpu().numpy(), outs[li]), "logits"
+        # the FC tail bnn_forward runs as one kernel (bnn_bfc_tail)
+        P = layers[li - 1]
+        if (P["kind"] == "bfc" and L["N"] <= 32 and algo != "valu" and N <= 512
+                and P["K"] % 1024 == 0 and P["N"] % 32 == 0
+                and ((N + 31) // 32) * (P["N"] // 32) <= 512):
+            dp = dev[li - 1]
+            lg = k == "bfc_logits"
+            tb = bnn.bnn_bfc_tail(pack_pm1(outs[li - 2].reshape(N, -1)), P["K"], dp["w"],
+                                  dp["thr"], dp.get("flip"), d["w"], L["N"], bnn.accum_buffer(),
+                                  None if lg else d["thr"], None if lg else d.get("flip"))
+            torch.cuda.synchronize()
+            if lg:
+                assert np.array_equal(tb.cpu().numpy(), outs[li]), "FC tail"
+            else:
+                assert np.array_equal(words_u32(tb), _packed(outs[li])), "FC tail"
