@@ -72,30 +72,46 @@ constexpr int window_iters() { return 9 * (CW / (2 * (CW % 4 == 0 ? 2 : 1))); }
 // read through a buffer resource, expanded per k-step.  Iterations IT0 ..
 // IT1 - 1 of the window (all of it by default).  Accumulators start from
 // acc.
-template <int CW, int TP, int RS, int PS, int IT0 = 0, int IT1 = window_iters<CW>()>
-__device__ __forceinline__ void conv_tile(const v4i* act, const int (&abase)[TP],
-                                          const uint32_t* w, int w_bytes, int ft, int lane,
-                                          uint32_t smask, uint32_t vfill, v16f (&acc)[TP]) {
-  constexpr int VW = CW % 4 == 0 ? 2 : 1;  // words per lane per iteration
-  constexpr int NCH = CW / (2 * VW);       // iterations per tap
+// Weight words of iteration `it` for lane (h, c) of 32-filter tile ft: VW
+// words of filter 32 ft + c at tap it / NCH, words 2 VW (it % NCH) + h VW ..
+template <int CW>
+__device__ __forceinline__ void tile_w_load(const uint32_t* w, int w_bytes, int ft, int lane,
+                                            int it, uint32_t (&ww)[CW % 4 == 0 ? 2 : 1]) {
+  constexpr int VW = CW % 4 == 0 ? 2 : 1;
+  constexpr int NCH = CW / (2 * VW);
   const int h = lane >> 5, c = lane & 31;
   const __amdgpu_buffer_rsrc_t rw =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(w), 0, w_bytes, kRsrcWord3);
   const uint32_t woff = static_cast<uint32_t>(((32 * ft + c) * 9 * CW + h * VW) * 4);
-  auto load_w = [&](int it, uint32_t (&ww)[VW]) {
-    const int tap = it / NCH, cc = (it - tap * NCH) * 2 * VW;
-    const uint32_t so = static_cast<uint32_t>((tap * CW + cc) * 4);
-    if constexpr (VW == 2) {
-      typedef unsigned int u2 __attribute__((ext_vector_type(2)));
-      const u2 t = __builtin_amdgcn_raw_buffer_load_b64(rw, woff, so, 0);
-      ww[0] = t[0];
-      ww[1] = t[1];
-    } else {
-      ww[0] = __builtin_amdgcn_raw_buffer_load_b32(rw, woff, so, 0);
-    }
-  };
+  const int tap = it / NCH, cc = (it - tap * NCH) * 2 * VW;
+  const uint32_t so = static_cast<uint32_t>((tap * CW + cc) * 4);
+  if constexpr (VW == 2) {
+    typedef unsigned int u2 __attribute__((ext_vector_type(2)));
+    const u2 t = __builtin_amdgcn_raw_buffer_load_b64(rw, woff, so, 0);
+    ww[0] = t[0];
+    ww[1] = t[1];
+  } else {
+    ww[0] = __builtin_amdgcn_raw_buffer_load_b32(rw, woff, so, 0);
+  }
+}
+
+// With `first` non-null it holds iteration IT0's weight words, loaded by the
+// caller (tile_w_load) ahead of its staging.
+template <int CW, int TP, int RS, int PS, int IT0 = 0, int IT1 = window_iters<CW>()>
+__device__ __forceinline__ void conv_tile(const v4i* act, const int (&abase)[TP],
+                                          const uint32_t* w, int w_bytes, int ft, int lane,
+                                          uint32_t smask, uint32_t vfill, v16f (&acc)[TP],
+                                          const uint32_t* first = nullptr) {
+  constexpr int VW = CW % 4 == 0 ? 2 : 1;  // words per lane per iteration
+  constexpr int NCH = CW / (2 * VW);       // iterations per tap
+  auto load_w = [&](int it, uint32_t (&ww)[VW]) { tile_w_load<CW>(w, w_bytes, ft, lane, it, ww); };
   uint32_t wr[2][VW];
-  load_w(IT0, wr[0]);
+  if (first) {
+#pragma unroll
+    for (int v = 0; v < VW; ++v) wr[0][v] = first[v];
+  } else {
+    load_w(IT0, wr[0]);
+  }
 #pragma unroll
   for (int it = IT0; it < IT1; ++it) {
     const int cur = (it - IT0) & 1;
@@ -375,6 +391,9 @@ __global__ __launch_bounds__(2 * FPB * 2) void bconv_img8_kernel(ImArgs a) {
   }
   const int32_t thv = a.thr[min(FPB * fg + tid, a.F - 1)];
   const uint32_t nfl = ~(a.flip ? a.flip[ft] : 0u);
+  // This wave's first weight words, in flight during the staging.
+  uint32_t wfirst[CW % 4 == 0 ? 2 : 1];
+  tile_w_load<CW>(a.w, a.w_bytes, ft, lane, kh ? HALF : 0, wfirst);
   const uint32_t smask = __builtin_amdgcn_readfirstlane(0x88888888u);
   uint32_t vfill;
   asm("v_mov_b32 %0, 0x22222222" : "=v"(vfill));
@@ -412,9 +431,11 @@ __global__ __launch_bounds__(2 * FPB * 2) void bconv_img8_kernel(ImArgs a) {
     acc[1] = t;
   }
   if (kh)
-    conv_tile<CW, 2, RS, PS, HALF, ITERS>(xa, bbase, a.w, a.w_bytes, ft, lane, smask, vfill, acc);
+    conv_tile<CW, 2, RS, PS, HALF, ITERS>(xa, bbase, a.w, a.w_bytes, ft, lane, smask, vfill, acc,
+                                          wfirst);
   else
-    conv_tile<CW, 2, RS, PS, 0, HALF>(xa, bbase, a.w, a.w_bytes, ft, lane, smask, vfill, acc);
+    conv_tile<CW, 2, RS, PS, 0, HALF>(xa, bbase, a.w, a.w_bytes, ft, lane, smask, vfill, acc,
+                                      wfirst);
   // The second half's partial tiles to LDS, one barrier, the first half adds
   // them (exact: integer sums below 2^24).
   float* pp = part[wave >> 1];
