@@ -45,11 +45,11 @@ _FP4 = ("paper_1808_00209_amd/csrc/fp4_expand.hpp",
 _LANE = ("paper_1808_00209_amd/csrc/lane_ops.hpp",
          "96ece7042c6ed72e9cd799fdd8e007525e30035bbd8d052a9ece380c5e3fda82")
 _KERN = ("paper_1808_00209_amd/csrc/kernels.hpp",
-         "43844ac76042685c6998681919abec925b4eee23c45b886f3800e646ab1541fa")
+         "eb768959ffadf5eb2d62938c518e392de2524164e10278487a5f14f55d69f013")
 MEASURED_TRAFFIC = {
     # profiles/fconv_bconv_cifar_b64.md
     ("cifar_bnn_b64", "L0+L1 fconv+bconv 32x32x3->128->128 k3 pool (fused)"): dict(
-        fetch_kib=980.8, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
+        fetch_kib=980.7, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/fconv_bconv.hip",
                        "b9775a39d56ce451c281b54dceafe567d2fc9cc81ff7a7752a4c1a83d8de96f3"),
                       ("paper_1808_00209_amd/csrc/fp32_split.hpp",
@@ -59,12 +59,12 @@ MEASURED_TRAFFIC = {
     ("cifar_bnn_b64", "L2+L3 bconv+bconv 16x16x128->256->256 k3 pool (fused)"): dict(
         fetch_kib=858.2, write_kib=128.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/bconv_bconv.hip",
-                       "a420dbc535694f6a02d8b0f9334f472acb9aeacd217f74d9783b7da0beed81b4"),
+                       "4967ccbad87efa16575172abf11b76792b74433995d15760fb64a86b724adf26"),
                       _FP4, _LANE, _KERN]), flags=_FLAGS),
     ("cifar_bnn_b64", "L5 bconv 8x8x512->512 k3 pool"): dict(
         fetch_kib=898.0, write_kib=128.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/bconv_bconv.hip",
-                       "a420dbc535694f6a02d8b0f9334f472acb9aeacd217f74d9783b7da0beed81b4"),
+                       "4967ccbad87efa16575172abf11b76792b74433995d15760fb64a86b724adf26"),
                       _FP4, _LANE, _KERN]), flags=_FLAGS),
 }
 
