@@ -273,10 +273,10 @@ def layer_shapes(layers, H, W, C, batch=None):
 
 def tail_fusable(L0, L1, batch):
     """Whether bnn_forward runs two FC layers as the FC tail kernel: at most
-    512 rows, the first layer's K a multiple of 1024 and N of 32 with at most
+    512 rows, the first layer's K at least 1024 and N a multiple of 32 with at most
     512 tiles of 32 x 32, the second with at most 32 outputs."""
     K, N0, N1 = L0["K"], L0["N"], L1["N"]
-    return (batch <= 512 and K % 1024 == 0 and N0 % 32 == 0 and N1 <= 32
+    return (batch <= 512 and K >= 1024 and N0 % 32 == 0 and N1 <= 32
             and ((batch + 31) // 32) * (N0 // 32) <= 512)
 
 

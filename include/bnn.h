@@ -428,7 +428,7 @@ bnn_status bnn_bfc_pair(int64_t M, int64_t K0, int64_t N0, int64_t N1,
  * e.g. the logits) or, with thr1, as a bit (out_bits), and zeroes its
  * accumulator.  The result equals two bnn_bgemm calls, bit for bit.
  *   M         rows, 1..512.
- *   K0        layer 0's input bits: a multiple of 1024.
+ *   K0        layer 0's input bits: at least 1024.
  *   N0        layer 0's outputs = layer 1's input bits: a multiple of 32,
  *             with ceil(M / 32) * N0 / 32 <= 512.
  *   N1        layer 1's outputs: 1..32.
@@ -525,14 +525,14 @@ bnn_status bnn_forward_workspace_size(const bnn_layer* layers,
  *    fuse_pair = 0 keeps them apart);
  *  - two consecutive FC layers not part of a chained run, the second with
  *    at most 32 outputs (Sec. III-B, Eq. 4: the classifier tail), run as
- *    one kernel: when the batch is at most 512 and the first has K a
- *    multiple of 1024, N a multiple of 32 and at most 512 output tiles of
- *    32 rows x 32 outputs, a workgroup per tile adds the second layer's
- *    partial sums over its 32 outputs into atomic accumulators (the
- *    workspace's first BNN_FORWARD_SYNC_BYTES: bnn_bfc_tail), and the add
- *    that completes an output writes it; otherwise, when they fit bnn_bfc_pair and have
- *    more rows than option gemv_max_rows, that kernel (option fuse_pair = 0
- *    keeps them apart);
+ *    one kernel: when the batch is at most 512 and the first has K of at
+ *    least 1024, N a multiple of 32 and at most 512 output tiles of 32 rows
+ *    x 32 outputs, a workgroup per tile adds the second layer's partial
+ *    sums over its 32 outputs into atomic accumulators (the workspace's
+ *    first BNN_FORWARD_SYNC_BYTES: bnn_bfc_tail), and the add that
+ *    completes an output writes it; otherwise, when they fit bnn_bfc_pair
+ *    and have more rows than option gemv_max_rows, that kernel (option
+ *    fuse_pair = 0 keeps them apart);
  *  - a run of 2-4 consecutive FC layers of at most 8192 weight words each,
  *    at batch <= 128, runs as one kernel that keeps the intermediate bits of
  *    each row in LDS (option fc_chain = 0 launches them one by one).

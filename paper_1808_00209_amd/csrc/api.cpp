@@ -174,9 +174,10 @@ bnn_status gemm_launch(int64_t M, int64_t N, int64_t K, const uint32_t* A,
   if (M <= g_opt.gemv_max_rows)
     return hip_status(bnn::launch_bgemv_valu(M, N, K, A, B, thr, flip, sums, bits, s),
                       "bgemm (gemv) launch");
-  // K a multiple of 1024: the FC kernel (bfc_gemm.hip), a workgroup per
-  // 32 x 32 output tile up to 512 tiles, per 2 x 2 tiles above that when N is
-  // a multiple of 64.  Graph-timed, bits only: 64 x 8192 -> 1024 4.7 us
+  // K >= 1024 and N a multiple of 32: the FC kernel (bfc_gemm.hip), a
+  // workgroup per 32 x 32 output tile up to 512 tiles, per 2 x 2 tiles above
+  // that when N is a multiple of 64 (K not a multiple of the K split:
+  // padded, see the kernel).  Graph-timed, bits only: 64 x 8192 -> 1024 4.7 us
   // against 6.65 us in the conv kernel, 256 x 18432 -> 1024 8.2 against
   // 10.4 us, 64 x 1024 -> 1024 3.7 against 4.2 us; 256 x 4096 -> 4096 with
   // int32 sums (1024 tiles) 7.55 against 9.2 us.  Larger grids with N not a
@@ -561,7 +562,7 @@ bnn_status bnn_bfc_tail(int64_t M, int64_t K0, int64_t N0, int64_t N1, const uin
                   (long long)M, (long long)K0, (long long)N0, (long long)N1);
     if (!bnn::bfc_tail_supported(M, K0, N0, N1))
       return fail(BNN_ERR_UNSUPPORTED,
-                  "bfc_tail: needs M <= 512, K0 a multiple of 1024, N0 a multiple of 32 with "
+                  "bfc_tail: needs M <= 512, K0 >= 1024, N0 a multiple of 32 with "
                   "ceil(M / 32) * N0 / 32 <= 512, and N1 <= 32");
     if (!A || !w0 || !w1) return fail(BNN_ERR_NULL, "bfc_tail: A, w0 or w1 is NULL");
     if (!thr0) return fail(BNN_ERR_NULL, "bfc_tail: thr0 is NULL");

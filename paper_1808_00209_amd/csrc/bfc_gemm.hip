@@ -1,7 +1,7 @@
 // Binary FC layer / GEMM (Sec. III-B, Eq. 4) for long rows at modest row
 // counts: S[m][n] = sum_k a[m][k] b[n][k] over +-1 values, with the
-// threshold / flip epilogue of bnn_bgemm.  K is a multiple of 1024 bits and N
-// a multiple of 32.
+// threshold / flip epilogue of bnn_bgemm.  K is at least 1024 bits and N a
+// multiple of 32.
 //
 // A workgroup computes one 32 x 32 output tile (32 rows x 32 outputs) with 8
 // waves, each taking one eighth of the K bits.  A wave loads its slice of
@@ -39,7 +39,9 @@ struct GmArgs {
   const uint32_t* flip;   // [N / 32] or null
   int32_t* sums;          // [M][N] or null
   uint32_t* bits;         // [M][N / 32] or null
-  int32_t M, N, Kw;       // Kw = K / 32, a multiple of 32
+  int32_t M, N, Kw;       // Kw = ceil(K / 32), the row length in words
+  int32_t Kwp;            // Kw rounded up to the K split (8 words per wave and chunk step)
+  int32_t K;              // bits
   int32_t a_bytes, b_bytes;
 };
 
@@ -138,8 +140,12 @@ __device__ __forceinline__ void fc_tail(const GmArgs& a, const TailArgs& t, cons
 }
 
 // With TAIL (one tile per workgroup only) the tile's thresholded bits feed the
-// tail layer instead of memory (fc_tail below).
-template <int TPB, int TFB, int KS, bool TAIL = false>
+// tail layer instead of memory (fc_tail below).  With KT, K is not 32 Kwp:
+// words at or past Kw read as 0 and the bits of the last word past K are
+// cleared, in both operands.  Each such bit is +1.0 in both fp4 operands, so
+// every sum comes out P = 32 Kwp - K too high, an exact integer that the
+// epilogue takes off (thresholds included).
+template <int TPB, int TFB, int KS, bool TAIL = false, bool KT = false>
 __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a, TailArgs t) {
   static_assert(TPB * TFB * KS == kNW, "8 waves");
   static_assert(!TAIL || (TPB * TFB == 1 && KS > 1), "the tail takes one tile per workgroup");
@@ -183,7 +189,17 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a, TailArgs t) {
   asm("v_mov_b32 %0, 0x22222222" : "=v"(vfill));
 
   // This wave's K slice: words k0 .. k0 + sw - 1 of every row.
-  const int sw = a.Kw / KS;
+  const int sw = a.Kwp / KS;
+  const uint32_t lastmask = tail_mask(a.K);  // valid bits of word Kw - 1
+  // Clears the words of a loaded piece (words g .. g + 3) at or past Kw and
+  // the bits past K of word Kw - 1.
+  auto clip = [&](v4i& v, int g) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t x = static_cast<uint32_t>(v[w]);
+      v[w] = static_cast<int>(g + w < a.Kw - 1 ? x : g + w == a.Kw - 1 ? x & lastmask : 0u);
+    }
+  };
   const int k0 = ks * sw;
   v16f acc = {};
   // A chunk of ch words (a multiple of 4, at most 32) of 32 rows is 8 ch
@@ -206,6 +222,10 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a, TailArgs t) {
                                           ra, static_cast<uint32_t>(m) * a.Kw * 4 + wo, 0, 0));
       pb[i] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
                                           rb, static_cast<uint32_t>(n0 + row) * a.Kw * 4 + wo, 0, 0));
+      if (KT && k0 + kc + ch >= a.Kw) {  // (wave-uniform: chunks that reach word Kw - 1)
+        clip(pa[i], k0 + kc + col);
+        clip(pb[i], k0 + kc + col);
+      }
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -236,9 +256,10 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a, TailArgs t) {
       acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(A1, B1, acc, 4, 4, 0, 127, 0, 127);
     }
   }
+  const int32_t P = 32 * a.Kwp - a.K;  // sums come out P too high (KT)
   if (th_lane) {
-    const int32_t K = 32 * a.Kw;
-    th[tid] = 0.5f - static_cast<float>(min(max(thv, -K - 1), K + 1));
+    const int32_t K = a.K;
+    th[tid] = 0.5f - static_cast<float>(min(max(thv, -K - 1), K + 1)) - static_cast<float>(P);
   }
   if (tail_lane) {
     w1c[tid - 64] = w1v;
@@ -285,7 +306,7 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a, TailArgs t) {
     int32_t* ts = reinterpret_cast<int32_t*>(&stg[wave][0][0]);  // 32 x 33 words
 #pragma unroll
     for (int e = 0; e < 16; ++e)
-      ts[c * 33 + 8 * (e >> 2) + 4 * h + (e & 3)] = static_cast<int32_t>(acc[e]);
+      ts[c * 33 + 8 * (e >> 2) + 4 * h + (e & 3)] = static_cast<int32_t>(acc[e]) - P;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = 8 * i + (lane >> 3), col = 4 * (lane & 7);
@@ -307,24 +328,11 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a, TailArgs t) {
   }
 }
 
-template <int TPB, int TFB, int KS>
-void launch_tiles(const GmArgs& a, hipStream_t s) {
-  const unsigned blocks =
-      static_cast<unsigned>(((a.M + 32 * TPB - 1) / (32 * TPB)) * (a.N / (32 * TFB)));
-  bfc_gemm_kernel<TPB, TFB, KS><<<blocks, kNT, 0, s>>>(a, TailArgs{});
-}
-
-}  // namespace
-
-bool bfc_gemm_supported(int64_t M, int64_t N, int64_t K) {
-  return M >= 1 && N >= 32 && N % 32 == 0 && K >= 1024 && K % 1024 == 0 &&
-         M * (K / 8) < (int64_t{1} << 31) && N * (K / 8) < (int64_t{1} << 31) &&
-         ((M + 31) / 32) * (N / 32) < (int64_t{1} << 31);
-}
-
-hipError_t launch_bfc_gemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
-                           const uint32_t* B, const int32_t* thr, const uint32_t* flip,
-                           int32_t* sums, uint32_t* bits, hipStream_t s) {
+// Kernel arguments for M x K rows against N x K weight rows, the row length
+// padded to a multiple of `split` words (4 words per wave of the K split).
+GmArgs gm_args(int64_t M, int64_t N, int64_t K, const uint32_t* A, const uint32_t* B,
+               const int32_t* thr, const uint32_t* flip, int32_t* sums, uint32_t* bits,
+               int split) {
   GmArgs a;
   a.A = A;
   a.B = B;
@@ -334,17 +342,44 @@ hipError_t launch_bfc_gemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
   a.bits = bits;
   a.M = static_cast<int32_t>(M);
   a.N = static_cast<int32_t>(N);
-  a.Kw = static_cast<int32_t>(K / 32);
-  a.a_bytes = static_cast<int32_t>(M * (K / 8));
-  a.b_bytes = static_cast<int32_t>(N * (K / 8));
+  a.Kw = static_cast<int32_t>((K + 31) / 32);
+  a.Kwp = (a.Kw + split - 1) / split * split;
+  a.K = static_cast<int32_t>(K);
+  a.a_bytes = static_cast<int32_t>(M * a.Kw * 4);
+  a.b_bytes = static_cast<int32_t>(N * a.Kw * 4);
+  return a;
+}
+
+template <int TPB, int TFB, int KS>
+void launch_tiles(const GmArgs& a, hipStream_t s) {
+  const unsigned blocks =
+      static_cast<unsigned>(((a.M + 32 * TPB - 1) / (32 * TPB)) * (a.N / (32 * TFB)));
+  if (a.K == 32 * a.Kwp)
+    bfc_gemm_kernel<TPB, TFB, KS><<<blocks, kNT, 0, s>>>(a, TailArgs{});
+  else
+    bfc_gemm_kernel<TPB, TFB, KS, false, true><<<blocks, kNT, 0, s>>>(a, TailArgs{});
+}
+
+}  // namespace
+
+bool bfc_gemm_supported(int64_t M, int64_t N, int64_t K) {
+  const int64_t kw = (K + 31) / 32 + 32;  // row words with the padding
+  return M >= 1 && N >= 32 && N % 32 == 0 && K >= 1024 && K < (int64_t{1} << 28) &&
+         M * kw * 4 < (int64_t{1} << 31) && N * kw * 4 < (int64_t{1} << 31) &&
+         ((M + 31) / 32) * (N / 32) < (int64_t{1} << 31);
+}
+
+hipError_t launch_bfc_gemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
+                           const uint32_t* B, const int32_t* thr, const uint32_t* flip,
+                           int32_t* sums, uint32_t* bits, hipStream_t s) {
   // One output tile per workgroup (K split 8 ways) up to 512 tiles; larger
   // grids take 2 x 2 tiles per workgroup with K split 2 ways (rows and
   // outputs in whole pairs of tiles).
   const int64_t tiles = ((M + 31) / 32) * (N / 32);
   if (tiles <= 512 || N % 64 != 0)
-    launch_tiles<1, 1, 8>(a, s);
+    launch_tiles<1, 1, 8>(gm_args(M, N, K, A, B, thr, flip, sums, bits, 32), s);
   else
-    launch_tiles<2, 2, 2>(a, s);
+    launch_tiles<2, 2, 2>(gm_args(M, N, K, A, B, thr, flip, sums, bits, 8), s);
   return hipGetLastError();
 }
 
@@ -357,18 +392,7 @@ hipError_t launch_bfc_tail(int64_t M, int64_t K0, int64_t N0, int64_t N1, const 
                            const uint32_t* w0, const int32_t* thr0, const uint32_t* flip0,
                            const uint32_t* w1, const int32_t* thr1, const uint32_t* flip1,
                            int32_t* sums, uint32_t* bits, void* accum, hipStream_t s) {
-  GmArgs a;
-  a.A = A;
-  a.B = w0;
-  a.thr = thr0;
-  a.flip = flip0;
-  a.sums = nullptr;
-  a.bits = nullptr;
-  a.M = static_cast<int32_t>(M);
-  a.N = static_cast<int32_t>(N0);
-  a.Kw = static_cast<int32_t>(K0 / 32);
-  a.a_bytes = static_cast<int32_t>(M * (K0 / 8));
-  a.b_bytes = static_cast<int32_t>(N0 * (K0 / 8));
+  const GmArgs a = gm_args(M, N0, K0, A, w0, thr0, flip0, nullptr, nullptr, 32);
   TailArgs t;
   t.w1 = w1;
   t.thr1 = thr1;
@@ -380,7 +404,10 @@ hipError_t launch_bfc_tail(int64_t M, int64_t K0, int64_t N0, int64_t N1, const 
                                                   kTailMaxRows * 32);
   t.N1 = static_cast<int32_t>(N1);
   const unsigned blocks = static_cast<unsigned>(((M + 31) / 32) * (N0 / 32));
-  bfc_gemm_kernel<1, 1, 8, true><<<blocks, kNT, 0, s>>>(a, t);
+  if (a.K == 32 * a.Kwp)
+    bfc_gemm_kernel<1, 1, 8, true><<<blocks, kNT, 0, s>>>(a, t);
+  else
+    bfc_gemm_kernel<1, 1, 8, true, true><<<blocks, kNT, 0, s>>>(a, t);
   return hipGetLastError();
 }
 

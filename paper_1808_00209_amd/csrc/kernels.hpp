@@ -140,7 +140,7 @@ hipError_t launch_bconv_img8(const ConvGeom& g, const uint32_t* in, const uint32
                              const int32_t* thr, const uint32_t* flip, uint32_t* bits,
                              hipStream_t s);
 
-// Binary FC layer / GEMM with K a multiple of 1024 bits and N a multiple of
+// Binary FC layer / GEMM with K >= 1024 bits and N a multiple of
 // 32 (bfc_gemm.hip): a workgroup per 32 x 32 output tile, K split over its 8
 // waves, both operands staged per wave through LDS with whole-line loads.
 // sums [M][N] and/or bits [M][N / 32]; thr non-null when bits is.
@@ -151,7 +151,7 @@ hipError_t launch_bfc_gemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
 
 // Two consecutive binary FC layers, the second with N1 <= 32 outputs, in one
 // launch of the FC kernel (bfc_gemm.hip): a workgroup per 32 x 32 tile of the
-// first layer (K0 a multiple of 1024, N0 of 32, at most 512 tiles, at most
+// first layer (K0 >= 1024, N0 a multiple of 32, at most 512 tiles, at most
 // kTailMaxRows rows), each adding the second layer's partial sums over its
 // 32 inputs to accumulators in `accum` (kTailAccumBytes, zero on entry and
 // left zero) with atomic adds; the add that completes an output writes it:

@@ -271,9 +271,9 @@ def test_bfc_tail_errors():
 
     for bad in (dict(M=0), dict(K0=0), dict(N0=0), dict(N1=0), dict(N1=-3)):
         assert call(**bad) == 2, bad
-    # K0 not a multiple of 1024, N0 not of 32, more than 512 rows or 512
+    # K0 below 1024, N0 not a multiple of 32, more than 512 rows or 512
     # tiles (64 rows x 9216 outputs: 2 x 288), N1 > 32
-    for uns in (dict(K0=1000), dict(K0=1536), dict(N0=1000), dict(M=513), dict(N0=9216),
+    for uns in (dict(K0=1000), dict(K0=1023), dict(N0=1000), dict(M=513), dict(N0=9216),
                 dict(M=40, N0=9216), dict(N1=33)):
         assert call(**uns) == 4, uns
     assert call(a=None) == 1

@@ -97,7 +97,7 @@ def test_fc_pair_no_flips_extreme_and_tied_thresholds():
 
 
 # FC tails inside bnn_forward: two FC layers whose second has at most 32
-# outputs, the first with K a multiple of 1024 and N of 32, run as one launch
+# outputs, the first with K >= 1024 and N a multiple of 32, run as one launch
 # of the FC kernel (a workgroup per 32 x 32 tile of the first layer, the last
 # workgroup of each 32-row block adding the second layer's partial sums).
 # The stacks sit behind a real-valued first layer on a 1 x 1 image (3x3,

@@ -293,13 +293,18 @@ GEMM_CASES = [(1, 1, 1), (1, 10, 1024), (2, 33, 31), (5, 100, 33), (16, 1024, 81
               # FC kernel with a workgroup per tile (ragged row tiles, K slices
               # of one chunk, of several chunks and of a short last chunk)
               (3, 32, 1024), (33, 64, 2048), (97, 96, 8192), (40, 32, 18432), (512, 1024, 1024),
-              # more than 512 tiles and N a multiple of 64: waves of 2 x 2
-              # tiles, K split over 4 waves (a ragged second row tile, one
-              # with no row in range, K slices of 8, 24 and 32 words and of
-              # a 32-word and an 8-word chunk); N not a multiple of 64 there
-              # stays with the conv kernel
+              # more than 512 tiles and N a multiple of 64: workgroups of 2 x 2
+              # tiles, two waves per tile with half of K each (a ragged second
+              # row tile, one with no row in range, K slices of 16, 48, 64 and
+              # 80 words); N not a multiple of 64 there stays with the conv
+              # kernel
               (100, 6144, 1024), (33, 16384, 1024), (130, 4096, 3072), (256, 4096, 4096),
-              (40, 16384, 5120), (600, 1056, 1024)]
+              (40, 16384, 5120), (600, 1056, 1024),
+              # K >= 1024 not a multiple of the K split: rows padded with
+              # cleared words and the last word's bits past K cleared (one
+              # valid bit, 4, 12, 31), in both forms
+              (5, 64, 1025), (70, 96, 4100), (100, 2048, 1100), (64, 4096, 2047),
+              (300, 4096, 4100), (600, 1088, 1056)]
 
 
 @pytest.mark.parametrize("case", GEMM_CASES, ids=[str(c) for c in GEMM_CASES])
