@@ -252,7 +252,7 @@ def layer_shapes(layers, H, W, C, batch=None):
               and layers[li + 1]["kind"] in ("bfc", "bfc_logits")
               and not fc_chained(layers, li, batch)
               and (tail_fusable(L, layers[li + 1], batch)
-                   or (batch > 2 and L["K"] in (512, 1024) and L["N"] in (256, 512, 1024)
+                   or (batch > 1 and L["K"] in (512, 1024) and L["N"] in (256, 512, 1024)
                        and layers[li + 1]["N"] <= 32))):
             # bnn_forward's two FC layers in one kernel: the FC tail kernel
             # (bnn_bfc_tail) where it fits, else bnn_bfc_pair

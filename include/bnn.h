@@ -108,7 +108,7 @@ typedef struct bnn_options {
                            /* groups when that cuts the bytes the L2s move   */
                            /* (2)                                            */
   int32_t gemv_max_rows;   /* FC layers of at most this many rows use the    */
-                           /* vector-ALU GEMV; 0..16, default 2              */
+                           /* vector-ALU GEMV; 0..16, default 1              */
   int32_t lds_weights;     /* matrix-core conv weights staged through LDS:   */
                            /* -1 where the heuristic picks it (default), 0   */
                            /* never, 1 wherever no K split is used (with     */

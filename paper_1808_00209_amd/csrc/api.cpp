@@ -26,7 +26,7 @@ bnn_options default_options() {
   o.fc_chain = 1;
   o.conv1x1 = 1;
   o.xcd_order = 1;
-  o.gemv_max_rows = 2;
+  o.gemv_max_rows = 1;
   o.lds_weights = -1;
   o.late_thresholds = -1;
   o.fuse_pair = 1;
@@ -167,10 +167,11 @@ bnn_status gemm_launch(int64_t M, int64_t N, int64_t K, const uint32_t* A,
                        const uint32_t* B, const int32_t* thr,
                        const uint32_t* flip, int32_t* sums, uint32_t* bits,
                        hipStream_t s) {
-  // At most 2 rows go to the vector-ALU GEMV, whose time grows with every
-  // row; from 3 rows on the matrix-core conv kernel (a 1 x M image with 1x1
-  // filters) is as fast or faster, and 3x faster at 16 rows (measured on the
-  // FC shapes of the networks here).  Option gemv_max_rows (0..16) moves it.
+  // One row goes to the vector-ALU GEMV, whose time grows with every row;
+  // from 2 rows on the matrix-core kernels are as fast or faster (the CIFAR
+  // forward at 2 rows 30.7-31.0 against 29.7-29.9 us with its 8192 -> 1024
+  // layer in the FC kernel; at one row the GEMV is 0.5-0.8 us faster), and
+  // 3x faster at 16 rows.  Option gemv_max_rows (0..16) moves the limit.
   if (M <= g_opt.gemv_max_rows)
     return hip_status(bnn::launch_bgemv_valu(M, N, K, A, B, thr, flip, sums, bits, s),
                       "bgemm (gemv) launch");

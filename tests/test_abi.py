@@ -415,7 +415,7 @@ def test_options_defaults_set_get_and_range_checks():
     d = bnn.bnn_default_options()
     assert (d.algo, d.fuse_input, d.fuse_first, d.fc_chain, d.conv1x1, d.xcd_order,
             d.gemv_max_rows, d.lds_weights, d.late_thresholds,
-            d.fuse_pair) == (0, 1, 1, 1, 1, 1, 2, -1, -1, 1)
+            d.fuse_pair) == (0, 1, 1, 1, 1, 1, 1, -1, -1, 1)
     try:
         bnn.bnn_set_options(algo=bnn.ALGO_VALU, gemv_max_rows=16, lds_weights=1)
         got = bnn.bnn_get_options()

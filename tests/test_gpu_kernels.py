@@ -327,7 +327,7 @@ GEMV_CASES = [(1, 1, 1), (2, 33, 31), (3, 100, 33), (5, 1024, 8192), (8, 64, 410
 @pytest.mark.parametrize("case", GEMV_CASES, ids=[str(c) for c in GEMV_CASES])
 def test_bgemv_all_row_counts_bit_exact(case):
     """The vector-ALU GEMV kernel at every row count it supports (1..16);
-    bnn_bgemm sends it only M <= 2 by default, option gemv_max_rows = 16 forces it."""
+    bnn_bgemm sends it only M = 1 by default, option gemv_max_rows = 16 forces it."""
     bnn.bnn_set_options(gemv_max_rows=16)
     M, N, K = case
     rng = np.random.default_rng(M * 7907 + N * 29 + K)
