@@ -14,7 +14,8 @@
 // Grids of more than 512 tiles (N a multiple of 64) take 2 x 2 tiles per
 // workgroup instead, two waves per tile with half of K each: a workgroup
 // holds about 100 KB of LDS, so one runs per CU, and 1024 one-tile
-// workgroups took four rounds.
+// workgroups took four rounds.  Rows whose length is not whole k-steps per
+// wave are padded with cleared words (the KT form of the kernel).
 // The general matrix-core kernel loads each operand row straight from memory,
 // 32 rows per load instruction, and runs the K split inside a workgroup of
 // one output tile column: the 8192 -> 1024 layer at 64 rows ran on 32
@@ -40,7 +41,7 @@ struct GmArgs {
   int32_t* sums;          // [M][N] or null
   uint32_t* bits;         // [M][N / 32] or null
   int32_t M, N, Kw;       // Kw = ceil(K / 32), the row length in words
-  int32_t Kwp;            // Kw rounded up to the K split (8 words per wave and chunk step)
+  int32_t Kwp;            // Kw rounded up to 4 KS words (whole k-steps per wave)
   int32_t K;              // bits
   int32_t a_bytes, b_bytes;
 };
@@ -78,9 +79,6 @@ __device__ __forceinline__ uint32_t sign_word(const v16f& acc, int h) {
   return wd;
 }
 
-// TPB x TFB output tiles of 32 x 32 per workgroup (rows x outputs) and KS
-// waves per tile, each taking 1 / KS of K (TPB TFB KS = 8 waves): wave w
-// computes tile (w % TPB, (w / TPB) % TFB) over slice w / (TPB TFB) of K.
 // The tail of an FC pair, run by every thread of the workgroup that holds
 // the first layer's 32 x 32 sums of rows m0 .. m0 + 31 and outputs
 // 32 ft .. 32 ft + 31 in `tile` (MFMA layout).  Wave 0 thresholds them into
@@ -139,8 +137,11 @@ __device__ __forceinline__ void fc_tail(const GmArgs& a, const TailArgs& t, cons
   }
 }
 
+// TPB x TFB output tiles of 32 x 32 per workgroup (rows x outputs) and KS
+// waves per tile, each taking 1 / KS of K (TPB TFB KS = 8 waves): wave w
+// computes tile (w % TPB, (w / TPB) % TFB) over slice w / (TPB TFB) of K.
 // With TAIL (one tile per workgroup only) the tile's thresholded bits feed the
-// tail layer instead of memory (fc_tail below).  With KT, K is not 32 Kwp:
+// tail layer instead of memory (fc_tail above).  With KT, K is not 32 Kwp:
 // words at or past Kw read as 0 and the bits of the last word past K are
 // cleared, in both operands.  Each such bit is +1.0 in both fp4 operands, so
 // every sum comes out P = 32 Kwp - K too high, an exact integer that the
