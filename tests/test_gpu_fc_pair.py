@@ -108,6 +108,7 @@ TAILS = {
     "bits_tail": (2048, [512, 32, 10]),  # the pair's second layer writes bits
     "one_output": (1024, [64, 1]),
     "three_slices": (3072, [96, 17]),
+    "padded_k": (1100, [256, 12]),      # K not a multiple of 32: padded rows
 }
 
 
@@ -187,7 +188,9 @@ TAIL_CASES = [(64, 1024, 1024, 10, True),   # the CIFAR-shaped net's tail at bat
               (33, 1024, 64, 1, True),       # a ragged second row block
               (100, 3072, 96, 17, False),    # three first-layer slices
               (512, 1024, 1024, 10, True),   # 512 rows and 512 tiles, the limits
-              (200, 1024, 2048, 5, False)]
+              (200, 1024, 2048, 5, False),
+              (50, 1500, 64, 7, True),       # K0 not a multiple of 32: padded rows
+              (20, 2047, 128, 32, False)]
 
 
 @pytest.mark.parametrize("case", TAIL_CASES, ids=[str(c) for c in TAIL_CASES])
