@@ -304,7 +304,9 @@ GEMM_CASES = [(1, 1, 1), (1, 10, 1024), (2, 33, 31), (5, 100, 33), (16, 1024, 81
               # cleared words and the last word's bits past K cleared (one
               # valid bit, 4, 12, 31), in both forms
               (5, 64, 1025), (70, 96, 4100), (100, 2048, 1100), (64, 4096, 2047),
-              (300, 4096, 4100), (600, 1088, 1056)]
+              (300, 4096, 4100), (600, 1088, 1056),
+              # two rows: the FC kernel by default (one row: the GEMV)
+              (2, 1024, 8192), (2, 64, 1025), (1, 1024, 8192)]
 
 
 @pytest.mark.parametrize("case", GEMM_CASES, ids=[str(c) for c in GEMM_CASES])
