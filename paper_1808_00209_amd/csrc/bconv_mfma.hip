@@ -21,8 +21,8 @@
 // wave computes 64 (or 32) filters x 64 pixels; with pooling, the 32 pixels
 // of a tile are eight 2x2 windows so that a window sits in 4 adjacent lanes.
 //
-// Requirements (bconv_mfma_supported): stride 1, C a multiple of 64, at most
-// 32 taps.
+// Requirements (bconv_mfma_supported): stride 1, C >= 32 (a C that is not a
+// multiple of 64 is padded to whole 64-bit chunks), at most 32 taps.
 #include <type_traits>
 
 #include "fp4_expand.hpp"
@@ -1115,13 +1115,13 @@ __global__ __launch_bounds__(256) void prepare_weights_kernel(const uint32_t* w,
 }  // namespace
 
 bool bconv_mfma_supported(const ConvGeom& g) {
-  // At least 64 channels (a C that is not a multiple of 64 is padded to
+  // At least 32 channels (a C that is not a multiple of 64 is padded to
   // whole chunks, at most half of them padding), at most 32 taps (per-lane
   // tap masks), fewer than 2^22 bit positions per window, padding included
   // (the fp32 accumulators, which may start at 0.5 - thr, stay exact), and
   // inputs and weights under 2 GiB (32-bit byte offsets of the raw buffer
   // loads).
-  return g.C >= 64 && g.KH * g.KW <= 32 &&
+  return g.C >= 32 && g.KH * g.KW <= 32 &&
          static_cast<int64_t>(g.KH) * g.KW * 32 * (g.Cw + 7) < (int64_t{1} << 22) &&
          static_cast<int64_t>(g.N) * g.H * g.W * g.Cw < (int64_t{1} << 29) &&
          static_cast<int64_t>(g.F) * g.KH * g.KW * g.Cw < (int64_t{1} << 29);

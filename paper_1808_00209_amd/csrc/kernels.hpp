@@ -47,7 +47,7 @@ hipError_t launch_bconv1x1(const ConvGeom& g, const uint32_t* in, const uint32_t
                            hipStream_t s);
 
 // Binary conv on the matrix cores (fp4 MFMA).  Supported when
-// bconv_mfma_supported(g): C >= 64 (padded to whole 64-bit chunks), at most
+// bconv_mfma_supported(g): C >= 32 (padded to whole 64-bit chunks), at most
 // 32 taps.
 // wprep: the weights prepared by launch_prepare_weights (used instead of w),
 // or null.

@@ -171,6 +171,15 @@ CONV_CASES = [
     (1, 7, 5, 65, 96, 3, 1, 0),
     (1, 6, 6, 130, 32, 3, 0, 0),
     (3, 5, 5, 200, 128, 1, 0, 2),
+    # 32 <= C < 64 on the matrix-core path: one word per tap padded to a
+    # 2-word chunk (C = 32), or a masked second word (C = 48, 63); 5x5
+    # windows as in Table II's second conv, a 1x1 and a single pixel
+    (1, 48, 48, 32, 32, 5, 2, 2),
+    (2, 13, 11, 32, 40, 5, 2, 0),
+    (3, 9, 9, 48, 64, 3, 1, 2),
+    (1, 7, 6, 63, 96, 5, 2, 0),
+    (2, 10, 10, 32, 128, 1, 0, 2),
+    (1, 1, 1, 32, 32, 5, 2, 0),
     # grids in the XCD order whose pixel blocks are not a multiple of 8, so
     # padding workgroups run with no valid pixel: a K split over 36 blocks,
     # 36 blocks of 4 waves, and 23 pooled blocks with a ragged last one
