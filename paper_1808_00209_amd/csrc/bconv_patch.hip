@@ -276,6 +276,231 @@ __global__ __launch_bounds__(256) void bconv_patch_kernel(PatchArgs a) {
   }
 }
 
+// Row-stream variant for bits-only output and a compile-time window whose
+// rows fit a word (KW * C <= 32 bits) and whose rows pack into at most 3
+// patch words.  The input tile is turned into one bit stream per tile row
+// (the codes of its TC pixels, MSB first), each 64-element stretch by one
+// wave ballot: with RGB thresholding straight from the image, whose tile row
+// is TC * C consecutive floats, otherwise from the pixel codes staged in LDS.
+// A window row of KW taps is then KW * C consecutive stream bits, which one
+// funnel shift extracts, and the KH rows go to fixed slots of the patch words
+// (RPW rows per word, the unused bits 0 in patches and filters alike, so the
+// popcounts do not change).  This replaces the per-tap assembly of the
+// general kernel, whose shifts and loop control cost as much as the
+// XOR-popcounts themselves.
+template <int KH, int KW, int C, bool POOL>
+__global__ __launch_bounds__(256) void bconv_patch_rows_kernel(PatchArgs a) {
+  constexpr int SW = KW * C;                   // bits per window row
+  constexpr int RPW = 32 / SW;                 // window rows per patch word
+  constexpr int PW = (KH + RPW - 1) / RPW;     // patch words
+  constexpr int TR = kTH + KH - 1, TC = kTW + KW - 1;
+  constexpr int E = TC * C;                    // stream bits per tile row
+  constexpr int NW = (E + 31) / 32;            // stream words per tile row
+  constexpr int RL = NW + 2;                   // stored: pad word, NW words, pad word
+  constexpr int CH = (E + 63) / 64;            // ballots per tile row
+  constexpr int JOBS = TR * CH;
+  constexpr int JPW = (JOBS + 2) / 3;          // ballots per wave (3 or 4 waves)
+  static_assert(SW <= 32 && PW <= 3, "window rows must fit the patch layout");
+  __shared__ uint32_t stream[TR * RL];
+  __shared__ uint32_t codes[C == 0 ? 1 : TR * TC];
+  __shared__ uint4 wsh[kFB];                   // patch words and bias per filter
+  __shared__ uint32_t wflip[kFB / 32];
+
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  int b = blockIdx.x;
+  const int bx = b % a.tiles_x;
+  b /= a.tiles_x;
+  const int by = b % a.tiles_y;
+  const int n = b / a.tiles_y;
+  const int i0 = by * kTH, j0 = bx * kTW;
+
+  auto stage_filters = [&](int f0, int nf) {
+    uint32_t pw[3] = {0u, 0u, 0u};
+    int32_t bias = 0;
+    if (t < nf) {
+      const int f = f0 + t;
+      const uint32_t* wf = a.w + static_cast<size_t>(f) * (KH * KW);  // one word per tap
+#pragma unroll
+      for (int kh = 0; kh < KH; ++kh) {
+        uint32_t seg = 0;
+#pragma unroll
+        for (int kw = 0; kw < KW; ++kw) seg = (seg << C) | (wf[kh * KW + kw] >> (32 - C));
+        pw[kh / RPW] |= seg << (32 - (kh % RPW + 1) * SW);
+      }
+      const int64_t d = static_cast<int64_t>(a.P) - a.thr[f];
+      int64_t q = d >= 0 ? d / 2 : -((1 - d) / 2);
+      q = q < -1 ? -1 : (q > a.P ? a.P : q);
+      bias = static_cast<int32_t>(-q - 1);
+    }
+    wsh[t] = make_uint4(pw[0], pw[1], pw[2], static_cast<uint32_t>(bias));
+    if (t < kFB / 32) wflip[t] = a.flip && 32 * t < nf ? a.flip[(f0 >> 5) + t] : 0u;
+  };
+
+  // Stream words of tile row r, 64 elements from element 64 q on: stored
+  // at 1 + 2q and 2 + 2q (bit i of the ballot is element 64 q + i, which
+  // goes to bit 31 - i % 32); the pad words around a row stay 0.
+  auto put_ballot = [&](int r, int q, uint64_t bal) {
+    const uint32_t lo = __builtin_bitreverse32(static_cast<uint32_t>(bal));
+    const uint32_t hi = __builtin_bitreverse32(static_cast<uint32_t>(bal >> 32));
+    uint32_t* row = stream + r * RL;
+    if (lane < 2) row[1 + 2 * q + lane] = lane ? hi : lo;
+    if (q == 0 && lane == 2) row[0] = 0u;
+    if constexpr (NW % 2 == 0)
+      if (q == CH - 1 && lane == 3) row[RL - 1] = 0u;
+  };
+
+  const int nf0 = min(kFB, a.F);
+  const bool split = nf0 <= 64;  // wave 0 stages the filters meanwhile
+  const int gi0 = i0 - a.pad, gj0 = j0 - a.pad;
+  if (a.in.mode == BNN_INPUT_THRESHOLD) {
+    if (split && wave == 0) {
+      stage_filters(0, nf0);
+    } else {
+      const int wv = split ? wave - 1 : wave, nw = split ? 3 : 4;
+      float off[C];
+#pragma unroll
+      for (int c = 0; c < C; ++c) off[c] = a.in.offset ? a.in.offset[c] : 0.0f;
+      // All of this wave's loads first, then the ballots.
+      float v[JPW];
+      bool in[JPW];
+#pragma unroll
+      for (int k = 0; k < JPW; ++k) {
+        const int jb = wv + k * nw;
+        const int r = jb / CH, e = (jb - r * CH) * 64 + lane;
+        const int px = e / C, gi = gi0 + r, gj = gj0 + px;
+        in[k] = jb < JOBS && e < E && gi >= 0 && gi < a.in.H && gj >= 0 && gj < a.in.W;
+        v[k] = in[k] ? a.in.x[((static_cast<size_t>(n) * a.in.H + gi) * a.in.W + gj) * C +
+                              (e - px * C)]
+                     : 0.0f;
+      }
+#pragma unroll
+      for (int k = 0; k < JPW; ++k) {
+        const int jb = wv + k * nw;
+        if (jb < JOBS) {
+          const int r = jb / CH, q = jb - r * CH;
+          const int ch = (q * 64 + lane) % C;
+          float o = off[0];
+#pragma unroll
+          for (int c = 1; c < C; ++c) o = ch == c ? off[c] : o;
+          put_ballot(r, q, __builtin_amdgcn_ballot_w64(in[k] && v[k] + o > 0.0f));
+        }
+      }
+      if (!split) stage_filters(0, nf0);
+    }
+    __syncthreads();
+  } else {
+    if (split && wave == 0) {
+      stage_filters(0, nf0);
+    } else {
+      const int e0 = split ? t - 64 : t, step = split ? 192 : 256;
+      for (int e = e0; e < TR * TC; e += step) {
+        const int r = e / TC, cc = e - r * TC;
+        const int gi = gi0 + r, gj = gj0 + cc;
+        codes[e] = (gi >= 0 && gi < a.in.H && gj >= 0 && gj < a.in.W)
+                       ? pixel_code(a.in, n, gi, gj)
+                       : 0u;
+      }
+      if (!split) stage_filters(0, nf0);
+    }
+    __syncthreads();
+    for (int jb = wave; jb < JOBS; jb += 4) {
+      const int r = jb / CH, q = jb - r * CH;
+      const int e = q * 64 + lane;
+      const int px = e / C, ch = e - px * C;
+      const bool bit = e < E && ((codes[r * TC + min(px, TC - 1)] >> (C - 1 - ch)) & 1u);
+      put_ballot(r, q, __builtin_amdgcn_ballot_w64(bit));
+    }
+    __syncthreads();
+  }
+
+  // This thread's output pixel; with pooling, lanes 4q..4q+3 are one window.
+  int oy, ox;
+  if constexpr (POOL) {
+    const int win = t >> 2, q = t & 3;
+    oy = 2 * (win / (kTW / 2)) + (q >> 1);
+    ox = 2 * (win % (kTW / 2)) + (q & 1);
+  } else {
+    oy = t / kTW;
+    ox = t % kTW;
+  }
+  const int i = i0 + oy, j = j0 + ox;
+
+  // Window row kh is stream bits ox*C .. ox*C + SW - 1 of tile row oy + kh:
+  // the top SW bits of alignbit(word, next word, 32 - bit offset), or of the
+  // word itself (alignbit by 0 of the pad or previous word and it) when the
+  // offset is 0.
+  const int p = ox * C, bo = p & 31;
+  const int base = (p >> 5) + (bo ? 1 : 0);
+  const uint32_t sh = static_cast<uint32_t>(32 - bo) & 31u;
+  uint32_t patch[PW];
+#pragma unroll
+  for (int q = 0; q < PW; ++q) patch[q] = 0u;
+#pragma unroll
+  for (int kh = 0; kh < KH; ++kh) {
+    const uint32_t* row = stream + (oy + kh) * RL + base;
+    const uint32_t seg = __builtin_amdgcn_alignbit(row[0], row[1], sh);
+    constexpr uint32_t top = SW == 32 ? ~0u : ~(~0u >> SW);
+    const int k = kh % RPW;
+    patch[kh / RPW] |= (seg >> (k * SW)) & (top >> (k * SW));
+  }
+
+  const int Wp = POOL ? a.Wo / 2 : a.Wo;
+  const int Hp = POOL ? a.Ho / 2 : a.Ho;
+  for (int f0 = 0; f0 < a.F; f0 += kFB) {
+    const int nf = min(kFB, a.F - f0);
+    if (f0 > 0) {
+      __syncthreads();  // the previous round's filters are no longer read
+      stage_filters(f0, nf);
+      __syncthreads();
+    }
+    for (int g = 0; g < nf; g += 32) {
+      const int fw = (f0 + g) >> 5;
+      uint32_t word = 0;
+#pragma unroll
+      for (int k = 0; k < 32; ++k) {
+        const uint4 wk = wsh[g + k];
+        uint32_t d = wk.w;
+        d += static_cast<uint32_t>(__builtin_popcount(patch[0] ^ wk.x));
+        if constexpr (PW > 1) d += static_cast<uint32_t>(__builtin_popcount(patch[1] ^ wk.y));
+        if constexpr (PW > 2) d += static_cast<uint32_t>(__builtin_popcount(patch[2] ^ wk.z));
+        word = __builtin_amdgcn_alignbit(word, d, 31);
+      }
+      word ^= wflip[g >> 5];
+      if (fw == a.Fw - 1) word &= tail_mask(a.F);
+      if constexpr (POOL) {
+        word = or_quad(word);
+        if ((t & 3) == 0 && (i >> 1) < Hp && (j >> 1) < Wp)
+          a.bits[((static_cast<size_t>(n) * Hp + (i >> 1)) * Wp + (j >> 1)) * a.Fw + fw] = word;
+      } else {
+        if (i < a.Ho && j < a.Wo)
+          a.bits[((static_cast<size_t>(n) * a.Ho + i) * a.Wo + j) * a.Fw + fw] = word;
+      }
+    }
+  }
+}
+
+template <int KH, int KW, int C>
+void launch_rows(const PatchArgs& a, bool pool, dim3 grid, hipStream_t s) {
+  if (pool)
+    bconv_patch_rows_kernel<KH, KW, C, true><<<grid, 256, 0, s>>>(a);
+  else
+    bconv_patch_rows_kernel<KH, KW, C, false><<<grid, 256, 0, s>>>(a);
+}
+
+// The row-stream kernel's instantiated windows (bits only).
+bool try_launch_rows(const PatchArgs& a, bool pool, dim3 grid, hipStream_t s) {
+  if (a.sums || !a.bits) return false;
+  const int C = a.in.C;
+  if (a.KH == 5 && a.KW == 5 && C == 3) launch_rows<5, 5, 3>(a, pool, grid, s);
+  else if (a.KH == 5 && a.KW == 5 && C == 1) launch_rows<5, 5, 1>(a, pool, grid, s);
+  else if (a.KH == 3 && a.KW == 3 && C == 3) launch_rows<3, 3, 3>(a, pool, grid, s);
+  else if (a.KH == 3 && a.KW == 3 && C == 1) launch_rows<3, 3, 1>(a, pool, grid, s);
+  else return false;
+  return true;
+}
+
 template <int PW, bool POOL>
 void launch_out(const PatchArgs& a, dim3 grid, hipStream_t s) {
   if (a.sums && a.bits)
@@ -334,6 +559,7 @@ hipError_t launch_bconv_patch(const ConvGeom& g, int mode, const float* x, const
   a.tiles_y = (g.Ho + kTH - 1) / kTH;
   const dim3 grid(static_cast<unsigned>(int64_t{g.N} * a.tiles_x * a.tiles_y));
   const bool pool = g.pool == 2;
+  if (try_launch_rows(a, pool, grid, s)) return hipGetLastError();
   switch ((a.P + 31) / 32) {
     case 1: launch_pw<1>(a, pool, grid, s); break;
     case 2: launch_pw<2>(a, pool, grid, s); break;

@@ -452,6 +452,39 @@ def test_bconv_input_patch_bit_exact(case):
     assert np.array_equal(words_u32(bits), oracle.pack_eq2(b))
 
 
+# Bits-only calls of 3x3 and 5x5 windows over 1 or 3 channels take the
+# row-stream kernel (each tile row's codes as one bit stream, window rows cut
+# out by funnel shifts); the extra cases add more than 64 filters (all four
+# waves binarize), more than 256 (a second round of staged filters), pad 0,
+# and the paper's first layer on whole 96 x 96 images.
+ROWS_CASES = PATCH_CASES + [
+    (1, 19, 45, 3, 100, 5, 5, 2, 2, T),
+    (1, 9, 40, 3, 300, 5, 5, 2, 0, T),
+    (1, 14, 40, 3, 33, 5, 5, 0, 2, T),
+    (1, 30, 33, 1, 70, 5, 5, 2, 0, G),
+    (1, 17, 29, 3, 96, 5, 5, 2, 2, L),
+    (1, 11, 70, 3, 290, 3, 3, 1, 2, T),
+    (2, 96, 96, 3, 32, 5, 5, 2, 2, T),
+    (1, 96, 96, 1, 32, 5, 5, 2, 2, G),
+]
+
+
+@pytest.mark.parametrize("case", ROWS_CASES)
+def test_bconv_input_bits_only_bit_exact(case):
+    N, H, W, C, F, KH, KW, pad, pool, mode = case
+    x, off, w, thr, flip = _patch_case(7 + sum(case), N, H, W, C, F, KH, KW, mode)
+    desc = bnn.conv_desc(N, H, W, C, F, KH, KW, 1, pad, pool)
+    offd = to_device(off) if mode != L else None
+    _, bits = bnn.bnn_bconv2d_input(desc, mode, to_device(x), offd, pack_pm1(w),
+                                    to_device(thr, torch.int32), pack_flips(flip),
+                                    want_sums=False)
+    torch.cuda.synchronize()
+    b = oracle.threshold(oracle.conv2d(_binarized(x, off, mode), w, 1, pad), thr, flip)
+    if pool:
+        b = oracle.maxpool2(b)
+    assert np.array_equal(words_u32(bits), oracle.pack_eq2(b))
+
+
 @pytest.mark.parametrize("mode,cin", [(T, 3), (T, 1), (T, 32), (T, 17), (G, 3), (L, 3)])
 def test_binarize_input_bit_exact(mode, cin):
     rng = np.random.default_rng(40 + 3 * mode + cin)
