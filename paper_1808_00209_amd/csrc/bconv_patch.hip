@@ -288,6 +288,14 @@ __global__ __launch_bounds__(256) void bconv_patch_kernel(PatchArgs a) {
 // popcounts do not change).  This replaces the per-tap assembly of the
 // general kernel, whose shifts and loop control cost as much as the
 // XOR-popcounts themselves.
+// popcount(x) + acc as one v_bcnt_u32_b32 (the compiler otherwise sums two or
+// three popcounts with a separate v_add3, one more instruction per filter).
+__device__ __forceinline__ uint32_t bcnt_acc(uint32_t x, uint32_t acc) {
+  uint32_t d;
+  asm("v_bcnt_u32_b32 %0, %1, %2" : "=v"(d) : "v"(x), "v"(acc));
+  return d;
+}
+
 template <int KH, int KW, int C, bool POOL>
 __global__ __launch_bounds__(256) void bconv_patch_rows_kernel(PatchArgs a) {
   constexpr int SW = KW * C;                   // bits per window row
@@ -359,31 +367,52 @@ __global__ __launch_bounds__(256) void bconv_patch_rows_kernel(PatchArgs a) {
       stage_filters(0, nf0);
     } else {
       const int wv = split ? wave - 1 : wave, nw = split ? 3 : 4;
-      float off[C];
+      // Per 64-element stretch q of a tile row, fixed for the lane: its
+      // element's offset in an image row, whether that column lies inside
+      // the image, and its channel's threshold offset.  A job then only
+      // picks its row (uniform) and stretch.
+      int eo[CH];
+      bool cok[CH];
+      float oq[CH];
 #pragma unroll
-      for (int c = 0; c < C; ++c) off[c] = a.in.offset ? a.in.offset[c] : 0.0f;
+      for (int q = 0; q < CH; ++q) {
+        const int e = q * 64 + lane, px = e / C, ch = e - px * C, gj = gj0 + px;
+        cok[q] = e < E && gj >= 0 && gj < a.in.W;
+        eo[q] = gj * C + ch;
+        float o = 0.0f;
+        if (a.in.offset) {
+#pragma unroll
+          for (int c = 0; c < C; ++c) o = ch == c ? a.in.offset[c] : o;
+        }
+        oq[q] = o;
+      }
       // All of this wave's loads first, then the ballots.
       float v[JPW];
       bool in[JPW];
 #pragma unroll
       for (int k = 0; k < JPW; ++k) {
         const int jb = wv + k * nw;
-        const int r = jb / CH, e = (jb - r * CH) * 64 + lane;
-        const int px = e / C, gi = gi0 + r, gj = gj0 + px;
-        in[k] = jb < JOBS && e < E && gi >= 0 && gi < a.in.H && gj >= 0 && gj < a.in.W;
-        v[k] = in[k] ? a.in.x[((static_cast<size_t>(n) * a.in.H + gi) * a.in.W + gj) * C +
-                              (e - px * C)]
-                     : 0.0f;
+        const int r = jb / CH, q = jb - r * CH, gi = gi0 + r;
+        const bool rok = jb < JOBS && gi >= 0 && gi < a.in.H;
+        int o = eo[0];
+        bool ok = cok[0];
+#pragma unroll
+        for (int qq = 1; qq < CH; ++qq)
+          if (q == qq) o = eo[qq], ok = cok[qq];
+        const float* rowp = a.in.x + (static_cast<size_t>(n) * a.in.H + (rok ? gi : 0)) *
+                                         static_cast<size_t>(a.in.W) * C;
+        in[k] = rok && ok;
+        v[k] = in[k] ? rowp[o] : 0.0f;
       }
 #pragma unroll
       for (int k = 0; k < JPW; ++k) {
         const int jb = wv + k * nw;
         if (jb < JOBS) {
           const int r = jb / CH, q = jb - r * CH;
-          const int ch = (q * 64 + lane) % C;
-          float o = off[0];
+          float o = oq[0];
 #pragma unroll
-          for (int c = 1; c < C; ++c) o = ch == c ? off[c] : o;
+          for (int qq = 1; qq < CH; ++qq)
+            if (q == qq) o = oq[qq];
           put_ballot(r, q, __builtin_amdgcn_ballot_w64(in[k] && v[k] + o > 0.0f));
         }
       }
@@ -461,10 +490,10 @@ __global__ __launch_bounds__(256) void bconv_patch_rows_kernel(PatchArgs a) {
 #pragma unroll
       for (int k = 0; k < 32; ++k) {
         const uint4 wk = wsh[g + k];
-        uint32_t d = wk.w;
-        d += static_cast<uint32_t>(__builtin_popcount(patch[0] ^ wk.x));
-        if constexpr (PW > 1) d += static_cast<uint32_t>(__builtin_popcount(patch[1] ^ wk.y));
-        if constexpr (PW > 2) d += static_cast<uint32_t>(__builtin_popcount(patch[2] ^ wk.z));
+        uint32_t d = PW == 1 ? wk.w + static_cast<uint32_t>(__builtin_popcount(patch[0] ^ wk.x))
+                             : bcnt_acc(patch[0] ^ wk.x, wk.w);
+        if constexpr (PW > 1) d = bcnt_acc(patch[1] ^ wk.y, d);
+        if constexpr (PW > 2) d = bcnt_acc(patch[2] ^ wk.z, d);
         word = __builtin_amdgcn_alignbit(word, d, 31);
       }
       word ^= wflip[g >> 5];
