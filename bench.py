@@ -45,11 +45,11 @@ _FP4 = ("paper_1808_00209_amd/csrc/fp4_expand.hpp",
 _LANE = ("paper_1808_00209_amd/csrc/lane_ops.hpp",
          "96ece7042c6ed72e9cd799fdd8e007525e30035bbd8d052a9ece380c5e3fda82")
 _KERN = ("paper_1808_00209_amd/csrc/kernels.hpp",
-         "ad749ccafdfc625c228f9cff0dbb25f3721b8b73722350766f32b04cdfe843b7")
+         "86ea13571370aad73483ad327b357f7a50c7ec024315d0dad4558ca5ae187d9e")
 MEASURED_TRAFFIC = {
     # profiles/fconv_bconv_cifar_b64.md
     ("cifar_bnn_b64", "L0+L1 fconv+bconv 32x32x3->128->128 k3 pool (fused)"): dict(
-        fetch_kib=980.8, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
+        fetch_kib=980.7, write_kib=256.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/fconv_bconv.hip",
                        "b9775a39d56ce451c281b54dceafe567d2fc9cc81ff7a7752a4c1a83d8de96f3"),
                       ("paper_1808_00209_amd/csrc/fp32_split.hpp",
