@@ -185,7 +185,7 @@ bnn_status gemm_launch(int64_t M, int64_t N, int64_t K, const uint32_t* A,
   // multiple of 64 stay with the conv kernel (one tile per workgroup took
   // 13.1 us on that shape).
   if (g_opt.algo != BNN_ALGO_VALU && bnn::bfc_gemm_supported(M, N, K) &&
-      (((M + 31) / 32) * (N / 32) <= 512 || N % 64 == 0))
+      (((M + 31) / 32) * ((N + 31) / 32) <= 512 || N % 64 == 0))
     return hip_status(bnn::launch_bfc_gemm(M, N, K, A, B, thr, flip, sums, bits, s),
                       "bgemm launch");
   // M rows of A are a 1 x M image with K channels; B holds N 1x1 filters.

@@ -1,7 +1,9 @@
 // Binary FC layer / GEMM (Sec. III-B, Eq. 4) for long rows at modest row
 // counts: S[m][n] = sum_k a[m][k] b[n][k] over +-1 values, with the
-// threshold / flip epilogue of bnn_bgemm.  K is at least 1024 bits and N a
-// multiple of 32.
+// threshold / flip epilogue of bnn_bgemm.  K is at least 1024 bits; an N that
+// is not a multiple of 32 leaves the last output tile partial (its weight rows
+// past N read as 0 through the buffer range, and its outputs past N are
+// neither stored nor set in the bits).  The FC tail needs whole tiles.
 //
 // A workgroup computes one 32 x 32 output tile (32 rows x 32 outputs) with 8
 // waves, each taking one eighth of the K bits.  A wave loads its slice of
@@ -37,9 +39,9 @@ struct GmArgs {
   const uint32_t* A;      // [M][Kw]
   const uint32_t* B;      // [N][Kw]
   const int32_t* thr;     // [N] (bits) or null
-  const uint32_t* flip;   // [N / 32] or null
+  const uint32_t* flip;   // [ceil(N / 32)] or null
   int32_t* sums;          // [M][N] or null
-  uint32_t* bits;         // [M][N / 32] or null
+  uint32_t* bits;         // [M][ceil(N / 32)] or null
   int32_t M, N, Kw;       // Kw = ceil(K / 32), the row length in words
   int32_t Kwp;            // Kw rounded up to 4 KS words (whole k-steps per wave)
   int32_t K;              // bits
@@ -161,7 +163,7 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a, TailArgs t) {
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, c = lane & 31;
-  const int ftb = a.N / (32 * TFB);                 // filter-tile groups
+  const int ftb = (a.N + 32 * TFB - 1) / (32 * TFB);  // filter-tile groups
   const int ft0 = TFB * (blockIdx.x % ftb);         // first filter tile
   const int m00 = 32 * TPB * (blockIdx.x / ftb);    // first row
   const int tp = wave % TPB, tf = (wave / TPB) % TFB, ks = wave / NTL;
@@ -174,7 +176,7 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a, TailArgs t) {
   int32_t thv = 0, t1v = 0;
   uint32_t w1v = 0;
   const bool th_lane = want_bits && tid < 32 * TFB;
-  if (th_lane) thv = a.thr[32 * ft0 + tid];
+  if (th_lane && 32 * ft0 + tid < a.N) thv = a.thr[32 * ft0 + tid];
   const bool tail_lane = TAIL && tid >= 64 && tid < 64 + t.N1;
   if (tail_lane) {
     w1v = t.w1[static_cast<size_t>(tid - 64) * (a.N / 32) + ft0];
@@ -311,10 +313,15 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a, TailArgs t) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = 8 * i + (lane >> 3), col = 4 * (lane & 7);
-      if (m0 + row < a.M) {
-        const int* src = &ts[row * 33 + col];
-        *reinterpret_cast<int4*>(&a.sums[static_cast<size_t>(m0 + row) * a.N + n0 + col]) =
-            int4{src[0], src[1], src[2], src[3]};
+      const int* src = &ts[row * 33 + col];
+      int32_t* dst = &a.sums[static_cast<size_t>(m0 + row) * a.N + n0 + col];
+      if (m0 + row < a.M && n0 + col + 4 <= a.N && (a.N & 3) == 0) {
+        *reinterpret_cast<int4*>(dst) = int4{src[0], src[1], src[2], src[3]};
+      } else if (m0 + row < a.M) {
+        // N not a multiple of 4: rows are not 16-byte aligned; past N: nothing
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (n0 + col + e < a.N) dst[e] = src[e];
       }
     }
   }
@@ -324,8 +331,10 @@ __global__ __launch_bounds__(kNT) void bfc_gemm_kernel(GmArgs a, TailArgs t) {
     for (int e = 0; e < 16; ++e)
       d[e] = acc[e] + th[32 * tf + 8 * (e >> 2) + 4 * h + (e & 3)];
     // output bit = (S >= thr) xor flip = sign xor ~flip
-    const uint32_t word = or_xor32(sign_word(d, h)) ^ ~(a.flip ? a.flip[ft] : 0u);
-    if (h == 0 && m < a.M) a.bits[static_cast<size_t>(m) * (a.N / 32) + ft] = word;
+    const int nw = (a.N + 31) / 32;
+    const uint32_t word = (or_xor32(sign_word(d, h)) ^ ~(a.flip ? a.flip[ft] : 0u)) &
+                          (ft == nw - 1 ? tail_mask(a.N) : ~0u);
+    if (h == 0 && m < a.M) a.bits[static_cast<size_t>(m) * nw + ft] = word;
   }
 }
 
@@ -354,7 +363,8 @@ GmArgs gm_args(int64_t M, int64_t N, int64_t K, const uint32_t* A, const uint32_
 template <int TPB, int TFB, int KS>
 void launch_tiles(const GmArgs& a, hipStream_t s) {
   const unsigned blocks =
-      static_cast<unsigned>(((a.M + 32 * TPB - 1) / (32 * TPB)) * (a.N / (32 * TFB)));
+      static_cast<unsigned>(((a.M + 32 * TPB - 1) / (32 * TPB)) *
+                            ((a.N + 32 * TFB - 1) / (32 * TFB)));
   if (a.K == 32 * a.Kwp)
     bfc_gemm_kernel<TPB, TFB, KS><<<blocks, kNT, 0, s>>>(a, TailArgs{});
   else
@@ -365,9 +375,9 @@ void launch_tiles(const GmArgs& a, hipStream_t s) {
 
 bool bfc_gemm_supported(int64_t M, int64_t N, int64_t K) {
   const int64_t kw = (K + 31) / 32 + 32;  // row words with the padding
-  return M >= 1 && N >= 32 && N % 32 == 0 && K >= 1024 && K < (int64_t{1} << 28) &&
+  return M >= 1 && N >= 1 && K >= 1024 && K < (int64_t{1} << 28) &&
          M * kw * 4 < (int64_t{1} << 31) && N * kw * 4 < (int64_t{1} << 31) &&
-         ((M + 31) / 32) * (N / 32) < (int64_t{1} << 31);
+         ((M + 31) / 32) * ((N + 31) / 32) < (int64_t{1} << 31);
 }
 
 hipError_t launch_bfc_gemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
@@ -376,7 +386,7 @@ hipError_t launch_bfc_gemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
   // One output tile per workgroup (K split 8 ways) up to 512 tiles; larger
   // grids take 2 x 2 tiles per workgroup with K split 2 ways (rows and
   // outputs in whole pairs of tiles).
-  const int64_t tiles = ((M + 31) / 32) * (N / 32);
+  const int64_t tiles = ((M + 31) / 32) * ((N + 31) / 32);
   if (tiles <= 512 || N % 64 != 0)
     launch_tiles<1, 1, 8>(gm_args(M, N, K, A, B, thr, flip, sums, bits, 32), s);
   else
@@ -385,7 +395,8 @@ hipError_t launch_bfc_gemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
 }
 
 bool bfc_tail_supported(int64_t M, int64_t K0, int64_t N0, int64_t N1) {
-  return bfc_gemm_supported(M, N0, K0) && M <= kTailMaxRows && N0 <= 32 * 1024 && N1 >= 1 &&
+  return bfc_gemm_supported(M, N0, K0) && N0 % 32 == 0 && M <= kTailMaxRows &&
+         N0 <= 32 * 1024 && N1 >= 1 &&
          N1 <= 32 && ((M + 31) / 32) * (N0 / 32) <= 512;
 }
 

@@ -140,10 +140,11 @@ hipError_t launch_bconv_img8(const ConvGeom& g, const uint32_t* in, const uint32
                              const int32_t* thr, const uint32_t* flip, uint32_t* bits,
                              hipStream_t s);
 
-// Binary FC layer / GEMM with K >= 1024 bits and N a multiple of
-// 32 (bfc_gemm.hip): a workgroup per 32 x 32 output tile, K split over its 8
-// waves, both operands staged per wave through LDS with whole-line loads.
-// sums [M][N] and/or bits [M][N / 32]; thr non-null when bits is.
+// Binary FC layer / GEMM with K >= 1024 bits (bfc_gemm.hip): a workgroup per
+// 32 x 32 output tile (the last one partial when N is not a multiple of 32),
+// K split over its 8 waves, both operands staged per wave through LDS with
+// whole-line loads.  sums [M][N] and/or bits [M][ceil(N / 32)]; thr non-null
+// when bits is.
 bool bfc_gemm_supported(int64_t M, int64_t N, int64_t K);
 hipError_t launch_bfc_gemm(int64_t M, int64_t N, int64_t K, const uint32_t* A,
                            const uint32_t* B, const int32_t* thr, const uint32_t* flip,

@@ -315,7 +315,12 @@ GEMM_CASES = [(1, 1, 1), (1, 10, 1024), (2, 33, 31), (5, 100, 33), (16, 1024, 81
               (5, 64, 1025), (70, 96, 4100), (100, 2048, 1100), (64, 4096, 2047),
               (300, 4096, 4100), (600, 1088, 1056),
               # two rows: the FC kernel by default (one row: the GEMV)
-              (2, 1024, 8192), (2, 64, 1025), (1, 1024, 8192)]
+              (2, 1024, 8192), (2, 64, 1025), (1, 1024, 8192),
+              # N not a multiple of 32 in the FC kernel: a partial last tile
+              # (Table II's 18432 -> 100 at 256 rows, N % 4 != 0 with
+              # element stores, a K tail, fewer than 32 outputs)
+              (256, 100, 18432), (64, 50, 4096), (70, 100, 2047), (40, 1000, 5120),
+              (33, 10, 1024), (5, 33, 1025)]
 
 
 @pytest.mark.parametrize("case", GEMM_CASES, ids=[str(c) for c in GEMM_CASES])
