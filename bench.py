@@ -45,7 +45,7 @@ _FP4 = ("paper_1808_00209_amd/csrc/fp4_expand.hpp",
 _LANE = ("paper_1808_00209_amd/csrc/lane_ops.hpp",
          "96ece7042c6ed72e9cd799fdd8e007525e30035bbd8d052a9ece380c5e3fda82")
 _KERN = ("paper_1808_00209_amd/csrc/kernels.hpp",
-         "86ea13571370aad73483ad327b357f7a50c7ec024315d0dad4558ca5ae187d9e")
+         "7c7597e1eef994edee640fb4fd62722dbf0e527b47da81498e019e6b9cb72943")
 MEASURED_TRAFFIC = {
     # profiles/fconv_bconv_cifar_b64.md
     ("cifar_bnn_b64", "L0+L1 fconv+bconv 32x32x3->128->128 k3 pool (fused)"): dict(
@@ -62,7 +62,7 @@ MEASURED_TRAFFIC = {
                        "4967ccbad87efa16575172abf11b76792b74433995d15760fb64a86b724adf26"),
                       _FP4, _LANE, _KERN]), flags=_FLAGS),
     ("cifar_bnn_b64", "L5 bconv 8x8x512->512 k3 pool"): dict(
-        fetch_kib=898.0, write_kib=128.0, fetch_scale=2.0, write_scale=1.0,
+        fetch_kib=898.1, write_kib=128.0, fetch_scale=2.0, write_scale=1.0,
         sources=dict([("paper_1808_00209_amd/csrc/bconv_bconv.hip",
                        "4967ccbad87efa16575172abf11b76792b74433995d15760fb64a86b724adf26"),
                       _FP4, _LANE, _KERN]), flags=_FLAGS),
