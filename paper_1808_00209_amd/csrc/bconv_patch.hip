@@ -311,6 +311,7 @@ __global__ __launch_bounds__(256) void bconv_patch_rows_kernel(PatchArgs a) {
   static_assert(SW <= 32 && PW <= 3, "window rows must fit the patch layout");
   __shared__ uint32_t stream[TR * RL];
   __shared__ uint32_t codes[C == 0 ? 1 : TR * TC];
+  __shared__ float gt[C == 3 ? (TR + 2) * (TC + 2) : 1];  // LBP: grays with a ring
   __shared__ uint4 wsh[kFB];                   // patch words and bias per filter
   __shared__ uint32_t wflip[kFB / 32];
 
@@ -417,6 +418,42 @@ __global__ __launch_bounds__(256) void bconv_patch_rows_kernel(PatchArgs a) {
         }
       }
       if (!split) stage_filters(0, nf0);
+    }
+    __syncthreads();
+  } else if (C == 3 && a.in.mode == BNN_INPUT_LBP) {
+    // LBP: the grays of the tile plus a one-pixel ring first (NaN outside
+    // the image, so such a neighbour never exceeds and a pixel outside the
+    // image gets code 0, the pad), then each code from four grays in LDS,
+    // rather than 12 global loads per pixel.
+    constexpr int GC = TC + 2;
+    if (split && wave == 0) {
+      stage_filters(0, nf0);
+    } else {
+      const int e0 = split ? t - 64 : t, step = split ? 192 : 256;
+      for (int e = e0; e < (TR + 2) * GC; e += step) {
+        const int r = e / GC, cc = e - r * GC;
+        const int gi = gi0 - 1 + r, gj = gj0 - 1 + cc;
+        gt[e] = (gi >= 0 && gi < a.in.H && gj >= 0 && gj < a.in.W)
+                    ? gray_of(a.in.x + ((static_cast<size_t>(n) * a.in.H + gi) * a.in.W + gj) *
+                                           a.in.Cin)
+                    : __builtin_nanf("");
+      }
+      if (!split) stage_filters(0, nf0);
+    }
+    __syncthreads();
+    for (int e = t; e < TR * TC; e += 256) {
+      const int r = e / TC, cc = e - r * TC;
+      const float* gc = gt + (r + 1) * GC + cc + 1;  // the pixel's gray
+      const float g = gc[0];
+      codes[e] = (gc[-GC - 1] > g ? 4u : 0u) | (gc[1] > g ? 2u : 0u) | (gc[GC - 1] > g ? 1u : 0u);
+    }
+    __syncthreads();
+    for (int jb = wave; jb < JOBS; jb += 4) {
+      const int r = jb / CH, q = jb - r * CH;
+      const int e = q * 64 + lane;
+      const int px = e / C, ch = e - px * C;
+      const bool bit = e < E && ((codes[r * TC + min(px, TC - 1)] >> (C - 1 - ch)) & 1u);
+      put_ballot(r, q, __builtin_amdgcn_ballot_w64(bit));
     }
     __syncthreads();
   } else {
